@@ -1,0 +1,182 @@
+/*
+ * sketch.h -- C ABI of the MI355X (gfx950) structured-sketch library.
+ *
+ * A sketch is a seeded random linear map S: R^N -> R^D applied to a batch of
+ * vectors that arrive as a ragged list of parameter tensors ("layers"), and its
+ * transpose S^T: R^D -> R^N.  Kinds, following "Efficient Sketches for
+ * Training Data Attribution and Studying the Loss Landscape" (Schioppa,
+ * NeurIPS 2024):
+ *
+ *   SK_FJL   y = sqrt(N/D) G_s H_N B x                  (eq. ailon_chazelle)
+ *   SK_FFD   y = sum_b B_b H_D Pi_b^T G_b H_D x_b         (eq. fastfood, used as
+ *            the transpose of the feature map; sigma_F = 1 as in the proof of
+ *            Thm. fastfood_bad_inputs)
+ *   SK_AFFD  y = R_D(sqrt(N/D) H^{pi2}_N G H^{pi1}_N B x) (eq. bami)
+ *   SK_AFJL  y = R_D(sqrt(N/D) G H^{pi1}_N B x)           (eq. frikadel)
+ *   SK_QK    Y = A X B^T per weight matrix X (m x n), A (dA x m) ~ N(0,1/dA),
+ *            B (dB x n) ~ N(0,1/dB)                       (eq. straight with two
+ *            Kronecker factors, contraction of eq. qk_proof_tensor_dec)
+ *
+ * H_N is the normalised Walsh-Hadamard matrix (appendix definition), R_D keeps
+ * the first D coordinates, B is a diagonal of random signs, G a diagonal of
+ * N(0,1) entries, and pi1/pi2 permute digits within the Kronecker factors of N
+ * (Sec. 3, "Removing the lookup bottleneck"; factors of at most 1024).
+ *
+ * Per layer l with n_l = rows*cols elements the FWHT kinds work on the padded
+ * length N'_l = 2^ceil(log2 max(n_l, D)) (padding is virtual: never read or
+ * written).  The FWHT kinds sum independent per-layer sketches (each with its
+ * own random streams, keyed on the layer's index in the list), which is the
+ * per-shard lift followed by a sum of the paper's model-parallel appendix.  QK
+ * concatenates the dA*dB blocks of its layers in list order (sum dA*dB = D).
+ *
+ * Every random quantity is regenerated from (seed, layer, stream, index) with a
+ * counter-based Philox4x32-10 generator; nothing of size N is stored.
+ *
+ * Conventions for every entry point:
+ *  - Return 0 (SK_OK) on success, a negative SK_E* code on failure.  Arguments
+ *    are validated before any device work is queued; on failure no output
+ *    buffer is touched.  sketch_last_error() gives a thread-local message.
+ *  - Device pointers are plain HIP device addresses on the sketch's device;
+ *    the arrays OF pointers (grads, out, theta0) are host memory and are read
+ *    during the call only.
+ *  - Work is queued asynchronously on `stream` (a hipStream_t; NULL = the
+ *    legacy default stream).  Results are ready when the stream is.
+ *  - A handle is immutable after creation, but owns one workspace: calls on the
+ *    same handle must be serialised on one stream (not thread-safe).
+ *  - The caller owns all input/output buffers; the handle owns its tables and
+ *    workspace, allocated at creation.  Apply calls never allocate or free.
+ *  - Results are bitwise deterministic for a fixed build, device, sketch and
+ *    input (no floating-point atomics).
+ */
+#ifndef SK_SKETCH_H
+#define SK_SKETCH_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SK_FJL = 0, SK_FFD = 1, SK_AFFD = 2, SK_AFJL = 3, SK_QK = 4 } sk_kind;
+typedef enum { SK_F32 = 0, SK_BF16 = 1 } sk_dtype;
+
+enum {
+  SK_OK = 0,
+  SK_EINVAL = -1,      /* bad argument: kind, D, shapes, null pointer, batch  */
+  SK_EDTYPE = -2,      /* unknown dtype                                       */
+  SK_ENOMEM = -3,      /* device allocation failed at creation                */
+  SK_EHIP = -4,        /* a HIP runtime call failed                           */
+  SK_EUNSUPPORTED = -5 /* valid in the math but outside what the kernels take */
+};
+
+/* One parameter tensor, row-major rows x cols (1-D tensors: rows = 1).
+ * qk_da, qk_db: the QK output block shape of this matrix (1 <= qk_da <= rows,
+ * 1 <= qk_db <= cols); ignored by the other kinds. */
+typedef struct {
+  int64_t rows, cols;
+  int32_t qk_da, qk_db;
+} sk_layer_shape;
+
+typedef struct sk_sketch sk_sketch;
+
+/* Introspection record (sketch_query). */
+typedef struct {
+  int32_t kind, n_layers;
+  int64_t D;
+  uint64_t seed;
+  int64_t total_numel;      /* sum of rows*cols                      */
+  int64_t total_padded;     /* sum of N'_l (FWHT kinds), else 0      */
+  int64_t workspace_bytes;  /* device workspace owned by the handle  */
+  int32_t rng_version;      /* version of the random-stream layout   */
+  int32_t device;
+} sk_info;
+
+/* Random-stream identifiers (the fourth Philox counter word). */
+enum {
+  SK_STREAM_SIGN = 1,    /* B signs, one per coordinate of N'_l            */
+  SK_STREAM_GAUSS = 2,   /* G entries (AFFD, FFD: N'_l; FJL, AFJL: D)      */
+  SK_STREAM_INDEX = 3,   /* FJL sample positions in [0, N'_l)              */
+  SK_STREAM_FFDPERM = 4, /* FFD block permutation Pi_b                     */
+  SK_STREAM_PI1 = 5,     /* digit permutation before the first H           */
+  SK_STREAM_PI2 = 6,     /* digit permutation after the second H (AFFD)    */
+  SK_STREAM_QKA = 7,     /* QK left factor                                 */
+  SK_STREAM_QKB = 8      /* QK right factor                                */
+};
+
+/*
+ * Create a sketch on HIP device `device`.
+ *   kind      one of sk_kind.
+ *   shapes    host array of n_layers >= 1 layer shapes (rows, cols >= 1).
+ *   D         target dimension.  FWHT kinds: a power of two, 16 <= D <= 2^20
+ *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
+ *   seed      64-bit key of every random stream.
+ *   flags     reserved, must be 0.
+ * On success *out receives the handle (destroy with sketch_destroy).  QK
+ * factors (bf16, rounded to nearest even from fp32) and the small per-layer
+ * tables are generated on the device here.
+ */
+int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, int64_t D, uint64_t seed,
+                  uint32_t flags, int32_t device, sk_sketch **out);
+
+/*
+ * Forward sketch y = sum over the selected layers of S_l x_l.
+ *   grads       host array of n_layers device pointers; grads[i] holds layer
+ *               first_layer+i as [batch, rows*cols] row-major, contiguous, in
+ *               `dtype` (SK_F32 or SK_BF16 bit patterns), 4-byte aligned.
+ *   batch       number of vectors (0 is a no-op).
+ *   out         device [batch, D] fp32.  accumulate = 0 overwrites, 1 adds to
+ *               what `out` holds (streaming a model layer group by layer
+ *               group).  For QK only the selected layers' column blocks of
+ *               `out` are written (or accumulated).
+ *   first_layer, n_layers  the contiguous layer range this call covers.
+ * Arithmetic is fp32 (bf16 inputs are widened exactly); QK multiplies bf16
+ * operands with fp32 accumulation.
+ */
+int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t batch, float *out,
+                 int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream);
+
+/*
+ * Transpose x_l = S_l^T z (+ theta0_l) for the selected layers.
+ *   z        device [batch, D] fp32.
+ *   out      host array of n_layers device pointers, out[i] is
+ *            [batch, rows*cols] of layer first_layer+i in `out_dtype`
+ *            (bf16 outputs are rounded to nearest even).
+ *   theta0   NULL, or a host array of n_layers device pointers, each NULL or
+ *            an fp32 [rows*cols] vector broadcast-added over the batch (the
+ *            intrinsic-dimension reparameterisation theta0 + S^T z).
+ */
+int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out, sk_dtype out_dtype,
+                   const void *const *theta0, int32_t first_layer, int32_t n_layers, void *stream);
+
+/* Free everything the handle owns (synchronises its device).  NULL is a no-op. */
+void sketch_destroy(sk_sketch *s);
+
+/* Fill *info.  Returns SK_EINVAL on NULL arguments. */
+int sketch_query(const sk_sketch *s, sk_info *info);
+
+/*
+ * Regenerate `count` values of a random stream ON THE DEVICE, starting at
+ * index `start`, and copy them to host memory `host_out` (synchronous).
+ *   SK_STREAM_SIGN               int8 +-1 per coordinate.
+ *   SK_STREAM_GAUSS/QKA/QKB      fp32 N(0,1) values (QK factors before the
+ *                                1/sqrt(d) scale and bf16 rounding).
+ *   SK_STREAM_INDEX              uint32 positions in [0, N'_layer).
+ *   SK_STREAM_PI1/PI2            uint32 pi(i) of the full digit permutation
+ *                                of [0, N'_layer).
+ *   SK_STREAM_FFDPERM            uint32 pi_b(i) on [0, D), b = `aux`.
+ * Out-of-range indices give SK_EINVAL.
+ */
+int sketch_debug_stream(sk_sketch *s, int32_t layer, int32_t stream_id, uint64_t start, uint64_t count,
+                        uint64_t aux, void *host_out);
+
+/* Thread-local message describing the last failure of this thread. */
+const char *sketch_last_error(void);
+
+/* Static text for a status code. */
+const char *sketch_status_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SK_SKETCH_H */

@@ -1,0 +1,619 @@
+// sk_api.hip -- C ABI of the sketch library: validation, planning (per-layer
+// digit structure, permutation tables, AFJL work items, FJL transpose lists,
+// QK factors), workspace ownership and dispatch of the kernels in sk_fwht.hip
+// and sk_qk.hip onto the caller's stream.
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+
+#include "sk_launch.h"
+
+using namespace sk;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string &msg) {
+  g_err = msg;
+  return code;
+}
+
+#define SK_HIP(call)                                                                              \
+  do {                                                                                            \
+    hipError_t e_ = (call);                                                                       \
+    if (e_ != hipSuccess) return fail(SK_EHIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+int ilog2(int64_t v) {
+  int l = 0;
+  while ((1ll << l) < v) ++l;
+  return l;
+}
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int64_t workspace_budget() {
+  const char *e = std::getenv("SK_WORKSPACE_MB");
+  int64_t mb = e ? std::atoll(e) : 4096;
+  if (mb < 16) mb = 16;
+  return mb << 20;
+}
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+void free_all(sk_sketch *s) {
+  auto f = [](void *p) {
+    if (p) (void)hipFree(p);
+  };
+  f(s->d_layers);
+  f(s->d_ptab);
+  f(s->d_gtab);
+  f(s->d_items);
+  f(s->d_rslot);
+  f(s->d_fjl_pos);
+  f(s->d_fjl_seg);
+  f(s->d_fjl_smp);
+  f(s->d_qkfac);
+  f(s->ws);
+}
+
+bool fwht_kind(int k) { return k == SK_FJL || k == SK_FFD || k == SK_AFFD || k == SK_AFJL; }
+
+// Bytes of workspace one vector needs for one call over layers [l0, l1).
+int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
+  int64_t need = 0;
+  for (int l = l0; l < l1; ++l) {
+    const LayerDesc &ld = s->layers[l];
+    int64_t b = 0;
+    switch (s->kind) {
+      case SK_AFJL:
+        b = transpose ? s->D * 4 : (int64_t)ld.n_items * s->Lw * 4;
+        break;
+      case SK_AFFD:
+        b = (ld.np + (1ll << ld.lo_len_lg)) * 4;
+        break;
+      case SK_FJL:
+        b = ld.np * 4;
+        break;
+      case SK_FFD:
+        if (ilog2(s->D) <= kFfdSmallMax)
+          b = transpose ? 0 : ffd_small_groups(s, l) * s->D * 4;
+        else
+          b = 2 * ffd_live_blocks(s, l) * s->D * 4;
+        break;
+      case SK_QK:
+        b = (int64_t)ld.m * ld.db * 4;
+        break;
+    }
+    need = std::max(need, b);
+  }
+  return need;
+}
+
+}  // namespace
+
+namespace sk {
+const char *set_error(int code, const std::string &msg) {
+  (void)code;
+  g_err = msg;
+  return g_err.c_str();
+}
+}  // namespace sk
+
+extern "C" {
+
+const char *sketch_last_error(void) { return g_err.c_str(); }
+
+const char *sketch_status_string(int code) {
+  switch (code) {
+    case SK_OK: return "ok";
+    case SK_EINVAL: return "invalid argument";
+    case SK_EDTYPE: return "invalid dtype";
+    case SK_ENOMEM: return "out of device memory";
+    case SK_EHIP: return "HIP runtime error";
+    case SK_EUNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+  }
+}
+
+int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, int64_t D, uint64_t seed,
+                  uint32_t flags, int32_t device, sk_sketch **out) {
+  if (!out) return fail(SK_EINVAL, "out is NULL");
+  *out = nullptr;
+  if ((int)kind < 0 || (int)kind > 4) return fail(SK_EINVAL, "unknown sketch kind");
+  if (!shapes || n_layers < 1) return fail(SK_EINVAL, "need at least one layer shape");
+  if (flags != 0) return fail(SK_EINVAL, "flags must be 0");
+  for (int l = 0; l < n_layers; ++l) {
+    if (shapes[l].rows < 1 || shapes[l].cols < 1)
+      return fail(SK_EINVAL, "layer " + std::to_string(l) + ": rows and cols must be >= 1");
+    if (shapes[l].rows > (1ll << 40) / shapes[l].cols)
+      return fail(SK_EUNSUPPORTED, "layer " + std::to_string(l) + " too large");
+  }
+  if (fwht_kind(kind)) {
+    if (!is_pow2(D)) return fail(SK_EINVAL, "D must be a power of two");
+    if (D < 16) return fail(SK_EUNSUPPORTED, "D < 16 is not supported by the kernels");
+    if (D > (1ll << 20)) return fail(SK_EUNSUPPORTED, "D > 2^20 is not supported by the kernels");
+  } else {
+    int64_t tot = 0;
+    for (int l = 0; l < n_layers; ++l) {
+      const sk_layer_shape &sh = shapes[l];
+      if (sh.qk_da < 1 || sh.qk_db < 1 || sh.qk_da > sh.rows || sh.qk_db > sh.cols)
+        return fail(SK_EINVAL, "layer " + std::to_string(l) + ": need 1 <= qk_da <= rows and 1 <= qk_db <= cols");
+      if (sh.rows > (1ll << 31) || sh.cols > (1ll << 31))
+        return fail(SK_EUNSUPPORTED, "QK matrix dimension above 2^31");
+      tot += (int64_t)sh.qk_da * sh.qk_db;
+    }
+    if (tot != D) return fail(SK_EINVAL, "QK: sum of qk_da*qk_db must equal D");
+  }
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(SK_EHIP, "no HIP device available");
+  if (device < 0 || device >= ndev) return fail(SK_EINVAL, "device index out of range");
+
+  sk_sketch *s = new (std::nothrow) sk_sketch();
+  if (!s) return fail(SK_ENOMEM, "host allocation failed");
+  s->kind = kind;
+  s->device = device;
+  s->D = D;
+  s->seed = seed;
+  s->key = make_key(seed);
+  s->layers.resize(n_layers);
+
+  std::vector<uint16_t> ptab;
+  const bool need_pi1 = kind == SK_AFFD || kind == SK_AFJL;
+  const bool need_pi2 = kind == SK_AFFD;
+  int64_t qk_col = 0, fac = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    LayerDesc &ld = s->layers[l];
+    std::memset(&ld, 0, sizeof(ld));
+    ld.n = shapes[l].rows * shapes[l].cols;
+    ld.layer_id = l;
+    s->total_numel += ld.n;
+    if (fwht_kind(kind)) {
+      ld.np = 1;
+      while (ld.np < std::max(ld.n, D)) ld.np <<= 1;
+      ld.lgnp = ilog2(ld.np);
+      int lg[8];
+      ld.K = kron_shapes_log2(ld.lgnp, lg);
+      if (ld.K > kMaxDigits) {
+        free_all(s);
+        delete s;
+        return fail(SK_EUNSUPPORTED, "layer too large (more than 4 Kronecker digits)");
+      }
+      for (int k = 0; k < ld.K; ++k) ld.lg[k] = lg[k];
+      ld.lgL = ld.lg[ld.K - 1];
+      ld.L = 1 << ld.lgL;
+      ld.lgdk1 = ld.K >= 2 ? ld.lg[ld.K - 2] : 0;
+      ld.dk1 = 1 << ld.lgdk1;
+      ld.rows_live = (ld.n + ld.L - 1) / ld.L;
+      s->total_padded += ld.np;
+      for (int si = 0; si < 2; ++si) {
+        if ((si == 0 && !need_pi1) || (si == 1 && !need_pi2)) continue;
+        const uint32_t stream = si == 0 ? ST_PI1 : ST_PI2;
+        for (int k = 0; k < ld.K; ++k) {
+          const int w = ld.lg[k];
+          const PermKey pk = perm_key((uint32_t)l, stream, (uint32_t)k, (uint32_t)w, s->key);
+          ld.poff[si][0][k] = (int32_t)ptab.size();
+          ld.poff[si][1][k] = (int32_t)ptab.size() + (1 << w);
+          ptab.resize(ptab.size() + 2 * (size_t)(1 << w));
+          uint16_t *fw = ptab.data() + ld.poff[si][0][k];
+          uint16_t *iv = ptab.data() + ld.poff[si][1][k];
+          for (uint32_t x = 0; x < (1u << w); ++x) {
+            const uint32_t y = perm_fwd(pk, x);
+            fw[x] = (uint16_t)y;
+            iv[y] = (uint16_t)x;
+          }
+        }
+      }
+      if (kind == SK_AFFD) {
+        // low block: the digits spanned by c < D
+        const int nlow = D > ld.L ? 2 : 1;
+        ld.lo_len_lg = ld.lgL + (nlow == 2 ? ld.lgdk1 : 0);
+        uint32_t hstar = 0;
+        int shift = 0;
+        for (int k = ld.K - 1 - nlow; k >= 0; --k) {
+          hstar |= (uint32_t)ptab[ld.poff[1][0][k] + 0] << shift;
+          shift += ld.lg[k];
+        }
+        ld.hstar = hstar;
+      }
+    } else {
+      ld.m = (int32_t)shapes[l].rows;
+      ld.nc = (int32_t)shapes[l].cols;
+      ld.da = shapes[l].qk_da;
+      ld.db = shapes[l].qk_db;
+      ld.qk_col = qk_col;
+      qk_col += (int64_t)ld.da * ld.db;
+      ld.fa_off = fac;
+      fac += (int64_t)ld.da * ld.m;
+      ld.fb_off = fac;
+      fac += (int64_t)ld.db * ld.nc;
+    }
+  }
+  s->qk_fac_elems = fac;
+
+  // AFJL work items: destination rows r of an R x Lw accumulator.
+  std::vector<int2> rslot;
+  if (kind == SK_AFJL) {
+    s->Lw = (int)std::min<int64_t>(D, 1024);
+    s->R = (int)(D / s->Lw);
+    const int R = s->R;
+    const int64_t rows_per_item = 64;
+    for (int l = 0; l < n_layers; ++l) {
+      LayerDesc &ld = s->layers[l];
+      ld.rslot_off = (int32_t)rslot.size();
+      ld.item_off = (int32_t)s->items.size();
+      if (R == 1) {
+        const int64_t T = ld.rows_live;
+        const int first = (int)s->items.size();
+        for (int64_t t0 = 0; t0 < T; t0 += rows_per_item)
+          s->items.push_back(FoldItem{l, 0, (int32_t)t0, (int32_t)std::min(T, t0 + rows_per_item)});
+        rslot.push_back(int2{first, (int)(s->items.size() - first)});
+      } else {
+        const int nk = ld.dk1 / R;
+        const int64_t ntop_live = (ld.rows_live + ld.dk1 - 1) / ld.dk1;
+        const int64_t T = ntop_live * nk;
+        const uint16_t *inv = ptab.data() + ld.poff[0][1][ld.K - 2];
+        for (int r = 0; r < R; ++r) {
+          // live rows mapped to r, to skip destination rows that receive nothing
+          int64_t live = 0;
+          for (int64_t t = 0; t < T && live == 0; ++t) {
+            const int64_t htop = t / nk, k = t % nk;
+            if (htop * ld.dk1 + inv[r + k * R] < ld.rows_live) live = 1;
+          }
+          const int first = (int)s->items.size();
+          if (live)
+            for (int64_t t0 = 0; t0 < T; t0 += rows_per_item)
+              s->items.push_back(FoldItem{l, r, (int32_t)t0, (int32_t)std::min(T, t0 + rows_per_item)});
+          rslot.push_back(int2{first, (int)(s->items.size() - first)});
+        }
+      }
+      ld.n_items = (int32_t)s->items.size() - ld.item_off;
+    }
+  }
+
+  // FJL transpose: samples grouped by position (deterministic order).
+  std::vector<uint32_t> fpos, fseg, fsmp;
+  if (kind == SK_FJL) {
+    s->fjl_uoff.assign(n_layers + 1, 0);
+    std::vector<std::pair<uint32_t, uint32_t>> v(D);
+    for (int l = 0; l < n_layers; ++l) {
+      const LayerDesc &ld = s->layers[l];
+      for (int64_t i = 0; i < D; ++i) v[i] = {sample_index((uint64_t)i, (uint32_t)l, s->key, (uint64_t)ld.np), (uint32_t)i};
+      std::sort(v.begin(), v.end());
+      const uint32_t base = (uint32_t)fsmp.size();
+      for (int64_t i = 0; i < D; ++i) {
+        if (i == 0 || v[i].first != v[i - 1].first) {
+          fpos.push_back(v[i].first);
+          fseg.push_back(base + (uint32_t)i);
+        }
+        fsmp.push_back(v[i].second);
+      }
+      fseg.push_back(base + (uint32_t)D);  // sentinel
+      s->fjl_uoff[l + 1] = (int64_t)fpos.size();
+    }
+  }
+
+  DeviceGuard guard(device);
+  auto alloc = [&](void **p, size_t bytes) -> int {
+    if (bytes == 0) return SK_OK;
+    if (hipMalloc(p, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(SK_ENOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+    }
+    return SK_OK;
+  };
+  int rc = SK_OK;
+#define SK_TRY(expr)      \
+  do {                    \
+    rc = (expr);          \
+    if (rc != SK_OK) {    \
+      free_all(s);        \
+      delete s;           \
+      return rc;          \
+    }                     \
+  } while (0)
+  SK_TRY(alloc((void **)&s->d_layers, sizeof(LayerDesc) * n_layers));
+  SK_TRY(alloc((void **)&s->d_ptab, sizeof(uint16_t) * ptab.size()));
+  if (kind == SK_AFJL || kind == SK_FJL) SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
+  SK_TRY(alloc((void **)&s->d_items, sizeof(FoldItem) * s->items.size()));
+  SK_TRY(alloc((void **)&s->d_rslot, sizeof(int2) * rslot.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_pos, sizeof(uint32_t) * fpos.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_seg, sizeof(uint32_t) * fseg.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
+  SK_TRY(alloc((void **)&s->d_qkfac, sizeof(uint16_t) * fac));
+
+  auto h2d = [&](void *d, const void *h, size_t bytes) -> int {
+    if (bytes == 0) return SK_OK;
+    if (hipMemcpy(d, h, bytes, hipMemcpyHostToDevice) != hipSuccess)
+      return fail(SK_EHIP, std::string("hipMemcpy: ") + hipGetErrorString(hipGetLastError()));
+    return SK_OK;
+  };
+  SK_TRY(h2d(s->d_layers, s->layers.data(), sizeof(LayerDesc) * n_layers));
+  SK_TRY(h2d(s->d_ptab, ptab.data(), sizeof(uint16_t) * ptab.size()));
+  SK_TRY(h2d(s->d_items, s->items.data(), sizeof(FoldItem) * s->items.size()));
+  SK_TRY(h2d(s->d_rslot, rslot.data(), sizeof(int2) * rslot.size()));
+  SK_TRY(h2d(s->d_fjl_pos, fpos.data(), sizeof(uint32_t) * fpos.size()));
+  SK_TRY(h2d(s->d_fjl_seg, fseg.data(), sizeof(uint32_t) * fseg.size()));
+  SK_TRY(h2d(s->d_fjl_smp, fsmp.data(), sizeof(uint32_t) * fsmp.size()));
+
+  // workspace: room for up to 64 vectors of the largest per-vector need
+  const int64_t pv = std::max(per_vector_bytes(s, 0, n_layers, false), per_vector_bytes(s, 0, n_layers, true));
+  const int64_t budget = workspace_budget();
+  if (pv > budget) {
+    free_all(s);
+    delete s;
+    return fail(SK_EUNSUPPORTED, "one vector needs " + std::to_string(pv) + " bytes of workspace, above the budget");
+  }
+  s->ws_bytes = std::min<int64_t>(budget, pv * 64);
+  if (s->ws_bytes > 0) SK_TRY(alloc((void **)&s->ws, (size_t)s->ws_bytes));
+
+  if (s->d_gtab) launch_gauss_table(s, s->d_gtab, nullptr);
+  if (kind == SK_QK) launch_qk_factors(s, nullptr);
+  if (hipDeviceSynchronize() != hipSuccess) {
+    const std::string m = hipGetErrorString(hipGetLastError());
+    free_all(s);
+    delete s;
+    return fail(SK_EHIP, "table generation failed: " + m);
+  }
+#undef SK_TRY
+  *out = s;
+  return SK_OK;
+}
+
+void sketch_destroy(sk_sketch *s) {
+  if (!s) return;
+  {
+    DeviceGuard guard(s->device);
+    (void)hipDeviceSynchronize();
+    free_all(s);
+  }
+  delete s;
+}
+
+int sketch_query(const sk_sketch *s, sk_info *info) {
+  if (!s || !info) return fail(SK_EINVAL, "NULL argument");
+  info->kind = s->kind;
+  info->n_layers = (int32_t)s->layers.size();
+  info->D = s->D;
+  info->seed = s->seed;
+  info->total_numel = s->total_numel;
+  info->total_padded = s->total_padded;
+  info->workspace_bytes = s->ws_bytes;
+  info->rng_version = kRngVersion;
+  info->device = s->device;
+  return SK_OK;
+}
+
+static int check_range(const sk_sketch *s, int32_t first_layer, int32_t n_layers) {
+  if (first_layer < 0 || n_layers < 1 || (int64_t)first_layer + n_layers > (int64_t)s->layers.size())
+    return fail(SK_EINVAL, "layer range out of bounds");
+  return SK_OK;
+}
+
+int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t batch, float *out,
+                 int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream) {
+  if (!s) return fail(SK_EINVAL, "sketch is NULL");
+  if (dtype != SK_F32 && dtype != SK_BF16) return fail(SK_EDTYPE, "dtype must be SK_F32 or SK_BF16");
+  if (batch < 0) return fail(SK_EINVAL, "batch must be >= 0");
+  if (int rc = check_range(s, first_layer, n_layers)) return rc;
+  if (batch == 0) return SK_OK;
+  if (!grads || !out) return fail(SK_EINVAL, "grads and out must be non-NULL");
+  for (int i = 0; i < n_layers; ++i)
+    if (!grads[i]) return fail(SK_EINVAL, "grads[" + std::to_string(i) + "] is NULL");
+  const int l0 = first_layer, l1 = first_layer + n_layers;
+  hipStream_t st = (hipStream_t)stream;
+  DeviceGuard guard(s->device);
+  const int64_t pv = per_vector_bytes(s, l0, l1, false);
+  int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
+  if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
+  const int esz = dtype == SK_BF16 ? 2 : 4;
+
+  for (int64_t b0 = 0; b0 < batch; b0 += bcmax) {
+    const int64_t bc = std::min(bcmax, batch - b0);
+    switch (s->kind) {
+      case SK_AFJL: {
+        // groups of layers whose fold partials fit in the workspace
+        int g0 = l0;
+        bool first = true;
+        while (g0 < l1) {
+          int g1 = g0;
+          int64_t items = 0;
+          while (g1 < l1 && g1 - g0 < kMaxPtrs) {
+            const int64_t add = s->layers[g1].n_items;
+            if (g1 > g0 && (items + add) * bc * s->Lw * 4 > s->ws_bytes) break;
+            items += add;
+            ++g1;
+          }
+          PtrPack pp{};
+          bool vec = true;
+          for (int l = g0; l < g1; ++l) {
+            pp.p[l - g0] = grads[l - l0];
+            if ((s->layers[l].n & 3) || ((uintptr_t)grads[l - l0] & (uintptr_t)(esz * 4 - 1))) vec = false;
+          }
+          const int it0 = s->layers[g0].item_off;
+          const int it1 = s->layers[g1 - 1].item_off + s->layers[g1 - 1].n_items;
+          launch_afjl_fold(s, pp, g0, dtype, vec, batch, b0, bc, it0, it1, s->ws, st);
+          launch_afjl_tail(s, g0, g1, it0, s->ws, bc, b0, batch, out, accumulate || !first, st);
+          first = false;
+          g0 = g1;
+        }
+        break;
+      }
+      case SK_AFFD:
+        for (int l = l0; l < l1; ++l) {
+          const LayerDesc &ld = s->layers[l];
+          float *w = s->ws;
+          float *f = s->ws + bc * ld.np;
+          launch_affd_prolog(s, l, grads[l - l0], dtype, b0, bc, w, st);
+          fwht_inplace(w, bc, ld.lgnp, st);
+          launch_affd_fold(s, l, w, bc, f, st);
+          fwht_inplace(f, bc, ld.lo_len_lg, st);
+          launch_affd_gather(s, l, f, b0, bc, out, accumulate || l > l0, st);
+        }
+        break;
+      case SK_FJL:
+        for (int l = l0; l < l1; ++l) {
+          const LayerDesc &ld = s->layers[l];
+          launch_fjl_prolog(s, l, grads[l - l0], dtype, b0, bc, s->ws, st);
+          fwht_inplace(s->ws, bc, ld.lgnp, st);
+          launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st);
+        }
+        break;
+      case SK_FFD: {
+        const int lgD = ilog2(s->D);
+        for (int l = l0; l < l1; ++l) {
+          if (lgD <= kFfdSmallMax) {
+            const int64_t groups = ffd_small_groups(s, l);
+            launch_ffd_small_fwd(s, l, grads[l - l0], dtype, b0, bc, s->ws, 0, groups, st);
+            launch_reduce_partials(s->ws, groups, bc, s->D, b0, out, accumulate || l > l0, st);
+          } else {
+            const int64_t nlive = ffd_live_blocks(s, l);
+            float *w = s->ws, *w2 = s->ws + bc * nlive * s->D;
+            launch_ffd_copy_blocks(s, l, grads[l - l0], dtype, b0, bc, w, st);
+            fwht_inplace(w, bc * nlive, lgD, st);
+            launch_ffd_gperm_fwd(s, l, w, bc, w2, st);
+            fwht_inplace(w2, bc * nlive, lgD, st);
+            launch_ffd_sum_signed(s, l, w2, b0, bc, out, accumulate || l > l0, st);
+          }
+        }
+        break;
+      }
+      case SK_QK:
+        for (int l = l0; l < l1; ++l)
+          launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, batch, out, accumulate != 0, st);
+        break;
+    }
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SK_EHIP, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  return SK_OK;
+}
+
+int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out, sk_dtype out_dtype,
+                   const void *const *theta0, int32_t first_layer, int32_t n_layers, void *stream) {
+  if (!s) return fail(SK_EINVAL, "sketch is NULL");
+  if (out_dtype != SK_F32 && out_dtype != SK_BF16) return fail(SK_EDTYPE, "out_dtype must be SK_F32 or SK_BF16");
+  if (batch < 0) return fail(SK_EINVAL, "batch must be >= 0");
+  if (int rc = check_range(s, first_layer, n_layers)) return rc;
+  if (batch == 0) return SK_OK;
+  if (!z || !out) return fail(SK_EINVAL, "z and out must be non-NULL");
+  for (int i = 0; i < n_layers; ++i)
+    if (!out[i]) return fail(SK_EINVAL, "out[" + std::to_string(i) + "] is NULL");
+  const int l0 = first_layer, l1 = first_layer + n_layers;
+  hipStream_t st = (hipStream_t)stream;
+  DeviceGuard guard(s->device);
+  const int64_t pv = per_vector_bytes(s, l0, l1, true);
+  int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
+  if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
+  const int lgD = ilog2(s->D);
+  for (int64_t b0 = 0; b0 < batch; b0 += bcmax) {
+    const int64_t bc = std::min(bcmax, batch - b0);
+    for (int l = l0; l < l1; ++l) {
+      const LayerDesc &ld = s->layers[l];
+      void *o = out[l - l0];
+      const float *th = theta0 ? (const float *)theta0[l - l0] : nullptr;
+      switch (s->kind) {
+        case SK_AFJL:
+          launch_afjl_T_prep(s, l, z, b0, bc, s->ws, st);
+          fwht_inplace(s->ws, bc, lgD, st);
+          launch_afjl_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st);
+          break;
+        case SK_AFFD:
+          launch_fill_zero(s->ws, bc * ld.np, st);
+          launch_affd_T_scatter(s, l, z, b0, bc, s->ws, st);
+          fwht_inplace(s->ws, bc, ld.lgnp, st);
+          launch_mul_gauss(s, l, s->ws, bc, st);
+          fwht_inplace(s->ws, bc, ld.lgnp, st);
+          launch_affd_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st);
+          break;
+        case SK_FJL:
+          launch_fill_zero(s->ws, bc * ld.np, st);
+          launch_fjl_T_scatter(s, l, z, b0, bc, s->ws, st);
+          fwht_inplace(s->ws, bc, ld.lgnp, st);
+          launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th, (float)std::sqrt((double)ld.np / (double)s->D),
+                            st);
+          break;
+        case SK_FFD:
+          if (lgD <= kFfdSmallMax) {
+            launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st);
+          } else {
+            const int64_t nlive = ffd_live_blocks(s, l);
+            float *w = s->ws, *w2 = s->ws + bc * nlive * s->D;
+            launch_ffd_expand_z(s, l, z, b0, bc, w, st);
+            fwht_inplace(w, bc * nlive, lgD, st);
+            launch_ffd_permg_T(s, l, w, bc, w2, st);
+            fwht_inplace(w2, bc * nlive, lgD, st);
+            launch_ffd_T_out(s, l, w2, b0, bc, o, out_dtype, th, st);
+          }
+          break;
+        case SK_QK:
+          launch_qk_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st);
+          break;
+      }
+    }
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SK_EHIP, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  return SK_OK;
+}
+
+int sketch_debug_stream(sk_sketch *s, int32_t layer, int32_t stream_id, uint64_t start, uint64_t count, uint64_t aux,
+                        void *host_out) {
+  if (!s || !host_out) return fail(SK_EINVAL, "NULL argument");
+  if (layer < 0 || layer >= (int32_t)s->layers.size()) return fail(SK_EINVAL, "layer out of range");
+  if (count == 0) return SK_OK;
+  const LayerDesc &ld = s->layers[layer];
+  size_t esz = 4;
+  uint64_t limit = ~0ull;
+  switch (stream_id) {
+    case SK_STREAM_SIGN:
+      esz = 1;
+      limit = fwht_kind(s->kind) ? (uint64_t)ld.np : ~0ull;
+      break;
+    case SK_STREAM_GAUSS:
+    case SK_STREAM_QKA:
+    case SK_STREAM_QKB:
+      break;
+    case SK_STREAM_INDEX:
+      if (!fwht_kind(s->kind)) return fail(SK_EINVAL, "index stream needs an FWHT kind");
+      limit = (uint64_t)s->D;
+      break;
+    case SK_STREAM_PI1:
+    case SK_STREAM_PI2:
+      if (!(s->kind == SK_AFJL || s->kind == SK_AFFD) || (stream_id == SK_STREAM_PI2 && s->kind != SK_AFFD))
+        return fail(SK_EINVAL, "this sketch has no such permutation");
+      limit = (uint64_t)ld.np;
+      break;
+    case SK_STREAM_FFDPERM:
+      if (s->kind != SK_FFD) return fail(SK_EINVAL, "FFD permutations need an FFD sketch");
+      limit = (uint64_t)s->D;
+      break;
+    default:
+      return fail(SK_EINVAL, "unknown stream id");
+  }
+  if (start > limit || count > limit - start) return fail(SK_EINVAL, "index range out of bounds");
+  DeviceGuard guard(s->device);
+  void *d = nullptr;
+  SK_HIP(hipMalloc(&d, count * esz));
+  launch_debug_stream(s, layer, stream_id, start, count, aux, d, nullptr);
+  hipError_t e = hipMemcpy(host_out, d, count * esz, hipMemcpyDeviceToHost);
+  (void)hipFree(d);
+  if (e != hipSuccess) return fail(SK_EHIP, std::string("debug stream: ") + hipGetErrorString(e));
+  return SK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,1158 @@
+// sk_fwht.hip -- Walsh-Hadamard based sketch kernels for gfx950 (wave64).
+//
+// Kinds: FJL (eq. ailon_chazelle), FFD (eq. fastfood, transposed), AFFD
+// (eq. bami) and AFJL (eq. frikadel).  Conventions shared by every kernel:
+//  - 256 threads per workgroup (four wave64 wavefronts);
+//  - H is the normalised Walsh-Hadamard matrix; a full transform of length
+//    2^m is a chain of LDS-tiled radix-2 passes whose per-pass scales multiply
+//    to 2^{-m/2};
+//  - random signs, Gaussians, sample positions and block permutations are
+//    regenerated from (seed, layer, stream, index) (sk_device.h); digit
+//    permutations of at most 1024 entries are small tables built at creation
+//    (the O(A+B) lookups of Sec. 3, "Removing the lookup bottleneck");
+//  - no floating-point atomics: every output element has one writer and a
+//    fixed summation order.
+#include "sk_launch.h"
+
+namespace sk {
+
+#define SK_CHECK_LAUNCH() (void)hipGetLastError()
+
+// log2 of a power of two held in 64 bits.
+static int log2_exact(int64_t v) {
+  int l = 0;
+  while ((1ll << l) < v) ++l;
+  return l;
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+__device__ __forceinline__ void store_out(void *out, int out_dtype, int64_t i, float v) {
+  if (out_dtype == SK_BF16)
+    ((uint16_t *)out)[i] = f32_to_bf16(v);
+  else
+    ((float *)out)[i] = v;
+}
+
+// Load up to 4 consecutive input elements starting at element e of a vector
+// whose valid prefix has `lim` (>= 1) elements from e on; missing -> 0.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void load4(const void *x, int64_t e, int64_t lim, float v[4]) {
+  if (VEC && lim >= 4) {
+    if (BF16) {
+      const uint2 u = *(const uint2 *)((const uint16_t *)x + e);
+      v[0] = __uint_as_float(u.x << 16);
+      v[1] = __uint_as_float(u.x & 0xFFFF0000u);
+      v[2] = __uint_as_float(u.y << 16);
+      v[3] = __uint_as_float(u.y & 0xFFFF0000u);
+    } else {
+      const float4 f = *(const float4 *)((const float *)x + e);
+      v[0] = f.x;
+      v[1] = f.y;
+      v[2] = f.z;
+      v[3] = f.w;
+    }
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (q < lim)
+      v[q] = BF16 ? bf16_to_f32(((const uint16_t *)x)[e + q]) : ((const float *)x)[e + q];
+    else
+      v[q] = 0.0f;
+  }
+}
+
+// In-place unnormalised radix-2 Walsh-Hadamard transform along the rows of an
+// LDS tile s[r << lgcs | c], 2^lgrows rows, 2^lgcs columns.  Ends synchronised.
+__device__ void lds_fwht(float *s, int lgrows, int lgcs) {
+  const int npairs = 1 << (lgrows - 1 + lgcs);
+  const int cmask = (1 << lgcs) - 1;
+  for (int st = 0; st < lgrows; ++st) {
+    __syncthreads();
+    const int hmask = (1 << st) - 1;
+    for (int p = threadIdx.x; p < npairs; p += blockDim.x) {
+      const int q = p >> lgcs, c = p & cmask;
+      const int r = ((q & ~hmask) << 1) | (q & hmask);
+      float *a = s + ((r << lgcs) | c);
+      float *b = a + (1 << (st + lgcs));
+      const float u = *a, w = *b;
+      *a = u + w;
+      *b = u - w;
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Generic pass: transform along index bits [lo, lo + w) of each vector.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_fwht_pass(float *data, int lgn, int lo, int w, int lgcs, float scale) {
+  extern __shared__ float s[];
+  const int64_t n = 1ll << lgn;
+  const int64_t tiles_per_vec = n >> (w + lgcs);
+  const int64_t v = blockIdx.x / tiles_per_vec;
+  const int64_t tv = blockIdx.x - v * tiles_per_vec;
+  const int lgcb = lo - lgcs;  // column blocks per high index
+  const int64_t a = tv >> lgcb;
+  const int64_t cb = tv & ((1ll << lgcb) - 1);
+  float *base = data + v * n + (a << (lo + w)) + (cb << lgcs);
+  const int total = 1 << (w + lgcs);
+  const int cmask = (1 << lgcs) - 1;
+  for (int e = threadIdx.x; e < total; e += 256) s[e] = base[((int64_t)(e >> lgcs) << lo) + (e & cmask)];
+  lds_fwht(s, w, lgcs);
+  for (int e = threadIdx.x; e < total; e += 256) base[((int64_t)(e >> lgcs) << lo) + (e & cmask)] = s[e] * scale;
+}
+
+void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) {
+  if (lgn == 0 || V == 0) return;
+  int lo = 0;
+  while (lo < lgn) {
+    int w, lgcs;
+    if (lo == 0) {
+      w = lgn < 13 ? lgn : 13;
+      lgcs = 0;
+    } else {
+      w = (lgn - lo) < 8 ? (lgn - lo) : 8;
+      lgcs = 13 - w;
+      if (lgcs > lo) lgcs = lo;
+    }
+    const int64_t tiles = V * ((1ll << lgn) >> (w + lgcs));
+    const float scale = (float)(1.0 / sqrt((double)(1ll << w)));
+    const size_t shm = sizeof(float) << (w + lgcs);
+    hipLaunchKernelGGL(k_fwht_pass, dim3((unsigned)tiles), dim3(256), shm, st, data, lgn, lo, w, lgcs, scale);
+    SK_CHECK_LAUNCH();
+    lo += w;
+  }
+}
+
+__global__ void k_fill_zero(float *p, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.0f;
+}
+
+void launch_fill_zero(float *p, int64_t n, hipStream_t st) {
+  if (n <= 0) return;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, st, p, n);
+  SK_CHECK_LAUNCH();
+}
+
+// ===========================================================================
+// AFJL.  With w = Scatter_pi1(B x), the restriction to the first D rows of a
+// normalised Hadamard transform of length N' is sqrt(D/N') H_D fold_D(w)
+// (fold_D sums the N'/D consecutive length-D chunks; this follows from the
+// Hadamard definition), so AFJL(x) = g_{<D} . H_D fold_D(Scatter_pi1 B x).
+// The digit structure of pi1 makes fold_D a row routing: row h (the L = 1024
+// consecutive coordinates sharing all digits but the last) lands in
+// destination row r = pi1_{K-2}(h mod dk1) mod R of an R x L accumulator
+// (D = R L), its columns permuted by pi1_{K-1}.  H_D = H_R (x) H_L: the fold
+// kernel applies H_L to each destination row, the tail kernel H_R, G and the
+// sum over layers.  For D < L the row is folded once more to D columns.
+// ===========================================================================
+template <int BT, bool BF16, bool VEC>
+__global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ items,
+                                                   const LayerDesc *__restrict__ layers,
+                                                   const uint16_t *__restrict__ ptab, PtrPack ptrs, int first_layer,
+                                                   int64_t batch, int64_t b_begin, int64_t bc, int item_begin, int R,
+                                                   int Lw, float *__restrict__ part, Key key) {
+  __shared__ float s[BT][1024];
+  const FoldItem it = items[item_begin + blockIdx.x];
+  const LayerDesc &ld = layers[it.layer];
+  const int64_t n = ld.n;
+  const int L = ld.L;
+  const int tid = threadIdx.x;
+  const int col0 = tid * 4;
+  const bool active = col0 < L;
+  const int bt0 = blockIdx.y * BT;
+  const void *xp = ptrs.p[it.layer - first_layer];
+  const int nb = (int)((batch - b_begin - bt0) < BT ? (batch - b_begin - bt0) : BT);  // rows of this tile
+  float acc[BT][4];
+#pragma unroll
+  for (int b = 0; b < BT; ++b)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[b][q] = 0.0f;
+
+  const int nk = R > 1 ? ld.dk1 / R : 1;
+  const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
+  if (active) {
+    for (int t = it.t0; t < it.t1; ++t) {
+      int64_t h;
+      if (R == 1) {
+        h = t;
+      } else {
+        const int htop = t / nk;
+        const int k = t - htop * nk;
+        h = (int64_t)htop * ld.dk1 + inv_k1[it.r + k * R];
+      }
+      if (h >= ld.rows_live) continue;
+      const int64_t j0 = h * L + col0;
+      const int64_t lim = n - j0;
+      if (lim <= 0) continue;
+      const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+      float v[BT][4];
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + j0, lim, v[b]);
+      }
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        if (b < nb) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[b][q] += flip(v[b][q], (bits >> q) & 1u);
+        }
+      }
+    }
+    // route the columns through pi1 of the last digit
+    const uint16_t *fwd_k = ptab + ld.poff[0][0][ld.K - 1];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int pc = fwd_k[col0 + q];
+#pragma unroll
+      for (int b = 0; b < BT; ++b) s[b][pc] = acc[b][q];
+    }
+  }
+  __syncthreads();
+  int lgw;
+  if (Lw < L) {
+    // fold the permuted row to Lw = D columns
+    float tmp[BT * 2];
+    const int tot = BT * Lw;
+    int cnt = 0;
+    for (int e = tid; e < tot; e += 256, ++cnt) {
+      const int b = e / Lw, c = e - (e / Lw) * Lw;
+      float v = 0.0f;
+      for (int k = 0; k < L; k += Lw) v += s[b][k + c];
+      tmp[cnt] = v;
+    }
+    __syncthreads();
+    cnt = 0;
+    for (int e = tid; e < tot; e += 256, ++cnt) s[e / Lw][e - (e / Lw) * Lw] = tmp[cnt];
+    __syncthreads();
+  }
+  lgw = 31 - __clz(Lw);
+  for (int b = 0; b < BT; ++b) {
+    // each row is a separate transform: reuse the tile routine with one column
+    lds_fwht(&s[b][0], lgw, 0);
+  }
+  const float sc = rsqrtf((float)Lw);
+  const int64_t slot = blockIdx.x;
+  for (int e = tid; e < nb * Lw; e += 256) {
+    const int b = e / Lw, c = e - (e / Lw) * Lw;
+    part[(slot * bc + bt0 + b) * Lw + c] = s[b][c] * sc;
+  }
+}
+
+void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,
+                      int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st) {
+  constexpr int BT = 8;
+  const int nitems = item_end - item_begin;
+  if (nitems <= 0) return;
+  const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
+  dim3 grid((unsigned)nitems, (unsigned)((rows + BT - 1) / BT));
+#define SK_FOLD(BF, VE)                                                                                              \
+  hipLaunchKernelGGL((k_afjl_fold<BT, BF, VE>), grid, dim3(256), 0, st, s->d_items, s->d_layers, s->d_ptab, ptrs,   \
+                     first_layer, batch, b_begin, bc, item_begin, s->R, s->Lw, part, s->key)
+  if (dtype == SK_BF16) {
+    if (vec) SK_FOLD(true, true); else SK_FOLD(true, false);
+  } else {
+    if (vec) SK_FOLD(false, true); else SK_FOLD(false, false);
+  }
+#undef SK_FOLD
+  SK_CHECK_LAUNCH();
+}
+
+// Tail: out[b, r' Lw + c] = sum_l g_l[r' Lw + c] * (H_R T_l[b, :, c])[r'],
+// T_l the sum of a layer's fold partials.
+template <int PER>
+__global__ __launch_bounds__(256) void k_afjl_tail(const LayerDesc *__restrict__ layers, const int2 *__restrict__ rslot,
+                                                   const float *__restrict__ part, const float *__restrict__ gtab,
+                                                   int l_begin, int l_end, int item_begin, int lgR, int Lw,
+                                                   int lgcs, int64_t D, int64_t bc, int64_t b_begin,
+                                                   int64_t batch, float *__restrict__ out, int accumulate) {
+  extern __shared__ float s[];
+  const int CS = 1 << lgcs;
+  const int R = 1 << lgR;
+  const int c0 = blockIdx.x * CS;
+  const int bl = blockIdx.y;
+  const int64_t b = b_begin + bl;
+  if (b >= batch) return;
+  const int tot = R * CS;
+  float acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.0f;
+  const float sc = rsqrtf((float)R);
+  for (int l = l_begin; l < l_end; ++l) {
+    const LayerDesc &ld = layers[l];
+    const int2 *rs = rslot + ld.rslot_off;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
+      if (e < tot) {
+        const int r = e >> lgcs, c = e & (CS - 1);
+        const int2 q = rs[r];
+        float v = 0.0f;
+        for (int k = 0; k < q.y; ++k) v += part[((int64_t)(q.x - item_begin + k) * bc + bl) * Lw + c0 + c];
+        s[e] = v;
+      }
+    }
+    if (R > 1)
+      lds_fwht(s, lgR, lgcs);
+    else
+      __syncthreads();
+    const float *g = gtab + (int64_t)l * D;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
+      if (e < tot) {
+        const int r = e >> lgcs, c = e & (CS - 1);
+        acc[i] += g[(int64_t)r * Lw + c0 + c] * (s[e] * sc);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = threadIdx.x + i * 256;
+    if (e < tot) {
+      const int r = e >> lgcs, c = e & (CS - 1);
+      const int64_t o = b * D + (int64_t)r * Lw + c0 + c;
+      out[o] = accumulate ? out[o] + acc[i] : acc[i];
+    }
+  }
+}
+
+void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
+                      int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st) {
+  const int R = s->R, Lw = s->Lw;
+  int lgR = 31 - __builtin_clz(R);
+  // tile of R rows x CS columns, at most 4096 elements
+  int lgcs = 12 - lgR;
+  const int lgLw = 31 - __builtin_clz(Lw);
+  if (lgcs > lgLw) lgcs = lgLw;
+  if (lgcs < 0) lgcs = 0;
+  const int tot = R << lgcs;
+  const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
+  dim3 grid((unsigned)(Lw >> lgcs), (unsigned)rows);
+  const size_t shm = sizeof(float) * tot;
+  if (tot <= 256 * 4)
+    hipLaunchKernelGGL(k_afjl_tail<4>, grid, dim3(256), shm, st, s->d_layers, s->d_rslot, part, s->d_gtab, l_begin,
+                       l_end, item_begin, lgR, Lw, lgcs, s->D, bc, b_begin, batch, out, (int)accumulate);
+  else
+    hipLaunchKernelGGL(k_afjl_tail<16>, grid, dim3(256), shm, st, s->d_layers, s->d_rslot, part, s->d_gtab, l_begin,
+                       l_end, item_begin, lgR, Lw, lgcs, s->D, bc, b_begin, batch, out, (int)accumulate);
+  SK_CHECK_LAUNCH();
+}
+
+// AFJL transpose.  H_N' R_D^T u = sqrt(D/N') tile(H_D u), so
+// AFJL^T z = B Gather_pi1 tile(H_D (g . z)): out[j] = b_j V[pi1(j) mod D].
+__global__ void k_afjl_T_prep(const float *__restrict__ gtab, int layer, const float *__restrict__ z, int64_t D,
+                              int64_t b_begin, int64_t bc, float *__restrict__ w) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= D) return;
+  const float g = gtab[(int64_t)layer * D + i];
+  for (int64_t v = 0; v < bc; ++v) w[v * D + i] = g * z[(b_begin + v) * D + i];
+}
+
+void launch_afjl_T_prep(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                        hipStream_t st) {
+  hipLaunchKernelGGL(k_afjl_T_prep, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_gtab, layer, z,
+                     s->D, b_begin, bc, w);
+  SK_CHECK_LAUNCH();
+}
+
+// One workgroup per source row h of the layer; each thread owns 4 columns.
+__global__ __launch_bounds__(256) void k_afjl_T_out(const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, int layer,
+                                                    const float *__restrict__ w, int64_t D, int R, int Lw,
+                                                    int64_t bc, int64_t b_begin, void *__restrict__ out,
+                                                    int out_dtype, const float *__restrict__ theta0, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t h = blockIdx.x;
+  const int L = ld.L;
+  const int col0 = threadIdx.x * 4;
+  if (col0 >= L) return;
+  const int64_t j0 = h * L + col0;
+  const int64_t lim = ld.n - j0;
+  if (lim <= 0) return;
+  int rbase = 0;
+  if (R > 1) {
+    const uint16_t *fk1 = ptab + ld.poff[0][0][ld.K - 2];
+    rbase = ((int)fk1[h & (ld.dk1 - 1)] & (R - 1)) * L;
+  }
+  const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
+  int idx[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) idx[q] = R > 1 ? rbase + fk[col0 + q] : (fk[col0 + q] & (Lw - 1));
+  const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+  float th[4] = {0.f, 0.f, 0.f, 0.f};
+  if (theta0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < lim) th[q] = theta0[j0 + q];
+  }
+  for (int64_t v = 0; v < bc; ++v) {
+    const float *wv = w + v * D;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < lim) store_out(out, out_dtype, (b_begin + v) * ld.n + j0 + q, flip(wv[idx[q]], (bits >> q) & 1u) + th[q]);
+    }
+  }
+}
+
+void launch_afjl_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  hipLaunchKernelGGL(k_afjl_T_out, dim3((unsigned)ld.rows_live), dim3(256), 0, st, s->d_layers, s->d_ptab, layer, w,
+                     s->D, s->R, s->Lw, bc, b_begin, out, out_dtype, theta0, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// ===========================================================================
+// AFFD.  w = Scatter_pi1(B x) is written in full (padded rows as zeros) by a
+// row kernel that reads source row pi1^{-1}(row) of x; then H_N' (generic
+// passes); then, since only the D coordinates pi2(c), c < D, of the second
+// transform are needed and those share the top digits h* = pi2_top(0), the
+// top digits are contracted first: F[q] = Ttop^{-1/2} sum_t (-1)^{<h*, t>}
+// g[t, q] v[t, q] (G fused), followed by H over the low block and the
+// gather of pi2_low(c).
+// ===========================================================================
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_affd_prolog(const LayerDesc *__restrict__ layers,
+                                                     const uint16_t *__restrict__ ptab, int layer,
+                                                     const void *__restrict__ x, int64_t b_begin, int64_t bc,
+                                                     float *__restrict__ w, Key key) {
+  __shared__ float s[1024];
+  const LayerDesc &ld = layers[layer];
+  const int64_t prow = blockIdx.x;
+  const int L = ld.L;
+  // source row = pi1^{-1} over the row digits 0..K-2
+  int64_t srow = 0, stride = 1;
+  for (int k = ld.K - 2; k >= 0; --k) {
+    const int64_t dig = (prow / stride) & ((1ll << ld.lg[k]) - 1);
+    srow += (int64_t)ptab[ld.poff[0][1][k] + dig] * stride;
+    stride <<= ld.lg[k];
+  }
+  const int col0 = threadIdx.x * 4;
+  const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
+  const int64_t j0 = srow * L + col0;
+  const int64_t lim = ld.n - j0;
+  const bool live = srow < ld.rows_live && col0 < L && lim > 0;
+  uint32_t bits = 0;
+  int pc[4] = {0, 0, 0, 0};
+  if (col0 < L) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) pc[q] = fk[col0 + q];
+  }
+  if (live) bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+  for (int64_t v = 0; v < bc; ++v) {
+    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    if (live) {
+      load4<BF16, false>(x, (b_begin + v) * ld.n + j0, lim, val);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) val[q] = flip(val[q], (bits >> q) & 1u);
+    }
+    if (col0 < L) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s[pc[q]] = val[q];
+    }
+    __syncthreads();
+    float *dst = w + v * ld.np + prow * L;
+    for (int c = threadIdx.x; c < L; c += 256) dst[c] = s[c];
+    __syncthreads();
+  }
+}
+
+void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                        float *w, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const unsigned rows = (unsigned)(ld.np / ld.L);
+  if (dtype == SK_BF16)
+    hipLaunchKernelGGL(k_affd_prolog<true>, dim3(rows), dim3(256), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin,
+                       bc, w, s->key);
+  else
+    hipLaunchKernelGGL(k_affd_prolog<false>, dim3(rows), dim3(256), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin,
+                       bc, w, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// F[v, q] over q < 2^lo_len_lg; thread: 4 consecutive q, 8 vectors.
+__global__ __launch_bounds__(256) void k_affd_fold(const LayerDesc *__restrict__ layers, int layer,
+                                                   const float *__restrict__ w, int64_t bc, float *__restrict__ f,
+                                                   Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t lo_len = 1ll << ld.lo_len_lg;
+  const int64_t q0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  if (q0 >= lo_len) return;
+  const int64_t v0 = blockIdx.y * 8;
+  const int nv = (int)((bc - v0) < 8 ? (bc - v0) : 8);
+  const int64_t ttop = ld.np >> ld.lo_len_lg;
+  float acc[8][4];
+#pragma unroll
+  for (int v = 0; v < 8; ++v)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[v][i] = 0.0f;
+  for (int64_t t = 0; t < ttop; ++t) {
+    const uint32_t sgn = __popcll((uint64_t)t & ld.hstar) & 1u;
+    const int64_t j = t * lo_len + q0;
+    float g[4];
+    gauss4((uint64_t)j >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      if (v < nv) {
+        const float4 x = *(const float4 *)(w + (v0 + v) * ld.np + j);
+        acc[v][0] += flip(g[0] * x.x, sgn);
+        acc[v][1] += flip(g[1] * x.y, sgn);
+        acc[v][2] += flip(g[2] * x.z, sgn);
+        acc[v][3] += flip(g[3] * x.w, sgn);
+      }
+    }
+  }
+  const float sc = (float)(1.0 / sqrt((double)ttop));
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    if (v < nv) {
+      float4 o = make_float4(acc[v][0] * sc, acc[v][1] * sc, acc[v][2] * sc, acc[v][3] * sc);
+      *(float4 *)(f + (v0 + v) * lo_len + q0) = o;
+    }
+  }
+}
+
+void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const int64_t lo_len = 1ll << ld.lo_len_lg;
+  dim3 grid((unsigned)((lo_len / 4 + 255) / 256), (unsigned)((bc + 7) / 8));
+  hipLaunchKernelGGL(k_affd_fold, grid, dim3(256), 0, st, s->d_layers, layer, w, bc, f, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// pi2 on the low block: index c < D -> position in F.
+__device__ __forceinline__ int64_t pi2_low(const LayerDesc &ld, const uint16_t *ptab, int64_t c, int64_t D) {
+  const int64_t L = ld.L;
+  if (D > L) {
+    const int64_t a = c >> ld.lgL, b = c & (L - 1);
+    return (int64_t)ptab[ld.poff[1][0][ld.K - 2] + a] * L + ptab[ld.poff[1][0][ld.K - 1] + b];
+  }
+  return ptab[ld.poff[1][0][ld.K - 1] + c];
+}
+
+__global__ void k_affd_gather(const LayerDesc *__restrict__ layers, const uint16_t *__restrict__ ptab, int layer,
+                              const float *__restrict__ f, int64_t D, int64_t b_begin, int64_t bc,
+                              float *__restrict__ out, int accumulate) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (c >= D) return;
+  const int64_t lo_len = 1ll << ld.lo_len_lg;
+  const int64_t p = pi2_low(ld, ptab, c, D);
+  const float sc = (float)sqrt((double)ld.np / (double)D);
+  for (int64_t v = 0; v < bc; ++v) {
+    const float val = sc * f[v * lo_len + p];
+    float *o = out + (b_begin + v) * D + c;
+    *o = accumulate ? *o + val : val;
+  }
+}
+
+void launch_affd_gather(const sk_sketch *s, int layer, const float *f, int64_t b_begin, int64_t bc, float *out,
+                        bool accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(k_affd_gather, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_layers, s->d_ptab,
+                     layer, f, s->D, b_begin, bc, out, (int)accumulate);
+  SK_CHECK_LAUNCH();
+}
+
+// AFFD transpose, first step: Scatter_pi2 R_D^T z into a zeroed w.
+__global__ void k_affd_T_scatter(const LayerDesc *__restrict__ layers, const uint16_t *__restrict__ ptab, int layer,
+                                 const float *__restrict__ z, int64_t D, int64_t b_begin, int64_t bc,
+                                 float *__restrict__ w) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (c >= D) return;
+  const int64_t p = ((int64_t)ld.hstar << ld.lo_len_lg) + pi2_low(ld, ptab, c, D);
+  for (int64_t v = 0; v < bc; ++v) w[v * ld.np + p] = z[(b_begin + v) * D + c];
+}
+
+void launch_affd_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(k_affd_T_scatter, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_layers,
+                     s->d_ptab, layer, z, s->D, b_begin, bc, w);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_mul_gauss(const LayerDesc *__restrict__ layers, int layer, float *__restrict__ w, int64_t bc,
+                            Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t j = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  if (j >= ld.np) return;
+  float g[4];
+  gauss4((uint64_t)j >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+  for (int64_t v = 0; v < bc; ++v) {
+    float4 *p = (float4 *)(w + v * ld.np + j);
+    float4 x = *p;
+    x.x *= g[0];
+    x.y *= g[1];
+    x.z *= g[2];
+    x.w *= g[3];
+    *p = x;
+  }
+}
+
+void launch_mul_gauss(const sk_sketch *s, int layer, float *w, int64_t bc, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  hipLaunchKernelGGL(k_mul_gauss, dim3((unsigned)((ld.np / 4 + 255) / 256)), dim3(256), 0, st, s->d_layers, layer, w,
+                     bc, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// out[j] = sqrt(N'/D) b_j w[pi1(j)] (+ theta0[j]); one workgroup per source row.
+__global__ __launch_bounds__(256) void k_affd_T_out(const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, int layer,
+                                                    const float *__restrict__ w, int64_t D, int64_t bc,
+                                                    int64_t b_begin, void *__restrict__ out, int out_dtype,
+                                                    const float *__restrict__ theta0, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t h = blockIdx.x;
+  const int L = ld.L;
+  const int col0 = threadIdx.x * 4;
+  if (col0 >= L) return;
+  const int64_t j0 = h * L + col0;
+  const int64_t lim = ld.n - j0;
+  if (lim <= 0) return;
+  int64_t prow = 0, stride = 1;
+  for (int k = ld.K - 2; k >= 0; --k) {
+    const int64_t dig = (h / stride) & ((1ll << ld.lg[k]) - 1);
+    prow += (int64_t)ptab[ld.poff[0][0][k] + dig] * stride;
+    stride <<= ld.lg[k];
+  }
+  const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
+  int64_t idx[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) idx[q] = prow * L + fk[col0 + q];
+  const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+  const float sc = (float)sqrt((double)ld.np / (double)D);
+  float th[4] = {0.f, 0.f, 0.f, 0.f};
+  if (theta0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < lim) th[q] = theta0[j0 + q];
+  }
+  for (int64_t v = 0; v < bc; ++v) {
+    const float *wv = w + v * ld.np;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < lim)
+        store_out(out, out_dtype, (b_begin + v) * ld.n + j0 + q, flip(sc * wv[idx[q]], (bits >> q) & 1u) + th[q]);
+  }
+}
+
+void launch_affd_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  hipLaunchKernelGGL(k_affd_T_out, dim3((unsigned)ld.rows_live), dim3(256), 0, st, s->d_layers, s->d_ptab, layer, w,
+                     s->D, bc, b_begin, out, out_dtype, theta0, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// ===========================================================================
+// FJL: w = B x zero-padded, H_N' (generic passes), y_i = sqrt(N'/D) g_i w[idx_i].
+// ===========================================================================
+template <bool BF16>
+__global__ void k_fjl_prolog(const LayerDesc *__restrict__ layers, int layer, const void *__restrict__ x,
+                             int64_t b_begin, int64_t bc, float *__restrict__ w, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t j0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  if (j0 >= ld.np) return;
+  const int64_t lim = ld.n - j0;
+  uint32_t bits = 0;
+  if (lim > 0) bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+  for (int64_t v = 0; v < bc; ++v) {
+    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    if (lim > 0) load4<BF16, false>(x, (b_begin + v) * ld.n + j0, lim, val);
+    float4 o = make_float4(flip(val[0], bits & 1u), flip(val[1], (bits >> 1) & 1u), flip(val[2], (bits >> 2) & 1u),
+                           flip(val[3], (bits >> 3) & 1u));
+    *(float4 *)(w + v * ld.np + j0) = o;
+  }
+}
+
+void launch_fjl_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                       float *w, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  dim3 grid((unsigned)((ld.np / 4 + 255) / 256));
+  if (dtype == SK_BF16)
+    hipLaunchKernelGGL(k_fjl_prolog<true>, grid, dim3(256), 0, st, s->d_layers, layer, x, b_begin, bc, w, s->key);
+  else
+    hipLaunchKernelGGL(k_fjl_prolog<false>, grid, dim3(256), 0, st, s->d_layers, layer, x, b_begin, bc, w, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_fjl_gather(const LayerDesc *__restrict__ layers, const float *__restrict__ gtab, int layer,
+                             const float *__restrict__ w, int64_t D, int64_t b_begin, int64_t bc,
+                             float *__restrict__ out, int accumulate, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= D) return;
+  const uint32_t idx = sample_index((uint64_t)i, (uint32_t)ld.layer_id, key, (uint64_t)ld.np);
+  const float g = gtab[(int64_t)layer * D + i] * (float)sqrt((double)ld.np / (double)D);
+  for (int64_t v = 0; v < bc; ++v) {
+    const float val = g * w[v * ld.np + idx];
+    float *o = out + (b_begin + v) * D + i;
+    *o = accumulate ? *o + val : val;
+  }
+}
+
+void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
+                       bool accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(k_fjl_gather, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_layers, s->d_gtab,
+                     layer, w, s->D, b_begin, bc, out, (int)accumulate, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// FJL transpose: w[pos] = sum over the samples at pos (in id order) of g_i z_i.
+__global__ void k_fjl_T_scatter(const float *__restrict__ gtab, int layer, const uint32_t *__restrict__ pos,
+                                const uint32_t *__restrict__ seg, const uint32_t *__restrict__ smp, int64_t nuniq,
+                                int64_t np, const float *__restrict__ z, int64_t D, int64_t b_begin, int64_t bc,
+                                float *__restrict__ w) {
+  const int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (u >= nuniq) return;
+  const uint32_t p = pos[u], s0 = seg[u], s1 = seg[u + 1];
+  const float *g = gtab + (int64_t)layer * D;
+  for (int64_t v = 0; v < bc; ++v) {
+    float acc = 0.0f;
+    for (uint32_t k = s0; k < s1; ++k) {
+      const uint32_t i = smp[k];
+      acc += g[i] * z[(b_begin + v) * D + i];
+    }
+    w[v * np + p] = acc;
+  }
+}
+
+void launch_fjl_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                          hipStream_t st) {
+  const int64_t u0 = s->fjl_uoff[layer], nuniq = s->fjl_uoff[layer + 1] - u0;
+  const int64_t seg0 = u0 + layer;  // one sentinel per layer
+  hipLaunchKernelGGL(k_fjl_T_scatter, dim3((unsigned)((nuniq + 255) / 256)), dim3(256), 0, st, s->d_gtab, layer,
+                     s->d_fjl_pos + u0, s->d_fjl_seg + seg0, s->d_fjl_smp, nuniq, s->layers[layer].np, z, s->D,
+                     b_begin, bc, w);
+  SK_CHECK_LAUNCH();
+}
+
+// out[j] = scale b_j w[j] (+ theta0[j]) for j < n.
+__global__ void k_signed_out(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ w,
+                             int64_t b_begin, int64_t bc, void *__restrict__ out, int out_dtype,
+                             const float *__restrict__ theta0, float scale, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t j0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int64_t lim = ld.n - j0;
+  if (lim <= 0) return;
+  const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
+  float th[4] = {0.f, 0.f, 0.f, 0.f};
+  if (theta0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < lim) th[q] = theta0[j0 + q];
+  }
+  for (int64_t v = 0; v < bc; ++v) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < lim)
+        store_out(out, out_dtype, (b_begin + v) * ld.n + j0 + q,
+                  flip(scale * w[v * ld.np + j0 + q], (bits >> q) & 1u) + th[q]);
+  }
+}
+
+void launch_signed_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, float scale, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  hipLaunchKernelGGL(k_signed_out, dim3((unsigned)((ld.n / 4 + 1 + 255) / 256)), dim3(256), 0, st, s->d_layers,
+                     layer, w, b_begin, bc, out, out_dtype, theta0, scale, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// ===========================================================================
+// FFD.  Forward (the explicit sketch) y = sum_b B_b H_D Pi_b^T G_b H_D x_b with
+// (Pi v)_i = v_{pi_b(i)}; transpose (the feature map of eq. fastfood) block b
+// = H_D G_b Pi_b H_D B_b z.  Blocks past the data are all zero (skipped).
+// Small D: a whole block lives in LDS.  Large D: generic passes over a
+// workspace holding every live block of every vector.
+// ===========================================================================
+int64_t ffd_live_blocks(const sk_sketch *s, int layer) {
+  const LayerDesc &ld = s->layers[layer];
+  return (ld.n + s->D - 1) / s->D;
+}
+
+constexpr int kFfdGroup = 8;  // blocks per workgroup (small D)
+
+int64_t ffd_small_groups(const sk_sketch *s, int layer) {
+  return (ffd_live_blocks(s, layer) + kFfdGroup - 1) / kFfdGroup;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_ffd_small_fwd(const LayerDesc *__restrict__ layers, int layer,
+                                                       const void *__restrict__ x, int lgD, int64_t b_begin,
+                                                       int64_t bc, float *__restrict__ part, int64_t slot0,
+                                                       int64_t nlive, Key key) {
+  extern __shared__ float sm[];
+  const int D = 1 << lgD;
+  float *s = sm;
+  float *u = sm + D;
+  const LayerDesc &ld = layers[layer];
+  const int64_t v = blockIdx.y;
+  const int64_t blk0 = (int64_t)blockIdx.x * kFfdGroup;
+  const int per = D / 256 > 0 ? D / 256 : 1;
+  float acc[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) acc[i] = 0.0f;
+  const float inv = 1.0f / (float)D;
+  for (int64_t b = blk0; b < blk0 + kFfdGroup && b < nlive; ++b) {
+    const int64_t base = b * D;
+    for (int i = threadIdx.x; i < D; i += 256) {
+      const int64_t j = base + i;
+      float val = 0.0f;
+      if (j < ld.n) {
+        const int64_t e = (b_begin + v) * ld.n + j;
+        val = BF16 ? bf16_to_f32(((const uint16_t *)x)[e]) : ((const float *)x)[e];
+      }
+      s[i] = val;
+    }
+    lds_fwht(s, lgD, 0);
+    const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
+    for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
+      float g[4];
+      gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u[perm_fwd(pk, (uint32_t)(i4 + q))] = g[q] * s[i4 + q];
+    }
+    lds_fwht(u, lgD, 0);
+    for (int k = 0; k < per; ++k) {
+      const int i = threadIdx.x + k * 256;
+      if (i < D) {
+        const uint32_t bit = (sign_word((uint64_t)(base + i), (uint32_t)ld.layer_id, key) >> ((base + i) & 31)) & 1u;
+        acc[k] += flip(u[i] * inv, bit);
+      }
+    }
+    __syncthreads();
+  }
+  float *dst = part + ((slot0 + blockIdx.x) * bc + v) * D;
+  for (int k = 0; k < per; ++k) {
+    const int i = threadIdx.x + k * 256;
+    if (i < D) dst[i] = acc[k];
+  }
+}
+
+void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                          float *part, int64_t slot0, int64_t groups, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  const size_t shm = 2 * sizeof(float) * s->D;
+  dim3 grid((unsigned)groups, (unsigned)bc);
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  if (dtype == SK_BF16)
+    hipLaunchKernelGGL(k_ffd_small_fwd<true>, grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, b_begin, bc, part,
+                       slot0, nlive, s->key);
+  else
+    hipLaunchKernelGGL(k_ffd_small_fwd<false>, grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, b_begin, bc,
+                       part, slot0, nlive, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_reduce_partials(const float *__restrict__ part, int64_t nslots, int64_t bc, int64_t D,
+                                  int64_t b_begin, float *__restrict__ out, int accumulate) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= bc * D) return;
+  const int64_t v = i / D, c = i - v * D;
+  float acc = 0.0f;
+  for (int64_t k = 0; k < nslots; ++k) acc += part[(k * bc + v) * D + c];
+  float *o = out + (b_begin + v) * D + c;
+  *o = accumulate ? *o + acc : acc;
+}
+
+void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64_t D, int64_t b_begin, float *out,
+                            bool accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(k_reduce_partials, dim3((unsigned)((bc * D + 255) / 256)), dim3(256), 0, st, part, nslots, bc, D,
+                     b_begin, out, (int)accumulate);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ __launch_bounds__(256) void k_ffd_small_T(const LayerDesc *__restrict__ layers, int layer,
+                                                     const float *__restrict__ z, int lgD, int64_t b_begin,
+                                                     void *__restrict__ out, int out_dtype,
+                                                     const float *__restrict__ theta0, Key key) {
+  extern __shared__ float sm[];
+  const int D = 1 << lgD;
+  float *s = sm;
+  float *u = sm + D;
+  const LayerDesc &ld = layers[layer];
+  const int64_t b = blockIdx.x;
+  const int64_t v = blockIdx.y;
+  const int64_t base = b * D;
+  for (int i = threadIdx.x; i < D; i += 256) {
+    const uint32_t bit = (sign_word((uint64_t)(base + i), (uint32_t)ld.layer_id, key) >> ((base + i) & 31)) & 1u;
+    s[i] = flip(z[(b_begin + v) * D + i], bit);
+  }
+  lds_fwht(s, lgD, 0);
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
+  for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
+    float g[4];
+    gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) u[i4 + q] = g[q] * s[perm_fwd(pk, (uint32_t)(i4 + q))];
+  }
+  lds_fwht(u, lgD, 0);
+  const float inv = 1.0f / (float)D;
+  for (int i = threadIdx.x; i < D; i += 256) {
+    const int64_t j = base + i;
+    if (j < ld.n) store_out(out, out_dtype, (b_begin + v) * ld.n + j, u[i] * inv + (theta0 ? theta0[j] : 0.0f));
+  }
+}
+
+void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
+                        int out_dtype, const float *theta0, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  const size_t shm = 2 * sizeof(float) * s->D;
+  dim3 grid((unsigned)ffd_live_blocks(s, layer), (unsigned)bc);
+  hipLaunchKernelGGL(k_ffd_small_T, grid, dim3(256), shm, st, s->d_layers, layer, z, lgD, b_begin, out, out_dtype,
+                     theta0, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// --- large D: workspace w[v][bb][i], bb < nlive ---
+template <bool BF16>
+__global__ void k_ffd_copy_blocks(const LayerDesc *__restrict__ layers, int layer, const void *__restrict__ x,
+                                  int64_t span, int64_t b_begin, float *__restrict__ w) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;  // within the live span
+  if (j >= span) return;
+  const int64_t v = blockIdx.y;
+  float val = 0.0f;
+  if (j < ld.n) {
+    const int64_t e = (b_begin + v) * ld.n + j;
+    val = BF16 ? bf16_to_f32(((const uint16_t *)x)[e]) : ((const float *)x)[e];
+  }
+  w[v * span + j] = val;
+}
+
+void launch_ffd_copy_blocks(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                            float *w, hipStream_t st) {
+  const int64_t span = ffd_live_blocks(s, layer) * s->D;
+  dim3 grid((unsigned)((span + 255) / 256), (unsigned)bc);
+  if (dtype == SK_BF16)
+    hipLaunchKernelGGL(k_ffd_copy_blocks<true>, grid, dim3(256), 0, st, s->d_layers, layer, x, span, b_begin, w);
+  else
+    hipLaunchKernelGGL(k_ffd_copy_blocks<false>, grid, dim3(256), 0, st, s->d_layers, layer, x, span, b_begin, w);
+  SK_CHECK_LAUNCH();
+}
+
+// w2[v][bb][pi_b(k)] = g_{b,k} w[v][bb][k]; one thread per 4 consecutive k, all vectors.
+__global__ void k_ffd_gperm_fwd(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ w,
+                                int lgD, int64_t nlive, int64_t bc, float *__restrict__ w2, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t D = 1ll << lgD;
+  const int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int64_t bb = t >> lgD;
+  if (bb >= nlive) return;
+  const int64_t k0 = t & (D - 1);
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)bb, (uint32_t)lgD, key);
+  float g[4];
+  gauss4((uint64_t)(bb * D + k0) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+  uint32_t p[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) p[q] = perm_fwd(pk, (uint32_t)(k0 + q));
+  const int64_t span = nlive * D;
+  for (int64_t v = 0; v < bc; ++v) {
+    const float4 x = *(const float4 *)(w + v * span + t);
+    float *dst = w2 + v * span + bb * D;
+    dst[p[0]] = g[0] * x.x;
+    dst[p[1]] = g[1] * x.y;
+    dst[p[2]] = g[2] * x.z;
+    dst[p[3]] = g[3] * x.w;
+  }
+}
+
+void launch_ffd_gperm_fwd(const sk_sketch *s, int layer, const float *w, int64_t bc, float *w2, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  const int64_t th = nlive * s->D / 4;
+  hipLaunchKernelGGL(k_ffd_gperm_fwd, dim3((unsigned)((th + 255) / 256)), dim3(256), 0, st, s->d_layers, layer, w,
+                     lgD, nlive, bc, w2, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_ffd_sum_signed(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ w2,
+                                 int64_t D, int64_t nlive, int64_t b_begin, int64_t bc, float *__restrict__ out,
+                                 int accumulate, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= D) return;
+  const int64_t v = blockIdx.y;
+  float acc = 0.0f;
+  for (int64_t bb = 0; bb < nlive; ++bb) {
+    const int64_t j = bb * D + i;
+    const uint32_t bit = (sign_word((uint64_t)j, (uint32_t)ld.layer_id, key) >> (j & 31)) & 1u;
+    acc += flip(w2[v * nlive * D + j], bit);
+  }
+  float *o = out + (b_begin + v) * D + i;
+  *o = accumulate ? *o + acc : acc;
+}
+
+void launch_ffd_sum_signed(const sk_sketch *s, int layer, const float *w2, int64_t b_begin, int64_t bc, float *out,
+                           bool accumulate, hipStream_t st) {
+  dim3 grid((unsigned)((s->D + 255) / 256), (unsigned)bc);
+  hipLaunchKernelGGL(k_ffd_sum_signed, grid, dim3(256), 0, st, s->d_layers, layer, w2, s->D,
+                     ffd_live_blocks(s, layer), b_begin, bc, out, (int)accumulate, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_ffd_expand_z(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ z,
+                               int lgD, int64_t nlive, int64_t b_begin, float *__restrict__ w, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t D = 1ll << lgD;
+  const int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (j >= nlive * D) return;
+  const int64_t v = blockIdx.y;
+  const uint32_t bit = (sign_word((uint64_t)j, (uint32_t)ld.layer_id, key) >> (j & 31)) & 1u;
+  w[v * nlive * D + j] = flip(z[(b_begin + v) * D + (j & (D - 1))], bit);
+}
+
+void launch_ffd_expand_z(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                         hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  dim3 grid((unsigned)((nlive * s->D + 255) / 256), (unsigned)bc);
+  hipLaunchKernelGGL(k_ffd_expand_z, grid, dim3(256), 0, st, s->d_layers, layer, z, lgD, nlive, b_begin, w, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// w2[v][bb][i] = g_{b,i} w[v][bb][pi_b(i)]
+__global__ void k_ffd_permg_T(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ w, int lgD,
+                              int64_t nlive, int64_t bc, float *__restrict__ w2, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t D = 1ll << lgD;
+  const int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int64_t bb = t >> lgD;
+  if (bb >= nlive) return;
+  const int64_t i0 = t & (D - 1);
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)bb, (uint32_t)lgD, key);
+  float g[4];
+  gauss4((uint64_t)(bb * D + i0) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+  uint32_t p[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) p[q] = perm_fwd(pk, (uint32_t)(i0 + q));
+  const int64_t span = nlive * D;
+  for (int64_t v = 0; v < bc; ++v) {
+    const float *src = w + v * span + bb * D;
+    float4 o = make_float4(g[0] * src[p[0]], g[1] * src[p[1]], g[2] * src[p[2]], g[3] * src[p[3]]);
+    *(float4 *)(w2 + v * span + t) = o;
+  }
+}
+
+void launch_ffd_permg_T(const sk_sketch *s, int layer, const float *w, int64_t bc, float *w2, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  const int64_t th = nlive * s->D / 4;
+  hipLaunchKernelGGL(k_ffd_permg_T, dim3((unsigned)((th + 255) / 256)), dim3(256), 0, st, s->d_layers, layer, w, lgD,
+                     nlive, bc, w2, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_ffd_T_out(const LayerDesc *__restrict__ layers, int layer, const float *__restrict__ w2,
+                            int64_t span, int64_t b_begin, void *__restrict__ out, int out_dtype,
+                            const float *__restrict__ theta0) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (j >= ld.n) return;
+  const int64_t v = blockIdx.y;
+  store_out(out, out_dtype, (b_begin + v) * ld.n + j, w2[v * span + j] + (theta0 ? theta0[j] : 0.0f));
+}
+
+void launch_ffd_T_out(const sk_sketch *s, int layer, const float *w2, int64_t b_begin, int64_t bc, void *out,
+                      int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const int64_t span = ffd_live_blocks(s, layer) * s->D;
+  dim3 grid((unsigned)((ld.n + 255) / 256), (unsigned)bc);
+  hipLaunchKernelGGL(k_ffd_T_out, grid, dim3(256), 0, st, s->d_layers, layer, w2, span, b_begin, out, out_dtype,
+                     theta0);
+  SK_CHECK_LAUNCH();
+}
+
+// ===========================================================================
+// Tables and stream export.
+// ===========================================================================
+__global__ void k_gauss_table(const LayerDesc *__restrict__ layers, int nl, int64_t D, float *__restrict__ gtab,
+                              Key key) {
+  const int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int l = blockIdx.y;
+  if (t >= D || l >= nl) return;
+  float g[4];
+  gauss4((uint64_t)t >> 2, (uint32_t)layers[l].layer_id, ST_GAUSS, key, g);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (t + q < D) gtab[(int64_t)l * D + t + q] = g[q];
+}
+
+void launch_gauss_table(const sk_sketch *s, float *gtab, hipStream_t st) {
+  dim3 grid((unsigned)((s->D / 4 + 255) / 256 + 1), (unsigned)s->layers.size());
+  hipLaunchKernelGGL(k_gauss_table, grid, dim3(256), 0, st, s->d_layers, (int)s->layers.size(), s->D, gtab, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+__global__ void k_debug_stream(const LayerDesc *__restrict__ layers, const uint16_t *__restrict__ ptab, int layer,
+                               int stream_id, uint64_t start, uint64_t count, uint64_t aux, int lgD, void *dout,
+                               Key key) {
+  const uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  const LayerDesc &ld = layers[layer];
+  const uint64_t j = start + i;
+  const uint32_t lid = (uint32_t)ld.layer_id;
+  switch (stream_id) {
+    case ST_SIGN:
+      ((int8_t *)dout)[i] = ((sign_word(j, lid, key) >> (j & 31)) & 1u) ? -1 : 1;
+      break;
+    case ST_GAUSS:
+    case ST_QKA:
+    case ST_QKB:
+      ((float *)dout)[i] = gauss(j, lid, (uint32_t)stream_id, key);
+      break;
+    case ST_INDEX:
+      ((uint32_t *)dout)[i] = sample_index(j, lid, key, (uint64_t)ld.np);
+      break;
+    case ST_PI1:
+    case ST_PI2: {
+      const int sidx = stream_id == ST_PI1 ? 0 : 1;
+      uint64_t r = 0, stride = 1;
+      for (int k = ld.K - 1; k >= 0; --k) {
+        const uint64_t dig = (j / stride) & ((1ull << ld.lg[k]) - 1);
+        r += (uint64_t)ptab[ld.poff[sidx][0][k] + dig] * stride;
+        stride <<= ld.lg[k];
+      }
+      ((uint32_t *)dout)[i] = (uint32_t)r;
+      break;
+    }
+    case ST_FFDPERM: {
+      const PermKey pk = perm_key(lid, ST_FFDPERM, (uint32_t)aux, (uint32_t)lgD, key);
+      ((uint32_t *)dout)[i] = perm_fwd(pk, (uint32_t)j);
+      break;
+    }
+    default:
+      break;
+  }
+}
+
+void launch_debug_stream(const sk_sketch *s, int layer, int stream_id, uint64_t start, uint64_t count, uint64_t aux,
+                         void *dout, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
+  hipLaunchKernelGGL(k_debug_stream, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, s->d_layers, s->d_ptab,
+                     layer, stream_id, start, count, aux, lgD, dout, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+}  // namespace sk

@@ -1,0 +1,86 @@
+// sk_internal.h -- plan records and kernel launchers of the sketch library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/sketch.h"
+#include "sk_device.h"
+
+namespace sk {
+
+constexpr int kMaxDigits = 4;  // N' <= 2^40
+constexpr int kMaxPtrs = 64;   // layers per launch (pointer pack in kernel arguments)
+constexpr int kFfdSmallMax = 13;  // log2 D up to which an FFD block lives in LDS
+
+// Per-layer plan record, mirrored on the device.
+struct LayerDesc {
+  int64_t n;          // elements rows*cols
+  int64_t np;         // padded length N' (FWHT kinds)
+  int32_t lgnp, K;    // log2 N', number of Kronecker digits
+  int32_t lg[kMaxDigits];  // digit widths, digit 0 most significant
+  int32_t L, lgL;     // size of the last digit (row length)
+  int32_t dk1, lgdk1; // size of the second-to-last digit (1 if K < 2)
+  int64_t rows_live;  // ceil(n / L)
+  int32_t poff[2][2][kMaxDigits];  // digit-permutation tables [pi1, pi2][fwd, inv][digit]
+  int32_t layer_id;   // RNG layer id (index in the list)
+  int32_t rslot_off;  // AFJL: offset of this layer's R (first item, chunk count) pairs
+  int32_t item_off;   // AFJL: first fold item of this layer
+  int32_t n_items;    // AFJL: fold items of this layer
+  int32_t m, nc, da, db;  // QK shape and block
+  int64_t qk_col;     // QK: first output column of the block
+  int64_t fa_off, fb_off;  // QK: element offsets of A (da x m) and B (db x nc) in the factor buffer
+  int32_t lo_len_lg;  // AFFD: log2 of the low block spanned by c < D
+  uint32_t hstar;     // AFFD: top-digit index of pi2 at the all-zero low part
+};
+
+// AFJL fold work item: rows t in [t0, t1) of destination row r of a layer.
+struct FoldItem {
+  int32_t layer;  // index into the layer table
+  int32_t r;
+  int32_t t0, t1;
+};
+
+struct PtrPack {
+  const void *p[kMaxPtrs];
+};
+struct OutPack {
+  void *p[kMaxPtrs];
+};
+
+const char *set_error(int code, const std::string &msg);
+
+}  // namespace sk
+
+struct sk_sketch {
+  int kind = 0;
+  int device = 0;
+  int64_t D = 0;
+  uint64_t seed = 0;
+  sk::Key key{};
+  std::vector<sk::LayerDesc> layers;
+  sk::LayerDesc *d_layers = nullptr;
+  uint16_t *d_ptab = nullptr;  // digit permutation tables (values < 1024)
+  float *d_gtab = nullptr;     // FJL/AFJL: per-layer G over [0, D)
+  // AFJL
+  int R = 1, Lw = 0;
+  std::vector<sk::FoldItem> items;
+  sk::FoldItem *d_items = nullptr;
+  int2 *d_rslot = nullptr;     // per layer, per destination row: (first item, chunks)
+  // FJL transpose: samples sorted by position, per layer
+  std::vector<int64_t> fjl_off;  // per layer: offset into the sorted arrays (n_layers+1)
+  std::vector<int64_t> fjl_uoff; // per layer: offset into the unique-position arrays
+  uint32_t *d_fjl_pos = nullptr;   // unique positions
+  uint32_t *d_fjl_seg = nullptr;   // segment starts into d_fjl_smp (per unique position, +1 sentinel per layer)
+  uint32_t *d_fjl_smp = nullptr;   // sample ids sorted by (position, id)
+  // QK
+  uint16_t *d_qkfac = nullptr;  // bf16 factors
+  int64_t qk_fac_elems = 0;
+  // workspace
+  float *ws = nullptr;
+  int64_t ws_bytes = 0;
+  int64_t total_numel = 0, total_padded = 0;
+};

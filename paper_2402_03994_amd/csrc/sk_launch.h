@@ -1,0 +1,79 @@
+// sk_launch.h -- host-side launchers of the sketch kernels (one per kernel).
+#pragma once
+
+#include "sk_internal.h"
+
+namespace sk {
+
+// Generic in-place normalised Walsh-Hadamard transform of V contiguous
+// vectors of length 2^lgn, as a sequence of LDS-tiled passes.
+void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st);
+
+void launch_fill_zero(float *p, int64_t n, hipStream_t st);
+
+// ---- AFJL ----
+void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,
+                      int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st);
+void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
+                      int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st);
+void launch_afjl_T_prep(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                        hipStream_t st);
+void launch_afjl_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, hipStream_t st);
+
+// ---- AFFD ----
+void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                        float *w, hipStream_t st);
+void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st);
+void launch_affd_gather(const sk_sketch *s, int layer, const float *f, int64_t b_begin, int64_t bc, float *out,
+                        bool accumulate, hipStream_t st);
+void launch_affd_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                           hipStream_t st);
+void launch_mul_gauss(const sk_sketch *s, int layer, float *w, int64_t bc, hipStream_t st);
+void launch_affd_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, hipStream_t st);
+
+// ---- FJL ----
+void launch_fjl_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                       float *w, hipStream_t st);
+void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
+                       bool accumulate, hipStream_t st);
+void launch_fjl_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                          hipStream_t st);
+void launch_signed_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
+                       int out_dtype, const float *theta0, float scale, hipStream_t st);
+
+// ---- FFD ----
+int64_t ffd_live_blocks(const sk_sketch *s, int layer);
+void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                          float *part, int64_t slot0, int64_t groups, hipStream_t st);
+int64_t ffd_small_groups(const sk_sketch *s, int layer);
+void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64_t D, int64_t b_begin, float *out,
+                            bool accumulate, hipStream_t st);
+void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
+                        int out_dtype, const float *theta0, hipStream_t st);
+void launch_ffd_copy_blocks(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                            float *w, hipStream_t st);
+void launch_ffd_gperm_fwd(const sk_sketch *s, int layer, const float *w, int64_t bc, float *w2, hipStream_t st);
+void launch_ffd_sum_signed(const sk_sketch *s, int layer, const float *w2, int64_t b_begin, int64_t bc, float *out,
+                           bool accumulate, hipStream_t st);
+void launch_ffd_expand_z(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
+                         hipStream_t st);
+void launch_ffd_permg_T(const sk_sketch *s, int layer, const float *w, int64_t bc, float *w2, hipStream_t st);
+void launch_ffd_T_out(const sk_sketch *s, int layer, const float *w2, int64_t b_begin, int64_t bc, void *out,
+                      int out_dtype, const float *theta0, hipStream_t st);
+
+// ---- tables / debug ----
+void launch_gauss_table(const sk_sketch *s, float *gtab, hipStream_t st);
+void launch_debug_stream(const sk_sketch *s, int layer, int stream_id, uint64_t start, uint64_t count, uint64_t aux,
+                         void *dout, hipStream_t st);
+
+// ---- QK ----
+void launch_qk_factors(const sk_sketch *s, hipStream_t st);
+void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                     float *t_ws, int64_t batch_total, float *out, bool accumulate, hipStream_t st);
+int64_t qk_workspace_elems(const sk_sketch *s, int layer, int64_t bc);
+void launch_qk_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *t_ws,
+                       void *out, int out_dtype, const float *theta0, hipStream_t st);
+
+}  // namespace sk

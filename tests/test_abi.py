@@ -1,0 +1,74 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point declared in include/sketch.h, and rejects invalid arguments
+before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2402_03994_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "sketch.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sketch_[a-z_T]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.load()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def shapes(*ss):
+    arr = (_lib.LayerShape * len(ss))()
+    for i, s in enumerate(ss):
+        arr[i].rows, arr[i].cols = s[0], s[1]
+        arr[i].qk_da = s[2] if len(s) > 2 else 0
+        arr[i].qk_db = s[3] if len(s) > 3 else 0
+    return arr
+
+
+@pytest.mark.parametrize("kind,shp,D,flags,code", [
+    (9, [(1, 10)], 64, 0, -1),            # unknown kind
+    (3, [(1, 10)], 63, 0, -1),            # D not a power of two
+    (3, [(1, 10)], 0, 0, -1),
+    (3, [(1, 10)], 8, 0, -5),             # below the kernels' minimum
+    (3, [(1, 10)], 1 << 21, 0, -5),       # above the kernels' maximum
+    (3, [(0, 10)], 64, 0, -1),            # empty layer
+    (3, [(1, 10)], 64, 1, -1),            # reserved flags
+    (4, [(4, 5, 2, 2)], 5, 0, -1),        # QK: sum dA*dB != D
+    (4, [(4, 5, 5, 2)], 10, 0, -1),       # QK: dA > rows
+    (4, [(4, 5, 0, 2)], 0, 0, -1),        # QK: dA < 1
+])
+def test_create_rejects_invalid_arguments(kind, shp, D, flags, code):
+    L = _lib.load()
+    h = ctypes.c_void_p(1234)
+    rc = L.sketch_create(kind, shapes(*shp), len(shp), D, 0, flags, 0, ctypes.byref(h))
+    assert rc == code, L.sketch_last_error()
+    assert h.value is None  # *out cleared on failure
+    assert len(L.sketch_last_error()) > 0
+
+
+def test_null_arguments():
+    L = _lib.load()
+    assert L.sketch_create(3, None, 1, 64, 0, 0, 0, ctypes.byref(ctypes.c_void_p())) == -1
+    assert L.sketch_create(3, shapes((1, 4)), 1, 64, 0, 0, 0, None) == -1
+    assert L.sketch_apply(None, None, 0, 1, None, 0, 1, 0, None) == -1
+    assert L.sketch_apply_T(None, None, 1, None, 0, None, 0, 1, None) == -1
+    assert L.sketch_query(None, None) == -1
+    L.sketch_destroy(None)  # no-op
+
+
+def test_status_strings():
+    L = _lib.load()
+    for code in [0, -1, -2, -3, -4, -5]:
+        assert L.sketch_status_string(code).decode() != "unknown status"

@@ -1,0 +1,177 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Error metric per batch row: max_i |y_i - o_i| / max(|o_i|, rms(o)), bounded by
+1e-5 for fp32 inputs and 2e-2 for bf16 inputs (fp32 arithmetic on the GPU);
+random signs, sample positions and permutations must match bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-5
+TOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2402_03994_amd import _lib
+    _lib.load()  # fail loudly if the HIP library is missing
+    return torch.device("cuda", 0)
+
+
+def sk(kind, shapes, D, seed, dev):
+    from paper_2402_03994_amd import Sketch
+    return Sketch(kind, shapes, D, seed, device=dev)
+
+
+def rel_err(y, o):
+    y = np.asarray(y, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    o2 = o.reshape(o.shape[0], -1)
+    y2 = y.reshape(y.shape[0], -1)
+    rms = np.sqrt((o2**2).mean(axis=1, keepdims=True))
+    den = np.maximum(np.abs(o2), rms)
+    den[den == 0] = 1.0
+    return float((np.abs(y2 - o2) / den).max())
+
+
+def rand_inputs(shapes, batch, seed, dtype=torch.float32, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    xs = [torch.randn((batch, s[0] * s[1]), generator=g, dtype=torch.float32) * scale for s in shapes]
+    if dtype == torch.bfloat16:
+        xs = [x.to(torch.bfloat16) for x in xs]
+    return xs
+
+
+def oracle_in(x):
+    if x.dtype == torch.bfloat16:
+        return x.view(torch.int16).numpy().view(np.uint16), "bf16"
+    return x.numpy(), "f32"
+
+
+# shapes spanning several tiles, ragged tails, n < D and n not a multiple of 4
+LAYERS = [(1, 30), (7, 111), (3, 1500), (1, 5003), (33, 1024), (1, 16)]
+CASES = [(LAYERS, 16), (LAYERS, 256), (LAYERS, 1024), (LAYERS, 4096), ([(1, 70000), (3, 500)], 65536),
+         ([(1, 2 ** 20 + 3), (1, 9)], 2048), ([(1, 3 * 2 ** 20 + 11)], 65536)]
+
+
+@pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_forward_parity_f32(kind, case, dev):
+    shapes, D = CASES[case]
+    seed = 100 + case
+    xs = rand_inputs(shapes, 3, seed)
+    s = sk(kind, shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply(kind, shapes, D, seed, [x.numpy() for x in xs])
+    assert rel_err(y, ref) < TOL_F32
+
+
+@pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
+@pytest.mark.parametrize("case", [1, 3, 4])
+def test_transpose_parity(kind, case, dev):
+    shapes, D = CASES[case]
+    seed = 200 + case
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((2, D), generator=g)
+    th = [torch.randn(s[0] * s[1], generator=g) * 0.02 for s in shapes]
+    th[0] = None
+    s = sk(kind, shapes, D, seed, dev)
+    outs = s.apply_T(z.to(dev), theta0=[None if t is None else t.to(dev) for t in th])
+    refs = O.apply_T(kind, shapes, D, seed, z.numpy().astype(np.float64),
+                     theta0=[None if t is None else t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL_F32
+
+
+@pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
+def test_forward_parity_bf16(kind, dev):
+    shapes, D = CASES[3]
+    seed = 300
+    xs = rand_inputs(shapes, 2, seed, dtype=torch.bfloat16, scale=0.01)
+    s = sk(kind, shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ins = [oracle_in(x)[0] for x in xs]
+    ref = O.apply(kind, shapes, D, seed, ins, dtype="bf16")
+    # bf16 inputs are widened exactly, so the fp32 bound holds too
+    assert rel_err(y, ref) < TOL_F32
+
+
+@pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
+def test_transpose_bf16_output(kind, dev):
+    shapes, D = CASES[1]
+    g = torch.Generator().manual_seed(5)
+    z = torch.randn((2, D), generator=g)
+    s = sk(kind, shapes, D, 5, dev)
+    outs = s.apply_T(z.to(dev), out_dtype=torch.bfloat16)
+    refs = O.apply_T(kind, shapes, D, 5, z.numpy().astype(np.float64))
+    for o, r in zip(outs, refs):
+        assert rel_err(o.float().cpu().numpy(), r) < TOL_BF16
+
+
+@pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd", "qk"])
+def test_streaming_accumulate_and_determinism(kind, dev):
+    if kind == "qk":
+        shapes, D = [(40, 70, 4, 5), (64, 33, 8, 2), (1, 300, 1, 9)], 20 + 16 + 9
+    else:
+        shapes, D = LAYERS, 1024
+    xs = [x.to(dev) for x in rand_inputs(shapes, 4, 9)]
+    s = sk(kind, shapes, D, 11, dev)
+    y1 = s.apply(xs)
+    y2 = s.apply(xs)
+    assert torch.equal(y1, y2)  # bitwise deterministic
+    out = torch.zeros_like(y1)
+    for l, x in enumerate(xs):
+        s.apply([x], out=out, first_layer=l, accumulate=True)
+    ref = O.apply(kind, shapes, D, 11, [x.cpu().numpy() for x in xs], qk_bf16=(kind == "qk"))
+    assert rel_err(out.cpu().numpy(), ref) < (1e-3 if kind == "qk" else TOL_F32)
+
+
+def test_debug_streams_bit_exact(dev):
+    seed = 0xDEADBEEF12345
+    shapes = [(1, 3000), (1, 70000)]
+    for kind in ["afjl", "affd", "fjl"]:
+        s = sk(kind, shapes, 1024, seed, dev)
+        for layer, (r, c) in enumerate(shapes):
+            np_len = O.padded(r * c, 1024)
+            cnt = min(20000, np_len - 5)
+            assert np.array_equal(s.debug_stream(layer, "sign", 5, cnt), O.signs(seed, layer, 5, cnt))
+            g = s.debug_stream(layer, "gauss", 0, 8192).astype(np.float64)
+            go = O.gauss(seed, layer, "gauss", 0, 8192)
+            assert np.abs(g - go).max() < 1e-5
+            if kind == "fjl":
+                assert np.array_equal(s.debug_stream(layer, "index", 0, 1024), O.indices(seed, layer, 0, 1024, np_len))
+            else:
+                assert np.array_equal(s.debug_stream(layer, "pi1", 0, np_len), O.digit_perm(seed, layer, "pi1", np_len))
+            if kind == "affd":
+                assert np.array_equal(s.debug_stream(layer, "pi2", 0, np_len), O.digit_perm(seed, layer, "pi2", np_len))
+    s = sk("ffd", [(1, 5000)], 4096, seed, dev)
+    for b in [0, 1]:
+        assert np.array_equal(s.debug_stream(0, "ffdperm", 0, 4096, aux=b), O.perm(seed, 0, "ffdperm", b, 12))
+    s = sk("ffd", [(1, 5000)], 1 << 20, seed, dev)
+    assert np.array_equal(s.debug_stream(0, "ffdperm", 0, 1 << 20, aux=3), O.perm(seed, 0, "ffdperm", 3, 20))
+
+
+@pytest.mark.parametrize("shapes,D", [([(40, 70, 4, 5), (64, 33, 8, 2), (1, 300, 1, 9)], 45),
+                                      ([(256, 512, 32, 16), (300, 200, 16, 32)], 32 * 16 * 2)])
+def test_qk_parity(shapes, D, dev):
+    seed = 21
+    xs = rand_inputs(shapes, 3, seed, dtype=torch.bfloat16, scale=0.01)
+    s = sk("qk", shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ins = [oracle_in(x)[0] for x in xs]
+    exact = O.apply("qk", shapes, D, seed, ins, dtype="bf16")
+    assert rel_err(y, exact) < TOL_BF16
+    rounded = O.apply("qk", shapes, D, seed, ins, dtype="bf16", qk_bf16=True)
+    assert rel_err(y, rounded) < 1e-3
+    g = torch.Generator().manual_seed(3)
+    z = torch.randn((2, D), generator=g)
+    outs = s.apply_T(z.to(dev))
+    refs = O.apply_T("qk", shapes, D, seed, z.numpy().astype(np.float64), qk_bf16=True)
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < 1e-3
