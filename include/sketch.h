@@ -169,6 +169,32 @@ int sketch_query(const sk_sketch *s, sk_info *info);
 int sketch_debug_stream(sk_sketch *s, int32_t layer, int32_t stream_id, uint64_t start, uint64_t count,
                         uint64_t aux, void *host_out);
 
+/*
+ * Kernel timing (diagnostics and roofline reports).  While profiling is on,
+ * every group of kernel launches a call issues is bracketed by HIP events on
+ * that call's stream, tagged with a kernel class and the algorithmic bytes the
+ * group moves (inputs read once plus outputs written once).
+ * sketch_profile(s, 1) allocates the event pool (up to 16384 groups) and clears
+ * the record; sketch_profile(s, 0) stops recording.  sketch_profile_read()
+ * waits for the recorded events and fills, per class (arrays of
+ * SK_PROF_CLASSES entries), the summed duration in ms, the number of groups
+ * and the summed algorithmic bytes, then clears the record.
+ */
+enum {
+  SK_PROF_AFJL_FOLD = 0, /* AFJL row fold + H_L                           */
+  SK_PROF_AFJL_TAIL = 1, /* AFJL H_R, G, layer sum                          */
+  SK_PROF_FWHT = 2,      /* generic Walsh-Hadamard passes                   */
+  SK_PROF_PROLOG = 3,    /* load / sign / permute of inputs (AFFD, FJL)     */
+  SK_PROF_AFFD_FOLD = 4, /* AFFD G + signed fold of the top digits          */
+  SK_PROF_GATHER = 5,    /* final gathers and output writes                 */
+  SK_PROF_FFD = 6,       /* FFD block kernels                               */
+  SK_PROF_QK = 7,        /* QK contractions                                 */
+  SK_PROF_OTHER = 8,
+  SK_PROF_CLASSES = 9
+};
+int sketch_profile(sk_sketch *s, int enable);
+int sketch_profile_read(sk_sketch *s, double *ms, int64_t *count, int64_t *bytes);
+
 /* Thread-local message describing the last failure of this thread. */
 const char *sketch_last_error(void);
 

@@ -12,7 +12,9 @@ SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8}
 EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", "sketch_query",
-           "sketch_debug_stream", "sketch_last_error", "sketch_status_string")
+           "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
+           "sketch_status_string")
+PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other"]
 
 
 class LayerShape(ctypes.Structure):
@@ -52,6 +54,10 @@ def load() -> ctypes.CDLL:
     L.sketch_query.restype = ctypes.c_int
     L.sketch_debug_stream.argtypes = [P, i32, i32, u64, u64, u64, P]
     L.sketch_debug_stream.restype = ctypes.c_int
+    L.sketch_profile.argtypes = [P, ctypes.c_int]
+    L.sketch_profile.restype = ctypes.c_int
+    L.sketch_profile_read.argtypes = [P, P, P, P]
+    L.sketch_profile_read.restype = ctypes.c_int
     L.sketch_last_error.argtypes = []
     L.sketch_last_error.restype = ctypes.c_char_p
     L.sketch_status_string.argtypes = [ctypes.c_int]

@@ -69,9 +69,33 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_smp);
   f(s->d_qkfac);
   f(s->ws);
+  for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
+  s->evpool.clear();
 }
 
 bool fwht_kind(int k) { return k == SK_FJL || k == SK_FFD || k == SK_AFFD || k == SK_AFJL; }
+
+// Brackets a group of launches with a pair of pooled events when profiling.
+struct ProfScope {
+  sk_sketch *s;
+  int idx = -1;
+  hipStream_t st;
+  ProfScope(sk_sketch *s_, int cls, int64_t bytes, hipStream_t st_) : s(s_), st(st_) {
+    if (!s->prof || s->evnext + 2 > (int)s->evpool.size()) return;
+    idx = s->evnext;
+    s->evnext += 2;
+    s->recs.push_back(sk_sketch::ProfRec{cls, idx, bytes});
+    (void)hipEventRecord(s->evpool[idx], st);
+  }
+  ~ProfScope() {
+    if (idx >= 0) (void)hipEventRecord(s->evpool[idx + 1], st);
+  }
+};
+#define SK_PROF(cls, bytes, stmt)        \
+  do {                                   \
+    ProfScope ps_(s, (cls), (bytes), st); \
+    stmt;                                \
+  } while (0)
 
 // Bytes of workspace one vector needs for one call over layers [l0, l1).
 int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
@@ -81,10 +105,10 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
     int64_t b = 0;
     switch (s->kind) {
       case SK_AFJL:
-        b = transpose ? s->D * 4 : (int64_t)ld.n_items * s->Lw * 4;
+        if (transpose) b = s->D * 4;
         break;
       case SK_AFFD:
-        b = (ld.np + (1ll << ld.lo_len_lg)) * 4;
+        b = transpose ? ld.np * 4 : (ld.np + (1ll << ld.lo_len_lg) + s->D) * 4;
         break;
       case SK_FJL:
         b = ld.np * 4;
@@ -100,6 +124,11 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
         break;
     }
     need = std::max(need, b);
+  }
+  if (s->kind == SK_AFJL && !transpose) {
+    // fold partials of every item of the call, plus the tail's per-group sums
+    const int64_t items = s->layers[l1 - 1].item_off + s->layers[l1 - 1].n_items - s->layers[l0].item_off;
+    need = std::max(need, items * s->Lw * 4 + (int64_t)kTailGroups * s->D * 4);
   }
   return need;
 }
@@ -421,56 +450,73 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
   int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
   if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
   const int esz = dtype == SK_BF16 ? 2 : 4;
+  if (s->kind == SK_AFFD) {
+    bool all_fast = true;
+    for (int l = l0; l < l1; ++l) all_fast = all_fast && affd_fast_path(s, l);
+    if (all_fast) bcmax = batch;  // the fast path tiles the batch per layer
+  }
 
   for (int64_t b0 = 0; b0 < batch; b0 += bcmax) {
     const int64_t bc = std::min(bcmax, batch - b0);
     switch (s->kind) {
       case SK_AFJL: {
-        // groups of layers whose fold partials fit in the workspace
-        int g0 = l0;
-        bool first = true;
-        while (g0 < l1) {
-          int g1 = g0;
-          int64_t items = 0;
-          while (g1 < l1 && g1 - g0 < kMaxPtrs) {
-            const int64_t add = s->layers[g1].n_items;
-            if (g1 > g0 && (items + add) * bc * s->Lw * 4 > s->ws_bytes) break;
-            items += add;
-            ++g1;
-          }
+        // fold launches of at most kMaxPtrs layers, then one tail over all layers
+        const int it_base = s->layers[l0].item_off;
+        int64_t in_bytes = 0;
+        for (int g0 = l0; g0 < l1; g0 += kMaxPtrs) {
+          const int g1 = std::min(l1, g0 + kMaxPtrs);
           PtrPack pp{};
           bool vec = true;
+          int64_t gb = 0;
           for (int l = g0; l < g1; ++l) {
             pp.p[l - g0] = grads[l - l0];
+            gb += bc * s->layers[l].n * esz;
             if ((s->layers[l].n & 3) || ((uintptr_t)grads[l - l0] & (uintptr_t)(esz * 4 - 1))) vec = false;
           }
+          in_bytes += gb;
           const int it0 = s->layers[g0].item_off;
           const int it1 = s->layers[g1 - 1].item_off + s->layers[g1 - 1].n_items;
-          launch_afjl_fold(s, pp, g0, dtype, vec, batch, b0, bc, it0, it1, s->ws, st);
-          launch_afjl_tail(s, g0, g1, it0, s->ws, bc, b0, batch, out, accumulate || !first, st);
-          first = false;
-          g0 = g1;
+          float *part = s->ws + (int64_t)(it0 - it_base) * bc * s->Lw;
+          SK_PROF(SK_PROF_AFJL_FOLD, gb,
+                  launch_afjl_fold(s, pp, g0, dtype, vec, batch, b0, bc, it0, it1, part, st));
         }
+        SK_PROF(SK_PROF_AFJL_TAIL, bc * s->D * 4,
+                launch_afjl_tail(s, l0, l1, it_base, s->ws, bc, b0, batch, out, accumulate != 0, st));
+        (void)in_bytes;
         break;
       }
       case SK_AFFD:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
+          if (affd_fast_path(s, l)) {
+            // batch tile sized so the layer's intermediate stays cache-resident between phases
+            const int64_t live = affd_live_bytes_per_vector(s, l);
+            int64_t tile = std::max<int64_t>(1, affd_tile_bytes() / std::max<int64_t>(live, 1));
+            tile = std::min(tile, std::max<int64_t>(1, s->ws_bytes / affd_fast_bytes_per_vector(s, l)));
+            for (int64_t t0 = b0; t0 < b0 + bc; t0 += tile) {
+              const int64_t tb = std::min(tile, b0 + bc - t0);
+              SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz + (l == l1 - 1 ? tb * s->D * 4 : 0),
+                      run_affd_fast(s, l, grads[l - l0], dtype, t0, tb, out, accumulate || l > l0, st));
+            }
+            continue;
+          }
           float *w = s->ws;
           float *f = s->ws + bc * ld.np;
-          launch_affd_prolog(s, l, grads[l - l0], dtype, b0, bc, w, st);
-          fwht_inplace(w, bc, ld.lgnp, st);
-          launch_affd_fold(s, l, w, bc, f, st);
-          fwht_inplace(f, bc, ld.lo_len_lg, st);
-          launch_affd_gather(s, l, f, b0, bc, out, accumulate || l > l0, st);
+          SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_affd_prolog(s, l, grads[l - l0], dtype, b0, bc, w, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w, bc, ld.lgnp, st));
+          SK_PROF(SK_PROF_AFFD_FOLD, 0, launch_affd_fold(s, l, w, bc, f, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(f, bc, ld.lo_len_lg, st));
+          SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                  launch_affd_gather(s, l, f, b0, bc, out, accumulate || l > l0, st));
         }
         break;
       case SK_FJL:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
-          launch_fjl_prolog(s, l, grads[l - l0], dtype, b0, bc, s->ws, st);
-          fwht_inplace(s->ws, bc, ld.lgnp, st);
-          launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st);
+          SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_prolog(s, l, grads[l - l0], dtype, b0, bc, s->ws, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+          SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                  launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st));
         }
         break;
       case SK_FFD: {
@@ -478,8 +524,10 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         for (int l = l0; l < l1; ++l) {
           if (lgD <= kFfdSmallMax) {
             const int64_t groups = ffd_small_groups(s, l);
-            launch_ffd_small_fwd(s, l, grads[l - l0], dtype, b0, bc, s->ws, 0, groups, st);
-            launch_reduce_partials(s->ws, groups, bc, s->D, b0, out, accumulate || l > l0, st);
+            SK_PROF(SK_PROF_FFD, bc * s->layers[l].n * esz,
+                    launch_ffd_small_fwd(s, l, grads[l - l0], dtype, b0, bc, s->ws, 0, groups, st));
+            SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                    launch_reduce_partials(s->ws, groups, bc, s->D, b0, out, accumulate || l > l0, st));
           } else {
             const int64_t nlive = ffd_live_blocks(s, l);
             float *w = s->ws, *w2 = s->ws + bc * nlive * s->D;
@@ -494,7 +542,8 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
       }
       case SK_QK:
         for (int l = l0; l < l1; ++l)
-          launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, batch, out, accumulate != 0, st);
+          SK_PROF(SK_PROF_QK, bc * s->layers[l].n * esz + bc * s->layers[l].da * s->layers[l].db * 4,
+                  launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, batch, out, accumulate != 0, st));
         break;
     }
   }
@@ -568,6 +617,42 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(SK_EHIP, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  return SK_OK;
+}
+
+int sketch_profile(sk_sketch *s, int enable) {
+  if (!s) return fail(SK_EINVAL, "sketch is NULL");
+  DeviceGuard guard(s->device);
+  if (enable) {
+    if (s->evpool.empty()) {
+      s->evpool.resize(2 * 16384);
+      for (auto &e : s->evpool) SK_HIP(hipEventCreate(&e));
+    }
+    s->evnext = 0;
+    s->recs.clear();
+  }
+  s->prof = enable != 0;
+  return SK_OK;
+}
+
+int sketch_profile_read(sk_sketch *s, double *ms, int64_t *count, int64_t *bytes) {
+  if (!s || !ms || !count || !bytes) return fail(SK_EINVAL, "NULL argument");
+  DeviceGuard guard(s->device);
+  for (int c = 0; c < SK_PROF_CLASSES; ++c) {
+    ms[c] = 0.0;
+    count[c] = 0;
+    bytes[c] = 0;
+  }
+  for (const auto &r : s->recs) {
+    SK_HIP(hipEventSynchronize(s->evpool[r.ev + 1]));
+    float t = 0.0f;
+    SK_HIP(hipEventElapsedTime(&t, s->evpool[r.ev], s->evpool[r.ev + 1]));
+    ms[r.cls] += t;
+    count[r.cls] += 1;
+    bytes[r.cls] += r.bytes;
+  }
+  s->recs.clear();
+  s->evnext = 0;
   return SK_OK;
 }
 

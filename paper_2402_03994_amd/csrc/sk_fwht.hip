@@ -12,6 +12,9 @@
 //    (the O(A+B) lookups of Sec. 3, "Removing the lookup bottleneck");
 //  - no floating-point atomics: every output element has one writer and a
 //    fixed summation order.
+#include <algorithm>
+
+#include "sk_kcommon.h"
 #include "sk_launch.h"
 
 namespace sk {
@@ -23,71 +26,6 @@ static int log2_exact(int64_t v) {
   int l = 0;
   while ((1ll << l) < v) ++l;
   return l;
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-__device__ __forceinline__ void store_out(void *out, int out_dtype, int64_t i, float v) {
-  if (out_dtype == SK_BF16)
-    ((uint16_t *)out)[i] = f32_to_bf16(v);
-  else
-    ((float *)out)[i] = v;
-}
-
-// Load up to 4 consecutive input elements starting at element e of a vector
-// whose valid prefix has `lim` (>= 1) elements from e on; missing -> 0.
-template <bool BF16, bool VEC>
-__device__ __forceinline__ void load4(const void *x, int64_t e, int64_t lim, float v[4]) {
-  if (VEC && lim >= 4) {
-    if (BF16) {
-      const uint2 u = *(const uint2 *)((const uint16_t *)x + e);
-      v[0] = __uint_as_float(u.x << 16);
-      v[1] = __uint_as_float(u.x & 0xFFFF0000u);
-      v[2] = __uint_as_float(u.y << 16);
-      v[3] = __uint_as_float(u.y & 0xFFFF0000u);
-    } else {
-      const float4 f = *(const float4 *)((const float *)x + e);
-      v[0] = f.x;
-      v[1] = f.y;
-      v[2] = f.z;
-      v[3] = f.w;
-    }
-    return;
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if (q < lim)
-      v[q] = BF16 ? bf16_to_f32(((const uint16_t *)x)[e + q]) : ((const float *)x)[e + q];
-    else
-      v[q] = 0.0f;
-  }
-}
-
-// In-place unnormalised radix-2 Walsh-Hadamard transform along the rows of an
-// LDS tile s[r << lgcs | c], 2^lgrows rows, 2^lgcs columns.  Ends synchronised.
-__device__ void lds_fwht(float *s, int lgrows, int lgcs) {
-  const int npairs = 1 << (lgrows - 1 + lgcs);
-  const int cmask = (1 << lgcs) - 1;
-  for (int st = 0; st < lgrows; ++st) {
-    __syncthreads();
-    const int hmask = (1 << st) - 1;
-    for (int p = threadIdx.x; p < npairs; p += blockDim.x) {
-      const int q = p >> lgcs, c = p & cmask;
-      const int r = ((q & ~hmask) << 1) | (q & hmask);
-      float *a = s + ((r << lgcs) | c);
-      float *b = a + (1 << (st + lgcs));
-      const float u = *a, w = *b;
-      *a = u + w;
-      *b = u - w;
-    }
-  }
-  __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
@@ -183,7 +121,8 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
   const int nk = R > 1 ? ld.dk1 / R : 1;
   const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
   if (active) {
-    for (int t = it.t0; t < it.t1; ++t) {
+    // source row of fold step t (or -1 when it lies past the data)
+    auto row_of = [&](int t) -> int64_t {
       int64_t h;
       if (R == 1) {
         h = t;
@@ -192,22 +131,41 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
         const int k = t - htop * nk;
         h = (int64_t)htop * ld.dk1 + inv_k1[it.r + k * R];
       }
-      if (h >= ld.rows_live) continue;
-      const int64_t j0 = h * L + col0;
-      const int64_t lim = n - j0;
-      if (lim <= 0) continue;
-      const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
-      float v[BT][4];
+      return (h < ld.rows_live && h * L + col0 < n) ? h : -1;
+    };
+    // two rows per iteration: twice the loads in flight
+    for (int t = it.t0; t < it.t1; t += 2) {
+      const int64_t ha = row_of(t);
+      const int64_t hb = (t + 1 < it.t1) ? row_of(t + 1) : -1;
+      float va[BT][4], vb[BT][4];
+      const int64_t ja = ha * L + col0, jb = hb * L + col0;
+      if (ha >= 0) {
 #pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + j0, lim, v[b]);
+        for (int b = 0; b < BT; ++b)
+          if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + ja, n - ja, va[b]);
       }
+      if (hb >= 0) {
 #pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        if (b < nb) {
+        for (int b = 0; b < BT; ++b)
+          if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + jb, n - jb, vb[b]);
+      }
+      if (ha >= 0) {
+        const uint32_t bits = sign_word((uint64_t)ja, (uint32_t)ld.layer_id, key) >> (ja & 31);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) acc[b][q] += flip(v[b][q], (bits >> q) & 1u);
-        }
+        for (int b = 0; b < BT; ++b)
+          if (b < nb) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[b][q] += flip(va[b][q], (bits >> q) & 1u);
+          }
+      }
+      if (hb >= 0) {
+        const uint32_t bits = sign_word((uint64_t)jb, (uint32_t)ld.layer_id, key) >> (jb & 31);
+#pragma unroll
+        for (int b = 0; b < BT; ++b)
+          if (b < nb) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[b][q] += flip(vb[b][q], (bits >> q) & 1u);
+          }
       }
     }
     // route the columns through pi1 of the last digit
@@ -329,9 +287,86 @@ __global__ __launch_bounds__(256) void k_afjl_tail(const LayerDesc *__restrict__
   }
 }
 
+// Tail for R <= 64: one thread per (vector, column) keeps the R values of its
+// column in registers across all layers (no LDS, no barriers).
+// Layers are split into contiguous groups (blockIdx.y); group gi writes its
+// sum to ysum[gi][bl][:], reduced in group order afterwards.
+template <int R>
+__global__ __launch_bounds__(256) void k_afjl_tail_reg(const LayerDesc *__restrict__ layers,
+                                                       const int2 *__restrict__ rslot, const float *__restrict__ part,
+                                                       const float *__restrict__ gtab, TailGroups grp,
+                                                       int item_begin, int Lw, int64_t D, int64_t bc, int64_t b_begin,
+                                                       int64_t batch, float *__restrict__ ysum) {
+  const int64_t gid = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int c = (int)(gid % Lw);
+  const int64_t bl = gid / Lw;
+  if (bl >= bc || b_begin + bl >= batch) return;
+  const int l_begin = grp.bound[blockIdx.y], l_end = grp.bound[blockIdx.y + 1];
+  float acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r] = 0.0f;
+  for (int l = l_begin; l < l_end; ++l) {
+    const int2 *rs = rslot + layers[l].rslot_off;
+    // first chunk of every row: independent loads issued together (an empty
+    // row reads slot 0 and is masked), further chunks afterwards
+    float v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int2 q = rs[r];
+      const int64_t slot = q.y > 0 ? q.x - item_begin : 0;
+      const float x = part[(slot * bc + bl) * Lw + c];
+      v[r] = q.y > 0 ? x : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int2 q = rs[r];
+      for (int k = 1; k < q.y; ++k) v[r] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * Lw + c];
+    }
+    fwht_regs_t<R>(v);
+    const float *g = gtab + (int64_t)l * D + c;
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] += g[(int64_t)r * Lw] * v[r];
+  }
+  const float sc = rsqrtf((float)R);
+  float *o = ysum + ((int64_t)blockIdx.y * bc + bl) * D + c;
+#pragma unroll
+  for (int r = 0; r < R; ++r) o[(int64_t)r * Lw] = acc[r] * sc;
+}
+
 void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
                       int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st) {
   const int R = s->R, Lw = s->Lw;
+  if (R <= 64) {
+    // balance the layer loop: groups of about equal live destination rows
+    TailGroups grp{};
+    int64_t total = 0;
+    for (int l = l_begin; l < l_end; ++l) total += s->layers[l].n_items;
+    const int G = std::min(kTailGroups, l_end - l_begin);
+    int ng = 0;
+    grp.bound[0] = l_begin;
+    int64_t accw = 0;
+    for (int l = l_begin; l < l_end; ++l) {
+      accw += s->layers[l].n_items;
+      if (ng < G - 1 && accw * G >= total * (ng + 1) && l + 1 < l_end) grp.bound[++ng] = l + 1;
+    }
+    grp.bound[++ng] = l_end;
+    float *ysum = s->ws + (s->ws_bytes / 4 - (int64_t)kTailGroups * bc * s->D);
+    const int64_t threads = bc * Lw;
+    dim3 grid((unsigned)((threads + 255) / 256), (unsigned)ng);
+#define SK_TAIL(RR)                                                                                              \
+  case RR:                                                                                                       \
+    hipLaunchKernelGGL(k_afjl_tail_reg<RR>, grid, dim3(256), 0, st, s->d_layers, s->d_rslot, part, s->d_gtab,    \
+                       grp, item_begin, Lw, s->D, bc, b_begin, batch, ysum);                                     \
+    break;
+    switch (R) {
+      SK_TAIL(1) SK_TAIL(2) SK_TAIL(4) SK_TAIL(8) SK_TAIL(16) SK_TAIL(32) SK_TAIL(64)
+      default: break;
+    }
+#undef SK_TAIL
+    launch_reduce_partials(ysum, ng, bc, s->D, b_begin, out, accumulate, st);
+    SK_CHECK_LAUNCH();
+    return;
+  }
   int lgR = 31 - __builtin_clz(R);
   // tile of R rows x CS columns, at most 4096 elements
   int lgcs = 12 - lgR;

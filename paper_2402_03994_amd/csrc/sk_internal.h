@@ -44,6 +44,11 @@ struct FoldItem {
   int32_t t0, t1;
 };
 
+constexpr int kTailGroups = 16;  // AFJL tail: parallel layer groups
+struct TailGroups {
+  int32_t bound[kTailGroups + 1];
+};
+
 struct PtrPack {
   const void *p[kMaxPtrs];
 };
@@ -79,6 +84,16 @@ struct sk_sketch {
   // QK
   uint16_t *d_qkfac = nullptr;  // bf16 factors
   int64_t qk_fac_elems = 0;
+  // kernel timing
+  struct ProfRec {
+    int cls;
+    int ev;
+    int64_t bytes;
+  };
+  bool prof = false;
+  std::vector<hipEvent_t> evpool;
+  int evnext = 0;
+  std::vector<ProfRec> recs;
   // workspace
   float *ws = nullptr;
   int64_t ws_bytes = 0;

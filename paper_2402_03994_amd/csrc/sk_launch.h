@@ -22,6 +22,13 @@ void launch_afjl_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_
                        int out_dtype, const float *theta0, hipStream_t st);
 
 // ---- AFFD ----
+// AFFD specialised for D > 1024, last digit 1024 and at most 64 top-digit values.
+bool affd_fast_path(const sk_sketch *s, int layer);
+int64_t affd_fast_bytes_per_vector(const sk_sketch *s, int layer);
+int64_t affd_live_bytes_per_vector(const sk_sketch *s, int layer);
+int64_t affd_tile_bytes();
+void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *out,
+                   bool accumulate, hipStream_t st);
 void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                         float *w, hipStream_t st);
 void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st);

@@ -100,6 +100,20 @@ class Sketch:
                                            n_layers, _stream_ptr(self.device)))
         return outs
 
+    def profile(self, enable: bool = True) -> None:
+        """Start (clearing earlier records) or stop per-kernel-class event timing."""
+        _lib.check(self.lib.sketch_profile(self._h, int(enable)))
+
+    def profile_read(self) -> dict:
+        """{class: (ms, groups, algorithmic bytes)} recorded since profile(True); clears the record."""
+        import numpy as np
+        n = len(_lib.PROF_CLASSES)
+        ms, cnt, by = np.zeros(n), np.zeros(n, dtype=np.int64), np.zeros(n, dtype=np.int64)
+        _lib.check(self.lib.sketch_profile_read(self._h, ms.ctypes.data_as(ctypes.c_void_p),
+                                                cnt.ctypes.data_as(ctypes.c_void_p),
+                                                by.ctypes.data_as(ctypes.c_void_p)))
+        return {c: (float(ms[i]), int(cnt[i]), int(by[i])) for i, c in enumerate(_lib.PROF_CLASSES) if cnt[i]}
+
     def debug_stream(self, layer: int, stream: str, start: int, count: int, aux: int = 0):
         import numpy as np
         dt = {"sign": np.int8, "gauss": np.float32, "qka": np.float32, "qkb": np.float32}.get(stream, np.uint32)
