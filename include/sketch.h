@@ -111,9 +111,9 @@ enum {
  *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
  *   seed      64-bit key of every random stream.
  *   flags     reserved, must be 0.
- * On success *out receives the handle (destroy with sketch_destroy).  QK
- * factors (bf16, rounded to nearest even from fp32) and the small per-layer
- * tables are generated on the device here.
+ * On success *out receives the handle (destroy with sketch_destroy).  The
+ * small per-layer tables and the QK factors are generated on the device here
+ * (QK: A in fp32; B in fp32 split into two bf16 terms for the MFMA units).
  */
 int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, int64_t D, uint64_t seed,
                   uint32_t flags, int32_t device, sk_sketch **out);
@@ -130,7 +130,8 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
  *               `out` are written (or accumulated).
  *   first_layer, n_layers  the contiguous layer range this call covers.
  * Arithmetic is fp32 (bf16 inputs are widened exactly); QK multiplies bf16
- * operands with fp32 accumulation.
+ * inputs by the bf16 hi and lo terms of B on the matrix cores with fp32
+ * accumulation, then by the fp32 A.
  */
 int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t batch, float *out,
                  int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream);

@@ -67,7 +67,8 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_pos);
   f(s->d_fjl_seg);
   f(s->d_fjl_smp);
-  f(s->d_qkfac);
+  f(s->d_qka);
+  f(s->d_qkb);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
   s->evpool.clear();
@@ -204,7 +205,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   std::vector<uint16_t> ptab;
   const bool need_pi1 = kind == SK_AFFD || kind == SK_AFJL;
   const bool need_pi2 = kind == SK_AFFD;
-  int64_t qk_col = 0, fac = 0;
+  int64_t qk_col = 0, fac_a = 0, fac_b = 0;
   for (int l = 0; l < n_layers; ++l) {
     LayerDesc &ld = s->layers[l];
     std::memset(&ld, 0, sizeof(ld));
@@ -266,13 +267,14 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       ld.db = shapes[l].qk_db;
       ld.qk_col = qk_col;
       qk_col += (int64_t)ld.da * ld.db;
-      ld.fa_off = fac;
-      fac += (int64_t)ld.da * ld.m;
-      ld.fb_off = fac;
-      fac += (int64_t)ld.db * ld.nc;
+      ld.fa_off = fac_a;
+      fac_a += (int64_t)ld.da * ld.m;
+      ld.fb_off = fac_b;
+      fac_b += (int64_t)ld.db * ld.nc;
     }
   }
-  s->qk_fac_elems = fac;
+  s->qk_a_elems = fac_a;
+  s->qk_b_elems = fac_b;
 
   // AFJL work items: destination rows r of an R x Lw accumulator.
   std::vector<int2> rslot;
@@ -363,7 +365,8 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_fjl_pos, sizeof(uint32_t) * fpos.size()));
   SK_TRY(alloc((void **)&s->d_fjl_seg, sizeof(uint32_t) * fseg.size()));
   SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
-  SK_TRY(alloc((void **)&s->d_qkfac, sizeof(uint16_t) * fac));
+  SK_TRY(alloc((void **)&s->d_qka, sizeof(float) * fac_a));
+  SK_TRY(alloc((void **)&s->d_qkb, sizeof(uint16_t) * 2 * fac_b));
 
   auto h2d = [&](void *d, const void *h, size_t bytes) -> int {
     if (bytes == 0) return SK_OK;

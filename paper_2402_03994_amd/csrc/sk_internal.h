@@ -32,7 +32,7 @@ struct LayerDesc {
   int32_t n_items;    // AFJL: fold items of this layer
   int32_t m, nc, da, db;  // QK shape and block
   int64_t qk_col;     // QK: first output column of the block
-  int64_t fa_off, fb_off;  // QK: element offsets of A (da x m) and B (db x nc) in the factor buffer
+  int64_t fa_off, fb_off;  // QK: element offsets of A (da x m, fp32) and B (db x nc, bf16 hi/lo pairs)
   int32_t lo_len_lg;  // AFFD: log2 of the low block spanned by c < D
   uint32_t hstar;     // AFFD: top-digit index of pi2 at the all-zero low part
 };
@@ -82,8 +82,9 @@ struct sk_sketch {
   uint32_t *d_fjl_seg = nullptr;   // segment starts into d_fjl_smp (per unique position, +1 sentinel per layer)
   uint32_t *d_fjl_smp = nullptr;   // sample ids sorted by (position, id)
   // QK
-  uint16_t *d_qkfac = nullptr;  // bf16 factors
-  int64_t qk_fac_elems = 0;
+  float *d_qka = nullptr;       // A factors, fp32
+  uint16_t *d_qkb = nullptr;    // B factors as bf16 hi terms, then bf16 lo terms (hi + lo ~ fp32 B)
+  int64_t qk_a_elems = 0, qk_b_elems = 0;
   // kernel timing
   struct ProfRec {
     int cls;

@@ -2,7 +2,10 @@
 // Y = A X B^T with A (dA x m) ~ N(0, 1/dA) and B (dB x n) ~ N(0, 1/dB)
 // (eq. straight with two Kronecker factors; the contraction is that of
 // eq. qk_proof_tensor_dec).  Factors are generated on the device at creation
-// in fp32 and rounded to nearest even into bf16; products accumulate in fp32.
+// in fp32.  A is kept in fp32; B is stored as two bf16 terms, hi = bf16(B)
+// and lo = bf16(B - hi) (both rounded to nearest even), so that the bf16
+// MFMA contraction X B^T = X hi^T + X lo^T sees B to 16 mantissa bits.
+// Products accumulate in fp32.
 #include "sk_launch.h"
 
 namespace sk {
@@ -14,20 +17,30 @@ __device__ __forceinline__ uint16_t qk_f2bf(float f) {
 }
 __device__ __forceinline__ float qk_bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-__global__ void k_qk_factor(uint16_t *__restrict__ dst, int64_t count, uint32_t layer, uint32_t stream, float scale,
-                            Key key) {
+__global__ void k_qk_factor_a(float *__restrict__ dst, int64_t count, uint32_t layer, float scale, Key key) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= count) return;
-  dst[i] = qk_f2bf(gauss((uint64_t)i, layer, stream, key) * scale);
+  dst[i] = gauss((uint64_t)i, layer, ST_QKA, key) * scale;
+}
+
+__global__ void k_qk_factor_b(uint16_t *__restrict__ hi, uint16_t *__restrict__ lo, int64_t count, uint32_t layer,
+                              float scale, Key key) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  const float g = gauss((uint64_t)i, layer, ST_QKB, key) * scale;
+  const uint16_t h = qk_f2bf(g);
+  hi[i] = h;
+  lo[i] = qk_f2bf(g - qk_bf2f(h));
 }
 
 void launch_qk_factors(const sk_sketch *s, hipStream_t st) {
   for (const LayerDesc &ld : s->layers) {
     const int64_t na = (int64_t)ld.da * ld.m, nb = (int64_t)ld.db * ld.nc;
-    hipLaunchKernelGGL(k_qk_factor, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, s->d_qkfac + ld.fa_off, na,
-                       (uint32_t)ld.layer_id, (uint32_t)ST_QKA, (float)(1.0 / sqrt((double)ld.da)), s->key);
-    hipLaunchKernelGGL(k_qk_factor, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, st, s->d_qkfac + ld.fb_off, nb,
-                       (uint32_t)ld.layer_id, (uint32_t)ST_QKB, (float)(1.0 / sqrt((double)ld.db)), s->key);
+    hipLaunchKernelGGL(k_qk_factor_a, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, s->d_qka + ld.fa_off, na,
+                       (uint32_t)ld.layer_id, (float)(1.0 / sqrt((double)ld.da)), s->key);
+    hipLaunchKernelGGL(k_qk_factor_b, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, st, s->d_qkb + ld.fb_off,
+                       s->d_qkb + s->qk_b_elems + ld.fb_off, nb, (uint32_t)ld.layer_id,
+                       (float)(1.0 / sqrt((double)ld.db)), s->key);
   }
   (void)hipGetLastError();
 }
@@ -39,8 +52,8 @@ int64_t qk_workspace_elems(const sk_sketch *s, int layer, int64_t bc) {
 
 // T[v][i][c] = sum_j X[v][i][j] B[c][j]
 template <bool BF16>
-__global__ void k_qk_xbt(const void *__restrict__ x, const uint16_t *__restrict__ B, int m, int n, int db,
-                         int64_t b_begin, float *__restrict__ t) {
+__global__ void k_qk_xbt(const void *__restrict__ x, const uint16_t *__restrict__ B, const uint16_t *__restrict__ Blo,
+                         int m, int n, int db, int64_t b_begin, float *__restrict__ t) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * db) return;
@@ -49,20 +62,125 @@ __global__ void k_qk_xbt(const void *__restrict__ x, const uint16_t *__restrict_
   float acc = 0.0f;
   for (int64_t j = 0; j < n; ++j) {
     const float xv = BF16 ? qk_bf2f(((const uint16_t *)x)[xo + j]) : ((const float *)x)[xo + j];
-    acc += xv * qk_bf2f(B[c * n + j]);
+    acc += xv * (qk_bf2f(B[c * n + j]) + qk_bf2f(Blo[c * n + j]));
   }
   t[(v * m + i) * db + c] = acc;
 }
 
+// ---------------------------------------------------------------------------
+// MFMA path (bf16 X, n % 128 == 0, dA and dB multiples of 16, dB <= 128).
+// Stage 1: T^T[v][c][i] = sum_j X[v][i][j] B[c][j], a tall-skinny GEMM over
+// the stacked rows of the batch (M = bc m, N = dB, K = n) on
+// v_mfma_f32_16x16x32_bf16.  Each wave owns 16 rows; each lane streams 64
+// contiguous bytes of its row per 128-wide K step and splits them over four
+// MFMAs.  The pairing of K positions to MFMA slots is a fixed permutation of
+// the contraction index applied identically to X and B, so it does not change
+// the sum.  Stage 2: Y[v][a][c] = sum_i A[a][i] T^T[v][c][i] on
+// v_mfma_f32_16x16x4f32 (fp32 T, bf16 A widened exactly).
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+union Pack8 {
+  uint4 u;
+  bf16x8 v;
+};
+
+template <int NT>
+__global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, const uint16_t *__restrict__ B,
+                                               const uint16_t *__restrict__ Blo, int64_t m, int64_t n,
+                                               int64_t b_begin, int64_t rows, float *__restrict__ tt) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * 64 + wave * 16;  // first stacked row of this wave
+  const int li = lane & 15, g = lane >> 4;
+  const int64_t row = r0 + li;
+  const bool rv = row < rows;
+  const uint16_t *xr = x + (b_begin * m + (rv ? row : 0)) * n + g * 32;
+  const uint16_t *br = B + (int64_t)li * n + g * 32;
+  const uint16_t *brl = Blo + (int64_t)li * n + g * 32;
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < n; k0 += 128) {
+    Pack8 a[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) a[cc].u = rv ? *(const uint4 *)(xr + k0 + cc * 8) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      Pack8 b[4], bl[4];
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        b[cc].u = *(const uint4 *)(br + (int64_t)t * 16 * n + k0 + cc * 8);
+        bl[cc].u = *(const uint4 *)(brl + (int64_t)t * 16 * n + k0 + cc * 8);
+      }
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cc].v, b[cc].v, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cc].v, bl[cc].v, acc[t], 0, 0, 0);
+      }
+    }
+  }
+  // D layout: lane holds rows 4 g .. 4 g + 3 of column li of each 16 x 16 tile
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t R = r0 + g * 4 + i;
+    if (R >= rows) continue;
+    const int64_t v = R / m, ii = R - (R / m) * m;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) tt[(v * (NT * 16) + t * 16 + li) * m + ii] = acc[t][i];
+  }
+}
+
+// one wave per (vector, 16 x 16 output tile); K = m in steps of 16
+__global__ __launch_bounds__(64) void k_qk_s2(const float *__restrict__ A, const float *__restrict__ tt, int64_t m,
+                                              int da, int db, int64_t D, int64_t col, int64_t b_begin,
+                                              float *__restrict__ out, int accumulate) {
+  const int lane = threadIdx.x;
+  const int ntb = db / 16;
+  const int ta = blockIdx.x / ntb, tb = blockIdx.x - (blockIdx.x / ntb) * ntb;
+  const int64_t v = blockIdx.y;
+  const int li = lane & 15, g = lane >> 4;
+  const float *ar = A + (int64_t)(ta * 16 + li) * m + g * 4;
+  const float *tr = tt + (v * db + tb * 16 + li) * m + g * 4;
+  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+  int64_t k0 = 0;
+  for (; k0 + 16 <= m; k0 += 16) {
+    const float4 av = *(const float4 *)(ar + k0);
+    const float4 tv = *(const float4 *)(tr + k0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, tv.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, tv.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, tv.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, tv.w, acc, 0, 0, 0);
+  }
+  for (int e = 0; e < 4; ++e) {  // ragged tail of K (m % 16 != 0)
+    const int64_t k = k0 + g * 4 + e;
+    const bool ok = k < m;
+    const float av = ok ? ar[k0 + e] : 0.0f;
+    const float tv = ok ? tr[k0 + e] : 0.0f;
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, tv, acc, 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int a = ta * 16 + g * 4 + i, c = tb * 16 + li;
+    float *o = out + (b_begin + v) * D + col + (int64_t)a * db + c;
+    *o = accumulate ? *o + acc[i] : acc[i];
+  }
+}
+
+bool qk_mfma_ok(const LayerDesc &ld, int dtype) {
+  return dtype == SK_BF16 && ld.nc % 128 == 0 && ld.m % 16 == 0 && ld.da % 16 == 0 && ld.db % 16 == 0 && ld.db <= 128;
+}
+
 // Y[v][a][c] = sum_i A[a][i] T[v][i][c]
-__global__ void k_qk_at(const uint16_t *__restrict__ A, const float *__restrict__ t, int m, int da, int db,
+__global__ void k_qk_at(const float *__restrict__ A, const float *__restrict__ t, int m, int da, int db,
                         int64_t D, int64_t col, int64_t b_begin, float *__restrict__ out, int accumulate) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)da * db) return;
   const int64_t a = e / db, c = e - (e / db) * db;
   float acc = 0.0f;
-  for (int64_t i = 0; i < m; ++i) acc += qk_bf2f(A[a * m + i]) * t[(v * m + i) * db + c];
+  for (int64_t i = 0; i < m; ++i) acc += A[a * m + i] * t[(v * m + i) * db + c];
   float *o = out + (b_begin + v) * D + col + e;
   *o = accumulate ? *o + acc : acc;
 }
@@ -71,12 +189,33 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
                      float *t_ws, int64_t batch_total, float *out, bool accumulate, hipStream_t st) {
   (void)batch_total;
   const LayerDesc &ld = s->layers[layer];
-  const uint16_t *A = s->d_qkfac + ld.fa_off, *B = s->d_qkfac + ld.fb_off;
+  const float *A = s->d_qka + ld.fa_off;
+  const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
+  if (qk_mfma_ok(ld, dtype)) {
+    const int64_t rows = bc * (int64_t)ld.m;
+    dim3 g1((unsigned)((rows + 63) / 64));
+#define SK_S1(NT)                                                                                              \
+  case NT:                                                                                                     \
+    hipLaunchKernelGGL(k_qk_s1<NT>, g1, dim3(256), 0, st, (const uint16_t *)x, B, Blo, (int64_t)ld.m,           \
+                       (int64_t)ld.nc,                                                                         \
+                       b_begin, rows, t_ws);                                                                   \
+    break;
+    switch (ld.db / 16) {
+      SK_S1(1) SK_S1(2) SK_S1(3) SK_S1(4) SK_S1(5) SK_S1(6) SK_S1(7) SK_S1(8)
+      default: break;
+    }
+#undef SK_S1
+    dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
+    hipLaunchKernelGGL(k_qk_s2, g2, dim3(64), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin,
+                       out, (int)accumulate);
+    (void)hipGetLastError();
+    return;
+  }
   dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
   if (dtype == SK_BF16)
-    hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, B, ld.m, ld.nc, ld.db, b_begin, t_ws);
+    hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
   else
-    hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, B, ld.m, ld.nc, ld.db, b_begin, t_ws);
+    hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
   dim3 g2((unsigned)(((int64_t)ld.da * ld.db + 255) / 256), (unsigned)bc);
   hipLaunchKernelGGL(k_qk_at, g2, dim3(256), 0, st, A, t_ws, ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, out,
                      (int)accumulate);
@@ -84,26 +223,27 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
 }
 
 // U[v][i][c] = sum_a A[a][i] Z[v][a][c]
-__global__ void k_qk_atz(const uint16_t *__restrict__ A, const float *__restrict__ z, int m, int da, int db, int64_t D,
+__global__ void k_qk_atz(const float *__restrict__ A, const float *__restrict__ z, int m, int da, int db, int64_t D,
                          int64_t col, int64_t b_begin, float *__restrict__ u) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * db) return;
   const int64_t i = e / db, c = e - (e / db) * db;
   float acc = 0.0f;
-  for (int64_t a = 0; a < da; ++a) acc += qk_bf2f(A[a * m + i]) * z[(b_begin + v) * D + col + a * db + c];
+  for (int64_t a = 0; a < da; ++a) acc += A[a * m + i] * z[(b_begin + v) * D + col + a * db + c];
   u[(v * m + i) * db + c] = acc;
 }
 
 // X'[v][i][j] = sum_c U[v][i][c] B[c][j] (+ theta0)
-__global__ void k_qk_ub(const uint16_t *__restrict__ B, const float *__restrict__ u, int m, int n, int db,
+__global__ void k_qk_ub(const uint16_t *__restrict__ B, const uint16_t *__restrict__ Blo, const float *__restrict__ u,
+                        int m, int n, int db,
                         int64_t b_begin, void *__restrict__ out, int out_dtype, const float *__restrict__ theta0) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * n) return;
   const int64_t i = e / n, j = e - (e / n) * n;
   float acc = 0.0f;
-  for (int64_t c = 0; c < db; ++c) acc += u[(v * m + i) * db + c] * qk_bf2f(B[c * n + j]);
+  for (int64_t c = 0; c < db; ++c) acc += u[(v * m + i) * db + c] * (qk_bf2f(B[c * n + j]) + qk_bf2f(Blo[c * n + j]));
   if (theta0) acc += theta0[e];
   const int64_t o = (b_begin + v) * (int64_t)m * n + e;
   if (out_dtype == SK_BF16)
@@ -115,11 +255,12 @@ __global__ void k_qk_ub(const uint16_t *__restrict__ B, const float *__restrict_
 void launch_qk_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *t_ws,
                        void *out, int out_dtype, const float *theta0, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
-  const uint16_t *A = s->d_qkfac + ld.fa_off, *B = s->d_qkfac + ld.fb_off;
+  const float *A = s->d_qka + ld.fa_off;
+  const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
   dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
   hipLaunchKernelGGL(k_qk_atz, g1, dim3(256), 0, st, A, z, ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, t_ws);
   dim3 g2((unsigned)(((int64_t)ld.m * ld.nc + 255) / 256), (unsigned)bc);
-  hipLaunchKernelGGL(k_qk_ub, g2, dim3(256), 0, st, B, t_ws, ld.m, ld.nc, ld.db, b_begin, out, out_dtype, theta0);
+  hipLaunchKernelGGL(k_qk_ub, g2, dim3(256), 0, st, B, Blo, t_ws, ld.m, ld.nc, ld.db, b_begin, out, out_dtype, theta0);
   (void)hipGetLastError();
 }
 

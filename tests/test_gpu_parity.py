@@ -128,8 +128,8 @@ def test_streaming_accumulate_and_determinism(kind, dev):
     out = torch.zeros_like(y1)
     for l, x in enumerate(xs):
         s.apply([x], out=out, first_layer=l, accumulate=True)
-    ref = O.apply(kind, shapes, D, 11, [x.cpu().numpy() for x in xs], qk_bf16=(kind == "qk"))
-    assert rel_err(out.cpu().numpy(), ref) < (1e-3 if kind == "qk" else TOL_F32)
+    ref = O.apply(kind, shapes, D, 11, [x.cpu().numpy() for x in xs])
+    assert rel_err(out.cpu().numpy(), ref) < (1e-4 if kind == "qk" else TOL_F32)
 
 
 def test_debug_streams_bit_exact(dev):
@@ -158,7 +158,9 @@ def test_debug_streams_bit_exact(dev):
 
 
 @pytest.mark.parametrize("shapes,D", [([(40, 70, 4, 5), (64, 33, 8, 2), (1, 300, 1, 9)], 45),
-                                      ([(256, 512, 32, 16), (300, 200, 16, 32)], 32 * 16 * 2)])
+                                      ([(256, 512, 32, 16), (300, 200, 16, 32)], 32 * 16 * 2),
+                                      ([(2048, 2048, 32, 16), (512, 1024, 32, 128), (1024, 256, 128, 32),
+                                        (208, 384, 64, 48)], 512 + 4096 + 4096 + 3072)])
 def test_qk_parity(shapes, D, dev):
     seed = 21
     xs = rand_inputs(shapes, 3, seed, dtype=torch.bfloat16, scale=0.01)
@@ -166,12 +168,13 @@ def test_qk_parity(shapes, D, dev):
     y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
     ins = [oracle_in(x)[0] for x in xs]
     exact = O.apply("qk", shapes, D, seed, ins, dtype="bf16")
+    # bound of the configuration for bf16 inputs; the factors carry ~16
+    # mantissa bits, so the error is far below it
     assert rel_err(y, exact) < TOL_BF16
-    rounded = O.apply("qk", shapes, D, seed, ins, dtype="bf16", qk_bf16=True)
-    assert rel_err(y, rounded) < 1e-3
+    assert rel_err(y, exact) < 1e-4
     g = torch.Generator().manual_seed(3)
     z = torch.randn((2, D), generator=g)
     outs = s.apply_T(z.to(dev))
-    refs = O.apply_T("qk", shapes, D, seed, z.numpy().astype(np.float64), qk_bf16=True)
+    refs = O.apply_T("qk", shapes, D, seed, z.numpy().astype(np.float64))
     for o, r in zip(outs, refs):
-        assert rel_err(o.cpu().numpy(), r) < 1e-3
+        assert rel_err(o.cpu().numpy(), r) < 1e-4
