@@ -1,19 +1,22 @@
 #!/usr/bin/env python3
-"""Throughput of the gradient sketches on one MI355X.
+"""Throughput of the structured sketches on one MI355X.
 
-Workload (default): per-example gradients shaped like GPT-2 small (148
-parameter tensors, N = 124,439,808 parameters), fp32 entries N(0, 1e-4),
-batch 64, sketched to D = 2^16 with AFJL and with AFFD (seed 1).  One step
-sketches the whole batch with both kinds; inputs are resident in HBM before
-the timed region.  Prints one JSON line.
+Default workload (--config c2): per-example gradients shaped like GPT-2 small
+(148 tensors, N = 124,439,808), fp32 entries N(0, 1e-4), batch 64, sketched to
+D = 2^16 by AFJL and by AFFD (seed 1).  One step sketches the whole batch with
+both kinds; inputs are resident in HBM before the timed region.  Other
+workloads (--config c1|c3|c4|c5) are described in workloads.py.  Prints one
+JSON line.
 
-The roofline object covers the kernel class with the largest share of device
-time, timed with HIP events on the stream its launches run on; its
-"achieved" figure is the algorithmic bytes of those launches (inputs read
-once, outputs written once) over their summed duration.  HBM traffic measured
-with rocprofv3 counters is read from profiles/ when it was taken on the
-current kernel source.  The fp64 oracle is timed on the host beside it on a
-bounded sample.
+"value" is parameter-space bytes per second: gradient bytes read by forward
+sketches plus parameter-vector bytes written by transposes, summed over the
+calls of a step.  The roofline object covers the kernel class with the largest
+share of device time, timed with HIP events on the stream its launches run
+on; "achieved" is the algorithmic bytes of those launches (inputs read once,
+outputs written once) over their summed duration.  HBM traffic measured with
+rocprofv3 counters is attached from profiles/ when it was taken on the
+current kernel source.  The fp64 oracle is timed on the host on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -27,22 +30,11 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+import workloads as W  # noqa: E402
+
 METRIC = "gradient GB/s sketched and vectors/s at N=124M, D=2^16; % HBM/MFMA peak"
 HBM_PEAK_GBS = 8000.0
-
-
-def gpt2_small_shapes():
-    """Parameter tensors of GPT-2 small in module order (wte, wpe, 12 blocks, ln_f)."""
-    s = [(50257, 768), (1024, 768)]
-    for _ in range(12):
-        s += [(1, 768), (1, 768),            # ln_1 weight, bias
-              (768, 2304), (1, 2304),        # attn.c_attn
-              (768, 768), (1, 768),          # attn.c_proj
-              (1, 768), (1, 768),            # ln_2
-              (768, 3072), (1, 3072),        # mlp.c_fc
-              (3072, 768), (1, 768)]         # mlp.c_proj
-    s += [(1, 768), (1, 768)]                # ln_f
-    return s
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def source_hash() -> str:
@@ -54,33 +46,161 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kclass: str):
-    """HBM bytes per algorithmic byte from a committed rocprofv3 counter summary, if current."""
-    p = os.path.join(ROOT, "profiles", f"traffic_{kclass}_gpt2s_b64_d65536.json")
+def measured_traffic(cfg: str, kclass: str):
+    """HBM bytes per launch of a kernel class from a committed rocprofv3 counter summary, if current."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{cfg}_{kclass.replace(':', '_')}.json")
     if not os.path.exists(p):
         return None
     rec = json.load(open(p))
     if rec.get("source_hash") != source_hash():
         return None
-    return rec
+    return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(shapes, D, seed, kinds):
-    """The fp64 oracle on one batch row (all layers, every kind of the step)."""
+# ------------------------------------------------------------------ CPU baseline
+def cpu_baseline(cfg: str):
+    """The fp64 oracle on a bounded sample of the workload (all host cores)."""
     import numpy as np
 
     import oracle as O
 
+    c = W.CONFIGS[cfg]
     cores = len(os.sched_getaffinity(0))
-    rng = np.random.default_rng(1002)
-    xs = [(rng.standard_normal((1, r * c), dtype=np.float32) * 0.01) for r, c in shapes]
+    rng = np.random.default_rng(W.INPUT_SEED[cfg])
+    shapes, D, seed = c["shapes"], c["D"], c["seed"]
+
+    def rows_for(sh, nrows, var=1e-4):
+        return [(rng.standard_normal((nrows, s[0] * s[1]), dtype=np.float32) * np.float32(np.sqrt(var)))
+                for s in sh]
+
     t0 = time.perf_counter()
-    for k in kinds:
-        O.apply(k, shapes, D, seed, xs, nthreads=cores)
+    if cfg == "c1":
+        xs = rows_for(shapes, c["batch"], 1.0)
+        z = rng.standard_normal((c["batch"], D))
+        for k in c["kinds"]:
+            O.apply(k, shapes, D, seed, xs, nthreads=cores)
+            O.apply_T(k, shapes, D, seed, z, nthreads=cores)
+        nbytes = 2 * len(c["kinds"]) * c["batch"] * shapes[0][1] * 4
+        sample = f"all {c['batch']} rows, FJL+FFD forward and transpose"
+    elif cfg == "c2":
+        xs = rows_for(shapes, 1)
+        for k in c["kinds"]:
+            O.apply(k, shapes, D, seed, xs, nthreads=cores)
+        nbytes = len(c["kinds"]) * sum(r * cc for r, cc in shapes) * 4
+        sample = f"1 of {c['batch']} rows, all {len(shapes)} tensors, AFJL+AFFD"
+    elif cfg == "c3":
+        sub = shapes[1:7]  # one decoder layer: q, k, v, o, fc1, fc2
+        bf = [W.bf16_bits(x) for x in rows_for(sub, 1)]
+        O.apply("qk", sub, sum(s[2] * s[3] for s in sub), seed, bf, dtype="bf16", layer0=1, nthreads=cores)
+        nbytes = sum(s[0] * s[1] for s in sub) * 2
+        sample = "1 of 256 rows, one decoder layer (6 of 145 matrices), QK"
+    elif cfg == "c4":
+        z = rng.standard_normal((1, D))
+        O.apply_T("ffd", shapes, D, seed, z, nthreads=cores)
+        xs = [rng.standard_t(3, size=(1, shapes[0][1])).astype(np.float32)]
+        O.apply("ffd", shapes, D, seed, xs, nthreads=cores)
+        nbytes = 2 * shapes[0][1] * 4
+        sample = "1 of 4 rows, FFD transpose and forward"
+    else:  # c5
+        first, cnt = W.llama3_8b_stream_groups()[1]
+        sub = shapes[first:first + cnt]
+        xs = rows_for(sub, 1, 1e-5)
+        bf = [W.bf16_bits(x) for x in xs]
+        O.apply("afjl", sub, D, seed, bf, dtype="bf16", layer0=first, nthreads=cores)
+        nbytes = sum(s[0] * s[1] for s in sub) * 2
+        sample = "1 of 8 rows, one transformer block (9 of 291 tensors), AFJL"
     dt = time.perf_counter() - t0
-    nbytes = len(kinds) * sum(r * c for r, c in shapes) * 4
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
-            "sample": f"1 of 64 batch rows, all {len(shapes)} tensors, {'+'.join(kinds)} ({dt:.1f} s)"}
+            "sample": f"{sample} ({dt:.1f} s)"}
+
+
+# ------------------------------------------------------------------ GPU steps
+def build_step(cfg: str, dev):
+    """Returns (sketches, step(evs), param_bytes_per_step, vectors_per_step, description)."""
+    import torch
+
+    from paper_2402_03994_amd import Sketch
+
+    c = W.CONFIGS[cfg]
+    shapes, D, B, seed = c["shapes"], c["D"], c["batch"], c["seed"]
+    numels = [s[0] * s[1] for s in shapes]
+    gen = W.generator(cfg, dev)
+    bf16 = c["dtype"] == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    sks = {k: Sketch(k, shapes, D, seed, device=dev) for k in c["kinds"]}
+
+    if cfg == "c1":
+        nrot = 16  # rotate inputs so they come from HBM, not the 256 MB cache
+        xs = [W.gaussian((B, numels[0]), 1.0, gen, dev) for _ in range(nrot)]
+        z = torch.randn((B, D), generator=gen, device=dev)
+        outs = {k: torch.empty((B, D), device=dev) for k in c["kinds"]}
+        touts = {k: [torch.empty((B, numels[0]), device=dev)] for k in c["kinds"]}
+        state = {"i": 0}
+
+        def step(ev):
+            x = xs[state["i"] % nrot]
+            state["i"] += 1
+            for k in c["kinds"]:
+                ev(k, "fwd", lambda k=k: sks[k].apply([x], out=outs[k]))
+                ev(k, "T", lambda k=k: sks[k].apply_T(z, outs=touts[k]))
+        return sks, step, 2 * len(c["kinds"]) * B * numels[0] * 4, B, \
+            f"flat fp32 vectors N=2^20 entries N(0,1), batch {B}, D=4096, seed 0: FJL and FFD forward + transpose"
+
+    if cfg == "c2":
+        xs = [W.gaussian((B, n), 1e-4, gen, dev) for n in numels]
+        outs = {k: torch.empty((B, D), device=dev) for k in c["kinds"]}
+
+        def step(ev):
+            for k in c["kinds"]:
+                ev(k, "fwd", lambda k=k: sks[k].apply(xs, out=outs[k]))
+        return sks, step, len(c["kinds"]) * B * sum(numels) * 4, B, \
+            (f"GPT-2-small-shaped fp32 gradients N(0,1e-4), {len(shapes)} tensors, N={sum(numels)}, batch {B}, "
+             f"D=2^16, seed 1: AFJL and AFFD")
+
+    if cfg == "c3":
+        # one resident input per distinct matrix shape, shared by the matrices of that shape
+        bufs = {}
+        for s in shapes:
+            key = (s[0], s[1])
+            if key not in bufs:
+                bufs[key] = W.gaussian((B, s[0] * s[1]), 1e-4, gen, dev, dtype=torch.bfloat16)
+        xs = [bufs[(s[0], s[1])] for s in shapes]
+        out = torch.empty((B, D), device=dev)
+
+        def step(ev):
+            ev("qk", "fwd", lambda: sks["qk"].apply(xs, out=out))
+        return sks, step, B * sum(numels) * 2, B, \
+            (f"QK on 1.3B-decoder-shaped bf16 gradients N(0,1e-4), {len(shapes)} matrices, N={sum(numels)}, "
+             f"batch {B}, D=2^18, (dA,dB) q/k/v/o 32x16, fc1 32x128, fc2 128x32, embed 256x64")
+
+    if cfg == "c4":
+        n = numels[0]
+        z = torch.randn((B, D), generator=gen, device=dev)
+        theta0 = W.gaussian((n,), 0.02 ** 2, gen, dev)
+        theta = [torch.empty((B, n), device=dev)]
+        x = W.student_t3((B, n), gen, dev)
+        out = torch.empty((B, D), device=dev)
+
+        def step(ev):
+            ev("ffd", "T", lambda: sks["ffd"].apply_T(z, theta0=[theta0], outs=theta))
+            ev("ffd", "fwd", lambda: sks["ffd"].apply([x], out=out))
+        return sks, step, 2 * B * n * 4, B, \
+            ("FFD on one 1e8-entry vector (padded to 2^27), D=2^20, batch 4: theta0 + S^T z (z ~ N(0,1)) and "
+             "S x for Student-t(3) x")
+
+    # c5
+    xs = [W.gaussian((B, n), 1e-5, gen, dev, dtype=torch.bfloat16) for n in numels]
+    out = torch.empty((B, D), device=dev)
+    groups = W.llama3_8b_stream_groups()
+
+    def step(ev):
+        def run():
+            for i, (f, cnt) in enumerate(groups):
+                sks["afjl"].apply(xs[f:f + cnt], out=out, first_layer=f, accumulate=i > 0)
+        ev("afjl", "fwd", run)
+    return sks, step, B * sum(numels) * 2, B, \
+        (f"AFJL on Llama-3-8B-shaped bf16 gradients N(0,1e-5), {len(shapes)} tensors, N={sum(numels)}, batch {B}, "
+         f"D=2^20, seed 7, streamed one transformer block per call")
 
 
 def main() -> int:
@@ -88,8 +208,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--kinds", default="afjl,affd")
-    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--config", default="c2", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -99,86 +218,78 @@ def main() -> int:
 
     import torch
 
-    from paper_2402_03994_amd import Sketch, _lib
-
     dev = torch.device("cuda", 0)
-    shapes = gpt2_small_shapes()
-    numels = [r * c for r, c in shapes]
-    N = sum(numels)
-    B, D, seed = args.batch, 1 << 16, 1
-    kinds = [k for k in args.kinds.split(",") if k]
+    cfg = args.config
+    sks, step, pbytes, vecs, desc = build_step(cfg, dev)
+    torch.cuda.synchronize()
 
-    gen = torch.Generator(device=dev).manual_seed(1002)
-    xs = [torch.randn((B, n), generator=gen, device=dev, dtype=torch.float32).mul_(0.01) for n in numels]
-    sks = {k: Sketch(k, shapes, D, seed, device=dev) for k in kinds}
-    outs = {k: torch.empty((B, D), device=dev, dtype=torch.float32) for k in kinds}
-
-    def step(evs=None):
-        for i, k in enumerate(kinds):
-            if evs is not None:
-                evs[k][0].record()
-            sks[k].apply(xs, out=outs[k])
-            if evs is not None:
-                evs[k][1].record()
+    def ev_none(kind, tag, fn):
+        fn()
 
     for _ in range(args.warmup):
-        step()
+        step(ev_none)
     torch.cuda.synchronize()
 
-    for k in kinds:
-        sks[k].profile(True)
-    per_kind = {k: 0.0 for k in kinds}
+    per_call = {}
+
+    def ev_timed(kind, tag, fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        per_call.setdefault(f"{kind}:{tag}", []).append((a, b))
+
+    for s in sks.values():
+        s.profile(True)
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        evs = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in kinds}
-        step(evs)
-        torch.cuda.synchronize()
-        for k in kinds:
-            per_kind[k] += evs[k][0].elapsed_time(evs[k][1])
+        step(ev_timed)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = {k: sks[k].profile_read() for k in kinds}
-    for k in kinds:
-        sks[k].profile(False)
+    prof = {k: s.profile_read() for k, s in sks.items()}
+    for s in sks.values():
+        s.profile(False)
 
     ms = (t1 - t0) * 1e3 / args.steps
-    bytes_step = len(kinds) * B * N * 4
-    value = bytes_step / (ms * 1e-3) / 1e9
+    value = pbytes / (ms * 1e-3) / 1e9
+    call_ms = {k: round(sum(a.elapsed_time(b) for a, b in v) / args.steps, 3) for k, v in per_call.items()}
 
-    # dominant kernel class by device time
     classes = {}
-    for k in kinds:
-        for c, (t, n, by) in prof[k].items():
-            e = classes.setdefault(f"{k}:{c}", [0.0, 0, 0])
+    for k in sks:
+        for cl, (t, n, by) in prof[k].items():
+            e = classes.setdefault(f"{k}:{cl}", [0.0, 0, 0])
             e[0] += t
             e[1] += n
             e[2] += by
     dom = max(classes, key=lambda c: classes[c][0])
     t_dom, n_dom, by_dom = classes[dom]
     achieved = by_dom / (t_dom * 1e-3) / 1e9 if t_dom > 0 else 0.0
-    tr = measured_traffic(dom.replace(":", "_"))
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": (round(tr["hbm_bytes_per_launch"]) if tr else None),
+                "traffic": measured_traffic(cfg, dom),
                 "launches": n_dom, "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),
                 "algorithmic_bytes_per_launch": round(by_dom / max(n_dom, 1))}
+    if cfg == "c3":
+        c = W.CONFIGS[cfg]
+        flops = sum(2 * s[0] * s[1] * s[3] + 2 * s[2] * s[0] * s[3] for s in c["shapes"]) * c["batch"]
+        roofline["mfma_tflops"] = round(flops / (t_dom * 1e-3 / args.steps) / 1e12, 1)
+        roofline["mfma_frac"] = round(roofline["mfma_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4)
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"GPT-2-small-shaped fp32 gradients N(0,1e-4), {len(shapes)} tensors, "
-                               f"N={N}, batch {B}, D=2^16, seed 1, kinds {'+'.join(kinds)}",
-                   "N": N, "batch": B, "D": D, "kinds": kinds},
-        "vectors_per_s": round(B / (ms * 1e-3), 1),
-        "per_kind_ms": {k: round(per_kind[k] / args.steps, 3) for k in kinds},
-        "per_kind_GBps": {k: round(B * N * 4 / (per_kind[k] / args.steps * 1e-3) / 1e9, 1) for k in kinds},
+        "vs_baseline": None, "dtype": W.CONFIGS[cfg]["dtype"], "data": "synthetic",
+        "config": {"workload": desc, "name": cfg, "batch": W.CONFIGS[cfg]["batch"], "D": W.CONFIGS[cfg]["D"],
+                   "kinds": list(W.CONFIGS[cfg]["kinds"])},
+        "vectors_per_s": round(vecs / (ms * 1e-3), 1),
+        "per_call_ms": call_ms,
         "kernel_classes_ms_per_step": {c: round(v[0] / args.steps, 3) for c, v in sorted(classes.items())},
         "roofline": roofline,
         "source_hash": source_hash(),
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(shapes, D, seed, kinds)
+        line["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -92,10 +92,10 @@ struct ProfScope {
     if (idx >= 0) (void)hipEventRecord(s->evpool[idx + 1], st);
   }
 };
-#define SK_PROF(cls, bytes, stmt)        \
-  do {                                   \
+#define SK_PROF(cls, bytes, ...)          \
+  do {                                    \
     ProfScope ps_(s, (cls), (bytes), st); \
-    stmt;                                \
+    __VA_ARGS__;                          \
   } while (0)
 
 // Bytes of workspace one vector needs for one call over layers [l0, l1).
@@ -382,7 +382,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(h2d(s->d_fjl_seg, fseg.data(), sizeof(uint32_t) * fseg.size()));
   SK_TRY(h2d(s->d_fjl_smp, fsmp.data(), sizeof(uint32_t) * fsmp.size()));
 
-  // workspace: room for up to 64 vectors of the largest per-vector need
+  // workspace: room for up to 256 vectors of the largest per-vector need
   const int64_t pv = std::max(per_vector_bytes(s, 0, n_layers, false), per_vector_bytes(s, 0, n_layers, true));
   const int64_t budget = workspace_budget();
   if (pv > budget) {
@@ -390,7 +390,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     delete s;
     return fail(SK_EUNSUPPORTED, "one vector needs " + std::to_string(pv) + " bytes of workspace, above the budget");
   }
-  s->ws_bytes = std::min<int64_t>(budget, pv * 64);
+  s->ws_bytes = std::min<int64_t>(budget, pv * 256);
   if (s->ws_bytes > 0) SK_TRY(alloc((void **)&s->ws, (size_t)s->ws_bytes));
 
   if (s->d_gtab) launch_gauss_table(s, s->d_gtab, nullptr);
@@ -534,11 +534,13 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
           } else {
             const int64_t nlive = ffd_live_blocks(s, l);
             float *w = s->ws, *w2 = s->ws + bc * nlive * s->D;
-            launch_ffd_copy_blocks(s, l, grads[l - l0], dtype, b0, bc, w, st);
-            fwht_inplace(w, bc * nlive, lgD, st);
-            launch_ffd_gperm_fwd(s, l, w, bc, w2, st);
-            fwht_inplace(w2, bc * nlive, lgD, st);
-            launch_ffd_sum_signed(s, l, w2, b0, bc, out, accumulate || l > l0, st);
+            SK_PROF(SK_PROF_PROLOG, bc * s->layers[l].n * esz,
+                    launch_ffd_copy_blocks(s, l, grads[l - l0], dtype, b0, bc, w, st));
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w, bc * nlive, lgD, st));
+            SK_PROF(SK_PROF_FFD, 0, launch_ffd_gperm_fwd(s, l, w, bc, w2, st));
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w2, bc * nlive, lgD, st));
+            SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                    launch_ffd_sum_signed(s, l, w2, b0, bc, out, accumulate || l > l0, st));
           }
         }
         break;
@@ -578,42 +580,50 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
       const LayerDesc &ld = s->layers[l];
       void *o = out[l - l0];
       const float *th = theta0 ? (const float *)theta0[l - l0] : nullptr;
+      const int osz = out_dtype == SK_BF16 ? 2 : 4;
+      const int64_t obytes = bc * ld.n * osz + (th ? ld.n * 4 : 0);  // output written, theta0 read
       switch (s->kind) {
         case SK_AFJL:
-          launch_afjl_T_prep(s, l, z, b0, bc, s->ws, st);
-          fwht_inplace(s->ws, bc, lgD, st);
-          launch_afjl_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st);
+          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_afjl_T_prep(s, l, z, b0, bc, s->ws, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, lgD, st));
+          SK_PROF(SK_PROF_GATHER, obytes, launch_afjl_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st));
           break;
         case SK_AFFD:
-          launch_fill_zero(s->ws, bc * ld.np, st);
-          launch_affd_T_scatter(s, l, z, b0, bc, s->ws, st);
-          fwht_inplace(s->ws, bc, ld.lgnp, st);
-          launch_mul_gauss(s, l, s->ws, bc, st);
-          fwht_inplace(s->ws, bc, ld.lgnp, st);
-          launch_affd_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st);
+          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, {
+            launch_fill_zero(s->ws, bc * ld.np, st);
+            launch_affd_T_scatter(s, l, z, b0, bc, s->ws, st);
+          });
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+          SK_PROF(SK_PROF_OTHER, 0, launch_mul_gauss(s, l, s->ws, bc, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+          SK_PROF(SK_PROF_GATHER, obytes, launch_affd_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st));
           break;
         case SK_FJL:
-          launch_fill_zero(s->ws, bc * ld.np, st);
-          launch_fjl_T_scatter(s, l, z, b0, bc, s->ws, st);
-          fwht_inplace(s->ws, bc, ld.lgnp, st);
-          launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th, (float)std::sqrt((double)ld.np / (double)s->D),
-                            st);
+          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, {
+            launch_fill_zero(s->ws, bc * ld.np, st);
+            launch_fjl_T_scatter(s, l, z, b0, bc, s->ws, st);
+          });
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+          SK_PROF(SK_PROF_GATHER, obytes,
+                  launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th,
+                                    (float)std::sqrt((double)ld.np / (double)s->D), st));
           break;
         case SK_FFD:
           if (lgD <= kFfdSmallMax) {
-            launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st);
+            SK_PROF(SK_PROF_FFD, obytes + bc * s->D * 4, launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st));
           } else {
             const int64_t nlive = ffd_live_blocks(s, l);
             float *w = s->ws, *w2 = s->ws + bc * nlive * s->D;
-            launch_ffd_expand_z(s, l, z, b0, bc, w, st);
-            fwht_inplace(w, bc * nlive, lgD, st);
-            launch_ffd_permg_T(s, l, w, bc, w2, st);
-            fwht_inplace(w2, bc * nlive, lgD, st);
-            launch_ffd_T_out(s, l, w2, b0, bc, o, out_dtype, th, st);
+            SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_ffd_expand_z(s, l, z, b0, bc, w, st));
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w, bc * nlive, lgD, st));
+            SK_PROF(SK_PROF_FFD, 0, launch_ffd_permg_T(s, l, w, bc, w2, st));
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w2, bc * nlive, lgD, st));
+            SK_PROF(SK_PROF_GATHER, obytes, launch_ffd_T_out(s, l, w2, b0, bc, o, out_dtype, th, st));
           }
           break;
         case SK_QK:
-          launch_qk_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st);
+          SK_PROF(SK_PROF_QK, obytes + bc * ld.da * ld.db * 4,
+                  launch_qk_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
           break;
       }
     }

@@ -1,0 +1,108 @@
+"""Synthetic workloads of the benchmark and the full-size parity tests.
+
+Shapes of the parameter tensors the sketches are applied to, and seeded input
+generators.  Nothing here computes any part of a sketch; both the benchmark
+(GPU inputs) and the tests (the same inputs handed to the oracle) take their
+inputs from this module.
+
+The paper measures real per-example gradients of fine-tuned language models;
+no checkpoint or dataset is available here, so model-shaped tensors with
+Gaussian (or heavy-tailed) entries stand in for them.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+
+def gpt2_small_shapes():
+    """GPT-2 small (N = 124,439,808): wte, wpe, 12 blocks, ln_f, in module order."""
+    s = [(50257, 768), (1024, 768)]
+    for _ in range(12):
+        s += [(1, 768), (1, 768),            # ln_1 weight, bias
+              (768, 2304), (1, 2304),        # attn.c_attn
+              (768, 768), (1, 768),          # attn.c_proj
+              (1, 768), (1, 768),            # ln_2
+              (768, 3072), (1, 3072),        # mlp.c_fc
+              (3072, 768), (1, 768)]         # mlp.c_proj
+    s += [(1, 768), (1, 768)]                # ln_f
+    return s
+
+
+def decoder_1p3b_qk_shapes():
+    """Weight matrices of a 1.3B-shaped decoder (24 layers, d=2048, ffn 8192,
+    vocab 50304) with their QK output blocks (dA, dB); sum dA*dB = 2^18."""
+    s = [(50304, 2048, 256, 64)]
+    for _ in range(24):
+        s += [(2048, 2048, 32, 16)] * 4     # q, k, v, o
+        s += [(2048, 8192, 32, 128),        # fc1
+              (8192, 2048, 128, 32)]        # fc2
+    return s
+
+
+def llama3_8b_shapes():
+    """Llama-3-8B parameter tensors (N = 8,030,261,248) in module order."""
+    s = [(128256, 4096)]
+    for _ in range(32):
+        s += [(4096, 4096), (1024, 4096), (1024, 4096), (4096, 4096),   # q, k, v, o
+              (14336, 4096), (14336, 4096), (4096, 14336),              # gate, up, down
+              (1, 4096), (1, 4096)]                                     # input / post-attention RMSNorm
+    s += [(1, 4096), (128256, 4096)]                                     # final norm, lm_head
+    return s
+
+
+def llama3_8b_stream_groups():
+    """Layer ranges (first, count) of the streamed calls: embedding, one call per
+    transformer block, then final norm + lm_head."""
+    g = [(0, 1)]
+    for b in range(32):
+        g.append((1 + 9 * b, 9))
+    g.append((1 + 9 * 32, 2))
+    return g
+
+
+CONFIGS = {
+    "c1": dict(kinds=("fjl", "ffd"), shapes=[(1, 1 << 20)], D=4096, batch=8, seed=0, dtype="f32"),
+    "c2": dict(kinds=("afjl", "affd"), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
+    "c3": dict(kinds=("qk",), shapes=decoder_1p3b_qk_shapes(), D=1 << 18, batch=256, seed=0, dtype="bf16"),
+    "c4": dict(kinds=("ffd",), shapes=[(1, 100_000_000)], D=1 << 20, batch=4, seed=0, dtype="f32"),
+    "c5": dict(kinds=("afjl",), shapes=llama3_8b_shapes(), D=1 << 20, batch=8, seed=7, dtype="bf16"),
+}
+INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005}
+# variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
+GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5}
+
+
+def gaussian(shape, var: float, gen: torch.Generator, device, dtype=torch.float32) -> torch.Tensor:
+    """Entries N(0, var); bf16 tensors are drawn in fp32 (one leading index at a
+    time) and rounded to nearest even."""
+    if dtype == torch.float32:
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32).mul_(math.sqrt(var))
+    out = torch.empty(shape, device=device, dtype=dtype)
+    for i in range(shape[0]):
+        out[i] = torch.randn(shape[1:], generator=gen, device=device, dtype=torch.float32).mul_(math.sqrt(var))
+    return out
+
+
+def student_t3(shape, gen: torch.Generator, device) -> torch.Tensor:
+    """Student-t with 3 degrees of freedom: Z / sqrt(chi2_3 / 3) (heavy-tailed, HVP-like)."""
+    z = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+    chi2 = torch.zeros(shape, device=device, dtype=torch.float32)
+    for _ in range(3):
+        e = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+        chi2.add_(e * e)
+    return z.div_(torch.sqrt(chi2.div_(3.0)))
+
+
+def bf16_bits(x):
+    """float32 numpy array -> bf16 bit patterns (uint16), rounded to nearest even."""
+    import numpy as np
+
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def generator(cfg: str, device) -> torch.Generator:
+    return torch.Generator(device=device).manual_seed(INPUT_SEED[cfg])
