@@ -474,7 +474,8 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
           for (int l = g0; l < g1; ++l) {
             pp.p[l - g0] = grads[l - l0];
             gb += bc * s->layers[l].n * esz;
-            if ((s->layers[l].n & 3) || ((uintptr_t)grads[l - l0] & (uintptr_t)(esz * 4 - 1))) vec = false;
+            // vector loads: 4 fp32 or 8 bf16 elements (16 bytes) per thread
+            if ((s->layers[l].n & (dtype == SK_BF16 ? 7 : 3)) || ((uintptr_t)grads[l - l0] & 15)) vec = false;
           }
           in_bytes += gb;
           const int it0 = s->layers[g0].item_off;

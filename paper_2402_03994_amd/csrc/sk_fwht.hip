@@ -95,7 +95,29 @@ void launch_fill_zero(float *p, int64_t n, hipStream_t st) {
 // kernel applies H_L to each destination row, the tail kernel H_R, G and the
 // sum over layers.  For D < L the row is folded once more to D columns.
 // ===========================================================================
-template <int BT, bool BF16, bool VEC>
+// Up to CPT consecutive input elements starting at element e (missing -> 0).
+template <int CPT, bool BF16, bool VEC>
+__device__ __forceinline__ void load_cols(const void *x, int64_t e, int64_t lim, float v[CPT]) {
+  if (CPT == 8 && BF16 && VEC && lim >= 8) {
+    const uint4 u = *(const uint4 *)((const uint16_t *)x + e);
+    v[0] = __uint_as_float(u.x << 16);
+    v[1] = __uint_as_float(u.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(u.y << 16);
+    v[3] = __uint_as_float(u.y & 0xFFFF0000u);
+    v[4] = __uint_as_float(u.z << 16);
+    v[5] = __uint_as_float(u.z & 0xFFFF0000u);
+    v[6] = __uint_as_float(u.w << 16);
+    v[7] = __uint_as_float(u.w & 0xFFFF0000u);
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < CPT; q += 4) load4<BF16, VEC>(x, e + q, lim - q, v + q);
+}
+
+// Fold kernel.  Each thread owns CPT consecutive columns of a row; when a row
+// needs fewer than 256 threads, NGR = 256 / (L / CPT) row groups take
+// interleaved rows and their sums are combined in LDS in group order.
+template <int BT, int CPT, bool BF16, bool VEC>
 __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ items,
                                                    const LayerDesc *__restrict__ layers,
                                                    const uint16_t *__restrict__ ptab, PtrPack ptrs, int first_layer,
@@ -107,16 +129,19 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
   const int64_t n = ld.n;
   const int L = ld.L;
   const int tid = threadIdx.x;
-  const int col0 = tid * 4;
-  const bool active = col0 < L;
+  const int tpr = L / CPT < 1 ? 1 : L / CPT;  // threads per row
+  const int ngr = 256 / tpr;                  // row groups
+  const int grp = tid / tpr;
+  const int col0 = (tid - grp * tpr) * CPT;
+  const bool active = grp < ngr && col0 < L;
   const int bt0 = blockIdx.y * BT;
   const void *xp = ptrs.p[it.layer - first_layer];
   const int nb = (int)((batch - b_begin - bt0) < BT ? (batch - b_begin - bt0) : BT);  // rows of this tile
-  float acc[BT][4];
+  float acc[BT][CPT];
 #pragma unroll
   for (int b = 0; b < BT; ++b)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[b][q] = 0.0f;
+    for (int q = 0; q < CPT; ++q) acc[b][q] = 0.0f;
 
   const int nk = R > 1 ? ld.dk1 / R : 1;
   const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
@@ -133,51 +158,51 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
       }
       return (h < ld.rows_live && h * L + col0 < n) ? h : -1;
     };
-    // two rows per iteration: twice the loads in flight
-    for (int t = it.t0; t < it.t1; t += 2) {
-      const int64_t ha = row_of(t);
-      const int64_t hb = (t + 1 < it.t1) ? row_of(t + 1) : -1;
-      float va[BT][4], vb[BT][4];
-      const int64_t ja = ha * L + col0, jb = hb * L + col0;
-      if (ha >= 0) {
+    // U rows per iteration (U * CPT = 8 elements of each vector per thread in flight)
+    constexpr int U = CPT >= 8 ? 1 : 8 / CPT;
+    for (int t = it.t0 + grp; t < it.t1; t += U * ngr) {
+      int64_t hs[U], js[U];
+      float v[U][BT][CPT];
 #pragma unroll
-        for (int b = 0; b < BT; ++b)
-          if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + ja, n - ja, va[b]);
+      for (int u = 0; u < U; ++u) {
+        hs[u] = (t + u * ngr < it.t1) ? row_of(t + u * ngr) : -1;
+        js[u] = hs[u] * L + col0;
+        if (hs[u] >= 0) {
+#pragma unroll
+          for (int b = 0; b < BT; ++b)
+            if (b < nb) load_cols<CPT, BF16, VEC>(xp, (b_begin + bt0 + b) * n + js[u], n - js[u], v[u][b]);
+        }
       }
-      if (hb >= 0) {
 #pragma unroll
-        for (int b = 0; b < BT; ++b)
-          if (b < nb) load4<BF16, VEC>(xp, (b_begin + bt0 + b) * n + jb, n - jb, vb[b]);
+      for (int u = 0; u < U; ++u) {
+        if (hs[u] >= 0) {
+          const uint32_t bits = sign_word((uint64_t)js[u], (uint32_t)ld.layer_id, key) >> (js[u] & 31);
+#pragma unroll
+          for (int b = 0; b < BT; ++b)
+            if (b < nb) {
+#pragma unroll
+              for (int q = 0; q < CPT; ++q) acc[b][q] += flip(v[u][b][q], (bits >> q) & 1u);
+            }
+        }
       }
-      if (ha >= 0) {
-        const uint32_t bits = sign_word((uint64_t)ja, (uint32_t)ld.layer_id, key) >> (ja & 31);
-#pragma unroll
-        for (int b = 0; b < BT; ++b)
-          if (b < nb) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) acc[b][q] += flip(va[b][q], (bits >> q) & 1u);
-          }
-      }
-      if (hb >= 0) {
-        const uint32_t bits = sign_word((uint64_t)jb, (uint32_t)ld.layer_id, key) >> (jb & 31);
-#pragma unroll
-        for (int b = 0; b < BT; ++b)
-          if (b < nb) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) acc[b][q] += flip(vb[b][q], (bits >> q) & 1u);
-          }
-      }
-    }
-    // route the columns through pi1 of the last digit
-    const uint16_t *fwd_k = ptab + ld.poff[0][0][ld.K - 1];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int pc = fwd_k[col0 + q];
-#pragma unroll
-      for (int b = 0; b < BT; ++b) s[b][pc] = acc[b][q];
     }
   }
-  __syncthreads();
+  // route the columns through pi1 of the last digit; row groups add in order
+  const uint16_t *fwd_k = ptab + ld.poff[0][0][ld.K - 1];
+  int pc[CPT];
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) pc[q] = fwd_k[col0 + q];
+  }
+  for (int gi = 0; gi < ngr; ++gi) {
+    if (active && grp == gi) {
+#pragma unroll
+      for (int q = 0; q < CPT; ++q)
+#pragma unroll
+        for (int b = 0; b < BT; ++b) s[b][pc[q]] = gi == 0 ? acc[b][q] : s[b][pc[q]] + acc[b][q];
+    }
+    __syncthreads();
+  }
   int lgw;
   if (Lw < L) {
     // fold the permuted row to Lw = D columns
@@ -215,13 +240,13 @@ void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, 
   if (nitems <= 0) return;
   const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
   dim3 grid((unsigned)nitems, (unsigned)((rows + BT - 1) / BT));
-#define SK_FOLD(BF, VE)                                                                                              \
-  hipLaunchKernelGGL((k_afjl_fold<BT, BF, VE>), grid, dim3(256), 0, st, s->d_items, s->d_layers, s->d_ptab, ptrs,   \
-                     first_layer, batch, b_begin, bc, item_begin, s->R, s->Lw, part, s->key)
+#define SK_FOLD(CPT, BF, VE)                                                                                       \
+  hipLaunchKernelGGL((k_afjl_fold<BT, CPT, BF, VE>), grid, dim3(256), 0, st, s->d_items, s->d_layers, s->d_ptab,   \
+                     ptrs, first_layer, batch, b_begin, bc, item_begin, s->R, s->Lw, part, s->key)
   if (dtype == SK_BF16) {
-    if (vec) SK_FOLD(true, true); else SK_FOLD(true, false);
+    if (vec) SK_FOLD(8, true, true); else SK_FOLD(4, true, false);
   } else {
-    if (vec) SK_FOLD(false, true); else SK_FOLD(false, false);
+    if (vec) SK_FOLD(4, false, true); else SK_FOLD(4, false, false);
   }
 #undef SK_FOLD
   SK_CHECK_LAUNCH();
@@ -333,8 +358,70 @@ __global__ __launch_bounds__(256) void k_afjl_tail_reg(const LayerDesc *__restri
   for (int r = 0; r < R; ++r) o[(int64_t)r * Lw] = acc[r] * sc;
 }
 
+// Tail for R = 1024 (D = 2^20): H_1024 = H_32 (x) H_32.  A workgroup owns 8
+// columns of one vector; each thread first transforms 32 rows r = 32 rh + j
+// (bits 0-4 of r) in registers, then, after one LDS exchange, 32 rows
+// r = 32 j + rl (bits 5-9), which it keeps as accumulators across layers.
+__global__ __launch_bounds__(256) void k_afjl_tail_1024(const LayerDesc *__restrict__ layers,
+                                                        const int2 *__restrict__ rslot, const float *__restrict__ part,
+                                                        const float *__restrict__ gtab, int l_begin, int l_end,
+                                                        int item_begin, int Lw, int64_t D, int64_t bc, int64_t b_begin,
+                                                        int64_t batch, float *__restrict__ out, int accumulate) {
+  __shared__ float s[1024 * 8];
+  const int c = threadIdx.x & 7, hi = threadIdx.x >> 3;  // hi: rh (phase 1) or rl (phase 2)
+  const int c0 = blockIdx.x * 8;
+  const int64_t bl = blockIdx.y;
+  if (b_begin + bl >= batch) return;
+  float acc[32];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) acc[j] = 0.0f;
+  for (int l = l_begin; l < l_end; ++l) {
+    const int2 *rs = rslot + layers[l].rslot_off;
+    float v[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const int2 q = rs[hi * 32 + j];
+      const int64_t slot = q.y > 0 ? q.x - item_begin : 0;
+      const float x = part[(slot * bc + bl) * Lw + c0 + c];
+      v[j] = q.y > 0 ? x : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const int2 q = rs[hi * 32 + j];
+      for (int k = 1; k < q.y; ++k) v[j] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * Lw + c0 + c];
+    }
+    fwht_regs_t<32>(v);
+#pragma unroll
+    for (int j = 0; j < 32; ++j) s[(hi * 32 + j) * 8 + c] = v[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = s[(j * 32 + hi) * 8 + c];
+    __syncthreads();
+    fwht_regs_t<32>(v);
+    const float *g = gtab + (int64_t)l * D + c0 + c;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) acc[j] += g[(int64_t)(j * 32 + hi) * Lw] * v[j];
+  }
+  const float sc = 1.0f / 32.0f;
+  float *o = out + (b_begin + bl) * D + c0 + c;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    const int64_t r = j * 32 + hi;
+    const float val = acc[j] * sc;
+    o[r * Lw] = accumulate ? o[r * Lw] + val : val;
+  }
+}
+
 void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
                       int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st) {
+  if (s->R == 1024 && s->Lw == 1024) {
+    const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
+    dim3 grid((unsigned)(s->Lw / 8), (unsigned)rows);
+    hipLaunchKernelGGL(k_afjl_tail_1024, grid, dim3(256), 0, st, s->d_layers, s->d_rslot, part, s->d_gtab, l_begin,
+                       l_end, item_begin, s->Lw, s->D, bc, b_begin, batch, out, (int)accumulate);
+    SK_CHECK_LAUNCH();
+    return;
+  }
   const int R = s->R, Lw = s->Lw;
   if (R <= 64) {
     // balance the layer loop: groups of about equal live destination rows
