@@ -86,85 +86,136 @@ union Pack8 {
   bf16x8 v;
 };
 
+constexpr int kQkMR = 4;                  // 16-row tiles per wave
+constexpr int kQkRows = 4 * kQkMR * 16;   // stacked rows per workgroup (4 waves)
+constexpr int kQkBRow = 128 * 2 + 16;     // bytes of one B row chunk in LDS (padded)
+
 template <int NT>
 __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, const uint16_t *__restrict__ B,
                                                const uint16_t *__restrict__ Blo, int64_t m, int64_t n,
                                                int64_t b_begin, int64_t rows, float *__restrict__ tt) {
+  constexpr int DB = NT * 16;
+  __shared__ __align__(16) unsigned char bs[2 * DB * kQkBRow];  // [hi|lo][row][128 bf16 + pad]
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t r0 = (int64_t)blockIdx.x * 64 + wave * 16;  // first stacked row of this wave
   const int li = lane & 15, g = lane >> 4;
-  const int64_t row = r0 + li;
-  const bool rv = row < rows;
-  const uint16_t *xr = x + (b_begin * m + (rv ? row : 0)) * n + g * 32;
-  const uint16_t *br = B + (int64_t)li * n + g * 32;
-  const uint16_t *brl = Blo + (int64_t)li * n + g * 32;
-  floatx4 acc[NT];
+  const int64_t r0 = (int64_t)blockIdx.x * kQkRows + wave * (kQkMR * 16);
+  const uint16_t *xr[kQkMR];
+  bool rv[kQkMR];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int mr = 0; mr < kQkMR; ++mr) {
+    const int64_t row = r0 + mr * 16 + li;
+    rv[mr] = row < rows;
+    xr[mr] = x + (b_begin * m + (rv[mr] ? row : 0)) * n + g * 32;
+  }
+  floatx4 acc[kQkMR][NT];
+#pragma unroll
+  for (int mr = 0; mr < kQkMR; ++mr)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[mr][t] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int64_t k0 = 0; k0 < n; k0 += 128) {
-    Pack8 a[4];
+    // this wave's X fragments: 64 contiguous bytes of each of its rows
+    Pack8 a[kQkMR][4];
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) a[cc].u = rv ? *(const uint4 *)(xr + k0 + cc * 8) : make_uint4(0, 0, 0, 0);
+    for (int mr = 0; mr < kQkMR; ++mr)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc)
+        a[mr][cc].u = rv[mr] ? *(const uint4 *)(xr[mr] + k0 + cc * 8) : make_uint4(0, 0, 0, 0);
+    __syncthreads();  // previous chunk of B consumed
+    // B[hi|lo][row][k0 .. k0+127] -> LDS, 16 bytes per thread per step
+    for (int e = threadIdx.x; e < 2 * DB * 16; e += 256) {
+      const int arr = e / (DB * 16), rem = e - arr * (DB * 16);
+      const int row = rem >> 4, c16 = rem & 15;
+      const uint16_t *src = (arr ? Blo : B) + (int64_t)row * n + k0 + c16 * 8;
+      *(uint4 *)(bs + (arr * DB + row) * kQkBRow + c16 * 16) = *(const uint4 *)src;
+    }
+    __syncthreads();
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      Pack8 b[4], bl[4];
+      const unsigned char *bh = bs + (t * 16 + li) * kQkBRow + g * 64;
+      const unsigned char *bl = bh + DB * kQkBRow;
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc) {
-        b[cc].u = *(const uint4 *)(br + (int64_t)t * 16 * n + k0 + cc * 8);
-        bl[cc].u = *(const uint4 *)(brl + (int64_t)t * 16 * n + k0 + cc * 8);
-      }
+        Pack8 vh, vl;
+        vh.u = *(const uint4 *)(bh + cc * 16);
+        vl.u = *(const uint4 *)(bl + cc * 16);
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cc].v, b[cc].v, acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cc].v, bl[cc].v, acc[t], 0, 0, 0);
+        for (int mr = 0; mr < kQkMR; ++mr) {
+          acc[mr][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mr][cc].v, vh.v, acc[mr][t], 0, 0, 0);
+          acc[mr][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mr][cc].v, vl.v, acc[mr][t], 0, 0, 0);
+        }
       }
     }
   }
   // D layout: lane holds rows 4 g .. 4 g + 3 of column li of each 16 x 16 tile
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t R = r0 + g * 4 + i;
-    if (R >= rows) continue;
-    const int64_t v = R / m, ii = R - (R / m) * m;
+  for (int mr = 0; mr < kQkMR; ++mr)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) tt[(v * (NT * 16) + t * 16 + li) * m + ii] = acc[t][i];
-  }
+    for (int i = 0; i < 4; ++i) {
+      const int64_t R = r0 + mr * 16 + g * 4 + i;
+      if (R >= rows) continue;
+      const int64_t v = R / m, ii = R - (R / m) * m;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) tt[(v * DB + t * 16 + li) * m + ii] = acc[mr][t][i];
+    }
 }
 
-// one wave per (vector, 16 x 16 output tile); K = m in steps of 16
-__global__ __launch_bounds__(64) void k_qk_s2(const float *__restrict__ A, const float *__restrict__ tt, int64_t m,
-                                              int da, int db, int64_t D, int64_t col, int64_t b_begin,
-                                              float *__restrict__ out, int accumulate) {
-  const int lane = threadIdx.x;
+// One workgroup (4 waves) per (vector, 16 x 16 output tile); the waves split
+// K = m into four ranges, each with four independent accumulators, and the
+// sixteen partial tiles are added in a fixed order through LDS.
+__global__ __launch_bounds__(256) void k_qk_s2(const float *__restrict__ A, const float *__restrict__ tt, int64_t m,
+                                               int da, int db, int64_t D, int64_t col, int64_t b_begin,
+                                               float *__restrict__ out, int accumulate) {
+  __shared__ float red[4][64][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntb = db / 16;
   const int ta = blockIdx.x / ntb, tb = blockIdx.x - (blockIdx.x / ntb) * ntb;
   const int64_t v = blockIdx.y;
   const int li = lane & 15, g = lane >> 4;
   const float *ar = A + (int64_t)(ta * 16 + li) * m + g * 4;
   const float *tr = tt + (v * db + tb * 16 + li) * m + g * 4;
-  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-  int64_t k0 = 0;
-  for (; k0 + 16 <= m; k0 += 16) {
-    const float4 av = *(const float4 *)(ar + k0);
-    const float4 tv = *(const float4 *)(tr + k0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, tv.x, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, tv.y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, tv.z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, tv.w, acc, 0, 0, 0);
-  }
-  for (int e = 0; e < 4; ++e) {  // ragged tail of K (m % 16 != 0)
-    const int64_t k = k0 + g * 4 + e;
-    const bool ok = k < m;
-    const float av = ok ? ar[k0 + e] : 0.0f;
-    const float tv = ok ? tr[k0 + e] : 0.0f;
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, tv, acc, 0, 0, 0);
-  }
+  const int64_t per = ((m + 63) / 64) * 16;  // K range per wave, a multiple of 16
+  const int64_t kb = wave * per, ke = kb + per < m ? kb + per : m;
+  floatx4 acc[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int a = ta * 16 + g * 4 + i, c = tb * 16 + li;
-    float *o = out + (b_begin + v) * D + col + (int64_t)a * db + c;
-    *o = accumulate ? *o + acc[i] : acc[i];
+  for (int u = 0; u < 4; ++u) acc[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+  int64_t k0 = kb;
+  for (; k0 + 64 <= ke; k0 += 64) {
+    float4 av[4], tv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      av[u] = *(const float4 *)(ar + k0 + 16 * u);
+      tv[u] = *(const float4 *)(tr + k0 + 16 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].x, tv[u].x, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].y, tv[u].y, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].z, tv[u].z, acc[u], 0, 0, 0);
+      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].w, tv[u].w, acc[u], 0, 0, 0);
+    }
+  }
+  for (; k0 < ke; k0 += 16) {  // remaining 16-wide steps, ragged at m
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = k0 + g * 4 + e < ke;
+      const float a = ok ? ar[k0 + e] : 0.0f;
+      const float t = ok ? tr[k0 + e] : 0.0f;
+      acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, t, acc[0], 0, 0, 0);
+    }
+  }
+  const floatx4 sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[wave][lane][i] = sum[i];
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float y = ((red[0][lane][i] + red[1][lane][i]) + red[2][lane][i]) + red[3][lane][i];
+      const int a = ta * 16 + g * 4 + i, c = tb * 16 + li;
+      float *o = out + (b_begin + v) * D + col + (int64_t)a * db + c;
+      *o = accumulate ? *o + y : y;
+    }
   }
 }
 
@@ -193,7 +244,7 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
   const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
   if (qk_mfma_ok(ld, dtype)) {
     const int64_t rows = bc * (int64_t)ld.m;
-    dim3 g1((unsigned)((rows + 63) / 64));
+    dim3 g1((unsigned)((rows + kQkRows - 1) / kQkRows));
 #define SK_S1(NT)                                                                                              \
   case NT:                                                                                                     \
     hipLaunchKernelGGL(k_qk_s1<NT>, g1, dim3(256), 0, st, (const uint16_t *)x, B, Blo, (int64_t)ld.m,           \
@@ -206,7 +257,7 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
     }
 #undef SK_S1
     dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
-    hipLaunchKernelGGL(k_qk_s2, g2, dim3(64), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin,
+    hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin,
                        out, (int)accumulate);
     (void)hipGetLastError();
     return;
