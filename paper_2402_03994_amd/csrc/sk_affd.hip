@@ -49,44 +49,55 @@ __device__ __forceinline__ int64_t dst_row(const LayerDesc &ld, const uint16_t *
 }  // namespace
 
 // ---- phase A -------------------------------------------------------------
-constexpr int kAffdVB = 4;  // vectors per workgroup in phase A
+constexpr int kAffdVB = 8;  // vectors per workgroup in phase A
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_affd_rows(const LayerDesc *__restrict__ layers,
                                                    const uint16_t *__restrict__ ptab, int layer,
                                                    const void *__restrict__ x, int64_t b_begin, int64_t bc,
                                                    float *__restrict__ w, Key key) {
-  __shared__ float s[kAffdVB][1024];
+  __shared__ __align__(16) float s[kAffdVB * 1024];
   const LayerDesc &ld = layers[layer];
   const int64_t h = blockIdx.x;
-  const int L = ld.L;
-  const int col0 = threadIdx.x * 4;
-  const int64_t j0 = h * L + col0;
+  const int col0 = threadIdx.x * 4;  // L == 1024 on this path
+  const int64_t j0 = h * 1024 + col0;
   const int64_t lim = ld.n - j0;
   const int64_t v0 = (int64_t)blockIdx.y * kAffdVB;
   const int nv = (int)((bc - v0) < kAffdVB ? (bc - v0) : kAffdVB);
   uint32_t bits = 0;
   if (lim > 0) bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
   const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
-  if (col0 < L) {
-    int pc[4];
+  int pc[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) pc[q] = fk[col0 + q];
+  for (int q = 0; q < 4; ++q) pc[q] = fk[col0 + q];
+  // load, sign, scatter the columns through pi1 of the last digit
 #pragma unroll
-    for (int v = 0; v < kAffdVB; ++v) {
-      float val[4] = {0.f, 0.f, 0.f, 0.f};
-      if (v < nv && lim > 0) load4<BF16, false>(x, (b_begin + v0 + v) * ld.n + j0, lim, val);
+  for (int v = 0; v < kAffdVB; ++v) {
+    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    if (v < nv && lim > 0) load4<BF16, false>(x, (b_begin + v0 + v) * ld.n + j0, lim, val);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[v][pc[q]] = flip(val[q], (bits >> q) & 1u);
-    }
+    for (int q = 0; q < 4; ++q) s[v * 1024 + pc[q]] = flip(val[q], (bits >> q) & 1u);
   }
-  const int lgL = ld.lgL;
-  for (int v = 0; v < nv; ++v) lds_fwht(&s[v][0], lgL, 0);
-  const float sc = rsqrtf((float)L);
+  __syncthreads();
+  float r[kAffdVB][4];
+#pragma unroll
+  for (int v = 0; v < kAffdVB; ++v) {
+    const float4 t = *(const float4 *)(s + v * 1024 + col0);
+    r[v][0] = t.x;
+    r[v][1] = t.y;
+    r[v][2] = t.z;
+    r[v][3] = t.w;
+  }
+  fwht1024_rows<kAffdVB>(r, s);
+  const float sc = 1.0f / 32.0f;  // 1024^{-1/2}
   const int64_t drow = dst_row(ld, ptab, h);
-  for (int e = threadIdx.x; e < nv * L; e += 256) {
-    const int v = e >> lgL, c = e & (L - 1);
-    w[(v0 + v) * ld.np + drow * L + c] = s[v][c] * sc;
+#pragma unroll
+  for (int v = 0; v < kAffdVB; ++v) {
+    if (v < nv) {
+      float *dst = w + (v0 + v) * ld.np + drow * 1024 + threadIdx.x;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) dst[256 * k] = r[v][k] * sc;
+    }
   }
 }
 
@@ -160,63 +171,135 @@ __global__ __launch_bounds__(256) void k_affd_cols(const LayerDesc *__restrict__
 }
 
 // ---- phase C -------------------------------------------------------------
-constexpr int kAffdCV = 16;  // vectors per workgroup in phase C
+// Live-slab mask and fold signs (-1)^{<h*, t>} of the top index t.
+__device__ __forceinline__ void top_masks(const LayerDesc &ld, const uint16_t *ptab, int tt, uint64_t &live,
+                                          uint64_t &sgn) {
+  live = 0;
+  sgn = 0;
+  for (int t = 0; t < tt; ++t) {
+    if (src_slab(ld, ptab, t) * ld.dk1 < ld.rows_live) live |= 1ull << t;
+    sgn |= (uint64_t)(__popc((uint32_t)t & ld.hstar) & 1u) << t;
+  }
+}
 
-template <int TT>
+// TT <= 16: thread owns 4 consecutive columns (one Philox block per 4
+// Gaussians); F rows of CV vectors are transformed by fwht1024_rows.
+template <int TT, int CV>
 __global__ __launch_bounds__(256) void k_affd_top(const LayerDesc *__restrict__ layers,
                                                   const uint16_t *__restrict__ ptab, int layer,
-                                                  const float *__restrict__ w, int64_t bc,
-                                                  float *__restrict__ f, Key key) {
-  __shared__ float fs[kAffdCV][1024];
+                                                  const float *__restrict__ w, int64_t bc, float *__restrict__ f,
+                                                  Key key) {
+  __shared__ __align__(16) float lds[CV * 1024];
   const LayerDesc &ld = layers[layer];
-  const int L = ld.L;
-  const int64_t lo_len = (int64_t)ld.dk1 * L;
+  const int64_t lo_len = (int64_t)ld.dk1 * 1024;
   const int64_t p = blockIdx.x;
-  const int64_t v0 = (int64_t)blockIdx.y * kAffdCV;
-  const int nv = (int)((bc - v0) < kAffdCV ? (bc - v0) : kAffdCV);
-  // live slabs and the fold signs
-  uint32_t live_mask_lo = 0, live_mask_hi = 0, sgn_lo = 0, sgn_hi = 0;
-  for (int t = 0; t < TT; ++t) {
-    const bool live = src_slab(ld, ptab, t) * ld.dk1 < ld.rows_live;
-    const uint32_t sg = __popc((uint32_t)t & ld.hstar) & 1u;
-    if (t < 32) {
-      live_mask_lo |= (uint32_t)live << t;
-      sgn_lo |= sg << t;
-    } else {
-      live_mask_hi |= (uint32_t)live << (t - 32);
-      sgn_hi |= sg << (t - 32);
+  const int64_t v0 = (int64_t)blockIdx.y * CV;
+  const int nv = (int)((bc - v0) < CV ? (bc - v0) : CV);
+  uint64_t live, sgn;
+  top_masks(ld, ptab, TT, live, sgn);
+  const int64_t q = p * 1024 + 4 * threadIdx.x;
+  float g[TT][4];
+#pragma unroll
+  for (int t = 0; t < TT; ++t) gauss4((uint64_t)(t * lo_len + q) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g[t]);
+#pragma unroll 1
+  for (int v = 0; v < CV; ++v) {
+    float x[4][TT];
+    const float *wv = w + (v0 + (v < nv ? v : 0)) * ld.np + q;
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (v < nv && ((live >> t) & 1ull)) val = *(const float4 *)(wv + (int64_t)t * lo_len);
+      x[0][t] = val.x;
+      x[1][t] = val.y;
+      x[2][t] = val.z;
+      x[3][t] = val.w;
     }
-  }
-  const float sc = 1.0f / (float)TT;
-  for (int cq = 0; cq < L; cq += 256) {
-    const int l = cq + threadIdx.x;
-    const int64_t q = p * L + l;
-    float g[TT];
+    float o[4];
 #pragma unroll
-    for (int t = 0; t < TT; ++t) g[t] = gauss((uint64_t)(t * lo_len + q), (uint32_t)ld.layer_id, ST_GAUSS, key);
-    for (int v = 0; v < nv; ++v) {
-      const float *wv = w + (v0 + v) * ld.np + q;
-      float x[TT];
-#pragma unroll
-      for (int t = 0; t < TT; ++t) {
-        const bool live = t < 32 ? (live_mask_lo >> t) & 1u : (live_mask_hi >> (t - 32)) & 1u;
-        x[t] = live ? wv[(int64_t)t * lo_len] : 0.0f;
-      }
-      fwht_regs_t<TT>(x);
+    for (int c = 0; c < 4; ++c) {
+      fwht_regs_t<TT>(x[c]);
       float acc = 0.0f;
 #pragma unroll
-      for (int t = 0; t < TT; ++t) {
-        const uint32_t sg = t < 32 ? (sgn_lo >> t) & 1u : (sgn_hi >> (t - 32)) & 1u;
-        acc += flip(g[t] * x[t], sg);
-      }
-      fs[v][l] = acc * sc;
+      for (int t = 0; t < TT; ++t) acc += flip(g[t][c] * x[c][t], (uint32_t)(sgn >> t) & 1u);
+      o[c] = acc;
+    }
+    *(float4 *)(lds + v * 1024 + 4 * threadIdx.x) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+  float F[CV][4];
+#pragma unroll
+  for (int v = 0; v < CV; ++v) {
+    const float4 t4 = *(const float4 *)(lds + v * 1024 + 4 * threadIdx.x);
+    F[v][0] = t4.x;
+    F[v][1] = t4.y;
+    F[v][2] = t4.z;
+    F[v][3] = t4.w;
+  }
+  fwht1024_rows<CV>(F, lds);
+  const float sc = 1.0f / (32.0f * (float)TT);  // H_TT twice (1/TT) and H_L (1024^{-1/2})
+#pragma unroll
+  for (int v = 0; v < CV; ++v) {
+    if (v < nv) {
+      float *dst = f + (v0 + v) * lo_len + p * 1024 + threadIdx.x;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) dst[256 * k] = F[v][k] * sc;
     }
   }
-  for (int v = 0; v < nv; ++v) lds_fwht(&fs[v][0], ld.lgL, 0);
-  const float scl = rsqrtf((float)L);
-  for (int e = threadIdx.x; e < nv * L; e += 256) {
-    const int v = e / L, l = e - (e / L) * L;
-    f[(v0 + v) * lo_len + p * L + l] = fs[v][l] * scl;
+}
+
+// TT in {32, 64}: thread owns one column per pass (TT Gaussians in registers).
+template <int TT, int CV>
+__global__ __launch_bounds__(256) void k_affd_top_wide(const LayerDesc *__restrict__ layers,
+                                                       const uint16_t *__restrict__ ptab, int layer,
+                                                       const float *__restrict__ w, int64_t bc,
+                                                       float *__restrict__ f, Key key) {
+  __shared__ __align__(16) float lds[CV * 1024];
+  const LayerDesc &ld = layers[layer];
+  const int64_t lo_len = (int64_t)ld.dk1 * 1024;
+  const int64_t p = blockIdx.x;
+  const int64_t v0 = (int64_t)blockIdx.y * CV;
+  const int nv = (int)((bc - v0) < CV ? (bc - v0) : CV);
+  uint64_t live, sgn;
+  top_masks(ld, ptab, TT, live, sgn);
+  for (int cq = 0; cq < 1024; cq += 256) {
+    const int l = cq + threadIdx.x;
+    const int64_t q = p * 1024 + l;
+    float g[TT];
+#pragma clang loop unroll(full)
+    for (int t = 0; t < TT; ++t) g[t] = gauss((uint64_t)(t * lo_len + q), (uint32_t)ld.layer_id, ST_GAUSS, key);
+#pragma unroll 1
+    for (int v = 0; v < CV; ++v) {
+      float acc = 0.0f;
+      if (v < nv) {
+        const float *wv = w + (v0 + v) * ld.np + q;
+        float x[TT];
+#pragma unroll
+        for (int t = 0; t < TT; ++t) x[t] = ((live >> t) & 1ull) ? wv[(int64_t)t * lo_len] : 0.0f;
+        fwht_regs_t<TT>(x);
+#pragma unroll
+        for (int t = 0; t < TT; ++t) acc += flip(g[t] * x[t], (uint32_t)(sgn >> t) & 1u);
+      }
+      lds[v * 1024 + l] = acc;
+    }
+  }
+  __syncthreads();
+  float F[CV][4];
+#pragma unroll
+  for (int v = 0; v < CV; ++v) {
+    const float4 t = *(const float4 *)(lds + v * 1024 + 4 * threadIdx.x);
+    F[v][0] = t.x;
+    F[v][1] = t.y;
+    F[v][2] = t.z;
+    F[v][3] = t.w;
+  }
+  fwht1024_rows<CV>(F, lds);
+  const float sc = 1.0f / (32.0f * (float)TT);
+#pragma unroll
+  for (int v = 0; v < CV; ++v) {
+    if (v < nv) {
+      float *dst = f + (v0 + v) * lo_len + p * 1024 + threadIdx.x;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) dst[256 * k] = F[v][k] * sc;
+    }
   }
 }
 
@@ -265,8 +348,12 @@ int64_t affd_tile_bytes() {
   return (mb < 1 ? 1 : mb) << 20;
 }
 
-void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin, int64_t bc,
                    float *out, bool accumulate, hipStream_t st) {
+  if (affd_transposed_path(s, layer)) {
+    run_affd_transposed(s, layer, x, dtype, vec, b_begin, bc, out, accumulate, st);
+    return;
+  }
   const LayerDesc &ld = s->layers[layer];
   const int64_t lo_len = (int64_t)ld.dk1 * ld.L;
   float *w = s->ws;
@@ -307,16 +394,22 @@ void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, int6
   cols(0, w, ld.np, TT);
   // C
   {
-    dim3 grid((unsigned)ld.dk1, (unsigned)((bc + kAffdCV - 1) / kAffdCV));
-#define SK_TOP(T)                                                                                             \
-  case T:                                                                                                     \
-    hipLaunchKernelGGL((k_affd_top<T>), grid, dim3(256), 0, st, s->d_layers, s->d_ptab, layer, w, bc, f, s->key); \
+#define SK_TOP(T, CV)                                                                                        \
+  case T:                                                                                                    \
+    hipLaunchKernelGGL((k_affd_top<T, CV>), dim3((unsigned)ld.dk1, (unsigned)((bc + CV - 1) / CV)), dim3(256), 0, \
+                       st, s->d_layers, s->d_ptab, layer, w, bc, f, s->key);                                 \
+    break;
+#define SK_TOPW(T, CV)                                                                                       \
+  case T:                                                                                                    \
+    hipLaunchKernelGGL((k_affd_top_wide<T, CV>), dim3((unsigned)ld.dk1, (unsigned)((bc + CV - 1) / CV)),     \
+                       dim3(256), 0, st, s->d_layers, s->d_ptab, layer, w, bc, f, s->key);                   \
     break;
     switch (TT) {
-      SK_TOP(1) SK_TOP(2) SK_TOP(4) SK_TOP(8) SK_TOP(16) SK_TOP(32) SK_TOP(64)
+      SK_TOP(1, 16) SK_TOP(2, 16) SK_TOP(4, 16) SK_TOP(8, 16) SK_TOP(16, 16) SK_TOPW(32, 16) SK_TOPW(64, 8)
       default: break;
     }
 #undef SK_TOP
+#undef SK_TOPW
   }
   // D
   cols(1, f, lo_len, 1);

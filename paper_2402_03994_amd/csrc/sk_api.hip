@@ -497,10 +497,11 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
             const int64_t live = affd_live_bytes_per_vector(s, l);
             int64_t tile = std::max<int64_t>(1, affd_tile_bytes() / std::max<int64_t>(live, 1));
             tile = std::min(tile, std::max<int64_t>(1, s->ws_bytes / affd_fast_bytes_per_vector(s, l)));
+            const bool vec = !(ld.n & 3) && !((uintptr_t)grads[l - l0] & 15);
             for (int64_t t0 = b0; t0 < b0 + bc; t0 += tile) {
               const int64_t tb = std::min(tile, b0 + bc - t0);
               SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz + (l == l1 - 1 ? tb * s->D * 4 : 0),
-                      run_affd_fast(s, l, grads[l - l0], dtype, t0, tb, out, accumulate || l > l0, st));
+                      run_affd_fast(s, l, grads[l - l0], dtype, vec, t0, tb, out, accumulate || l > l0, st));
             }
             continue;
           }

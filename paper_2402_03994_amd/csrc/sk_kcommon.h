@@ -70,19 +70,154 @@ __device__ __forceinline__ void lds_fwht(float *s, int lgrows, int lgcs) {
   __syncthreads();
 }
 
-// Unnormalised Walsh-Hadamard transform of N values held in registers.
+// Unnormalised Walsh-Hadamard transform of N values held in registers (the
+// stages are expanded at compile time so every index is static).
+template <int N, int H>
+struct FwhtStage {
+  static __device__ __forceinline__ void run(float *v) {
+    if constexpr (H < N) {
+#pragma clang loop unroll(full)
+      for (int i = 0; i < N; i += 2 * H)
+#pragma clang loop unroll(full)
+        for (int j = i; j < i + H; ++j) {
+          const float a = v[j], b = v[j + H];
+          v[j] = a + b;
+          v[j + H] = a - b;
+        }
+      FwhtStage<N, 2 * H>::run(v);
+    }
+  }
+};
+
 template <int N>
 __device__ __forceinline__ void fwht_regs_t(float *v) {
+  FwhtStage<N, 1>::run(v);
+}
+
+// 1024-point unnormalised Walsh-Hadamard transform of NV rows spread over a
+// 256-thread workgroup.  On entry thread t holds columns 4t .. 4t+3 of every
+// row in v[r][0..3]; on exit it holds columns t, t+256, t+512, t+768 in
+// v[r][0..3].  Column bits 0-1 are transformed in the thread, bits 2-7 (lane
+// bits 0-5) by cross-lane exchanges, bits 8-9 (wave index) after one pass
+// through `lds` (NV x 1024 floats).  Ends synchronised.
+template <int NV>
+__device__ __forceinline__ void fwht1024_rows(float (&v)[NV][4], float *lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
 #pragma unroll
-  for (int h = 1; h < N; h <<= 1)
+  for (int r = 0; r < NV; ++r) {
+    const float a0 = v[r][0] + v[r][1], a1 = v[r][0] - v[r][1];
+    const float a2 = v[r][2] + v[r][3], a3 = v[r][2] - v[r][3];
+    v[r][0] = a0 + a2;
+    v[r][1] = a1 + a3;
+    v[r][2] = a0 - a2;
+    v[r][3] = a1 - a3;
+  }
 #pragma unroll
-    for (int i = 0; i < N; i += 2 * h)
+  for (int sbit = 0; sbit < 6; ++sbit) {
+    const int mask = 1 << sbit;
+    const bool upper = (lane & mask) != 0;
 #pragma unroll
-      for (int j = i; j < i + h; ++j) {
-        const float a = v[j], b = v[j + h];
-        v[j] = a + b;
-        v[j + h] = a - b;
+    for (int r = 0; r < NV; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float o = __shfl_xor(v[r][q], mask, 64);
+        v[r][q] = upper ? o - v[r][q] : v[r][q] + o;
       }
+  }
+  __syncthreads();  // lds may still be read by the caller's previous step
+#pragma unroll
+  for (int r = 0; r < NV; ++r)
+    *(float4 *)(lds + r * 1024 + 4 * tid) = make_float4(v[r][0], v[r][1], v[r][2], v[r][3]);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < NV; ++r) {
+    const float b0 = lds[r * 1024 + tid], b1 = lds[r * 1024 + tid + 256];
+    const float b2 = lds[r * 1024 + tid + 512], b3 = lds[r * 1024 + tid + 768];
+    const float a0 = b0 + b1, a1 = b0 - b1, a2 = b2 + b3, a3 = b2 - b3;
+    v[r][0] = a0 + a2;
+    v[r][1] = a1 + a3;
+    v[r][2] = a0 - a2;
+    v[r][3] = a1 - a3;
+  }
+  __syncthreads();
+}
+
+
+// NV (8 or 16) rows of 1024 floats in LDS: one pad word after every E = 4 NV
+// floats and a row stride of 16 (NV = 16) or 32 (NV = 8) banks modulo 32, so
+// that both passes of fwht1024_lds touch 32 distinct banks per half-wave.
+template <int NV>
+struct Lds1024 {
+  static_assert(NV == 8 || NV == 16, "8 or 16 rows");
+  static constexpr int kLgE = NV == 16 ? 6 : 5;
+  static constexpr int kStride = NV == 16 ? 1040 : 1056;
+  static constexpr int kFloats = NV * kStride;
+  static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> kLgE); }
+};
+
+// In-place unnormalised 1024-point Walsh-Hadamard transform of the NV rows of
+// an Lds1024<NV> block; 256 threads; every butterfly runs inside a thread.
+// Thread (row i = tid / C, c = tid % C), C = 256 / NV, E = 1024 / C values:
+// pass 1 holds columns c + C k and transforms column bits log2 C .. 9; pass 2
+// holds the E consecutive columns E c .. E c + E - 1 (G = E / C runs of C)
+// and transforms bits 0 .. log2 C - 1.  The caller synchronises after
+// filling the block; ends synchronised.
+template <int NV>
+__device__ __forceinline__ void fwht1024_lds_pass2(float *lds) {
+  constexpr int C = 256 / NV, E = 1024 / C, G = E / C;
+  using L = Lds1024<NV>;
+  const int i = threadIdx.x / C, c = threadIdx.x % C;
+  // columns E c + m (m < E) sit at (E + 1) c + m
+  float *b = lds + i * L::kStride + (E + 1) * c;
+  float e[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) e[m] = b[m];
+#pragma unroll
+  for (int g = 0; g < G; ++g) fwht_regs_t<C>(e + g * C);
+#pragma unroll
+  for (int m = 0; m < E; ++m) b[m] = e[m];
+  __syncthreads();
+}
+
+// Offset of column c + C k from column c in an Lds1024<NV> row (c < C).
+template <int NV>
+__device__ __forceinline__ constexpr int lds1024_pass1_off(int k) {
+  constexpr int C = 256 / NV;
+  return C * k + ((C * k) >> Lds1024<NV>::kLgE);
+}
+
+template <int NV>
+__device__ __forceinline__ void fwht1024_lds(float *lds) {
+  constexpr int C = 256 / NV, E = 1024 / C;
+  using L = Lds1024<NV>;
+  static_assert(E == (1 << L::kLgE), "pad period");
+  const int i = threadIdx.x / C, c = threadIdx.x % C;
+  float *b = lds + i * L::kStride + c;
+  float e[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) e[k] = b[lds1024_pass1_off<NV>(k)];
+  fwht_regs_t<E>(e);
+#pragma unroll
+  for (int k = 0; k < E; ++k) b[lds1024_pass1_off<NV>(k)] = e[k];
+  __syncthreads();
+  fwht1024_lds_pass2<NV>(lds);
+}
+
+// Same transform with the first pass fed from registers: e[k] holds column
+// c + C k of row i (i = tid / C, c = tid % C), e.g. straight from global
+// memory.  The block needs no synchronisation on entry beyond the caller's
+// own (its previous readers must be done); ends synchronised.
+template <int NV>
+__device__ __forceinline__ void fwht1024_lds_regs(float *lds, float (&e)[1024 * NV / 256]) {
+  constexpr int C = 256 / NV;
+  using L = Lds1024<NV>;
+  const int i = threadIdx.x / C, c = threadIdx.x % C;
+  fwht_regs_t<1024 * NV / 256>(e);
+  float *b = lds + i * L::kStride + c;
+#pragma unroll
+  for (int k = 0; k < 1024 * NV / 256; ++k) b[lds1024_pass1_off<NV>(k)] = e[k];
+  __syncthreads();
+  fwht1024_lds_pass2<NV>(lds);
 }
 
 }  // namespace sk

@@ -27,8 +27,12 @@ bool affd_fast_path(const sk_sketch *s, int layer);
 int64_t affd_fast_bytes_per_vector(const sk_sketch *s, int layer);
 int64_t affd_live_bytes_per_vector(const sk_sketch *s, int layer);
 int64_t affd_tile_bytes();
-void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *out,
-                   bool accumulate, hipStream_t st);
+void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin, int64_t bc,
+                   float *out, bool accumulate, hipStream_t st);
+// AFFD for layers whose second-to-last digit is 1024 wide (slabs stored transposed).
+bool affd_transposed_path(const sk_sketch *s, int layer);
+void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
+                         int64_t bc, float *out, bool accumulate, hipStream_t st);
 void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                         float *w, hipStream_t st);
 void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st);
