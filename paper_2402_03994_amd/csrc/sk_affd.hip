@@ -350,10 +350,6 @@ int64_t affd_tile_bytes() {
 
 void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin, int64_t bc,
                    float *out, bool accumulate, hipStream_t st) {
-  if (affd_transposed_path(s, layer)) {
-    run_affd_transposed(s, layer, x, dtype, vec, b_begin, bc, out, accumulate, st);
-    return;
-  }
   const LayerDesc &ld = s->layers[layer];
   const int64_t lo_len = (int64_t)ld.dk1 * ld.L;
   float *w = s->ws;

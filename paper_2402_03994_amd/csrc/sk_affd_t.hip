@@ -15,6 +15,9 @@
 //      h*, H_p again, keep the rows pi2_p(a), a < R             -> G^T[l][a]
 //   E  H_l along each row a of G, gather pi2_l(b), scale, add  -> out
 // Three passes over the data (read x, write W^T, read W^T) for TT <= 8.
+#include <algorithm>
+#include <cstdlib>
+
 #include "sk_kcommon.h"
 #include "sk_launch.h"
 
@@ -369,6 +372,19 @@ __global__ __launch_bounds__(256) void k_affdT_out(const LayerDesc *__restrict__
 
 constexpr unsigned kRowsGrid = 512;
 
+// Vectors per call for TT <= 8: a multiple of 16 (one Gaussian pass per 16
+// vectors in phase C) whose W^T (live slabs x 4 MB per vector) stays within
+// the 256 MB memory-side cache between phases A and C, so that the W^T round
+// trip rarely reaches HBM.  0 = no preference (TT > 8: W^T is far larger).
+int64_t affd_transposed_tile(const sk_sketch *s, int layer) {
+  const LayerDesc &ld = s->layers[layer];
+  if (!affd_transposed_path(s, layer) || ld.lgnp - 20 > 3) return 0;
+  const char *e = std::getenv("SK_AFFD_MALL_MB");
+  const int64_t budget = (e ? std::atoll(e) : 192) << 20;
+  const int64_t wbytes = ((ld.rows_live + 1023) / 1024) * (4ll << 20);
+  return 16 * std::max<int64_t>(1, budget / (16 * wbytes));
+}
+
 bool affd_transposed_path(const sk_sketch *s, int layer) {
   const LayerDesc &ld = s->layers[layer];
   if (s->D <= 1024 || ld.K < 2 || ld.L != 1024 || ld.dk1 != 1024) return false;
@@ -377,12 +393,11 @@ bool affd_transposed_path(const sk_sketch *s, int layer) {
 }
 
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *out, bool accumulate, hipStream_t st) {
+                         int64_t bc, float *gbuf, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const int R = (int)(s->D / 1024);
   float *w = s->ws;
-  float *gbuf = w + bc * ld.np;
   // A
   {
     // two resident workgroups per CU (64 KB of LDS each); a multiple of 8
@@ -420,8 +435,13 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
 #undef SK_CT
 #undef SK_CTW
   }
-  // E
-  hipLaunchKernelGGL(k_affdT_out, dim3((unsigned)((R + 15) / 16), (unsigned)bc), dim3(256), 0, st, s->d_layers,
+  (void)hipGetLastError();
+}
+
+void run_affd_transposed_out(const sk_sketch *s, int layer, const float *gbuf, int64_t b_begin, int64_t gb,
+                             float *out, bool accumulate, hipStream_t st) {
+  const int R = (int)(s->D / 1024);
+  hipLaunchKernelGGL(k_affdT_out, dim3((unsigned)((R + 15) / 16), (unsigned)gb), dim3(256), 0, st, s->d_layers,
                      s->d_ptab, layer, gbuf, R, s->D, b_begin, out, (int)accumulate);
   (void)hipGetLastError();
 }

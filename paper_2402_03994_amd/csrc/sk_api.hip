@@ -7,6 +7,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "sk_launch.h"
 
@@ -489,20 +490,48 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         (void)in_bytes;
         break;
       }
-      case SK_AFFD:
+      case SK_AFFD: {
+        bool acc_now = accumulate != 0;  // false until the first layer has written out
+        std::vector<int> small;
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
+          if (affd_small_path(s, l)) {
+            small.push_back(l);
+            continue;
+          }
           if (affd_fast_path(s, l)) {
             // batch tile sized so the layer's intermediate stays cache-resident between phases
             const int64_t live = affd_live_bytes_per_vector(s, l);
             int64_t tile = std::max<int64_t>(1, affd_tile_bytes() / std::max<int64_t>(live, 1));
+            if (const int64_t tt = affd_transposed_tile(s, l)) tile = tt;
             tile = std::min(tile, std::max<int64_t>(1, s->ws_bytes / affd_fast_bytes_per_vector(s, l)));
             const bool vec = !(ld.n & 3) && !((uintptr_t)grads[l - l0] & 15);
+            if (affd_transposed_path(s, l)) {
+              // W^T of one tile at the start of the workspace, then G^T of up to
+              // gmax vectors; phase E runs once per gmax vectors
+              const int64_t g4 = s->D * 4;
+              tile = std::min(tile, bc);
+              const int64_t gmax = std::max(tile, (s->ws_bytes - tile * ld.np * 4) / g4 / tile * tile);
+              float *gbuf = s->ws + tile * ld.np;
+              for (int64_t g0 = b0; g0 < b0 + bc; g0 += gmax) {
+                const int64_t gb = std::min(gmax, b0 + bc - g0);
+                for (int64_t t0 = g0; t0 < g0 + gb; t0 += tile) {
+                  const int64_t tb = std::min(tile, g0 + gb - t0);
+                  SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz,
+                          run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gbuf + (t0 - g0) * s->D, st));
+                }
+                SK_PROF(SK_PROF_GATHER, gb * g4 * (l == l1 - 1 ? 2 : 1),
+                        run_affd_transposed_out(s, l, gbuf, g0, gb, out, acc_now, st));
+              }
+              acc_now = true;
+              continue;
+            }
             for (int64_t t0 = b0; t0 < b0 + bc; t0 += tile) {
               const int64_t tb = std::min(tile, b0 + bc - t0);
               SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz + (l == l1 - 1 ? tb * s->D * 4 : 0),
-                      run_affd_fast(s, l, grads[l - l0], dtype, vec, t0, tb, out, accumulate || l > l0, st));
+                      run_affd_fast(s, l, grads[l - l0], dtype, vec, t0, tb, out, acc_now, st));
             }
+            acc_now = true;
             continue;
           }
           float *w = s->ws;
@@ -512,9 +541,33 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
           SK_PROF(SK_PROF_AFFD_FOLD, 0, launch_affd_fold(s, l, w, bc, f, st));
           SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(f, bc, ld.lo_len_lg, st));
           SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
-                  launch_affd_gather(s, l, f, b0, bc, out, accumulate || l > l0, st));
+                  launch_affd_gather(s, l, f, b0, bc, out, acc_now, st));
+          acc_now = true;
+        }
+        if (!small.empty()) {
+          // groups of up to kMaxPtrs small layers; vectors tiled so that W and F
+          // of every slot fit the workspace
+          const int64_t per = affd_small_bytes_per_vector(s);
+          const int64_t vt = std::min<int64_t>(bc, std::max<int64_t>(1, s->ws_bytes / per));
+          const int S = (int)std::min<int64_t>(kMaxPtrs, std::max<int64_t>(1, s->ws_bytes / (vt * per)));
+          for (size_t i0 = 0; i0 < small.size(); i0 += S) {
+            const int ns = (int)std::min<size_t>(S, small.size() - i0);
+            SmallGroup g{};
+            int64_t nsum = 0;
+            for (int j = 0; j < ns; ++j) {
+              g.layer[j] = small[i0 + j];
+              g.x[j] = grads[small[i0 + j] - l0];
+              nsum += s->layers[small[i0 + j]].n;
+            }
+            for (int64_t t0 = b0; t0 < b0 + bc; t0 += vt) {
+              const int64_t tb = std::min(vt, b0 + bc - t0);
+              SK_PROF(SK_PROF_AFFD_FOLD, tb * nsum * esz, run_affd_small(s, g, ns, dtype, t0, tb, out, acc_now, st));
+            }
+            acc_now = true;
+          }
         }
         break;
+      }
       case SK_FJL:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];

@@ -30,9 +30,28 @@ int64_t affd_tile_bytes();
 void run_affd_fast(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin, int64_t bc,
                    float *out, bool accumulate, hipStream_t st);
 // AFFD for layers whose second-to-last digit is 1024 wide (slabs stored transposed).
+// Small layers (N' = D, two digits, at most kSmallRows source rows of 1024):
+// phases of up to kMaxPtrs such layers run as one launch each.
+constexpr int kSmallRows = 8;
+constexpr int kSmallMaxDk1 = 512;
+struct SmallGroup {
+  int32_t layer[kMaxPtrs];
+  const void *x[kMaxPtrs];
+};
+bool affd_small_path(const sk_sketch *s, int layer);
+// workspace bytes per (layer, vector) of a group: W and F, D floats each
+int64_t affd_small_bytes_per_vector(const sk_sketch *s);
+void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dtype, int64_t b_begin, int64_t bc,
+                    float *out, bool accumulate, hipStream_t st);
+int64_t affd_transposed_tile(const sk_sketch *s, int layer);
 bool affd_transposed_path(const sk_sketch *s, int layer);
+// Phases A-C of the transposed path for vectors b_begin .. b_begin + bc - 1,
+// writing G^T of vector b_begin + v at gbuf + v D; the W^T workspace is s->ws.
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *out, bool accumulate, hipStream_t st);
+                         int64_t bc, float *gbuf, hipStream_t st);
+// Phase E for gb vectors whose G^T starts at gbuf: out rows b_begin ...
+void run_affd_transposed_out(const sk_sketch *s, int layer, const float *gbuf, int64_t b_begin, int64_t gb,
+                             float *out, bool accumulate, hipStream_t st);
 void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                         float *w, hipStream_t st);
 void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st);

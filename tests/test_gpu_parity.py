@@ -57,7 +57,10 @@ def oracle_in(x):
 # shapes spanning several tiles, ragged tails, n < D and n not a multiple of 4
 LAYERS = [(1, 30), (7, 111), (3, 1500), (1, 5003), (33, 1024), (1, 16)]
 CASES = [(LAYERS, 16), (LAYERS, 256), (LAYERS, 1024), (LAYERS, 4096), ([(1, 70000), (3, 500)], 65536),
-         ([(1, 2 ** 20 + 3), (1, 9)], 2048), ([(1, 3 * 2 ** 20 + 11)], 65536)]
+         ([(1, 2 ** 20 + 3), (1, 9)], 2048), ([(1, 3 * 2 ** 20 + 11)], 65536),
+         # transformer-like mix: small layers grouped (N' = D, <= 8 rows), a
+         # two-digit layer with 128 rows and one with 9 source rows
+         ([(1, 768), (1, 2304), (96, 1024), (1, 3072), (2, 3000), (1, 8200)], 65536)]
 
 
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
