@@ -65,7 +65,8 @@ def cpu_baseline(cfg: str):
     import oracle as O
 
     c = W.CONFIGS[cfg]
-    cores = len(os.sched_getaffinity(0))
+    # the host's CPU share: OMP_NUM_THREADS where the machine sets it, else every core
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
     rng = np.random.default_rng(W.INPUT_SEED[cfg])
     shapes, D, seed = c["shapes"], c["D"], c["seed"]
 

@@ -85,9 +85,17 @@ __device__ __forceinline__ void load_rows16(const LayerDesc &ld, const uint16_t 
   }
 }
 
-// Tile row i (destination row p0 + i) is kept in LDS row 4 (i mod 4) + i / 4,
-// which makes the column reads of the W^T writes free of bank conflicts.
-__device__ __forceinline__ int tile_lds_row(int i) { return ((i & 3) << 2) | (i >> 2); }
+// LDS block of the 16 tile rows for the row kernel: one pad word per 64 floats
+// and a row stride of 2 banks modulo 32.  The transform runs with the row
+// index fastest (thread (i = tid % 16, c = tid / 16)): pass 1 holds columns
+// c + 16 k, pass 2 the 64 consecutive columns 64 c .. 64 c + 63, so in both
+// passes a half-wave touches 32 distinct banks, and after pass 2 the 16 lanes
+// of a column write its 16 consecutive p (64 bytes) straight from registers.
+struct RowsLds {
+  static constexpr int kStride = 1058;
+  static constexpr int kFloats = 16 * kStride;
+  static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> 6); }
+};
 }  // namespace
 
 template <bool BF16, bool VEC>
@@ -95,7 +103,7 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const void *__restrict__ x, int64_t b_begin, int64_t bc,
                                                     float *__restrict__ w, Key key) {
-  using L = Lds1024<16>;
+  using L = RowsLds;
   __shared__ __align__(16) float s[L::kFloats];
   __shared__ __align__(16) uint32_t sg[16 * 32];
   __shared__ uint16_t s_invp[1024];
@@ -124,9 +132,7 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
   int64_t sslab = s_slab[cur.t];
   float val[16][4];
   load_rows16<BF16, VEC>(ld, s_invp, sslab, cur.p0, x, b_begin + cur.v, col0, val);
-  const int lane = threadIdx.x & 63;
-  const int qq = lane >> 4;                                // p = p0 + 4 qq .. 4 qq + 3
-  const int lb = (lane & 15) + 16 * (threadIdx.x >> 6);   // l = lb + 64 m
+  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;  // transform: row ri, column group rc
   for (;;) {
     __syncthreads();  // the previous tile's reads of s and sg are done
     // sign words of the 16 rows: 8 Philox blocks of 128 signs per row, one per
@@ -142,7 +148,7 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
     for (int i = 0; i < 16; ++i) {
       const uint32_t bits = sg[i * 32 + (threadIdx.x >> 3)] >> (col0 & 31);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[L::idx(tile_lds_row(i), pc[q])] = flip(val[i][q], (bits >> q) & 1u);
+      for (int q = 0; q < 4; ++q) s[L::idx(i, pc[q])] = flip(val[i][q], (bits >> q) & 1u);
     }
     // prefetch the next tile into the registers just consumed
     const int64_t ntile = tile + G;
@@ -155,17 +161,27 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
       load_rows16<BF16, VEC>(ld, s_invp, nslab, nxt.p0, x, b_begin + nxt.v, col0, val);
     }
     __syncthreads();
-    fwht1024_lds<16>(s);
-    // 4 x 16 lanes write the 16 consecutive p of 16 columns l (64 bytes each)
-    const float sc = 1.0f / 32.0f;
-    float *dst0 = w + cur.v * ld.np + cur.t * lo_len + cur.p0 + 4 * qq;
+    // H_l (unnormalised; the 1/32 is applied by the readers of W^T)
+    float e[64];
+    {
+      float *b = s + ri * L::kStride + rc;
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int l = lb + 64 * m;
-      *(float4 *)(dst0 + (int64_t)l * 1024) =
-          make_float4(s[L::idx(qq, l)] * sc, s[L::idx(4 + qq, l)] * sc, s[L::idx(8 + qq, l)] * sc,
-                      s[L::idx(12 + qq, l)] * sc);
+      for (int k = 0; k < 64; ++k) e[k] = b[16 * k + (k >> 2)];
+      fwht_regs_t<64>(e);
+#pragma unroll
+      for (int k = 0; k < 64; ++k) b[16 * k + (k >> 2)] = e[k];
     }
+    __syncthreads();
+    {
+      const float *b = s + ri * L::kStride + 65 * rc;
+#pragma unroll
+      for (int m = 0; m < 64; ++m) e[m] = b[m];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) fwht_regs_t<16>(e + 16 * g);
+    }
+    float *dst = w + cur.v * ld.np + cur.t * lo_len + (int64_t)(64 * rc) * 1024 + cur.p0 + ri;
+#pragma unroll
+    for (int m = 0; m < 64; ++m) dst[(int64_t)m * 1024] = e[m];
     if (!more) break;
     tile = ntile;
     cur = nxt;
@@ -193,7 +209,7 @@ __global__ __launch_bounds__(256) void k_affdT_prow(const LayerDesc *__restrict_
     for (int k = 0; k < 64; ++k) e[k] = src[16 * k];
   }
   fwht1024_lds_regs<16>(s, e);
-  const float sc = 1.0f / 32.0f;
+  const float sc = 1.0f / 1024.0f;  // H_p here and H_l of phase A
 #pragma unroll
   for (int i = 0; i < 16; ++i)
 #pragma unroll
@@ -277,8 +293,8 @@ __global__ __launch_bounds__(256) void k_affdT_top(const LayerDesc *__restrict__
 #pragma unroll
       for (int k = 0; k < 4; ++k) f[v][k] += m[k][t] * lds[L::idx(v, threadIdx.x + 256 * k)];
   }
-  // H_p (1/32) twice and H_TT (1/TT)
-  affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (1024.0f * (float)TT), gout);
+  // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
+  affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
 }
 
 // TT in {16, 32, 64}: W^T rows already carry H_p (phase B); one p per thread and
