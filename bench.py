@@ -37,6 +37,11 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
+# kernel launched by each single-kernel profile class (the rocprofv3 name)
+KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
+             "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffd_copy_blocks", "fjl:prolog": "k_fjl_prolog"}
+
+
 def source_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2402_03994_amd", "csrc")
@@ -55,6 +60,60 @@ def measured_traffic(cfg: str, kclass: str):
     if rec.get("source_hash") != source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def copy_probe() -> int:
+    """A plain device copy of 1 GiB, three times: the reference whose rocprofv3
+    FETCH_SIZE / WRITE_SIZE readings calibrate those counters to bytes."""
+    import torch
+
+    n = (1 << 30) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4, "copies": 3}), flush=True)
+    return 0
+
+
+def _counter_per_launch(csv_path: str, name: str, counter: str):
+    import csv
+
+    vals = {}
+    for r in csv.DictReader(open(csv_path)):
+        if name in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise SystemExit(f"no {counter} records for kernels named {name!r} in {csv_path}")
+    return sum(vals.values()) / len(vals), len(vals)
+
+
+def traffic_json(cfg: str, kclass: str, fetch_csv: str, write_csv: str, copy_fetch_csv: str,
+                 copy_write_csv: str) -> int:
+    """Per-launch HBM bytes of a kernel class from rocprofv3 --pmc FETCH_SIZE and
+    WRITE_SIZE runs (KiB per dispatch), each scaled by the reading for the 1 GiB
+    copy of copy_probe(); written to profiles/ with the current source hash."""
+    kname = KERNEL_OF[kclass]
+    f_kib, nf = _counter_per_launch(fetch_csv, kname, "FETCH_SIZE")
+    w_kib, nw = _counter_per_launch(write_csv, kname, "WRITE_SIZE")
+    cf_kib, _ = _counter_per_launch(copy_fetch_csv, "copy", "FETCH_SIZE")
+    cw_kib, _ = _counter_per_launch(copy_write_csv, "copy", "WRITE_SIZE")
+    ref_kib = (1 << 30) / 1024
+    cal_f, cal_w = ref_kib / cf_kib, ref_kib / cw_kib
+    rec = {"config": cfg, "class": kclass, "kernel": kname, "source_hash": source_hash(),
+           "fetch_kib_per_launch": round(f_kib, 1), "write_kib_per_launch": round(w_kib, 1), "launches": nf,
+           "copy_fetch_kib_per_gib": round(cf_kib, 1), "copy_write_kib_per_gib": round(cw_kib, 1),
+           "fetch_scale": round(cal_f, 4), "write_scale": round(cal_w, 4),
+           "hbm_read_bytes_per_launch": round(f_kib * 1024 * cal_f),
+           "hbm_write_bytes_per_launch": round(w_kib * 1024 * cal_w),
+           "hbm_bytes_per_launch": round(f_kib * 1024 * cal_f + w_kib * 1024 * cal_w)}
+    out = os.path.join(ROOT, "profiles", f"traffic_{cfg}_{kclass.replace(':', '_')}.json")
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
+    return 0
 
 
 # ------------------------------------------------------------------ CPU baseline
@@ -211,7 +270,15 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c2", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true", help="run the 1 GiB copy used to calibrate counters")
+    ap.add_argument("--traffic-json", nargs=5, metavar=("CLASS", "FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                        "COPY_WRITE_CSV"),
+                    help="write profiles/traffic_<config>_<class>.json from rocprofv3 counter CSVs")
     args = ap.parse_args()
+    if args.copy_probe:
+        return copy_probe()
+    if args.traffic_json:
+        return traffic_json(args.config, *args.traffic_json)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the sketch shards by "
               "batch or by layer groups with one all-reduce of [batch, D]; see DESIGN.md)", file=sys.stderr)
@@ -263,10 +330,13 @@ def main() -> int:
             e[0] += t
             e[1] += n
             e[2] += by
-    dom = max(classes, key=lambda c: classes[c][0])
+    # the dominant kernel class among those that read the gradients (or write
+    # the parameter vectors): the others move only intermediates
+    dom = max((c for c in classes if classes[c][2] > 0), key=lambda c: classes[c][0])
     t_dom, n_dom, by_dom = classes[dom]
     achieved = by_dom / (t_dom * 1e-3) / 1e9 if t_dom > 0 else 0.0
-    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+    roofline = {"bound": "hbm", "kernel": KERNEL_OF.get(dom, dom), "class": dom, "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(cfg, dom),
                 "launches": n_dom, "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),

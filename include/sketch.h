@@ -191,7 +191,9 @@ enum {
   SK_PROF_FFD = 6,       /* FFD block kernels                               */
   SK_PROF_QK = 7,        /* QK contractions                                 */
   SK_PROF_OTHER = 8,
-  SK_PROF_CLASSES = 9
+  SK_PROF_AFFD_ROWS = 9, /* AFFD row kernel: load, sign, pi1, H_l (one launch) */
+  SK_PROF_QK_XB = 10,    /* QK first contraction X B^T (reads the gradients) */
+  SK_PROF_CLASSES = 11
 };
 int sketch_profile(sk_sketch *s, int enable);
 int sketch_profile_read(sk_sketch *s, double *ms, int64_t *count, int64_t *bytes);

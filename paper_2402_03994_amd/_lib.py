@@ -14,7 +14,8 @@ STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, 
 EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", "sketch_query",
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
            "sketch_status_string")
-PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other"]
+PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
+                "affd_rows", "qk_xb"]
 
 
 class LayerShape(ctypes.Structure):

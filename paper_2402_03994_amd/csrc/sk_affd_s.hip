@@ -187,7 +187,7 @@ bool affd_small_path(const sk_sketch *s, int layer) {
 int64_t affd_small_bytes_per_vector(const sk_sketch *s) { return 2 * s->D * 4; }
 
 void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dtype, int64_t b_begin, int64_t bc,
-                    float *out, bool accumulate, hipStream_t st) {
+                    int phases, float *out, bool accumulate, hipStream_t st) {
   if (nslots <= 0 || bc <= 0) return;
   const int64_t D = s->D;
   const int R = (int)(D / 1024);
@@ -195,12 +195,15 @@ void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dty
   float *w = s->ws;
   float *f = w + nslots * wslot;
   const unsigned zs = (unsigned)nslots;
-  if (dtype == SK_BF16)
-    hipLaunchKernelGGL(k_affdS_rows<true>, dim3(kSmallRows, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st,
-                       s->d_layers, s->d_ptab, g, b_begin, bc, w, wslot, s->key);
-  else
-    hipLaunchKernelGGL(k_affdS_rows<false>, dim3(kSmallRows, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st,
-                       s->d_layers, s->d_ptab, g, b_begin, bc, w, wslot, s->key);
+  if (phases & 1) {
+    if (dtype == SK_BF16)
+      hipLaunchKernelGGL(k_affdS_rows<true>, dim3(kSmallRows, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st,
+                         s->d_layers, s->d_ptab, g, b_begin, bc, w, wslot, s->key);
+    else
+      hipLaunchKernelGGL(k_affdS_rows<false>, dim3(kSmallRows, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st,
+                         s->d_layers, s->d_ptab, g, b_begin, bc, w, wslot, s->key);
+  }
+  if (!(phases & 2)) return;
   hipLaunchKernelGGL(k_affdS_top, dim3((unsigned)R, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st, s->d_layers,
                      s->d_ptab, g, bc, w, wslot, f, s->key);
 #define SK_SCOLS(E)                                                                                           \

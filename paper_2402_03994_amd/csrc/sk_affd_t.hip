@@ -409,13 +409,12 @@ bool affd_transposed_path(const sk_sketch *s, int layer) {
 }
 
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *gbuf, hipStream_t st) {
+                         int64_t bc, float *gbuf, int phases, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const int R = (int)(s->D / 1024);
   float *w = s->ws;
-  // A
-  {
+  if (phases & 1) {  // A
     // two resident workgroups per CU (64 KB of LDS each); a multiple of 8
     const dim3 grid(kRowsGrid);
 #define SK_AROWS(BF, VE)                                                                                  \
@@ -428,6 +427,7 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
     }
 #undef SK_AROWS
   }
+  if (!(phases & 2)) return;
   // B, C
   if (TT > 8) {
     dim3 gb((unsigned)((int64_t)TT * 1024 / 16), (unsigned)bc);

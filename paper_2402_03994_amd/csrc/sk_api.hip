@@ -517,8 +517,10 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
                 const int64_t gb = std::min(gmax, b0 + bc - g0);
                 for (int64_t t0 = g0; t0 < g0 + gb; t0 += tile) {
                   const int64_t tb = std::min(tile, g0 + gb - t0);
-                  SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz,
-                          run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gbuf + (t0 - g0) * s->D, st));
+                  float *gt = gbuf + (t0 - g0) * s->D;
+                  SK_PROF(SK_PROF_AFFD_ROWS, tb * ld.n * esz,
+                          run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 1, st));
+                  SK_PROF(SK_PROF_AFFD_FOLD, 0, run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 2, st));
                 }
                 SK_PROF(SK_PROF_GATHER, gb * g4 * (l == l1 - 1 ? 2 : 1),
                         run_affd_transposed_out(s, l, gbuf, g0, gb, out, acc_now, st));
@@ -561,7 +563,8 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
             }
             for (int64_t t0 = b0; t0 < b0 + bc; t0 += vt) {
               const int64_t tb = std::min(vt, b0 + bc - t0);
-              SK_PROF(SK_PROF_AFFD_FOLD, tb * nsum * esz, run_affd_small(s, g, ns, dtype, t0, tb, out, acc_now, st));
+              SK_PROF(SK_PROF_PROLOG, tb * nsum * esz, run_affd_small(s, g, ns, dtype, t0, tb, 1, out, acc_now, st));
+              SK_PROF(SK_PROF_AFFD_FOLD, 0, run_affd_small(s, g, ns, dtype, t0, tb, 2, out, acc_now, st));
             }
             acc_now = true;
           }
@@ -601,9 +604,12 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         break;
       }
       case SK_QK:
-        for (int l = l0; l < l1; ++l)
-          SK_PROF(SK_PROF_QK, bc * s->layers[l].n * esz + bc * s->layers[l].da * s->layers[l].db * 4,
-                  launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, batch, out, accumulate != 0, st));
+        for (int l = l0; l < l1; ++l) {
+          SK_PROF(SK_PROF_QK_XB, bc * s->layers[l].n * esz,
+                  launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, 1, out, accumulate != 0, st));
+          SK_PROF(SK_PROF_QK, bc * s->layers[l].da * s->layers[l].db * 4,
+                  launch_qk_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, 2, out, accumulate != 0, st));
+        }
         break;
     }
   }

@@ -41,14 +41,16 @@ struct SmallGroup {
 bool affd_small_path(const sk_sketch *s, int layer);
 // workspace bytes per (layer, vector) of a group: W and F, D floats each
 int64_t affd_small_bytes_per_vector(const sk_sketch *s);
+// phases: bit 0 = the row kernel (reads the gradients), bit 1 = the rest
 void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dtype, int64_t b_begin, int64_t bc,
-                    float *out, bool accumulate, hipStream_t st);
+                    int phases, float *out, bool accumulate, hipStream_t st);
 int64_t affd_transposed_tile(const sk_sketch *s, int layer);
 bool affd_transposed_path(const sk_sketch *s, int layer);
 // Phases A-C of the transposed path for vectors b_begin .. b_begin + bc - 1,
 // writing G^T of vector b_begin + v at gbuf + v D; the W^T workspace is s->ws.
+// phases: bit 0 = A (the row kernel, reads the gradients), bit 1 = B and C
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *gbuf, hipStream_t st);
+                         int64_t bc, float *gbuf, int phases, hipStream_t st);
 // Phase E for gb vectors whose G^T starts at gbuf: out rows b_begin ...
 void run_affd_transposed_out(const sk_sketch *s, int layer, const float *gbuf, int64_t b_begin, int64_t gb,
                              float *out, bool accumulate, hipStream_t st);
@@ -100,8 +102,9 @@ void launch_debug_stream(const sk_sketch *s, int layer, int stream_id, uint64_t 
 
 // ---- QK ----
 void launch_qk_factors(const sk_sketch *s, hipStream_t st);
+// stages: bit 0 = T = X B^T (reads the gradients), bit 1 = out (+)= A T
 void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                     float *t_ws, int64_t batch_total, float *out, bool accumulate, hipStream_t st);
+                     float *t_ws, int stages, float *out, bool accumulate, hipStream_t st);
 int64_t qk_workspace_elems(const sk_sketch *s, int layer, int64_t bc);
 void launch_qk_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *t_ws,
                        void *out, int out_dtype, const float *theta0, hipStream_t st);

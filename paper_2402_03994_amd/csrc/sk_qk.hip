@@ -237,14 +237,14 @@ __global__ void k_qk_at(const float *__restrict__ A, const float *__restrict__ t
 }
 
 void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                     float *t_ws, int64_t batch_total, float *out, bool accumulate, hipStream_t st) {
-  (void)batch_total;
+                     float *t_ws, int stages, float *out, bool accumulate, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const float *A = s->d_qka + ld.fa_off;
   const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
   if (qk_mfma_ok(ld, dtype)) {
     const int64_t rows = bc * (int64_t)ld.m;
     dim3 g1((unsigned)((rows + kQkRows - 1) / kQkRows));
+    if (stages & 1) {
 #define SK_S1(NT)                                                                                              \
   case NT:                                                                                                     \
     hipLaunchKernelGGL(k_qk_s1<NT>, g1, dim3(256), 0, st, (const uint16_t *)x, B, Blo, (int64_t)ld.m,           \
@@ -256,20 +256,27 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
       default: break;
     }
 #undef SK_S1
-    dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
-    hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin,
-                       out, (int)accumulate);
+    }
+    if (stages & 2) {
+      dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
+      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col,
+                         b_begin, out, (int)accumulate);
+    }
     (void)hipGetLastError();
     return;
   }
-  dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
-  if (dtype == SK_BF16)
-    hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
-  else
-    hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
-  dim3 g2((unsigned)(((int64_t)ld.da * ld.db + 255) / 256), (unsigned)bc);
-  hipLaunchKernelGGL(k_qk_at, g2, dim3(256), 0, st, A, t_ws, ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, out,
-                     (int)accumulate);
+  if (stages & 1) {
+    dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
+    if (dtype == SK_BF16)
+      hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
+    else
+      hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
+  }
+  if (stages & 2) {
+    dim3 g2((unsigned)(((int64_t)ld.da * ld.db + 255) / 256), (unsigned)bc);
+    hipLaunchKernelGGL(k_qk_at, g2, dim3(256), 0, st, A, t_ws, ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, out,
+                       (int)accumulate);
+  }
   (void)hipGetLastError();
 }
 
