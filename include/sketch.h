@@ -110,13 +110,25 @@ enum {
  *   D         target dimension.  FWHT kinds: a power of two, 16 <= D <= 2^20
  *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
  *   seed      64-bit key of every random stream.
- *   flags     reserved, must be 0.
+ *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).
  * On success *out receives the handle (destroy with sketch_destroy).  The
  * small per-layer tables and the QK factors are generated on the device here
  * (QK: A in fp32; B in fp32 split into two bf16 terms for the MFMA units).
  */
 int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, int64_t D, uint64_t seed,
                   uint32_t flags, int32_t device, sk_sketch **out);
+
+/*
+ * AFFD layers whose second-to-last Kronecker digit has 1024 values: by default
+ * sketch_create stores, per such layer, the N'_l values
+ *   M[t'][p][l] = sum_t H[t][t'] (-1)^<h*, t> g[t, p, l]
+ * (the Gaussian diagonal G combined with the signed top-digit fold; fp32, one
+ * copy per sketch) when all of them together fit in SK_AFFD_MTAB_MB MiB of
+ * device memory (environment, default 8192), so that sketch_apply reads them
+ * instead of regenerating G.  With SK_FLAG_AFFD_NO_MTAB nothing is stored and
+ * G is regenerated on every call; the results agree to rounding.
+ */
+#define SK_FLAG_AFFD_NO_MTAB 1u
 
 /*
  * Forward sketch y = sum over the selected layers of S_l x_l.

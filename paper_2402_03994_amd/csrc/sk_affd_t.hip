@@ -351,6 +351,88 @@ __global__ __launch_bounds__(256, 1) void k_affdT_top_wide(const LayerDesc *__re
   affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32.0f * (float)TT), gout);
 }
 
+// ---- C with a stored M --------------------------------------------------------
+// M[t'][l][p] = (H_TT (c . g[., p, l]))[t'], c_t = (-1)^<h*, t>, written once
+// per sketch: thread per (p, l) with p fastest so the TT rows are coalesced.
+template <int TT>
+__global__ __launch_bounds__(256) void k_affd_mtab(const LayerDesc *__restrict__ layers, int layer,
+                                                   float *__restrict__ m, Key key) {
+  const LayerDesc &ld = layers[layer];
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;  // < 2^20
+  const int64_t p = q & 1023, l = q >> 10;
+  const int64_t lo_len = 1ll << 20;
+  float v[TT];
+#pragma clang loop unroll(full)
+  for (int t = 0; t < TT; ++t)
+    v[t] = flip(gauss((uint64_t)(t * lo_len + p * 1024 + l), (uint32_t)ld.layer_id, ST_GAUSS, key),
+                (uint32_t)__popc((uint32_t)t & ld.hstar) & 1u);
+  fwht_regs_t<TT>(v);
+#pragma clang loop unroll(full)
+  for (int t = 0; t < TT; ++t) m[t * lo_len + l * 1024 + p] = v[t];
+}
+
+// Any TT <= 64 with M stored: per live slab row t of the column l, H_p of the
+// VB vectors' rows (fed from global memory in the first pass's layout), then
+// acc += M[t][l][p] x.  No Gaussians are generated and W^T is read once.
+template <int VB>
+__global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, int layer,
+                                                    const float *__restrict__ w, int64_t bc, int R,
+                                                    const float *__restrict__ mt, float *__restrict__ gout) {
+  using L = Lds1024<VB>;
+  __shared__ __align__(16) float lds[L::kFloats];
+  const LayerDesc &ld = layers[layer];
+  const int TT = 1 << (ld.lgnp - 20);
+  const int64_t lo_len = 1ll << 20;
+  const int64_t l = blockIdx.x;
+  const int64_t v0 = (int64_t)blockIdx.y * VB;
+  const int nv = (int)((bc - v0) < VB ? (bc - v0) : VB);
+  uint64_t live, sgn;
+  masks_t(ld, ptab, TT, live, sgn);
+  constexpr int C = 256 / VB, E = 4 * VB;
+  const int vr = threadIdx.x / C;
+  const float *src = w + (v0 + vr) * ld.np + l * 1024 + (threadIdx.x % C);
+  const float *mcol = mt + l * 1024 + threadIdx.x;
+  float f[VB][4];
+#pragma unroll
+  for (int v = 0; v < VB; ++v)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) f[v][k] = 0.0f;
+#pragma unroll 1
+  for (int t = 0; t < TT; ++t) {
+    if (!((live >> t) & 1ull)) continue;  // uniform: all-zero slab
+    float e[E], mm[4];
+#pragma unroll
+    for (int k = 0; k < E; ++k) e[k] = vr < nv ? src[t * lo_len + C * k] : 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mm[k] = mcol[t * lo_len + 256 * k];
+    __syncthreads();  // the previous slab row's reads of lds are done
+    fwht1024_lds_regs<VB>(lds, e);
+#pragma unroll
+    for (int v = 0; v < VB; ++v)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) f[v][k] += mm[k] * lds[L::idx(v, threadIdx.x + 256 * k)];
+  }
+  // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
+  affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
+}
+
+void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const dim3 grid(1u << 12);  // 2^20 (p, l) pairs
+  switch (ld.lgnp - 20) {
+    case 0: hipLaunchKernelGGL(k_affd_mtab<1>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 1: hipLaunchKernelGGL(k_affd_mtab<2>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 2: hipLaunchKernelGGL(k_affd_mtab<4>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 3: hipLaunchKernelGGL(k_affd_mtab<8>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 4: hipLaunchKernelGGL(k_affd_mtab<16>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 5: hipLaunchKernelGGL(k_affd_mtab<32>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    case 6: hipLaunchKernelGGL(k_affd_mtab<64>, grid, dim3(256), 0, st, s->d_layers, layer, m, s->key); break;
+    default: break;
+  }
+  (void)hipGetLastError();
+}
+
 // ---- E ---------------------------------------------------------------------
 // One workgroup per (vector, block of 16 values of a): reads G^T[v][l][a0..a0+15]
 // for every l (64-byte pieces), transposes through LDS, H_l, gathers pi2_l.
@@ -428,6 +510,12 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
 #undef SK_AROWS
   }
   if (!(phases & 2)) return;
+  if (s->d_mtab && s->mtab_off[layer] >= 0) {
+    hipLaunchKernelGGL(k_affdT_topM<16>, dim3(1024u, (unsigned)((bc + 15) / 16)), dim3(256), 0, st, s->d_layers,
+                       s->d_ptab, layer, w, bc, R, s->d_mtab + s->mtab_off[layer], gbuf);
+    (void)hipGetLastError();
+    return;
+  }
   // B, C
   if (TT > 8) {
     dim3 gb((unsigned)((int64_t)TT * 1024 / 16), (unsigned)bc);

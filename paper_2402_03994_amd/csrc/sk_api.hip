@@ -70,6 +70,7 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_smp);
   f(s->d_qka);
   f(s->d_qkb);
+  f(s->d_mtab);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
   s->evpool.clear();
@@ -167,7 +168,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   *out = nullptr;
   if ((int)kind < 0 || (int)kind > 4) return fail(SK_EINVAL, "unknown sketch kind");
   if (!shapes || n_layers < 1) return fail(SK_EINVAL, "need at least one layer shape");
-  if (flags != 0) return fail(SK_EINVAL, "flags must be 0");
+  if (flags & ~SK_FLAG_AFFD_NO_MTAB) return fail(SK_EINVAL, "unknown flags");
   for (int l = 0; l < n_layers; ++l) {
     if (shapes[l].rows < 1 || shapes[l].cols < 1)
       return fail(SK_EINVAL, "layer " + std::to_string(l) + ": rows and cols must be >= 1");
@@ -394,6 +395,25 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   s->ws_bytes = std::min<int64_t>(budget, pv * 256);
   if (s->ws_bytes > 0) SK_TRY(alloc((void **)&s->ws, (size_t)s->ws_bytes));
 
+  if (kind == SK_AFFD && !(flags & SK_FLAG_AFFD_NO_MTAB)) {
+    // M tables of the transposed-path layers, when they fit the budget
+    int64_t total = 0;
+    s->mtab_off.assign(n_layers, -1);
+    for (int l = 0; l < n_layers; ++l)
+      if (affd_transposed_path(s, l)) {
+        s->mtab_off[l] = total;
+        total += s->layers[l].np;
+      }
+    const char *e = std::getenv("SK_AFFD_MTAB_MB");
+    const int64_t mb = e ? std::atoll(e) : 8192;
+    if (total > 0 && total * 4 <= (mb << 20)) {
+      SK_TRY(alloc((void **)&s->d_mtab, (size_t)total * 4));
+      for (int l = 0; l < n_layers; ++l)
+        if (s->mtab_off[l] >= 0) launch_affd_mtab(s, l, s->d_mtab + s->mtab_off[l], nullptr);
+    } else {
+      s->mtab_off.assign(n_layers, -1);
+    }
+  }
   if (s->d_gtab) launch_gauss_table(s, s->d_gtab, nullptr);
   if (kind == SK_QK) launch_qk_factors(s, nullptr);
   if (hipDeviceSynchronize() != hipSuccess) {

@@ -85,6 +85,9 @@ struct sk_sketch {
   float *d_qka = nullptr;       // A factors, fp32
   uint16_t *d_qkb = nullptr;    // B factors as bf16 hi terms, then bf16 lo terms (hi + lo ~ fp32 B)
   int64_t qk_a_elems = 0, qk_b_elems = 0;
+  // AFFD: precomputed M = H_TT (signs . G) per transposed-path layer
+  float *d_mtab = nullptr;
+  std::vector<int64_t> mtab_off;  // per layer: float offset into d_mtab, -1 if none
   // kernel timing
   struct ProfRec {
     int cls;

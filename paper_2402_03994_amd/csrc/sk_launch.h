@@ -48,6 +48,8 @@ int64_t affd_transposed_tile(const sk_sketch *s, int layer);
 bool affd_transposed_path(const sk_sketch *s, int layer);
 // Phases A-C of the transposed path for vectors b_begin .. b_begin + bc - 1,
 // writing G^T of vector b_begin + v at gbuf + v D; the W^T workspace is s->ws.
+// M[t'][l][p] = (H_TT (signs . g[., p, l]))[t'] for a transposed-path layer
+void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st);
 // phases: bit 0 = A (the row kernel, reads the gradients), bit 1 = B and C
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
                          int64_t bc, float *gbuf, int phases, hipStream_t st);

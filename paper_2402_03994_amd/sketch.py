@@ -24,9 +24,13 @@ class Sketch:
     """A seeded structured sketch S: R^N -> R^D over a list of parameter shapes.
 
     shapes: per layer (rows, cols) or (rows, cols, qk_da, qk_db) for QK.
+    flags: sketch_create flags (AFFD_NO_MTAB: regenerate the AFFD Gaussians on
+    every call instead of storing the per-layer M tables).
     """
 
-    def __init__(self, kind: str, shapes: Sequence[Sequence[int]], D: int, seed: int, device=None):
+    AFFD_NO_MTAB = 1
+
+    def __init__(self, kind: str, shapes: Sequence[Sequence[int]], D: int, seed: int, device=None, flags: int = 0):
         self.lib = _lib.load()
         self.kind = kind
         self.D = int(D)
@@ -40,7 +44,7 @@ class Sketch:
             arr[i].qk_da = s[2] if len(s) > 2 else 0
             arr[i].qk_db = s[3] if len(s) > 3 else 0
         h = ctypes.c_void_p()
-        _lib.check(self.lib.sketch_create(KINDS[kind], arr, len(self.shapes), self.D, self.seed, 0,
+        _lib.check(self.lib.sketch_create(KINDS[kind], arr, len(self.shapes), self.D, self.seed, int(flags),
                                           self.device.index, ctypes.byref(h)))
         self._h = h
 

@@ -44,7 +44,7 @@ def shapes(*ss):
     (3, [(1, 10)], 8, 0, -5),             # below the kernels' minimum
     (3, [(1, 10)], 1 << 21, 0, -5),       # above the kernels' maximum
     (3, [(0, 10)], 64, 0, -1),            # empty layer
-    (3, [(1, 10)], 64, 1, -1),            # reserved flags
+    (3, [(1, 10)], 64, 2, -1),            # unknown flags
     (4, [(4, 5, 2, 2)], 5, 0, -1),        # QK: sum dA*dB != D
     (4, [(4, 5, 5, 2)], 10, 0, -1),       # QK: dA > rows
     (4, [(4, 5, 0, 2)], 0, 0, -1),        # QK: dA < 1

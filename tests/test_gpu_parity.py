@@ -75,6 +75,21 @@ def test_forward_parity_f32(kind, case, dev):
     assert rel_err(y, ref) < TOL_F32
 
 
+@pytest.mark.parametrize("mtab", [True, False])
+@pytest.mark.parametrize("shapes", [[(3, 2 ** 20 + 77), (1, 5000)], [(1, 9 * 2 ** 20 + 5)], [(37, 2 ** 20)]])
+def test_affd_mtab_parity(shapes, mtab, dev):
+    """AFFD layers on the transposed path (one to sixteen top slabs), with the
+    stored M tables and with the Gaussians regenerated per call."""
+    from paper_2402_03994_amd import Sketch
+    D, seed, batch = 65536, 21, 5
+    s = Sketch("affd", shapes, D, seed, device=dev, flags=0 if mtab else Sketch.AFFD_NO_MTAB)
+    xs = rand_inputs(shapes, batch, 99)
+    y = s.apply([x.to(dev) for x in xs])
+    o = O.apply("affd", shapes, D, seed, [oracle_in(x)[0] for x in xs])
+    assert rel_err(y.cpu().numpy(), o) <= TOL_F32
+    s.close()
+
+
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
 @pytest.mark.parametrize("case", [1, 3, 4])
 def test_transpose_parity(kind, case, dev):
