@@ -398,20 +398,39 @@ __global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict_
   for (int v = 0; v < VB; ++v)
 #pragma unroll
     for (int k = 0; k < 4; ++k) f[v][k] = 0.0f;
-#pragma unroll 1
-  for (int t = 0; t < TT; ++t) {
-    if (!((live >> t) & 1ull)) continue;  // uniform: all-zero slab
-    float e[E], mm[4];
+  // the loads of the next live slab row are issued before the transform of
+  // the current one
+  float e[E], mm[4];
+  auto fetch = [&](int t) {
 #pragma unroll
     for (int k = 0; k < E; ++k) e[k] = vr < nv ? src[t * lo_len + C * k] : 0.0f;
 #pragma unroll
     for (int k = 0; k < 4; ++k) mm[k] = mcol[t * lo_len + 256 * k];
+  };
+  uint64_t rest = live;  // never empty: slab 0 holds source row 0
+  int t = __builtin_ctzll(rest);
+  rest &= rest - 1;
+  fetch(t);
+#pragma unroll 1
+  for (;;) {
+    float ec[E], mc[4];
+#pragma unroll
+    for (int k = 0; k < E; ++k) ec[k] = e[k];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mc[k] = mm[k];
+    const bool more = rest != 0;
+    if (more) {
+      t = __builtin_ctzll(rest);
+      rest &= rest - 1;
+      fetch(t);
+    }
     __syncthreads();  // the previous slab row's reads of lds are done
-    fwht1024_lds_regs<VB>(lds, e);
+    fwht1024_lds_regs<VB>(lds, ec);
 #pragma unroll
     for (int v = 0; v < VB; ++v)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) f[v][k] += mm[k] * lds[L::idx(v, threadIdx.x + 256 * k)];
+      for (int k = 0; k < 4; ++k) f[v][k] += mc[k] * lds[L::idx(v, threadIdx.x + 256 * k)];
+    if (!more) break;
   }
   // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
   affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
@@ -470,17 +489,17 @@ __global__ __launch_bounds__(256) void k_affdT_out(const LayerDesc *__restrict__
 
 constexpr unsigned kRowsGrid = 512;
 
-// Vectors per call for TT <= 8: a multiple of 16 (one Gaussian pass per 16
-// vectors in phase C) whose W^T (live slabs x 4 MB per vector) stays within
-// the 256 MB memory-side cache between phases A and C, so that the W^T round
-// trip rarely reaches HBM.  0 = no preference (TT > 8: W^T is far larger).
+// Vectors per call for TT <= 8: a multiple of 8 (the vectors of one phase-C
+// workgroup) whose W^T (live slabs x 4 MB per vector) stays within the 256 MB
+// memory-side cache between phases A and C, so that the W^T round trip rarely
+// reaches HBM.  0 = no preference (TT > 8: W^T is far larger).
 int64_t affd_transposed_tile(const sk_sketch *s, int layer) {
   const LayerDesc &ld = s->layers[layer];
   if (!affd_transposed_path(s, layer) || ld.lgnp - 20 > 3) return 0;
   const char *e = std::getenv("SK_AFFD_MALL_MB");
   const int64_t budget = (e ? std::atoll(e) : 192) << 20;
   const int64_t wbytes = ((ld.rows_live + 1023) / 1024) * (4ll << 20);
-  return 16 * std::max<int64_t>(1, budget / (16 * wbytes));
+  return 8 * std::max<int64_t>(1, budget / (8 * wbytes));
 }
 
 bool affd_transposed_path(const sk_sketch *s, int layer) {
@@ -511,7 +530,7 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
   }
   if (!(phases & 2)) return;
   if (s->d_mtab && s->mtab_off[layer] >= 0) {
-    hipLaunchKernelGGL(k_affdT_topM<16>, dim3(1024u, (unsigned)((bc + 15) / 16)), dim3(256), 0, st, s->d_layers,
+    hipLaunchKernelGGL(k_affdT_topM<8>, dim3(1024u, (unsigned)((bc + 7) / 8)), dim3(256), 0, st, s->d_layers,
                        s->d_ptab, layer, w, bc, R, s->d_mtab + s->mtab_off[layer], gbuf);
     (void)hipGetLastError();
     return;
