@@ -284,7 +284,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     s->Lw = (int)std::min<int64_t>(D, 1024);
     s->R = (int)(D / s->Lw);
     const int R = s->R;
-    const int64_t rows_per_item = 64;
+    const int64_t rows_per_item = kFoldRowsPerItem;
     for (int l = 0; l < n_layers; ++l) {
       LayerDesc &ld = s->layers[l];
       ld.rslot_off = (int32_t)rslot.size();

@@ -114,16 +114,47 @@ __device__ __forceinline__ void load_cols(const void *x, int64_t e, int64_t lim,
   for (int q = 0; q < CPT; q += 4) load4<BF16, VEC>(x, e + q, lim - q, v + q);
 }
 
+// CPT (4 fp32 or up to 8 bf16) consecutive elements from element e as their raw
+// bit patterns in 16 bytes; elements at or past lim read as zero.
+template <int CPT, bool BF16, bool VEC>
+__device__ __forceinline__ uint4 load_raw16(const void *x, int64_t e, int64_t lim) {
+  if (VEC && lim >= CPT && (BF16 ? CPT == 8 : CPT == 4))
+    return BF16 ? *(const uint4 *)((const uint16_t *)x + e) : *(const uint4 *)((const float *)x + e);
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) {
+    if (q < lim) {
+      if (BF16)
+        w[q >> 1] |= (uint32_t)((const uint16_t *)x)[e + q] << (16 * (q & 1));
+      else
+        w[q] = ((const uint32_t *)x)[e + q];
+    }
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+template <bool BF16>
+__device__ __forceinline__ float raw16_value(const uint4 &r, int q) {
+  const uint32_t w = (q >> (BF16 ? 1 : 0)) == 0 ? r.x : (q >> (BF16 ? 1 : 0)) == 1 ? r.y
+                   : (q >> (BF16 ? 1 : 0)) == 2 ? r.z : r.w;
+  return BF16 ? __uint_as_float((q & 1) ? (w & 0xFFFF0000u) : (w << 16)) : __uint_as_float(w);
+}
+
 // Fold kernel.  Each thread owns CPT consecutive columns of a row; when a row
 // needs fewer than 256 threads, NGR = 256 / (L / CPT) row groups take
-// interleaved rows and their sums are combined in LDS in group order.
+// interleaved rows and their sums are combined in LDS in group order.  The
+// item's source rows are resolved into LDS first, and the loads of a group's
+// next row are issued before the current one is added.
 template <int BT, int CPT, bool BF16, bool VEC>
 __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ items,
                                                    const LayerDesc *__restrict__ layers,
                                                    const uint16_t *__restrict__ ptab, PtrPack ptrs, int first_layer,
                                                    int64_t batch, int64_t b_begin, int64_t bc, int item_begin, int R,
                                                    int Lw, float *__restrict__ part, Key key) {
-  __shared__ float s[BT][1024];
+  using LF = Lds1024<BT>;
+  __shared__ __align__(16) float s_raw[LF::kFloats > BT * 1024 ? LF::kFloats : BT * 1024];
+  __shared__ int32_t srow[kFoldRowsPerItem];
+  float(*s)[1024] = reinterpret_cast<float(*)[1024]>(s_raw);
   const FoldItem it = items[item_begin + blockIdx.x];
   const LayerDesc &ld = layers[it.layer];
   const int64_t n = ld.n;
@@ -137,17 +168,13 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
   const int bt0 = blockIdx.y * BT;
   const void *xp = ptrs.p[it.layer - first_layer];
   const int nb = (int)((batch - b_begin - bt0) < BT ? (batch - b_begin - bt0) : BT);  // rows of this tile
-  float acc[BT][CPT];
-#pragma unroll
-  for (int b = 0; b < BT; ++b)
-#pragma unroll
-    for (int q = 0; q < CPT; ++q) acc[b][q] = 0.0f;
-
-  const int nk = R > 1 ? ld.dk1 / R : 1;
-  const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
-  if (active) {
-    // source row of fold step t (or -1 when it lies past the data)
-    auto row_of = [&](int t) -> int64_t {
+  const int nt = it.t1 - it.t0;  // <= kFoldRowsPerItem
+  // source row of each fold step (-1 past the data)
+  {
+    const int nk = R > 1 ? ld.dk1 / R : 1;
+    const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
+    if (tid < nt) {
+      const int t = it.t0 + tid;
       int64_t h;
       if (R == 1) {
         h = t;
@@ -156,44 +183,77 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
         const int k = t - htop * nk;
         h = (int64_t)htop * ld.dk1 + inv_k1[it.r + k * R];
       }
-      return (h < ld.rows_live && h * L + col0 < n) ? h : -1;
-    };
-    // U rows per iteration (U * CPT = 8 elements of each vector per thread in flight)
-    constexpr int U = CPT >= 8 ? 1 : 8 / CPT;
-    for (int t = it.t0 + grp; t < it.t1; t += U * ngr) {
-      int64_t hs[U], js[U];
-      float v[U][BT][CPT];
+      srow[tid] = h < ld.rows_live ? (int32_t)h : -1;
+    }
+    __syncthreads();
+  }
+  float acc[BT][CPT];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        hs[u] = (t + u * ngr < it.t1) ? row_of(t + u * ngr) : -1;
-        js[u] = hs[u] * L + col0;
-        if (hs[u] >= 0) {
+  for (int b = 0; b < BT; ++b)
 #pragma unroll
-          for (int b = 0; b < BT; ++b)
-            if (b < nb) load_cols<CPT, BF16, VEC>(xp, (b_begin + bt0 + b) * n + js[u], n - js[u], v[u][b]);
-        }
+    for (int q = 0; q < CPT; ++q) acc[b][q] = 0.0f;
+  if (active) {
+    // raw 16-byte pieces (CPT fp32 or bf16 values) of the next row, per vector
+    uint4 v[BT];
+    int64_t jn = -1;
+    auto fetch = [&](int i) {
+      const int32_t h = i < nt ? srow[i] : -1;
+      jn = h >= 0 ? (int64_t)h * L + col0 : -1;
+      if (jn >= n) jn = -1;
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        v[b] = make_uint4(0u, 0u, 0u, 0u);
+        if (jn >= 0 && b < nb) v[b] = load_raw16<CPT, BF16, VEC>(xp, (b_begin + bt0 + b) * n + jn, n - jn);
       }
+    };
+    fetch(grp);
+    for (int i = grp; i < nt; i += ngr) {
+      uint4 cur[BT];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (hs[u] >= 0) {
-          const uint32_t bits = sign_word((uint64_t)js[u], (uint32_t)ld.layer_id, key) >> (js[u] & 31);
+      for (int b = 0; b < BT; ++b) cur[b] = v[b];
+      const int64_t j = jn;
+      fetch(i + ngr);
+      if (j >= 0) {
+        const uint32_t bits = sign_word((uint64_t)j, (uint32_t)ld.layer_id, key) >> (j & 31);
 #pragma unroll
-          for (int b = 0; b < BT; ++b)
-            if (b < nb) {
+        for (int b = 0; b < BT; ++b)
 #pragma unroll
-              for (int q = 0; q < CPT; ++q) acc[b][q] += flip(v[u][b][q], (bits >> q) & 1u);
-            }
-        }
+          for (int q = 0; q < CPT; ++q) acc[b][q] += flip(raw16_value<BF16>(cur[b], q), (bits >> q) & 1u);
       }
     }
   }
-  // route the columns through pi1 of the last digit; row groups add in order
+  // route the columns through pi1 of the last digit
   const uint16_t *fwd_k = ptab + ld.poff[0][0][ld.K - 1];
   int pc[CPT];
   if (active) {
 #pragma unroll
     for (int q = 0; q < CPT; ++q) pc[q] = fwd_k[col0 + q];
   }
+  const int64_t slot = blockIdx.x;
+  if (L == 1024 && Lw == 1024) {
+    // row groups add in order, then H_L of the BT rows in a conflict-free LDS block
+    for (int gi = 0; gi < ngr; ++gi) {
+      if (active && grp == gi) {
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+#pragma unroll
+          for (int b = 0; b < BT; ++b) {
+            float *d = s_raw + LF::idx(b, pc[q]);
+            *d = gi == 0 ? acc[b][q] : *d + acc[b][q];
+          }
+      }
+      __syncthreads();
+    }
+    fwht1024_lds<BT>(s_raw);
+    for (int b = 0; b < nb; ++b)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = tid + 256 * k;
+        part[(slot * bc + bt0 + b) * 1024 + c] = s_raw[LF::idx(b, c)] * (1.0f / 32.0f);
+      }
+    return;
+  }
+  // row groups add in order
   for (int gi = 0; gi < ngr; ++gi) {
     if (active && grp == gi) {
 #pragma unroll
@@ -226,7 +286,6 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
     lds_fwht(&s[b][0], lgw, 0);
   }
   const float sc = rsqrtf((float)Lw);
-  const int64_t slot = blockIdx.x;
   for (int e = tid; e < nb * Lw; e += 256) {
     const int b = e / Lw, c = e - (e / Lw) * Lw;
     part[(slot * bc + bt0 + b) * Lw + c] = s[b][c] * sc;
@@ -358,57 +417,57 @@ __global__ __launch_bounds__(256) void k_afjl_tail_reg(const LayerDesc *__restri
   for (int r = 0; r < R; ++r) o[(int64_t)r * Lw] = acc[r] * sc;
 }
 
-// Tail for R = 1024 (D = 2^20): H_1024 = H_32 (x) H_32.  A workgroup owns 8
-// columns of one vector; each thread first transforms 32 rows r = 32 rh + j
-// (bits 0-4 of r) in registers, then, after one LDS exchange, 32 rows
-// r = 32 j + rl (bits 5-9), which it keeps as accumulators across layers.
-__global__ __launch_bounds__(256) void k_afjl_tail_1024(const LayerDesc *__restrict__ layers,
-                                                        const int2 *__restrict__ rslot, const float *__restrict__ part,
-                                                        const float *__restrict__ gtab, int l_begin, int l_end,
-                                                        int item_begin, int Lw, int64_t D, int64_t bc, int64_t b_begin,
-                                                        int64_t batch, float *__restrict__ out, int accumulate) {
-  __shared__ float s[1024 * 8];
-  const int c = threadIdx.x & 7, hi = threadIdx.x >> 3;  // hi: rh (phase 1) or rl (phase 2)
-  const int c0 = blockIdx.x * 8;
+// R = Lw = 1024 with 1024 threads: workgroup per (32 columns, vector), so every
+// partial and G row piece is a full 128-byte line; thread (hi, c) holds rows
+// hi * 32 + j of column c0 + c, H_R = H_32 (x) H_32 with one LDS transpose
+// (128 KB); four waves per SIMD hide the load latency.
+__global__ __launch_bounds__(1024) void k_afjl_tail_1024w(const LayerDesc *__restrict__ layers,
+                                                          const int2 *__restrict__ rslot,
+                                                          const float *__restrict__ part,
+                                                          const float *__restrict__ gtab, int l_begin, int l_end,
+                                                          int item_begin, int64_t D, int64_t bc, int64_t b_begin,
+                                                          float *__restrict__ out, int accumulate) {
+  __shared__ float s[1024 * 32];
+  const int c = threadIdx.x & 31, hi = threadIdx.x >> 5;
+  // workgroup x runs on XCD x mod 8: each XCD takes 4 consecutive column blocks
+  const int c0 = ((blockIdx.x & 7) * 4 + (blockIdx.x >> 3)) * 32;
   const int64_t bl = blockIdx.y;
-  if (b_begin + bl >= batch) return;
   float acc[32];
 #pragma unroll
   for (int j = 0; j < 32; ++j) acc[j] = 0.0f;
   for (int l = l_begin; l < l_end; ++l) {
-    const int2 *rs = rslot + layers[l].rslot_off;
     float v[32];
+    const int2 *rs = rslot + layers[l].rslot_off;
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
       const int2 q = rs[hi * 32 + j];
       const int64_t slot = q.y > 0 ? q.x - item_begin : 0;
-      const float x = part[(slot * bc + bl) * Lw + c0 + c];
-      v[j] = q.y > 0 ? x : 0.0f;
+      v[j] = part[(slot * bc + bl) * 1024 + c0 + c];
     }
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
       const int2 q = rs[hi * 32 + j];
-      for (int k = 1; k < q.y; ++k) v[j] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * Lw + c0 + c];
+      if (q.y <= 0) v[j] = 0.0f;
+      for (int k = 1; k < q.y; ++k) v[j] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * 1024 + c0 + c];
     }
     fwht_regs_t<32>(v);
 #pragma unroll
-    for (int j = 0; j < 32; ++j) s[(hi * 32 + j) * 8 + c] = v[j];
+    for (int j = 0; j < 32; ++j) s[(hi * 32 + j) * 32 + c] = v[j];
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < 32; ++j) v[j] = s[(j * 32 + hi) * 8 + c];
+    for (int j = 0; j < 32; ++j) v[j] = s[(j * 32 + hi) * 32 + c];
     __syncthreads();
     fwht_regs_t<32>(v);
     const float *g = gtab + (int64_t)l * D + c0 + c;
 #pragma unroll
-    for (int j = 0; j < 32; ++j) acc[j] += g[(int64_t)(j * 32 + hi) * Lw] * v[j];
+    for (int j = 0; j < 32; ++j) acc[j] += g[(int64_t)(j * 32 + hi) * 1024] * v[j];
   }
-  const float sc = 1.0f / 32.0f;
   float *o = out + (b_begin + bl) * D + c0 + c;
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
     const int64_t r = j * 32 + hi;
-    const float val = acc[j] * sc;
-    o[r * Lw] = accumulate ? o[r * Lw] + val : val;
+    const float val = acc[j] * (1.0f / 32.0f);
+    o[r * 1024] = accumulate ? o[r * 1024] + val : val;
   }
 }
 
@@ -416,9 +475,8 @@ void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin
                       int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st) {
   if (s->R == 1024 && s->Lw == 1024) {
     const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
-    dim3 grid((unsigned)(s->Lw / 8), (unsigned)rows);
-    hipLaunchKernelGGL(k_afjl_tail_1024, grid, dim3(256), 0, st, s->d_layers, s->d_rslot, part, s->d_gtab, l_begin,
-                       l_end, item_begin, s->Lw, s->D, bc, b_begin, batch, out, (int)accumulate);
+    hipLaunchKernelGGL(k_afjl_tail_1024w, dim3(32u, (unsigned)rows), dim3(1024), 0, st, s->d_layers, s->d_rslot, part,
+                       s->d_gtab, l_begin, l_end, item_begin, s->D, bc, b_begin, out, (int)accumulate);
     SK_CHECK_LAUNCH();
     return;
   }
