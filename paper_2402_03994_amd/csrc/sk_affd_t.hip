@@ -85,17 +85,6 @@ __device__ __forceinline__ void load_rows16(const LayerDesc &ld, const uint16_t 
   }
 }
 
-// LDS block of the 16 tile rows for the row kernel: one pad word per 64 floats
-// and a row stride of 2 banks modulo 32.  The transform runs with the row
-// index fastest (thread (i = tid % 16, c = tid / 16)): pass 1 holds columns
-// c + 16 k, pass 2 the 64 consecutive columns 64 c .. 64 c + 63, so in both
-// passes a half-wave touches 32 distinct banks, and after pass 2 the 16 lanes
-// of a column write its 16 consecutive p (64 bytes) straight from registers.
-struct RowsLds {
-  static constexpr int kStride = 1058;
-  static constexpr int kFloats = 16 * kStride;
-  static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> 6); }
-};
 }  // namespace
 
 template <bool BF16, bool VEC>
@@ -103,7 +92,7 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const void *__restrict__ x, int64_t b_begin, int64_t bc,
                                                     float *__restrict__ w, Key key) {
-  using L = RowsLds;
+  using L = Lds1024R;
   __shared__ __align__(16) float s[L::kFloats];
   __shared__ __align__(16) uint32_t sg[16 * 32];
   __shared__ uint16_t s_invp[1024];
@@ -163,22 +152,7 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
     __syncthreads();
     // H_l (unnormalised; the 1/32 is applied by the readers of W^T)
     float e[64];
-    {
-      float *b = s + ri * L::kStride + rc;
-#pragma unroll
-      for (int k = 0; k < 64; ++k) e[k] = b[16 * k + (k >> 2)];
-      fwht_regs_t<64>(e);
-#pragma unroll
-      for (int k = 0; k < 64; ++k) b[16 * k + (k >> 2)] = e[k];
-    }
-    __syncthreads();
-    {
-      const float *b = s + ri * L::kStride + 65 * rc;
-#pragma unroll
-      for (int m = 0; m < 64; ++m) e[m] = b[m];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) fwht_regs_t<16>(e + 16 * g);
-    }
+    fwht1024_rows16_r(s, e);
     float *dst = w + cur.v * ld.np + cur.t * lo_len + (int64_t)(64 * rc) * 1024 + cur.p0 + ri;
 #pragma unroll
     for (int m = 0; m < 64; ++m) dst[(int64_t)m * 1024] = e[m];

@@ -220,4 +220,40 @@ __device__ __forceinline__ void fwht1024_lds_regs(float *lds, float (&e)[1024 * 
   fwht1024_lds_pass2<NV>(lds);
 }
 
+// LDS block of 16 rows of 1024 for the row kernels: one pad word per 64 floats
+// and a row stride of 2 banks modulo 32.  The transform runs with the row
+// index fastest (thread (i = tid % 16, c = tid / 16)): pass 1 holds columns
+// c + 16 k, pass 2 the 64 consecutive columns 64 c .. 64 c + 63, so in both
+// passes a half-wave touches 32 distinct banks, and after pass 2 the 16 lanes
+// of a column write its 16 consecutive p (64 bytes) straight from registers.
+struct Lds1024R {
+  static constexpr int kStride = 1058;
+  static constexpr int kFloats = 16 * kStride;
+  static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> 6); }
+};
+
+
+// Unnormalised 1024-point transform of the 16 rows of an Lds1024R block that
+// the caller has filled and synchronised.  On return thread (ri = tid % 16,
+// rc = tid / 16) holds columns 64 rc + m of row ri in e[m]; the block holds
+// pass-1 data and may be refilled after the caller's next barrier.
+__device__ __forceinline__ void fwht1024_rows16_r(float *s, float (&e)[64]) {
+  using L = Lds1024R;
+  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;
+  {
+    float *b = s + ri * L::kStride + rc;
+#pragma unroll
+    for (int k = 0; k < 64; ++k) e[k] = b[16 * k + (k >> 2)];
+    fwht_regs_t<64>(e);
+#pragma unroll
+    for (int k = 0; k < 64; ++k) b[16 * k + (k >> 2)] = e[k];
+  }
+  __syncthreads();
+  const float *b = s + ri * L::kStride + 65 * rc;
+#pragma unroll
+  for (int m = 0; m < 64; ++m) e[m] = b[m];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) fwht_regs_t<16>(e + 16 * g);
+}
+
 }  // namespace sk

@@ -102,6 +102,14 @@ void launch_gauss_table(const sk_sketch *s, float *gtab, hipStream_t st);
 void launch_debug_stream(const sk_sketch *s, int layer, int stream_id, uint64_t start, uint64_t count, uint64_t aux,
                          void *dout, hipStream_t st);
 
+// FFD with D = 2^20: rows/cols kernels over transposed intermediates.
+// phases: bit 0 = the kernel that reads the input, bit 1 = the rest.
+bool ffd_large_path(const sk_sketch *s);
+void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                       float *out, bool accumulate, int phases, hipStream_t st);
+void run_ffd_large_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
+                     int out_dtype, const float *theta0, int phases, hipStream_t st);
+
 // ---- QK ----
 void launch_qk_factors(const sk_sketch *s, hipStream_t st);
 // stages: bit 0 = T = X B^T (reads the gradients), bit 1 = out (+)= A T

@@ -107,6 +107,27 @@ def test_transpose_parity(kind, case, dev):
         assert rel_err(o.cpu().numpy(), r) < TOL_F32
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ffd_large_D(dtype, dev):
+    """FFD with D = 2^20 (rows/cols kernels over transposed intermediates):
+    forward over three blocks with a ragged tail and a one-block layer, and
+    theta0 + S^T z with fp32 and bf16 outputs."""
+    shapes, D, seed = [(1, 2 ** 21 + 5), (3, 1000)], 2 ** 20, 41
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xs = rand_inputs(shapes, 3, seed, dtype=tdt)
+    s = sk("ffd", shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("ffd", shapes, D, seed, [oracle_in(x)[0] for x in xs], dtype=dtype)
+    assert rel_err(y, ref) < TOL_F32
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((2, D), generator=g)
+    th = [torch.randn(sh[0] * sh[1], generator=g) * 0.02 for sh in shapes]
+    outs = s.apply_T(z.to(dev), out_dtype=tdt, theta0=[t.to(dev) for t in th])
+    refs = O.apply_T("ffd", shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.float().cpu().numpy(), r) < (TOL_BF16 if dtype == "bf16" else TOL_F32)
+
+
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
 def test_forward_parity_bf16(kind, dev):
     shapes, D = CASES[3]
