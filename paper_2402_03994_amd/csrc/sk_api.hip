@@ -70,6 +70,8 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_smp);
   f(s->d_qka);
   f(s->d_qkb);
+  f(s->d_qkah);
+  f(s->d_qkbf);
   f(s->d_mtab);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
@@ -122,8 +124,8 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
         else
           b = 2 * ffd_live_blocks(s, l) * s->D * 4;
         break;
-      case SK_QK:
-        b = (int64_t)ld.m * ld.db * 4;
+      case SK_QK:  // T = X B^T (m x dB) or, A first, U = A X (dA x n)
+        b = std::max((int64_t)ld.m * ld.db, (int64_t)ld.da * ld.nc) * 4;
         break;
     }
     need = std::max(need, b);
@@ -369,6 +371,8 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
   SK_TRY(alloc((void **)&s->d_qka, sizeof(float) * fac_a));
   SK_TRY(alloc((void **)&s->d_qkb, sizeof(uint16_t) * 2 * fac_b));
+  SK_TRY(alloc((void **)&s->d_qkah, sizeof(uint16_t) * 2 * fac_a));
+  SK_TRY(alloc((void **)&s->d_qkbf, sizeof(float) * fac_b));
 
   auto h2d = [&](void *d, const void *h, size_t bytes) -> int {
     if (bytes == 0) return SK_OK;

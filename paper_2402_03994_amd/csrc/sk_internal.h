@@ -84,6 +84,8 @@ struct sk_sketch {
   uint32_t *d_fjl_smp = nullptr;   // sample ids sorted by (position, id)
   // QK
   float *d_qka = nullptr;       // A factors, fp32
+  uint16_t *d_qkah = nullptr;   // A factors as bf16 hi terms, then bf16 lo terms (A-first contraction)
+  float *d_qkbf = nullptr;      // B factors, fp32 (second stage of the A-first contraction)
   uint16_t *d_qkb = nullptr;    // B factors as bf16 hi terms, then bf16 lo terms (hi + lo ~ fp32 B)
   int64_t qk_a_elems = 0, qk_b_elems = 0;
   // AFFD: precomputed M = H_TT (signs . G) per transposed-path layer

@@ -6,6 +6,8 @@
 // and lo = bf16(B - hi) (both rounded to nearest even), so that the bf16
 // MFMA contraction X B^T = X hi^T + X lo^T sees B to 16 mantissa bits.
 // Products accumulate in fp32.
+#include <algorithm>
+
 #include "sk_launch.h"
 
 namespace sk {
@@ -17,17 +19,25 @@ __device__ __forceinline__ uint16_t qk_f2bf(float f) {
 }
 __device__ __forceinline__ float qk_bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-__global__ void k_qk_factor_a(float *__restrict__ dst, int64_t count, uint32_t layer, float scale, Key key) {
+// A in fp32 and as bf16 hi / lo terms (for the contraction that applies A first)
+__global__ void k_qk_factor_a(float *__restrict__ dst, uint16_t *__restrict__ hi, uint16_t *__restrict__ lo,
+                              int64_t count, uint32_t layer, float scale, Key key) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= count) return;
-  dst[i] = gauss((uint64_t)i, layer, ST_QKA, key) * scale;
+  const float g = gauss((uint64_t)i, layer, ST_QKA, key) * scale;
+  dst[i] = g;
+  const uint16_t h = qk_f2bf(g);
+  hi[i] = h;
+  lo[i] = qk_f2bf(g - qk_bf2f(h));
 }
 
-__global__ void k_qk_factor_b(uint16_t *__restrict__ hi, uint16_t *__restrict__ lo, int64_t count, uint32_t layer,
-                              float scale, Key key) {
+// B in fp32 and as bf16 hi / lo terms
+__global__ void k_qk_factor_b(float *__restrict__ dst, uint16_t *__restrict__ hi, uint16_t *__restrict__ lo,
+                              int64_t count, uint32_t layer, float scale, Key key) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= count) return;
   const float g = gauss((uint64_t)i, layer, ST_QKB, key) * scale;
+  dst[i] = g;
   const uint16_t h = qk_f2bf(g);
   hi[i] = h;
   lo[i] = qk_f2bf(g - qk_bf2f(h));
@@ -36,10 +46,11 @@ __global__ void k_qk_factor_b(uint16_t *__restrict__ hi, uint16_t *__restrict__ 
 void launch_qk_factors(const sk_sketch *s, hipStream_t st) {
   for (const LayerDesc &ld : s->layers) {
     const int64_t na = (int64_t)ld.da * ld.m, nb = (int64_t)ld.db * ld.nc;
-    hipLaunchKernelGGL(k_qk_factor_a, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, s->d_qka + ld.fa_off, na,
-                       (uint32_t)ld.layer_id, (float)(1.0 / sqrt((double)ld.da)), s->key);
-    hipLaunchKernelGGL(k_qk_factor_b, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, st, s->d_qkb + ld.fb_off,
-                       s->d_qkb + s->qk_b_elems + ld.fb_off, nb, (uint32_t)ld.layer_id,
+    hipLaunchKernelGGL(k_qk_factor_a, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, s->d_qka + ld.fa_off,
+                       s->d_qkah + ld.fa_off, s->d_qkah + s->qk_a_elems + ld.fa_off, na, (uint32_t)ld.layer_id,
+                       (float)(1.0 / sqrt((double)ld.da)), s->key);
+    hipLaunchKernelGGL(k_qk_factor_b, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, st, s->d_qkbf + ld.fb_off,
+                       s->d_qkb + ld.fb_off, s->d_qkb + s->qk_b_elems + ld.fb_off, nb, (uint32_t)ld.layer_id,
                        (float)(1.0 / sqrt((double)ld.db)), s->key);
   }
   (void)hipGetLastError();
@@ -47,7 +58,7 @@ void launch_qk_factors(const sk_sketch *s, hipStream_t st) {
 
 int64_t qk_workspace_elems(const sk_sketch *s, int layer, int64_t bc) {
   const LayerDesc &ld = s->layers[layer];
-  return bc * (int64_t)ld.m * ld.db;
+  return bc * std::max((int64_t)ld.m * ld.db, (int64_t)ld.da * ld.nc);
 }
 
 // T[v][i][c] = sum_j X[v][i][j] B[c][j]
@@ -160,20 +171,106 @@ __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, c
     }
 }
 
+// A first (dA < dB, so A X costs fewer products than X B^T): stage 1
+// U[v][a][j] = sum_i A[a][i] X[v][i][j] on v_mfma_f32_16x16x32_bf16 with A as
+// bf16 hi + lo.  X's contiguous index j is the output column, so each lane
+// reads 8 bytes (columns j0 .. j0 + 3) of 8 consecutive rows and packs the
+// 16-bit halves into the K fragments of four MFMAs (one per column), i.e. four
+// 16-column sets interleaved with stride 4.  Each step takes 64 rows; the
+// next step's rows load during the current MFMAs.  Stage 2 is k_qk_s2 with U
+// per vector and B in fp32.
+template <int MT>
+__global__ __launch_bounds__(256) void k_qk_s1a(const uint16_t *__restrict__ x, const uint16_t *__restrict__ Ah,
+                                                const uint16_t *__restrict__ Al, int64_t m, int64_t n,
+                                                int64_t b_begin, float *__restrict__ u) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int64_t v = blockIdx.y;
+  const int64_t j0 = (int64_t)blockIdx.x * 256 + wave * 64 + 4 * li;  // this lane's four columns
+  const uint16_t *xc = x + (b_begin + v) * m * n + j0 + (int64_t)(g * 8) * n;
+  const uint16_t *ah = Ah + (int64_t)li * m + g * 8;
+  const uint16_t *al = Al + (int64_t)li * m + g * 8;
+  floatx4 acc[MT][4];
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[t][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint2 w[2][8];  // rows k0 + 32 h + 8 g + r
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 8; ++r) w[h][r] = *(const uint2 *)(xc + (k0 + 32 * h + r) * n);
+  };
+  fetch(0);
+  for (int64_t k0 = 0; k0 < m; k0 += 64) {
+    uint2 c[2][8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 8; ++r) c[h][r] = w[h][r];
+    if (k0 + 64 < m) fetch(k0 + 64);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // K fragments (rows k0 + 32 h + 8 g .. + 7) of columns j0 + q
+      Pack8 f[4];
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        uint32_t e[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) e[r] = p ? c[h][r].y : c[h][r].x;
+        f[2 * p].u = make_uint4(__builtin_amdgcn_perm(e[1], e[0], 0x05040100u),
+                                __builtin_amdgcn_perm(e[3], e[2], 0x05040100u),
+                                __builtin_amdgcn_perm(e[5], e[4], 0x05040100u),
+                                __builtin_amdgcn_perm(e[7], e[6], 0x05040100u));
+        f[2 * p + 1].u = make_uint4(__builtin_amdgcn_perm(e[1], e[0], 0x07060302u),
+                                    __builtin_amdgcn_perm(e[3], e[2], 0x07060302u),
+                                    __builtin_amdgcn_perm(e[5], e[4], 0x07060302u),
+                                    __builtin_amdgcn_perm(e[7], e[6], 0x07060302u));
+      }
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        Pack8 hv, lv;
+        hv.u = *(const uint4 *)(ah + (int64_t)(t * 16) * m + k0 + 32 * h);
+        lv.u = *(const uint4 *)(al + (int64_t)(t * 16) * m + k0 + 32 * h);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hv.v, f[q].v, acc[t][q], 0, 0, 0);
+          acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lv.v, f[q].v, acc[t][q], 0, 0, 0);
+        }
+      }
+    }
+  }
+  // D layout: lane holds rows 4 g .. 4 g + 3 (a) of its column in each set
+  float *ub = u + v * (int64_t)(MT * 16) * n + j0;
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t a = t * 16 + g * 4 + i;
+      *(float4 *)(ub + a * n) = make_float4(acc[t][0][i], acc[t][1][i], acc[t][2][i], acc[t][3][i]);
+    }
+}
+
+bool qk_afirst_ok(const LayerDesc &ld, int dtype) {
+  return dtype == SK_BF16 && ld.da < ld.db && ld.da % 16 == 0 && ld.da <= 64 && ld.db % 16 == 0 && ld.m % 64 == 0 &&
+         ld.nc % 256 == 0;
+}
+
 // One workgroup (4 waves) per (vector, 16 x 16 output tile); the waves split
 // K = m into four ranges, each with four independent accumulators, and the
 // sixteen partial tiles are added in a fixed order through LDS.
-__global__ __launch_bounds__(256) void k_qk_s2(const float *__restrict__ A, const float *__restrict__ tt, int64_t m,
-                                               int da, int db, int64_t D, int64_t col, int64_t b_begin,
-                                               float *__restrict__ out, int accumulate) {
+__global__ __launch_bounds__(256) void k_qk_s2(const float *__restrict__ A, int64_t a_vs, const float *__restrict__ tt,
+                                               int64_t t_vs, int64_t m, int da, int db, int64_t D, int64_t col,
+                                               int64_t b_begin, float *__restrict__ out, int accumulate) {
   __shared__ float red[4][64][4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntb = db / 16;
   const int ta = blockIdx.x / ntb, tb = blockIdx.x - (blockIdx.x / ntb) * ntb;
   const int64_t v = blockIdx.y;
   const int li = lane & 15, g = lane >> 4;
-  const float *ar = A + (int64_t)(ta * 16 + li) * m + g * 4;
-  const float *tr = tt + (v * db + tb * 16 + li) * m + g * 4;
+  const float *ar = A + v * a_vs + (int64_t)(ta * 16 + li) * m + g * 4;
+  const float *tr = tt + v * t_vs + (int64_t)(tb * 16 + li) * m + g * 4;
   const int64_t per = ((m + 63) / 64) * 16;  // K range per wave, a multiple of 16
   const int64_t kb = wave * per, ke = kb + per < m ? kb + per : m;
   floatx4 acc[4];
@@ -241,6 +338,30 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
   const LayerDesc &ld = s->layers[layer];
   const float *A = s->d_qka + ld.fa_off;
   const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
+  if (qk_afirst_ok(ld, dtype)) {
+    if (stages & 1) {
+      const uint16_t *Ah = s->d_qkah + ld.fa_off, *Al = s->d_qkah + s->qk_a_elems + ld.fa_off;
+      const dim3 g1((unsigned)(ld.nc / 256), (unsigned)bc);
+      switch (ld.da / 16) {
+        case 1: hipLaunchKernelGGL(k_qk_s1a<1>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                                   (int64_t)ld.nc, b_begin, t_ws); break;
+        case 2: hipLaunchKernelGGL(k_qk_s1a<2>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                                   (int64_t)ld.nc, b_begin, t_ws); break;
+        case 3: hipLaunchKernelGGL(k_qk_s1a<3>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                                   (int64_t)ld.nc, b_begin, t_ws); break;
+        default: hipLaunchKernelGGL(k_qk_s1a<4>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                                    (int64_t)ld.nc, b_begin, t_ws); break;
+      }
+    }
+    if (stages & 2) {
+      // Y[v][a][c] = sum_j U[v][a][j] B[c][j]
+      dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
+      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, t_ws, (int64_t)ld.da * ld.nc, s->d_qkbf + ld.fb_off,
+                         (int64_t)0, (int64_t)ld.nc, ld.da, ld.db, s->D, ld.qk_col, b_begin, out, (int)accumulate);
+    }
+    (void)hipGetLastError();
+    return;
+  }
   if (qk_mfma_ok(ld, dtype)) {
     const int64_t rows = bc * (int64_t)ld.m;
     dim3 g1((unsigned)((rows + kQkRows - 1) / kQkRows));
@@ -259,8 +380,8 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
     }
     if (stages & 2) {
       dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
-      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, t_ws, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col,
-                         b_begin, out, (int)accumulate);
+      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, (int64_t)0, t_ws, (int64_t)ld.db * ld.m, (int64_t)ld.m,
+                         ld.da, ld.db, s->D, ld.qk_col, b_begin, out, (int)accumulate);
     }
     (void)hipGetLastError();
     return;

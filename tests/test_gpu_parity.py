@@ -199,7 +199,10 @@ def test_debug_streams_bit_exact(dev):
 @pytest.mark.parametrize("shapes,D", [([(40, 70, 4, 5), (64, 33, 8, 2), (1, 300, 1, 9)], 45),
                                       ([(256, 512, 32, 16), (300, 200, 16, 32)], 32 * 16 * 2),
                                       ([(2048, 2048, 32, 16), (512, 1024, 32, 128), (1024, 256, 128, 32),
-                                        (208, 384, 64, 48)], 512 + 4096 + 4096 + 3072)])
+                                        (208, 384, 64, 48)], 512 + 4096 + 4096 + 3072),
+                                      # dA < dB: the A-first contraction, one to four 16-row tiles of A
+                                      ([(64, 512, 48, 64), (128, 256, 16, 32), (192, 768, 64, 80)],
+                                       48 * 64 + 16 * 32 + 64 * 80)])
 def test_qk_parity(shapes, D, dev):
     seed = 21
     xs = rand_inputs(shapes, 3, seed, dtype=torch.bfloat16, scale=0.01)
