@@ -151,10 +151,11 @@ __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, c
         vh.u = *(const uint4 *)(bh + cc * 16);
         vl.u = *(const uint4 *)(bl + cc * 16);
 #pragma unroll
-        for (int mr = 0; mr < kQkMR; ++mr) {
+        for (int mr = 0; mr < kQkMR; ++mr)
           acc[mr][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mr][cc].v, vh.v, acc[mr][t], 0, 0, 0);
+#pragma unroll
+        for (int mr = 0; mr < kQkMR; ++mr)
           acc[mr][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mr][cc].v, vl.v, acc[mr][t], 0, 0, 0);
-        }
       }
     }
   }
@@ -234,10 +235,9 @@ __global__ __launch_bounds__(256) void k_qk_s1a(const uint16_t *__restrict__ x, 
         hv.u = *(const uint4 *)(ah + (int64_t)(t * 16) * m + k0 + 32 * h);
         lv.u = *(const uint4 *)(al + (int64_t)(t * 16) * m + k0 + 32 * h);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hv.v, f[q].v, acc[t][q], 0, 0, 0);
-          acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lv.v, f[q].v, acc[t][q], 0, 0, 0);
-        }
+        for (int q = 0; q < 4; ++q) acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hv.v, f[q].v, acc[t][q], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lv.v, f[q].v, acc[t][q], 0, 0, 0);
       }
     }
   }
@@ -257,63 +257,131 @@ bool qk_afirst_ok(const LayerDesc &ld, int dtype) {
          ld.nc % 256 == 0;
 }
 
-// One workgroup (4 waves) per (vector, 16 x 16 output tile); the waves split
-// K = m into four ranges, each with four independent accumulators, and the
-// sixteen partial tiles are added in a fixed order through LDS.
-__global__ __launch_bounds__(256) void k_qk_s2(const float *__restrict__ A, int64_t a_vs, const float *__restrict__ tt,
-                                               int64_t t_vs, int64_t m, int da, int db, int64_t D, int64_t col,
-                                               int64_t b_begin, float *__restrict__ out, int accumulate) {
-  __shared__ float red[4][64][4];
+// Stage 2: Y[v][a][c] = sum_k P[a][k] Q[c][k] (P: dA rows, Q: dB rows, both
+// with the contraction index contiguous; each may be per vector) on
+// v_mfma_f32_16x16x4f32.  One workgroup per (vector, block of TA x TB output
+// tiles of 16 x 16): each wave keeps the TA x TB accumulators of the block over
+// a quarter of K, so every P and Q row is read once per workgroup, and the four
+// partial blocks are added in a fixed order through LDS.
+template <int TA, int TB>
+__global__ __launch_bounds__(256) void k_qk_s2(const float *__restrict__ P, int64_t p_vs,
+                                               const float *__restrict__ Q, int64_t q_vs, int64_t K, int da, int db,
+                                               int64_t D, int64_t col, int64_t b_begin, float *__restrict__ out,
+                                               int accumulate) {
+  __shared__ float red[4][TA * TB][64][4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ntb = db / 16;
-  const int ta = blockIdx.x / ntb, tb = blockIdx.x - (blockIdx.x / ntb) * ntb;
+  const int nbb = db / (16 * TB);
+  const int ba = blockIdx.x / nbb, bb = blockIdx.x - (blockIdx.x / nbb) * nbb;
   const int64_t v = blockIdx.y;
   const int li = lane & 15, g = lane >> 4;
-  const float *ar = A + v * a_vs + (int64_t)(ta * 16 + li) * m + g * 4;
-  const float *tr = tt + v * t_vs + (int64_t)(tb * 16 + li) * m + g * 4;
-  const int64_t per = ((m + 63) / 64) * 16;  // K range per wave, a multiple of 16
-  const int64_t kb = wave * per, ke = kb + per < m ? kb + per : m;
-  floatx4 acc[4];
+  const float *pr = P + v * p_vs + (int64_t)(ba * TA * 16 + li) * K + g * 4;
+  const float *qr = Q + v * q_vs + (int64_t)(bb * TB * 16 + li) * K + g * 4;
+  const int64_t per = ((K + 63) / 64) * 16;  // K range per wave, a multiple of 16
+  const int64_t kb = wave * per, ke = kb + per < K ? kb + per : K;
+  floatx4 acc[TA][TB];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) acc[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // U steps of 16 per iteration: all of an iteration's loads are in flight together
+  constexpr int U = TA * TB >= 8 ? 2 : 4;
   int64_t k0 = kb;
-  for (; k0 + 64 <= ke; k0 += 64) {
-    float4 av[4], tv[4];
+  for (; k0 + 16 * U <= ke; k0 += 16 * U) {
+    float4 pv[U][TA], qv[U][TB];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      av[u] = *(const float4 *)(ar + k0 + 16 * u);
-      tv[u] = *(const float4 *)(tr + k0 + 16 * u);
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int i = 0; i < TA; ++i) pv[u][i] = *(const float4 *)(pr + (int64_t)(i * 16) * K + k0 + 16 * u);
+#pragma unroll
+      for (int j = 0; j < TB; ++j) qv[u][j] = *(const float4 *)(qr + (int64_t)(j * 16) * K + k0 + 16 * u);
     }
+    // consecutive MFMAs go to different accumulators so none waits on the last
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].x, tv[u].x, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].y, tv[u].y, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].z, tv[u].z, acc[u], 0, 0, 0);
-      acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u].w, tv[u].w, acc[u], 0, 0, 0);
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[u][i].x, qv[u][j].x, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[u][i].y, qv[u][j].y, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[u][i].z, qv[u][j].z, acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[u][i].w, qv[u][j].w, acc[i][j], 0, 0, 0);
     }
   }
-  for (; k0 < ke; k0 += 16) {  // remaining 16-wide steps, ragged at m
+  for (; k0 + 16 <= ke; k0 += 16) {
+    float4 pv[TA], qv[TB];
+#pragma unroll
+    for (int i = 0; i < TA; ++i) pv[i] = *(const float4 *)(pr + (int64_t)(i * 16) * K + k0);
+#pragma unroll
+    for (int j = 0; j < TB; ++j) qv[j] = *(const float4 *)(qr + (int64_t)(j * 16) * K + k0);
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int j = 0; j < TB; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].x, qv[j].x, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].y, qv[j].y, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].z, qv[j].z, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i].w, qv[j].w, acc[i][j], 0, 0, 0);
+      }
+  }
+  if (k0 < ke) {  // ragged end of K (K not a multiple of 16)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool ok = k0 + g * 4 + e < ke;
-      const float a = ok ? ar[k0 + e] : 0.0f;
-      const float t = ok ? tr[k0 + e] : 0.0f;
-      acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, t, acc[0], 0, 0, 0);
+      float pe[TA], qe[TB];
+#pragma unroll
+      for (int i = 0; i < TA; ++i) pe[i] = ok ? pr[(int64_t)(i * 16) * K + k0 + e] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < TB; ++j) qe[j] = ok ? qr[(int64_t)(j * 16) * K + k0 + e] : 0.0f;
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pe[i], qe[j], acc[i][j], 0, 0, 0);
     }
   }
-  const floatx4 sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) red[wave][lane][i] = sum[i];
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[wave][i * TB + j][lane][q] = acc[i][j][q];
   __syncthreads();
-  if (wave == 0) {
+  // lane (li, g) of tile (i, j): rows 4 g .. 4 g + 3 of column li
+  for (int e = threadIdx.x; e < TA * TB * 64; e += 256) {
+    const int tile = e >> 6, ln = e & 63;
+    const int i = tile / TB, j = tile - (tile / TB) * TB;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float y = ((red[0][lane][i] + red[1][lane][i]) + red[2][lane][i]) + red[3][lane][i];
-      const int a = ta * 16 + g * 4 + i, c = tb * 16 + li;
+    for (int q = 0; q < 4; ++q) {
+      const float y = ((red[0][tile][ln][q] + red[1][tile][ln][q]) + red[2][tile][ln][q]) + red[3][tile][ln][q];
+      const int a = (ba * TA + i) * 16 + (ln >> 4) * 4 + q, c = (bb * TB + j) * 16 + (ln & 15);
       float *o = out + (b_begin + v) * D + col + (int64_t)a * db + c;
       *o = accumulate ? *o + y : y;
     }
   }
+}
+
+// Tiles per block along a side of n16 tiles: the largest of 4, 2, 1 dividing it.
+static int qk_block_tiles(int n16) { return n16 % 4 == 0 ? 4 : n16 % 2 == 0 ? 2 : 1; }
+
+static void launch_qk_s2(const float *P, int64_t p_vs, const float *Q, int64_t q_vs, int64_t K, int da, int db,
+                         int64_t D, int64_t col, int64_t b_begin, int64_t bc, float *out, bool accumulate,
+                         hipStream_t st) {
+  const int ta = qk_block_tiles(da / 16), tb = qk_block_tiles(db / 16);
+  const dim3 grid((unsigned)((da / (16 * ta)) * (db / (16 * tb))), (unsigned)bc);
+#define SK_S2(A, B)                                                                                      \
+  if (ta == A && tb == B)                                                                                \
+  hipLaunchKernelGGL((k_qk_s2<A, B>), grid, dim3(256), 0, st, P, p_vs, Q, q_vs, K, da, db, D, col, b_begin, out, \
+                     (int)accumulate)
+  SK_S2(1, 1); SK_S2(1, 2); SK_S2(1, 4); SK_S2(2, 1); SK_S2(2, 2); SK_S2(2, 4); SK_S2(4, 1); SK_S2(4, 2); SK_S2(4, 4);
+#undef SK_S2
 }
 
 bool qk_mfma_ok(const LayerDesc &ld, int dtype) {
@@ -355,9 +423,8 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
     }
     if (stages & 2) {
       // Y[v][a][c] = sum_j U[v][a][j] B[c][j]
-      dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
-      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, t_ws, (int64_t)ld.da * ld.nc, s->d_qkbf + ld.fb_off,
-                         (int64_t)0, (int64_t)ld.nc, ld.da, ld.db, s->D, ld.qk_col, b_begin, out, (int)accumulate);
+      launch_qk_s2(t_ws, (int64_t)ld.da * ld.nc, s->d_qkbf + ld.fb_off, 0, (int64_t)ld.nc, ld.da, ld.db, s->D,
+                   ld.qk_col, b_begin, bc, out, accumulate, st);
     }
     (void)hipGetLastError();
     return;
@@ -379,9 +446,8 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
 #undef SK_S1
     }
     if (stages & 2) {
-      dim3 g2((unsigned)((ld.da / 16) * (ld.db / 16)), (unsigned)bc);
-      hipLaunchKernelGGL(k_qk_s2, g2, dim3(256), 0, st, A, (int64_t)0, t_ws, (int64_t)ld.db * ld.m, (int64_t)ld.m,
-                         ld.da, ld.db, s->D, ld.qk_col, b_begin, out, (int)accumulate);
+      launch_qk_s2(A, 0, t_ws, (int64_t)ld.db * ld.m, (int64_t)ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, bc, out,
+                   accumulate, st);
     }
     (void)hipGetLastError();
     return;
