@@ -39,7 +39,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 # kernel launched by each single-kernel profile class (the rocprofv3 name)
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
-             "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffd_copy_blocks", "fjl:prolog": "k_fjl_prolog"}
+             "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
+             "fjl:prolog": "k_fjl_prolog"}
 
 
 def source_hash() -> str:

@@ -616,7 +616,7 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
           } else if (ffd_large_path(s)) {
             SK_PROF(SK_PROF_PROLOG, bc * s->layers[l].n * esz,
                     run_ffd_large_fwd(s, l, grads[l - l0], dtype, b0, bc, out, accumulate || l > l0, 1, st));
-            SK_PROF(SK_PROF_FFD, (l == l1 - 1 ? bc * s->D * 4 : 0),
+            SK_PROF(SK_PROF_FFD, 0,
                     run_ffd_large_fwd(s, l, grads[l - l0], dtype, b0, bc, out, accumulate || l > l0, 2, st));
           } else {
             const int64_t nlive = ffd_live_blocks(s, l);
@@ -700,7 +700,8 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           break;
         case SK_FFD:
           if (lgD <= kFfdSmallMax) {
-            SK_PROF(SK_PROF_FFD, obytes + bc * s->D * 4, launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st));
+            SK_PROF(SK_PROF_GATHER, obytes + bc * s->D * 4,
+                    launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st));
           } else if (ffd_large_path(s)) {
             SK_PROF(SK_PROF_FFD, 0, run_ffd_large_T(s, l, z, b0, bc, o, out_dtype, th, 1, st));
             SK_PROF(SK_PROF_GATHER, obytes + bc * s->D * 4, run_ffd_large_T(s, l, z, b0, bc, o, out_dtype, th, 2, st));
