@@ -10,13 +10,17 @@
 // transform along p runs over contiguous memory:
 //   A  16 destination rows per workgroup: load, sign, pi1 on the columns,
 //      H_l, write 16 consecutive p of every column l            -> W^T
-//   B  (TT > 8 only) H_p along each W^T row                    -> W^T
-//   C  per column l: H_p (TT <= 8), H_TT in registers, x g, signed sum onto
-//      h*, H_p again, keep the rows pi2_p(a), a < R             -> G^T[l][a]
-//   E  H_l along each row a of G, gather pi2_l(b), scale, add  -> out
-// Three passes over the data (read x, write W^T, read W^T) for TT <= 8.
+//   C  per column l, with the stored M = H_TT (s . g): for each live slab
+//      H_p and F += M[t] x; then H_p again, keep the rows pi2_p(a), a < R
+//                                                               -> G^T[l][a]
+//   E  for all the layers of a call at once: H_l along each row a of G,
+//      gather pi2_l(b), scale, sum, write                     -> out
+// Three passes over the data: read x, write W^T, read W^T.  Without the
+// stored tables C regenerates g (TT <= 8: H_TT in registers; TT > 8: phase B
+// applies H_p along each W^T row first).
 #include <algorithm>
 #include <cstdlib>
+#include <cmath>
 
 #include "sk_kcommon.h"
 #include "sk_launch.h"
@@ -52,47 +56,93 @@ __device__ __forceinline__ void masks_t(const LayerDesc &ld, const uint16_t *pta
 // (vector, slab t, 16 destination rows p0..p0+15).  Workgroup b runs on XCD
 // b mod 8; the tile map gives each XCD a contiguous range per sweep, so one
 // XCD writes all 64 tiles of a slab and its W^T lines are completed in one L2.
-// The 16 row loads of the next tile are issued before the transform of the
+// The row loads of the next tile are issued before the transform of the
 // current one; the row tables live in LDS so no load waits on another.
 namespace {
 struct RowTile {
   int64_t v, t, p0;
+  int sl;  // index of slab t among the group's live slabs
 };
 
-__device__ __forceinline__ RowTile decode_tile(int64_t tile, int64_t per_v, uint64_t live) {
+// Tiles of one vector: 64 per live slab of the group (live slabs s_first ..
+// s_first + nsl - 1 in increasing t).
+__device__ __forceinline__ RowTile decode_tile(int64_t tile, int64_t per_v, uint64_t live, int s_first) {
   RowTile r;
   r.v = tile / per_v;
   const int64_t rem = tile - r.v * per_v;
-  const int sl = (int)(rem >> 6);
+  r.sl = (int)(rem >> 6);
   r.p0 = (rem & 63) * 16;
   uint64_t m = live;
-  for (int i = 0; i < sl; ++i) m &= m - 1;
+  for (int i = 0; i < s_first + r.sl; ++i) m &= m - 1;
   r.t = __builtin_ctzll(m);
   return r;
 }
 
-template <bool BF16, bool VEC>
-__device__ __forceinline__ void load_rows16(const LayerDesc &ld, const uint16_t *s_invp, int64_t sslab, int64_t p0,
-                                            const void *x, int64_t xrow, int col0, float (&val)[16][4]) {
+// Rows 2k + half (k < 8) of a tile: thread column col0..col0+3.  General
+// form: any alignment and length.
+template <bool BF16>
+__device__ __forceinline__ void load_rows8(const LayerDesc &ld, const uint16_t *s_invp, int64_t sslab, int64_t p0,
+                                           int half, const void *x, int64_t xrow, int col0, float (&val)[8][4]) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int64_t h = sslab * 1024 + s_invp[p0 + i];
+  for (int k = 0; k < 8; ++k) {
+    const int64_t h = sslab * 1024 + s_invp[p0 + 2 * k + half];
     const int64_t j0 = h * 1024 + col0;
     const int64_t lim = ld.n - j0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) val[i][q] = 0.0f;
-    if (h < ld.rows_live && lim > 0) load4<BF16, VEC>(x, xrow * ld.n + j0, lim, val[i]);
+    for (int q = 0; q < 4; ++q) val[k][q] = 0.0f;
+    if (h < ld.rows_live && lim > 0) load4<BF16, false>(x, xrow * ld.n + j0, lim, val[k]);
+  }
+}
+
+// Same rows through a buffer resource over the vector's n elements (n a
+// multiple of 4, n elt < 2^31): the row index is uniform over the wave, so
+// rows without data are skipped by a scalar branch and the end of the last
+// row is zero-filled by the hardware range check (the whole byte offset is in
+// the vector operand, which the check covers).
+template <bool BF16>
+__device__ __forceinline__ void load_rows8_buf(const LayerDesc &ld, const uint16_t *s_invp, int sslab, int p0,
+                                               int half, __amdgpu_buffer_rsrc_t rs, int voff, float (&val)[8][4]) {
+  typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+  typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int h = __builtin_amdgcn_readfirstlane(sslab * 1024 + (int)s_invp[p0 + 2 * k + half]);
+    if (h < ld.rows_live) {
+      if (BF16) {
+        const u2 u = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + h * 2048, 0, 0);
+        val[k][0] = __uint_as_float(u.x << 16);
+        val[k][1] = __uint_as_float(u.x & 0xFFFF0000u);
+        val[k][2] = __uint_as_float(u.y << 16);
+        val[k][3] = __uint_as_float(u.y & 0xFFFF0000u);
+      } else {
+        const u4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + h * 4096, 0, 0);
+        val[k][0] = __uint_as_float(u.x);
+        val[k][1] = __uint_as_float(u.y);
+        val[k][2] = __uint_as_float(u.z);
+        val[k][3] = __uint_as_float(u.w);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) val[k][q] = 0.0f;
+    }
   }
 }
 
 }  // namespace
 
+// 512 threads per workgroup: thread tid loads columns col0 = 4 (tid % 256)
+// .. col0 + 3 of tile rows 2k + tid / 256 and ends holding 32 columns of one
+// row after the transform; W^T is written through a buffer resource whose
+// offsets are scalar constants, 16 threads x 4 bytes = 64 bytes per column.
+// W^T of the tile's slab with group index sl (slab t) of vector v starts at
+// w + v vstride + (compact ? sl : t) 2^20.
 template <bool BF16, bool VEC>
-__global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict__ layers,
+__global__ __launch_bounds__(512) void k_affdT_rows(const LayerDesc *__restrict__ layers,
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const void *__restrict__ x, int64_t b_begin, int64_t bc,
-                                                    float *__restrict__ w, Key key) {
-  using L = Lds1024R;
+                                                    float *__restrict__ w, int s_first, int nsl, int64_t vstride,
+                                                    int compact, Key key) {
+  using L = Lds1024R32;
   __shared__ __align__(16) float s[L::kFloats];
   __shared__ __align__(16) uint32_t sg[16 * 32];
   __shared__ uint16_t s_invp[1024];
@@ -100,32 +150,43 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
   const LayerDesc &ld = layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const uint16_t *invp = ptab + ld.poff[0][1][ld.K - 2];
-  for (int e = threadIdx.x; e < 1024; e += 256) s_invp[e] = invp[e];
+  for (int e = threadIdx.x; e < 1024; e += 512) s_invp[e] = invp[e];
   if (threadIdx.x < TT) s_slab[threadIdx.x] = (int32_t)src_slab_t(ld, ptab, threadIdx.x);
   __syncthreads();
   uint64_t live = 0;
   for (int t = 0; t < TT; ++t)
     if ((int64_t)s_slab[t] * 1024 < ld.rows_live) live |= 1ull << t;
-  const int64_t per_v = (int64_t)__popcll(live) * 64;
+  const int64_t per_v = (int64_t)nsl * 64;
   const int64_t ntiles = bc * per_v;
   const int64_t G = gridDim.x;
   int64_t tile = (int64_t)(blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   if (tile >= ntiles) return;  // uniform over the workgroup
   const int64_t lo_len = 1ll << 20;
   const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
-  const int col0 = threadIdx.x * 4;
+  const int half = threadIdx.x >> 8;  // uniform over each wave
+  const int col0 = (threadIdx.x & 255) * 4;
+  const int elt = BF16 ? 2 : 4;
   int pc[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) pc[q] = fk[col0 + q];
-  RowTile cur = decode_tile(tile, per_v, live);
+  RowTile cur = decode_tile(tile, per_v, live, s_first);
   int64_t sslab = s_slab[cur.t];
-  float val[16][4];
-  load_rows16<BF16, VEC>(ld, s_invp, sslab, cur.p0, x, b_begin + cur.v, col0, val);
-  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;  // transform: row ri, column group rc
+  float val[8][4];
+  auto load = [&](const RowTile &rt, int64_t slab) {
+    const int64_t xrow = b_begin + rt.v;
+    if (VEC)
+      load_rows8_buf<BF16>(ld, s_invp, (int)slab, (int)rt.p0, half,
+                           buf_rsrc((const char *)x + xrow * ld.n * elt, (uint32_t)(ld.n * elt)), col0 * elt, val);
+    else
+      load_rows8<BF16>(ld, s_invp, slab, rt.p0, half, x, xrow, col0, val);
+  };
+  load(cur, sslab);
+  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;  // transform: row ri, columns 32 rc ..
+  const int soff = (32 * rc * 1024 + ri) * 4;
   for (;;) {
     __syncthreads();  // the previous tile's reads of s and sg are done
     // sign words of the 16 rows: 8 Philox blocks of 128 signs per row, one per
-    // thread of the first half, shared through LDS (word index = col0 / 32)
+    // thread of the first 128, shared through LDS (word index = col0 / 32)
     if (threadIdx.x < 128) {
       const int i = threadIdx.x >> 3;
       const int64_t h = sslab * 1024 + s_invp[cur.p0 + i];
@@ -134,10 +195,11 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t bits = sg[i * 32 + (threadIdx.x >> 3)] >> (col0 & 31);
+    for (int k = 0; k < 8; ++k) {
+      const int i = 2 * k + half;
+      const uint32_t bits = sg[i * 32 + (col0 >> 5)] >> (col0 & 31);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[L::idx(i, pc[q])] = flip(val[i][q], (bits >> q) & 1u);
+      for (int q = 0; q < 4; ++q) s[L::idx(i, pc[q])] = flip(val[k][q], (bits >> q) & 1u);
     }
     // prefetch the next tile into the registers just consumed
     const int64_t ntile = tile + G;
@@ -145,17 +207,19 @@ __global__ __launch_bounds__(256) void k_affdT_rows(const LayerDesc *__restrict_
     RowTile nxt = cur;
     int64_t nslab = sslab;
     if (more) {
-      nxt = decode_tile(ntile, per_v, live);
+      nxt = decode_tile(ntile, per_v, live, s_first);
       nslab = s_slab[nxt.t];
-      load_rows16<BF16, VEC>(ld, s_invp, nslab, nxt.p0, x, b_begin + nxt.v, col0, val);
+      load(nxt, nslab);
     }
     __syncthreads();
     // H_l (unnormalised; the 1/32 is applied by the readers of W^T)
-    float e[64];
-    fwht1024_rows16_r(s, e);
-    float *dst = w + cur.v * ld.np + cur.t * lo_len + (int64_t)(64 * rc) * 1024 + cur.p0 + ri;
+    float e[32];
+    fwht1024_rows16_r32(s, e);
+    // column 32 rc + m, row p0 + ri of slab t: byte (32 rc + m) 4096 + 4 (p0 + ri)
+    const __amdgpu_buffer_rsrc_t ws = buf_rsrc(w + cur.v * vstride + (compact ? cur.sl : cur.t) * lo_len + cur.p0,
+                                               (uint32_t)((lo_len - cur.p0) * 4));
 #pragma unroll
-    for (int m = 0; m < 64; ++m) dst[(int64_t)m * 1024] = e[m];
+    for (int m = 0; m < 32; ++m) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m]), ws, soff, m * 4096, 0);
     if (!more) break;
     tile = ntile;
     cur = nxt;
@@ -348,66 +412,149 @@ __global__ __launch_bounds__(256) void k_affd_mtab(const LayerDesc *__restrict__
 // Any TT <= 64 with M stored: per live slab row t of the column l, H_p of the
 // VB vectors' rows (fed from global memory in the first pass's layout), then
 // acc += M[t][l][p] x.  No Gaussians are generated and W^T is read once.
+// Stored-M top kernel, 8 vectors per workgroup.  Thread (i = tid / 32,
+// c = tid % 32) loads column c + 32 k (k < 32) of the slab row of vector i
+// straight into registers (pass-1 order), and after the LDS exchange holds the
+// 32 consecutive columns 32 c .. 32 c + 31, where it applies M (staged in LDS
+// once per slab) and accumulates F.  Two register sets alternate between the
+// slab being transformed and the next live slab being loaded.
+// The slabs are the group's live slabs s_first .. s_first + nsl - 1, stored
+// compactly (W^T of group slab j of vector v at w + v vstride + j 2^20).  A
+// layer whose slabs come in several groups carries F between launches in
+// facc[v][l][p] (fmode bit 0: start from facc, bit 1: last group, finish).
+namespace {
+constexpr int kMPad(int p) { return p + 4 * (p >> 5); }  // 16-byte reads of 8 lanes hit 32 banks
+
+// F of vector i at p = 32 c + m in f[m]: second H_p (bits 0..4 in registers,
+// bits 5..9 after one LDS exchange), keep the rows pi2_p(a), a < R.
+__device__ __forceinline__ void affdT_finish8(const LayerDesc &ld, const uint16_t *ptab, float (&f)[32], float *lds,
+                                              int64_t l, int64_t v0, int nv, int R, float sc,
+                                              float *__restrict__ gout) {
+  using L = Lds1024<8>;
+  const int i = threadIdx.x >> 5, c = threadIdx.x & 31;
+  fwht_regs_t<32>(f);
+  __syncthreads();  // the last slab's readers of lds are done
+  float *b2 = lds + i * L::kStride + 33 * c;  // column 32 c + m
+#pragma unroll
+  for (int m = 0; m < 32; ++m) b2[m] = f[m];
+  __syncthreads();
+  float *b1 = lds + i * L::kStride + c;  // column c + 32 k
+#pragma unroll
+  for (int k = 0; k < 32; ++k) f[k] = b1[33 * k];
+  fwht_regs_t<32>(f);
+#pragma unroll
+  for (int k = 0; k < 32; ++k) b1[33 * k] = f[k];
+  __syncthreads();
+  const uint16_t *p2 = ptab + ld.poff[1][0][ld.K - 2];
+  for (int e = threadIdx.x; e < 8 * R; e += 256) {
+    const int v = e / R, a = e - (e / R) * R;
+    if (v < nv) gout[((v0 + v) * 1024 + l) * R + a] = lds[L::idx(v, p2[a])] * sc;
+  }
+}
+}  // namespace
+
 template <int VB>
 __global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict__ layers,
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const float *__restrict__ w, int64_t bc, int R,
-                                                    const float *__restrict__ mt, float *__restrict__ gout) {
-  using L = Lds1024<VB>;
+                                                    const float *__restrict__ mt, int s_first, int nsl,
+                                                    int64_t vstride, float *__restrict__ facc, int fmode,
+                                                    float *__restrict__ gout) {
+  static_assert(VB == 8, "8 vectors per workgroup");
+  using L = Lds1024<8>;
   __shared__ __align__(16) float lds[L::kFloats];
+  __shared__ __align__(16) float sm[kMPad(1024)];
   const LayerDesc &ld = layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const int64_t lo_len = 1ll << 20;
   const int64_t l = blockIdx.x;
-  const int64_t v0 = (int64_t)blockIdx.y * VB;
-  const int nv = (int)((bc - v0) < VB ? (bc - v0) : VB);
+  const int64_t v0 = (int64_t)blockIdx.y * 8;
+  const int nv = (int)((bc - v0) < 8 ? (bc - v0) : 8);
   uint64_t live, sgn;
   masks_t(ld, ptab, TT, live, sgn);
-  constexpr int C = 256 / VB, E = 4 * VB;
-  const int vr = threadIdx.x / C;
-  const float *src = w + (v0 + vr) * ld.np + l * 1024 + (threadIdx.x % C);
-  const float *mcol = mt + l * 1024 + threadIdx.x;
-  float f[VB][4];
+  const int i = threadIdx.x >> 5, c = threadIdx.x & 31;
+  // rows of absent vectors (i >= nv) load vector v0's data and are discarded
+  const int64_t vi = v0 + (i < nv ? i : 0);
+  const float *src = w + vi * vstride + l * 1024 + c;
+  const float *mcol = mt + l * 1024 + 4 * threadIdx.x;
+  float4 *mst = (float4 *)(sm + kMPad(4 * threadIdx.x));
+  const float4 *mld = (const float4 *)(sm + kMPad(32 * c));
+  float *b1 = lds + i * L::kStride + c;       // column c + 32 k at 33 k
+  float *b2 = lds + i * L::kStride + 33 * c;  // column 32 c + m at m
+  float f[32];
+  float *fv = facc + (vi * 1024 + l) * 1024 + 32 * c;  // F at p = 32 c + m
+  if (fmode & 1) {
 #pragma unroll
-  for (int v = 0; v < VB; ++v)
+    for (int q = 0; q < 8; ++q) {
+      const float4 u = ((const float4 *)fv)[q];
+      f[4 * q] = u.x;
+      f[4 * q + 1] = u.y;
+      f[4 * q + 2] = u.z;
+      f[4 * q + 3] = u.w;
+    }
+  } else {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) f[v][k] = 0.0f;
-  // the loads of the next live slab row are issued before the transform of
-  // the current one
-  float e[E], mm[4];
-  auto fetch = [&](int t) {
+    for (int m = 0; m < 32; ++m) f[m] = 0.0f;
+  }
+  // group slab j (slab t): W^T at src + j 2^20, M at mcol + t 2^20
+  int j = 0;
+  auto fetch = [&](int t, float(&e)[32], float4 &mv) {
 #pragma unroll
-    for (int k = 0; k < E; ++k) e[k] = vr < nv ? src[t * lo_len + C * k] : 0.0f;
+    for (int k = 0; k < 32; ++k) e[k] = src[j * lo_len + 32 * k];
+    mv = *(const float4 *)(mcol + t * lo_len);
+    ++j;
+  };
+  auto step = [&](float(&e)[32], const float4 &mv) {
+    fwht_regs_t<32>(e);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) mm[k] = mcol[t * lo_len + 256 * k];
+    for (int k = 0; k < 32; ++k) b1[33 * k] = e[k];
+    *mst = mv;
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < 32; ++m) e[m] = b2[m];
+    fwht_regs_t<32>(e);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float4 mm = mld[q];
+      f[4 * q] += mm.x * e[4 * q];
+      f[4 * q + 1] += mm.y * e[4 * q + 1];
+      f[4 * q + 2] += mm.z * e[4 * q + 2];
+      f[4 * q + 3] += mm.w * e[4 * q + 3];
+    }
+    __syncthreads();  // before the next slab's writes of lds and sm
   };
   uint64_t rest = live;  // never empty: slab 0 holds source row 0
-  int t = __builtin_ctzll(rest);
-  rest &= rest - 1;
-  fetch(t);
+  for (int q = 0; q < s_first; ++q) rest &= rest - 1;
+  int left = nsl;  // >= 1
+  auto next = [&]() {
+    const int t = __builtin_ctzll(rest);
+    rest &= rest - 1;
+    --left;
+    return t;
+  };
+  float ea[32], eb[32];
+  float4 ma, mb;
+  fetch(next(), ea, ma);
 #pragma unroll 1
   for (;;) {
-    float ec[E], mc[4];
-#pragma unroll
-    for (int k = 0; k < E; ++k) ec[k] = e[k];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) mc[k] = mm[k];
-    const bool more = rest != 0;
-    if (more) {
-      t = __builtin_ctzll(rest);
-      rest &= rest - 1;
-      fetch(t);
-    }
-    __syncthreads();  // the previous slab row's reads of lds are done
-    fwht1024_lds_regs<VB>(lds, ec);
-#pragma unroll
-    for (int v = 0; v < VB; ++v)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) f[v][k] += mc[k] * lds[L::idx(v, threadIdx.x + 256 * k)];
+    bool more = left > 0;
+    if (more) fetch(next(), eb, mb);
+    step(ea, ma);
+    if (!more) break;
+    more = left > 0;
+    if (more) fetch(next(), ea, ma);
+    step(eb, mb);
     if (!more) break;
   }
+  if (!(fmode & 2)) {
+    if (i < nv) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) ((float4 *)fv)[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
+    }
+    return;
+  }
   // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
-  affdT_finish<VB>(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
+  affdT_finish8(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
 }
 
 void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st) {
@@ -426,54 +573,136 @@ void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st) {
   (void)hipGetLastError();
 }
 
-// ---- E ---------------------------------------------------------------------
-// One workgroup per (vector, block of 16 values of a): reads G^T[v][l][a0..a0+15]
-// for every l (64-byte pieces), transposes through LDS, H_l, gathers pi2_l.
-__global__ __launch_bounds__(256) void k_affdT_out(const LayerDesc *__restrict__ layers,
-                                                   const uint16_t *__restrict__ ptab, int layer,
-                                                   const float *__restrict__ gin, int R, int64_t D, int64_t b_begin,
-                                                   float *__restrict__ out, int accumulate) {
+// Phase E for several layers at once: workgroup per (16 rows a, vector);
+// for each listed layer in order, H_l along the 16 rows of its G, gather
+// pi2_l(b) and add (times the layer's scale) into registers; out is written
+// once.  The next layer's G rows are loaded during the current transform.
+__global__ __launch_bounds__(256) void k_affdT_outm(const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, OutLayers ol, int R,
+                                                    int64_t D, int64_t b_begin, int64_t gstride,
+                                                    float *__restrict__ out, int accumulate) {
   using L = Lds1024<16>;
   __shared__ __align__(16) float s[L::kFloats];
-  const LayerDesc &ld = layers[layer];
   const int a0 = blockIdx.x * 16;
   const int na = (R - a0) < 16 ? (R - a0) : 16;
   const int64_t v = blockIdx.y;
+  float acc[16][4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int l = threadIdx.x + 256 * k;
-    const float *src = gin + (v * 1024 + l) * R + a0;
+  for (int i = 0; i < 16; ++i)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[L::idx(i, l)] = i < na ? src[i] : 0.0f;
+    for (int k = 0; k < 4; ++k) acc[i][k] = 0.0f;
+  // thread: columns l = tid + 256 k, rows a0 .. a0 + 15 (four 16-byte pieces)
+  float4 g[4][4];
+  auto fetch = [&](int j) {
+    const float *src = ol.g[j] + v * gstride + (int64_t)threadIdx.x * R + a0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float *p = src + (int64_t)256 * k * R + 4 * q;
+        if (4 * q + 4 <= na) {  // R is a power of two: whole pieces when R >= 4
+          g[k][q] = *(const float4 *)p;
+        } else {
+          g[k][q].x = 4 * q < na ? p[0] : 0.0f;
+          g[k][q].y = 4 * q + 1 < na ? p[1] : 0.0f;
+          g[k][q].z = 4 * q + 2 < na ? p[2] : 0.0f;
+          g[k][q].w = 4 * q + 3 < na ? p[3] : 0.0f;
+        }
+      }
+  };
+  fetch(0);
+  for (int j = 0; j < ol.n; ++j) {
+    __syncthreads();  // the previous layer's gathers from s are done
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int l = threadIdx.x + 256 * k;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        s[L::idx(4 * q, l)] = g[k][q].x;
+        s[L::idx(4 * q + 1, l)] = g[k][q].y;
+        s[L::idx(4 * q + 2, l)] = g[k][q].z;
+        s[L::idx(4 * q + 3, l)] = g[k][q].w;
+      }
+    }
+    if (j + 1 < ol.n) fetch(j + 1);
+    __syncthreads();
+    fwht1024_lds<16>(s);
+    const LayerDesc &ld = layers[ol.layer[j]];
+    const uint16_t *p2l = ptab + ld.poff[1][0][ld.K - 1];
+    const float sc = ol.scale[j];
+    int src[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) src[k] = p2l[threadIdx.x + 256 * k];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[i][k] += s[L::idx(i, src[k])] * sc;
   }
-  __syncthreads();
-  fwht1024_lds<16>(s);
-  const uint16_t *p2l = ptab + ld.poff[1][0][ld.K - 1];
-  const float sc = (float)(sqrt((double)ld.np / (double)D) / 32.0);
   for (int i = 0; i < na; ++i) {
     float *o = out + (b_begin + v) * D + (int64_t)(a0 + i) * 1024;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int b = threadIdx.x + 256 * k;
-      const float val = s[L::idx(i, p2l[b])] * sc;
-      o[b] = accumulate ? o[b] + val : val;
+      o[b] = accumulate ? o[b] + acc[i][k] : acc[i][k];
     }
   }
 }
 
 constexpr unsigned kRowsGrid = 512;
 
-// Vectors per call for TT <= 8: a multiple of 8 (the vectors of one phase-C
-// workgroup) whose W^T (live slabs x 4 MB per vector) stays within the 256 MB
-// memory-side cache between phases A and C, so that the W^T round trip rarely
-// reaches HBM.  0 = no preference (TT > 8: W^T is far larger).
-int64_t affd_transposed_tile(const sk_sketch *s, int layer) {
+// Live slabs of a transposed-path layer: the images of the source slabs
+// that hold data (the top-digit permutation is a bijection).
+int affd_transposed_nlive(const sk_sketch *s, int layer) {
+  return (int)((s->layers[layer].rows_live + 1023) / 1024);
+}
+
+// Vectors per call and live slabs per group.  A layer whose live slabs for 8
+// vectors (the vectors of one top workgroup) fit the budget takes a multiple
+// of 8 vectors that keeps one call's W^T (4 MB per vector and live slab)
+// within the 256 MB memory-side cache between the row and top kernels.  A
+// larger layer takes 16 vectors (W^T then goes through HBM), and with the
+// stored M tables, if the workspace cannot hold all their live slabs, as many
+// slabs per group as fit, F being carried between the groups.  Without the
+// tables (top kernels that regenerate G) TT > 8 has no preferred tile.
+AffdTPlan affd_transposed_plan(const sk_sketch *s, int layer) {
   const LayerDesc &ld = s->layers[layer];
-  if (!affd_transposed_path(s, layer) || ld.lgnp - 20 > 3) return 0;
+  const int nlive = affd_transposed_nlive(s, layer);
+  AffdTPlan pl{0, nlive, false};
+  if (!affd_transposed_path(s, layer)) return pl;
   const char *e = std::getenv("SK_AFFD_MALL_MB");
-  const int64_t budget = (e ? std::atoll(e) : 192) << 20;
-  const int64_t wbytes = ((ld.rows_live + 1023) / 1024) * (4ll << 20);
-  return 8 * std::max<int64_t>(1, budget / (8 * wbytes));
+  const int64_t budget = std::max<int64_t>(1, e ? std::atoll(e) : 192) << 20;
+  const int64_t wbytes = (int64_t)nlive * (4ll << 20);
+  pl.compact = s->d_mtab && s->mtab_off[layer] >= 0;
+  if (!pl.compact && ld.lgnp - 20 > 3) return pl;
+  if (8 * wbytes <= budget || !pl.compact) {
+    pl.tile = 8 * std::max<int64_t>(1, budget / (8 * wbytes));
+    return pl;
+  }
+  pl.tile = 16;
+  const int64_t avail = s->ws_bytes / 4 / pl.tile - s->D;  // floats per vector for W^T (and F)
+  if (((int64_t)nlive << 20) > avail) pl.gsl = (int)std::max<int64_t>(1, (avail >> 20) - 1);
+  return pl;
+}
+
+// Input elements of the source slabs behind live slabs s_first .. s_first +
+// nsl - 1 (in increasing t) of a transposed-path layer.
+int64_t affd_transposed_group_elems(const sk_sketch *s, int layer, int s_first, int nsl) {
+  const LayerDesc &ld = s->layers[layer];
+  const int TT = 1 << (ld.lgnp - 20);
+  int64_t n = 0;
+  int li = 0;
+  for (int t = 0; t < TT; ++t) {
+    int64_t src = 0, stride = 1;
+    for (int k = ld.K - 3; k >= 0; --k) {
+      const int64_t dig = (t / stride) & ((1ll << ld.lg[k]) - 1);
+      src += (int64_t)s->h_ptab[ld.poff[0][1][k] + dig] * stride;
+      stride <<= ld.lg[k];
+    }
+    if (src * 1024 >= ld.rows_live) continue;
+    if (li >= s_first && li < s_first + nsl) n += std::min<int64_t>(ld.n, (src + 1) << 20) - (src << 20);
+    ++li;
+  }
+  return n;
 }
 
 bool affd_transposed_path(const sk_sketch *s, int layer) {
@@ -484,17 +713,20 @@ bool affd_transposed_path(const sk_sketch *s, int layer) {
 }
 
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *gbuf, int phases, hipStream_t st) {
+                         int64_t bc, float *gbuf, int phases, const AffdTGroup &grp, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const int R = (int)(s->D / 1024);
   float *w = s->ws;
+  const int64_t vstride = grp.compact ? ((int64_t)grp.vslabs << 20) : ld.np;
   if (phases & 1) {  // A
-    // two resident workgroups per CU (64 KB of LDS each); a multiple of 8
+    // two resident workgroups per CU (72 KB of LDS each); a multiple of 8
     const dim3 grid(kRowsGrid);
+    // buffer loads take 32-bit byte offsets
+    if (ld.n * (dtype == SK_BF16 ? 2 : 4) >= (1ll << 31)) vec = false;
 #define SK_AROWS(BF, VE)                                                                                  \
-  hipLaunchKernelGGL((k_affdT_rows<BF, VE>), grid, dim3(256), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin, \
-                     bc, w, s->key)
+  hipLaunchKernelGGL((k_affdT_rows<BF, VE>), grid, dim3(512), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin, \
+                     bc, w, grp.s_first, grp.nsl, vstride, (int)grp.compact, s->key)
     if (dtype == SK_BF16) {
       if (vec) SK_AROWS(true, true); else SK_AROWS(true, false);
     } else {
@@ -503,9 +735,10 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
 #undef SK_AROWS
   }
   if (!(phases & 2)) return;
-  if (s->d_mtab && s->mtab_off[layer] >= 0) {
+  if (grp.compact) {
     hipLaunchKernelGGL(k_affdT_topM<8>, dim3(1024u, (unsigned)((bc + 7) / 8)), dim3(256), 0, st, s->d_layers,
-                       s->d_ptab, layer, w, bc, R, s->d_mtab + s->mtab_off[layer], gbuf);
+                       s->d_ptab, layer, w, bc, R, s->d_mtab + s->mtab_off[layer], grp.s_first, grp.nsl, vstride,
+                       grp.facc, grp.fmode, gbuf);
     (void)hipGetLastError();
     return;
   }
@@ -535,12 +768,16 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
   (void)hipGetLastError();
 }
 
-void run_affd_transposed_out(const sk_sketch *s, int layer, const float *gbuf, int64_t b_begin, int64_t gb,
-                             float *out, bool accumulate, hipStream_t st) {
+void run_affd_transposed_outm(const sk_sketch *s, const OutLayers &ol, int64_t gstride, int64_t b_begin,
+                              int64_t gb, float *out, bool accumulate, hipStream_t st) {
   const int R = (int)(s->D / 1024);
-  hipLaunchKernelGGL(k_affdT_out, dim3((unsigned)((R + 15) / 16), (unsigned)gb), dim3(256), 0, st, s->d_layers,
-                     s->d_ptab, layer, gbuf, R, s->D, b_begin, out, (int)accumulate);
+  hipLaunchKernelGGL(k_affdT_outm, dim3((unsigned)((R + 15) / 16), (unsigned)gb), dim3(256), 0, st, s->d_layers,
+                     s->d_ptab, ol, R, s->D, b_begin, gstride, out, (int)accumulate);
   (void)hipGetLastError();
+}
+
+float affd_transposed_out_scale(const sk_sketch *s, int layer) {
+  return (float)(std::sqrt((double)s->layers[layer].np / (double)s->D) / 32.0);
 }
 
 }  // namespace sk

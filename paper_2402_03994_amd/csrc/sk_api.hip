@@ -363,6 +363,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   } while (0)
   SK_TRY(alloc((void **)&s->d_layers, sizeof(LayerDesc) * n_layers));
   SK_TRY(alloc((void **)&s->d_ptab, sizeof(uint16_t) * ptab.size()));
+  s->h_ptab = ptab;
   if (kind == SK_AFJL || kind == SK_FJL) SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
   SK_TRY(alloc((void **)&s->d_items, sizeof(FoldItem) * s->items.size()));
   SK_TRY(alloc((void **)&s->d_rslot, sizeof(int2) * rslot.size()));
@@ -517,41 +518,108 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
       case SK_AFFD: {
         bool acc_now = accumulate != 0;  // false until the first layer has written out
         std::vector<int> small;
+        // Transposed-path layers: the W^T region of the largest tile of the
+        // call at the start of the workspace, then one G^T slot (bc x D
+        // floats) per layer waiting for the shared output pass, which runs
+        // when the slots are full, before any other kind of layer uses the
+        // workspace, and at the end.
+        const int64_t ws_f = s->ws_bytes / 4;
+        struct TPlan {
+          int64_t tile, wt_pv, fa_pv;
+          int gsl, ngroups, nlive;
+          bool compact;
+        };
+        auto tplan = [&](int l) {
+          const LayerDesc &ld = s->layers[l];
+          const AffdTPlan pl = affd_transposed_plan(s, l);
+          TPlan t{};
+          t.tile = pl.tile ? pl.tile
+                           : std::max<int64_t>(1, affd_tile_bytes() / std::max<int64_t>(affd_live_bytes_per_vector(s, l), 1));
+          t.nlive = affd_transposed_nlive(s, l);
+          t.gsl = pl.gsl;
+          t.ngroups = (t.nlive + pl.gsl - 1) / pl.gsl;
+          t.compact = pl.compact;
+          t.wt_pv = pl.compact ? ((int64_t)pl.gsl << 20) : ld.np;
+          t.fa_pv = t.ngroups > 1 ? (1ll << 20) : 0;
+          t.tile = std::min({t.tile, bc, std::max<int64_t>(1, ws_f / (t.wt_pv + t.fa_pv + s->D))});
+          return t;
+        };
+        int64_t wt_region = 0;
+        for (int l = l0; l < l1; ++l)
+          if (!affd_small_path(s, l) && affd_fast_path(s, l) && affd_transposed_path(s, l)) {
+            const TPlan t = tplan(l);
+            wt_region = std::max(wt_region, t.tile * (t.wt_pv + t.fa_pv));
+          }
+        const int64_t gslot = bc * s->D;
+        const int64_t nslots = std::min<int64_t>(kMaxPtrs, (ws_f - wt_region) / gslot);
+        OutLayers ol{};
+        auto flush = [&]() {
+          if (!ol.n) return;
+          SK_PROF(SK_PROF_GATHER, bc * s->D * 4, run_affd_transposed_outm(s, ol, s->D, b0, bc, out, acc_now, st));
+          acc_now = true;
+          ol.n = 0;
+        };
+        // rows and top kernels of one transposed layer for vectors g0 .. g0 + gb - 1,
+        // G^T of vector g0 + v at gbuf + v D
+        auto run_t = [&](int l, const TPlan &t, int64_t g0, int64_t gb, float *gbuf) {
+          const LayerDesc &ld = s->layers[l];
+          const bool vec = !(ld.n & 3) && !((uintptr_t)grads[l - l0] & 15);
+          float *facc = s->ws + t.tile * t.wt_pv;
+          for (int64_t t0 = g0; t0 < g0 + gb; t0 += t.tile) {
+            const int64_t tb = std::min(t.tile, g0 + gb - t0);
+            float *gt = gbuf + (t0 - g0) * s->D;
+            for (int gi = 0; gi < t.ngroups; ++gi) {
+              AffdTGroup grp{gi * t.gsl, std::min(t.gsl, t.nlive - gi * t.gsl), t.gsl, t.compact, facc,
+                             (gi > 0 ? 1 : 0) | (gi == t.ngroups - 1 ? 2 : 0)};
+              const int64_t gel = t.ngroups > 1 ? affd_transposed_group_elems(s, l, grp.s_first, grp.nsl) : ld.n;
+              SK_PROF(SK_PROF_AFFD_ROWS, tb * gel * esz,
+                      run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 1, grp, st));
+              SK_PROF(SK_PROF_AFFD_FOLD, 0,
+                      run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 2, grp, st));
+            }
+          }
+        };
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
           if (affd_small_path(s, l)) {
             small.push_back(l);
             continue;
           }
+          if (affd_fast_path(s, l) && affd_transposed_path(s, l)) {
+            const TPlan t = tplan(l);
+            if (nslots >= 1) {
+              if (ol.n == nslots) flush();
+              float *gbuf = s->ws + wt_region + ol.n * gslot;
+              run_t(l, t, b0, bc, gbuf);
+              ol.layer[ol.n] = l;
+              ol.scale[ol.n] = affd_transposed_out_scale(s, l);
+              ol.g[ol.n] = gbuf;
+              ++ol.n;
+              continue;
+            }
+            // small workspace: G^T of up to gmax vectors after this layer's W^T tile
+            const int64_t gmax = std::max(t.tile, (ws_f - t.tile * (t.wt_pv + t.fa_pv)) / s->D / t.tile * t.tile);
+            float *gbuf = s->ws + t.tile * (t.wt_pv + t.fa_pv);
+            for (int64_t g0 = b0; g0 < b0 + bc; g0 += gmax) {
+              const int64_t gb = std::min(gmax, b0 + bc - g0);
+              run_t(l, t, g0, gb, gbuf);
+              OutLayers one{};
+              one.n = 1;
+              one.layer[0] = l;
+              one.scale[0] = affd_transposed_out_scale(s, l);
+              one.g[0] = gbuf;
+              SK_PROF(SK_PROF_GATHER, gb * s->D * 4, run_affd_transposed_outm(s, one, s->D, g0, gb, out, acc_now, st));
+            }
+            acc_now = true;
+            continue;
+          }
+          flush();  // the other paths use the workspace from its start
           if (affd_fast_path(s, l)) {
             // batch tile sized so the layer's intermediate stays cache-resident between phases
             const int64_t live = affd_live_bytes_per_vector(s, l);
             int64_t tile = std::max<int64_t>(1, affd_tile_bytes() / std::max<int64_t>(live, 1));
-            if (const int64_t tt = affd_transposed_tile(s, l)) tile = tt;
-            tile = std::min(tile, std::max<int64_t>(1, s->ws_bytes / affd_fast_bytes_per_vector(s, l)));
             const bool vec = !(ld.n & 3) && !((uintptr_t)grads[l - l0] & 15);
-            if (affd_transposed_path(s, l)) {
-              // W^T of one tile at the start of the workspace, then G^T of up to
-              // gmax vectors; phase E runs once per gmax vectors
-              const int64_t g4 = s->D * 4;
-              tile = std::min(tile, bc);
-              const int64_t gmax = std::max(tile, (s->ws_bytes - tile * ld.np * 4) / g4 / tile * tile);
-              float *gbuf = s->ws + tile * ld.np;
-              for (int64_t g0 = b0; g0 < b0 + bc; g0 += gmax) {
-                const int64_t gb = std::min(gmax, b0 + bc - g0);
-                for (int64_t t0 = g0; t0 < g0 + gb; t0 += tile) {
-                  const int64_t tb = std::min(tile, g0 + gb - t0);
-                  float *gt = gbuf + (t0 - g0) * s->D;
-                  SK_PROF(SK_PROF_AFFD_ROWS, tb * ld.n * esz,
-                          run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 1, st));
-                  SK_PROF(SK_PROF_AFFD_FOLD, 0, run_affd_transposed(s, l, grads[l - l0], dtype, vec, t0, tb, gt, 2, st));
-                }
-                SK_PROF(SK_PROF_GATHER, gb * g4 * (l == l1 - 1 ? 2 : 1),
-                        run_affd_transposed_out(s, l, gbuf, g0, gb, out, acc_now, st));
-              }
-              acc_now = true;
-              continue;
-            }
+            tile = std::min(tile, std::max<int64_t>(1, s->ws_bytes / affd_fast_bytes_per_vector(s, l)));
             for (int64_t t0 = b0; t0 < b0 + bc; t0 += tile) {
               const int64_t tb = std::min(tile, b0 + bc - t0);
               SK_PROF(SK_PROF_AFFD_FOLD, tb * ld.n * esz + (l == l1 - 1 ? tb * s->D * 4 : 0),
@@ -570,6 +638,7 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
                   launch_affd_gather(s, l, f, b0, bc, out, acc_now, st));
           acc_now = true;
         }
+        flush();
         if (!small.empty()) {
           // groups of up to kMaxPtrs small layers; vectors tiled so that W and F
           // of every slot fit the workspace

@@ -70,6 +70,7 @@ struct sk_sketch {
   std::vector<sk::LayerDesc> layers;
   sk::LayerDesc *d_layers = nullptr;
   uint16_t *d_ptab = nullptr;  // digit permutation tables (values < 1024)
+  std::vector<uint16_t> h_ptab;  // host copy
   float *d_gtab = nullptr;     // FJL/AFJL: per-layer G over [0, D)
   // AFJL
   int R = 1, Lw = 0;

@@ -256,4 +256,44 @@ __device__ __forceinline__ void fwht1024_rows16_r(float *s, float (&e)[64]) {
   for (int g = 0; g < 4; ++g) fwht_regs_t<16>(e + 16 * g);
 }
 
+
+// Row-fastest 16-row block for 512-thread workgroups: one pad word per 32
+// floats and a row stride of 2 banks modulo 32, so that both passes of
+// fwht1024_rows16_r32 touch 32 distinct banks in every half-wave.
+struct Lds1024R32 {
+  static constexpr int kStride = 1058;  // 1056 used
+  static constexpr int kFloats = 16 * kStride;
+  static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> 5); }
+};
+
+// Unnormalised 1024-point transform of the 16 rows of an Lds1024R32 block
+// that the caller has filled and synchronised, by 512 threads.  Pass 1: thread
+// (ri = tid % 16, rc = tid / 16) transforms columns rc + 32 k (the high five
+// column bits); pass 2: columns 32 rc + m (the low five).  On return e[m]
+// holds column 32 rc + m of row ri; the block may be refilled after the
+// caller's next barrier.
+__device__ __forceinline__ void fwht1024_rows16_r32(float *s, float (&e)[32]) {
+  using L = Lds1024R32;
+  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;
+  {
+    float *b = s + ri * L::kStride + rc;  // column rc + 32 k sits at rc + 33 k
+#pragma unroll
+    for (int k = 0; k < 32; ++k) e[k] = b[33 * k];
+    fwht_regs_t<32>(e);
+#pragma unroll
+    for (int k = 0; k < 32; ++k) b[33 * k] = e[k];
+  }
+  __syncthreads();
+  const float *b = s + ri * L::kStride + 33 * rc;  // column 32 rc + m sits at 33 rc + m
+#pragma unroll
+  for (int m = 0; m < 32; ++m) e[m] = b[m];
+  fwht_regs_t<32>(e);
+}
+
+// Raw buffer resource over [base, base + bytes): loads past the end return
+// zero, stores past the end are dropped (offsets are bytes, unsigned 32-bit).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 }  // namespace sk

@@ -44,18 +44,44 @@ int64_t affd_small_bytes_per_vector(const sk_sketch *s);
 // phases: bit 0 = the row kernel (reads the gradients), bit 1 = the rest
 void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dtype, int64_t b_begin, int64_t bc,
                     int phases, float *out, bool accumulate, hipStream_t st);
-int64_t affd_transposed_tile(const sk_sketch *s, int layer);
 bool affd_transposed_path(const sk_sketch *s, int layer);
+// Vectors per call (0 = no preference), live slabs per group, and whether W^T
+// is stored compactly per group (stored M tables) or at the slab's own index.
+struct AffdTPlan {
+  int64_t tile;
+  int gsl;
+  bool compact;
+};
+AffdTPlan affd_transposed_plan(const sk_sketch *s, int layer);
+int affd_transposed_nlive(const sk_sketch *s, int layer);
+int64_t affd_transposed_group_elems(const sk_sketch *s, int layer, int s_first, int nsl);
+// One slab group of a call: live slabs s_first .. s_first + nsl - 1; W^T
+// holds vslabs slabs per vector when compact; F is carried in facc between
+// groups (fmode bit 0: read facc first, bit 1: last group).
+struct AffdTGroup {
+  int s_first, nsl, vslabs;
+  bool compact;
+  float *facc;
+  int fmode;
+};
 // Phases A-C of the transposed path for vectors b_begin .. b_begin + bc - 1,
 // writing G^T of vector b_begin + v at gbuf + v D; the W^T workspace is s->ws.
 // M[t'][l][p] = (H_TT (signs . g[., p, l]))[t'] for a transposed-path layer
 void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st);
 // phases: bit 0 = A (the row kernel, reads the gradients), bit 1 = B and C
 void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype, bool vec, int64_t b_begin,
-                         int64_t bc, float *gbuf, int phases, hipStream_t st);
-// Phase E for gb vectors whose G^T starts at gbuf: out rows b_begin ...
-void run_affd_transposed_out(const sk_sketch *s, int layer, const float *gbuf, int64_t b_begin, int64_t gb,
-                             float *out, bool accumulate, hipStream_t st);
+                         int64_t bc, float *gbuf, int phases, const AffdTGroup &grp, hipStream_t st);
+// Phase E of up to kMaxPtrs layers in one launch: G^T of layer j for vector
+// v at g[j] + v gstride; out (+)= sum_j scale[j] (contribution of layer j).
+struct OutLayers {
+  int32_t n;
+  int32_t layer[kMaxPtrs];
+  float scale[kMaxPtrs];
+  const float *g[kMaxPtrs];
+};
+void run_affd_transposed_outm(const sk_sketch *s, const OutLayers &ol, int64_t gstride, int64_t b_begin,
+                              int64_t gb, float *out, bool accumulate, hipStream_t st);
+float affd_transposed_out_scale(const sk_sketch *s, int layer);
 void launch_affd_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                         float *w, hipStream_t st);
 void launch_affd_fold(const sk_sketch *s, int layer, const float *w, int64_t bc, float *f, hipStream_t st);

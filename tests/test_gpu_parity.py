@@ -90,6 +90,45 @@ def test_affd_mtab_parity(shapes, mtab, dev):
     s.close()
 
 
+def test_affd_slab_groups_small_workspace(dev, monkeypatch):
+    """A ten-slab transposed-path layer under an 80 MB workspace: the live
+    slabs go through the row and top kernels one group at a time with F
+    carried between the groups; the result matches the oracle and the default
+    single-group schedule."""
+    from paper_2402_03994_amd import Sketch
+    shapes = [(1, 9 * 2 ** 20 + 5), (1, 3000)]
+    D, seed, batch = 65536, 29, 11
+    xs = rand_inputs(shapes, batch, 97)
+    o = O.apply("affd", shapes, D, seed, [oracle_in(x)[0] for x in xs])
+    big = Sketch("affd", shapes, D, seed, device=dev)
+    y_big = big.apply([x.to(dev) for x in xs]).cpu().numpy()
+    big.close()
+    monkeypatch.setenv("SK_WORKSPACE_MB", "80")
+    small = Sketch("affd", shapes, D, seed, device=dev)
+    y_small = small.apply([x.to(dev) for x in xs]).cpu().numpy()
+    small.close()
+    assert rel_err(y_small, o) <= TOL_F32
+    assert rel_err(y_big, o) <= TOL_F32
+    assert rel_err(y_small, y_big.astype(np.float64)) <= TOL_F32
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_affd_transposed_vector_loads(dtype, dev):
+    """Transposed-path AFFD layers whose length is a multiple of 4 (16- or
+    8-byte row loads) with a partial last source row, in fp32 and bf16.  The
+    oracle reads the same bf16 values exactly and the kernels compute in fp32,
+    so both dtypes are held to the fp32 bound."""
+    from paper_2402_03994_amd import Sketch
+    shapes = [(1, 2 ** 21 + 1000), (5, 2 ** 18 + 4)]
+    D, seed, batch = 65536, 23, 4
+    s = Sketch("affd", shapes, D, seed, device=dev)
+    xs = rand_inputs(shapes, batch, 98, dtype=dtype)
+    y = s.apply([x.to(dev) for x in xs])
+    o = O.apply("affd", shapes, D, seed, [oracle_in(x)[0] for x in xs], dtype=oracle_in(xs[0])[1])
+    assert rel_err(y.cpu().numpy(), o) <= TOL_F32
+    s.close()
+
+
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
 @pytest.mark.parametrize("case", [1, 3, 4])
 def test_transpose_parity(kind, case, dev):
