@@ -64,28 +64,28 @@ struct RowTile {
   int sl;  // index of slab t among the group's live slabs
 };
 
-// Tiles of one vector: 64 per live slab of the group (live slabs s_first ..
+// Tiles of one vector: 32 per live slab of the group (live slabs s_first ..
 // s_first + nsl - 1 in increasing t).
 __device__ __forceinline__ RowTile decode_tile(int64_t tile, int64_t per_v, uint64_t live, int s_first) {
   RowTile r;
   r.v = tile / per_v;
   const int64_t rem = tile - r.v * per_v;
-  r.sl = (int)(rem >> 6);
-  r.p0 = (rem & 63) * 16;
+  r.sl = (int)(rem >> 5);
+  r.p0 = (rem & 31) * 32;
   uint64_t m = live;
   for (int i = 0; i < s_first + r.sl; ++i) m &= m - 1;
   r.t = __builtin_ctzll(m);
   return r;
 }
 
-// Rows 2k + half (k < 8) of a tile: thread column col0..col0+3.  General
+// Rows 4k + quarter (k < 8) of a tile: thread column col0..col0+3.  General
 // form: any alignment and length.
 template <bool BF16>
 __device__ __forceinline__ void load_rows8(const LayerDesc &ld, const uint16_t *s_invp, int64_t sslab, int64_t p0,
-                                           int half, const void *x, int64_t xrow, int col0, float (&val)[8][4]) {
+                                           int quarter, const void *x, int64_t xrow, int col0, float (&val)[8][4]) {
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const int64_t h = sslab * 1024 + s_invp[p0 + 2 * k + half];
+    const int64_t h = sslab * 1024 + s_invp[p0 + 4 * k + quarter];
     const int64_t j0 = h * 1024 + col0;
     const int64_t lim = ld.n - j0;
 #pragma unroll
@@ -101,12 +101,12 @@ __device__ __forceinline__ void load_rows8(const LayerDesc &ld, const uint16_t *
 // the vector operand, which the check covers).
 template <bool BF16>
 __device__ __forceinline__ void load_rows8_buf(const LayerDesc &ld, const uint16_t *s_invp, int sslab, int p0,
-                                               int half, __amdgpu_buffer_rsrc_t rs, int voff, float (&val)[8][4]) {
+                                               int quarter, __amdgpu_buffer_rsrc_t rs, int voff, float (&val)[8][4]) {
   typedef unsigned int u4 __attribute__((ext_vector_type(4)));
   typedef unsigned int u2 __attribute__((ext_vector_type(2)));
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const int h = __builtin_amdgcn_readfirstlane(sslab * 1024 + (int)s_invp[p0 + 2 * k + half]);
+    const int h = __builtin_amdgcn_readfirstlane(sslab * 1024 + (int)s_invp[p0 + 4 * k + quarter]);
     if (h < ld.rows_live) {
       if (BF16) {
         const u2 u = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + h * 2048, 0, 0);
@@ -130,40 +130,42 @@ __device__ __forceinline__ void load_rows8_buf(const LayerDesc &ld, const uint16
 
 }  // namespace
 
-// 512 threads per workgroup: thread tid loads columns col0 = 4 (tid % 256)
-// .. col0 + 3 of tile rows 2k + tid / 256 and ends holding 32 columns of one
-// row after the transform; W^T is written through a buffer resource whose
-// offsets are scalar constants, 16 threads x 4 bytes = 64 bytes per column.
+// 1024 threads per workgroup (one per CU), tiles of 32 destination rows:
+// thread tid loads columns col0 = 4 (tid % 256) .. col0 + 3 of tile rows
+// 4k + tid / 256 and ends holding 32 columns of one row after the transform;
+// W^T is written through a buffer resource whose offsets are scalar
+// constants, 32 threads x 4 bytes = one 128-byte line per column (64-byte
+// pieces write at about two thirds of the rate).
 // W^T of the tile's slab with group index sl (slab t) of vector v starts at
 // w + v vstride + (compact ? sl : t) 2^20.
 template <bool BF16, bool VEC>
-__global__ __launch_bounds__(512) void k_affdT_rows(const LayerDesc *__restrict__ layers,
+__global__ __launch_bounds__(1024) void k_affdT_rows(const LayerDesc *__restrict__ layers,
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const void *__restrict__ x, int64_t b_begin, int64_t bc,
                                                     float *__restrict__ w, int s_first, int nsl, int64_t vstride,
                                                     int compact, Key key) {
   using L = Lds1024R32;
   __shared__ __align__(16) float s[L::kFloats];
-  __shared__ __align__(16) uint32_t sg[16 * 32];
+  __shared__ __align__(16) uint32_t sg[32 * 32];
   __shared__ uint16_t s_invp[1024];
   __shared__ int32_t s_slab[64];
   const LayerDesc &ld = layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const uint16_t *invp = ptab + ld.poff[0][1][ld.K - 2];
-  for (int e = threadIdx.x; e < 1024; e += 512) s_invp[e] = invp[e];
+  s_invp[threadIdx.x] = invp[threadIdx.x];
   if (threadIdx.x < TT) s_slab[threadIdx.x] = (int32_t)src_slab_t(ld, ptab, threadIdx.x);
   __syncthreads();
   uint64_t live = 0;
   for (int t = 0; t < TT; ++t)
     if ((int64_t)s_slab[t] * 1024 < ld.rows_live) live |= 1ull << t;
-  const int64_t per_v = (int64_t)nsl * 64;
+  const int64_t per_v = (int64_t)nsl * 32;
   const int64_t ntiles = bc * per_v;
   const int64_t G = gridDim.x;
   int64_t tile = (int64_t)(blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   if (tile >= ntiles) return;  // uniform over the workgroup
   const int64_t lo_len = 1ll << 20;
   const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
-  const int half = threadIdx.x >> 8;  // uniform over each wave
+  const int quarter = threadIdx.x >> 8;  // uniform over each wave
   const int col0 = (threadIdx.x & 255) * 4;
   const int elt = BF16 ? 2 : 4;
   int pc[4];
@@ -175,19 +177,19 @@ __global__ __launch_bounds__(512) void k_affdT_rows(const LayerDesc *__restrict_
   auto load = [&](const RowTile &rt, int64_t slab) {
     const int64_t xrow = b_begin + rt.v;
     if (VEC)
-      load_rows8_buf<BF16>(ld, s_invp, (int)slab, (int)rt.p0, half,
+      load_rows8_buf<BF16>(ld, s_invp, (int)slab, (int)rt.p0, quarter,
                            buf_rsrc((const char *)x + xrow * ld.n * elt, (uint32_t)(ld.n * elt)), col0 * elt, val);
     else
-      load_rows8<BF16>(ld, s_invp, slab, rt.p0, half, x, xrow, col0, val);
+      load_rows8<BF16>(ld, s_invp, slab, rt.p0, quarter, x, xrow, col0, val);
   };
   load(cur, sslab);
-  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;  // transform: row ri, columns 32 rc ..
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;  // transform: row ri, columns 32 rc ..
   const int soff = (32 * rc * 1024 + ri) * 4;
   for (;;) {
     __syncthreads();  // the previous tile's reads of s and sg are done
-    // sign words of the 16 rows: 8 Philox blocks of 128 signs per row, one per
-    // thread of the first 128, shared through LDS (word index = col0 / 32)
-    if (threadIdx.x < 128) {
+    // sign words of the 32 rows: 8 Philox blocks of 128 signs per row, one per
+    // thread of the first 256, shared through LDS (word index = col0 / 32)
+    if (threadIdx.x < 256) {
       const int i = threadIdx.x >> 3;
       const int64_t h = sslab * 1024 + s_invp[cur.p0 + i];
       const W4 q = philox((uint64_t)(h * 8 + (threadIdx.x & 7)), (uint32_t)ld.layer_id, ST_SIGN, key);
@@ -196,7 +198,7 @@ __global__ __launch_bounds__(512) void k_affdT_rows(const LayerDesc *__restrict_
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      const int i = 2 * k + half;
+      const int i = 4 * k + quarter;
       const uint32_t bits = sg[i * 32 + (col0 >> 5)] >> (col0 & 31);
 #pragma unroll
       for (int q = 0; q < 4; ++q) s[L::idx(i, pc[q])] = flip(val[k][q], (bits >> q) & 1u);
@@ -214,7 +216,7 @@ __global__ __launch_bounds__(512) void k_affdT_rows(const LayerDesc *__restrict_
     __syncthreads();
     // H_l (unnormalised; the 1/32 is applied by the readers of W^T)
     float e[32];
-    fwht1024_rows16_r32(s, e);
+    fwht1024_rows32(s, e);
     // column 32 rc + m, row p0 + ri of slab t: byte (32 rc + m) 4096 + 4 (p0 + ri)
     const __amdgpu_buffer_rsrc_t ws = buf_rsrc(w + cur.v * vstride + (compact ? cur.sl : cur.t) * lo_len + cur.p0,
                                                (uint32_t)((lo_len - cur.p0) * 4));
@@ -648,7 +650,7 @@ __global__ __launch_bounds__(256) void k_affdT_outm(const LayerDesc *__restrict_
   }
 }
 
-constexpr unsigned kRowsGrid = 512;
+constexpr unsigned kRowsGrid = 256;
 
 // Live slabs of a transposed-path layer: the images of the source slabs
 // that hold data (the top-digit permutation is a bijection).
@@ -720,12 +722,12 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
   float *w = s->ws;
   const int64_t vstride = grp.compact ? ((int64_t)grp.vslabs << 20) : ld.np;
   if (phases & 1) {  // A
-    // two resident workgroups per CU (72 KB of LDS each); a multiple of 8
+    // one resident workgroup per CU (141 KB of LDS); a multiple of 8
     const dim3 grid(kRowsGrid);
     // buffer loads take 32-bit byte offsets
     if (ld.n * (dtype == SK_BF16 ? 2 : 4) >= (1ll << 31)) vec = false;
 #define SK_AROWS(BF, VE)                                                                                  \
-  hipLaunchKernelGGL((k_affdT_rows<BF, VE>), grid, dim3(512), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin, \
+  hipLaunchKernelGGL((k_affdT_rows<BF, VE>), grid, dim3(1024), 0, st, s->d_layers, s->d_ptab, layer, x, b_begin, \
                      bc, w, grp.s_first, grp.nsl, vstride, (int)grp.compact, s->key)
     if (dtype == SK_BF16) {
       if (vec) SK_AROWS(true, true); else SK_AROWS(true, false);

@@ -257,24 +257,25 @@ __device__ __forceinline__ void fwht1024_rows16_r(float *s, float (&e)[64]) {
 }
 
 
-// Row-fastest 16-row block for 512-thread workgroups: one pad word per 32
-// floats and a row stride of 2 banks modulo 32, so that both passes of
-// fwht1024_rows16_r32 touch 32 distinct banks in every half-wave.
+// Row-fastest 32-row block for 1024-thread workgroups: one pad word per 32
+// floats and an odd row stride, so that both passes of fwht1024_rows32 touch
+// 32 distinct banks in every half-wave (the 32 rows of one column group).
 struct Lds1024R32 {
-  static constexpr int kStride = 1058;  // 1056 used
-  static constexpr int kFloats = 16 * kStride;
+  static constexpr int kRows = 32;
+  static constexpr int kStride = 1057;  // 1056 used
+  static constexpr int kFloats = kRows * kStride;
   static __device__ __forceinline__ int idx(int row, int l) { return row * kStride + l + (l >> 5); }
 };
 
-// Unnormalised 1024-point transform of the 16 rows of an Lds1024R32 block
-// that the caller has filled and synchronised, by 512 threads.  Pass 1: thread
-// (ri = tid % 16, rc = tid / 16) transforms columns rc + 32 k (the high five
-// column bits); pass 2: columns 32 rc + m (the low five).  On return e[m]
-// holds column 32 rc + m of row ri; the block may be refilled after the
-// caller's next barrier.
-__device__ __forceinline__ void fwht1024_rows16_r32(float *s, float (&e)[32]) {
+// Unnormalised 1024-point transform of the 32 rows of an Lds1024R32 block
+// that the caller has filled and synchronised, by 1024 threads.  Pass 1:
+// thread (ri = tid % 32, rc = tid / 32) transforms columns rc + 32 k (the high
+// five column bits); pass 2: columns 32 rc + m (the low five).  On return e[m]
+// holds column 32 rc + m of row ri, so the 32 lanes of a column hold its 32
+// consecutive rows; the block may be refilled after the caller's next barrier.
+__device__ __forceinline__ void fwht1024_rows32(float *s, float (&e)[32]) {
   using L = Lds1024R32;
-  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
   {
     float *b = s + ri * L::kStride + rc;  // column rc + 32 k sits at rc + 33 k
 #pragma unroll
