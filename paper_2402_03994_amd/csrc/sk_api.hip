@@ -65,6 +65,7 @@ void free_all(sk_sketch *s) {
   f(s->d_gtab);
   f(s->d_items);
   f(s->d_rslot);
+  f(s->d_rfirst);
   f(s->d_fjl_pos);
   f(s->d_fjl_seg);
   f(s->d_fjl_smp);
@@ -317,6 +318,8 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
         }
       }
       ld.n_items = (int32_t)s->items.size() - ld.item_off;
+      ld.rmaxch = 0;
+      for (size_t i = ld.rslot_off; i < rslot.size(); ++i) ld.rmaxch = std::max(ld.rmaxch, rslot[i].y);
     }
   }
 
@@ -367,6 +370,9 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   if (kind == SK_AFJL || kind == SK_FJL) SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
   SK_TRY(alloc((void **)&s->d_items, sizeof(FoldItem) * s->items.size()));
   SK_TRY(alloc((void **)&s->d_rslot, sizeof(int2) * rslot.size()));
+  std::vector<int32_t> rfirst(rslot.size());
+  for (size_t i = 0; i < rslot.size(); ++i) rfirst[i] = rslot[i].y > 0 ? rslot[i].x : -1;
+  SK_TRY(alloc((void **)&s->d_rfirst, sizeof(int32_t) * rfirst.size()));
   SK_TRY(alloc((void **)&s->d_fjl_pos, sizeof(uint32_t) * fpos.size()));
   SK_TRY(alloc((void **)&s->d_fjl_seg, sizeof(uint32_t) * fseg.size()));
   SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
@@ -385,6 +391,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(h2d(s->d_ptab, ptab.data(), sizeof(uint16_t) * ptab.size()));
   SK_TRY(h2d(s->d_items, s->items.data(), sizeof(FoldItem) * s->items.size()));
   SK_TRY(h2d(s->d_rslot, rslot.data(), sizeof(int2) * rslot.size()));
+  SK_TRY(h2d(s->d_rfirst, rfirst.data(), sizeof(int32_t) * rfirst.size()));
   SK_TRY(h2d(s->d_fjl_pos, fpos.data(), sizeof(uint32_t) * fpos.size()));
   SK_TRY(h2d(s->d_fjl_seg, fseg.data(), sizeof(uint32_t) * fseg.size()));
   SK_TRY(h2d(s->d_fjl_smp, fsmp.data(), sizeof(uint32_t) * fsmp.size()));

@@ -371,50 +371,111 @@ __global__ __launch_bounds__(256) void k_afjl_tail(const LayerDesc *__restrict__
   }
 }
 
-// Tail for R <= 64: one thread per (vector, column) keeps the R values of its
-// column in registers across all layers (no LDS, no barriers).
-// Layers are split into contiguous groups (blockIdx.y); group gi writes its
-// sum to ysum[gi][bl][:], reduced in group order afterwards.
+// v[j] = sum of the fold partials of destination row j (rs[j] = first item,
+// item count; rf[j] = first item or -1) at one column of one vector.  The
+// layer's partials are read through the buffer resource pr: item item0 + i at
+// byte i stride + voff0 (missing rows read past the end, i.e. zero).  With at
+// most one item per row the J loads go out together; otherwise chunk k of
+// every row is added in turn, the row records being re-read for each chunk
+// rather than held in registers.
+template <int J>
+__device__ __forceinline__ void tail_gather(int maxch, const int2 *rs, const int32_t *rf, __amdgpu_buffer_rsrc_t pr,
+                                            uint32_t stride, uint32_t voff0, int item0, float (&v)[J]) {
+  constexpr uint32_t kNone = 0x80000000u;  // beyond the resource (< 2^31 bytes)
+  if (maxch <= 1) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int f = rf[j];
+      const uint32_t off = f >= 0 ? (uint32_t)(f - item0) * stride + voff0 : kNone;
+      v[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(pr, (int)off, 0, 0));
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) v[j] = 0.0f;
+  for (int k = 0; k < maxch; ++k) {
+#pragma unroll
+    for (int j0 = 0; j0 < J; j0 += 16) {
+      asm volatile("" ::: "memory");  // re-read the row records
+#pragma unroll
+      for (int j = j0; j < j0 + 16 && j < J; ++j) {
+        const int2 q = rs[j];
+        const uint32_t off = k < q.y ? (uint32_t)(q.x + k - item0) * stride + voff0 : kNone;
+        v[j] += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(pr, (int)off, 0, 0));
+      }
+    }
+  }
+}
+
+// The partials of layer ld as a buffer resource (the callers keep each
+// layer's partials below 2^31 bytes).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tail_part_rsrc(const LayerDesc &ld, const float *part, int item_begin,
+                                                                 int64_t bc, int Lw) {
+  return buf_rsrc(part + (int64_t)(ld.item_off - item_begin) * bc * Lw, (uint32_t)((int64_t)ld.n_items * bc * Lw * 4));
+}
+
+// Tail for R <= 64: the R values of a (vector, column) stay in registers
+// across all layers (no LDS, no barriers).  R <= 32: one thread per column;
+// R = 64: two threads (the two halves of a wave, 32 columns per wave) hold
+// rows 32 h + j, H_64 = H_2 (across the halves) (x) H_32 (in registers).  The
+// G loads of a layer go out with its partial loads.  Layers are split into
+// contiguous groups (blockIdx.y); group gi writes its sum to ysum[gi][bl][:],
+// reduced in group order afterwards.
 template <int R>
-__global__ __launch_bounds__(256) void k_afjl_tail_reg(const LayerDesc *__restrict__ layers,
-                                                       const int2 *__restrict__ rslot, const float *__restrict__ part,
+__global__ __launch_bounds__(256, 4) void k_afjl_tail_reg(const LayerDesc *__restrict__ layers,
+                                                       const int2 *__restrict__ rslot,
+                                                       const int32_t *__restrict__ rfirst, const float *__restrict__ part,
                                                        const float *__restrict__ gtab, TailGroups grp,
                                                        int item_begin, int Lw, int64_t D, int64_t bc, int64_t b_begin,
                                                        int64_t batch, float *__restrict__ ysum) {
+  constexpr int H = R > 32 ? 2 : 1, J = R / H;
   const int64_t gid = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  const int c = (int)(gid % Lw);
-  const int64_t bl = gid / Lw;
+  int c, h;
+  int64_t bl;
+  if (H == 1) {
+    c = (int)(gid % Lw);
+    bl = gid / Lw;
+    h = 0;
+  } else {  // Lw % 32 == 0; bl is uniform over the wave
+    const int64_t wv = gid >> 6;
+    const int nb = Lw / 32;
+    bl = wv / nb;
+    c = (int)(wv % nb) * 32 + (int)(threadIdx.x & 31);
+    h = (int)((threadIdx.x >> 5) & 1);
+  }
   if (bl >= bc || b_begin + bl >= batch) return;
   const int l_begin = grp.bound[blockIdx.y], l_end = grp.bound[blockIdx.y + 1];
-  float acc[R];
+  float acc[J];
 #pragma unroll
-  for (int r = 0; r < R; ++r) acc[r] = 0.0f;
+  for (int j = 0; j < J; ++j) acc[j] = 0.0f;
   for (int l = l_begin; l < l_end; ++l) {
-    const int2 *rs = rslot + layers[l].rslot_off;
-    // first chunk of every row: independent loads issued together (an empty
-    // row reads slot 0 and is masked), further chunks afterwards
-    float v[R];
+    const LayerDesc &ld = layers[l];
+    const int2 *rs = rslot + ld.rslot_off + h * J;
+    const int32_t *rf = rfirst + ld.rslot_off + h * J;
+    // G of the layer through a buffer resource: the row offsets are scalars
+    const __amdgpu_buffer_rsrc_t gr = buf_rsrc(gtab + (int64_t)l * D, (uint32_t)(D * 4));
+    const int goff = (h * J * Lw + c) * 4;
+    float v[J], gv[J];
+    tail_gather<J>(ld.rmaxch, rs, rf, tail_part_rsrc(ld, part, item_begin, bc, Lw), (uint32_t)(bc * Lw * 4),
+                   (uint32_t)((bl * Lw + c) * 4), ld.item_off, v);
+    // the G loads go out while the partials are in flight
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int2 q = rs[r];
-      const int64_t slot = q.y > 0 ? q.x - item_begin : 0;
-      const float x = part[(slot * bc + bl) * Lw + c];
-      v[r] = q.y > 0 ? x : 0.0f;
+    for (int j = 0; j < J; ++j) gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(gr, goff, j * Lw * 4, 0));
+    fwht_regs_t<J>(v);
+    if (H == 2) {
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const float o = __shfl_xor(v[j], 32);
+        v[j] = h ? o - v[j] : v[j] + o;
+      }
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int2 q = rs[r];
-      for (int k = 1; k < q.y; ++k) v[r] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * Lw + c];
-    }
-    fwht_regs_t<R>(v);
-    const float *g = gtab + (int64_t)l * D + c;
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] += g[(int64_t)r * Lw] * v[r];
+    for (int j = 0; j < J; ++j) acc[j] += gv[j] * v[j];
   }
   const float sc = rsqrtf((float)R);
-  float *o = ysum + ((int64_t)blockIdx.y * bc + bl) * D + c;
+  float *o = ysum + ((int64_t)blockIdx.y * bc + bl) * D + (int64_t)h * J * Lw + c;
 #pragma unroll
-  for (int r = 0; r < R; ++r) o[(int64_t)r * Lw] = acc[r] * sc;
+  for (int j = 0; j < J; ++j) o[(int64_t)j * Lw] = acc[j] * sc;
 }
 
 // R = Lw = 1024 with 1024 threads: workgroup per (32 columns, vector), so every
@@ -423,6 +484,7 @@ __global__ __launch_bounds__(256) void k_afjl_tail_reg(const LayerDesc *__restri
 // (128 KB); four waves per SIMD hide the load latency.
 __global__ __launch_bounds__(1024) void k_afjl_tail_1024w(const LayerDesc *__restrict__ layers,
                                                           const int2 *__restrict__ rslot,
+                                                          const int32_t *__restrict__ rfirst,
                                                           const float *__restrict__ part,
                                                           const float *__restrict__ gtab, int l_begin, int l_end,
                                                           int item_begin, int64_t D, int64_t bc, int64_t b_begin,
@@ -436,20 +498,17 @@ __global__ __launch_bounds__(1024) void k_afjl_tail_1024w(const LayerDesc *__res
 #pragma unroll
   for (int j = 0; j < 32; ++j) acc[j] = 0.0f;
   for (int l = l_begin; l < l_end; ++l) {
-    float v[32];
+    float v[32], gv[32];
     const int2 *rs = rslot + layers[l].rslot_off;
+    // the G loads go out while the partials are in flight (one memory
+    // latency per layer), through a buffer resource with scalar row offsets
+    const __amdgpu_buffer_rsrc_t gr = buf_rsrc(gtab + (int64_t)l * D, (uint32_t)(D * 4));
+    const int goff = (hi * 1024 + c0 + c) * 4;
+    const LayerDesc &ld = layers[l];
+    tail_gather<32>(ld.rmaxch, rs + hi * 32, rfirst + ld.rslot_off + hi * 32, tail_part_rsrc(ld, part, item_begin, bc, 1024),
+                    (uint32_t)(bc * 1024 * 4), (uint32_t)((bl * 1024 + c0 + c) * 4), ld.item_off, v);
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      const int2 q = rs[hi * 32 + j];
-      const int64_t slot = q.y > 0 ? q.x - item_begin : 0;
-      v[j] = part[(slot * bc + bl) * 1024 + c0 + c];
-    }
-#pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      const int2 q = rs[hi * 32 + j];
-      if (q.y <= 0) v[j] = 0.0f;
-      for (int k = 1; k < q.y; ++k) v[j] += part[((int64_t)(q.x - item_begin + k) * bc + bl) * 1024 + c0 + c];
-    }
+    for (int j = 0; j < 32; ++j) gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(gr, goff, j * 32 * 4096, 0));
     fwht_regs_t<32>(v);
 #pragma unroll
     for (int j = 0; j < 32; ++j) s[(hi * 32 + j) * 32 + c] = v[j];
@@ -458,9 +517,8 @@ __global__ __launch_bounds__(1024) void k_afjl_tail_1024w(const LayerDesc *__res
     for (int j = 0; j < 32; ++j) v[j] = s[(j * 32 + hi) * 32 + c];
     __syncthreads();
     fwht_regs_t<32>(v);
-    const float *g = gtab + (int64_t)l * D + c0 + c;
 #pragma unroll
-    for (int j = 0; j < 32; ++j) acc[j] += g[(int64_t)(j * 32 + hi) * 1024] * v[j];
+    for (int j = 0; j < 32; ++j) acc[j] += gv[j] * v[j];
   }
   float *o = out + (b_begin + bl) * D + c0 + c;
 #pragma unroll
@@ -473,15 +531,20 @@ __global__ __launch_bounds__(1024) void k_afjl_tail_1024w(const LayerDesc *__res
 
 void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
                       int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st) {
-  if (s->R == 1024 && s->Lw == 1024) {
+  // the register tails read each layer's partials through a buffer resource
+  bool small_parts = true;
+  for (int l = l_begin; l < l_end; ++l)
+    small_parts = small_parts && (int64_t)s->layers[l].n_items * bc * s->Lw * 4 < (1ll << 31);
+  if (s->R == 1024 && s->Lw == 1024 && small_parts) {
     const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
-    hipLaunchKernelGGL(k_afjl_tail_1024w, dim3(32u, (unsigned)rows), dim3(1024), 0, st, s->d_layers, s->d_rslot, part,
-                       s->d_gtab, l_begin, l_end, item_begin, s->D, bc, b_begin, out, (int)accumulate);
+    hipLaunchKernelGGL(k_afjl_tail_1024w, dim3(32u, (unsigned)rows), dim3(1024), 0, st, s->d_layers, s->d_rslot,
+                       s->d_rfirst, part, s->d_gtab, l_begin, l_end, item_begin, s->D, bc, b_begin, out,
+                       (int)accumulate);
     SK_CHECK_LAUNCH();
     return;
   }
   const int R = s->R, Lw = s->Lw;
-  if (R <= 64) {
+  if (R <= 64 && small_parts) {
     // balance the layer loop: groups of about equal live destination rows
     TailGroups grp{};
     int64_t total = 0;
@@ -496,12 +559,12 @@ void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin
     }
     grp.bound[++ng] = l_end;
     float *ysum = s->ws + (s->ws_bytes / 4 - (int64_t)kTailGroups * bc * s->D);
-    const int64_t threads = bc * Lw;
+    const int64_t threads = bc * Lw * (R > 32 ? 2 : 1);
     dim3 grid((unsigned)((threads + 255) / 256), (unsigned)ng);
 #define SK_TAIL(RR)                                                                                              \
   case RR:                                                                                                       \
-    hipLaunchKernelGGL(k_afjl_tail_reg<RR>, grid, dim3(256), 0, st, s->d_layers, s->d_rslot, part, s->d_gtab,    \
-                       grp, item_begin, Lw, s->D, bc, b_begin, batch, ysum);                                     \
+    hipLaunchKernelGGL(k_afjl_tail_reg<RR>, grid, dim3(256), 0, st, s->d_layers, s->d_rslot, s->d_rfirst, part,  \
+                       s->d_gtab, grp, item_begin, Lw, s->D, bc, b_begin, batch, ysum);                          \
     break;
     switch (R) {
       SK_TAIL(1) SK_TAIL(2) SK_TAIL(4) SK_TAIL(8) SK_TAIL(16) SK_TAIL(32) SK_TAIL(64)

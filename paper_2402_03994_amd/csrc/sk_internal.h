@@ -30,6 +30,7 @@ struct LayerDesc {
   int32_t rslot_off;  // AFJL: offset of this layer's R (first item, chunk count) pairs
   int32_t item_off;   // AFJL: first fold item of this layer
   int32_t n_items;    // AFJL: fold items of this layer
+  int32_t rmaxch;     // AFJL: most fold items of one destination row
   int32_t m, nc, da, db;  // QK shape and block
   int64_t qk_col;     // QK: first output column of the block
   int64_t fa_off, fb_off;  // QK: element offsets of A (da x m, fp32) and B (db x nc, bf16 hi/lo pairs)
@@ -77,6 +78,7 @@ struct sk_sketch {
   std::vector<sk::FoldItem> items;
   sk::FoldItem *d_items = nullptr;
   int2 *d_rslot = nullptr;     // per layer, per destination row: (first item, chunks)
+  int32_t *d_rfirst = nullptr; // per layer, per destination row: first item, -1 if none
   // FJL transpose: samples sorted by position, per layer
   std::vector<int64_t> fjl_off;  // per layer: offset into the sorted arrays (n_layers+1)
   std::vector<int64_t> fjl_uoff; // per layer: offset into the unique-position arrays
