@@ -116,6 +116,125 @@ __global__ __launch_bounds__(256) void k_affdS_top(const LayerDesc *__restrict__
       fz[(v0 + v) * ld.np + (int64_t)p * 1024 + threadIdx.x + 256 * k] = s[L::idx(v, src[k])] * (1.0f / 32.0f);
 }
 
+// B + C with the stored G (dk1 a multiple of 8): workgroup per (slot, 8 rows
+// p, vector); the vector's live W rows are loaded once for the 8 rows, each
+// row of (H_p (x) I) W is their signed sum, times g, H_l -> rows of F'.  Same
+// arithmetic, in the same order, as k_affdS_top.
+__global__ __launch_bounds__(256) void k_affdS_top8(const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, SmallGroup g,
+                                                    const float *__restrict__ w, int64_t wslot, float *__restrict__ f) {
+  using L = Lds1024<8>;
+  __shared__ __align__(16) float s[L::kFloats];
+  const int z = blockIdx.z;
+  const LayerDesc &ld = layers[g.layer[z]];
+  const int p0 = blockIdx.x * 8;
+  const int64_t v = blockIdx.y;
+  const int nh = (int)ld.rows_live;  // <= kSmallRows
+  const float rs = rsqrtf((float)ld.dk1);
+  const float *wz = w + z * wslot + v * ld.np + threadIdx.x;
+  float wv[kSmallRows][4];
+  int q[kSmallRows];
+#pragma unroll
+  for (int h = 0; h < kSmallRows; ++h) {
+    q[h] = h < nh ? ptab[ld.poff[0][0][0] + h] : 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) wv[h][k] = h < nh ? wz[(int64_t)q[h] * 1024 + 256 * k] : 0.0f;
+  }
+  const float *gz = g.gt[z] + threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int p = p0 + i;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int h = 0; h < kSmallRows; ++h)
+        if (h < nh) acc += flip(wv[h][k], (uint32_t)__popc((uint32_t)(p & q[h])) & 1u);
+      s[L::idx(i, threadIdx.x + 256 * k)] = acc * (gz[(int64_t)p * 1024 + 256 * k] * rs);
+    }
+  }
+  __syncthreads();
+  fwht1024_lds<8>(s);
+  // F'[p][b] = F[p][pi2_l(b)]
+  const uint16_t *p2l = ptab + ld.poff[1][0][1];
+  int src[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) src[k] = p2l[threadIdx.x + 256 * k];
+  float *fz = f + z * wslot + v * ld.np + (int64_t)p0 * 1024 + threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) fz[i * 1024 + 256 * k] = s[L::idx(i, src[k])] * (1.0f / 32.0f);
+}
+
+// D + E for dk1 = 64: workgroup per (32 output columns b, vector); thread
+// (cc = tid % 32, rg = tid / 32) loads rows rg + 8 m (m < 8) of column cc of
+// each slot's F' (128-byte row pieces), H_8 over m in registers, one LDS
+// exchange, H_8 over the low three row bits, then adds rows pi2_p(a) for
+// a = rg + 8 m.  Slots in order; the next slot's loads go out first.
+__global__ __launch_bounds__(256) void k_affdS_cols64(const LayerDesc *__restrict__ layers,
+                                                      const uint16_t *__restrict__ ptab, SmallGroup g, int nslots,
+                                                      const float *__restrict__ f, int64_t wslot, int64_t b_begin,
+                                                      float *__restrict__ out, int accumulate) {
+  __shared__ float s[64 * 33];
+  const int cb = blockIdx.x;
+  const int64_t v = blockIdx.y;
+  const int cc = threadIdx.x & 31, rg = threadIdx.x >> 5;
+  const int64_t np = layers[g.layer[0]].np;  // = D for every slot
+  float acc[8], nx[8];
+#pragma unroll
+  for (int m = 0; m < 8; ++m) acc[m] = 0.0f;
+  auto fetch = [&](int z) {
+    const float *fz = f + z * wslot + v * np + cb * 32 + cc;
+#pragma unroll
+    for (int m = 0; m < 8; ++m) nx[m] = fz[(int64_t)(rg + 8 * m) * 1024];
+  };
+  fetch(0);
+  for (int z = 0; z < nslots; ++z) {
+    float x[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) x[m] = nx[m];
+    if (z + 1 < nslots) fetch(z + 1);
+    fwht_regs_t<8>(x);  // row bits 3..5
+    __syncthreads();    // the previous slot's gathers from s are done
+#pragma unroll
+    for (int m = 0; m < 8; ++m) s[(rg + 8 * m) * 33 + cc] = x[m];
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < 8; ++m) x[m] = s[(8 * rg + m) * 33 + cc];
+    fwht_regs_t<8>(x);  // row bits 0..2
+#pragma unroll
+    for (int m = 0; m < 8; ++m) s[(8 * rg + m) * 33 + cc] = x[m];
+    __syncthreads();
+    const uint16_t *p2 = ptab + layers[g.layer[z]].poff[1][0][0];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc[m] += s[p2[rg + 8 * m] * 33 + cc];
+  }
+  float *o = out + (b_begin + v) * np + cb * 32 + cc;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    float *d = o + (int64_t)(rg + 8 * m) * 1024;
+    const float val = acc[m] * 0.125f;  // 1 / sqrt(dk1)
+    *d = accumulate ? *d + val : val;
+  }
+}
+
+__global__ void k_affdS_gtab(const LayerDesc *__restrict__ layers, int layer, int64_t D, float *__restrict__ gt,
+                             Key key) {
+  const int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  if (t >= D) return;
+  float gq[4];
+  gauss4((uint64_t)t >> 2, (uint32_t)layers[layer].layer_id, ST_GAUSS, key, gq);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) gt[t + q] = gq[q];
+}
+
+void launch_affd_small_gtab(const sk_sketch *s, int layer, float *g, hipStream_t st) {
+  hipLaunchKernelGGL(k_affdS_gtab, dim3((unsigned)((s->D / 4 + 255) / 256)), dim3(256), 0, st, s->d_layers, layer, s->D,
+                     g, s->key);
+  (void)hipGetLastError();
+}
+
 // D + E: workgroup per (16 output columns b, vector); for every slot in order:
 // H_p along the dk1 rows of F'[.][b], add rows pi2_p(a), a < R, to out[a][b].
 // The next slot's tile and row indices are loaded during the current
@@ -204,8 +323,19 @@ void run_affd_small(const sk_sketch *s, const SmallGroup &g, int nslots, int dty
                          s->d_layers, s->d_ptab, g, b_begin, bc, w, wslot, s->key);
   }
   if (!(phases & 2)) return;
-  hipLaunchKernelGGL(k_affdS_top, dim3((unsigned)R, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st, s->d_layers,
-                     s->d_ptab, g, bc, w, wslot, f, s->key);
+  const int dk1 = s->layers[g.layer[0]].dk1;  // = R for every slot (N' = D)
+  if (s->d_gsmall && dk1 % 8 == 0)
+    hipLaunchKernelGGL(k_affdS_top8, dim3((unsigned)(R / 8), (unsigned)bc, zs), dim3(256), 0, st, s->d_layers,
+                       s->d_ptab, g, w, wslot, f);
+  else
+    hipLaunchKernelGGL(k_affdS_top, dim3((unsigned)R, (unsigned)((bc + 7) / 8), zs), dim3(256), 0, st, s->d_layers,
+                       s->d_ptab, g, bc, w, wslot, f, s->key);
+  if (dk1 == 64) {
+    hipLaunchKernelGGL(k_affdS_cols64, dim3(32u, (unsigned)bc), dim3(256), 0, st, s->d_layers, s->d_ptab, g, nslots, f,
+                       wslot, b_begin, out, (int)accumulate);
+    (void)hipGetLastError();
+    return;
+  }
 #define SK_SCOLS(E)                                                                                           \
   hipLaunchKernelGGL(k_affdS_cols<E>, dim3(64u, (unsigned)bc), dim3(256), 0, st, s->d_layers, s->d_ptab, g, nslots, f, \
                      wslot, R, b_begin, out, (int)accumulate)

@@ -74,6 +74,7 @@ void free_all(sk_sketch *s) {
   f(s->d_qkah);
   f(s->d_qkbf);
   f(s->d_mtab);
+  f(s->d_gsmall);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
   s->evpool.clear();
@@ -426,6 +427,21 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       s->mtab_off.assign(n_layers, -1);
     }
   }
+  if (kind == SK_AFFD) {
+    // G of the small-path layers (N' = D floats each)
+    int64_t total = 0;
+    s->gsmall_off.assign(n_layers, -1);
+    for (int l = 0; l < n_layers; ++l)
+      if (affd_small_path(s, l)) {
+        s->gsmall_off[l] = total;
+        total += D;
+      }
+    if (total > 0) {
+      SK_TRY(alloc((void **)&s->d_gsmall, (size_t)total * 4));
+      for (int l = 0; l < n_layers; ++l)
+        if (s->gsmall_off[l] >= 0) launch_affd_small_gtab(s, l, s->d_gsmall + s->gsmall_off[l], nullptr);
+    }
+  }
   if (s->d_gtab) launch_gauss_table(s, s->d_gtab, nullptr);
   if (kind == SK_QK) launch_qk_factors(s, nullptr);
   if (hipDeviceSynchronize() != hipSuccess) {
@@ -659,6 +675,7 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
             for (int j = 0; j < ns; ++j) {
               g.layer[j] = small[i0 + j];
               g.x[j] = grads[small[i0 + j] - l0];
+              g.gt[j] = s->d_gsmall ? s->d_gsmall + s->gsmall_off[small[i0 + j]] : nullptr;
               nsum += s->layers[small[i0 + j]].n;
             }
             for (int64_t t0 = b0; t0 < b0 + bc; t0 += vt) {

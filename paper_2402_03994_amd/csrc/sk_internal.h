@@ -94,6 +94,9 @@ struct sk_sketch {
   // AFFD: precomputed M = H_TT (signs . G) per transposed-path layer
   float *d_mtab = nullptr;
   std::vector<int64_t> mtab_off;  // per layer: float offset into d_mtab, -1 if none
+  // AFFD: G over [0, D) of each small-path layer (N' = D)
+  float *d_gsmall = nullptr;
+  std::vector<int64_t> gsmall_off;  // per layer: float offset into d_gsmall, -1 if none
   // kernel timing
   struct ProfRec {
     int cls;

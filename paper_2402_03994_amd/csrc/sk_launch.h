@@ -37,7 +37,10 @@ constexpr int kSmallMaxDk1 = 512;
 struct SmallGroup {
   int32_t layer[kMaxPtrs];
   const void *x[kMaxPtrs];
+  const float *gt[kMaxPtrs];  // stored G of the layer over [0, D), or null
 };
+// stored G rows of the small-path layers: g[j] = gauss(j) of the layer, j < D
+void launch_affd_small_gtab(const sk_sketch *s, int layer, float *g, hipStream_t st);
 bool affd_small_path(const sk_sketch *s, int layer);
 // workspace bytes per (layer, vector) of a group: W and F, D floats each
 int64_t affd_small_bytes_per_vector(const sk_sketch *s);
