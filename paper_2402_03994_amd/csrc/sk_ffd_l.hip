@@ -26,31 +26,34 @@ __device__ __forceinline__ uint32_t tpos(uint32_t i) { return ((i & 1023u) << 10
 
 enum RowsMode { kRowsX = 0, kRowsZ = 1, kRowsPermFwd = 2, kRowsPermT = 3 };
 
-// Rows kernel: workgroup per (16 rows r0.., block b, vector v).
+// Rows kernel: 1024 threads per (32 rows r0.., block b, vector v).  After the
+// transform thread (ri = tid % 32, rc = tid / 32) holds columns c = 32 rc + m
+// of row r0 + ri, so for each m the 32 lanes of a column write 32 consecutive
+// positions pos = c 1024 + r0 .. r0 + 31: one 128-byte line.
 template <int MODE, bool BF16>
-__global__ __launch_bounds__(256) void k_ffdL_rows(const LayerDesc *__restrict__ layers, int layer,
-                                                   const void *__restrict__ src, int64_t b_begin, int64_t nlive,
-                                                   float *__restrict__ dst, Key key) {
-  using L = Lds1024R;
+__global__ __launch_bounds__(1024) void k_ffdL_rows(const LayerDesc *__restrict__ layers, int layer,
+                                                    const void *__restrict__ src, int64_t b_begin, int64_t nlive,
+                                                    float *__restrict__ dst, Key key) {
+  using L = Lds1024R32;
   __shared__ __align__(16) float s[L::kFloats];
-  __shared__ __align__(16) uint32_t sg[16 * 32];
+  __shared__ __align__(16) uint32_t sg[32 * 32];
   const LayerDesc &ld = layers[layer];
-  int r0 = blockIdx.x * 16;
+  int r0 = blockIdx.x * 32;
   int64_t b = blockIdx.y, v = blockIdx.z;
   if ((MODE == kRowsPermFwd || MODE == kRowsPermT) && (nlive * gridDim.z) % 8 == 0) {
     // workgroup id g runs on XCD g mod 8: XCD x takes (vector, block) pairs
     // x, x + 8, ... one at a time, so its random reads stay in its own L2
-    const int64_t g = blockIdx.x + 64 * (blockIdx.y + nlive * blockIdx.z);
+    const int64_t g = blockIdx.x + 32 * (blockIdx.y + nlive * blockIdx.z);
     const int64_t k = g >> 3;
-    const int64_t pair = 8 * (k >> 6) + (g & 7);
-    r0 = (int)(k & 63) * 16;
+    const int64_t pair = 8 * (k >> 5) + (g & 7);
+    r0 = (int)(k & 31) * 32;
     v = pair / nlive;
     b = pair - v * nlive;
   }
   const int64_t blk = (v * nlive + b) * kD;  // this block in the workspace
   if (MODE == kRowsZ) {
-    // B_b signs of the 16 rows: 8 Philox blocks of 128 per row, shared in LDS
-    if (threadIdx.x < 128) {
+    // B_b signs of the 32 rows: 8 Philox blocks of 128 per row, shared in LDS
+    if (threadIdx.x < 256) {
       const int i = threadIdx.x >> 3;
       const W4 q = philox((uint64_t)((b * kD + (int64_t)(r0 + i) * 1024) >> 7) + (threadIdx.x & 7),
                           (uint32_t)ld.layer_id, ST_SIGN, key);
@@ -61,111 +64,130 @@ __global__ __launch_bounds__(256) void k_ffdL_rows(const LayerDesc *__restrict__
   PermKey pk;
   if (MODE == kRowsPermFwd || MODE == kRowsPermT)
     pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
-  // all 64 loads of a thread are issued before any LDS write
-  float val[16][4];
+  // thread: rows 4 k + quarter (k < 8); all its loads are issued before any LDS write
+  const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+  float val[8][4];
   if (MODE == kRowsPermT) {
     // u_i = g_i w[pi(i)]: four consecutive columns per thread share one Philox block
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t e0 = (uint32_t)(r0 + i) * 1024u + 4u * threadIdx.x;
+    for (int k = 0; k < 8; ++k) {
+      const uint32_t e0 = (uint32_t)(r0 + 4 * k + quarter) * 1024u + 4u * t;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) val[i][q] = ((const float *)src)[blk + tpos(perm_fwd(pk, e0 + q))];
+      for (int q = 0; q < 4; ++q) val[k][q] = ((const float *)src)[blk + tpos(perm_fwd(pk, e0 + q))];
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t e0 = (uint32_t)(r0 + i) * 1024u + 4u * threadIdx.x;
+    for (int k = 0; k < 8; ++k) {
+      const int i = 4 * k + quarter;
+      const uint32_t e0 = (uint32_t)(r0 + i) * 1024u + 4u * t;
       float g[4];
       gauss4((uint64_t)(b * kD + e0) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[L::idx(i, 4 * threadIdx.x + q)] = g[q] * val[i][q];
+      for (int q = 0; q < 4; ++q) s[L::idx(i, 4 * t + q)] = g[q] * val[k][q];
     }
   } else {
+    // thread: columns c = t + 256 q (q < 4), consecutive over the lanes
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int k = 0; k < 8; ++k) {
+      const int i = 4 * k + quarter;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = threadIdx.x + 256 * k;
+      for (int q = 0; q < 4; ++q) {
+        const int c = t + 256 * q;
         const uint32_t e = (uint32_t)(r0 + i) * 1024u + (uint32_t)c;
         if (MODE == kRowsX) {
           const int64_t j = b * kD + e;
           const int64_t x = (b_begin + v) * ld.n + j;
-          val[i][k] = j < ld.n ? (BF16 ? bf16_to_f32(((const uint16_t *)src)[x]) : ((const float *)src)[x]) : 0.0f;
+          val[k][q] = j < ld.n ? (BF16 ? bf16_to_f32(((const uint16_t *)src)[x]) : ((const float *)src)[x]) : 0.0f;
         } else if (MODE == kRowsZ) {
           const uint32_t bit = (sg[i * 32 + (c >> 5)] >> (c & 31)) & 1u;
-          val[i][k] = flip(((const float *)src)[(b_begin + v) * kD + e], bit);
+          val[k][q] = flip(((const float *)src)[(b_begin + v) * kD + e], bit);
         } else {  // kRowsPermFwd: d = e, k = pi^{-1}(d)
-          val[i][k] = ((const float *)src)[blk + tpos(perm_inv(pk, e))];
+          val[k][q] = ((const float *)src)[blk + tpos(perm_inv(pk, e))];
         }
       }
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
+    for (int k = 0; k < 8; ++k)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) s[L::idx(i, threadIdx.x + 256 * k)] = val[i][k];
+      for (int q = 0; q < 4; ++q) s[L::idx(4 * k + quarter, t + 256 * q)] = val[k][q];
   }
   __syncthreads();
-  float e[64];
-  fwht1024_rows16_r(s, e);
-  const int ri = threadIdx.x & 15, rc = threadIdx.x >> 4;
-  float *o = dst + blk + (int64_t)(64 * rc) * 1024 + r0 + ri;
+  float e[32];
+  fwht1024_rows32(s, e);
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
+  // column 32 rc + m, row r0 + ri: byte (32 rc + m) 4096 + 4 (r0 + ri) of the block
+  const __amdgpu_buffer_rsrc_t ws = buf_rsrc(dst + blk + r0, (uint32_t)((kD - r0) * 4));
+  const int soff = (32 * rc * 1024 + ri) * 4;
 #pragma unroll
-  for (int m = 0; m < 64; ++m) o[(int64_t)m * 1024] = e[m] * (1.0f / 32.0f);
+  for (int m = 0; m < 32; ++m)
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m] * (1.0f / 32.0f)), ws, soff, m * 4096, 0);
 }
 
 enum ColsMode { kColsG = 0, kColsPlain = 1, kColsOutT = 2 };
 
-// Cols kernel: workgroup per (16 columns c0.., block b, vector v); the 16
-// columns are 16 contiguous rows of the transposed block.
+// Cols kernel: 1024 threads per (32 columns c0.., block b, vector v); the 32
+// columns are 32 contiguous rows (4 KB each) of the transposed block.  After
+// the transform thread (ri, rc) holds r = 32 rc + m of column c0 + ri:
+// kColsOutT writes the natural order from registers (32 lanes = 32
+// consecutive columns of a row r); the other modes go back through LDS and
+// write pos order with the lanes along r (and gauss4 per 4 columns for g).
 template <int MODE>
-__global__ __launch_bounds__(256) void k_ffdL_cols(const LayerDesc *__restrict__ layers, int layer,
-                                                   const float *__restrict__ src, int64_t b_begin, int64_t nlive,
-                                                   float *__restrict__ dst, void *__restrict__ out, int out_dtype,
-                                                   const float *__restrict__ theta0, Key key) {
-  using L = Lds1024<16>;
-  __shared__ __align__(16) float lds[L::kFloats];
+__global__ __launch_bounds__(1024) void k_ffdL_cols(const LayerDesc *__restrict__ layers, int layer,
+                                                    const float *__restrict__ src, int64_t b_begin, int64_t nlive,
+                                                    float *__restrict__ dst, void *__restrict__ out, int out_dtype,
+                                                    const float *__restrict__ theta0, Key key) {
+  using L = Lds1024R32;
+  __shared__ __align__(16) float s[L::kFloats];
   const LayerDesc &ld = layers[layer];
-  const int c0 = blockIdx.x * 16;
+  const int c0 = blockIdx.x * 32;
   const int64_t b = blockIdx.y, v = blockIdx.z;
   const int64_t blk = (v * nlive + b) * kD;
-  float e[64];
   {
-    const float *p = src + blk + (int64_t)(c0 + (threadIdx.x >> 4)) * 1024 + (threadIdx.x & 15);
+    // thread: rows 4 k + quarter, elements r = 4 t .. 4 t + 3 (16-byte loads)
+    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+    float4 val[8];
 #pragma unroll
-    for (int k = 0; k < 64; ++k) e[k] = p[16 * k];
+    for (int k = 0; k < 8; ++k)
+      val[k] = *(const float4 *)(src + blk + (int64_t)(c0 + 4 * k + quarter) * 1024 + 4 * t);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = 4 * k + quarter;
+      s[L::idx(i, 4 * t)] = val[k].x;
+      s[L::idx(i, 4 * t + 1)] = val[k].y;
+      s[L::idx(i, 4 * t + 2)] = val[k].z;
+      s[L::idx(i, 4 * t + 3)] = val[k].w;
+    }
   }
-  fwht1024_lds_regs<16>(lds, e);
+  __syncthreads();
+  float e[32];
+  fwht1024_rows32(s, e);
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
   if (MODE == kColsOutT) {
-    // natural order: the 16 lanes of a row r write its 16 columns (64 bytes)
-    const int cc = threadIdx.x & 15;
 #pragma unroll 8
-    for (int j = 0; j < 64; ++j) {
-      const int r = (threadIdx.x >> 4) + 16 * j;
-      const int64_t jj = b * kD + (int64_t)r * 1024 + c0 + cc;
+    for (int m = 0; m < 32; ++m) {
+      const int r = 32 * rc + m;
+      const int64_t jj = b * kD + (int64_t)r * 1024 + c0 + ri;
       if (jj < ld.n)
-        store_out(out, out_dtype, (b_begin + v) * ld.n + jj,
-                  lds[L::idx(cc, r)] * (1.0f / 32.0f) + (theta0 ? theta0[jj] : 0.0f));
+        store_out(out, out_dtype, (b_begin + v) * ld.n + jj, e[m] * (1.0f / 32.0f) + (theta0 ? theta0[jj] : 0.0f));
     }
     return;
   }
-  // thread: rows r = tid + 256 j, column groups c0 + 4 q4 .. + 3; writes in pos order
-#pragma unroll 2
-  for (int j = 0; j < 4; ++j) {
-    const int r = threadIdx.x + 256 * j;
+  // back to the block (column c0 + ri at row ri, element r), then thread r
+  // takes the 32 columns of its row
+  __syncthreads();  // every thread's pass-2 reads are done
+  float *bq = s + ri * L::kStride + 33 * rc;
 #pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      const int cb = c0 + 4 * q4;
-      float val[4];
+  for (int m = 0; m < 32; ++m) bq[m] = e[m];
+  __syncthreads();
+  const int r = threadIdx.x;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) val[q] = lds[L::idx(4 * q4 + q, r)] * (1.0f / 32.0f);
-      if (MODE == kColsG) {
-        float g[4];
-        gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + cb) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+  for (int a = 0; a < 8; ++a) {
+    float g[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    if (MODE == kColsG)
+      gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + c0 + 4 * a) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) dst[blk + (int64_t)(cb + q) * 1024 + r] = g[q] * val[q];
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) dst[blk + (int64_t)(cb + q) * 1024 + r] = val[q];
-      }
+    for (int q = 0; q < 4; ++q) {
+      const int cc = 4 * a + q;
+      dst[blk + (int64_t)(c0 + cc) * 1024 + r] = g[q] * (s[L::idx(cc, r)] * (1.0f / 32.0f));
     }
   }
 }
@@ -246,19 +268,19 @@ void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, 
                        float *out, bool accumulate, int phases, hipStream_t st) {
   const int64_t nlive = ffd_live_blocks(s, layer);
   float *A = s->ws, *B = s->ws + bc * nlive * kD;
-  const dim3 gr(64u, (unsigned)nlive, (unsigned)bc);
+  const dim3 gr(32u, (unsigned)nlive, (unsigned)bc);
   if (phases & 1) {
     if (dtype == SK_BF16)
-      hipLaunchKernelGGL((k_ffdL_rows<kRowsX, true>), gr, dim3(256), 0, st, s->d_layers, layer, x, b_begin, nlive, A,
+      hipLaunchKernelGGL((k_ffdL_rows<kRowsX, true>), gr, dim3(1024), 0, st, s->d_layers, layer, x, b_begin, nlive, A,
                          s->key);
     else
-      hipLaunchKernelGGL((k_ffdL_rows<kRowsX, false>), gr, dim3(256), 0, st, s->d_layers, layer, x, b_begin, nlive,
+      hipLaunchKernelGGL((k_ffdL_rows<kRowsX, false>), gr, dim3(1024), 0, st, s->d_layers, layer, x, b_begin, nlive,
                          A, s->key);
   }
   if (phases & 2) {
-    hipLaunchKernelGGL(k_ffdL_cols<kColsG>, gr, dim3(256), 0, st, s->d_layers, layer, A, b_begin, nlive, B, nullptr,
+    hipLaunchKernelGGL(k_ffdL_cols<kColsG>, gr, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B, nullptr,
                        0, nullptr, s->key);
-    hipLaunchKernelGGL((k_ffdL_rows<kRowsPermFwd, false>), gr, dim3(256), 0, st, s->d_layers, layer, B, b_begin,
+    hipLaunchKernelGGL((k_ffdL_rows<kRowsPermFwd, false>), gr, dim3(1024), 0, st, s->d_layers, layer, B, b_begin,
                        nlive, A, s->key);
     hipLaunchKernelGGL(k_ffdL_sum, dim3(128u, (unsigned)bc), dim3(256), 0, st, s->d_layers, layer, A, b_begin, nlive,
                        out, (int)accumulate, s->key);
@@ -270,17 +292,17 @@ void run_ffd_large_T(const sk_sketch *s, int layer, const float *z, int64_t b_be
                      int out_dtype, const float *theta0, int phases, hipStream_t st) {
   const int64_t nlive = ffd_live_blocks(s, layer);
   float *A = s->ws, *B = s->ws + bc * nlive * kD;
-  const dim3 gr(64u, (unsigned)nlive, (unsigned)bc);
+  const dim3 gr(32u, (unsigned)nlive, (unsigned)bc);
   if (phases & 1) {
-    hipLaunchKernelGGL((k_ffdL_rows<kRowsZ, false>), gr, dim3(256), 0, st, s->d_layers, layer, z, b_begin, nlive, A,
+    hipLaunchKernelGGL((k_ffdL_rows<kRowsZ, false>), gr, dim3(1024), 0, st, s->d_layers, layer, z, b_begin, nlive, A,
                        s->key);
-    hipLaunchKernelGGL(k_ffdL_cols<kColsPlain>, gr, dim3(256), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
+    hipLaunchKernelGGL(k_ffdL_cols<kColsPlain>, gr, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
                        nullptr, 0, nullptr, s->key);
-    hipLaunchKernelGGL((k_ffdL_rows<kRowsPermT, false>), gr, dim3(256), 0, st, s->d_layers, layer, B, b_begin, nlive,
+    hipLaunchKernelGGL((k_ffdL_rows<kRowsPermT, false>), gr, dim3(1024), 0, st, s->d_layers, layer, B, b_begin, nlive,
                        A, s->key);
   }
   if (phases & 2)
-    hipLaunchKernelGGL(k_ffdL_cols<kColsOutT>, gr, dim3(256), 0, st, s->d_layers, layer, A, b_begin, nlive, nullptr,
+    hipLaunchKernelGGL(k_ffdL_cols<kColsOutT>, gr, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, nullptr,
                        out, out_dtype, theta0, s->key);
   (void)hipGetLastError();
 }
