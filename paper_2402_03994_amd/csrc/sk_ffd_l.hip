@@ -138,8 +138,18 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols(const LayerDesc *__restrict_
   using L = Lds1024R32;
   __shared__ __align__(16) float s[L::kFloats];
   const LayerDesc &ld = layers[layer];
-  const int c0 = blockIdx.x * 32;
-  const int64_t b = blockIdx.y, v = blockIdx.z;
+  int c0 = blockIdx.x * 32;
+  int64_t b = blockIdx.y, v = blockIdx.z;
+  if (MODE == kColsOutT && theta0) {
+    // workgroup id g runs on XCD g mod 8; the vectors of one (column block,
+    // block) follow each other on one XCD, so theta0 is read from HBM once
+    const int64_t g = blockIdx.x + 32 * (blockIdx.y + nlive * blockIdx.z);
+    const int64_t k = g >> 3, bc = gridDim.z;
+    v = k % bc;
+    const int64_t u = (k / bc) * 8 + (g & 7);
+    c0 = (int)(u & 31) * 32;
+    b = u >> 5;
+  }
   const int64_t blk = (v * nlive + b) * kD;
   {
     // thread: rows 4 k + quarter, elements r = 4 t .. 4 t + 3 (16-byte loads)
