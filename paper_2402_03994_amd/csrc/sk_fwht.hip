@@ -153,6 +153,7 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
                                                    int Lw, float *__restrict__ part, Key key) {
   using LF = Lds1024<BT>;
   __shared__ __align__(16) float s_raw[LF::kFloats > BT * 1024 ? LF::kFloats : BT * 1024];
+  static_assert(kFoldRowsPerItem <= 256, "one thread per source row of an item");
   __shared__ int32_t srow[kFoldRowsPerItem];
   float(*s)[1024] = reinterpret_cast<float(*)[1024]>(s_raw);
   const FoldItem it = items[item_begin + blockIdx.x];

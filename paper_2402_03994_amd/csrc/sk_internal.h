@@ -45,7 +45,7 @@ struct FoldItem {
   int32_t t0, t1;
 };
 
-constexpr int kFoldRowsPerItem = 64;  // AFJL: source rows of one fold work item
+constexpr int kFoldRowsPerItem = 256;  // AFJL: source rows of one fold work item
 constexpr int kTailGroups = 16;  // AFJL tail: parallel layer groups
 struct TailGroups {
   int32_t bound[kTailGroups + 1];
