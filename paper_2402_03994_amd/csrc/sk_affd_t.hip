@@ -452,11 +452,16 @@ __device__ __forceinline__ void affdT_finish8(const LayerDesc &ld, const uint16_
     const int v = e / R, a = e - (e / R) * R;
     if (v < nv) gout[((v0 + v) * 1024 + l) * R + a] = lds[L::idx(v, p2[a])] * sc;
   }
+  __syncthreads();  // the block is free for the workgroup's next item
 }
 }  // namespace
 
+// Persistent: gridDim.x workgroups walk the items (column l, 8 vectors),
+// item = vector group * 1024 + l, workgroup b taking items b, b + G, ...; the
+// slab sequence runs on across items, so the first slab of the next item
+// loads during the last slab (and the final transform) of the current one.
 template <int VB>
-__global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict__ layers,
+__global__ __launch_bounds__(256, 3) void k_affdT_topM(const LayerDesc *__restrict__ layers,
                                                     const uint16_t *__restrict__ ptab, int layer,
                                                     const float *__restrict__ w, int64_t bc, int R,
                                                     const float *__restrict__ mt, int s_first, int nsl,
@@ -466,45 +471,67 @@ __global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict_
   using L = Lds1024<8>;
   __shared__ __align__(16) float lds[L::kFloats];
   __shared__ __align__(16) float sm[kMPad(1024)];
+  __shared__ int32_t s_t[64];  // slab id of group slab j
   const LayerDesc &ld = layers[layer];
   const int TT = 1 << (ld.lgnp - 20);
   const int64_t lo_len = 1ll << 20;
-  const int64_t l = blockIdx.x;
-  const int64_t v0 = (int64_t)blockIdx.y * 8;
-  const int nv = (int)((bc - v0) < 8 ? (bc - v0) : 8);
-  uint64_t live, sgn;
-  masks_t(ld, ptab, TT, live, sgn);
+  const int64_t nitems = 1024 * ((bc + 7) / 8);
+  const int64_t G = gridDim.x;
+  int64_t item = blockIdx.x;
+  if (item >= nitems) return;  // uniform over the workgroup
+  if (threadIdx.x == 0) {
+    uint64_t live, sgn;
+    masks_t(ld, ptab, TT, live, sgn);
+    uint64_t rest = live;  // never empty: slab 0 holds source row 0
+    for (int q = 0; q < s_first; ++q) rest &= rest - 1;
+    for (int q = 0; q < nsl; ++q) {
+      s_t[q] = __builtin_ctzll(rest);
+      rest &= rest - 1;
+    }
+  }
+  __syncthreads();
   const int i = threadIdx.x >> 5, c = threadIdx.x & 31;
-  // rows of absent vectors (i >= nv) load vector v0's data and are discarded
-  const int64_t vi = v0 + (i < nv ? i : 0);
-  const float *src = w + vi * vstride + l * 1024 + c;
-  const float *mcol = mt + l * 1024 + 4 * threadIdx.x;
   float4 *mst = (float4 *)(sm + kMPad(4 * threadIdx.x));
   const float4 *mld = (const float4 *)(sm + kMPad(32 * c));
   float *b1 = lds + i * L::kStride + c;       // column c + 32 k at 33 k
   float *b2 = lds + i * L::kStride + 33 * c;  // column 32 c + m at m
+  // an item's scalars; its pointers are formed where they are used
+  struct Item {
+    int64_t l, v0;
+    int nv;
+  };
+  auto open = [&](int64_t it) {
+    Item r;
+    r.l = it & 1023;
+    r.v0 = (it >> 10) * 8;
+    r.nv = (int)((bc - r.v0) < 8 ? (bc - r.v0) : 8);
+    return r;
+  };
+  // rows of absent vectors (i >= nv) load vector v0's data and are discarded
+  auto vrow = [&](const Item &it) { return it.v0 + (i < it.nv ? i : 0); };
+  auto fvp = [&](const Item &it) { return facc + (vrow(it) * 1024 + it.l) * 1024 + 32 * c; };  // F at p = 32 c + m
   float f[32];
-  float *fv = facc + (vi * 1024 + l) * 1024 + 32 * c;  // F at p = 32 c + m
-  if (fmode & 1) {
+  auto init_f = [&](const Item &it) {
+    if (fmode & 1) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const float4 u = ((const float4 *)fv)[q];
-      f[4 * q] = u.x;
-      f[4 * q + 1] = u.y;
-      f[4 * q + 2] = u.z;
-      f[4 * q + 3] = u.w;
+      for (int q = 0; q < 8; ++q) {
+        const float4 u = ((const float4 *)fvp(it))[q];
+        f[4 * q] = u.x;
+        f[4 * q + 1] = u.y;
+        f[4 * q + 2] = u.z;
+        f[4 * q + 3] = u.w;
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 32; ++m) f[m] = 0.0f;
     }
-  } else {
+  };
+  auto fetch = [&](const Item &it, int j, float(&e)[32], float4 &mv) {
+    // W^T of group slab j, M of slab s_t[j]
+    const float *src = w + vrow(it) * vstride + j * lo_len + it.l * 1024 + c;
 #pragma unroll
-    for (int m = 0; m < 32; ++m) f[m] = 0.0f;
-  }
-  // group slab j (slab t): W^T at src + j 2^20, M at mcol + t 2^20
-  int j = 0;
-  auto fetch = [&](int t, float(&e)[32], float4 &mv) {
-#pragma unroll
-    for (int k = 0; k < 32; ++k) e[k] = src[j * lo_len + 32 * k];
-    mv = *(const float4 *)(mcol + t * lo_len);
-    ++j;
+    for (int k = 0; k < 32; ++k) e[k] = src[32 * k];
+    mv = *(const float4 *)(mt + (int64_t)s_t[j] * lo_len + it.l * 1024 + 4 * threadIdx.x);
   };
   auto step = [&](float(&e)[32], const float4 &mv) {
     fwht_regs_t<32>(e);
@@ -525,38 +552,55 @@ __global__ __launch_bounds__(256) void k_affdT_topM(const LayerDesc *__restrict_
     }
     __syncthreads();  // before the next slab's writes of lds and sm
   };
-  uint64_t rest = live;  // never empty: slab 0 holds source row 0
-  for (int q = 0; q < s_first; ++q) rest &= rest - 1;
-  int left = nsl;  // >= 1
-  auto next = [&]() {
-    const int t = __builtin_ctzll(rest);
-    rest &= rest - 1;
-    --left;
-    return t;
+  auto end_item = [&](const Item &it) {
+    if (!(fmode & 2)) {
+      if (i < it.nv) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          ((float4 *)fvp(it))[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
+      }
+      return;
+    }
+    // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
+    affdT_finish8(ld, ptab, f, lds, it.l, it.v0, it.nv, R, 1.0f / (32768.0f * (float)TT), gout);
+  };
+  Item cur = open(item), nx = cur;
+  init_f(cur);
+  int j = 0;
+  // one slab: prefetch the next (item, slab) into the other register set,
+  // transform this one; false at the end of the workgroup's items
+  auto iter = [&](float(&ec)[32], float4 &mc, float(&en)[32], float4 &mn) {
+    int jn = j + 1;
+    int64_t itn = item;
+    if (jn == nsl) {
+      jn = 0;
+      itn = item + G;
+    }
+    const bool more = itn < nitems;
+    if (more) {
+      if (jn == 0) nx = open(itn);
+      fetch(jn == 0 ? nx : cur, jn, en, mn);
+    }
+    step(ec, mc);
+    if (j == nsl - 1) {
+      end_item(cur);
+      if (more) {
+        cur = nx;
+        init_f(cur);
+      }
+    }
+    item = itn;
+    j = jn;
+    return more;
   };
   float ea[32], eb[32];
   float4 ma, mb;
-  fetch(next(), ea, ma);
+  fetch(cur, 0, ea, ma);
 #pragma unroll 1
   for (;;) {
-    bool more = left > 0;
-    if (more) fetch(next(), eb, mb);
-    step(ea, ma);
-    if (!more) break;
-    more = left > 0;
-    if (more) fetch(next(), ea, ma);
-    step(eb, mb);
-    if (!more) break;
+    if (!iter(ea, ma, eb, mb)) break;
+    if (!iter(eb, mb, ea, ma)) break;
   }
-  if (!(fmode & 2)) {
-    if (i < nv) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) ((float4 *)fv)[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
-    }
-    return;
-  }
-  // H_l of phase A, H_p twice (1/32 each) and H_TT (1/TT)
-  affdT_finish8(ld, ptab, f, lds, l, v0, nv, R, 1.0f / (32768.0f * (float)TT), gout);
 }
 
 void launch_affd_mtab(const sk_sketch *s, int layer, float *m, hipStream_t st) {
@@ -738,7 +782,17 @@ void run_affd_transposed(const sk_sketch *s, int layer, const void *x, int dtype
   }
   if (!(phases & 2)) return;
   if (grp.compact) {
-    hipLaunchKernelGGL(k_affdT_topM<8>, dim3(1024u, (unsigned)((bc + 7) / 8)), dim3(256), 0, st, s->d_layers,
+    static int resident = 0;  // workgroups of the top kernel resident on the device at once
+    if (!resident) {
+      int per_cu = 0, cus = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_affdT_topM<8>, 256, 0) != hipSuccess || per_cu < 1)
+        per_cu = 1;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, s->device) != hipSuccess || cus < 1)
+        cus = 1;
+      resident = per_cu * cus;
+    }
+    const int64_t nitems = 1024 * ((bc + 7) / 8);
+    hipLaunchKernelGGL(k_affdT_topM<8>, dim3((unsigned)std::min<int64_t>(nitems, resident)), dim3(256), 0, st, s->d_layers,
                        s->d_ptab, layer, w, bc, R, s->d_mtab + s->mtab_off[layer], grp.s_first, grp.nsl, vstride,
                        grp.facc, grp.fmode, gbuf);
     (void)hipGetLastError();
