@@ -184,11 +184,15 @@ int sketch_debug_stream(sk_sketch *s, int32_t layer, int32_t stream_id, uint64_t
 
 /*
  * Kernel timing (diagnostics and roofline reports).  While profiling is on,
- * every group of kernel launches a call issues is bracketed by HIP events on
- * that call's stream, tagged with a kernel class and the algorithmic bytes the
- * group moves (inputs read once plus outputs written once).
- * sketch_profile(s, 1) allocates the event pool (up to 16384 groups) and clears
- * the record; sketch_profile(s, 0) stops recording.  sketch_profile_read()
+ * every group of kernel launches of a selected class that a call issues is
+ * bracketed by HIP events on that call's stream, tagged with the class and the
+ * algorithmic bytes the group moves (inputs read once plus outputs written
+ * once).  sketch_profile(s, classes) with a nonzero bit mask (bit c selects
+ * class c below; SK_PROF_ALL selects every class) allocates the event pool (up
+ * to 16384 groups) on first use and clears the record; sketch_profile(s, 0)
+ * stops recording; bits outside SK_PROF_ALL give SK_EINVAL.  Each event pair
+ * costs a little device time, so selecting only the class of interest keeps
+ * the timed stream closest to an unprofiled one.  sketch_profile_read()
  * waits for the recorded events and fills, per class (arrays of
  * SK_PROF_CLASSES entries), the summed duration in ms, the number of groups
  * and the summed algorithmic bytes, then clears the record.
@@ -207,7 +211,8 @@ enum {
   SK_PROF_QK_XB = 10,    /* QK first contraction X B^T (reads the gradients) */
   SK_PROF_CLASSES = 11
 };
-int sketch_profile(sk_sketch *s, int enable);
+#define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
+int sketch_profile(sk_sketch *s, uint32_t classes);
 int sketch_profile_read(sk_sketch *s, double *ms, int64_t *count, int64_t *bytes);
 
 /* Thread-local message describing the last failure of this thread. */

@@ -55,7 +55,7 @@ def load() -> ctypes.CDLL:
     L.sketch_query.restype = ctypes.c_int
     L.sketch_debug_stream.argtypes = [P, i32, i32, u64, u64, u64, P]
     L.sketch_debug_stream.restype = ctypes.c_int
-    L.sketch_profile.argtypes = [P, ctypes.c_int]
+    L.sketch_profile.argtypes = [P, ctypes.c_uint32]
     L.sketch_profile.restype = ctypes.c_int
     L.sketch_profile_read.argtypes = [P, P, P, P]
     L.sketch_profile_read.restype = ctypes.c_int

@@ -88,7 +88,7 @@ struct ProfScope {
   int idx = -1;
   hipStream_t st;
   ProfScope(sk_sketch *s_, int cls, int64_t bytes, hipStream_t st_) : s(s_), st(st_) {
-    if (!s->prof || s->evnext + 2 > (int)s->evpool.size()) return;
+    if (!((s->prof_mask >> cls) & 1u) || s->evnext + 2 > (int)s->evpool.size()) return;
     idx = s->evnext;
     s->evnext += 2;
     s->recs.push_back(sk_sketch::ProfRec{cls, idx, bytes});
@@ -820,10 +820,11 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
   return SK_OK;
 }
 
-int sketch_profile(sk_sketch *s, int enable) {
+int sketch_profile(sk_sketch *s, uint32_t classes) {
   if (!s) return fail(SK_EINVAL, "sketch is NULL");
+  if (classes & ~(uint32_t)SK_PROF_ALL) return fail(SK_EINVAL, "unknown kernel class in profiling mask");
   DeviceGuard guard(s->device);
-  if (enable) {
+  if (classes) {
     if (s->evpool.empty()) {
       s->evpool.resize(2 * 16384);
       for (auto &e : s->evpool) SK_HIP(hipEventCreate(&e));
@@ -831,7 +832,7 @@ int sketch_profile(sk_sketch *s, int enable) {
     s->evnext = 0;
     s->recs.clear();
   }
-  s->prof = enable != 0;
+  s->prof_mask = classes;
   return SK_OK;
 }
 

@@ -103,7 +103,7 @@ struct sk_sketch {
     int ev;
     int64_t bytes;
   };
-  bool prof = false;
+  uint32_t prof_mask = 0;  // classes whose launch groups are timed
   std::vector<hipEvent_t> evpool;
   int evnext = 0;
   std::vector<ProfRec> recs;

@@ -104,9 +104,19 @@ class Sketch:
                                            n_layers, _stream_ptr(self.device)))
         return outs
 
-    def profile(self, enable: bool = True) -> None:
-        """Start (clearing earlier records) or stop per-kernel-class event timing."""
-        _lib.check(self.lib.sketch_profile(self._h, int(enable)))
+    def profile(self, enable: bool = True, classes=None) -> None:
+        """Start (clearing earlier records) or stop per-kernel-class event timing.
+
+        classes: names from PROF_CLASSES to time (default: all of them)."""
+        if not enable:
+            mask = 0
+        elif classes is None:
+            mask = (1 << len(_lib.PROF_CLASSES)) - 1
+        else:
+            mask = 0
+            for c in classes:
+                mask |= 1 << _lib.PROF_CLASSES.index(c)
+        _lib.check(self.lib.sketch_profile(self._h, mask))
 
     def profile_read(self) -> dict:
         """{class: (ms, groups, algorithmic bytes)} recorded since profile(True); clears the record."""
