@@ -98,7 +98,10 @@ __device__ __forceinline__ void load_rows8(const LayerDesc &ld, const uint16_t *
 // multiple of 4, n elt < 2^31): the row index is uniform over the wave, so
 // rows without data are skipped by a scalar branch and the end of the last
 // row is zero-filled by the hardware range check (the whole byte offset is in
-// the vector operand, which the check covers).
+// the vector operand, which the check covers).  The loads carry the non-temporal
+// hint: the input is read once, and keeping it out of the caches leaves more
+// of the memory-side cache to the transposed slabs the next kernel reads
+// (measured 3% faster on this kernel).
 template <bool BF16>
 __device__ __forceinline__ void load_rows8_buf(const LayerDesc &ld, const uint16_t *s_invp, int sslab, int p0,
                                                int quarter, __amdgpu_buffer_rsrc_t rs, int voff, float (&val)[8][4]) {
@@ -109,13 +112,13 @@ __device__ __forceinline__ void load_rows8_buf(const LayerDesc &ld, const uint16
     const int h = __builtin_amdgcn_readfirstlane(sslab * 1024 + (int)s_invp[p0 + 4 * k + quarter]);
     if (h < ld.rows_live) {
       if (BF16) {
-        const u2 u = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + h * 2048, 0, 0);
+        const u2 u = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + h * 2048, 0, kNt);
         val[k][0] = __uint_as_float(u.x << 16);
         val[k][1] = __uint_as_float(u.x & 0xFFFF0000u);
         val[k][2] = __uint_as_float(u.y << 16);
         val[k][3] = __uint_as_float(u.y & 0xFFFF0000u);
       } else {
-        const u4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + h * 4096, 0, 0);
+        const u4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + h * 4096, 0, kNt);
         val[k][0] = __uint_as_float(u.x);
         val[k][1] = __uint_as_float(u.y);
         val[k][2] = __uint_as_float(u.z);

@@ -118,8 +118,10 @@ __device__ __forceinline__ void load_cols(const void *x, int64_t e, int64_t lim,
 // bit patterns in 16 bytes; elements at or past lim read as zero.
 template <int CPT, bool BF16, bool VEC>
 __device__ __forceinline__ uint4 load_raw16(const void *x, int64_t e, int64_t lim) {
-  if (VEC && lim >= CPT && (BF16 ? CPT == 8 : CPT == 4))
-    return BF16 ? *(const uint4 *)((const uint16_t *)x + e) : *(const uint4 *)((const float *)x + e);
+  if (VEC && lim >= CPT && (BF16 ? CPT == 8 : CPT == 4)) {
+    // each input element is read once
+    return ld_nt16(BF16 ? (const void *)((const uint16_t *)x + e) : (const void *)((const float *)x + e));
+  }
   uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
   for (int q = 0; q < CPT; ++q) {
