@@ -708,7 +708,10 @@ int affd_transposed_nlive(const sk_sketch *s, int layer) {
 // Vectors per call and live slabs per group.  A layer whose live slabs for 8
 // vectors (the vectors of one top workgroup) fit the budget takes a multiple
 // of 8 vectors that keeps one call's W^T (4 MB per vector and live slab)
-// within the 256 MB memory-side cache between the row and top kernels.  A
+// within the size of the 256 MB memory-side cache between the row and top
+// kernels (measured on the GPT-2-small workload: 256 MB 31.0 ms per step,
+// 192 MB 31.5, 128 MB 33.7, 512 MB 32.3: larger calls amortise the ramp of
+// each launch, W^T beyond the cache slows the top kernel).  A
 // larger layer takes 16 vectors (W^T then goes through HBM), and with the
 // stored M tables, if the workspace cannot hold all their live slabs, as many
 // slabs per group as fit, F being carried between the groups.  Without the
@@ -719,7 +722,7 @@ AffdTPlan affd_transposed_plan(const sk_sketch *s, int layer) {
   AffdTPlan pl{0, nlive, false};
   if (!affd_transposed_path(s, layer)) return pl;
   const char *e = std::getenv("SK_AFFD_MALL_MB");
-  const int64_t budget = std::max<int64_t>(1, e ? std::atoll(e) : 192) << 20;
+  const int64_t budget = std::max<int64_t>(1, e ? std::atoll(e) : 256) << 20;
   const int64_t wbytes = (int64_t)nlive * (4ll << 20);
   pl.compact = s->d_mtab && s->mtab_off[layer] >= 0;
   if (!pl.compact && ld.lgnp - 20 > 3) return pl;
