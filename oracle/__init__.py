@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for the structured sketches (FJL, FFD, AFFD, AFJL, QK).
+"""fp64 CPU oracle for the structured sketches (FJL, FFD, AFFD, AFJL, QK, QKH, AFJLQ).
 
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import this package.  The product
@@ -7,7 +7,8 @@ library never imports it; the two share no code.
 The arithmetic lives in ``sk_oracle.c`` (plain C, double precision, textbook
 Walsh-Hadamard transform, literal operator chains of the paper's equations
 ailon_chazelle, fastfood, bami, frikadel and straight).  This module only
-marshals numpy arrays into that library.
+marshals numpy arrays into that library.  The kinds with the random-orthogonal
+Kronecker pre-conditioner (QKH, AFJLQ) are in ``qhaar.py`` (numpy, fp64).
 """
 from __future__ import annotations
 
@@ -22,8 +23,10 @@ _SRC = os.path.join(_HERE, "sk_oracle.c")
 _LIB = os.path.join(_HERE, "libsk_oracle.so")
 
 KINDS = {"fjl": 0, "ffd": 1, "affd": 2, "afjl": 3, "qk": 4}
+# kinds with the random-orthogonal Kronecker pre-conditioner (numpy, qhaar.py)
+QKINDS = ("qkh", "afjlq")
 DTYPES = {"f32": 0, "bf16": 1}
-STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8}
+STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}
 
 
 def build() -> str:
@@ -160,6 +163,9 @@ def apply(kind: str, shapes, D: int, seed: int, xs, dtype: str = "f32", layer0: 
     shapes: per layer (rows, cols[, dA, dB]); xs: per layer an array [batch, rows*cols]
     (float32 for "f32", uint16 bf16 bit patterns for "bf16").  Layers carry RNG
     layer ids layer0, layer0+1, ...  Returns fp64 [batch, D]."""
+    if kind in QKINDS:
+        from . import qhaar
+        return qhaar.apply(kind, shapes, D, seed, xs, dtype, layer0)
     rows, cols, da, db = _shape_arrays(shapes)
     want = np.float32 if dtype == "f32" else np.uint16
     arrs = [np.ascontiguousarray(x, dtype=want) for x in xs]
@@ -179,6 +185,9 @@ def apply_T(kind: str, shapes, D: int, seed: int, z: np.ndarray, layer0: int = 0
             qk_bf16: bool = False, theta0=None):
     """Transpose S^T z of a batch z [batch, D]; returns a list of fp64 [batch, rows*cols].
     With theta0 (a list of per-layer vectors or None entries) the result is theta0 + S^T z."""
+    if kind in QKINDS:
+        from . import qhaar
+        return qhaar.apply_T(kind, shapes, D, seed, z, layer0, theta0)
     rows, cols, da, db = _shape_arrays(shapes)
     z = np.ascontiguousarray(z, dtype=np.float64)
     batch = z.shape[0]
