@@ -16,16 +16,23 @@
  *   SK_QK    Y = A X B^T per weight matrix X (m x n), A (dA x m) ~ N(0,1/dA),
  *            B (dB x n) ~ N(0,1/dB)                       (eq. straight with two
  *            Kronecker factors, contraction of eq. qk_proof_tensor_dec)
+ *   SK_QKH   y = sqrt(N/D) R_D Q_N x                      (eq. straight on the
+ *            flattened layer: Q_N is the Kronecker product of Haar-orthogonal
+ *            factors of the sizes of N, restricted to their first D_i rows)
+ *   SK_AFJLQ y = sqrt(N/D) G R_D Q_N x                    (eq. frikadel with the
+ *            pre-conditioner H_N replaced by Q, Sec. 3 "Alternative
+ *            pre-conditioners")
  *
  * H_N is the normalised Walsh-Hadamard matrix (appendix definition), R_D keeps
  * the first D coordinates, B is a diagonal of random signs, G a diagonal of
  * N(0,1) entries, and pi1/pi2 permute digits within the Kronecker factors of N
  * (Sec. 3, "Removing the lookup bottleneck"; factors of at most 1024).
  *
- * Per layer l with n_l = rows*cols elements the FWHT kinds work on the padded
- * length N'_l = 2^ceil(log2 max(n_l, D)) (padding is virtual: never read or
- * written).  The FWHT kinds sum independent per-layer sketches (each with its
- * own random streams, keyed on the layer's index in the list), which is the
+ * Per layer l with n_l = rows*cols elements the FWHT kinds (and SK_QKH,
+ * SK_AFJLQ) work on the padded length N'_l = 2^ceil(log2 max(n_l, D)) (padding
+ * is virtual: never read or written).  They sum independent per-layer sketches
+ * (each with its own random streams, keyed on the layer's index in the list),
+ * which is the
  * per-shard lift followed by a sum of the paper's model-parallel appendix.  QK
  * concatenates the dA*dB blocks of its layers in list order (sum dA*dB = D).
  *
@@ -57,7 +64,7 @@
 extern "C" {
 #endif
 
-typedef enum { SK_FJL = 0, SK_FFD = 1, SK_AFFD = 2, SK_AFJL = 3, SK_QK = 4 } sk_kind;
+typedef enum { SK_FJL = 0, SK_FFD = 1, SK_AFFD = 2, SK_AFJL = 3, SK_QK = 4, SK_QKH = 5, SK_AFJLQ = 6 } sk_kind;
 typedef enum { SK_F32 = 0, SK_BF16 = 1 } sk_dtype;
 
 enum {
@@ -100,7 +107,12 @@ enum {
   SK_STREAM_PI1 = 5,     /* digit permutation before the first H           */
   SK_STREAM_PI2 = 6,     /* digit permutation after the second H (AFFD)    */
   SK_STREAM_QKA = 7,     /* QK left factor                                 */
-  SK_STREAM_QKB = 8      /* QK right factor                                */
+  SK_STREAM_QKB = 8,     /* QK right factor                                */
+  SK_STREAM_QH = 9       /* SK_QKH / SK_AFJLQ factor k of a layer: Gaussian
+                            numbers k 2^20 + r b + c form the b x b matrix
+                            whose normalised QR factor (R with a positive
+                            diagonal) is factor k; computed in fp64 on the
+                            host at creation, stored in fp32               */
 };
 
 /*
@@ -109,6 +121,8 @@ enum {
  *   shapes    host array of n_layers >= 1 layer shapes (rows, cols >= 1).
  *   D         target dimension.  FWHT kinds: a power of two, 16 <= D <= 2^20
  *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
+ *             SK_QKH, SK_AFJLQ: a power of two, 2048 <= D <= 2^20 (smaller D
+ *             is SK_EUNSUPPORTED by the kernels).
  *   seed      64-bit key of every random stream.
  *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).
  * On success *out receives the handle (destroy with sketch_destroy).  The
@@ -209,7 +223,9 @@ enum {
   SK_PROF_OTHER = 8,
   SK_PROF_AFFD_ROWS = 9, /* AFFD row kernel: load, sign, pi1, H_l (one launch) */
   SK_PROF_QK_XB = 10,    /* QK first contraction X B^T (reads the gradients) */
-  SK_PROF_CLASSES = 11
+  SK_PROF_QH_FIRST = 11, /* SK_QKH/SK_AFJLQ contraction that reads the input */
+  SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ second contraction (and transpose) */
+  SK_PROF_CLASSES = 13
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

@@ -7,15 +7,15 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsketch.so")
 
-SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK = range(5)
+SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ = range(7)
 SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
-STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8}
+STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}
 EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", "sketch_query",
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
            "sketch_status_string")
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
-                "affd_rows", "qk_xb"]
+                "affd_rows", "qk_xb", "qh_first", "qh_second"]
 
 
 class LayerShape(ctypes.Structure):

@@ -75,12 +75,16 @@ void free_all(sk_sketch *s) {
   f(s->d_qkbf);
   f(s->d_mtab);
   f(s->d_gsmall);
+  f(s->d_qh);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
   s->evpool.clear();
 }
 
 bool fwht_kind(int k) { return k == SK_FJL || k == SK_FFD || k == SK_AFFD || k == SK_AFJL; }
+bool q_kind(int k) { return k == SK_QKH || k == SK_AFJLQ; }
+// kinds on the padded per-layer length N' with its Kronecker digits
+bool padded_kind(int k) { return fwht_kind(k) || q_kind(k); }
 
 // Brackets a group of launches with a pair of pooled events when profiling.
 struct ProfScope {
@@ -126,6 +130,10 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
         else
           b = 2 * ffd_live_blocks(s, l) * s->D * 4;
         break;
+      case SK_QKH:
+      case SK_AFJLQ:
+        b = qh_bytes_per_vector(s, l, transpose);
+        break;
       case SK_QK:  // T = X B^T (m x dB) or, A first, U = A X (dA x n)
         b = std::max((int64_t)ld.m * ld.db, (int64_t)ld.da * ld.nc) * 4;
         break;
@@ -170,7 +178,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
                   uint32_t flags, int32_t device, sk_sketch **out) {
   if (!out) return fail(SK_EINVAL, "out is NULL");
   *out = nullptr;
-  if ((int)kind < 0 || (int)kind > 4) return fail(SK_EINVAL, "unknown sketch kind");
+  if ((int)kind < 0 || (int)kind > 6) return fail(SK_EINVAL, "unknown sketch kind");
   if (!shapes || n_layers < 1) return fail(SK_EINVAL, "need at least one layer shape");
   if (flags & ~SK_FLAG_AFFD_NO_MTAB) return fail(SK_EINVAL, "unknown flags");
   for (int l = 0; l < n_layers; ++l) {
@@ -179,9 +187,10 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     if (shapes[l].rows > (1ll << 40) / shapes[l].cols)
       return fail(SK_EUNSUPPORTED, "layer " + std::to_string(l) + " too large");
   }
-  if (fwht_kind(kind)) {
+  if (padded_kind(kind)) {
     if (!is_pow2(D)) return fail(SK_EINVAL, "D must be a power of two");
-    if (D < 16) return fail(SK_EUNSUPPORTED, "D < 16 is not supported by the kernels");
+    if (D < (q_kind(kind) ? 2048 : 16))
+      return fail(SK_EUNSUPPORTED, std::string("D < ") + (q_kind(kind) ? "2048" : "16") + " is not supported by the kernels");
     if (D > (1ll << 20)) return fail(SK_EUNSUPPORTED, "D > 2^20 is not supported by the kernels");
   } else {
     int64_t tot = 0;
@@ -218,7 +227,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     ld.n = shapes[l].rows * shapes[l].cols;
     ld.layer_id = l;
     s->total_numel += ld.n;
-    if (fwht_kind(kind)) {
+    if (padded_kind(kind)) {
       ld.np = 1;
       while (ld.np < std::max(ld.n, D)) ld.np <<= 1;
       ld.lgnp = ilog2(ld.np);
@@ -281,6 +290,19 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
   s->qk_a_elems = fac_a;
   s->qk_b_elems = fac_b;
+  int64_t qh_floats = 0;
+  if (q_kind(kind)) {
+    for (int l = 0; l < n_layers; ++l) {
+      LayerDesc &ld = s->layers[l];
+      if (qh_plan_layer(ld, D) != SK_OK) {
+        free_all(s);
+        delete s;
+        return fail(SK_EUNSUPPORTED, "layer " + std::to_string(l) + ": Kronecker shape not supported");
+      }
+      ld.qoff = qh_floats;
+      qh_floats += (qh_layer_floats(ld) + 3) & ~3ll;  // 16-byte aligned blocks
+    }
+  }
 
   // AFJL work items: destination rows r of an R x Lw accumulator.
   std::vector<int2> rslot;
@@ -368,7 +390,18 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_layers, sizeof(LayerDesc) * n_layers));
   SK_TRY(alloc((void **)&s->d_ptab, sizeof(uint16_t) * ptab.size()));
   s->h_ptab = ptab;
-  if (kind == SK_AFJL || kind == SK_FJL) SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
+  if (kind == SK_AFJL || kind == SK_FJL || kind == SK_AFJLQ)
+    SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
+  if (qh_floats > 0) {
+    SK_TRY(alloc((void **)&s->d_qh, sizeof(float) * qh_floats));
+    std::vector<float> host((size_t)qh_floats, 0.0f);
+    qh_generate_factors(s, host);
+    if (hipMemcpy(s->d_qh, host.data(), sizeof(float) * qh_floats, hipMemcpyHostToDevice) != hipSuccess) {
+      free_all(s);
+      delete s;
+      return fail(SK_EHIP, std::string("hipMemcpy: ") + hipGetErrorString(hipGetLastError()));
+    }
+  }
   SK_TRY(alloc((void **)&s->d_items, sizeof(FoldItem) * s->items.size()));
   SK_TRY(alloc((void **)&s->d_rslot, sizeof(int2) * rslot.size()));
   std::vector<int32_t> rfirst(rslot.size());
@@ -725,6 +758,16 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         }
         break;
       }
+      case SK_QKH:
+      case SK_AFJLQ:
+        for (int l = l0; l < l1; ++l) {
+          const bool acc = accumulate || l > l0;
+          SK_PROF(SK_PROF_QH_FIRST, bc * s->layers[l].n * esz,
+                  run_qh_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 1, st));
+          SK_PROF(SK_PROF_QH_SECOND, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                  run_qh_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 2, st));
+        }
+        break;
       case SK_QK:
         for (int l = l0; l < l1; ++l) {
           SK_PROF(SK_PROF_QK_XB, bc * s->layers[l].n * esz,
@@ -807,6 +850,10 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
             SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(w2, bc * nlive, lgD, st));
             SK_PROF(SK_PROF_GATHER, obytes, launch_ffd_T_out(s, l, w2, b0, bc, o, out_dtype, th, st));
           }
+          break;
+        case SK_QKH:
+        case SK_AFJLQ:
+          SK_PROF(SK_PROF_QH_SECOND, obytes, run_qh_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
           break;
         case SK_QK:
           SK_PROF(SK_PROF_QK, obytes + bc * ld.da * ld.db * 4,

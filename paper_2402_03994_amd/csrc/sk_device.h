@@ -34,6 +34,7 @@ enum Stream : uint32_t {
   ST_PI2 = 6,
   ST_QKA = 7,
   ST_QKB = 8,
+  ST_QH = 9,
 };
 
 struct Key {

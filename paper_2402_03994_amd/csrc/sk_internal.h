@@ -36,6 +36,9 @@ struct LayerDesc {
   int64_t fa_off, fb_off;  // QK: element offsets of A (da x m, fp32) and B (db x nc, bf16 hi/lo pairs)
   int32_t lo_len_lg;  // AFFD: log2 of the low block spanned by c < D
   uint32_t hstar;     // AFFD: top-digit index of pi2 at the all-zero low part
+  int32_t qbm, qdm;   // QKH/AFJLQ: size of factor K-2 and its rows kept (D / 1024)
+  int64_t qP;         // QKH/AFJLQ: slabs of qbm x 1024 (product of the leading factors)
+  int64_t qoff;       // QKH/AFJLQ: float offset of the layer's A, A^T, Qt, Qt^T, w
 };
 
 // AFJL fold work item: rows t in [t0, t1) of destination row r of a layer.
@@ -97,6 +100,8 @@ struct sk_sketch {
   // AFFD: G over [0, D) of each small-path layer (N' = D)
   float *d_gsmall = nullptr;
   std::vector<int64_t> gsmall_off;  // per layer: float offset into d_gsmall, -1 if none
+  // QKH / AFJLQ: per layer A, A^T, Qt, Qt^T, w (fp32)
+  float *d_qh = nullptr;
   // kernel timing
   struct ProfRec {
     int cls;

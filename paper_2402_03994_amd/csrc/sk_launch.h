@@ -11,6 +11,16 @@ void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st);
 
 void launch_fill_zero(float *p, int64_t n, hipStream_t st);
 
+// ---- QKH / AFJLQ (random-orthogonal Kronecker pre-conditioner) ----
+int qh_plan_layer(LayerDesc &ld, int64_t D);
+int64_t qh_layer_floats(const LayerDesc &ld);
+void qh_generate_factors(const sk_sketch *s, std::vector<float> &host);
+int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose);
+void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
+                  float *out, bool accumulate, int phases, hipStream_t st);
+void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws, void *out,
+                    int out_dtype, const float *theta0, hipStream_t st);
+
 // ---- AFJL ----
 void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,
                       int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st);

@@ -1,0 +1,595 @@
+// sk_qhaar.hip -- sketches with the random-orthogonal Kronecker pre-conditioner
+// Q (Sec. 3, paragraphs "Alternative pre-conditioners" and "Direct usage of the
+// pre-conditioner Q"; eq. straight; Table tab:gains_design_choices, rows
+// "H_N -> Q"):
+//
+//   QKH    y = sqrt(N/D) R_D Q_N x       eq. straight on the flattened layer
+//   AFJLQ  y = sqrt(N/D) G R_D Q_N x     eq. frikadel with H_N replaced by Q
+//
+// Q_N = Q_0 (x) ... (x) Q_{K-1} over the Kronecker factor sizes of N (at most
+// 1024 each).  Factor k of a layer is Haar on the orthogonal group: the Q of the
+// QR factorisation, with R's diagonal made positive, of the b_k x b_k matrix of
+// the layer's QH Gaussian stream (number k 2^20 + r b_k + c at row r, column
+// c).  The text applies Q without the sign diagonal B; a Haar factor needs no
+// digit permutation either.
+//
+// With 2048 <= D <= 2^20, R_D keeps all 1024 rows of the last factor (T =
+// 1024), the first D_m = D / 1024 rows of factor m = K - 2 and the first row of
+// every leading factor.  Per layer and vector, with X_t the t-th b_m x T slab
+// of the padded layer (row-major) and P = N / (b_m T) slabs:
+//   Y (D_m x T) = A X' Qt^T,   X' = sum_t w[t] X_t,
+//   A = sqrt(N/D) Q_m[:D_m, :],  Qt = Q_{K-1},  w = (x)_{k<m} Q_k[0, :],
+// and the layer adds g . vec(Y) (AFJLQ) or vec(Y) (QKH) to the output.  The
+// transpose is X' = A^T (Z Qt) written w[t] X' into every slab t (Z = the
+// output vector as D_m x T, times g for AFJLQ).
+//
+// The factors are generated at creation on the host in double precision
+// (Householder QR of each Gaussian matrix, one factor per thread) and stored
+// in fp32: A, A^T, Qt, Qt^T and w per layer.  The contractions run on
+// v_mfma_f32_16x16x4f32 (fp32 products, fp32 accumulation).  Which operand is
+// contracted first follows the cost: a layer with fewer live rows of X than
+// D_m (P = 1: biases and norms padded to N = D) multiplies by Qt^T first and
+// then by the live columns of A; on the transpose side the same layers form
+// only their live output rows.
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <thread>
+#include <vector>
+
+#include "sk_kcommon.h"
+#include "sk_launch.h"
+
+namespace sk {
+
+namespace {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- factors
+// Householder QR of a (b x b, column-major, overwritten) and the explicit Q
+// with the signs of its columns set so that R has a positive diagonal.
+void haar_from_gaussian(double *a, int b, double *q) {
+  std::vector<double> tau(b, 0.0), rdiag(b, 0.0);
+  for (int j = 0; j < b; ++j) {
+    double *aj = a + (int64_t)j * b;
+    double nrm2 = 0.0;
+    for (int i = j; i < b; ++i) nrm2 += aj[i] * aj[i];
+    const double alpha = aj[j], nrm = std::sqrt(nrm2);
+    if (nrm == 0.0) continue;  // probability zero for Gaussian data: H_j = I
+    const double beta = alpha >= 0.0 ? -nrm : nrm;
+    const double v0 = alpha - beta;
+    tau[j] = (beta - alpha) / beta;
+    for (int i = j + 1; i < b; ++i) aj[i] /= v0;
+    aj[j] = beta;
+    rdiag[j] = beta;
+    for (int c = j + 1; c < b; ++c) {
+      double *ac = a + (int64_t)c * b;
+      double s = ac[j];
+      for (int i = j + 1; i < b; ++i) s += aj[i] * ac[i];
+      s *= tau[j];
+      ac[j] -= s;
+      for (int i = j + 1; i < b; ++i) ac[i] -= s * aj[i];
+    }
+  }
+  // Q = H_0 H_1 ... H_{b-1}: accumulate backwards onto the identity
+  std::fill(q, q + (int64_t)b * b, 0.0);
+  for (int i = 0; i < b; ++i) q[(int64_t)i * b + i] = 1.0;
+  for (int j = b - 1; j >= 0; --j) {
+    if (tau[j] == 0.0) continue;
+    const double *v = a + (int64_t)j * b;  // v[j] = 1 (implicit), v[i] for i > j
+    for (int c = j; c < b; ++c) {
+      double *qc = q + (int64_t)c * b;
+      double s = qc[j];
+      for (int i = j + 1; i < b; ++i) s += v[i] * qc[i];
+      s *= tau[j];
+      qc[j] -= s;
+      for (int i = j + 1; i < b; ++i) qc[i] -= s * v[i];
+    }
+  }
+  for (int c = 0; c < b; ++c)
+    if (rdiag[c] < 0.0)
+      for (int i = 0; i < b; ++i) q[(int64_t)c * b + i] = -q[(int64_t)c * b + i];
+}
+
+// Standard normal number j of a stream in double precision: the Box-Muller
+// transform of the stream specification (two 24-bit uniforms of a word pair).
+double gauss64(uint64_t j, uint32_t layer, uint32_t stream, Key key) {
+  const W4 w = philox(j >> 2, layer, stream, key);
+  const uint32_t wa = w.w[((j >> 1) & 1) * 2], wb = w.w[((j >> 1) & 1) * 2 + 1];
+  const double u1 = ((double)(wa >> 8) + 1.0) * (1.0 / 16777216.0);
+  const double u2 = (double)(wb >> 8) * (1.0 / 16777216.0);
+  const double r = std::sqrt(-2.0 * std::log(u1));
+  const double t = 2.0 * M_PI * u2;
+  return (j & 1) ? r * std::sin(t) : r * std::cos(t);
+}
+
+// ---------------------------------------------------------------- kernels
+enum { kPBuf = 0, kPInput = 1 };              // P operand: fp32 buffer / the layer's input
+enum { kQNT = 0, kQNNBuf = 1, kQNNFold = 2 };  // Q operand: rows N (K-contiguous) / rows K from a buffer / folded input
+enum { kEStore = 0, kEOut = 1, kEBcast = 2 };  // epilogue: fp32 store / sketch output / parameter-vector write
+
+struct QhArgs {
+  // C (M x N) = P (M x K) . op(Q); batch index v = blockIdx.y
+  int M, N, K;
+  const void *p;  // P: fp32 rows of ldp, batch stride p_vs; or the input (dtype, n_in per vector)
+  int64_t p_vs;
+  int ldp;
+  int p_vec;      // 16-byte loads of P allowed (ldp % 4 == 0, aligned base)
+  const void *q;  // Q: NT: fp32 N x K (ldq = K); NN buffer: fp32 K x N; NN fold: the input
+  int64_t q_vs;
+  int dtype;      // input dtype (kPInput, kQNNFold)
+  int64_t n_in;   // input elements per vector
+  int64_t b_in;   // first batch row of the input
+  const float *w; // fold / broadcast weights (P slabs)
+  int nslab;      // P
+  int64_t slab;   // elements per slab (b_m T)
+  // epilogue
+  void *dst;
+  int64_t c_vs;
+  int ldc;
+  int dst_dtype;
+  int64_t n_out;  // kEBcast: elements of the parameter vector
+  int64_t D;      // kEOut: output row length
+  int64_t b_out;  // first batch row of the output
+  const float *g;       // kEOut: per-element factor (nullable)
+  const float *theta0;  // kEBcast: added (nullable)
+  int accumulate;
+};
+
+__device__ __forceinline__ float load_in(const void *x, int dtype, int64_t i) {
+  return dtype == SK_BF16 ? bf16_to_f32(((const uint16_t *)x)[i]) : ((const float *)x)[i];
+}
+
+// Four values of P at row `row`, columns k .. k + 3 (zero outside M x K or the input).
+template <int PM>
+__device__ __forceinline__ f4v load_p4(const QhArgs &a, int64_t v, int row, int k) {
+  f4v r = {0.f, 0.f, 0.f, 0.f};
+  if (row >= a.M) return r;
+  if (PM == kPBuf) {
+    const float *p = (const float *)a.p + v * a.p_vs + (int64_t)row * a.ldp;
+    if (a.p_vec && k + 3 < a.K) return *(const f4v *)(p + k);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (k + e < a.K) r[e] = p[k + e];
+  } else {
+    const int64_t base = (a.b_in + v) * a.n_in;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t f = (int64_t)row * a.ldp + k + e;
+      if (k + e < a.K && f < a.n_in) r[e] = load_in(a.p, a.dtype, base + f);
+    }
+  }
+  return r;
+}
+
+// Q operand value at (k, col) for the NN forms (zero for k >= K).
+template <int QM, int PF>
+__device__ __forceinline__ float load_qnn(const QhArgs &a, int64_t v, int k, int col) {
+  if (k >= a.K) return 0.0f;
+  if (QM == kQNNBuf) return ((const float *)a.q)[v * a.q_vs + (int64_t)k * a.N + col];
+  const int64_t base = (a.b_in + v) * a.n_in;
+  float s = 0.0f;
+#pragma unroll
+  for (int t = 0; t < PF; ++t) {
+    const int64_t f = t * a.slab + (int64_t)k * a.N + col;
+    const float x = f < a.n_in ? load_in(a.q, a.dtype, base + f) : 0.0f;
+    s = PF == 1 ? x : s + a.w[t] * x;
+  }
+  return s;
+}
+
+// One workgroup per (16 TA x 16 TB output block, vector); the four waves take
+// quarters of K and their partial blocks are added in wave order through LDS.
+// Lane (li, g) of a 16 x 16 tile: P row li and Q column li, K slice 4 g .. 4 g
+// + 3 of each 16-wide step (one MFMA per slice element), output rows 4 g .. 4 g
+// + 3 of column li.
+template <int TA, int TB, int PM, int QM, int PF, int EP>
+__global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
+  __shared__ float red[4][TA * TB][64][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int nbb = a.N / (16 * TB);
+  const int ba = blockIdx.x / nbb, bb = blockIdx.x - (blockIdx.x / nbb) * nbb;
+  const int64_t v = blockIdx.y;
+  const int r0 = ba * TA * 16, c0 = bb * TB * 16;
+  const int per = ((a.K + 63) / 64) * 16;
+  const int kb = wave * per, ke = kb + per < a.K ? kb + per : a.K;
+  f4v acc[TA][TB];
+#pragma unroll
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j) acc[i][j] = f4v{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = kb; k0 < ke; k0 += 16) {
+    f4v pv[TA], qv[TB];
+#pragma unroll
+    for (int i = 0; i < TA; ++i) pv[i] = load_p4<PM>(a, v, r0 + 16 * i + li, k0 + 4 * g);
+    if (QM == kQNT) {
+      // Q rows are output columns, K-contiguous; K is a multiple of 16 here
+#pragma unroll
+      for (int j = 0; j < TB; ++j)
+        qv[j] = *(const f4v *)((const float *)a.q + v * a.q_vs + (int64_t)(c0 + 16 * j + li) * a.K + k0 + 4 * g);
+    } else {
+#pragma unroll
+      for (int j = 0; j < TB; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qv[j][e] = load_qnn<QM, PF>(a, v, k0 + 4 * g + e, c0 + 16 * j + li);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int i = 0; i < TA; ++i)
+#pragma unroll
+        for (int j = 0; j < TB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i][e], qv[j][e], acc[i][j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[wave][i * TB + j][lane][q] = acc[i][j][q];
+  __syncthreads();
+  for (int e = threadIdx.x; e < TA * TB * 64; e += 256) {
+    const int tile = e >> 6, ln = e & 63;
+    const int i = tile / TB, j = tile - (tile / TB) * TB;
+    const int col = c0 + 16 * j + (ln & 15);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int row = r0 + 16 * i + (ln >> 4) * 4 + q;
+      if (row >= a.M) continue;
+      const float y = ((red[0][tile][ln][q] + red[1][tile][ln][q]) + red[2][tile][ln][q]) + red[3][tile][ln][q];
+      if (EP == kEStore) {
+        ((float *)a.dst)[v * a.c_vs + (int64_t)row * a.ldc + col] = y;
+      } else if (EP == kEOut) {
+        const int64_t idx = (int64_t)row * a.N + col;
+        float *o = (float *)a.dst + (a.b_out + v) * a.D + idx;
+        const float val = a.g ? a.g[idx] * y : y;
+        *o = a.accumulate ? *o + val : val;
+      } else {
+        const int64_t idx = (int64_t)row * a.N + col;
+        for (int t = 0; t < a.nslab; ++t) {
+          const int64_t f = t * a.slab + idx;
+          if (f >= a.n_out) break;
+          float val = a.w ? a.w[t] * y : y;
+          if (a.theta0) val += a.theta0[f];
+          store_out(a.dst, a.dst_dtype, (a.b_out + v) * a.n_out + f, val);
+        }
+      }
+    }
+  }
+}
+
+// X'[v] (K x N) = sum_t w[t] X_t of the input (P slabs of K N elements), fp32.
+__global__ __launch_bounds__(256) void k_qh_fold(const void *x, int dtype, int64_t n_in, int64_t b_in,
+                                                 const float *__restrict__ w, int nslab, int64_t slab,
+                                                 float *__restrict__ dst) {
+  const int64_t e = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int64_t v = blockIdx.y;
+  if (e >= slab) return;
+  const int64_t base = (b_in + v) * n_in;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < nslab; ++t) {
+    const float wt = w[t];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t f = t * slab + e + q;
+      if (f < n_in) s[q] += wt * load_in(x, dtype, base + f);
+    }
+  }
+  *(f4v *)(dst + v * slab + e) = f4v{s[0], s[1], s[2], s[3]};
+}
+
+// Y[v] (M x T) = A[:, :r] U[v] (r x T), A row-major with lda; epilogue as k_qh_gemm's
+// kEStore (dst rows of T) or kEOut (sketch output with g).
+template <int EP>
+__global__ __launch_bounds__(256) void k_qh_small(const float *__restrict__ A, int lda, int M, int r,
+                                                  const float *__restrict__ U, int64_t u_vs, int T, void *dst,
+                                                  int64_t c_vs, int64_t D, int64_t b_out, const float *g,
+                                                  int accumulate) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int row = blockIdx.z;
+  const int64_t v = blockIdx.y;
+  if (c >= T) return;
+  const float *u = U + v * u_vs + c;
+  const float *ar = A + (int64_t)row * lda;
+  float s = 0.0f;
+  for (int h = 0; h < r; ++h) s += ar[h] * u[(int64_t)h * T];
+  if (EP == kEStore) {
+    ((float *)dst)[v * c_vs + (int64_t)row * T + c] = s;
+  } else {
+    const int64_t idx = (int64_t)row * T + c;
+    float *o = (float *)dst + (b_out + v) * D + idx;
+    const float val = g ? g[idx] * s : s;
+    *o = accumulate ? *o + val : val;
+  }
+  (void)M;
+}
+
+// w[v][i] = z[b + v][i] (times g[i])
+__global__ void k_qh_zg(const float *__restrict__ z, int64_t D, int64_t b_in, const float *g, float *__restrict__ w) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int64_t v = blockIdx.y;
+  if (i >= D) return;
+  const float zz = z[(b_in + v) * D + i];
+  w[v * D + i] = g ? zz * g[i] : zz;
+}
+
+int tiles_for(int m) { return m >= 64 ? 4 : m > 16 ? 2 : 1; }
+
+template <int PM, int QM, int PF, int EP>
+void launch_gemm(const QhArgs &a, int64_t bc, hipStream_t st) {
+  const int ta = tiles_for(a.M);
+  constexpr int TB = 4;  // N = 1024
+  const unsigned nba = (unsigned)((a.M + 16 * ta - 1) / (16 * ta));
+  const dim3 grid(nba * (unsigned)(a.N / (16 * TB)), (unsigned)bc);
+  if (ta == 4)
+    hipLaunchKernelGGL((k_qh_gemm<4, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+  else if (ta == 2)
+    hipLaunchKernelGGL((k_qh_gemm<2, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_qh_gemm<1, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- plan
+int qh_plan_layer(LayerDesc &ld, int64_t D) {
+  // factor m = K - 2 keeps D / 1024 rows; the last factor all 1024
+  if (ld.K < 2 || ld.lg[ld.K - 1] != 10) return SK_EUNSUPPORTED;
+  ld.qbm = 1 << ld.lg[ld.K - 2];
+  ld.qdm = (int32_t)(D >> 10);
+  ld.qP = ld.np / ((int64_t)ld.qbm << 10);
+  return ld.qdm >= 1 && ld.qdm <= ld.qbm ? SK_OK : SK_EUNSUPPORTED;
+}
+
+int64_t qh_layer_floats(const LayerDesc &ld) {
+  return 2ll * ld.qdm * ld.qbm + 2ll * 1024 * 1024 + ld.qP;
+}
+
+// Generates every layer's factors (host, fp64, threads over factors) and
+// writes A, A^T, Qt, Qt^T and w in fp32 into host[] at the layers' offsets.
+void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
+  struct Job {
+    int layer, k, b;
+  };
+  std::vector<Job> jobs;
+  for (int l = 0; l < (int)s->layers.size(); ++l) {
+    const LayerDesc &ld = s->layers[l];
+    for (int k = 0; k < ld.K; ++k) jobs.push_back(Job{l, k, 1 << ld.lg[k]});
+  }
+  // largest factors first so the threads finish together
+  std::stable_sort(jobs.begin(), jobs.end(), [](const Job &x, const Job &y) { return x.b > y.b; });
+  // first rows of the leading factors, per layer and factor
+  std::vector<std::vector<std::vector<double>>> lead(s->layers.size());
+  for (size_t l = 0; l < s->layers.size(); ++l) lead[l].resize(s->layers[l].K);
+  std::atomic<size_t> next{0};
+  auto work = [&]() {
+    std::vector<double> a, q;
+    for (;;) {
+      const size_t j = next.fetch_add(1);
+      if (j >= jobs.size()) return;
+      const Job jb = jobs[j];
+      const LayerDesc &ld = s->layers[jb.layer];
+      const int b = jb.b;
+      a.resize((size_t)b * b);
+      q.resize((size_t)b * b);
+      // A[r][c] = number k 2^20 + r b + c, stored column-major
+      for (int r = 0; r < b; ++r)
+        for (int c = 0; c < b; ++c)
+          a[(size_t)c * b + r] = gauss64(((uint64_t)jb.k << 20) + (uint64_t)r * b + c, (uint32_t)ld.layer_id, ST_QH,
+                                         s->key);
+      haar_from_gaussian(a.data(), b, q.data());
+      // q is column-major: Q[r][c] = q[c b + r]
+      float *base = host.data() + ld.qoff;
+      const double sc = std::sqrt((double)ld.np / (double)s->D);
+      if (jb.k == ld.K - 2) {
+        float *A = base, *At = base + (int64_t)ld.qdm * ld.qbm;
+        for (int r = 0; r < ld.qdm; ++r)
+          for (int c = 0; c < b; ++c) {
+            const float x = (float)(sc * q[(size_t)c * b + r]);
+            A[(int64_t)r * b + c] = x;
+            At[(int64_t)c * ld.qdm + r] = x;
+          }
+      } else if (jb.k == ld.K - 1) {
+        float *Qt = base + 2ll * ld.qdm * ld.qbm, *QtT = Qt + 1024 * 1024;
+        for (int r = 0; r < b; ++r)
+          for (int c = 0; c < b; ++c) {
+            const float x = (float)q[(size_t)c * b + r];
+            Qt[(int64_t)r * b + c] = x;
+            QtT[(int64_t)c * b + r] = x;
+          }
+      } else {
+        std::vector<double> row(b);
+        for (int c = 0; c < b; ++c) row[c] = q[(size_t)c * b];
+        lead[jb.layer][jb.k] = std::move(row);  // distinct slot per job
+      }
+    }
+  };
+  unsigned nt = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  nt = (unsigned)std::min<size_t>(nt, jobs.size());
+  std::vector<std::thread> th;
+  for (unsigned i = 1; i < nt; ++i) th.emplace_back(work);
+  work();
+  for (auto &t : th) t.join();
+  // w = Kronecker product of the leading factors' first rows (digit 0 most significant)
+  for (size_t l = 0; l < s->layers.size(); ++l) {
+    const LayerDesc &ld = s->layers[l];
+    std::vector<double> w(1, 1.0);
+    for (int k = 0; k < ld.K - 2; ++k) {
+      std::vector<double> nw(w.size() * lead[l][k].size());
+      for (size_t i = 0; i < w.size(); ++i)
+        for (size_t c = 0; c < lead[l][k].size(); ++c) nw[i * lead[l][k].size() + c] = w[i] * lead[l][k][c];
+      w.swap(nw);
+    }
+    float *wp = host.data() + ld.qoff + 2ll * ld.qdm * ld.qbm + 2ll * 1024 * 1024;
+    for (int64_t t = 0; t < ld.qP; ++t) wp[t] = (float)w[t];
+  }
+}
+
+// Live rows of X (P = 1): rows of 1024 that hold input elements.
+static int64_t qh_live_rows(const LayerDesc &ld) { return (ld.n + 1023) / 1024; }
+
+static bool qh_b_first(const LayerDesc &ld) { return ld.qP == 1 && qh_live_rows(ld) < ld.qdm; }
+
+int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose) {
+  const LayerDesc &ld = s->layers[layer];
+  const int64_t T = 1024;
+  if (!transpose) {
+    if (qh_b_first(ld)) return qh_live_rows(ld) * T * 4;
+    const bool fold = !(ld.qP == 1 || ld.qP == 2 || ld.qP == 4);
+    return (ld.qdm * T + (fold ? (int64_t)ld.qbm * T : 0)) * 4;
+  }
+  const int64_t rows = std::max<int64_t>(ld.qdm, ld.qP == 1 ? std::min<int64_t>(qh_live_rows(ld), ld.qbm) : 0);
+  return (s->D + rows * T) * 4;
+}
+
+void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
+                  float *out, bool accumulate, int phases, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const float *base = s->d_qh + ld.qoff;
+  const float *A = base, *Qt = base + 2ll * ld.qdm * ld.qbm, *w = Qt + 2ll * 1024 * 1024;
+  const float *g = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)layer * s->D : nullptr;
+  const int T = 1024;
+  QhArgs a{};
+  a.dtype = dtype;
+  a.n_in = ld.n;
+  a.b_in = b_begin;
+  a.D = s->D;
+  a.b_out = b_begin;
+  a.g = g;
+  a.accumulate = accumulate;
+  if (qh_b_first(ld)) {
+    const int r = (int)qh_live_rows(ld);
+    if (phases & 1) {  // U (r x T) = X[:r] Qt^T
+      a.M = r;
+      a.N = T;
+      a.K = T;
+      a.p = x;
+      a.ldp = T;
+      a.q = Qt;
+      a.dst = ws;
+      a.c_vs = (int64_t)r * T;
+      a.ldc = T;
+      launch_gemm<kPInput, kQNT, 1, kEStore>(a, bc, st);
+    }
+    if (phases & 2) {  // out (+)= g . (A[:, :r] U)
+      const dim3 grid(T / 256, (unsigned)bc, (unsigned)ld.qdm);
+      hipLaunchKernelGGL(k_qh_small<kEOut>, grid, dim3(256), 0, st, A, ld.qbm, ld.qdm, r, ws, (int64_t)r * T, T,
+                         (void *)out, (int64_t)0, s->D, b_begin, g, (int)accumulate);
+    }
+    return;
+  }
+  float *tbuf = ws, *xf = ws + bc * (int64_t)ld.qdm * T;
+  if (phases & 1) {  // T (D_m x T) = A X'
+    a.M = ld.qdm;
+    a.N = T;
+    a.K = ld.qbm;
+    a.p = A;
+    a.p_vs = 0;
+    a.ldp = ld.qbm;
+    a.p_vec = ld.qbm % 4 == 0;
+    a.dst = tbuf;
+    a.c_vs = (int64_t)ld.qdm * T;
+    a.ldc = T;
+    a.q = x;
+    a.w = w;
+    a.nslab = (int)ld.qP;
+    a.slab = (int64_t)ld.qbm * T;
+    if (ld.qP == 1) {
+      launch_gemm<kPBuf, kQNNFold, 1, kEStore>(a, bc, st);
+    } else if (ld.qP == 2) {
+      launch_gemm<kPBuf, kQNNFold, 2, kEStore>(a, bc, st);
+    } else if (ld.qP == 4) {
+      launch_gemm<kPBuf, kQNNFold, 4, kEStore>(a, bc, st);
+    } else {
+      const dim3 fg((unsigned)((a.slab / 4 + 255) / 256), (unsigned)bc);
+      hipLaunchKernelGGL(k_qh_fold, fg, dim3(256), 0, st, x, dtype, ld.n, b_begin, w, (int)ld.qP, a.slab, xf);
+      a.q = xf;
+      a.q_vs = a.slab;
+      launch_gemm<kPBuf, kQNNBuf, 1, kEStore>(a, bc, st);
+    }
+  }
+  if (phases & 2) {  // out (+)= g . (T Qt^T)
+    QhArgs b = a;
+    b.M = ld.qdm;
+    b.N = T;
+    b.K = T;
+    b.p = tbuf;
+    b.p_vs = (int64_t)ld.qdm * T;
+    b.ldp = T;
+    b.p_vec = 1;
+    b.q = Qt;
+    b.q_vs = 0;
+    b.dst = out;
+    launch_gemm<kPBuf, kQNT, 1, kEOut>(b, bc, st);
+  }
+}
+
+void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws, void *out,
+                    int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const float *base = s->d_qh + ld.qoff;
+  const float *At = base + (int64_t)ld.qdm * ld.qbm;
+  const float *Qt = base + 2ll * ld.qdm * ld.qbm, *QtT = Qt + 1024 * 1024, *w = QtT + 1024 * 1024;
+  const float *g = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)layer * s->D : nullptr;
+  const int T = 1024;
+  float *zg = ws, *u = ws + bc * s->D;
+  {
+    const dim3 grid((unsigned)((s->D + 255) / 256), (unsigned)bc);
+    hipLaunchKernelGGL(k_qh_zg, grid, dim3(256), 0, st, z, s->D, b_begin, g, zg);
+  }
+  QhArgs a{};
+  a.N = T;
+  a.dst = out;
+  a.dst_dtype = out_dtype;
+  a.n_out = ld.n;
+  a.b_out = b_begin;
+  a.theta0 = theta0;
+  a.slab = (int64_t)ld.qbm * T;
+  const int64_t live = qh_live_rows(ld);
+  if (ld.qP == 1 && live < ld.qdm) {
+    // V (live x T) = A^T[:live] Zg, then out = V Qt (rows beyond n dropped)
+    const int r = (int)live;
+    const dim3 grid(T / 256, (unsigned)bc, (unsigned)r);
+    hipLaunchKernelGGL(k_qh_small<kEStore>, grid, dim3(256), 0, st, At, ld.qdm, r, ld.qdm, zg, s->D, T, (void *)u,
+                       (int64_t)r * T, s->D, (int64_t)0, (const float *)nullptr, 0);
+    a.M = r;
+    a.K = T;
+    a.p = u;
+    a.p_vs = (int64_t)r * T;
+    a.ldp = T;
+    a.p_vec = 1;
+    a.q = QtT;
+    a.nslab = 1;
+    a.w = nullptr;
+    launch_gemm<kPBuf, kQNT, 1, kEBcast>(a, bc, st);
+    return;
+  }
+  // U (D_m x T) = Zg Qt, then every slab t gets w[t] A^T U
+  QhArgs b{};
+  b.M = ld.qdm;
+  b.N = T;
+  b.K = T;
+  b.p = zg;
+  b.p_vs = s->D;
+  b.ldp = T;
+  b.p_vec = 1;
+  b.q = QtT;
+  b.dst = u;
+  b.c_vs = (int64_t)ld.qdm * T;
+  b.ldc = T;
+  launch_gemm<kPBuf, kQNT, 1, kEStore>(b, bc, st);
+  a.M = ld.qbm;
+  a.K = ld.qdm;
+  a.p = At;
+  a.p_vs = 0;
+  a.ldp = ld.qdm;
+  a.p_vec = ld.qdm % 4 == 0;
+  a.q = u;
+  a.q_vs = (int64_t)ld.qdm * T;
+  a.nslab = (int)ld.qP;
+  a.w = w;
+  launch_gemm<kPBuf, kQNNBuf, 1, kEBcast>(a, bc, st);
+}
+
+}  // namespace sk

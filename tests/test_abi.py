@@ -48,6 +48,10 @@ def shapes(*ss):
     (4, [(4, 5, 2, 2)], 5, 0, -1),        # QK: sum dA*dB != D
     (4, [(4, 5, 5, 2)], 10, 0, -1),       # QK: dA > rows
     (4, [(4, 5, 0, 2)], 0, 0, -1),        # QK: dA < 1
+    (5, [(1, 10)], 1024, 0, -5),          # QKH: D below 2048
+    (6, [(1, 10)], 1 << 21, 0, -5),       # AFJLQ: D above 2^20
+    (6, [(1, 10)], 3000, 0, -1),          # AFJLQ: D not a power of two
+    (7, [(1, 10)], 4096, 0, -1),          # unknown kind
 ])
 def test_create_rejects_invalid_arguments(kind, shp, D, flags, code):
     L = _lib.load()
