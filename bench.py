@@ -5,7 +5,7 @@ Default workload (--config c2): per-example gradients shaped like GPT-2 small
 (148 tensors, N = 124,439,808), fp32 entries N(0, 1e-4), batch 64, sketched to
 D = 2^16 by AFJL and by AFFD (seed 1).  One step sketches the whole batch with
 both kinds; inputs are resident in HBM before the timed region.  Other
-workloads (--config c1|c3|c4|c5) are described in workloads.py.  Prints one
+workloads (--config c1|c3|c4|c5|c6) are described in workloads.py.  Prints one
 JSON line.
 
 "value" is parameter-space bytes per second: gradient bytes read by forward
@@ -38,12 +38,36 @@ import workloads as W  # noqa: E402
 METRIC = "gradient GB/s sketched and vectors/s at N=124M, D=2^16; % HBM/MFMA peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+MFMA_F32_PEAK_TFLOPS = 157.3
 
 
 # kernel launched by each single-kernel profile class (the rocprofv3 name)
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
              "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
-             "fjl:prolog": "k_fjl_prolog"}
+             "fjl:prolog": "k_fjl_prolog", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
+             "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm"}
+
+
+def qh_flops(shapes, D):
+    """Multiply-add flops (2 per product) per vector of the two contractions of the Q kinds, per
+    class (qh_first reads the input, qh_second forms the output), with the library's operand order."""
+    first = second = 0
+    for r, c in shapes:
+        n = r * c
+        np_len = 1
+        while np_len < max(n, D):
+            np_len *= 2
+        bm = min(1024, np_len // 1024)  # factor K - 2 (the last factor is 1024 wide)
+        dm, T = D // 1024, 1024
+        P = np_len // (bm * T)
+        live = -(-n // T)
+        if P == 1 and live < dm:  # Qt first on the live rows, then A's live columns
+            first += 2 * live * T * T
+            second += 2 * dm * live * T
+        else:
+            first += 2 * dm * bm * T
+            second += 2 * dm * T * T
+    return {"qh_first": first, "qh_second": second}
 
 
 def source_hash() -> str:
@@ -165,6 +189,14 @@ def cpu_baseline(cfg: str):
         O.apply("ffd", shapes, D, seed, xs, nthreads=cores)
         nbytes = 2 * shapes[0][1] * 4
         sample = "1 of 4 rows, FFD transpose and forward"
+    elif cfg == "c6":
+        sub = shapes[2:14]  # one transformer block: ln_1, attn, ln_2, mlp (12 tensors)
+        xs = rows_for(sub, 1)
+        for k in c["kinds"]:
+            O.apply(k, sub, D, seed, xs, layer0=2)
+        nbytes = len(c["kinds"]) * sum(r * cc for r, cc in sub) * 4
+        sample = f"1 of {c['batch']} rows, one transformer block (12 of {len(shapes)} tensors), AFJLQ+QKH, " \
+                 "factor generation included"
     else:  # c5
         first, cnt = W.llama3_8b_stream_groups()[1]
         sub = shapes[first:first + cnt]
@@ -210,16 +242,17 @@ def build_step(cfg: str, dev):
         return sks, step, 2 * len(c["kinds"]) * B * numels[0] * 4, B, \
             f"flat fp32 vectors N=2^20 entries N(0,1), batch {B}, D=4096, seed 0: FJL and FFD forward + transpose"
 
-    if cfg == "c2":
+    if cfg in ("c2", "c6"):
         xs = [W.gaussian((B, n), 1e-4, gen, dev) for n in numels]
         outs = {k: torch.empty((B, D), device=dev) for k in c["kinds"]}
 
         def step(ev):
             for k in c["kinds"]:
                 ev(k, "fwd", lambda k=k: sks[k].apply(xs, out=outs[k]))
+        names = " and ".join(k.upper() for k in c["kinds"])
         return sks, step, len(c["kinds"]) * B * sum(numels) * 4, B, \
             (f"GPT-2-small-shaped fp32 gradients N(0,1e-4), {len(shapes)} tensors, N={sum(numels)}, batch {B}, "
-             f"D=2^16, seed 1: AFJL and AFFD")
+             f"D=2^16, seed 1: {names}")
 
     if cfg == "c3":
         # one resident input per distinct matrix shape, shared by the matrices of that shape
@@ -362,6 +395,17 @@ def main() -> int:
         flops = sum(2 * s[0] * s[1] * s[3] + 2 * s[2] * s[0] * s[3] for s in c["shapes"]) * c["batch"]
         roofline["mfma_tflops"] = round(flops / (t_dom * 1e-3 / args.steps) / 1e12, 1)
         roofline["mfma_frac"] = round(roofline["mfma_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4)
+    if cfg == "c6":
+        # fp32 MFMA contractions: the bound is the larger of the two fractions
+        c = W.CONFIGS[cfg]
+        flops = qh_flops(c["shapes"], c["D"])[dom.split(":")[1]] * c["batch"] * args.steps
+        tf = flops / (t_dom * 1e-3) / 1e12 if t_dom > 0 else 0.0
+        roofline["mfma_tflops"] = round(tf, 1)
+        roofline["mfma_frac"] = round(tf / MFMA_F32_PEAK_TFLOPS, 4)
+        roofline["flops_per_launch"] = round(flops / max(n_dom, 1))
+        if tf / MFMA_F32_PEAK_TFLOPS > roofline["frac"]:
+            roofline.update({"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_F32_PEAK_TFLOPS,
+                             "unit": "TFLOP/s", "frac": round(tf / MFMA_F32_PEAK_TFLOPS, 4)})
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,

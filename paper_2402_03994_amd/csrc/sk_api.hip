@@ -140,6 +140,7 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
     }
     need = std::max(need, b);
   }
+  if (q_kind(s->kind) && !transpose) need = std::max(need, qh_small_bytes_per_vector(s, l0, l1));
   if (s->kind == SK_AFJL && !transpose) {
     // fold partials of every item of the call, plus the tail's per-group sums
     const int64_t items = s->layers[l1 - 1].item_off + s->layers[l1 - 1].n_items - s->layers[l0].item_off;
@@ -759,15 +760,32 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         break;
       }
       case SK_QKH:
-      case SK_AFJLQ:
+      case SK_AFJLQ: {
+        // the Qt-first layers in groups (one launch per phase and group), then the others
+        bool acc = accumulate != 0;
+        const int ngr = qh_small_group_count(s, l0, l1);
+        for (int gi = 0; gi < ngr; ++gi) {
+          int64_t gb = 0;
+          for (int l = l0; l < l1; ++l)
+            if (qh_small_layer(s, l)) gb += bc * s->layers[l].n * esz;  // reported with the first group
+          SK_PROF(SK_PROF_QH_FIRST, gi == 0 ? gb : 0,
+                  run_qh_small_group(s, l0, l1, gi, grads, dtype, b0, bc, s->ws, out, acc, 1, st));
+          SK_PROF(SK_PROF_QH_SECOND, 0, run_qh_small_group(s, l0, l1, gi, grads, dtype, b0, bc, s->ws, out, acc, 2, st));
+          acc = true;
+        }
+        int last = -1;
+        for (int l = l0; l < l1; ++l)
+          if (!qh_small_layer(s, l)) last = l;
         for (int l = l0; l < l1; ++l) {
-          const bool acc = accumulate || l > l0;
+          if (qh_small_layer(s, l)) continue;
           SK_PROF(SK_PROF_QH_FIRST, bc * s->layers[l].n * esz,
                   run_qh_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 1, st));
-          SK_PROF(SK_PROF_QH_SECOND, (l == l1 - 1 ? bc * s->D * 4 : 0),
+          SK_PROF(SK_PROF_QH_SECOND, (l == last ? bc * s->D * 4 : 0),
                   run_qh_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 2, st));
+          acc = true;
         }
         break;
+      }
       case SK_QK:
         for (int l = l0; l < l1; ++l) {
           SK_PROF(SK_PROF_QK_XB, bc * s->layers[l].n * esz,

@@ -16,6 +16,13 @@ int qh_plan_layer(LayerDesc &ld, int64_t D);
 int64_t qh_layer_floats(const LayerDesc &ld);
 void qh_generate_factors(const sk_sketch *s, std::vector<float> &host);
 int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose);
+// Layers whose live rows are fewer than D / 1024 (P = 1): forward in groups.
+bool qh_small_layer(const sk_sketch *s, int layer);
+int64_t qh_small_bytes_per_vector(const sk_sketch *s, int l0, int l1);
+int qh_small_group_count(const sk_sketch *s, int l0, int l1);
+void run_qh_small_group(const sk_sketch *s, int l0, int l1, int gi, const void *const *x, int dtype,
+                        int64_t b_begin, int64_t bc, float *ws, float *out, bool accumulate, int phases,
+                        hipStream_t st);
 void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
                   float *out, bool accumulate, int phases, hipStream_t st);
 void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws, void *out,

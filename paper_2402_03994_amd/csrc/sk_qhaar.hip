@@ -105,7 +105,8 @@ double gauss64(uint64_t j, uint32_t layer, uint32_t stream, Key key) {
 }
 
 // ---------------------------------------------------------------- kernels
-enum { kPBuf = 0, kPInput = 1 };              // P operand: fp32 buffer / the layer's input
+// P operand: fp32 buffer / the layer's input, rows v r + h = row h of vector v
+enum { kPBuf = 0, kPStacked = 1 };
 enum { kQNT = 0, kQNNBuf = 1, kQNNFold = 2 };  // Q operand: rows N (K-contiguous) / rows K from a buffer / folded input
 enum { kEStore = 0, kEOut = 1, kEBcast = 2 };  // epilogue: fp32 store / sketch output / parameter-vector write
 
@@ -116,6 +117,9 @@ struct QhArgs {
   int64_t p_vs;
   int ldp;
   int p_vec;      // 16-byte loads of P allowed (ldp % 4 == 0, aligned base)
+  int p_rows;     // kPStacked: rows per vector
+  int nvec;       // slot form: vectors stacked
+  int q_vec;      // NN fold: 16-byte (fp32) / 8-byte (bf16) loads of the input allowed
   const void *q;  // Q: NT: fp32 N x K (ldq = K); NN buffer: fp32 K x N; NN fold: the input
   int64_t q_vs;
   int dtype;      // input dtype (kPInput, kQNNFold)
@@ -137,6 +141,20 @@ struct QhArgs {
   int accumulate;
 };
 
+// Up to kQhSlots layers of the Qt-first form in one launch (grid z = slot).
+constexpr int kQhSlots = 32;
+struct QhSlots {
+  int n;
+  const void *x[kQhSlots];  // input [batch, n_in]
+  int64_t n_in[kQhSlots];
+  int rows[kQhSlots];       // live rows r
+  const float *qt[kQhSlots];
+  const float *A[kQhSlots];  // A (D_m x b_m)
+  int lda[kQhSlots];
+  const float *g[kQhSlots];  // G over [0, D) or null
+  int64_t uoff[kQhSlots];    // float offset of the slot's U (bc r x T) in the workspace
+};
+
 __device__ __forceinline__ float load_in(const void *x, int dtype, int64_t i) {
   return dtype == SK_BF16 ? bf16_to_f32(((const uint16_t *)x)[i]) : ((const float *)x)[i];
 }
@@ -153,40 +171,81 @@ __device__ __forceinline__ f4v load_p4(const QhArgs &a, int64_t v, int row, int 
     for (int e = 0; e < 4; ++e)
       if (k + e < a.K) r[e] = p[k + e];
   } else {
-    const int64_t base = (a.b_in + v) * a.n_in;
+    const int vv = row / a.p_rows, h = row - (row / a.p_rows) * a.p_rows;
+    const int64_t base = (a.b_in + vv) * a.n_in;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t f = (int64_t)row * a.ldp + k + e;
+      const int64_t f = (int64_t)h * a.ldp + k + e;
       if (k + e < a.K && f < a.n_in) r[e] = load_in(a.p, a.dtype, base + f);
     }
   }
+  (void)v;
   return r;
 }
 
-// Q operand value at (k, col) for the NN forms (zero for k >= K).
+// NN forms: rows k0 .. k0 + 15, columns c0 .. c0 + 63 of the Q operand, raw.
+// Lane L loads row 4 q + L / 16, columns c0 + 4 (L % 16) .. + 3 (q < 4) of
+// each of the PF slabs: 16-byte loads, 256 contiguous bytes per row.
 template <int QM, int PF>
-__device__ __forceinline__ float load_qnn(const QhArgs &a, int64_t v, int k, int col) {
-  if (k >= a.K) return 0.0f;
-  if (QM == kQNNBuf) return ((const float *)a.q)[v * a.q_vs + (int64_t)k * a.N + col];
-  const int64_t base = (a.b_in + v) * a.n_in;
-  float s = 0.0f;
+__device__ __forceinline__ void load_tile(const QhArgs &a, int64_t v, int k0, int c0, int lane, f4v (&r)[PF][4]) {
+  const int cc = c0 + 4 * (lane & 15);
 #pragma unroll
-  for (int t = 0; t < PF; ++t) {
-    const int64_t f = t * a.slab + (int64_t)k * a.N + col;
-    const float x = f < a.n_in ? load_in(a.q, a.dtype, base + f) : 0.0f;
-    s = PF == 1 ? x : s + a.w[t] * x;
+  for (int q = 0; q < 4; ++q) {
+    const int k = k0 + 4 * q + (lane >> 4);
+#pragma unroll
+    for (int t = 0; t < PF; ++t) r[t][q] = f4v{0.f, 0.f, 0.f, 0.f};
+    if (k >= a.K) continue;
+    if (QM == kQNNBuf) {
+      r[0][q] = *(const f4v *)((const float *)a.q + v * a.q_vs + (int64_t)k * a.N + cc);
+      continue;
+    }
+    const int64_t base = (a.b_in + v) * a.n_in;
+#pragma unroll
+    for (int t = 0; t < PF; ++t) {
+      const int64_t f = t * a.slab + (int64_t)k * a.N + cc;
+      if (a.q_vec && f + 3 < a.n_in) {
+        if (a.dtype == SK_BF16) {
+          const uint2 u = *(const uint2 *)((const uint16_t *)a.q + base + f);
+          r[t][q] = f4v{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                        __uint_as_float(u.y & 0xFFFF0000u)};
+        } else {
+          r[t][q] = *(const f4v *)((const float *)a.q + base + f);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (f + e < a.n_in) r[t][q][e] = load_in(a.q, a.dtype, base + f + e);
+      }
+    }
   }
-  return s;
 }
+
+constexpr int kStageLd = 68;  // floats per staged row (64 + 4: 16-byte aligned rows)
 
 // One workgroup per (16 TA x 16 TB output block, vector); the four waves take
 // quarters of K and their partial blocks are added in wave order through LDS.
 // Lane (li, g) of a 16 x 16 tile: P row li and Q column li, K slice 4 g .. 4 g
 // + 3 of each 16-wide step (one MFMA per slice element), output rows 4 g .. 4 g
-// + 3 of column li.
-template <int TA, int TB, int PM, int QM, int PF, int EP>
-__global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
-  __shared__ float red[4][TA * TB][64][4];
+// + 3 of column li.  In the NN forms each wave stages its 16 x 64 tile of the
+// Q operand in its own part of the LDS block (loaded one step ahead, slabs
+// summed with their weights on the way in) and reads the MFMA fragments from
+// there.
+template <int TA, int TB, int PM, int QM, int PF, int EP, bool SL = false>
+__global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a, QhSlots sl) {
+  if (SL) {  // the slot's layer: Qt-first form, vectors' rows stacked
+    const int z = blockIdx.z;
+    a.p = sl.x[z];
+    a.n_in = sl.n_in[z];
+    a.p_rows = sl.rows[z];
+    a.M = a.p_rows * a.nvec;
+    a.q = sl.qt[z];
+    a.dst = (float *)a.dst + sl.uoff[z];
+    if ((int)(blockIdx.x / (a.N / (16 * TB))) * TA * 16 >= a.M) return;  // whole workgroup
+    a.c_vs = 0;
+  }
+  constexpr int kRed = TA * TB * 256;
+  constexpr int kWave = kRed > 16 * kStageLd ? kRed : 16 * kStageLd;
+  __shared__ __align__(16) float red[4][kWave];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int li = lane & 15, g = lane >> 4;
   const int nbb = a.N / (16 * TB);
@@ -195,11 +254,15 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
   const int r0 = ba * TA * 16, c0 = bb * TB * 16;
   const int per = ((a.K + 63) / 64) * 16;
   const int kb = wave * per, ke = kb + per < a.K ? kb + per : a.K;
+  float *stage = red[wave];
   f4v acc[TA][TB];
 #pragma unroll
   for (int i = 0; i < TA; ++i)
 #pragma unroll
     for (int j = 0; j < TB; ++j) acc[i][j] = f4v{0.f, 0.f, 0.f, 0.f};
+  constexpr int NR = QM == kQNT ? 1 : PF;
+  f4v raw[NR][4];
+  if (QM != kQNT && kb < ke) load_tile<QM, NR>(a, v, kb, c0, lane, raw);
   for (int k0 = kb; k0 < ke; k0 += 16) {
     f4v pv[TA], qv[TB];
 #pragma unroll
@@ -211,9 +274,22 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
         qv[j] = *(const f4v *)((const float *)a.q + v * a.q_vs + (int64_t)(c0 + 16 * j + li) * a.K + k0 + 4 * g);
     } else {
 #pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f4v x = raw[0][q];
+        if (PF > 1) {
+          x = a.w[0] * x;
+#pragma unroll
+          for (int t = 1; t < NR; ++t) x += a.w[t] * raw[t][q];
+        }
+        *(f4v *)(stage + (4 * q + (lane >> 4)) * kStageLd + 4 * (lane & 15)) = x;
+      }
+      if (k0 + 16 < ke) load_tile<QM, NR>(a, v, k0 + 16, c0, lane, raw);
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
       for (int j = 0; j < TB; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qv[j][e] = load_qnn<QM, PF>(a, v, k0 + 4 * g + e, c0 + 16 * j + li);
+        for (int e = 0; e < 4; ++e) qv[j][e] = stage[(4 * g + e) * kStageLd + 16 * j + li];
+      __builtin_amdgcn_wave_barrier();
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e)
@@ -227,7 +303,7 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
 #pragma unroll
     for (int j = 0; j < TB; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) red[wave][i * TB + j][lane][q] = acc[i][j][q];
+      for (int q = 0; q < 4; ++q) red[wave][((i * TB + j) * 64 + lane) * 4 + q] = acc[i][j][q];
   __syncthreads();
   for (int e = threadIdx.x; e < TA * TB * 64; e += 256) {
     const int tile = e >> 6, ln = e & 63;
@@ -237,7 +313,8 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
     for (int q = 0; q < 4; ++q) {
       const int row = r0 + 16 * i + (ln >> 4) * 4 + q;
       if (row >= a.M) continue;
-      const float y = ((red[0][tile][ln][q] + red[1][tile][ln][q]) + red[2][tile][ln][q]) + red[3][tile][ln][q];
+      const int o = (tile * 64 + ln) * 4 + q;
+      const float y = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
       if (EP == kEStore) {
         ((float *)a.dst)[v * a.c_vs + (int64_t)row * a.ldc + col] = y;
       } else if (EP == kEOut) {
@@ -260,23 +337,43 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a) {
 }
 
 // X'[v] (K x N) = sum_t w[t] X_t of the input (P slabs of K N elements), fp32.
+// The slabs are read with 16-byte (fp32) or 8-byte (bf16) loads when vec is
+// set, four slabs in flight per step.
 __global__ __launch_bounds__(256) void k_qh_fold(const void *x, int dtype, int64_t n_in, int64_t b_in,
-                                                 const float *__restrict__ w, int nslab, int64_t slab,
+                                                 const float *__restrict__ w, int nslab, int64_t slab, int vec,
                                                  float *__restrict__ dst) {
   const int64_t e = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
   const int64_t v = blockIdx.y;
   if (e >= slab) return;
   const int64_t base = (b_in + v) * n_in;
-  float s[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int t = 0; t < nslab; ++t) {
-    const float wt = w[t];
+  f4v s = {0.f, 0.f, 0.f, 0.f};
+  for (int t0 = 0; t0 < nslab; t0 += 4) {
+    f4v r[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t f = t * slab + e + q;
-      if (f < n_in) s[q] += wt * load_in(x, dtype, base + f);
+    for (int u = 0; u < 4; ++u) {
+      const int t = t0 + u;
+      const int64_t f = t * slab + e;
+      r[u] = f4v{0.f, 0.f, 0.f, 0.f};
+      if (t >= nslab) continue;
+      if (vec && f + 3 < n_in) {
+        if (dtype == SK_BF16) {
+          const uint2 q = *(const uint2 *)((const uint16_t *)x + base + f);
+          r[u] = f4v{__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xFFFF0000u), __uint_as_float(q.y << 16),
+                     __uint_as_float(q.y & 0xFFFF0000u)};
+        } else {
+          r[u] = *(const f4v *)((const float *)x + base + f);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (f + q < n_in) r[u][q] = load_in(x, dtype, base + f + q);
+      }
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (t0 + u < nslab) s += w[t0 + u] * r[u];
   }
-  *(f4v *)(dst + v * slab + e) = f4v{s[0], s[1], s[2], s[3]};
+  *(f4v *)(dst + v * slab + e) = s;
 }
 
 // Y[v] (M x T) = A[:, :r] U[v] (r x T), A row-major with lda; epilogue as k_qh_gemm's
@@ -322,12 +419,34 @@ void launch_gemm(const QhArgs &a, int64_t bc, hipStream_t st) {
   constexpr int TB = 4;  // N = 1024
   const unsigned nba = (unsigned)((a.M + 16 * ta - 1) / (16 * ta));
   const dim3 grid(nba * (unsigned)(a.N / (16 * TB)), (unsigned)bc);
+  const QhSlots none{};
   if (ta == 4)
-    hipLaunchKernelGGL((k_qh_gemm<4, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_qh_gemm<4, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a, none);
   else if (ta == 2)
-    hipLaunchKernelGGL((k_qh_gemm<2, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_qh_gemm<2, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a, none);
   else
-    hipLaunchKernelGGL((k_qh_gemm<1, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_qh_gemm<1, TB, PM, QM, PF, EP>), grid, dim3(256), 0, st, a, none);
+}
+
+// out[v][idx] (+)= sum over the slots in order of g . (A[:, :r] U): one thread per (column, vector, row).
+__global__ __launch_bounds__(256) void k_qh_small_slots(QhSlots sl, int T, const float *__restrict__ ws, float *out,
+                                                        int64_t D, int64_t b_out, int accumulate) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int row = blockIdx.z;
+  const int64_t v = blockIdx.y;
+  if (c >= T) return;
+  const int64_t idx = (int64_t)row * T + c;
+  float total = 0.0f;
+  for (int z = 0; z < sl.n; ++z) {
+    const int r = sl.rows[z];
+    const float *u = ws + sl.uoff[z] + v * r * (int64_t)T + c;
+    const float *ar = sl.A[z] + (int64_t)row * sl.lda[z];
+    float sum = 0.0f;
+    for (int h = 0; h < r; ++h) sum += ar[h] * u[(int64_t)h * T];
+    total += sl.g[z] ? sl.g[z][idx] * sum : sum;
+  }
+  float *o = out + (b_out + v) * D + idx;
+  *o = accumulate ? *o + total : total;
 }
 
 }  // namespace
@@ -435,12 +554,93 @@ int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose) {
   const LayerDesc &ld = s->layers[layer];
   const int64_t T = 1024;
   if (!transpose) {
-    if (qh_b_first(ld)) return qh_live_rows(ld) * T * 4;
+    if (qh_b_first(ld)) return 0;  // grouped: qh_small_bytes_per_vector
     const bool fold = !(ld.qP == 1 || ld.qP == 2 || ld.qP == 4);
     return (ld.qdm * T + (fold ? (int64_t)ld.qbm * T : 0)) * 4;
   }
   const int64_t rows = std::max<int64_t>(ld.qdm, ld.qP == 1 ? std::min<int64_t>(qh_live_rows(ld), ld.qbm) : 0);
   return (s->D + rows * T) * 4;
+}
+
+bool qh_small_layer(const sk_sketch *s, int layer) { return qh_b_first(s->layers[layer]); }
+
+// Groups of up to kQhSlots consecutive Qt-first layers (in list order).
+static std::vector<std::vector<int>> qh_groups(const sk_sketch *s, int l0, int l1) {
+  std::vector<std::vector<int>> gs;
+  for (int l = l0; l < l1; ++l) {
+    if (!qh_b_first(s->layers[l])) continue;
+    if (gs.empty() || (int)gs.back().size() == kQhSlots) gs.emplace_back();
+    gs.back().push_back(l);
+  }
+  return gs;
+}
+
+int64_t qh_small_bytes_per_vector(const sk_sketch *s, int l0, int l1) {
+  int64_t need = 0;
+  for (const auto &grp : qh_groups(s, l0, l1)) {
+    int64_t b = 0;
+    for (int l : grp) b += qh_live_rows(s->layers[l]) * 1024 * 4;
+    need = std::max(need, b);
+  }
+  return need;
+}
+
+int qh_small_group_count(const sk_sketch *s, int l0, int l1) { return (int)qh_groups(s, l0, l1).size(); }
+
+// Group gi of the Qt-first layers in [l0, l1): phase 1 forms every slot's U
+// (one launch), phase 2 adds the slots' contributions to out in slot order
+// (one launch).  x[l - l0] is layer l's input.
+void run_qh_small_group(const sk_sketch *s, int l0, int l1, int gi, const void *const *x, int dtype,
+                        int64_t b_begin, int64_t bc, float *ws, float *out, bool accumulate, int phases,
+                        hipStream_t st) {
+  const std::vector<int> grp = qh_groups(s, l0, l1)[gi];
+  QhSlots sl{};
+  sl.n = (int)grp.size();
+  int64_t uoff = 0;
+  int maxr = 0, dm = 0;
+  for (int z = 0; z < sl.n; ++z) {
+    const int l = grp[z];
+    const LayerDesc &ld = s->layers[l];
+    const float *base = s->d_qh + ld.qoff;
+    sl.x[z] = x[l - l0];
+    sl.n_in[z] = ld.n;
+    sl.rows[z] = (int)qh_live_rows(ld);
+    sl.qt[z] = base + 2ll * ld.qdm * ld.qbm;
+    sl.A[z] = base;
+    sl.lda[z] = ld.qbm;
+    sl.g[z] = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)l * s->D : nullptr;
+    sl.uoff[z] = uoff;
+    uoff += bc * sl.rows[z] * 1024;
+    maxr = std::max(maxr, sl.rows[z]);
+    dm = ld.qdm;
+  }
+  const int T = 1024;
+  if (phases & 1) {
+    QhArgs a{};
+    a.N = T;
+    a.K = T;
+    a.ldp = T;
+    a.dtype = dtype;
+    a.b_in = b_begin;
+    a.nvec = (int)bc;
+    a.dst = ws;
+    a.ldc = T;
+    const int mmax = (int)(bc * maxr);
+    const int ta = tiles_for(mmax);
+    const unsigned nba = (unsigned)((mmax + 16 * ta - 1) / (16 * ta));
+    const dim3 grid(nba * (unsigned)(T / 64), 1u, (unsigned)sl.n);
+    if (ta == 4)
+      hipLaunchKernelGGL((k_qh_gemm<4, 4, kPStacked, kQNT, 1, kEStore, true>), grid, dim3(256), 0, st, a, sl);
+    else if (ta == 2)
+      hipLaunchKernelGGL((k_qh_gemm<2, 4, kPStacked, kQNT, 1, kEStore, true>), grid, dim3(256), 0, st, a, sl);
+    else
+      hipLaunchKernelGGL((k_qh_gemm<1, 4, kPStacked, kQNT, 1, kEStore, true>), grid, dim3(256), 0, st, a, sl);
+  }
+  if (phases & 2) {
+    const dim3 grid(T / 256, (unsigned)bc, (unsigned)dm);
+    hipLaunchKernelGGL(k_qh_small_slots, grid, dim3(256), 0, st, sl, T, (const float *)ws, out, s->D, b_begin,
+                       (int)accumulate);
+  }
 }
 
 void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
@@ -458,27 +658,7 @@ void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64
   a.b_out = b_begin;
   a.g = g;
   a.accumulate = accumulate;
-  if (qh_b_first(ld)) {
-    const int r = (int)qh_live_rows(ld);
-    if (phases & 1) {  // U (r x T) = X[:r] Qt^T
-      a.M = r;
-      a.N = T;
-      a.K = T;
-      a.p = x;
-      a.ldp = T;
-      a.q = Qt;
-      a.dst = ws;
-      a.c_vs = (int64_t)r * T;
-      a.ldc = T;
-      launch_gemm<kPInput, kQNT, 1, kEStore>(a, bc, st);
-    }
-    if (phases & 2) {  // out (+)= g . (A[:, :r] U)
-      const dim3 grid(T / 256, (unsigned)bc, (unsigned)ld.qdm);
-      hipLaunchKernelGGL(k_qh_small<kEOut>, grid, dim3(256), 0, st, A, ld.qbm, ld.qdm, r, ws, (int64_t)r * T, T,
-                         (void *)out, (int64_t)0, s->D, b_begin, g, (int)accumulate);
-    }
-    return;
-  }
+  // (the Qt-first layers go through run_qh_small_group)
   float *tbuf = ws, *xf = ws + bc * (int64_t)ld.qdm * T;
   if (phases & 1) {  // T (D_m x T) = A X'
     a.M = ld.qdm;
@@ -492,6 +672,7 @@ void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64
     a.c_vs = (int64_t)ld.qdm * T;
     a.ldc = T;
     a.q = x;
+    a.q_vec = ld.n % 4 == 0 && ((uintptr_t)x & (dtype == SK_BF16 ? 7 : 15)) == 0;
     a.w = w;
     a.nslab = (int)ld.qP;
     a.slab = (int64_t)ld.qbm * T;
@@ -503,7 +684,8 @@ void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64
       launch_gemm<kPBuf, kQNNFold, 4, kEStore>(a, bc, st);
     } else {
       const dim3 fg((unsigned)((a.slab / 4 + 255) / 256), (unsigned)bc);
-      hipLaunchKernelGGL(k_qh_fold, fg, dim3(256), 0, st, x, dtype, ld.n, b_begin, w, (int)ld.qP, a.slab, xf);
+      hipLaunchKernelGGL(k_qh_fold, fg, dim3(256), 0, st, x, dtype, ld.n, b_begin, w, (int)ld.qP, a.slab, a.q_vec,
+                         xf);
       a.q = xf;
       a.q_vs = a.slab;
       launch_gemm<kPBuf, kQNNBuf, 1, kEStore>(a, bc, st);

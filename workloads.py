@@ -68,10 +68,12 @@ CONFIGS = {
     "c3": dict(kinds=("qk",), shapes=decoder_1p3b_qk_shapes(), D=1 << 18, batch=256, seed=0, dtype="bf16"),
     "c4": dict(kinds=("ffd",), shapes=[(1, 100_000_000)], D=1 << 20, batch=4, seed=0, dtype="f32"),
     "c5": dict(kinds=("afjl",), shapes=llama3_8b_shapes(), D=1 << 20, batch=8, seed=7, dtype="bf16"),
+    # the C2 gradients through the sketches with the random-orthogonal pre-conditioner Q
+    "c6": dict(kinds=("afjlq", "qkh"), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
 }
-INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005}
+INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002}
 # variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
-GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5}
+GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4}
 
 
 def gaussian(shape, var: float, gen: torch.Generator, device, dtype=torch.float32) -> torch.Tensor:
