@@ -24,7 +24,7 @@ _LIB = os.path.join(_HERE, "libsk_oracle.so")
 
 KINDS = {"fjl": 0, "ffd": 1, "affd": 2, "afjl": 3, "qk": 4}
 # kinds with the random-orthogonal Kronecker pre-conditioner (numpy, qhaar.py)
-QKINDS = ("qkh", "afjlq")
+QKINDS = ("qkh", "afjlq", "affdq")
 DTYPES = {"f32": 0, "bf16": 1}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}
 

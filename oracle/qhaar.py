@@ -26,6 +26,10 @@ of the other kinds) and Kronecker factor sizes (b_0, ..., b_{K-1}) = ks(N):
   diagonal B, and a Haar factor needs no digit permutation):
       y = sqrt(N / D) G R_D Q_N pad(x),  G = diag(g_0 .. g_{D-1})
   with g the layer's "gauss" stream (the same g as AFJL).
+* AFFDQ (eq. bami with both H_N -> Q):
+      y = sqrt(N / D) R_D Q'_N G Q_N pad(x),  G = diag(g_0 .. g_{N-1})
+  with Q_N the factors above and Q'_N an independent set (factor k of Q'_N is
+  factor 8 + k of the layer's stream), g the layer's "gauss" stream over N.
 * Several layers: the sum of the per-layer sketches (as for AFFD / AFJL).
 * Transposes: the exact adjoints, truncated to the layer's n entries.
 
@@ -53,9 +57,9 @@ def haar_factor(seed: int, layer: int, k: int, b: int) -> np.ndarray:
         q, r = np.linalg.qr(a, mode="complete")
         s = np.sign(np.diag(r))
         s[s == 0] = 1.0
-        _cache[key] = q * s[None, :]
-        if len(_cache) > 4096:
+        if len(_cache) >= 4096:
             _cache.clear()
+        _cache[key] = q * s[None, :]
     return _cache[key]
 
 
@@ -81,12 +85,22 @@ def _mode_product(t: np.ndarray, m: np.ndarray, axis: int) -> np.ndarray:
     return np.moveaxis(np.tensordot(m, t, axes=([1], [axis])), 0, axis)
 
 
+SECOND = 8  # factor index offset of the second set (AFFDQ)
+
+
 def layer_forward(kind: str, x: np.ndarray, n: int, D: int, seed: int, layer: int) -> np.ndarray:
     """One layer, one vector (fp64 x of length n): the D-vector of the layer's sketch."""
     np_len, dims, dk = layer_plan(n, D)
     t = np.zeros(np_len, dtype=np.float64)
     t[:n] = x
     t = t.reshape(dims)
+    if kind == "affdq":
+        for k, b in enumerate(dims):
+            t = _mode_product(t, haar_factor(seed, layer, k, b), k)
+        t = t * gauss(seed, layer, "gauss", 0, np_len).reshape(dims)
+        for k, b in enumerate(dims):
+            t = _mode_product(t, haar_factor(seed, layer, SECOND + k, b)[: dk[k], :], k)
+        return t.reshape(-1) * np.sqrt(np_len / D)
     for k, b in enumerate(dims):
         t = _mode_product(t, haar_factor(seed, layer, k, b)[: dk[k], :], k)
     y = t.reshape(-1) * np.sqrt(np_len / D)
@@ -99,6 +113,14 @@ def layer_transpose(kind: str, z: np.ndarray, n: int, D: int, seed: int, layer: 
     """One layer, one vector: the adjoint applied to z (length D), truncated to n entries."""
     np_len, dims, dk = layer_plan(n, D)
     u = np.array(z, dtype=np.float64) * np.sqrt(np_len / D)
+    if kind == "affdq":
+        t = u.reshape(dk)
+        for k, b in enumerate(dims):
+            t = _mode_product(t, haar_factor(seed, layer, SECOND + k, b)[: dk[k], :].T, k)
+        t = t * gauss(seed, layer, "gauss", 0, np_len).reshape(dims)
+        for k, b in enumerate(dims):
+            t = _mode_product(t, haar_factor(seed, layer, k, b).T, k)
+        return t.reshape(-1)[:n]
     if kind == "afjlq":
         u = u * gauss(seed, layer, "gauss", 0, D)
     t = u.reshape(dk)
@@ -146,6 +168,12 @@ def dense(kind: str, n: int, D: int, seed: int, layer: int) -> np.ndarray:
     m = np.ones((1, 1))
     for k, b in enumerate(dims):
         m = np.kron(m, haar_factor(seed, layer, k, b))
+    if kind == "affdq":
+        m2 = np.ones((1, 1))
+        for k, b in enumerate(dims):
+            m2 = np.kron(m2, haar_factor(seed, layer, SECOND + k, b))
+        g = gauss(seed, layer, "gauss", 0, np_len)
+        return (m2[:D, :] * g[None, :]) @ m[:, :n] * np.sqrt(np_len / D)
     s = m[:D, :n] * np.sqrt(np_len / D)
     if kind == "afjlq":
         s = s * gauss(seed, layer, "gauss", 0, D)[:, None]

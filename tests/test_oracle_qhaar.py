@@ -1,6 +1,6 @@
 """Pins of the fp64 oracle for the kinds with the random-orthogonal Kronecker
 pre-conditioner (QKH: eq. straight on the flattened layer; AFJLQ: eq. frikadel
-with H_N -> Q, Table tab:gains_design_choices).
+with H_N -> Q; AFFDQ: eq. bami with both H_N -> Q; Table tab:gains_design_choices).
 
 Each pin checks the oracle against something other than itself: the QR
 identity and its uniqueness, Haar statistics, the dense Kronecker product,
@@ -52,7 +52,7 @@ def test_haar_statistics():
     assert np.allclose(np.abs(det), 1.0)
 
 
-@pytest.mark.parametrize("kind", ["qkh", "afjlq"])
+@pytest.mark.parametrize("kind", ["qkh", "afjlq", "affdq"])
 @pytest.mark.parametrize("n,D", [(1, 16), (100, 16), (3000, 64), (4096, 4096), (4096, 1024), (5000, 1024),
                                  (2048, 4096), (1500, 2)])
 def test_restricted_factors_equal_dense_restriction(kind, n, D):
@@ -103,11 +103,27 @@ def test_worked_example_first_row(n, D):
     assert np.abs(y - g0 * want).max() < 1e-12 * np.sqrt(np_len / D) * max(1.0, abs(g0))
 
 
+@pytest.mark.parametrize("n,D", [(70000, 4096), (4096, 4096), (3000, 64)])
+def test_affdq_worked_example(n, D):
+    """AFFDQ(Q_N^T e_0) = sqrt(N/D) g_0 (first column of Q'_N)[:D]: the first transform maps x* to e_0,
+    G scales it by g_0, the second transform's restriction keeps D rows of its first column."""
+    seed, layer = 4, 1
+    np_len, dims, _ = Q.layer_plan(n, D)
+    row, col2 = np.ones(1), np.ones(1)
+    for k, b in enumerate(dims):
+        row = np.kron(row, Q.haar_factor(seed, layer, k, b)[0])
+        col2 = np.kron(col2, Q.haar_factor(seed, layer, Q.SECOND + k, b)[:, 0])
+    g0 = O.gauss(seed, layer, "gauss", 0, 1)[0]
+    want = np.sqrt(np_len / D) * g0 * col2[:D]
+    y = Q.layer_forward("affdq", row, np_len, D, seed, layer)
+    assert np.abs(y - want).max() < 1e-12 * max(1.0, np.abs(want).max())
+
+
 def test_isometry_in_expectation():
-    """E ||S x||^2 = ||x||^2 over seeds (QKH; AFJLQ adds E g^2 = 1), as a z-test on the mean ratio."""
+    """E ||S x||^2 = ||x||^2 over seeds (QKH; AFJLQ and AFFDQ add E g^2 = 1), as a z-test on the mean ratio."""
     n, D, m = 200, 32, 600
     x = np.random.default_rng(0).standard_normal(n)
-    for kind in ("qkh", "afjlq"):
+    for kind in ("qkh", "afjlq", "affdq"):
         r = np.array([np.sum(Q.layer_forward(kind, x, n, D, s, 0) ** 2) for s in range(m)]) / np.dot(x, x)
         assert abs(r.mean() - 1.0) < 4.5 * r.std() / np.sqrt(m), (kind, r.mean(), r.std())
 
