@@ -22,6 +22,9 @@
  *   SK_AFJLQ y = sqrt(N/D) G R_D Q_N x                    (eq. frikadel with the
  *            pre-conditioner H_N replaced by Q, Sec. 3 "Alternative
  *            pre-conditioners")
+ *   SK_AFFDQ y = sqrt(N/D) R_D Q'_N G Q_N x               (eq. bami with both
+ *            H_N replaced by independent Q_N, Q'_N; G over N'.  Dense work:
+ *            about 4 GFLOP per vector and 2^20-element slab)
  *
  * H_N is the normalised Walsh-Hadamard matrix (appendix definition), R_D keeps
  * the first D coordinates, B is a diagonal of random signs, G a diagonal of
@@ -29,7 +32,7 @@
  * (Sec. 3, "Removing the lookup bottleneck"; factors of at most 1024).
  *
  * Per layer l with n_l = rows*cols elements the FWHT kinds (and SK_QKH,
- * SK_AFJLQ) work on the padded length N'_l = 2^ceil(log2 max(n_l, D)) (padding
+ * SK_AFJLQ, SK_AFFDQ) work on the padded length N'_l = 2^ceil(log2 max(n_l, D)) (padding
  * is virtual: never read or written).  They sum independent per-layer sketches
  * (each with its own random streams, keyed on the layer's index in the list),
  * which is the
@@ -64,7 +67,16 @@
 extern "C" {
 #endif
 
-typedef enum { SK_FJL = 0, SK_FFD = 1, SK_AFFD = 2, SK_AFJL = 3, SK_QK = 4, SK_QKH = 5, SK_AFJLQ = 6 } sk_kind;
+typedef enum {
+  SK_FJL = 0,
+  SK_FFD = 1,
+  SK_AFFD = 2,
+  SK_AFJL = 3,
+  SK_QK = 4,
+  SK_QKH = 5,
+  SK_AFJLQ = 6,
+  SK_AFFDQ = 7
+} sk_kind;
 typedef enum { SK_F32 = 0, SK_BF16 = 1 } sk_dtype;
 
 enum {
@@ -108,7 +120,8 @@ enum {
   SK_STREAM_PI2 = 6,     /* digit permutation after the second H (AFFD)    */
   SK_STREAM_QKA = 7,     /* QK left factor                                 */
   SK_STREAM_QKB = 8,     /* QK right factor                                */
-  SK_STREAM_QH = 9       /* SK_QKH / SK_AFJLQ factor k of a layer: Gaussian
+  SK_STREAM_QH = 9       /* SK_QKH / SK_AFJLQ / SK_AFFDQ factor k of a layer
+                            (SK_AFFDQ second set: k = 8 + digit): Gaussian
                             numbers k 2^20 + r b + c form the b x b matrix
                             whose normalised QR factor (R with a positive
                             diagonal) is factor k; computed in fp64 on the
@@ -121,8 +134,9 @@ enum {
  *   shapes    host array of n_layers >= 1 layer shapes (rows, cols >= 1).
  *   D         target dimension.  FWHT kinds: a power of two, 16 <= D <= 2^20
  *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
- *             SK_QKH, SK_AFJLQ: a power of two, 2048 <= D <= 2^20 (smaller D
- *             is SK_EUNSUPPORTED by the kernels).
+ *             SK_QKH, SK_AFJLQ, SK_AFFDQ: a power of two, 2048 <= D <= 2^20
+ *             (smaller D is SK_EUNSUPPORTED by the kernels); SK_AFFDQ also
+ *             needs N'_l <= 2^26 for every layer.
  *   seed      64-bit key of every random stream.
  *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).
  * On success *out receives the handle (destroy with sketch_destroy).  The

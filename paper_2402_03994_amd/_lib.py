@@ -7,7 +7,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsketch.so")
 
-SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ = range(7)
+SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ, SK_AFFDQ = range(8)
 SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}

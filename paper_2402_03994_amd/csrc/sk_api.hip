@@ -82,7 +82,7 @@ void free_all(sk_sketch *s) {
 }
 
 bool fwht_kind(int k) { return k == SK_FJL || k == SK_FFD || k == SK_AFFD || k == SK_AFJL; }
-bool q_kind(int k) { return k == SK_QKH || k == SK_AFJLQ; }
+bool q_kind(int k) { return k == SK_QKH || k == SK_AFJLQ || k == SK_AFFDQ; }
 // kinds on the padded per-layer length N' with its Kronecker digits
 bool padded_kind(int k) { return fwht_kind(k) || q_kind(k); }
 
@@ -132,6 +132,7 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
         break;
       case SK_QKH:
       case SK_AFJLQ:
+      case SK_AFFDQ:
         b = qh_bytes_per_vector(s, l, transpose);
         break;
       case SK_QK:  // T = X B^T (m x dB) or, A first, U = A X (dA x n)
@@ -140,7 +141,8 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
     }
     need = std::max(need, b);
   }
-  if (q_kind(s->kind) && !transpose) need = std::max(need, qh_small_bytes_per_vector(s, l0, l1));
+  if ((s->kind == SK_QKH || s->kind == SK_AFJLQ) && !transpose)
+    need = std::max(need, qh_small_bytes_per_vector(s, l0, l1));
   if (s->kind == SK_AFJL && !transpose) {
     // fold partials of every item of the call, plus the tail's per-group sums
     const int64_t items = s->layers[l1 - 1].item_off + s->layers[l1 - 1].n_items - s->layers[l0].item_off;
@@ -179,7 +181,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
                   uint32_t flags, int32_t device, sk_sketch **out) {
   if (!out) return fail(SK_EINVAL, "out is NULL");
   *out = nullptr;
-  if ((int)kind < 0 || (int)kind > 6) return fail(SK_EINVAL, "unknown sketch kind");
+  if ((int)kind < 0 || (int)kind > 7) return fail(SK_EINVAL, "unknown sketch kind");
   if (!shapes || n_layers < 1) return fail(SK_EINVAL, "need at least one layer shape");
   if (flags & ~SK_FLAG_AFFD_NO_MTAB) return fail(SK_EINVAL, "unknown flags");
   for (int l = 0; l < n_layers; ++l) {
@@ -193,6 +195,10 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     if (D < (q_kind(kind) ? 2048 : 16))
       return fail(SK_EUNSUPPORTED, std::string("D < ") + (q_kind(kind) ? "2048" : "16") + " is not supported by the kernels");
     if (D > (1ll << 20)) return fail(SK_EUNSUPPORTED, "D > 2^20 is not supported by the kernels");
+    if (kind == SK_AFFDQ)
+      for (int l = 0; l < n_layers; ++l)
+        if (shapes[l].rows * shapes[l].cols > (1ll << 26))
+          return fail(SK_EUNSUPPORTED, "AFFDQ: layer " + std::to_string(l) + " pads beyond 2^26 elements");
   } else {
     int64_t tot = 0;
     for (int l = 0; l < n_layers; ++l) {
@@ -295,13 +301,13 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   if (q_kind(kind)) {
     for (int l = 0; l < n_layers; ++l) {
       LayerDesc &ld = s->layers[l];
-      if (qh_plan_layer(ld, D) != SK_OK) {
+      if (qh_plan_layer(ld, D, kind) != SK_OK) {
         free_all(s);
         delete s;
         return fail(SK_EUNSUPPORTED, "layer " + std::to_string(l) + ": Kronecker shape not supported");
       }
       ld.qoff = qh_floats;
-      qh_floats += (qh_layer_floats(ld) + 3) & ~3ll;  // 16-byte aligned blocks
+      qh_floats += (qh_layer_floats(ld, kind) + 3) & ~3ll;  // 16-byte aligned blocks
     }
   }
 
@@ -402,6 +408,8 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       delete s;
       return fail(SK_EHIP, std::string("hipMemcpy: ") + hipGetErrorString(hipGetLastError()));
     }
+    if (kind == SK_AFFDQ)
+      for (int l = 0; l < n_layers; ++l) launch_affdq_mtab(s, l, nullptr);
   }
   SK_TRY(alloc((void **)&s->d_items, sizeof(FoldItem) * s->items.size()));
   SK_TRY(alloc((void **)&s->d_rslot, sizeof(int2) * rslot.size()));
@@ -786,6 +794,15 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         }
         break;
       }
+      case SK_AFFDQ:
+        for (int l = l0; l < l1; ++l) {
+          const bool acc = accumulate || l > l0;
+          SK_PROF(SK_PROF_QH_FIRST, bc * s->layers[l].n * esz,
+                  run_affdq_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 1, st));
+          SK_PROF(SK_PROF_QH_SECOND, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                  run_affdq_apply(s, l, grads[l - l0], dtype, b0, bc, s->ws, out, acc, 2, st));
+        }
+        break;
       case SK_QK:
         for (int l = l0; l < l1; ++l) {
           SK_PROF(SK_PROF_QK_XB, bc * s->layers[l].n * esz,
@@ -872,6 +889,9 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
         case SK_QKH:
         case SK_AFJLQ:
           SK_PROF(SK_PROF_QH_SECOND, obytes, run_qh_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
+          break;
+        case SK_AFFDQ:
+          SK_PROF(SK_PROF_QH_SECOND, obytes, run_affdq_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
           break;
         case SK_QK:
           SK_PROF(SK_PROF_QK, obytes + bc * ld.da * ld.db * 4,

@@ -12,8 +12,17 @@ void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st);
 void launch_fill_zero(float *p, int64_t n, hipStream_t st);
 
 // ---- QKH / AFJLQ (random-orthogonal Kronecker pre-conditioner) ----
-int qh_plan_layer(LayerDesc &ld, int64_t D);
-int64_t qh_layer_floats(const LayerDesc &ld);
+constexpr int kQhMaxLead = 64;  // AFFDQ: slabs of one layer (N' <= 2^26)
+constexpr int kQhSecond = 8;   // AFFDQ: stream factor index of the second set's digit 0
+// Float offsets of a layer's factors in the factor block (per kind).
+struct QhLayout {
+  int64_t a, at, qt, qtt, w;                 // restricted set: A, A^T, Qt, Qt^T, w
+  int64_t q1m, q1mt, q1l, q1lt, c, m;        // AFFDQ first set, c (P x P), M (P x b_m x 1024)
+  int64_t total;
+};
+int qh_plan_layer(LayerDesc &ld, int64_t D, int kind);
+QhLayout qh_layout(const LayerDesc &ld, int kind);
+int64_t qh_layer_floats(const LayerDesc &ld, int kind);
 void qh_generate_factors(const sk_sketch *s, std::vector<float> &host);
 int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose);
 // Layers whose live rows are fewer than D / 1024 (P = 1): forward in groups.
@@ -27,6 +36,11 @@ void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64
                   float *out, bool accumulate, int phases, hipStream_t st);
 void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws, void *out,
                     int out_dtype, const float *theta0, hipStream_t st);
+void launch_affdq_mtab(const sk_sketch *s, int layer, hipStream_t st);
+void run_affdq_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
+                     float *out, bool accumulate, int phases, hipStream_t st);
+void run_affdq_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws,
+                       void *out, int out_dtype, const float *theta0, hipStream_t st);
 
 // ---- AFJL ----
 void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,

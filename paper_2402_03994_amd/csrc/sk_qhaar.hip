@@ -107,8 +107,11 @@ double gauss64(uint64_t j, uint32_t layer, uint32_t stream, Key key) {
 // ---------------------------------------------------------------- kernels
 // P operand: fp32 buffer / the layer's input, rows v r + h = row h of vector v
 enum { kPBuf = 0, kPStacked = 1 };
-enum { kQNT = 0, kQNNBuf = 1, kQNNFold = 2 };  // Q operand: rows N (K-contiguous) / rows K from a buffer / folded input
-enum { kEStore = 0, kEOut = 1, kEBcast = 2 };  // epilogue: fp32 store / sketch output / parameter-vector write
+// Q operand: rows N (K-contiguous) / rows K from a buffer / folded input / a
+// buffer times the table at w, element by element
+enum { kQNT = 0, kQNNBuf = 1, kQNNFold = 2, kQNNMul = 3 };
+// epilogue: fp32 store / sketch output / parameter-vector write / fp32 (+)= table at g times the product
+enum { kEStore = 0, kEOut = 1, kEBcast = 2, kEMulAcc = 3 };
 
 struct QhArgs {
   // C (M x N) = P (M x K) . op(Q); batch index v = blockIdx.y
@@ -118,6 +121,8 @@ struct QhArgs {
   int ldp;
   int p_vec;      // 16-byte loads of P allowed (ldp % 4 == 0, aligned base)
   int p_rows;     // kPStacked: rows per vector
+  int64_t p_off;  // kPStacked: first element of the rows (a slab's offset)
+  int64_t o_off;  // kEBcast: first element written (a slab's offset)
   int nvec;       // slot form: vectors stacked
   int q_vec;      // NN fold: 16-byte (fp32) / 8-byte (bf16) loads of the input allowed
   const void *q;  // Q: NT: fp32 N x K (ldq = K); NN buffer: fp32 K x N; NN fold: the input
@@ -175,7 +180,7 @@ __device__ __forceinline__ f4v load_p4(const QhArgs &a, int64_t v, int row, int 
     const int64_t base = (a.b_in + vv) * a.n_in;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t f = (int64_t)h * a.ldp + k + e;
+      const int64_t f = a.p_off + (int64_t)h * a.ldp + k + e;
       if (k + e < a.K && f < a.n_in) r[e] = load_in(a.p, a.dtype, base + f);
     }
   }
@@ -195,8 +200,9 @@ __device__ __forceinline__ void load_tile(const QhArgs &a, int64_t v, int k0, in
 #pragma unroll
     for (int t = 0; t < PF; ++t) r[t][q] = f4v{0.f, 0.f, 0.f, 0.f};
     if (k >= a.K) continue;
-    if (QM == kQNNBuf) {
+    if (QM == kQNNBuf || QM == kQNNMul) {
       r[0][q] = *(const f4v *)((const float *)a.q + v * a.q_vs + (int64_t)k * a.N + cc);
+      if (QM == kQNNMul) r[0][q] *= *(const f4v *)(a.w + (int64_t)k * a.N + cc);
       continue;
     }
     const int64_t base = (a.b_in + v) * a.n_in;
@@ -322,10 +328,14 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a, QhSlots sl) {
         float *o = (float *)a.dst + (a.b_out + v) * a.D + idx;
         const float val = a.g ? a.g[idx] * y : y;
         *o = a.accumulate ? *o + val : val;
+      } else if (EP == kEMulAcc) {
+        float *o = (float *)a.dst + v * a.c_vs + (int64_t)row * a.ldc + col;
+        const float val = a.g[(int64_t)row * a.N + col] * y;
+        *o = a.accumulate ? *o + val : val;
       } else {
         const int64_t idx = (int64_t)row * a.N + col;
         for (int t = 0; t < a.nslab; ++t) {
-          const int64_t f = t * a.slab + idx;
+          const int64_t f = a.o_off + t * a.slab + idx;
           if (f >= a.n_out) break;
           float val = a.w ? a.w[t] * y : y;
           if (a.theta0) val += a.theta0[f];
@@ -411,6 +421,24 @@ __global__ void k_qh_zg(const float *__restrict__ z, int64_t D, int64_t b_in, co
   w[v * D + i] = g ? zz * g[i] : zz;
 }
 
+// AFFDQ: M[t][e] = sum_t' c[t'][t] g[t' slab + e] over the layer's G stream
+// (e < slab = b_m 1024); one thread per e holds the P <= kQhMaxLead values of g.
+__global__ __launch_bounds__(256) void k_qh_mtab(const float *__restrict__ c, int P, int64_t slab, uint32_t layer_id,
+                                                 Key key, float *__restrict__ m) {
+  const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (e >= slab) return;
+  float g[kQhMaxLead];
+#pragma unroll
+  for (int t = 0; t < kQhMaxLead; ++t) g[t] = t < P ? gauss((uint64_t)(t * slab + e), layer_id, ST_GAUSS, key) : 0.0f;
+  for (int t = 0; t < P; ++t) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int tp = 0; tp < kQhMaxLead; ++tp)
+      if (tp < P) acc += c[tp * P + t] * g[tp];
+    m[t * slab + e] = acc;
+  }
+}
+
 int tiles_for(int m) { return m >= 64 ? 4 : m > 16 ? 2 : 1; }
 
 template <int PM, int QM, int PF, int EP>
@@ -452,35 +480,72 @@ __global__ __launch_bounds__(256) void k_qh_small_slots(QhSlots sl, int T, const
 }  // namespace
 
 // ---------------------------------------------------------------- plan
-int qh_plan_layer(LayerDesc &ld, int64_t D) {
+int qh_plan_layer(LayerDesc &ld, int64_t D, int kind) {
   // factor m = K - 2 keeps D / 1024 rows; the last factor all 1024
   if (ld.K < 2 || ld.lg[ld.K - 1] != 10) return SK_EUNSUPPORTED;
   ld.qbm = 1 << ld.lg[ld.K - 2];
   ld.qdm = (int32_t)(D >> 10);
   ld.qP = ld.np / ((int64_t)ld.qbm << 10);
+  if (kind == SK_AFFDQ && ld.qP > kQhMaxLead) return SK_EUNSUPPORTED;
   return ld.qdm >= 1 && ld.qdm <= ld.qbm ? SK_OK : SK_EUNSUPPORTED;
 }
 
-int64_t qh_layer_floats(const LayerDesc &ld) {
-  return 2ll * ld.qdm * ld.qbm + 2ll * 1024 * 1024 + ld.qP;
+QhLayout qh_layout(const LayerDesc &ld, int kind) {
+  const int64_t T2 = 1024 * 1024, bm = ld.qbm, dm = ld.qdm, P = ld.qP;
+  QhLayout o{};
+  if (kind != SK_AFFDQ) {
+    o.a = 0;
+    o.at = dm * bm;
+    o.qt = 2 * dm * bm;
+    o.qtt = o.qt + T2;
+    o.w = o.qtt + T2;
+    o.total = o.w + P;
+  } else {
+    o.q1m = 0;
+    o.q1mt = bm * bm;
+    o.q1l = 2 * bm * bm;
+    o.q1lt = o.q1l + T2;
+    o.a = o.q1lt + T2;
+    o.at = o.a + dm * bm;
+    o.qt = o.at + dm * bm;
+    o.qtt = o.qt + T2;
+    o.c = o.qtt + T2;
+    o.m = (o.c + P * P + 3) & ~3ll;
+    o.total = o.m + P * bm * 1024;
+  }
+  return o;
 }
 
+int64_t qh_layer_floats(const LayerDesc &ld, int kind) { return qh_layout(ld, kind).total; }
+
 // Generates every layer's factors (host, fp64, threads over factors) and
-// writes A, A^T, Qt, Qt^T and w in fp32 into host[] at the layers' offsets.
+// writes them in fp32 into host[] at the layers' offsets (qh_layout): for
+// QKH/AFJLQ A, A^T, Qt, Qt^T and w; for AFFDQ the first set's factor K - 2 and
+// its transpose, last factor and its transpose, the second set's A, A^T, Qt,
+// Qt^T, and c[t'][t] = w2[t'] Qlead[t'][t] (w2: the second set's leading first
+// rows, Qlead: the first set's leading factors) from which the device forms M.
 void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
   struct Job {
-    int layer, k, b;
+    int layer, k, b;  // k: factor index in the stream (second set: kQhSecond + digit)
   };
+  const bool affd = s->kind == SK_AFFDQ;
   std::vector<Job> jobs;
   for (int l = 0; l < (int)s->layers.size(); ++l) {
     const LayerDesc &ld = s->layers[l];
-    for (int k = 0; k < ld.K; ++k) jobs.push_back(Job{l, k, 1 << ld.lg[k]});
+    for (int k = 0; k < ld.K; ++k) {
+      jobs.push_back(Job{l, k, 1 << ld.lg[k]});
+      if (affd) jobs.push_back(Job{l, kQhSecond + k, 1 << ld.lg[k]});
+    }
   }
   // largest factors first so the threads finish together
   std::stable_sort(jobs.begin(), jobs.end(), [](const Job &x, const Job &y) { return x.b > y.b; });
-  // first rows of the leading factors, per layer and factor
-  std::vector<std::vector<std::vector<double>>> lead(s->layers.size());
-  for (size_t l = 0; l < s->layers.size(); ++l) lead[l].resize(s->layers[l].K);
+  // per layer and digit: first rows (QKH/AFJLQ, AFFDQ second set) and whole
+  // leading factors (AFFDQ first set), row-major
+  std::vector<std::vector<std::vector<double>>> lead(s->layers.size()), whole(s->layers.size());
+  for (size_t l = 0; l < s->layers.size(); ++l) {
+    lead[l].resize(s->layers[l].K);
+    whole[l].resize(s->layers[l].K);
+  }
   std::atomic<size_t> next{0};
   auto work = [&]() {
     std::vector<double> a, q;
@@ -490,6 +555,8 @@ void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
       const Job jb = jobs[j];
       const LayerDesc &ld = s->layers[jb.layer];
       const int b = jb.b;
+      const bool second = jb.k >= kQhSecond;
+      const int digit = second ? jb.k - kQhSecond : jb.k;
       a.resize((size_t)b * b);
       q.resize((size_t)b * b);
       // A[r][c] = number k 2^20 + r b + c, stored column-major
@@ -500,27 +567,32 @@ void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
       haar_from_gaussian(a.data(), b, q.data());
       // q is column-major: Q[r][c] = q[c b + r]
       float *base = host.data() + ld.qoff;
+      const QhLayout o = qh_layout(ld, s->kind);
       const double sc = std::sqrt((double)ld.np / (double)s->D);
-      if (jb.k == ld.K - 2) {
-        float *A = base, *At = base + (int64_t)ld.qdm * ld.qbm;
-        for (int r = 0; r < ld.qdm; ++r)
+      auto put = [&](int64_t off, int64_t offt, int rows, double scale) {  // rows x b and its transpose
+        for (int r = 0; r < rows; ++r)
           for (int c = 0; c < b; ++c) {
-            const float x = (float)(sc * q[(size_t)c * b + r]);
-            A[(int64_t)r * b + c] = x;
-            At[(int64_t)c * ld.qdm + r] = x;
+            const float x = (float)(scale * q[(size_t)c * b + r]);
+            base[off + (int64_t)r * b + c] = x;
+            base[offt + (int64_t)c * rows + r] = x;
           }
-      } else if (jb.k == ld.K - 1) {
-        float *Qt = base + 2ll * ld.qdm * ld.qbm, *QtT = Qt + 1024 * 1024;
-        for (int r = 0; r < b; ++r)
-          for (int c = 0; c < b; ++c) {
-            const float x = (float)q[(size_t)c * b + r];
-            Qt[(int64_t)r * b + c] = x;
-            QtT[(int64_t)c * b + r] = x;
-          }
-      } else {
+      };
+      const bool restricted = !affd || second;  // the set R_D applies to
+      if (digit == ld.K - 2) {
+        if (restricted) put(o.a, o.at, ld.qdm, sc);
+        else put(o.q1m, o.q1mt, b, 1.0);
+      } else if (digit == ld.K - 1) {
+        if (restricted) put(o.qt, o.qtt, b, 1.0);
+        else put(o.q1l, o.q1lt, b, 1.0);
+      } else if (restricted) {
         std::vector<double> row(b);
         for (int c = 0; c < b; ++c) row[c] = q[(size_t)c * b];
-        lead[jb.layer][jb.k] = std::move(row);  // distinct slot per job
+        lead[jb.layer][digit] = std::move(row);  // distinct slot per job
+      } else {
+        std::vector<double> m((size_t)b * b);
+        for (int r = 0; r < b; ++r)
+          for (int c = 0; c < b; ++c) m[(size_t)r * b + c] = q[(size_t)c * b + r];
+        whole[jb.layer][digit] = std::move(m);
       }
     }
   };
@@ -530,9 +602,10 @@ void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
   for (unsigned i = 1; i < nt; ++i) th.emplace_back(work);
   work();
   for (auto &t : th) t.join();
-  // w = Kronecker product of the leading factors' first rows (digit 0 most significant)
   for (size_t l = 0; l < s->layers.size(); ++l) {
     const LayerDesc &ld = s->layers[l];
+    const QhLayout o = qh_layout(ld, s->kind);
+    // w = Kronecker product of the leading first rows (digit 0 most significant)
     std::vector<double> w(1, 1.0);
     for (int k = 0; k < ld.K - 2; ++k) {
       std::vector<double> nw(w.size() * lead[l][k].size());
@@ -540,8 +613,27 @@ void qh_generate_factors(const sk_sketch *s, std::vector<float> &host) {
         for (size_t c = 0; c < lead[l][k].size(); ++c) nw[i * lead[l][k].size() + c] = w[i] * lead[l][k][c];
       w.swap(nw);
     }
-    float *wp = host.data() + ld.qoff + 2ll * ld.qdm * ld.qbm + 2ll * 1024 * 1024;
-    for (int64_t t = 0; t < ld.qP; ++t) wp[t] = (float)w[t];
+    float *base = host.data() + ld.qoff;
+    if (!affd) {
+      for (int64_t t = 0; t < ld.qP; ++t) base[o.w + t] = (float)w[t];
+      continue;
+    }
+    // Qlead = Kronecker product of the first set's leading factors (P x P)
+    std::vector<double> ql(1, 1.0);
+    int64_t dim = 1;
+    for (int k = 0; k < ld.K - 2; ++k) {
+      const int64_t b = 1ll << ld.lg[k];
+      std::vector<double> nq((size_t)(dim * b) * (dim * b));
+      for (int64_t i = 0; i < dim; ++i)
+        for (int64_t j = 0; j < dim; ++j)
+          for (int64_t r = 0; r < b; ++r)
+            for (int64_t c = 0; c < b; ++c)
+              nq[(size_t)((i * b + r) * dim * b + j * b + c)] = ql[(size_t)(i * dim + j)] * whole[l][k][(size_t)(r * b + c)];
+      ql.swap(nq);
+      dim *= b;
+    }
+    for (int64_t tp = 0; tp < ld.qP; ++tp)
+      for (int64_t t = 0; t < ld.qP; ++t) base[o.c + tp * ld.qP + t] = (float)(w[tp] * ql[(size_t)(tp * ld.qP + t)]);
   }
 }
 
@@ -553,6 +645,7 @@ static bool qh_b_first(const LayerDesc &ld) { return ld.qP == 1 && qh_live_rows(
 int64_t qh_bytes_per_vector(const sk_sketch *s, int layer, bool transpose) {
   const LayerDesc &ld = s->layers[layer];
   const int64_t T = 1024;
+  if (s->kind == SK_AFFDQ) return (2ll * ld.qbm + ld.qdm) * T * 4;  // U + F + T2, or U2 + F' + W
   if (!transpose) {
     if (qh_b_first(ld)) return 0;  // grouped: qh_small_bytes_per_vector
     const bool fold = !(ld.qP == 1 || ld.qP == 2 || ld.qP == 4);
@@ -602,11 +695,12 @@ void run_qh_small_group(const sk_sketch *s, int l0, int l1, int gi, const void *
     const int l = grp[z];
     const LayerDesc &ld = s->layers[l];
     const float *base = s->d_qh + ld.qoff;
+    const QhLayout o = qh_layout(ld, s->kind);
     sl.x[z] = x[l - l0];
     sl.n_in[z] = ld.n;
     sl.rows[z] = (int)qh_live_rows(ld);
-    sl.qt[z] = base + 2ll * ld.qdm * ld.qbm;
-    sl.A[z] = base;
+    sl.qt[z] = base + o.qt;
+    sl.A[z] = base + o.a;
     sl.lda[z] = ld.qbm;
     sl.g[z] = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)l * s->D : nullptr;
     sl.uoff[z] = uoff;
@@ -647,7 +741,8 @@ void run_qh_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64
                   float *out, bool accumulate, int phases, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const float *base = s->d_qh + ld.qoff;
-  const float *A = base, *Qt = base + 2ll * ld.qdm * ld.qbm, *w = Qt + 2ll * 1024 * 1024;
+  const QhLayout o = qh_layout(ld, s->kind);
+  const float *A = base + o.a, *Qt = base + o.qt, *w = base + o.w;
   const float *g = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)layer * s->D : nullptr;
   const int T = 1024;
   QhArgs a{};
@@ -711,8 +806,8 @@ void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_beg
                     int out_dtype, const float *theta0, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const float *base = s->d_qh + ld.qoff;
-  const float *At = base + (int64_t)ld.qdm * ld.qbm;
-  const float *Qt = base + 2ll * ld.qdm * ld.qbm, *QtT = Qt + 1024 * 1024, *w = QtT + 1024 * 1024;
+  const QhLayout o = qh_layout(ld, s->kind);
+  const float *At = base + o.at, *QtT = base + o.qtt, *w = base + o.w;
   const float *g = s->kind == SK_AFJLQ ? s->d_gtab + (int64_t)layer * s->D : nullptr;
   const int T = 1024;
   float *zg = ws, *u = ws + bc * s->D;
@@ -772,6 +867,178 @@ void run_qh_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_beg
   a.nslab = (int)ld.qP;
   a.w = w;
   launch_gemm<kPBuf, kQNNBuf, 1, kEBcast>(a, bc, st);
+}
+
+// ---------------------------------------------------------------- AFFDQ
+void launch_affdq_mtab(const sk_sketch *s, int layer, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const QhLayout o = qh_layout(ld, s->kind);
+  const int64_t slab = (int64_t)ld.qbm * 1024;
+  hipLaunchKernelGGL(k_qh_mtab, dim3((unsigned)((slab + 255) / 256)), dim3(256), 0, st, s->d_qh + ld.qoff + o.c,
+                     (int)ld.qP, slab, (uint32_t)ld.layer_id, s->key, s->d_qh + ld.qoff + o.m);
+}
+
+// Live rows (of 1024) of slab t of a layer.
+static int affdq_slab_rows(const LayerDesc &ld, int64_t t) {
+  const int64_t slab = (int64_t)ld.qbm * 1024;
+  const int64_t left = ld.n - t * slab;
+  if (left <= 0) return 0;
+  return (int)std::min<int64_t>(ld.qbm, (left + 1023) / 1024);
+}
+
+// Forward.  Phase 1: F = sum_t M_t . (Q1m X_t Q1L^T) over the live slabs (per
+// slab U = X_t Q1L^T on the live rows with the vectors stacked, then
+// F (+)= M_t . (Q1m[:, :r] U)).  Phase 2: T2 = A2 F, out (+)= T2 Q2L^T.
+void run_affdq_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *ws,
+                     float *out, bool accumulate, int phases, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const float *base = s->d_qh + ld.qoff;
+  const QhLayout o = qh_layout(ld, s->kind);
+  const int T = 1024, bm = ld.qbm;
+  const int64_t slab = (int64_t)bm * T;
+  float *u = ws, *f = ws + bc * slab, *t2 = f + bc * slab;
+  if (phases & 1) {
+    bool first = true;
+    for (int64_t t = 0; t < ld.qP; ++t) {
+      const int r = affdq_slab_rows(ld, t);
+      if (r == 0) break;
+      QhArgs a{};
+      a.M = (int)(bc * r);
+      a.N = T;
+      a.K = T;
+      a.p = x;
+      a.ldp = T;
+      a.p_rows = r;
+      a.p_off = t * slab;
+      a.dtype = dtype;
+      a.n_in = ld.n;
+      a.b_in = b_begin;
+      a.q = base + o.q1l;
+      a.dst = u;
+      a.ldc = T;
+      launch_gemm<kPStacked, kQNT, 1, kEStore>(a, 1, st);
+      QhArgs b{};
+      b.M = bm;
+      b.N = T;
+      b.K = r;
+      b.p = base + o.q1m;
+      b.ldp = bm;
+      b.p_vec = bm % 4 == 0;
+      b.q = u;
+      b.q_vs = (int64_t)r * T;
+      b.dst = f;
+      b.c_vs = slab;
+      b.ldc = T;
+      b.g = base + o.m + t * slab;
+      b.accumulate = !first;
+      launch_gemm<kPBuf, kQNNBuf, 1, kEMulAcc>(b, bc, st);
+      first = false;
+    }
+    if (first) launch_fill_zero(f, bc * slab, st);  // no live slab (empty layer cannot occur; kept total)
+  }
+  if (phases & 2) {
+    QhArgs a{};
+    a.M = ld.qdm;
+    a.N = T;
+    a.K = bm;
+    a.p = base + o.a;
+    a.ldp = bm;
+    a.p_vec = bm % 4 == 0;
+    a.q = f;
+    a.q_vs = slab;
+    a.dst = t2;
+    a.c_vs = (int64_t)ld.qdm * T;
+    a.ldc = T;
+    launch_gemm<kPBuf, kQNNBuf, 1, kEStore>(a, bc, st);
+    QhArgs b{};
+    b.M = ld.qdm;
+    b.N = T;
+    b.K = T;
+    b.p = t2;
+    b.p_vs = (int64_t)ld.qdm * T;
+    b.ldp = T;
+    b.p_vec = 1;
+    b.q = base + o.qt;
+    b.dst = out;
+    b.D = s->D;
+    b.b_out = b_begin;
+    b.accumulate = accumulate;
+    launch_gemm<kPBuf, kQNT, 1, kEOut>(b, bc, st);
+  }
+}
+
+// Transpose: U2 = Z Q2L, F' = A2^T U2, then per live slab t the output rows
+// X'_t[:r] = Q1m^T[:r] (M_t . F') Q1L.
+void run_affdq_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws,
+                       void *out, int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const float *base = s->d_qh + ld.qoff;
+  const QhLayout o = qh_layout(ld, s->kind);
+  const int T = 1024, bm = ld.qbm;
+  const int64_t slab = (int64_t)bm * T;
+  float *u2 = ws, *fp = ws + bc * (int64_t)ld.qdm * T, *w = fp + bc * slab;
+  QhArgs a{};
+  a.M = ld.qdm;
+  a.N = T;
+  a.K = T;
+  a.p = z + b_begin * s->D;
+  a.p_vs = s->D;
+  a.ldp = T;
+  a.p_vec = 1;
+  a.q = base + o.qtt;
+  a.dst = u2;
+  a.c_vs = (int64_t)ld.qdm * T;
+  a.ldc = T;
+  launch_gemm<kPBuf, kQNT, 1, kEStore>(a, bc, st);
+  QhArgs b{};
+  b.M = bm;
+  b.N = T;
+  b.K = ld.qdm;
+  b.p = base + o.at;
+  b.ldp = ld.qdm;
+  b.p_vec = ld.qdm % 4 == 0;
+  b.q = u2;
+  b.q_vs = (int64_t)ld.qdm * T;
+  b.dst = fp;
+  b.c_vs = slab;
+  b.ldc = T;
+  launch_gemm<kPBuf, kQNNBuf, 1, kEStore>(b, bc, st);
+  for (int64_t t = 0; t < ld.qP; ++t) {
+    const int r = affdq_slab_rows(ld, t);
+    if (r == 0) break;
+    QhArgs c{};
+    c.M = r;
+    c.N = T;
+    c.K = bm;
+    c.p = base + o.q1mt;
+    c.ldp = bm;
+    c.p_vec = bm % 4 == 0;
+    c.q = fp;
+    c.q_vs = slab;
+    c.w = base + o.m + t * slab;
+    c.dst = w;
+    c.c_vs = (int64_t)r * T;
+    c.ldc = T;
+    launch_gemm<kPBuf, kQNNMul, 1, kEStore>(c, bc, st);
+    QhArgs d{};
+    d.M = r;
+    d.N = T;
+    d.K = T;
+    d.p = w;
+    d.p_vs = (int64_t)r * T;
+    d.ldp = T;
+    d.p_vec = 1;
+    d.q = base + o.q1lt;
+    d.dst = out;
+    d.dst_dtype = out_dtype;
+    d.n_out = ld.n;
+    d.b_out = b_begin;
+    d.theta0 = theta0;
+    d.nslab = 1;
+    d.slab = slab;
+    d.o_off = t * slab;
+    launch_gemm<kPBuf, kQNT, 1, kEBcast>(d, bc, st);
+  }
 }
 
 }  // namespace sk

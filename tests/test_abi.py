@@ -51,7 +51,8 @@ def shapes(*ss):
     (5, [(1, 10)], 1024, 0, -5),          # QKH: D below 2048
     (6, [(1, 10)], 1 << 21, 0, -5),       # AFJLQ: D above 2^20
     (6, [(1, 10)], 3000, 0, -1),          # AFJLQ: D not a power of two
-    (7, [(1, 10)], 4096, 0, -1),          # unknown kind
+    (8, [(1, 10)], 4096, 0, -1),          # unknown kind
+    (7, [(1, 1 << 27)], 4096, 0, -5),     # AFFDQ: N' above 2^26
 ])
 def test_create_rejects_invalid_arguments(kind, shp, D, flags, code):
     L = _lib.load()

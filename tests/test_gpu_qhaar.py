@@ -1,5 +1,6 @@
 """GPU parity of the kinds with the random-orthogonal Kronecker pre-conditioner
-(QKH: eq. straight on the flattened layer; AFJLQ: eq. frikadel with H_N -> Q)
+(QKH: eq. straight on the flattened layer; AFJLQ: eq. frikadel with H_N -> Q;
+AFFDQ: eq. bami with both H_N -> Q)
 through the C ABI, against the fp64 oracle.  Same error metric and fp32
 tolerance as the other kinds: per batch row max_i |y_i - o_i| / max(|o_i|, rms(o)).
 
@@ -146,3 +147,51 @@ def test_gpt2_small_full_size_sampled_rows(dev):
     rows = [0, batch - 1]
     ref = O.apply("afjlq", shapes, D, seed, [x[rows].cpu().numpy() for x in xs])
     assert rel_err(y[rows], ref) < TOL
+
+
+# AFFDQ: dense per slab, so smaller cases (live slabs 1 .. 2, Qt-first-sized small layers, D = 2048 .. 2^16)
+AFFDQ_CASES = [
+    ([(1, 768), (3, 1000), (64, 64), (1, 2 ** 21 - 5)], 4096),
+    ([(7, 300), (1, 2 ** 20 + 1)], 2048),
+    ([(1, 768), (768, 768)], 65536),
+]
+
+
+@pytest.mark.parametrize("case", range(len(AFFDQ_CASES)))
+def test_affdq_forward_parity(case, dev):
+    shapes, D = AFFDQ_CASES[case]
+    seed = 500 + case
+    xs = inputs(shapes, 2, seed)
+    s = sketch("affdq", shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("affdq", shapes, D, seed, [x.numpy() for x in xs])
+    assert rel_err(y, ref) < TOL
+
+
+@pytest.mark.parametrize("case", range(len(AFFDQ_CASES)))
+def test_affdq_transpose_parity(case, dev):
+    shapes, D = AFFDQ_CASES[case]
+    seed = 600 + case
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((2, D), generator=g)
+    th = [None if i == 0 else torch.randn(r * c, generator=g) * 0.02 for i, (r, c) in enumerate(shapes)]
+    s = sketch("affdq", shapes, D, seed, dev)
+    outs = s.apply_T(z.to(dev), theta0=[None if t is None else t.to(dev) for t in th])
+    refs = O.apply_T("affdq", shapes, D, seed, z.numpy().astype(np.float64),
+                     theta0=[None if t is None else t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL
+
+
+def test_affdq_bf16_streaming(dev):
+    shapes, D = AFFDQ_CASES[1]
+    xs = [x.to(dev) for x in inputs(shapes, 2, 31, torch.bfloat16)]
+    s = sketch("affdq", shapes, D, 32, dev)
+    y1 = s.apply(xs)
+    assert torch.equal(y1, s.apply(xs))
+    out = torch.zeros_like(y1)
+    for l, x in enumerate(xs):
+        s.apply([x], out=out, first_layer=l, accumulate=True)
+    ins = [as_oracle(x.cpu()) for x in xs]
+    ref = O.apply("affdq", shapes, D, 32, [a for a, _ in ins], dtype="bf16")
+    assert rel_err(out.cpu().numpy(), ref) < TOL
