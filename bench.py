@@ -5,7 +5,7 @@ Default workload (--config c2): per-example gradients shaped like GPT-2 small
 (148 tensors, N = 124,439,808), fp32 entries N(0, 1e-4), batch 64, sketched to
 D = 2^16 by AFJL and by AFFD (seed 1).  One step sketches the whole batch with
 both kinds; inputs are resident in HBM before the timed region.  Other
-workloads (--config c1|c3|c4|c5|c6) are described in workloads.py.  Prints one
+workloads (--config c1|c3|c4|c5|c6|c7) are described in workloads.py.  Prints one
 JSON line.
 
 "value" is parameter-space bytes per second: gradient bytes read by forward
@@ -45,29 +45,41 @@ MFMA_F32_PEAK_TFLOPS = 157.3
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
              "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
              "fjl:prolog": "k_fjl_prolog", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
-             "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm"}
+             "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
+             "affdq:qh_t": "k_qh_gemm"}
 
 
-def qh_flops(shapes, D):
-    """Multiply-add flops (2 per product) per vector of the two contractions of the Q kinds, per
-    class (qh_first reads the input, qh_second forms the output), with the library's operand order."""
-    first = second = 0
+def qh_flops(kind, shapes, D):
+    """Multiply-add flops (2 per product) per vector of the contractions of the Q kinds, per profile
+    class (qh_first reads the input, qh_second forms the output, qh_t the transpose), following the
+    library's operand order."""
+    first = second = trans = 0
+    T, dm = 1024, D // 1024
     for r, c in shapes:
         n = r * c
         np_len = 1
         while np_len < max(n, D):
             np_len *= 2
         bm = min(1024, np_len // 1024)  # factor K - 2 (the last factor is 1024 wide)
-        dm, T = D // 1024, 1024
         P = np_len // (bm * T)
+        if kind == "affdq":
+            for t in range(P):
+                rt = min(bm, max(0, -(-(n - t * bm * T) // T)))
+                first += 2 * rt * T * T + 2 * bm * rt * T
+                trans += 2 * rt * bm * T + 2 * rt * T * T
+            second += 2 * dm * bm * T + 2 * dm * T * T
+            trans += 2 * dm * T * T + 2 * bm * dm * T
+            continue
         live = -(-n // T)
         if P == 1 and live < dm:  # Qt first on the live rows, then A's live columns
             first += 2 * live * T * T
             second += 2 * dm * live * T
+            trans += 2 * live * dm * T + 2 * live * T * T
         else:
             first += 2 * dm * bm * T
             second += 2 * dm * T * T
-    return {"qh_first": first, "qh_second": second}
+            trans += 2 * dm * T * T + 2 * bm * dm * T
+    return {"qh_first": first, "qh_second": second, "qh_t": trans}
 
 
 def source_hash() -> str:
@@ -189,6 +201,13 @@ def cpu_baseline(cfg: str):
         O.apply("ffd", shapes, D, seed, xs, nthreads=cores)
         nbytes = 2 * shapes[0][1] * 4
         sample = "1 of 4 rows, FFD transpose and forward"
+    elif cfg == "c7":
+        xs = rows_for(shapes, 1, 1.0)
+        z = rng.standard_normal((1, D))
+        O.apply("affdq", shapes, D, seed, xs)
+        O.apply_T("affdq", shapes, D, seed, z)
+        nbytes = 2 * shapes[0][1] * 4
+        sample = f"1 of {c['batch']} rows, AFFDQ forward and transpose, factor generation included"
     elif cfg == "c6":
         sub = shapes[2:14]  # one transformer block: ln_1, attn, ln_2, mlp (12 tensors)
         xs = rows_for(sub, 1)
@@ -225,7 +244,7 @@ def build_step(cfg: str, dev):
     dt = torch.bfloat16 if bf16 else torch.float32
     sks = {k: Sketch(k, shapes, D, seed, device=dev) for k in c["kinds"]}
 
-    if cfg == "c1":
+    if cfg in ("c1", "c7"):
         nrot = 16  # rotate inputs so they come from HBM, not the 256 MB cache
         xs = [W.gaussian((B, numels[0]), 1.0, gen, dev) for _ in range(nrot)]
         z = torch.randn((B, D), generator=gen, device=dev)
@@ -239,8 +258,9 @@ def build_step(cfg: str, dev):
             for k in c["kinds"]:
                 ev(k, "fwd", lambda k=k: sks[k].apply([x], out=outs[k]))
                 ev(k, "T", lambda k=k: sks[k].apply_T(z, outs=touts[k]))
+        names = " and ".join(k.upper() for k in c["kinds"])
         return sks, step, 2 * len(c["kinds"]) * B * numels[0] * 4, B, \
-            f"flat fp32 vectors N=2^20 entries N(0,1), batch {B}, D=4096, seed 0: FJL and FFD forward + transpose"
+            f"flat fp32 vectors N=2^20 entries N(0,1), batch {B}, D=4096, seed 0: {names} forward + transpose"
 
     if cfg in ("c2", "c6"):
         xs = [W.gaussian((B, n), 1e-4, gen, dev) for n in numels]
@@ -395,10 +415,10 @@ def main() -> int:
         flops = sum(2 * s[0] * s[1] * s[3] + 2 * s[2] * s[0] * s[3] for s in c["shapes"]) * c["batch"]
         roofline["mfma_tflops"] = round(flops / (t_dom * 1e-3 / args.steps) / 1e12, 1)
         roofline["mfma_frac"] = round(roofline["mfma_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4)
-    if cfg == "c6":
+    if cfg in ("c6", "c7"):
         # fp32 MFMA contractions: the bound is the larger of the two fractions
         c = W.CONFIGS[cfg]
-        flops = qh_flops(c["shapes"], c["D"])[dom.split(":")[1]] * c["batch"] * args.steps
+        flops = qh_flops(dom_kind, c["shapes"], c["D"])[dom_cls] * c["batch"] * args.steps
         tf = flops / (t_dom * 1e-3) / 1e12 if t_dom > 0 else 0.0
         roofline["mfma_tflops"] = round(tf, 1)
         roofline["mfma_frac"] = round(tf / MFMA_F32_PEAK_TFLOPS, 4)

@@ -238,8 +238,9 @@ enum {
   SK_PROF_AFFD_ROWS = 9, /* AFFD row kernel: load, sign, pi1, H_l (one launch) */
   SK_PROF_QK_XB = 10,    /* QK first contraction X B^T (reads the gradients) */
   SK_PROF_QH_FIRST = 11, /* SK_QKH/SK_AFJLQ contraction that reads the input */
-  SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ second contraction (and transpose) */
-  SK_PROF_CLASSES = 13
+  SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ/SK_AFFDQ second contraction        */
+  SK_PROF_QH_T = 13,     /* SK_QKH/SK_AFJLQ/SK_AFFDQ transposes               */
+  SK_PROF_CLASSES = 14
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

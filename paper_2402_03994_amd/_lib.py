@@ -15,7 +15,7 @@ EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", 
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
            "sketch_status_string")
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
-                "affd_rows", "qk_xb", "qh_first", "qh_second"]
+                "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t"]
 
 
 class LayerShape(ctypes.Structure):

@@ -888,10 +888,10 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           break;
         case SK_QKH:
         case SK_AFJLQ:
-          SK_PROF(SK_PROF_QH_SECOND, obytes, run_qh_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
+          SK_PROF(SK_PROF_QH_T, obytes, run_qh_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
           break;
         case SK_AFFDQ:
-          SK_PROF(SK_PROF_QH_SECOND, obytes, run_affdq_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
+          SK_PROF(SK_PROF_QH_T, obytes, run_affdq_apply_T(s, l, z, b0, bc, s->ws, o, out_dtype, th, st));
           break;
         case SK_QK:
           SK_PROF(SK_PROF_QK, obytes + bc * ld.da * ld.db * 4,

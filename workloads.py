@@ -70,10 +70,12 @@ CONFIGS = {
     "c5": dict(kinds=("afjl",), shapes=llama3_8b_shapes(), D=1 << 20, batch=8, seed=7, dtype="bf16"),
     # the C2 gradients through the sketches with the random-orthogonal pre-conditioner Q
     "c6": dict(kinds=("afjlq", "qkh"), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
+    # AFFD with Q (dense: ~4.3 GFLOP per vector and 2^20-element slab each way) on C1's vectors
+    "c7": dict(kinds=("affdq",), shapes=[(1, 1 << 20)], D=4096, batch=8, seed=0, dtype="f32"),
 }
-INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002}
+INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001}
 # variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
-GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4}
+GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4, "c7": 1.0}
 
 
 def gaussian(shape, var: float, gen: torch.Generator, device, dtype=torch.float32) -> torch.Tensor:
