@@ -8,7 +8,9 @@ The arithmetic lives in ``sk_oracle.c`` (plain C, double precision, textbook
 Walsh-Hadamard transform, literal operator chains of the paper's equations
 ailon_chazelle, fastfood, bami, frikadel and straight).  This module only
 marshals numpy arrays into that library.  The kinds with the random-orthogonal
-Kronecker pre-conditioner (QKH, AFJLQ) are in ``qhaar.py`` (numpy, fp64).
+Kronecker pre-conditioner (QKH, AFJLQ, AFFDQ) are in ``qhaar.py`` (numpy, fp64);
+the synthetic Hessian, the sketched HVP operator and the Arnoldi iteration on
+it are in ``krylov.py``.
 """
 from __future__ import annotations
 
@@ -26,7 +28,8 @@ KINDS = {"fjl": 0, "ffd": 1, "affd": 2, "afjl": 3, "qk": 4}
 # kinds with the random-orthogonal Kronecker pre-conditioner (numpy, qhaar.py)
 QKINDS = ("qkh", "afjlq", "affdq")
 DTYPES = {"f32": 0, "bf16": 1}
-STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}
+STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9,
+           "hvp": 10}
 
 
 def build() -> str:
@@ -76,6 +79,11 @@ def lib():
         L.orc_gauss_range.argtypes = [u64, u32, u32, u64, u64, P]
         L.orc_index_range.argtypes = [u64, u32, u64, u64, u64, P]
         L.orc_perm_table.argtypes = [u64, u32, u32, u32, u32, P]
+        L.orc_hvp_sign.argtypes = [u64, u32, u32, u64]
+        L.orc_hvp_sign.restype = ctypes.c_int
+        L.orc_hvp_signs.argtypes = [u64, u32, u32, u64, u64, P]
+        L.orc_hvp_dots.argtypes = [u64, u32, ctypes.c_int, u64, P, P]
+        L.orc_hvp_combine.argtypes = [u64, u32, ctypes.c_int, u64, ctypes.c_double, P, P, P]
         _lib = L
     return _lib
 

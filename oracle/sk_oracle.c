@@ -589,3 +589,47 @@ void orc_index_range(uint64_t seed, uint32_t layer, uint64_t start, uint64_t cou
 void orc_perm_table(uint64_t seed, uint32_t layer, uint32_t stream, uint32_t pid, uint32_t w, uint32_t *out) {
   for (uint32_t x = 0; x < (1u << w); ++x) out[x] = orc_perm(seed, layer, stream, pid, w, x);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Synthetic Hessian for the sketched HVP operator v -> S HVP(S^T v) of      */
+/* Sec. 2 (sketching the Hessian-vector product) and Sec. 4 ("Scaling        */
+/* eigenvalue estimation").  It stands in for the model's HVP:               */
+/*   H = shift I + sum_{j < r} lambda_j v_j v_j^T                            */
+/* on the concatenated parameters (N_tot = sum of the layers' element        */
+/* counts), v_j = s_j / sqrt(N_tot), s_j a Rademacher vector.  Coordinate e  */
+/* of layer l takes, for vector j, bit (e mod 32) of word ((e / 32) mod 4)   */
+/* of the Philox block with counter (e / 128, (l << 6) | j, ST_HVP); bit 1   */
+/* means -1.  The scaling by lambda_j / N_tot is left to the caller.         */
+/* ------------------------------------------------------------------------ */
+enum { ST_HVP = 10 };
+
+int orc_hvp_sign(uint64_t seed, uint32_t layer, uint32_t j, uint64_t e) {
+  uint32_t w[4];
+  block(seed, (layer << 6) | j, ST_HVP, e >> 7, w);
+  return ((w[(e >> 5) & 3] >> (e & 31)) & 1u) ? -1 : 1;
+}
+
+void orc_hvp_signs(uint64_t seed, uint32_t layer, uint32_t j, uint64_t start, uint64_t count, int8_t *out) {
+  for (uint64_t i = 0; i < count; ++i) out[i] = (int8_t)orc_hvp_sign(seed, layer, j, start + i);
+}
+
+/* t[j] += sum_e s_j(e) x[e] over the n coordinates of one layer, j < r. */
+void orc_hvp_dots(uint64_t seed, uint32_t layer, int r, uint64_t n, const double *x, double *t) {
+#pragma omp parallel for schedule(static)
+  for (int j = 0; j < r; ++j) {
+    double acc = 0.0;
+    for (uint64_t e = 0; e < n; ++e) acc += orc_hvp_sign(seed, layer, (uint32_t)j, e) * x[e];
+    t[j] += acc;
+  }
+}
+
+/* y[e] = shift x[e] + sum_j coef[j] s_j(e) over the n coordinates of one layer. */
+void orc_hvp_combine(uint64_t seed, uint32_t layer, int r, uint64_t n, double shift, const double *coef,
+                     const double *x, double *y) {
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < (int64_t)n; ++e) {
+    double acc = shift * x[e];
+    for (int j = 0; j < r; ++j) acc += coef[j] * orc_hvp_sign(seed, layer, (uint32_t)j, (uint64_t)e);
+    y[e] = acc;
+  }
+}
