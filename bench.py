@@ -5,7 +5,8 @@ Default workload (--config c2): per-example gradients shaped like GPT-2 small
 (148 tensors, N = 124,439,808), fp32 entries N(0, 1e-4), batch 64, sketched to
 D = 2^16 by AFJL and by AFFD (seed 1).  One step sketches the whole batch with
 both kinds; inputs are resident in HBM before the timed region.  Other
-workloads (--config c1|c3|c4|c5|c6|c7) are described in workloads.py.  Prints one
+workloads (--config c1|c3|c4|c5|c6|c7|c8) are described in workloads.py; c8 times
+Arnoldi on the sketched HVP operator (a step = 64 Krylov steps).  Prints one
 JSON line.
 
 "value" is parameter-space bytes per second: gradient bytes read by forward
@@ -46,7 +47,8 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
              "fjl:prolog": "k_fjl_prolog", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
              "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
-             "affdq:qh_t": "k_qh_gemm"}
+             "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
+             "afjl:gather": "k_afjl_T_out"}
 
 
 def qh_flops(kind, shapes, D):
@@ -216,6 +218,16 @@ def cpu_baseline(cfg: str):
         nbytes = len(c["kinds"]) * sum(r * cc for r, cc in sub) * 4
         sample = f"1 of {c['batch']} rows, one transformer block (12 of {len(shapes)} tensors), AFJLQ+QKH, " \
                  "factor generation included"
+    elif cfg == "c8":
+        from oracle import krylov as K
+
+        lam = np.array(W.C8_LAMBDAS, dtype=np.float32)
+        hp = dict(rank=len(lam), lambdas=lam, shift=float(np.float32(W.C8_SHIFT)), seed=W.C8_HSEED)
+        v = rng.standard_normal((1, D))
+        K.sketched_hvp(c["kinds"][0], shapes, D, seed, hp, v)
+        nbytes = 2 * sum(r * cc for r, cc in shapes) * 4
+        sample = f"1 of {c['krylov']} Krylov steps: S H S^T v (AFJL transpose, rank-16 Hessian, AFJL), the " \
+                 "forward sketch as three fp32 parts of the fp64 HVP"
     else:  # c5
         first, cnt = W.llama3_8b_stream_groups()[1]
         sub = shapes[first:first + cnt]
@@ -305,6 +317,24 @@ def build_step(cfg: str, dev):
             ("FFD on one 1e8-entry vector (padded to 2^27), D=2^20, batch 4: theta0 + S^T z (z ~ N(0,1)) and "
              "S x for Student-t(3) x")
 
+    if cfg == "c8":
+        from paper_2402_03994_amd import arnoldi
+
+        H, _ = W.c8_hessian(dev)
+        k = c["krylov"]
+        v0 = torch.randn(D, generator=gen, device=dev)
+        Q = torch.empty((k + 1, D), device=dev)
+        Hb = torch.empty((k + 1, k), device=dev)
+        sks["hvp"] = H
+        sks["_result"] = Hb
+
+        def step(ev):
+            ev(c["kinds"][0], "arnoldi", lambda: arnoldi(sks[c["kinds"][0]], H, v0, k, Q=Q, Hbar=Hb))
+        return sks, step, k * 2 * sum(numels) * 4, k, \
+            (f"sketched Hessian eigenvalues: {k} Arnoldi steps (two Gram-Schmidt passes each) on v -> S H S^T v, "
+             f"S = {c['kinds'][0].upper()} over GPT-2-small parameters (N={sum(numels)}), D=2^16, H = 1e-5 I + "
+             f"rank-16 spike (Rademacher vectors, 14 positive and 2 negative outliers)")
+
     # c5
     xs = [W.gaussian((B, n), 1e-5, gen, dev, dtype=torch.bfloat16) for n in numels]
     out = torch.empty((B, D), device=dev)
@@ -341,11 +371,13 @@ def main() -> int:
               "batch or by layer groups with one all-reduce of [batch, D]; see DESIGN.md)", file=sys.stderr)
         return 2
 
+    import numpy as np
     import torch
 
     dev = torch.device("cuda", 0)
     cfg = args.config
     sks, step, pbytes, vecs, desc = build_step(cfg, dev)
+    result = sks.pop("_result", None)
     torch.cuda.synchronize()
 
     def ev_none(kind, tag, fn):
@@ -439,6 +471,14 @@ def main() -> int:
         "roofline": roofline,
         "source_hash": source_hash(),
     }
+    if cfg == "c8":
+        from paper_2402_03994_amd import ritz_values
+
+        ritz = np.sort(ritz_values(result).real)[::-1]
+        line["config"]["krylov"] = W.CONFIGS[cfg]["krylov"]
+        line["krylov_steps_per_s"] = line.pop("vectors_per_s")
+        line["ritz_top"] = [round(float(v), 4) for v in ritz[:6]] + [round(float(v), 4) for v in ritz[-2:]]
+        line["hessian_spikes"] = sorted(W.C8_LAMBDAS, reverse=True)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(line), flush=True)

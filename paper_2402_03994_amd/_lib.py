@@ -1,4 +1,5 @@
-"""ctypes declarations of the C ABI in include/sketch.h (argument marshalling only)."""
+"""ctypes declarations of the C ABI in include/sketch.h and include/sketch_hvp.h (argument
+marshalling only)."""
 from __future__ import annotations
 
 import ctypes
@@ -10,10 +11,15 @@ LIB_PATH = os.path.join(HERE, "libsketch.so")
 SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ, SK_AFFDQ = range(8)
 SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
-STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9}
+STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9,
+           "hvp": 10}
 EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", "sketch_query",
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
-           "sketch_status_string")
+           "sketch_status_string", "sk_hvp_create", "sk_hvp_apply", "sk_hvp_destroy", "sketch_hvp",
+           "sketch_arnoldi_work_floats", "sketch_arnoldi_step", "sketch_arnoldi", "sk_hvp_profile",
+           "sk_hvp_profile_read")
+HVP_PROF_CLASSES = ["hvp_dots", "hvp_combine", "arnoldi_orth"]
+HVP_MAX_RANK = 32
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
                 "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t"]
 
@@ -63,6 +69,25 @@ def load() -> ctypes.CDLL:
     L.sketch_last_error.restype = ctypes.c_char_p
     L.sketch_status_string.argtypes = [ctypes.c_int]
     L.sketch_status_string.restype = ctypes.c_char_p
+    f32 = ctypes.c_float
+    L.sk_hvp_create.argtypes = [ctypes.POINTER(LayerShape), i32, i32, P, f32, u64, i64, i32, ctypes.POINTER(P)]
+    L.sk_hvp_create.restype = ctypes.c_int
+    L.sk_hvp_apply.argtypes = [P, ctypes.POINTER(P), i64, ctypes.POINTER(P), P]
+    L.sk_hvp_apply.restype = ctypes.c_int
+    L.sk_hvp_destroy.argtypes = [P]
+    L.sk_hvp_destroy.restype = None
+    L.sketch_hvp.argtypes = [P, P, P, i64, P, P]
+    L.sketch_hvp.restype = ctypes.c_int
+    L.sketch_arnoldi_work_floats.argtypes = [i64, i32]
+    L.sketch_arnoldi_work_floats.restype = i64
+    L.sketch_arnoldi_step.argtypes = [P, i64, i32, P, i32, P, P]
+    L.sketch_arnoldi_step.restype = ctypes.c_int
+    L.sketch_arnoldi.argtypes = [P, P, P, i32, P, P, P]
+    L.sketch_arnoldi.restype = ctypes.c_int
+    L.sk_hvp_profile.argtypes = [P, u32]
+    L.sk_hvp_profile.restype = ctypes.c_int
+    L.sk_hvp_profile_read.argtypes = [P, P, P, P]
+    L.sk_hvp_profile_read.restype = ctypes.c_int
     _lib = L
     return L
 

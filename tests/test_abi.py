@@ -1,5 +1,5 @@
 """Host-side checks of the C ABI (no GPU needed): the library loads, exports
-every entry point declared in include/sketch.h, and rejects invalid arguments
+every entry point declared in include/*.h, and rejects invalid arguments
 before touching a device."""
 import ctypes
 import os
@@ -13,9 +13,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def declared_functions():
-    src = open(os.path.join(ROOT, "include", "sketch.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(sketch_[a-z_T]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", h)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b((?:sketch|sk_hvp)_[a-z_T]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_and_binding_agree():
@@ -77,3 +81,22 @@ def test_status_strings():
     L = _lib.load()
     for code in [0, -1, -2, -3, -4, -5]:
         assert L.sketch_status_string(code).decode() != "unknown status"
+
+
+def test_hvp_entry_points_reject_invalid_arguments():
+    L = _lib.load()
+    lam = (ctypes.c_float * 2)(1.0, 2.0)
+    h = ctypes.c_void_p(99)
+    assert L.sk_hvp_create(shapes((1, 10)), 1, 0, lam, 0.0, 0, 1, 0, ctypes.byref(h)) == -1   # rank 0
+    assert h.value is None
+    assert L.sk_hvp_create(shapes((1, 10)), 1, 33, lam, 0.0, 0, 1, 0, ctypes.byref(h)) == -1  # rank > 32
+    assert L.sk_hvp_create(shapes((1, 10)), 1, 2, None, 0.0, 0, 1, 0, ctypes.byref(h)) == -1  # no lambdas
+    assert L.sk_hvp_create(shapes((1, 10)), 1, 2, lam, 0.0, 0, 0, 0, ctypes.byref(h)) == -1   # max_batch 0
+    assert L.sk_hvp_create(shapes((0, 10)), 1, 2, lam, 0.0, 0, 1, 0, ctypes.byref(h)) == -1   # empty layer
+    assert L.sk_hvp_apply(None, None, 1, None, None) == -1
+    assert L.sketch_hvp(None, None, None, 1, None, None) == -1
+    assert L.sketch_arnoldi(None, None, None, 4, None, None, None) == -1
+    assert L.sketch_arnoldi_step(None, 16, 0, None, 4, None, None) == -1
+    assert L.sketch_arnoldi_work_floats(0, 4) == 0
+    assert L.sketch_arnoldi_work_floats(4096, 10) == 2 * 12 + 12 + 4
+    L.sk_hvp_destroy(None)  # no-op

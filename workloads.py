@@ -72,8 +72,15 @@ CONFIGS = {
     "c6": dict(kinds=("afjlq", "qkh"), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
     # AFFD with Q (dense: ~4.3 GFLOP per vector and 2^20-element slab each way) on C1's vectors
     "c7": dict(kinds=("affdq",), shapes=[(1, 1 << 20)], D=4096, batch=8, seed=0, dtype="f32"),
+    # sketched Hessian eigenvalues: Arnoldi (64 steps) on v -> S H S^T v, GPT-2-small parameters, a
+    # synthetic rank-16 spiked Hessian (c8_hessian), AFJL sketch to D = 2^16
+    "c8": dict(kinds=("afjl",), shapes=gpt2_small_shapes(), D=1 << 16, batch=1, seed=1, dtype="f32", krylov=64),
 }
-INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001}
+# the synthetic Hessian of c8: 14 positive outliers, 2 negative ones, a flat bulk of 1e-5
+C8_LAMBDAS = (20.0, 15.0, 11.0, 8.5, 6.5, 5.0, 4.0, 3.0, 2.5, 2.0, 1.6, 1.3, 1.1, 1.0, -3.0, -1.5)
+C8_SHIFT = 1e-5
+C8_HSEED = 4242
+INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001, "c8": 1008}
 # variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
 GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4, "c7": 1.0}
 
@@ -110,3 +117,14 @@ def bf16_bits(x):
 
 def generator(cfg: str, device) -> torch.Generator:
     return torch.Generator(device=device).manual_seed(INPUT_SEED[cfg])
+
+
+def c8_hessian(device):
+    """The synthetic Hessian of c8 on `device` and its parameters as the oracle takes them."""
+    import numpy as np
+
+    from paper_2402_03994_amd import SyntheticHessian
+
+    lam = np.array(C8_LAMBDAS, dtype=np.float32)
+    H = SyntheticHessian(CONFIGS["c8"]["shapes"], len(lam), lam, C8_SHIFT, C8_HSEED, max_batch=1, device=device)
+    return H, dict(rank=len(lam), lambdas=lam, shift=float(np.float32(C8_SHIFT)), seed=C8_HSEED)
