@@ -835,19 +835,38 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
   int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
   if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
   const int lgD = ilog2(s->D);
+  const int osz = out_dtype == SK_BF16 ? 2 : 4;
   for (int64_t b0 = 0; b0 < batch; b0 += bcmax) {
     const int64_t bc = std::min(bcmax, batch - b0);
+    if (s->kind == SK_AFJL) {
+      // layer groups: as many layers per launch as the workspace holds (bc * D floats each)
+      const int gmax = (int)std::max<int64_t>(1, std::min<int64_t>(kMaxPtrs, s->ws_bytes / (bc * s->D * 4)));
+      for (int la = l0; la < l1; la += gmax) {
+        const int ng = std::min(gmax, l1 - la);
+        AfjlTGroup g{};
+        int64_t obytes = 0;
+        g.row0[0] = 0;
+        for (int i = 0; i < ng; ++i) {
+          const LayerDesc &ld = s->layers[la + i];
+          g.layer[i] = la + i;
+          g.out[i] = out[la + i - l0];
+          g.th[i] = theta0 ? (const float *)theta0[la + i - l0] : nullptr;
+          g.row0[i + 1] = g.row0[i] + ld.rows_live;
+          obytes += bc * ld.n * osz + (g.th[i] ? ld.n * 4 : 0);
+        }
+        SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_afjl_T_prep(s, la, ng, z, b0, bc, s->ws, st));
+        SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, (int64_t)ng * bc, lgD, st));
+        SK_PROF(SK_PROF_GATHER, obytes, launch_afjl_T_out(s, g, ng, s->ws, b0, bc, out_dtype, st));
+      }
+      continue;
+    }
     for (int l = l0; l < l1; ++l) {
       const LayerDesc &ld = s->layers[l];
       void *o = out[l - l0];
       const float *th = theta0 ? (const float *)theta0[l - l0] : nullptr;
-      const int osz = out_dtype == SK_BF16 ? 2 : 4;
       const int64_t obytes = bc * ld.n * osz + (th ? ld.n * 4 : 0);  // output written, theta0 read
       switch (s->kind) {
-        case SK_AFJL:
-          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_afjl_T_prep(s, l, z, b0, bc, s->ws, st));
-          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, lgD, st));
-          SK_PROF(SK_PROF_GATHER, obytes, launch_afjl_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st));
+        case SK_AFJL:  // grouped above
           break;
         case SK_AFFD:
           SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, {

@@ -599,29 +599,41 @@ void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin
 
 // AFJL transpose.  H_N' R_D^T u = sqrt(D/N') tile(H_D u), so
 // AFJL^T z = B Gather_pi1 tile(H_D (g . z)): out[j] = b_j V[pi1(j) mod D].
-__global__ void k_afjl_T_prep(const float *__restrict__ gtab, int layer, const float *__restrict__ z, int64_t D,
+// The layers of a call go through in groups: one launch forms g_l . z for
+// every layer and vector of the group, one set of transform passes covers all
+// of them, and one launch writes every output row of the group (a vector
+// with one layer per launch would be launch-bound for small batches: three
+// launches per tensor).
+__global__ void k_afjl_T_prep(const float *__restrict__ gtab, int l_first, const float *__restrict__ z, int64_t D,
                               int64_t b_begin, int64_t bc, float *__restrict__ w) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= D) return;
-  const float g = gtab[(int64_t)layer * D + i];
-  for (int64_t v = 0; v < bc; ++v) w[v * D + i] = g * z[(b_begin + v) * D + i];
+  const int gl = blockIdx.y;
+  const float g = gtab[(int64_t)(l_first + gl) * D + i];
+  float *wl = w + (int64_t)gl * bc * D;
+  for (int64_t v = 0; v < bc; ++v) wl[v * D + i] = g * z[(b_begin + v) * D + i];
 }
 
-void launch_afjl_T_prep(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
-                        hipStream_t st) {
-  hipLaunchKernelGGL(k_afjl_T_prep, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_gtab, layer, z,
-                     s->D, b_begin, bc, w);
+void launch_afjl_T_prep(const sk_sketch *s, int l_first, int ng, const float *z, int64_t b_begin, int64_t bc,
+                        float *w, hipStream_t st) {
+  hipLaunchKernelGGL(k_afjl_T_prep, dim3((unsigned)((s->D + 255) / 256), (unsigned)ng), dim3(256), 0, st, s->d_gtab,
+                     l_first, z, s->D, b_begin, bc, w);
   SK_CHECK_LAUNCH();
 }
 
-// One workgroup per source row h of the layer; each thread owns 4 columns.
+// One workgroup per source row h of a layer of the group (rows of the group's
+// layers numbered consecutively); each thread owns 4 columns.
 __global__ __launch_bounds__(256) void k_afjl_T_out(const LayerDesc *__restrict__ layers,
-                                                    const uint16_t *__restrict__ ptab, int layer,
+                                                    const uint16_t *__restrict__ ptab, AfjlTGroup g, int ng,
                                                     const float *__restrict__ w, int64_t D, int R, int Lw,
-                                                    int64_t bc, int64_t b_begin, void *__restrict__ out,
-                                                    int out_dtype, const float *__restrict__ theta0, Key key) {
-  const LayerDesc &ld = layers[layer];
-  const int64_t h = blockIdx.x;
+                                                    int64_t bc, int64_t b_begin, int out_dtype, Key key) {
+  int gl = 0;
+  while (gl + 1 < ng && (int64_t)blockIdx.x >= g.row0[gl + 1]) ++gl;
+  const LayerDesc &ld = layers[g.layer[gl]];
+  void *__restrict__ out = g.out[gl];
+  const float *__restrict__ theta0 = g.th[gl];
+  const float *wl = w + (int64_t)gl * bc * D;
+  const int64_t h = (int64_t)blockIdx.x - g.row0[gl];
   const int L = ld.L;
   const int col0 = threadIdx.x * 4;
   if (col0 >= L) return;
@@ -645,7 +657,7 @@ __global__ __launch_bounds__(256) void k_afjl_T_out(const LayerDesc *__restrict_
       if (q < lim) th[q] = theta0[j0 + q];
   }
   for (int64_t v = 0; v < bc; ++v) {
-    const float *wv = w + v * D;
+    const float *wv = wl + v * D;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (q < lim) store_out(out, out_dtype, (b_begin + v) * ld.n + j0 + q, flip(wv[idx[q]], (bits >> q) & 1u) + th[q]);
@@ -653,11 +665,10 @@ __global__ __launch_bounds__(256) void k_afjl_T_out(const LayerDesc *__restrict_
   }
 }
 
-void launch_afjl_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
-                       int out_dtype, const float *theta0, hipStream_t st) {
-  const LayerDesc &ld = s->layers[layer];
-  hipLaunchKernelGGL(k_afjl_T_out, dim3((unsigned)ld.rows_live), dim3(256), 0, st, s->d_layers, s->d_ptab, layer, w,
-                     s->D, s->R, s->Lw, bc, b_begin, out, out_dtype, theta0, s->key);
+void launch_afjl_T_out(const sk_sketch *s, const AfjlTGroup &g, int ng, const float *w, int64_t b_begin, int64_t bc,
+                       int out_dtype, hipStream_t st) {
+  hipLaunchKernelGGL(k_afjl_T_out, dim3((unsigned)g.row0[ng]), dim3(256), 0, st, s->d_layers, s->d_ptab, g, ng, w,
+                     s->D, s->R, s->Lw, bc, b_begin, out_dtype, s->key);
   SK_CHECK_LAUNCH();
 }
 

@@ -47,10 +47,19 @@ void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, 
                       int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st);
 void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin, const float *part, int64_t bc,
                       int64_t b_begin, int64_t batch, float *out, bool accumulate, hipStream_t st);
-void launch_afjl_T_prep(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
-                        hipStream_t st);
-void launch_afjl_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
-                       int out_dtype, const float *theta0, hipStream_t st);
+// AFJL transpose over a group of up to kMaxPtrs consecutive layers: g_l . z
+// for all of them into w ([layer][vector][D]), then (after the transform of
+// all ng * bc vectors) every output row of the group in one launch.
+struct AfjlTGroup {
+  int32_t layer[kMaxPtrs];
+  int64_t row0[kMaxPtrs + 1];  // first output row of each layer in the launch grid (+ total)
+  void *out[kMaxPtrs];
+  const float *th[kMaxPtrs];
+};
+void launch_afjl_T_prep(const sk_sketch *s, int l_first, int ng, const float *z, int64_t b_begin, int64_t bc,
+                        float *w, hipStream_t st);
+void launch_afjl_T_out(const sk_sketch *s, const AfjlTGroup &g, int ng, const float *w, int64_t b_begin, int64_t bc,
+                       int out_dtype, hipStream_t st);
 
 // ---- AFFD ----
 // AFFD specialised for D > 1024, last digit 1024 and at most 64 top-digit values.

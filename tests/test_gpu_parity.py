@@ -259,3 +259,26 @@ def test_qk_parity(shapes, D, dev):
     refs = O.apply_T("qk", shapes, D, seed, z.numpy().astype(np.float64))
     for o, r in zip(outs, refs):
         assert rel_err(o.cpu().numpy(), r) < 1e-4
+
+
+@pytest.mark.parametrize("ws_mb", [None, 16])
+def test_afjl_transpose_layer_groups(ws_mb, dev, monkeypatch):
+    """AFJL transposes run in groups of layers per launch (at most 64, fewer when the workspace holds fewer
+    D-vectors per batch): 71 layers, a call over a sub-range, theta0 on some layers, and a 16 MB workspace
+    that forces groups of 21 layers at D = 2^16, batch 3."""
+    from paper_2402_03994_amd import Sketch
+    if ws_mb is not None:
+        monkeypatch.setenv("SK_WORKSPACE_MB", str(ws_mb))
+    shapes = [(1, 37 + 11 * i) for i in range(70)] + [(3, 5000)]
+    D, seed, f, cnt = (1 << 16, 31, 0, 71) if ws_mb else (1024, 30, 5, 66)
+    s = Sketch("afjl", shapes, D, seed, device=dev)
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((3, D), generator=g)
+    th = [torch.randn(r * c, generator=g) * 0.02 if i % 3 == 0 else None for i, (r, c) in enumerate(shapes)]
+    sub = th[f:f + cnt]
+    outs = s.apply_T(z.to(dev), theta0=[None if t is None else t.to(dev) for t in sub], first_layer=f, n_layers=cnt)
+    refs = O.apply_T("afjl", shapes[f:f + cnt], D, seed, z.numpy().astype(np.float64), layer0=f,
+                     theta0=[None if t is None else t.numpy() for t in sub])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL_F32
+    s.close()
