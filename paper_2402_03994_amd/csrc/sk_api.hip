@@ -845,13 +845,13 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
         const int ng = std::min(gmax, l1 - la);
         AfjlTGroup g{};
         int64_t obytes = 0;
-        g.row0[0] = 0;
+        g.tile0[0] = 0;
         for (int i = 0; i < ng; ++i) {
           const LayerDesc &ld = s->layers[la + i];
           g.layer[i] = la + i;
           g.out[i] = out[la + i - l0];
           g.th[i] = theta0 ? (const float *)theta0[la + i - l0] : nullptr;
-          g.row0[i + 1] = g.row0[i] + ld.rows_live;
+          g.tile0[i + 1] = g.tile0[i] + (ld.rows_live + kAfjlTRows - 1) / kAfjlTRows;
           obytes += bc * ld.n * osz + (g.th[i] ? ld.n * 4 : 0);
         }
         SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_afjl_T_prep(s, la, ng, z, b0, bc, s->ws, st));

@@ -295,12 +295,129 @@ __global__ __launch_bounds__(256) void k_afjl_fold(const FoldItem *__restrict__ 
   }
 }
 
+// Fold kernel for a single vector (batch tiles of one row) of layers with
+// L = Lw = 1024.  With one vector the per-thread sign block of the tiled
+// kernel is not shared by any other vector, so here the item's sign words are
+// built first, one Philox block per 128 coordinates (8 per source row) into
+// LDS, and each row group keeps PF rows of 16-byte loads in flight (one
+// vector gives a workgroup too little work to hide the latency otherwise).
+template <int CPT, bool BF16, bool VEC>
+__global__ __launch_bounds__(256) void k_afjl_fold1(const FoldItem *__restrict__ items,
+                                                    const LayerDesc *__restrict__ layers,
+                                                    const uint16_t *__restrict__ ptab, PtrPack ptrs, int first_layer,
+                                                    int64_t b_row, int64_t bc, int64_t slot_row, int item_begin, int R,
+                                                    float *__restrict__ part, Key key) {
+  constexpr int PF = 4;
+  constexpr int TPR = 1024 / CPT;  // threads per row
+  constexpr int NGR = 256 / TPR;   // row groups
+  __shared__ float s[1024];
+  __shared__ int32_t srow[kFoldRowsPerItem];
+  __shared__ __align__(16) uint32_t sgn[kFoldRowsPerItem * 32];
+  const FoldItem it = items[item_begin + blockIdx.x];
+  const LayerDesc &ld = layers[it.layer];
+  const int64_t n = ld.n;
+  const int tid = threadIdx.x;
+  const int grp = tid / TPR;
+  const int col0 = (tid - grp * TPR) * CPT;
+  const void *xp = ptrs.p[it.layer - first_layer];
+  const int nt = it.t1 - it.t0;  // <= kFoldRowsPerItem
+  {
+    const int nk = R > 1 ? ld.dk1 / R : 1;
+    const uint16_t *inv_k1 = ptab + ld.poff[0][1][ld.K >= 2 ? ld.K - 2 : 0];
+    if (tid < nt) {
+      const int t = it.t0 + tid;
+      int64_t h;
+      if (R == 1) {
+        h = t;
+      } else {
+        const int htop = t / nk;
+        const int k = t - htop * nk;
+        h = (int64_t)htop * ld.dk1 + inv_k1[it.r + k * R];
+      }
+      srow[tid] = h < ld.rows_live ? (int32_t)h : -1;
+    }
+    __syncthreads();
+  }
+  // sign words of the item's rows: 8 Philox blocks of 128 coordinates per row
+  for (int u = tid; u < nt * 8; u += 256) {
+    const int32_t h = srow[u >> 3];
+    if (h >= 0) {
+      const W4 w = philox((uint64_t)h * 8u + (uint64_t)(u & 7), (uint32_t)ld.layer_id, ST_SIGN, key);
+      *reinterpret_cast<uint4 *>(&sgn[4 * u]) = make_uint4(w.w[0], w.w[1], w.w[2], w.w[3]);
+    }
+  }
+  __syncthreads();
+  float acc[CPT];
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) acc[q] = 0.0f;
+  const int64_t xrow = b_row * n;
+  uint4 ring[PF];
+  int64_t jr[PF];
+  auto fetch = [&](int i, uint4 &v, int64_t &jn) {
+    const int32_t h = i < nt ? srow[i] : -1;
+    jn = h >= 0 ? (int64_t)h * 1024 + col0 : -1;
+    if (jn >= n) jn = -1;
+    v = make_uint4(0u, 0u, 0u, 0u);
+    if (jn >= 0) v = load_raw16<CPT, BF16, VEC>(xp, xrow + jn, n - jn);
+  };
+#pragma unroll
+  for (int p = 0; p < PF; ++p) fetch(grp + p * NGR, ring[p], jr[p]);
+  for (int i0 = grp; i0 < nt; i0 += PF * NGR) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int i = i0 + p * NGR;
+      const uint4 cur = ring[p];
+      const int64_t j = jr[p];
+      fetch(i + PF * NGR, ring[p], jr[p]);
+      if (j >= 0) {
+        const uint32_t bits = sgn[i * 32 + (col0 >> 5)] >> (col0 & 31);
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) acc[q] += flip(raw16_value<BF16>(cur, q), (bits >> q) & 1u);
+      }
+    }
+  }
+  // route the columns through pi1 of the last digit; row groups add in order
+  const uint16_t *fwd_k = ptab + ld.poff[0][0][ld.K - 1];
+  int pc[CPT];
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) pc[q] = fwd_k[col0 + q];
+  for (int gi = 0; gi < NGR; ++gi) {
+    if (grp == gi) {
+#pragma unroll
+      for (int q = 0; q < CPT; ++q) s[pc[q]] = gi == 0 ? acc[q] : s[pc[q]] + acc[q];
+    }
+    __syncthreads();
+  }
+  lds_fwht(s, 10, 0);
+  const int64_t slot = blockIdx.x;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = tid + 256 * k;
+    part[(slot * bc + slot_row) * 1024 + c] = s[c] * (1.0f / 32.0f);
+  }
+}
+
 void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,
                       int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st) {
   constexpr int BT = 8;
   const int nitems = item_end - item_begin;
   if (nitems <= 0) return;
   const int64_t rows = (batch - b_begin) < bc ? (batch - b_begin) : bc;
+  bool one = rows == 1 && s->Lw == 1024;
+  for (int i = item_begin; i < item_end && one; ++i) one = s->layers[s->items[i].layer].L == 1024;
+  if (one) {
+#define SK_FOLD1(CPT, BF, VE)                                                                                        \
+  hipLaunchKernelGGL((k_afjl_fold1<CPT, BF, VE>), dim3((unsigned)nitems), dim3(256), 0, st, s->d_items, s->d_layers, \
+                     s->d_ptab, ptrs, first_layer, b_begin, bc, (int64_t)0, item_begin, s->R, part, s->key)
+    if (dtype == SK_BF16) {
+      if (vec) SK_FOLD1(8, true, true); else SK_FOLD1(4, true, false);
+    } else {
+      if (vec) SK_FOLD1(4, false, true); else SK_FOLD1(4, false, false);
+    }
+#undef SK_FOLD1
+    SK_CHECK_LAUNCH();
+    return;
+  }
   dim3 grid((unsigned)nitems, (unsigned)((rows + BT - 1) / BT));
 #define SK_FOLD(CPT, BF, VE)                                                                                       \
   hipLaunchKernelGGL((k_afjl_fold<BT, CPT, BF, VE>), grid, dim3(256), 0, st, s->d_items, s->d_layers, s->d_ptab,   \
@@ -621,53 +738,73 @@ void launch_afjl_T_prep(const sk_sketch *s, int l_first, int ng, const float *z,
   SK_CHECK_LAUNCH();
 }
 
-// One workgroup per source row h of a layer of the group (rows of the group's
-// layers numbered consecutively); each thread owns 4 columns.
+// One workgroup per tile of kAfjlTRows source rows of a layer of the group
+// (tiles of the group's layers numbered consecutively).  The tile's sign words
+// come from one Philox block per 128 coordinates, each computed by one thread
+// into LDS (a thread per 4 coordinates would repeat every block 32 times);
+// each thread then writes 4 consecutive coordinates per 1024-coordinate step,
+// gathering V through the digit permutation, with 16-byte stores where the
+// output row allows them.
 __global__ __launch_bounds__(256) void k_afjl_T_out(const LayerDesc *__restrict__ layers,
                                                     const uint16_t *__restrict__ ptab, AfjlTGroup g, int ng,
                                                     const float *__restrict__ w, int64_t D, int R, int Lw,
                                                     int64_t bc, int64_t b_begin, int out_dtype, Key key) {
+  __shared__ uint32_t sgn[kAfjlTRows * 1024 / 32];
   int gl = 0;
-  while (gl + 1 < ng && (int64_t)blockIdx.x >= g.row0[gl + 1]) ++gl;
+  while (gl + 1 < ng && (int64_t)blockIdx.x >= g.tile0[gl + 1]) ++gl;
   const LayerDesc &ld = layers[g.layer[gl]];
   void *__restrict__ out = g.out[gl];
   const float *__restrict__ theta0 = g.th[gl];
   const float *wl = w + (int64_t)gl * bc * D;
-  const int64_t h = (int64_t)blockIdx.x - g.row0[gl];
-  const int L = ld.L;
-  const int col0 = threadIdx.x * 4;
-  if (col0 >= L) return;
-  const int64_t j0 = h * L + col0;
-  const int64_t lim = ld.n - j0;
-  if (lim <= 0) return;
-  int rbase = 0;
-  if (R > 1) {
-    const uint16_t *fk1 = ptab + ld.poff[0][0][ld.K - 2];
-    rbase = ((int)fk1[h & (ld.dk1 - 1)] & (R - 1)) * L;
+  const int L = ld.L, lgL = ld.lgL;
+  const int64_t h0 = ((int64_t)blockIdx.x - g.tile0[gl]) * kAfjlTRows;
+  const int64_t e0 = h0 * L;  // a multiple of 512 (L >= 16)
+  const int64_t tile_n = ld.n - e0 < (int64_t)kAfjlTRows * L ? ld.n - e0 : (int64_t)kAfjlTRows * L;
+  const int t = threadIdx.x;
+  if ((int64_t)t * 128 < tile_n) {
+    const W4 wd = philox(((uint64_t)e0 >> 7) + (uint64_t)t, (uint32_t)ld.layer_id, ST_SIGN, key);
+    *reinterpret_cast<uint4 *>(&sgn[4 * t]) = make_uint4(wd.w[0], wd.w[1], wd.w[2], wd.w[3]);
   }
+  __syncthreads();
   const uint16_t *fk = ptab + ld.poff[0][0][ld.K - 1];
-  int idx[4];
+  const uint16_t *fk1 = R > 1 ? ptab + ld.poff[0][0][ld.K - 2] : nullptr;
+  const bool out16 = out_dtype == SK_F32 && (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
+  for (int64_t e = 4 * t; e < tile_n; e += 1024) {
+    const int64_t h = h0 + (e >> lgL);
+    const int c = (int)(e & (L - 1));
+    const int rbase = R > 1 ? ((int)fk1[h & (ld.dk1 - 1)] & (R - 1)) * L : 0;
+    int idx[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) idx[q] = R > 1 ? rbase + fk[col0 + q] : (fk[col0 + q] & (Lw - 1));
-  const uint32_t bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
-  float th[4] = {0.f, 0.f, 0.f, 0.f};
-  if (theta0) {
+    for (int q = 0; q < 4; ++q) idx[q] = R > 1 ? rbase + fk[c + q] : (fk[c + q] & (Lw - 1));
+    const uint32_t bits = sgn[e >> 5] >> (e & 31);
+    const int64_t j = e0 + e;
+    const int64_t lim = tile_n - e;
+    float th[4] = {0.f, 0.f, 0.f, 0.f};
+    if (theta0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (q < lim) th[q] = theta0[j0 + q];
-  }
-  for (int64_t v = 0; v < bc; ++v) {
-    const float *wv = wl + v * D;
+      for (int q = 0; q < 4; ++q)
+        if (q < lim) th[q] = theta0[j + q];
+    }
+    for (int64_t v = 0; v < bc; ++v) {
+      const float *wv = wl + v * D;
+      float o[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < lim) store_out(out, out_dtype, (b_begin + v) * ld.n + j0 + q, flip(wv[idx[q]], (bits >> q) & 1u) + th[q]);
+      for (int q = 0; q < 4; ++q) o[q] = flip(wv[idx[q]], (bits >> q) & 1u) + th[q];
+      const int64_t pos = (b_begin + v) * ld.n + j;
+      if (out16 && lim >= 4 && (pos & 3) == 0) {
+        *reinterpret_cast<float4 *>((float *)out + pos) = make_float4(o[0], o[1], o[2], o[3]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (q < lim) store_out(out, out_dtype, pos + q, o[q]);
+      }
     }
   }
 }
 
 void launch_afjl_T_out(const sk_sketch *s, const AfjlTGroup &g, int ng, const float *w, int64_t b_begin, int64_t bc,
                        int out_dtype, hipStream_t st) {
-  hipLaunchKernelGGL(k_afjl_T_out, dim3((unsigned)g.row0[ng]), dim3(256), 0, st, s->d_layers, s->d_ptab, g, ng, w,
+  hipLaunchKernelGGL(k_afjl_T_out, dim3((unsigned)g.tile0[ng]), dim3(256), 0, st, s->d_layers, s->d_ptab, g, ng, w,
                      s->D, s->R, s->Lw, bc, b_begin, out_dtype, s->key);
   SK_CHECK_LAUNCH();
 }

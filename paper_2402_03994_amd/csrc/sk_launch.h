@@ -50,9 +50,10 @@ void launch_afjl_tail(const sk_sketch *s, int l_begin, int l_end, int item_begin
 // AFJL transpose over a group of up to kMaxPtrs consecutive layers: g_l . z
 // for all of them into w ([layer][vector][D]), then (after the transform of
 // all ng * bc vectors) every output row of the group in one launch.
+constexpr int kAfjlTRows = 32;  // source rows per workgroup of the AFJL transpose output kernel
 struct AfjlTGroup {
   int32_t layer[kMaxPtrs];
-  int64_t row0[kMaxPtrs + 1];  // first output row of each layer in the launch grid (+ total)
+  int64_t tile0[kMaxPtrs + 1];  // first tile of kAfjlTRows rows of each layer in the launch grid (+ total)
   void *out[kMaxPtrs];
   const float *th[kMaxPtrs];
 };

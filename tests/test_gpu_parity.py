@@ -282,3 +282,19 @@ def test_afjl_transpose_layer_groups(ws_mb, dev, monkeypatch):
     for o, r in zip(outs, refs):
         assert rel_err(o.cpu().numpy(), r) < TOL_F32
     s.close()
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_afjl_single_vector(dtype, aligned, dev):
+    """One vector (the single-vector fold kernel: shared sign blocks, deeper prefetch): 16-byte and scalar
+    loads, fp32 and bf16, ragged rows, a layer of 1025 source rows (several fold items), D = 4096."""
+    from paper_2402_03994_amd import Sketch
+    shapes = [(1, 3000), (64, 1024), (1025, 1024)] if aligned else [(1, 3001), (7, 1001), (1, 2 ** 20 + 3)]
+    D, seed = 4096, 77
+    xs = rand_inputs(shapes, 1, seed, dtype=dtype, scale=0.01)
+    s = Sketch("afjl", shapes, D, seed, device=dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("afjl", shapes, D, seed, [oracle_in(x)[0] for x in xs], dtype=oracle_in(xs[0])[1])
+    assert rel_err(y, ref) < TOL_F32
+    s.close()
