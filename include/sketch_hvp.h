@@ -68,7 +68,10 @@ int sk_hvp_create(const sk_layer_shape *shapes, int32_t n_layers, int32_t rank, 
 /*
  * y = H x for a batch of parameter vectors given per layer: x[i] and y[i]
  * (host arrays of n_layers device pointers) hold layer i as [batch, rows*cols]
- * fp32 row-major.  y may not alias x.  Two passes: the r inner products
+ * fp32 row-major.  y may not alias x.  The pointers reach the kernels as a
+ * small table copied to the device on `stream` (from pinned memory the
+ * handle owns; a call waits for the previous call's copy before refilling
+ * it).  Two passes, one launch each over all layers: the r inner products
  * s_j . x (fp32 per 8192-element chunk, chunks summed in fp64 in a fixed
  * order), then y = shift x + sum_j (lambda_j / N_tot)(s_j . x) s_j.
  * 1 <= batch <= max_batch.

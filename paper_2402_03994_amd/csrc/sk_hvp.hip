@@ -43,10 +43,12 @@ struct HvpItem {
   int64_t e0;     // first coordinate (a multiple of kChunk)
 };
 
-struct HvpPtrs {
-  const float *x[kMaxPtrs];
-  float *y[kMaxPtrs];
-  int64_t n[kMaxPtrs];
+// Per-layer input and output of one H x pass (a device table, so that one
+// launch covers every layer).
+struct HvpLayerPtr {
+  const float *x;
+  float *y;
+  int64_t n;
 };
 
 int fail(int code, const std::string &msg) {
@@ -79,18 +81,20 @@ struct sk_hvp {
   std::vector<int64_t> n, off;     // per layer: elements, offset in the concatenation
   std::vector<float> lambdas;
   std::vector<HvpItem> items;
-  std::vector<int32_t> layer_item0;  // first item of each layer (+ sentinel)
   HvpItem *d_items = nullptr;
   float *d_lambda = nullptr;
   float *d_part = nullptr;   // [items][batch][r] per-chunk inner products
   float *d_coef = nullptr;   // [batch][r]
   float *X = nullptr, *Y = nullptr;  // sketch_hvp workspace, ws_floats each (>= max_batch * N_tot)
   int64_t ws_floats = 0;
-  // per-layer pointers into X and Y, typed for the HVP passes and for the sketch entry points
-  std::vector<const float *> xin;
-  std::vector<float *> yout;
+  // per-layer pointers into X and Y for the sketch entry points, and the device tables of the
+  // H x passes: X -> Y (filled at creation) and the caller's buffers of sk_hvp_apply (uploaded per
+  // call from pinned host memory; the upload's event guards the host copy's reuse)
   std::vector<void *> xsk;
   std::vector<const void *> ysk;
+  HvpLayerPtr *d_ws_tab = nullptr, *d_user_tab = nullptr, *h_user_tab = nullptr;
+  hipEvent_t user_ev = nullptr;
+  bool user_ev_pending = false;
   // kernel timing
   struct Rec {
     int cls, ev;
@@ -158,20 +162,20 @@ __device__ __forceinline__ void load4(const float *row, int64_t p, int len_left,
 }
 
 template <int RB>
-__global__ __launch_bounds__(256) void k_hvp_dots(const HvpItem *__restrict__ items, HvpPtrs ptrs, int item0,
-                                                  int layer_base, int r, int64_t batch, Key key,
+__global__ __launch_bounds__(256) void k_hvp_dots(const HvpItem *__restrict__ items,
+                                                  const HvpLayerPtr *__restrict__ tab, int r, int64_t batch, Key key,
                                                   float *__restrict__ part) {
   __shared__ __align__(16) uint32_t sw[kBlocksPerChunk * RB * 4];
   __shared__ float red[4][RB];
-  const HvpItem it = items[item0 + blockIdx.x];
+  const HvpItem it = items[blockIdx.x];
   build_sign_table(sw, it, r, key);
   __syncthreads();
-  const int li = it.layer - layer_base;
-  const int64_t n = ptrs.n[li];
+  const HvpLayerPtr lp = tab[it.layer];
+  const int64_t n = lp.n;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int q = (t >> 3) & 3, sh = (t & 7) * 4;
   for (int64_t b = 0; b < batch; ++b) {
-    const float *row = ptrs.x[li] + b * n + it.e0;
+    const float *row = lp.x + b * n + it.e0;
     const bool vec = ((reinterpret_cast<uintptr_t>(row) & 15u) == 0);
     float acc[RB];
 #pragma unroll
@@ -226,20 +230,20 @@ __global__ __launch_bounds__(256) void k_hvp_coef(const float *__restrict__ part
 }
 
 template <int RB>
-__global__ __launch_bounds__(256) void k_hvp_combine(const HvpItem *__restrict__ items, HvpPtrs ptrs, int item0,
-                                                     int layer_base, int r, int64_t batch, Key key, float shift,
-                                                     const float *__restrict__ coef) {
+__global__ __launch_bounds__(256) void k_hvp_combine(const HvpItem *__restrict__ items,
+                                                     const HvpLayerPtr *__restrict__ tab, int r, int64_t batch,
+                                                     Key key, float shift, const float *__restrict__ coef) {
   __shared__ __align__(16) uint32_t sw[kBlocksPerChunk * RB * 4];
-  const HvpItem it = items[item0 + blockIdx.x];
+  const HvpItem it = items[blockIdx.x];
   build_sign_table(sw, it, r, key);
   __syncthreads();
-  const int li = it.layer - layer_base;
-  const int64_t n = ptrs.n[li];
+  const HvpLayerPtr lp = tab[it.layer];
+  const int64_t n = lp.n;
   const int t = threadIdx.x;
   const int q = (t >> 3) & 3, sh = (t & 7) * 4;
   for (int64_t b = 0; b < batch; ++b) {
-    const float *row = ptrs.x[li] + b * n + it.e0;
-    float *yrow = ptrs.y[li] + b * n + it.e0;
+    const float *row = lp.x + b * n + it.e0;
+    float *yrow = lp.y + b * n + it.e0;
     const bool vec = ((reinterpret_cast<uintptr_t>(row) & 15u) == 0) && ((reinterpret_cast<uintptr_t>(yrow) & 15u) == 0);
     float c[RB];
 #pragma unroll
@@ -398,39 +402,27 @@ void arnoldi_step(float *Q, int64_t D, int j, float *Hbar, int k, float *work, h
 }
 
 template <int RB>
-void launch_hvp(sk_hvp *h, const HvpPtrs &p, int item0, int nitems, int layer_base, int64_t batch, int pass,
-                hipStream_t st) {
+void launch_hvp(sk_hvp *h, const HvpLayerPtr *tab, int64_t batch, int pass, hipStream_t st) {
+  const unsigned nitems = (unsigned)h->items.size();
   if (pass == 0)
-    hipLaunchKernelGGL(k_hvp_dots<RB>, dim3((unsigned)nitems), dim3(256), 0, st, h->d_items, p, item0, layer_base,
-                       h->rank, batch, h->key, h->d_part + (int64_t)item0 * batch * h->rank);
+    hipLaunchKernelGGL(k_hvp_dots<RB>, dim3(nitems), dim3(256), 0, st, h->d_items, tab, h->rank, batch, h->key,
+                       h->d_part);
   else
-    hipLaunchKernelGGL(k_hvp_combine<RB>, dim3((unsigned)nitems), dim3(256), 0, st, h->d_items, p, item0,
-                       layer_base, h->rank, batch, h->key, h->shift, h->d_coef);
+    hipLaunchKernelGGL(k_hvp_combine<RB>, dim3(nitems), dim3(256), 0, st, h->d_items, tab, h->rank, batch, h->key,
+                       h->shift, h->d_coef);
 }
 
-// Queues H x -> y for `batch` vectors (validated).
-void hvp_run(sk_hvp *h, const float *const *x, int64_t batch, float *const *y, hipStream_t st) {
-  const int nl = (int)h->n.size();
+// Queues H x -> y for `batch` vectors (validated); tab: the device table of the layers' x, y, n.
+void hvp_run(sk_hvp *h, const HvpLayerPtr *tab, int64_t batch, hipStream_t st) {
   const int64_t bytes = batch * h->total * 4;
   for (int pass = 0; pass < 2; ++pass) {
     HvpProf ps(h, pass, pass == 0 ? bytes : 2 * bytes, st);
-    for (int l0 = 0; l0 < nl; l0 += kMaxPtrs) {
-      const int l1 = std::min(nl, l0 + kMaxPtrs);
-      HvpPtrs p{};
-      for (int l = l0; l < l1; ++l) {
-        p.x[l - l0] = x[l];
-        p.y[l - l0] = y[l];
-        p.n[l - l0] = h->n[l];
-      }
-      const int item0 = h->layer_item0[l0], nitems = h->layer_item0[l1] - item0;
-      if (nitems == 0) continue;
-      if (h->rank <= 8)
-        launch_hvp<8>(h, p, item0, nitems, l0, batch, pass, st);
-      else if (h->rank <= 16)
-        launch_hvp<16>(h, p, item0, nitems, l0, batch, pass, st);
-      else
-        launch_hvp<32>(h, p, item0, nitems, l0, batch, pass, st);
-    }
+    if (h->rank <= 8)
+      launch_hvp<8>(h, tab, batch, pass, st);
+    else if (h->rank <= 16)
+      launch_hvp<16>(h, tab, batch, pass, st);
+    else
+      launch_hvp<32>(h, tab, batch, pass, st);
     if (pass == 0)
       hipLaunchKernelGGL(k_hvp_coef, dim3((unsigned)(batch * h->rank)), dim3(256), 0, st, h->d_part,
                          (int64_t)h->items.size(), batch, h->rank, h->d_lambda, 1.0 / (double)h->total, h->d_coef);
@@ -448,6 +440,10 @@ void free_hvp(sk_hvp *h) {
   f(h->d_coef);
   f(h->X);
   f(h->Y);
+  f(h->d_ws_tab);
+  f(h->d_user_tab);
+  if (h->h_user_tab) (void)hipHostFree(h->h_user_tab);
+  if (h->user_ev) (void)hipEventDestroy(h->user_ev);
   for (hipEvent_t e : h->evpool) (void)hipEventDestroy(e);
   h->evpool.clear();
 }
@@ -480,7 +476,6 @@ int sk_hvp_create(const sk_layer_shape *shapes, int32_t n_layers, int32_t rank, 
   h->key = make_key(seed);
   h->max_batch = max_batch;
   h->lambdas.assign(lambdas, lambdas + rank);
-  h->layer_item0.push_back(0);
   for (int l = 0; l < n_layers; ++l) {
     const int64_t n = shapes[l].rows * shapes[l].cols;
     h->off.push_back(h->total);
@@ -488,7 +483,6 @@ int sk_hvp_create(const sk_layer_shape *shapes, int32_t n_layers, int32_t rank, 
     h->total += n;
     for (int64_t e0 = 0; e0 < n; e0 += kChunk)
       h->items.push_back(HvpItem{l, (int32_t)std::min<int64_t>(kChunk, n - e0), e0});
-    h->layer_item0.push_back((int32_t)h->items.size());
   }
   DeviceGuard guard(device);
   auto alloc = [&](void **p, size_t bytes) -> bool {
@@ -510,7 +504,11 @@ int sk_hvp_create(const sk_layer_shape *shapes, int32_t n_layers, int32_t rank, 
       !alloc((void **)&h->d_lambda, sizeof(float) * rank) ||
       !alloc((void **)&h->d_part, sizeof(float) * h->items.size() * max_batch * rank) ||
       !alloc((void **)&h->d_coef, sizeof(float) * max_batch * rank) || !alloc((void **)&h->X, ws) ||
-      !alloc((void **)&h->Y, ws)) {
+      !alloc((void **)&h->Y, ws) || !alloc((void **)&h->d_ws_tab, sizeof(HvpLayerPtr) * n_layers) ||
+      !alloc((void **)&h->d_user_tab, sizeof(HvpLayerPtr) * n_layers) ||
+      hipHostMalloc((void **)&h->h_user_tab, sizeof(HvpLayerPtr) * n_layers) != hipSuccess ||
+      hipEventCreateWithFlags(&h->user_ev, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
     free_hvp(h);
     delete h;
     return fail(SK_ENOMEM, "hipMalloc failed (workspace of 2 x " + std::to_string(ws) + " bytes)");
@@ -522,12 +520,17 @@ int sk_hvp_create(const sk_layer_shape *shapes, int32_t n_layers, int32_t rank, 
     delete h;
     return fail(SK_EHIP, "hipMemcpy of the item table failed");
   }
+  std::vector<HvpLayerPtr> wtab(n_layers);
   for (int l = 0; l < n_layers; ++l) {
     float *xl = h->X + woff[l], *yl = h->Y + woff[l];
-    h->xin.push_back(xl);
     h->xsk.push_back(xl);
-    h->yout.push_back(yl);
     h->ysk.push_back(yl);
+    wtab[l] = HvpLayerPtr{xl, yl, h->n[l]};
+  }
+  if (hipMemcpy(h->d_ws_tab, wtab.data(), sizeof(HvpLayerPtr) * n_layers, hipMemcpyHostToDevice) != hipSuccess) {
+    free_hvp(h);
+    delete h;
+    return fail(SK_EHIP, "hipMemcpy of the workspace table failed");
   }
   *out = h;
   return SK_OK;
@@ -539,7 +542,16 @@ int sk_hvp_apply(sk_hvp *h, const float *const *x, int64_t batch, float *const *
   for (size_t l = 0; l < h->n.size(); ++l)
     if (!x[l] || !y[l]) return fail(SK_EINVAL, "NULL layer pointer");
   DeviceGuard guard(h->device);
-  hvp_run(h, x, batch, y, (hipStream_t)stream);
+  hipStream_t st = (hipStream_t)stream;
+  if (h->user_ev_pending && hipEventSynchronize(h->user_ev) != hipSuccess)
+    return fail(SK_EHIP, "hipEventSynchronize failed");
+  for (size_t l = 0; l < h->n.size(); ++l) h->h_user_tab[l] = HvpLayerPtr{x[l], y[l], h->n[l]};
+  if (hipMemcpyAsync(h->d_user_tab, h->h_user_tab, sizeof(HvpLayerPtr) * h->n.size(), hipMemcpyHostToDevice, st) !=
+          hipSuccess ||
+      hipEventRecord(h->user_ev, st) != hipSuccess)
+    return fail(SK_EHIP, "upload of the layer table failed");
+  h->user_ev_pending = true;
+  hvp_run(h, h->d_user_tab, batch, st);
   return SK_OK;
 }
 
@@ -566,7 +578,7 @@ int sketch_hvp(sk_sketch *s, sk_hvp *h, const float *v, int64_t batch, float *ou
     const int64_t bc = std::min(h->max_batch, batch - b0);
     int rc = sketch_apply_T(s, v + b0 * s->D, bc, h->xsk.data(), SK_F32, nullptr, 0, nl, stream);
     if (rc != SK_OK) return rc;
-    hvp_run(h, h->xin.data(), bc, h->yout.data(), (hipStream_t)stream);
+    hvp_run(h, h->d_ws_tab, bc, (hipStream_t)stream);
     rc = sketch_apply(s, h->ysk.data(), SK_F32, bc, out + b0 * s->D, 0, nl, 0, stream);
     if (rc != SK_OK) return rc;
   }
