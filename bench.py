@@ -48,7 +48,7 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "fjl:prolog": "k_fjl_prolog", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
              "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
              "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
-             "afjl:gather": "k_afjl_T_out"}
+             "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T"}
 
 
 def qh_flops(kind, shapes, D):

@@ -240,7 +240,8 @@ enum {
   SK_PROF_QH_FIRST = 11, /* SK_QKH/SK_AFJLQ contraction that reads the input */
   SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ/SK_AFFDQ second contraction        */
   SK_PROF_QH_T = 13,     /* SK_QKH/SK_AFJLQ/SK_AFFDQ transposes               */
-  SK_PROF_CLASSES = 14
+  SK_PROF_FFD_T = 14,    /* FFD transpose with D <= 2^13 (one launch)        */
+  SK_PROF_CLASSES = 15
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

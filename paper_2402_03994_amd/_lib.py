@@ -21,7 +21,7 @@ EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", 
 HVP_PROF_CLASSES = ["hvp_dots", "hvp_combine", "arnoldi_orth"]
 HVP_MAX_RANK = 32
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
-                "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t"]
+                "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t", "ffd_t"]
 
 
 class LayerShape(ctypes.Structure):

@@ -890,7 +890,7 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           break;
         case SK_FFD:
           if (lgD <= kFfdSmallMax) {
-            SK_PROF(SK_PROF_GATHER, obytes + bc * s->D * 4,
+            SK_PROF(SK_PROF_FFD_T, obytes + bc * s->D * 4,
                     launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st));
           } else if (ffd_large_path(s)) {
             SK_PROF(SK_PROF_FFD, 0, run_ffd_large_T(s, l, z, b0, bc, o, out_dtype, th, 1, st));

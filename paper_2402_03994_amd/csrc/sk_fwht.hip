@@ -43,9 +43,9 @@ __global__ __launch_bounds__(256) void k_fwht_pass(float *data, int lgn, int lo,
   float *base = data + v * n + (a << (lo + w)) + (cb << lgcs);
   const int total = 1 << (w + lgcs);
   const int cmask = (1 << lgcs) - 1;
-  for (int e = threadIdx.x; e < total; e += 256) s[e] = base[((int64_t)(e >> lgcs) << lo) + (e & cmask)];
-  lds_fwht(s, w, lgcs);
-  for (int e = threadIdx.x; e < total; e += 256) base[((int64_t)(e >> lgcs) << lo) + (e & cmask)] = s[e] * scale;
+  for (int e = threadIdx.x; e < total; e += 256) s[p16(e)] = base[((int64_t)(e >> lgcs) << lo) + (e & cmask)];
+  lds_fwht_regs(s, w + lgcs, lgcs);
+  for (int e = threadIdx.x; e < total; e += 256) base[((int64_t)(e >> lgcs) << lo) + (e & cmask)] = s[p16(e)] * scale;
 }
 
 void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) {
@@ -63,7 +63,7 @@ void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) {
     }
     const int64_t tiles = V * ((1ll << lgn) >> (w + lgcs));
     const float scale = (float)(1.0 / sqrt((double)(1ll << w)));
-    const size_t shm = sizeof(float) << (w + lgcs);
+    const size_t shm = sizeof(float) * p16_floats(1 << (w + lgcs));
     hipLaunchKernelGGL(k_fwht_pass, dim3((unsigned)tiles), dim3(256), shm, st, data, lgn, lo, w, lgcs, scale);
     SK_CHECK_LAUNCH();
     lo += w;
@@ -1179,78 +1179,166 @@ int64_t ffd_live_blocks(const sk_sketch *s, int layer) {
   return (ld.n + s->D - 1) / s->D;
 }
 
-constexpr int kFfdGroup = 8;  // blocks per workgroup (small D)
+constexpr int kFfdGroup = 2;  // blocks per workgroup (small D)
 
 int64_t ffd_small_groups(const sk_sketch *s, int layer) {
   return (ffd_live_blocks(s, layer) + kFfdGroup - 1) / kFfdGroup;
 }
 
-template <bool BF16>
+// The random ingredients of block b of the layer, built once per workgroup into
+// LDS and shared by its tile of vectors: Pi_b as a table (16-bit entries,
+// D <= 2^13), g_b, and the sign words of the block's coordinates.
+__device__ __forceinline__ void ffd_block_tables(const LayerDesc &ld, int64_t b, int lgD, Key key, uint16_t *tperm,
+                                                 float *tg, uint32_t *tsgn) {
+  const int D = 1 << lgD;
+  const int64_t base = b * D;
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
+  for (int i = threadIdx.x; i < D; i += 256) tperm[i] = (uint16_t)perm_fwd(pk, (uint32_t)i);
+  for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
+    float g[4];
+    gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (i4 + q < D) tg[i4 + q] = g[q];
+  }
+  // sign words of the global 32-coordinate runs the block touches (blocks of D < 128 need not
+  // start on a Philox block): word w covers coordinates 32 ((base >> 5) + w) ..
+  const int nw = (int)(((base + D - 1) >> 5) - (base >> 5)) + 1;
+  for (int w = threadIdx.x; w < nw; w += 256) tsgn[w] = sign_word((uint64_t)(((base >> 5) + w) << 5), (uint32_t)ld.layer_id, key);
+}
+
+// Sign bit of coordinate i of the block starting at base, from ffd_block_tables' words.
+__device__ __forceinline__ uint32_t ffd_sign_bit(const uint32_t *tsgn, int64_t base, int i) {
+  const int64_t j = base + i;
+  return (tsgn[(j >> 5) - (base >> 5)] >> (j & 31)) & 1u;
+}
+
+// Forward, D <= 2^13: a workgroup takes kFfdGroup blocks and VT vectors; per
+// block the tables are built once, then for each vector: load, H_D, scatter
+// through Pi_b with g, H_D, signs, accumulated over the group's blocks in
+// registers (PER = D / 256 values per thread and vector).
+template <bool BF16, int VT, int PER>
 __global__ __launch_bounds__(256) void k_ffd_small_fwd(const LayerDesc *__restrict__ layers, int layer,
                                                        const void *__restrict__ x, int lgD, int64_t b_begin,
                                                        int64_t bc, float *__restrict__ part, int64_t slot0,
                                                        int64_t nlive, Key key) {
   extern __shared__ float sm[];
   const int D = 1 << lgD;
-  float *s = sm;
-  float *u = sm + D;
+  float *s = sm;                  // p16 layout
+  float *u = sm + p16_floats(D);  // p16 layout
+  float *tg = sm + 2 * p16_floats(D);
+  uint32_t *tsgn = reinterpret_cast<uint32_t *>(tg + D);
+  uint16_t *tperm = reinterpret_cast<uint16_t *>(tsgn + (D + 31) / 32 + 4);
   const LayerDesc &ld = layers[layer];
-  const int64_t v = blockIdx.y;
+  const int64_t v0 = (int64_t)blockIdx.y * VT;
   const int64_t blk0 = (int64_t)blockIdx.x * kFfdGroup;
-  const int per = D / 256 > 0 ? D / 256 : 1;
-  float acc[32];
+  float acc[VT][PER];
 #pragma unroll
-  for (int i = 0; i < 32; ++i) acc[i] = 0.0f;
+  for (int v = 0; v < VT; ++v)
+#pragma unroll
+    for (int k = 0; k < PER; ++k) acc[v][k] = 0.0f;
   const float inv = 1.0f / (float)D;
   for (int64_t b = blk0; b < blk0 + kFfdGroup && b < nlive; ++b) {
     const int64_t base = b * D;
-    for (int i = threadIdx.x; i < D; i += 256) {
-      const int64_t j = base + i;
-      float val = 0.0f;
-      if (j < ld.n) {
-        const int64_t e = (b_begin + v) * ld.n + j;
-        val = BF16 ? bf16_to_f32(((const uint16_t *)x)[e]) : ((const float *)x)[e];
-      }
-      s[i] = val;
-    }
-    lds_fwht(s, lgD, 0);
-    const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
-    for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
-      float g[4];
-      gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) u[perm_fwd(pk, (uint32_t)(i4 + q))] = g[q] * s[i4 + q];
-    }
-    lds_fwht(u, lgD, 0);
-    for (int k = 0; k < per; ++k) {
-      const int i = threadIdx.x + k * 256;
-      if (i < D) {
-        const uint32_t bit = (sign_word((uint64_t)(base + i), (uint32_t)ld.layer_id, key) >> ((base + i) & 31)) & 1u;
-        acc[k] += flip(u[i] * inv, bit);
-      }
-    }
+    __syncthreads();  // the previous block's readers of the tables are done
+    ffd_block_tables(ld, b, lgD, key, tperm, tg, tsgn);
     __syncthreads();
+    // the next vector's coordinates are loaded into registers while the current one is transformed
+    // (PER independent loads in flight instead of one dependent load per loop trip)
+    float xr[PER];
+    auto load_x = [&](int64_t vv) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int i = threadIdx.x + k * 256;
+        const int64_t j = base + i;
+        float val = 0.0f;
+        if (i < D && j < ld.n && vv < bc) {
+          const int64_t e = (b_begin + vv) * ld.n + j;
+          val = BF16 ? bf16_to_f32(((const uint16_t *)x)[e]) : ((const float *)x)[e];
+        }
+        xr[k] = val;
+      }
+    };
+    load_x(v0);
+#pragma unroll
+    for (int v = 0; v < VT; ++v) {
+      if (v0 + v >= bc) break;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int i = threadIdx.x + k * 256;
+        if (i < D) s[p16(i)] = xr[k];
+      }
+      if (v + 1 < VT) load_x(v0 + v + 1);
+      lds_fwht_regs(s, lgD, 0);
+      for (int i = threadIdx.x; i < D; i += 256) u[p16(tperm[i])] = tg[i] * s[p16(i)];
+      lds_fwht_regs(u, lgD, 0);
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int i = threadIdx.x + k * 256;
+        if (i < D) acc[v][k] += flip(u[p16(i)] * inv, ffd_sign_bit(tsgn, base, i));
+      }
+    }
   }
-  float *dst = part + ((slot0 + blockIdx.x) * bc + v) * D;
-  for (int k = 0; k < per; ++k) {
-    const int i = threadIdx.x + k * 256;
-    if (i < D) dst[i] = acc[k];
+#pragma unroll
+  for (int v = 0; v < VT; ++v) {
+    if (v0 + v >= bc) break;
+    float *dst = part + ((slot0 + blockIdx.x) * bc + v0 + v) * D;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = threadIdx.x + k * 256;
+      if (i < D) dst[i] = acc[v][k];
+    }
   }
+}
+
+// LDS of the small-D FFD kernels: s, u (p16 layout), g (D floats), sign words, Pi (16-bit).
+static size_t ffd_small_shm(int64_t D) {
+  return (size_t)(2 * p16_floats((int)D) + D) * 4 + ((D + 31) / 32 + 4) * 4 + (size_t)D * 2 + 16;
+}
+
+// Dynamic LDS above 64 KB (D = 2^13: 116 KB of the 160 KB a gfx950 workgroup may use) is
+// requested explicitly.
+static void ffd_allow_shm(const void *fn, size_t shm) {
+  if (shm > 65536) (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+}
+
+template <int VT>
+static void ffd_small_fwd_go(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                             float *part, int64_t slot0, int64_t groups, int lgD, hipStream_t st) {
+  const dim3 grid((unsigned)groups, (unsigned)((bc + VT - 1) / VT));
+  const size_t shm = ffd_small_shm(s->D);
+  const int64_t nlive = ffd_live_blocks(s, layer);
+#define SK_FFDS(PER)                                                                                             \
+  do {                                                                                                           \
+    if (dtype == SK_BF16) {                                                                                      \
+      ffd_allow_shm((const void *)k_ffd_small_fwd<true, VT, PER>, shm);                                          \
+      hipLaunchKernelGGL((k_ffd_small_fwd<true, VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, \
+                         b_begin, bc, part, slot0, nlive, s->key);                                                \
+    } else {                                                                                                     \
+      ffd_allow_shm((const void *)k_ffd_small_fwd<false, VT, PER>, shm);                                         \
+      hipLaunchKernelGGL((k_ffd_small_fwd<false, VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, x,     \
+                         lgD, b_begin, bc, part, slot0, nlive, s->key);                                           \
+    }                                                                                                            \
+  } while (0)
+  switch (lgD <= 8 ? 1 : 1 << (lgD - 8)) {
+    case 1: SK_FFDS(1); break;
+    case 2: SK_FFDS(2); break;
+    case 4: SK_FFDS(4); break;
+    case 8: SK_FFDS(8); break;
+    case 16: SK_FFDS(16); break;
+    default: SK_FFDS(32); break;
+  }
+#undef SK_FFDS
 }
 
 void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                           float *part, int64_t slot0, int64_t groups, hipStream_t st) {
   const int lgD = log2_exact(s->D);
-  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
-  const size_t shm = 2 * sizeof(float) * s->D;
-  dim3 grid((unsigned)groups, (unsigned)bc);
-  const int64_t nlive = ffd_live_blocks(s, layer);
-  if (dtype == SK_BF16)
-    hipLaunchKernelGGL(k_ffd_small_fwd<true>, grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, b_begin, bc, part,
-                       slot0, nlive, s->key);
+  if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
+  if (lgD == kFfdSmallMax)
+    ffd_small_fwd_go<2>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, st);
   else
-    hipLaunchKernelGGL(k_ffd_small_fwd<false>, grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, b_begin, bc,
-                       part, slot0, nlive, s->key);
+    ffd_small_fwd_go<4>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, st);
   SK_CHECK_LAUNCH();
 }
 
@@ -1272,46 +1360,78 @@ void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64
   SK_CHECK_LAUNCH();
 }
 
+// Transpose, D <= 2^13: a workgroup takes one block and VT vectors; the
+// block's tables are built once, then per vector: signs, H_D, gather through
+// Pi_b with g, H_D, theta0, store.
+template <int VT, int PER>
 __global__ __launch_bounds__(256) void k_ffd_small_T(const LayerDesc *__restrict__ layers, int layer,
                                                      const float *__restrict__ z, int lgD, int64_t b_begin,
-                                                     void *__restrict__ out, int out_dtype,
+                                                     int64_t bc, void *__restrict__ out, int out_dtype,
                                                      const float *__restrict__ theta0, Key key) {
   extern __shared__ float sm[];
   const int D = 1 << lgD;
-  float *s = sm;
-  float *u = sm + D;
+  float *s = sm;                  // p16 layout
+  float *u = sm + p16_floats(D);  // p16 layout
+  float *tg = sm + 2 * p16_floats(D);
+  uint32_t *tsgn = reinterpret_cast<uint32_t *>(tg + D);
+  uint16_t *tperm = reinterpret_cast<uint16_t *>(tsgn + (D + 31) / 32 + 4);
   const LayerDesc &ld = layers[layer];
   const int64_t b = blockIdx.x;
-  const int64_t v = blockIdx.y;
+  const int64_t v0 = (int64_t)blockIdx.y * VT;
   const int64_t base = b * D;
-  for (int i = threadIdx.x; i < D; i += 256) {
-    const uint32_t bit = (sign_word((uint64_t)(base + i), (uint32_t)ld.layer_id, key) >> ((base + i) & 31)) & 1u;
-    s[i] = flip(z[(b_begin + v) * D + i], bit);
-  }
-  lds_fwht(s, lgD, 0);
-  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
-  for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
-    float g[4];
-    gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) u[i4 + q] = g[q] * s[perm_fwd(pk, (uint32_t)(i4 + q))];
-  }
-  lds_fwht(u, lgD, 0);
+  ffd_block_tables(ld, b, lgD, key, tperm, tg, tsgn);
+  __syncthreads();
   const float inv = 1.0f / (float)D;
-  for (int i = threadIdx.x; i < D; i += 256) {
-    const int64_t j = base + i;
-    if (j < ld.n) store_out(out, out_dtype, (b_begin + v) * ld.n + j, u[i] * inv + (theta0 ? theta0[j] : 0.0f));
+  float zr[PER];
+  auto load_z = [&](int64_t vv) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = threadIdx.x + k * 256;
+      zr[k] = (i < D && vv < bc) ? z[(b_begin + vv) * D + i] : 0.0f;
+    }
+  };
+  load_z(v0);
+  for (int v = 0; v < VT; ++v) {
+    if (v0 + v >= bc) break;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = threadIdx.x + k * 256;
+      if (i < D) s[p16(i)] = flip(zr[k], ffd_sign_bit(tsgn, base, i));
+    }
+    if (v + 1 < VT) load_z(v0 + v + 1);
+    lds_fwht_regs(s, lgD, 0);
+    for (int i = threadIdx.x; i < D; i += 256) u[p16(i)] = tg[i] * s[p16(tperm[i])];
+    lds_fwht_regs(u, lgD, 0);
+    for (int i = threadIdx.x; i < D; i += 256) {
+      const int64_t j = base + i;
+      if (j < ld.n)
+        store_out(out, out_dtype, (b_begin + v0 + v) * ld.n + j, u[p16(i)] * inv + (theta0 ? theta0[j] : 0.0f));
+    }
   }
 }
 
 void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
                         int out_dtype, const float *theta0, hipStream_t st) {
   const int lgD = log2_exact(s->D);
-  if (lgD < 4 || lgD > 20) return;  // create() admits 2^4 <= D <= 2^20 only
-  const size_t shm = 2 * sizeof(float) * s->D;
-  dim3 grid((unsigned)ffd_live_blocks(s, layer), (unsigned)bc);
-  hipLaunchKernelGGL(k_ffd_small_T, grid, dim3(256), shm, st, s->d_layers, layer, z, lgD, b_begin, out, out_dtype,
-                     theta0, s->key);
+  if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
+  constexpr int VT = 4;
+  const dim3 grid((unsigned)ffd_live_blocks(s, layer), (unsigned)((bc + VT - 1) / VT));
+  const size_t shm = ffd_small_shm(s->D);
+#define SK_FFDT(PER)                                                                                              \
+  do {                                                                                                            \
+    ffd_allow_shm((const void *)k_ffd_small_T<VT, PER>, shm);                                                     \
+    hipLaunchKernelGGL((k_ffd_small_T<VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, z, lgD, b_begin, bc, \
+                       out, out_dtype, theta0, s->key);                                                           \
+  } while (0)
+  switch (lgD <= 8 ? 1 : 1 << (lgD - 8)) {
+    case 1: SK_FFDT(1); break;
+    case 2: SK_FFDT(2); break;
+    case 4: SK_FFDT(4); break;
+    case 8: SK_FFDT(8); break;
+    case 16: SK_FFDT(16); break;
+    default: SK_FFDT(32); break;
+  }
+#undef SK_FFDT
   SK_CHECK_LAUNCH();
 }
 

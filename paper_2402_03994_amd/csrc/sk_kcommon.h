@@ -94,6 +94,55 @@ __device__ __forceinline__ void fwht_regs_t(float *v) {
   FwhtStage<N, 1>::run(v);
 }
 
+// LDS tiles in the "p16" layout: one pad word after every 16 floats
+// (element i at i + i / 16), so that the register passes below touch 32
+// distinct banks per half-wave whichever index bits they hold.
+__device__ __forceinline__ int p16(int i) { return i + (i >> 4); }
+__host__ __device__ constexpr int p16_floats(int n) { return n + n / 16; }
+
+// One pass of lds_fwht_regs: every thread takes groups of 2^W elements that
+// differ in index bits [p, p + W) (the other bits from the group number),
+// transforms them in registers and writes them back.
+template <int W>
+__device__ __forceinline__ void fwht_pass_p16(float *s, int lgn, int p) {
+  constexpr int G = 1 << W;
+  const int ngroups = 1 << (lgn - W);
+  const int lowmask = (1 << p) - 1;
+  for (int g = threadIdx.x; g < ngroups; g += blockDim.x) {
+    const int base = ((g >> p) << (p + W)) | (g & lowmask);
+    float e[G];
+#pragma unroll
+    for (int m = 0; m < G; ++m) e[m] = s[p16(base + (m << p))];
+    fwht_regs_t<G>(e);
+#pragma unroll
+    for (int m = 0; m < G; ++m) s[p16(base + (m << p))] = e[m];
+  }
+}
+
+// In-place unnormalised Walsh-Hadamard transform along index bits
+// [p0, lgn) of a 2^lgn-element LDS tile in the p16 layout (p0 > 0 leaves the
+// low bits as independent columns), four bits per pass held in registers:
+// a quarter of the barriers and LDS round trips of the radix-2 lds_fwht.
+// Ends synchronised.
+__device__ __forceinline__ void lds_fwht_regs(float *s, int lgn, int p0) {
+  int p = p0;
+  for (; p + 4 <= lgn; p += 4) {
+    __syncthreads();
+    fwht_pass_p16<4>(s, lgn, p);
+  }
+  const int rem = lgn - p;
+  if (rem > 0) {
+    __syncthreads();
+    if (rem == 1)
+      fwht_pass_p16<1>(s, lgn, p);
+    else if (rem == 2)
+      fwht_pass_p16<2>(s, lgn, p);
+    else
+      fwht_pass_p16<3>(s, lgn, p);
+  }
+  __syncthreads();
+}
+
 // 1024-point unnormalised Walsh-Hadamard transform of NV rows spread over a
 // 256-thread workgroup.  On entry thread t holds columns 4t .. 4t+3 of every
 // row in v[r][0..3]; on exit it holds columns t, t+256, t+512, t+768 in

@@ -298,3 +298,25 @@ def test_afjl_single_vector(dtype, aligned, dev):
     ref = O.apply("afjl", shapes, D, seed, [oracle_in(x)[0] for x in xs], dtype=oracle_in(xs[0])[1])
     assert rel_err(y, ref) < TOL_F32
     s.close()
+
+
+@pytest.mark.parametrize("D", [16, 64, 4096, 8192])
+def test_ffd_small_D_vector_tiles(D, dev):
+    """FFD with D <= 2^13 (one workgroup per block group and tile of vectors, the block's permutation,
+    Gaussians and signs built once in LDS): 5 vectors (a partial tile), ragged tail, blocks of D < 128
+    that do not start on a 128-coordinate boundary, forward and theta0 + S^T z."""
+    shapes = [(1, 5 * D + 7), (3, D // 2 + 1)]
+    seed = 60 + D
+    xs = rand_inputs(shapes, 5, seed)
+    s = sk("ffd", shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("ffd", shapes, D, seed, [x.numpy() for x in xs])
+    assert rel_err(y, ref) < TOL_F32
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((5, D), generator=g)
+    th = [torch.randn(r * c, generator=g) * 0.02 for r, c in shapes]
+    outs = s.apply_T(z.to(dev), theta0=[t.to(dev) for t in th])
+    refs = O.apply_T("ffd", shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL_F32
+    s.close()
