@@ -159,3 +159,83 @@ def top_rel_mae(est, truth, m: int = 10) -> float:
     e = np.sort(np.real(np.asarray(est)))[::-1][:m]
     t = np.sort(np.asarray(truth, dtype=np.float64))[::-1][:m]
     return float(np.mean(np.abs(e - t) / np.abs(t)))
+
+
+# --- intrinsic-dimension search ------------------------------------------------
+def id_decide(tau_new: float, tau_old: float, d: int, tau_target: float, delta: float, D_max: int):
+    """One decision of the search (Sec. 4, "Improving the search for the intrinsic dimension"): returns
+    ("done", d) when the metric reached its target, ("fail", d) when doubling would pass D_max, else
+    ("go", d') with d' = 2 d if the round improved the metric by less than delta, d otherwise."""
+    if tau_new >= tau_target:
+        return "done", d
+    if tau_new - tau_old < delta:
+        d = 2 * d
+        if d > D_max:
+            return "fail", d
+    return "go", d
+
+
+def id_search(kind: str, shapes, D: int, seed: int, hp: dict, theta0, d_min: int, tau_target: float, c: int,
+              delta: float, max_rounds: int):
+    """The intrinsic-dimension search on the synthetic quadratic objective L(theta) = 1/2 theta^T H theta
+    (minimum 0 at theta* = 0), metric tau = 1 - L(theta) / L(theta0) (the fraction of the loss the
+    finetuning removes; the full model reaches 1).
+
+    Finetuning (the listing leaves it abstract): theta = theta0 + S^T omega with omega in R^D (D = D_max)
+    and only omega[:d] free (the listing zeros the gradient's other components); c steps of linear
+    conjugate gradients on omega[:d], restarted every round from the current omega.  For this objective
+    f(omega) = L(theta0 + S^T omega) has gradient S H theta and Hessian M = S H S^T, so one CG step costs
+    one sketched HVP.  A step with p.Mp <= 0 or r.r = 0 leaves the state unchanged.
+    After each round: tau from the definition (lift, HVP, inner product) and id_decide.
+
+    theta0: per layer a [n_l] array.  Returns dict(d, status, taus, ds, omega, L0) with status 0 (target
+    reached, d the estimate), 1 (D_max exceeded) or 2 (max_rounds used)."""
+    theta0 = [np.asarray(t, dtype=np.float64).reshape(1, -1) for t in theta0]
+    omega = np.zeros(D, dtype=np.float64)
+
+    def lift(om):
+        st = _sk_apply_T(kind, shapes, D, seed, om[None, :])
+        return [t + u for t, u in zip(theta0, st)]
+
+    def loss_hx(th):
+        hx = hvp(shapes, xs=th, **hp)
+        return 0.5 * sum(float((a * b).sum()) for a, b in zip(th, hx)), hx
+
+    def grad(om):
+        _, hx = loss_hx(lift(om))
+        return _apply_fp64(kind, shapes, D, seed, hx)[0]
+
+    def M(p):
+        return sketched_hvp(kind, shapes, D, seed, hp, p[None, :])[0]
+
+    L0, _ = loss_hx(lift(omega))
+    tau_old, d = 0.0, int(d_min)
+    taus, ds = [], []
+    for _ in range(max_rounds):
+        r = grad(omega)
+        r[d:] = 0.0
+        p = -r
+        rr = float(r @ r)
+        for _ in range(c):
+            q = M(p)
+            q[d:] = 0.0
+            pq = float(p @ q)
+            if pq <= 0.0 or rr == 0.0:
+                continue
+            alpha = rr / pq
+            omega += alpha * p
+            r = r + alpha * q
+            rr_new = float(r @ r)
+            p = -r + (rr_new / rr) * p
+            rr = rr_new
+        L, _ = loss_hx(lift(omega))
+        tau = 1.0 - L / L0
+        taus.append(tau)
+        ds.append(d)
+        verdict, d_next = id_decide(tau, tau_old, d, tau_target, delta, D)
+        if verdict == "done":
+            return dict(d=d, status=0, taus=taus, ds=ds, omega=omega, L0=L0)
+        if verdict == "fail":
+            return dict(d=0, status=1, taus=taus, ds=ds, omega=omega, L0=L0)
+        d, tau_old = d_next, tau
+    return dict(d=0, status=2, taus=taus, ds=ds, omega=omega, L0=L0)

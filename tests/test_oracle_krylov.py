@@ -190,3 +190,75 @@ def test_sketched_top_eigenvalues_near_hessian(kind, D):
     _, Hb = K.arnoldi(op, np.random.default_rng(13).standard_normal(D), 14)
     truth = K.hessian_spectrum_top(shapes, **hp)
     assert K.top_rel_mae(K.ritz_values(Hb), truth, 10) < 0.1
+
+
+# --- intrinsic-dimension search (Sec. 4, "Improving the search for the intrinsic dimension") -------------
+def test_id_decide_rules():
+    """The listing's rules: stop at the target; double d when a round improves the metric by less than delta
+    (failing past D_max); otherwise keep d."""
+    assert K.id_decide(0.95, 0.1, 8, 0.9, 0.05, 64) == ("done", 8)
+    assert K.id_decide(0.30, 0.28, 8, 0.9, 0.05, 64) == ("go", 16)
+    assert K.id_decide(0.30, 0.20, 8, 0.9, 0.05, 64) == ("go", 8)
+    assert K.id_decide(0.30, 0.28, 64, 0.9, 0.05, 64) == ("fail", 128)
+    assert K.id_decide(0.90, 0.89, 64, 0.9, 0.05, 64) == ("done", 64)  # the target wins over a small step
+
+
+def _id_problem(rank=4, shift=0.0, shapes=((1, 3000), (20, 250))):
+    hp = dict(rank=rank, lambdas=np.ones(rank, dtype=np.float32), shift=shift, seed=9)
+    g = np.random.default_rng(0)
+    x = [g.standard_normal((1, a * b)) for a, b in shapes]
+    th0 = [t[0] for t in K.hvp(list(shapes), xs=x, **dict(hp, shift=0.0))]  # theta0 in the span of the v_j
+    return list(shapes), hp, th0
+
+
+def test_id_objective_gradient_by_finite_differences():
+    """The finetuning gradient S H (theta0 + S^T omega) against central differences of
+    L(theta0 + S^T omega) = 1/2 theta^T H theta, on a few coordinates of omega."""
+    shapes, hp, th0 = _id_problem(shift=0.25)
+    D, seed = 64, 3
+    om = np.random.default_rng(1).standard_normal(D) * 0.1
+
+    def loss(o):
+        th = [t + u for t, u in zip([np.asarray(t)[None, :] for t in th0],
+                                    O.apply_T("afjl", shapes, D, seed, o[None, :]))]
+        return 0.5 * sum(float((a * b).sum()) for a, b in zip(th, K.hvp(shapes, xs=th, **hp)))
+
+    th = [t[None, :] + u for t, u in zip(th0, O.apply_T("afjl", shapes, D, seed, om[None, :]))]
+    g = K._apply_fp64("afjl", shapes, D, seed, K.hvp(shapes, xs=th, **hp))[0]
+    eps = 1e-4
+    for i in [0, 5, 63]:
+        e = np.zeros(D)
+        e[i] = eps
+        fd = (loss(om + e) - loss(om - e)) / (2 * eps)
+        assert abs(fd - g[i]) < 1e-6 * max(1.0, abs(g[i]))
+
+
+def test_id_search_known_answer():
+    """A rank-4 quadratic with theta0 in the span of its spikes and no bulk: a d-dimensional subspace
+    removes all of the loss exactly when d >= 4 (CG converges in at most rank steps), so the search
+    from d = 1 returns 4; the frozen coordinates of omega stay zero."""
+    shapes, hp, th0 = _id_problem()
+    res = K.id_search("afjl", shapes, 256, 3, hp, th0, 1, 0.9, 6, 0.05, 12)
+    assert res["status"] == 0 and res["d"] == 4
+    assert res["taus"][-1] > 1 - 1e-9
+    assert all(t < 0.9 for t in res["taus"][:-1])
+    assert np.all(res["omega"][4:] == 0.0)
+
+
+def test_id_search_round_minimises_on_the_subspace():
+    """With c >= rank CG steps a round reaches the minimum of L on theta0 + S^T span(e_0..e_{d-1}): the
+    gradient's free components vanish."""
+    shapes, hp, th0 = _id_problem(rank=3, shift=0.0)
+    D, seed = 128, 4
+    res = K.id_search("afjl", shapes, D, seed, hp, th0, 2, 1.1, 5, -1.0, 1)  # one round at d = 2
+    om = res["omega"]
+    th = [t[None, :] + u for t, u in zip(th0, O.apply_T("afjl", shapes, D, seed, om[None, :]))]
+    g = K._apply_fp64("afjl", shapes, D, seed, K.hvp(shapes, xs=th, **hp))[0]
+    g0 = K._apply_fp64("afjl", shapes, D, seed, K.hvp(shapes, xs=[t[None, :] for t in th0], **hp))[0]
+    assert np.abs(g[:2]).max() < 1e-9 * np.abs(g0).max()
+
+
+def test_id_search_fails_past_D_max():
+    shapes, hp, th0 = _id_problem(rank=8)
+    res = K.id_search("afjl", shapes, 16, 3, hp, th0, 4, 0.999999, 2, 0.5, 20)
+    assert res["status"] == 1 and res["d"] == 0
