@@ -25,7 +25,9 @@
  * `shift` (multiplicity N_tot - r) and shift + eig(L^1/2 G L^1/2) with
  * L = diag(lambda), G = V^T V (a spike of r outliers over a flat bulk, the
  * structure the paper's Hessian-spectrum experiments look for).  Any other
- * HVP can be used with sketch_arnoldi_step, which only orthogonalises.
+ * HVP can be used with sketch_arnoldi_step, which only orthogonalises.  The
+ * same Hessian defines the quadratic objective of the intrinsic-dimension
+ * search below.
  *
  * Conventions: return 0 or a negative SK_E* code (sketch_last_error() gives
  * the message); device pointers are plain HIP addresses on the handle's
@@ -120,6 +122,43 @@ int sketch_arnoldi_step(float *Q, int64_t D, int32_t j, float *Hbar, int32_t k, 
  * sketch_arnoldi_work_floats(D, k) floats, else SK_EUNSUPPORTED).
  */
 int sketch_arnoldi(sk_sketch *s, sk_hvp *h, const float *v0, int32_t k, float *Q, float *Hbar, void *stream);
+
+/*
+ * Intrinsic-dimension search (Sec. 4, "Improving the search for the intrinsic
+ * dimension", and the appendix listing of the search) on the synthetic
+ * quadratic objective L(theta) = 1/2 theta^T H theta (minimum 0 at theta = 0)
+ * with the metric tau = 1 - L(theta) / L(theta0), the fraction of the loss the
+ * finetuning removes (the full model reaches 1).
+ *   theta  = theta0 + S^T omega, omega in R^D (D = the sketch's D, the largest
+ *            dimension allowed); only omega[0..d) is trained, the listing's
+ *            zeroed gradient components.
+ *   round  c steps of linear conjugate gradients on omega[0..d) (restarted
+ *          from the current omega each round; gradient S H theta, Hessian
+ *          S H S^T, one sketched HVP per step; a step with p.Mp <= 0 or r.r = 0
+ *          changes nothing), then tau from the quadratic's expansion
+ *          L = L0 + g0.omega + 1/2 omega.(S H S^T omega), g0 = S H theta0.
+ *   rule   tau >= tau_target: done, res->d = d (status 0); else if the round
+ *          improved tau by less than delta: d = 2 d, failing with status 1
+ *          when d > D; status 2 when max_rounds rounds end undecided.
+ *   theta0     host array of n_layers device pointers, fp32 [rows*cols].
+ *   d_min      first d (1 <= d_min <= D); c, max_rounds >= 1.
+ *   work       device, sketch_id_search_work_floats(D) floats; on return
+ *              work[0..D) holds omega.
+ *   tau_trace, d_trace  NULL or host arrays of max_rounds entries: tau and d
+ *              of every round run.
+ * Synchronises `stream` once per round to read tau (the decision is taken on
+ * the host in double precision).
+ */
+typedef struct {
+  int64_t d;       /* the estimate (0 unless status 0)                  */
+  int32_t status;  /* 0 target reached, 1 D exceeded, 2 rounds exhausted */
+  int32_t rounds;  /* rounds run                                          */
+  double L0;       /* L(theta0)                                           */
+} sk_id_result;
+int64_t sketch_id_search_work_floats(int64_t D);
+int sketch_id_search(sk_sketch *s, sk_hvp *h, const float *const *theta0, int64_t d_min, float tau_target,
+                     float delta, int32_t c, int32_t max_rounds, float *work, double *tau_trace, int64_t *d_trace,
+                     sk_id_result *res, void *stream);
 
 /*
  * Kernel timing, as sketch_profile / sketch_profile_read, for the launches

@@ -6,4 +6,4 @@ marshals torch tensors into that library.
 """
 from .sketch import KINDS, Sketch  # noqa: F401
 from ._lib import SketchError  # noqa: F401
-from .hvp import SyntheticHessian, arnoldi, arnoldi_step, ritz_values, sketch_hvp  # noqa: F401
+from .hvp import SyntheticHessian, arnoldi, arnoldi_step, id_search, ritz_values, sketch_hvp  # noqa: F401

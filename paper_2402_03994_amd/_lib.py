@@ -17,11 +17,16 @@ EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", 
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
            "sketch_status_string", "sk_hvp_create", "sk_hvp_apply", "sk_hvp_destroy", "sketch_hvp",
            "sketch_arnoldi_work_floats", "sketch_arnoldi_step", "sketch_arnoldi", "sk_hvp_profile",
-           "sk_hvp_profile_read")
+           "sk_hvp_profile_read", "sketch_id_search_work_floats", "sketch_id_search")
 HVP_PROF_CLASSES = ["hvp_dots", "hvp_combine", "arnoldi_orth"]
 HVP_MAX_RANK = 32
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
                 "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t", "ffd_t"]
+
+
+class IdResult(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int64), ("status", ctypes.c_int32), ("rounds", ctypes.c_int32),
+                ("L0", ctypes.c_double)]
 
 
 class LayerShape(ctypes.Structure):
@@ -88,6 +93,11 @@ def load() -> ctypes.CDLL:
     L.sk_hvp_profile.restype = ctypes.c_int
     L.sk_hvp_profile_read.argtypes = [P, P, P, P]
     L.sk_hvp_profile_read.restype = ctypes.c_int
+    L.sketch_id_search_work_floats.argtypes = [i64]
+    L.sketch_id_search_work_floats.restype = i64
+    L.sketch_id_search.argtypes = [P, P, ctypes.POINTER(P), i64, f32, f32, i32, i32, P, P, P,
+                                   ctypes.POINTER(IdResult), P]
+    L.sketch_id_search.restype = ctypes.c_int
     _lib = L
     return L
 

@@ -20,13 +20,18 @@
 //    the coefficients and Hbar, k_arn_update subtracts Q^T c (four waves split
 //    the rows, combined in a fixed order), k_arn_normalize divides by |w| or
 //    zeroes the row on breakdown.  No atomics: results are deterministic.
+//  * Intrinsic-dimension search (Sec. 4, the doubling search): conjugate
+//    gradients on the free coordinates of omega for the quadratic
+//    L(theta0 + S^T omega) (one sketched HVP per step; the vector updates and
+//    their fp64 dot products in single-workgroup kernels), the metric from the
+//    quadratic's expansion at theta0, the doubling decision on the host.
 #include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
 
 #include "../../include/sketch_hvp.h"
-#include "sk_internal.h"
+#include "sk_launch.h"
 
 using namespace sk;
 
@@ -430,6 +435,111 @@ void hvp_run(sk_hvp *h, const HvpLayerPtr *tab, int64_t batch, hipStream_t st) {
   (void)hipGetLastError();
 }
 
+// ---- intrinsic-dimension search ----------------------------------------------
+// Per-item partial inner products x . y over every layer of a table (one vector).
+__global__ __launch_bounds__(256) void k_tab_dot(const HvpItem *__restrict__ items, const HvpLayerPtr *__restrict__ tab,
+                                                 float *__restrict__ part) {
+  __shared__ float red[4];
+  const HvpItem it = items[blockIdx.x];
+  const HvpLayerPtr lp = tab[it.layer];
+  float a = 0.0f;
+  for (int i = threadIdx.x; i < it.len; i += 256) a += lp.x[it.e0 + i] * lp.y[it.e0 + i];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) a += __shfl_xor(a, m, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// out = scale * sum of n partials (fp64, fixed order; one workgroup).
+__global__ __launch_bounds__(256) void k_sum_f64(const float *__restrict__ part, int64_t n, double scale,
+                                                 double *__restrict__ out) {
+  __shared__ double red[256];
+  double a = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) a += (double)part[i];
+  red[threadIdx.x] = a;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = scale * red[0];
+}
+
+// Block-wide fp64 sum over a 1024-thread workgroup (every thread gets the total).
+__device__ __forceinline__ double block_sum_1024(double v, double *red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int st = 512; st > 0; st >>= 1) {
+    if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+    __syncthreads();
+  }
+  const double t = red[0];
+  __syncthreads();
+  return t;
+}
+
+enum { kIdL0 = 0, kIdRR = 1, kIdL = 2, kIdTau = 3 };  // slots of the search's fp64 scalars
+
+// Round start: r = (g0 + w) on the free coordinates (i < d), 0 elsewhere; p = -r; rr = r.r.
+__global__ __launch_bounds__(1024) void k_cg_start(const float *__restrict__ g0, const float *__restrict__ w,
+                                                   float *__restrict__ r, float *__restrict__ p, int64_t d,
+                                                   int64_t D, double *__restrict__ scal) {
+  __shared__ double red[1024];
+  double a = 0.0;
+  for (int64_t i = threadIdx.x; i < D; i += 1024) {
+    const float ri = i < d ? g0[i] + w[i] : 0.0f;
+    r[i] = ri;
+    p[i] = -ri;
+    a += (double)ri * ri;
+  }
+  const double rr = block_sum_1024(a, red);
+  if (threadIdx.x == 0) scal[kIdRR] = rr;
+}
+
+// One conjugate-gradient step on the free coordinates, q = (S H S^T p) given: alpha = rr / p.q,
+// omega += alpha p, r += alpha q, beta = r.r / rr, p = -r + beta p.  p.q <= 0 or rr = 0 leaves the
+// state unchanged.
+__global__ __launch_bounds__(1024) void k_cg_step(float *__restrict__ omega, float *__restrict__ r,
+                                                  float *__restrict__ p, const float *__restrict__ q, int64_t d,
+                                                  double *__restrict__ scal) {
+  __shared__ double red[1024];
+  double a = 0.0;
+  for (int64_t i = threadIdx.x; i < d; i += 1024) a += (double)p[i] * q[i];
+  const double pq = block_sum_1024(a, red);
+  const double rr = scal[kIdRR];
+  if (!(pq > 0.0) || rr == 0.0) return;  // uniform over the workgroup
+  const float alpha = (float)(rr / pq);
+  double b = 0.0;
+  for (int64_t i = threadIdx.x; i < d; i += 1024) {
+    omega[i] += alpha * p[i];
+    const float ri = r[i] + alpha * q[i];
+    r[i] = ri;
+    b += (double)ri * ri;
+  }
+  const double rr_new = block_sum_1024(b, red);
+  const float beta = (float)(rr_new / rr);
+  for (int64_t i = threadIdx.x; i < d; i += 1024) p[i] = -r[i] + beta * p[i];
+  if (threadIdx.x == 0) scal[kIdRR] = rr_new;
+}
+
+// L = L0 + g0 . omega + 1/2 omega . w (w = S H S^T omega; the quadratic's expansion at theta0),
+// tau = 1 - L / L0.
+__global__ __launch_bounds__(1024) void k_id_eval(const float *__restrict__ g0, const float *__restrict__ w,
+                                                  const float *__restrict__ omega, int64_t D,
+                                                  double *__restrict__ scal) {
+  __shared__ double red[1024];
+  double a = 0.0;
+  for (int64_t i = threadIdx.x; i < D; i += 1024) a += (double)omega[i] * ((double)g0[i] + 0.5 * (double)w[i]);
+  const double t = block_sum_1024(a, red);
+  if (threadIdx.x == 0) {
+    const double L0 = scal[kIdL0];
+    const double L = L0 + t;
+    scal[kIdL] = L;
+    scal[kIdTau] = 1.0 - L / L0;
+  }
+}
+
 void free_hvp(sk_hvp *h) {
   auto f = [](void *p) {
     if (p) (void)hipFree(p);
@@ -618,6 +728,87 @@ int sketch_arnoldi(sk_sketch *s, sk_hvp *h, const float *v0, int32_t k, float *Q
     const int rc = sketch_hvp(s, h, Q + (int64_t)j * D, 1, Q + (int64_t)(j + 1) * D, stream);
     if (rc != SK_OK) return rc;
     arnoldi_step(Q, D, j, Hbar, k, work, st, h);
+  }
+  return SK_OK;
+}
+
+int64_t sketch_id_search_work_floats(int64_t D) { return D < 1 ? 0 : 6 * D + 32; }
+
+int sketch_id_search(sk_sketch *s, sk_hvp *h, const float *const *theta0, int64_t d_min, float tau_target,
+                     float delta, int32_t c, int32_t max_rounds, float *work, double *tau_trace, int64_t *d_trace,
+                     sk_id_result *res, void *stream) {
+  if (!s || !h || !theta0 || !work || !res) return fail(SK_EINVAL, "NULL argument");
+  const int64_t D = s->D;
+  if (d_min < 1 || d_min > D) return fail(SK_EINVAL, "need 1 <= d_min <= D");
+  if (c < 1 || max_rounds < 1) return fail(SK_EINVAL, "need c >= 1 and max_rounds >= 1");
+  if (s->device != h->device) return fail(SK_EINVAL, "sketch and Hessian live on different devices");
+  if (s->layers.size() != h->n.size()) return fail(SK_EINVAL, "sketch and Hessian have different layer lists");
+  for (size_t l = 0; l < h->n.size(); ++l) {
+    if (s->layers[l].n != h->n[l]) return fail(SK_EINVAL, "layer " + std::to_string(l) + " differs in size");
+    if (!theta0[l]) return fail(SK_EINVAL, "theta0[" + std::to_string(l) + "] is NULL");
+  }
+  DeviceGuard guard(h->device);
+  hipStream_t st = (hipStream_t)stream;
+  const int nl = (int)h->n.size();
+  float *omega = work, *r = work + D, *p = work + 2 * D, *q = work + 3 * D, *g0 = work + 4 * D, *w = work + 5 * D;
+  double *scal = reinterpret_cast<double *>(work + 6 * D);
+  // L0 = 1/2 theta0 . H theta0 and g0 = S H theta0 (H theta0 into the Y workspace)
+  if (h->user_ev_pending && hipEventSynchronize(h->user_ev) != hipSuccess)
+    return fail(SK_EHIP, "hipEventSynchronize failed");
+  for (int l = 0; l < nl; ++l)
+    h->h_user_tab[l] = HvpLayerPtr{theta0[l], (float *)h->ysk[l], h->n[l]};
+  if (hipMemcpyAsync(h->d_user_tab, h->h_user_tab, sizeof(HvpLayerPtr) * nl, hipMemcpyHostToDevice, st) !=
+          hipSuccess ||
+      hipEventRecord(h->user_ev, st) != hipSuccess)
+    return fail(SK_EHIP, "upload of the layer table failed");
+  h->user_ev_pending = true;
+  hvp_run(h, h->d_user_tab, 1, st);
+  hipLaunchKernelGGL(k_tab_dot, dim3((unsigned)h->items.size()), dim3(256), 0, st, h->d_items, h->d_user_tab,
+                     h->d_part);
+  hipLaunchKernelGGL(k_sum_f64, dim3(1), dim3(256), 0, st, h->d_part, (int64_t)h->items.size(), 0.5,
+                     scal + kIdL0);
+  int rc = sketch_apply(s, h->ysk.data(), SK_F32, 1, g0, 0, nl, 0, stream);
+  if (rc != SK_OK) return rc;
+  launch_fill_zero(omega, D, st);
+  launch_fill_zero(w, D, st);  // S H S^T omega at omega = 0
+  double tau_old = 0.0;
+  int64_t d = d_min;
+  res->d = 0;
+  res->status = 2;
+  res->rounds = 0;
+  res->L0 = 0.0;
+  for (int k = 0; k < max_rounds; ++k) {
+    hipLaunchKernelGGL(k_cg_start, dim3(1), dim3(1024), 0, st, g0, w, r, p, d, D, scal);
+    for (int i = 0; i < c; ++i) {
+      rc = sketch_hvp(s, h, p, 1, q, stream);
+      if (rc != SK_OK) return rc;
+      hipLaunchKernelGGL(k_cg_step, dim3(1), dim3(1024), 0, st, omega, r, p, q, d, scal);
+    }
+    rc = sketch_hvp(s, h, omega, 1, w, stream);
+    if (rc != SK_OK) return rc;
+    hipLaunchKernelGGL(k_id_eval, dim3(1), dim3(1024), 0, st, g0, w, omega, D, scal);
+    double hs[4];
+    if (hipMemcpyAsync(hs, scal, sizeof(hs), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return fail(SK_EHIP, "reading the metric back failed");
+    const double tau = hs[kIdTau];
+    res->L0 = hs[kIdL0];
+    res->rounds = k + 1;
+    if (tau_trace) tau_trace[k] = tau;
+    if (d_trace) d_trace[k] = d;
+    if (tau >= (double)tau_target) {
+      res->d = d;
+      res->status = 0;
+      return SK_OK;
+    }
+    if (tau - tau_old < (double)delta) {
+      d *= 2;
+      if (d > D) {
+        res->status = 1;
+        return SK_OK;
+      }
+    }
+    tau_old = tau;
   }
   return SK_OK;
 }

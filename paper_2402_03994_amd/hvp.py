@@ -152,3 +152,31 @@ def ritz_values(Hbar: torch.Tensor) -> np.ndarray:
     k = h.shape[1]
     ev = np.linalg.eigvals(h[:k, :k])
     return ev[np.argsort(-ev.real)]
+
+
+def id_search(sk: Sketch, hess: SyntheticHessian, theta0: Sequence[torch.Tensor], d_min: int, tau_target: float,
+              delta: float, c: int, max_rounds: int, work: Optional[torch.Tensor] = None) -> dict:
+    """Intrinsic-dimension search (Sec. 4) on L(theta) = 1/2 theta^T H theta over theta0 + S^T omega:
+    rounds of c conjugate-gradient steps on omega[:d], d doubled when a round improves
+    tau = 1 - L/L(theta0) by less than delta, stop at tau >= tau_target.  theta0: per layer float32
+    [numel] on the device.  Returns dict(d, status, rounds, L0, taus, ds, omega)."""
+    theta0 = list(theta0)
+    for t, n in zip(theta0, hess.numels):
+        if t.dtype != torch.float32 or t.device != sk.device or not t.is_contiguous() or t.numel() != n:
+            raise ValueError(f"theta0 tensors must be contiguous float32 with {n} entries on {sk.device}")
+    nw = int(sk.lib.sketch_id_search_work_floats(sk.D))
+    if work is None:
+        work = torch.empty(nw, dtype=torch.float32, device=sk.device)
+    if work.dtype != torch.float32 or work.numel() < nw or work.device != sk.device:
+        raise ValueError("work too small")
+    taus = np.zeros(max_rounds, dtype=np.float64)
+    ds = np.zeros(max_rounds, dtype=np.int64)
+    res = _lib.IdResult()
+    tp = (ctypes.c_void_p * len(theta0))(*[t.data_ptr() for t in theta0])
+    _lib.check(sk.lib.sketch_id_search(sk._h, hess._h, tp, int(d_min), float(tau_target), float(delta), int(c),
+                                       int(max_rounds), work.data_ptr(), taus.ctypes.data_as(ctypes.c_void_p),
+                                       ds.ctypes.data_as(ctypes.c_void_p), ctypes.byref(res),
+                                       _stream_ptr(sk.device)))
+    k = res.rounds
+    return dict(d=int(res.d), status=int(res.status), rounds=k, L0=float(res.L0), taus=taus[:k].tolist(),
+                ds=ds[:k].tolist(), omega=work[:sk.D])

@@ -100,3 +100,11 @@ def test_hvp_entry_points_reject_invalid_arguments():
     assert L.sketch_arnoldi_work_floats(0, 4) == 0
     assert L.sketch_arnoldi_work_floats(4096, 10) == 2 * 12 + 12 + 4
     L.sk_hvp_destroy(None)  # no-op
+
+
+def test_id_search_rejects_invalid_arguments():
+    L = _lib.load()
+    res = _lib.IdResult()
+    assert L.sketch_id_search(None, None, None, 1, 0.9, 0.05, 4, 4, None, None, None, ctypes.byref(res), None) == -1
+    assert L.sketch_id_search_work_floats(0) == 0
+    assert L.sketch_id_search_work_floats(1024) == 6 * 1024 + 32

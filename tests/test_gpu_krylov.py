@@ -210,3 +210,41 @@ def test_sketched_hvp_full_size_gpt2_small(dev):
     Hg = Hb.cpu().double().numpy()
     assert abs(Hg[0, 0] - h00) < 1e-5 * abs(aq).max() * np.sqrt(D)
     assert abs(Hg[1, 0] - h10) < 1e-5 * h10
+
+
+# --- intrinsic-dimension search (Sec. 4) --------------------------------------------------------
+ID_CASES = [
+    # kind, shapes, D, seed, rank, lambdas, shift, hessian seed, d_min, tau_target, c, delta, max_rounds
+    ("afjl", [(1, 3000), (20, 250)], 256, 3, 4, [1, 1, 1, 1], 0.0, 9, 1, 0.9, 6, 0.05, 12),
+    ("affd", [(64, 512), (1, 4000), (30, 300)], 1024, 5, 8, [8, 6, 5, 4, 3, 2.5, 2, 1.5], 2.0 ** -12, 21, 1, 0.9,
+     8, 0.02, 16),
+    ("ffd", [(1, 100_000), (7, 333)], 4096, 7, 8, [8, 6, 5, 4, 3, 2.5, 2, 1.5], 2.0 ** -10, 22, 2, 0.9, 8, 0.02,
+     16),
+    ("afjl", [(1, 300), (20, 40)], 16, 3, 8, [1] * 8, 0.0, 9, 4, 0.999999, 2, 0.5, 20),  # D exceeded
+]
+
+
+@pytest.mark.parametrize("case", range(len(ID_CASES)))
+def test_id_search_matches_oracle(dev, case):
+    """The search's decisions (d per round, the estimate, the status) equal the oracle's, every round's metric
+    agrees to 1e-4, and the frozen coordinates of omega stay exactly zero.  The cases keep every decision
+    at least 6e-3 away from its threshold in the oracle, far above the fp32 error of the metric."""
+    from paper_2402_03994_amd import Sketch, SyntheticHessian, id_search
+    kind, shapes, D, seed, rank, lam, shift, hseed, d_min, tau_t, c, delta, rounds = ID_CASES[case]
+    lam = np.asarray(lam, dtype=np.float32)
+    hp = dict(rank=rank, lambdas=lam, shift=shift, seed=hseed)
+    g = np.random.default_rng(0)
+    x = [g.standard_normal((1, a * b)) for a, b in shapes]
+    th0 = [t[0] for t in K.hvp(shapes, xs=x, **dict(hp, shift=0.0, lambdas=np.ones(rank, dtype=np.float32)))]
+    th0_32 = [t.astype(np.float32) for t in th0]
+    ref = K.id_search(kind, shapes, D, seed, hp, [t.astype(np.float64) for t in th0_32], d_min, tau_t, c, delta,
+                      rounds)
+    sk = Sketch(kind, shapes, D, seed, device=dev)
+    H = SyntheticHessian(shapes, rank, lam, shift, hseed, device=dev)
+    got = id_search(sk, H, [torch.tensor(t, device=dev) for t in th0_32], d_min, tau_t, delta, c, rounds)
+    assert got["status"] == ref["status"] and got["d"] == ref["d"]
+    assert got["ds"] == ref["ds"]
+    assert np.abs(np.array(got["taus"]) - np.array(ref["taus"])).max() < 1e-4
+    assert abs(got["L0"] - ref["L0"]) < 1e-5 * ref["L0"]
+    om = got["omega"].cpu().numpy()
+    assert np.all(om[ref["ds"][-1]:] == 0.0)
