@@ -5,9 +5,9 @@ Default workload (--config c2): per-example gradients shaped like GPT-2 small
 (148 tensors, N = 124,439,808), fp32 entries N(0, 1e-4), batch 64, sketched to
 D = 2^16 by AFJL and by AFFD (seed 1).  One step sketches the whole batch with
 both kinds; inputs are resident in HBM before the timed region.  Other
-workloads (--config c1|c3|c4|c5|c6|c7|c8) are described in workloads.py; c8 times
-Arnoldi on the sketched HVP operator (a step = 64 Krylov steps).  Prints one
-JSON line.
+workloads (--config c1|c3|c4|c5|c6|c7|c8|c9) are described in workloads.py; c8 times
+Arnoldi on the sketched HVP operator (a step = 64 Krylov steps), c9 one whole
+intrinsic-dimension search.  Prints one JSON line.
 
 "value" is parameter-space bytes per second: gradient bytes read by forward
 sketches plus parameter-vector bytes written by transposes, summed over the
@@ -218,6 +218,17 @@ def cpu_baseline(cfg: str):
         nbytes = len(c["kinds"]) * sum(r * cc for r, cc in sub) * 4
         sample = f"1 of {c['batch']} rows, one transformer block (12 of {len(shapes)} tensors), AFJLQ+QKH, " \
                  "factor generation included"
+    elif cfg == "c9":
+        from oracle import krylov as K
+
+        lam = np.array(W.C9_LAMBDAS, dtype=np.float32)
+        hp = dict(rank=len(lam), lambdas=lam, shift=0.0, seed=W.C9_HSEED)
+        v = rng.standard_normal((1, D))
+        sub = [(1, 1 << 25)]  # the first 2^25 of the 1e8 entries: 32 of the 96 live FFD blocks
+        K.sketched_hvp(c["kinds"][0], sub, D, seed, hp, v)
+        nbytes = 2 * sub[0][1] * 4
+        sample = "one conjugate-gradient step of the search on the first 2^25 entries: S H S^T p (FFD transpose, " \
+                 "rank-8 Hessian, FFD as three fp32 parts of the fp64 HVP)"
     elif cfg == "c8":
         from oracle import krylov as K
 
@@ -316,6 +327,27 @@ def build_step(cfg: str, dev):
         return sks, step, 2 * B * n * 4, B, \
             ("FFD on one 1e8-entry vector (padded to 2^27), D=2^20, batch 4: theta0 + S^T z (z ~ N(0,1)) and "
              "S x for Student-t(3) x")
+
+    if cfg == "c9":
+        from paper_2402_03994_amd import id_search
+
+        H, _, theta0 = W.c9_problem(dev)
+        work = torch.empty(int(sks[c["kinds"][0]].lib.sketch_id_search_work_floats(D)), device=dev)
+        sks["hvp"] = H
+        box = {}
+        sks["_result"] = box
+
+        def step(ev):
+            def run():
+                box["r"] = id_search(sks[c["kinds"][0]], H, theta0, c["d_min"], c["tau_target"], c["delta"],
+                                     c["cg_steps"], c["max_rounds"], work=work)
+            ev(c["kinds"][0], "id_search", run)
+        # parameter-space bytes per sketched HVP (S^T written, S read); the count per search is known after
+        # the first run (rounds x (cg_steps + 1) + the gradient at theta0)
+        return sks, step, 0, 1, \
+            (f"intrinsic-dimension search: FFD on a 1e8-entry vector (padded to 2^27), D_max = 2^20, quadratic "
+             f"1/2 theta^T H theta with H a rank-8 synthetic Hessian, theta0 in its span; from d = {c['d_min']}, "
+             f"{c['cg_steps']} CG steps per round, tau_target {c['tau_target']}, delta {c['delta']}")
 
     if cfg == "c8":
         from paper_2402_03994_amd import arnoldi
@@ -433,6 +465,11 @@ def main() -> int:
     sks[dom_kind].profile(False)
 
     ms = (t1 - t0) * 1e3 / args.steps
+    if cfg == "c9":
+        r = result["r"]
+        c = W.CONFIGS[cfg]
+        hvps = r["rounds"] * (c["cg_steps"] + 1)  # the sketched HVPs of the search (+ the gradient at theta0)
+        pbytes = (2 * hvps + 1) * c["shapes"][0][0] * c["shapes"][0][1] * 4
     value = pbytes / (ms * 1e-3) / 1e9
     call_ms = {k: round(sum(a.elapsed_time(b) for a, b in v) / ncal, 3) for k, v in per_call.items()}
     achieved = by_dom / (t_dom * 1e-3) / 1e9 if t_dom > 0 else 0.0
@@ -471,6 +508,12 @@ def main() -> int:
         "roofline": roofline,
         "source_hash": source_hash(),
     }
+    if cfg == "c9":
+        r = result["r"]
+        line.pop("vectors_per_s")
+        line["searches_per_s"] = round(1e3 / ms, 2)
+        line["search"] = {"d": r["d"], "status": r["status"], "rounds": r["rounds"], "ds": r["ds"],
+                          "taus": [round(t, 4) for t in r["taus"]]}
     if cfg == "c8":
         from paper_2402_03994_amd import ritz_values
 

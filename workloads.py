@@ -75,12 +75,20 @@ CONFIGS = {
     # sketched Hessian eigenvalues: Arnoldi (64 steps) on v -> S H S^T v, GPT-2-small parameters, a
     # synthetic rank-16 spiked Hessian (c8_hessian), AFJL sketch to D = 2^16
     "c8": dict(kinds=("afjl",), shapes=gpt2_small_shapes(), D=1 << 16, batch=1, seed=1, dtype="f32", krylov=64),
+    # intrinsic-dimension search: FFD on C4's 1e8-entry vector (padded to 2^27), D_max = 2^20, on the
+    # quadratic 1/2 theta^T H theta of a rank-8 synthetic Hessian (c9_problem)
+    "c9": dict(kinds=("ffd",), shapes=[(1, 100_000_000)], D=1 << 20, batch=1, seed=0, dtype="f32", d_min=2,
+               tau_target=0.9, delta=0.02, cg_steps=8, max_rounds=16),
 }
+# the objective of c9: 8 spikes, no bulk; theta0 = V V^T x (x ~ N(0, 1)) lies in their span
+C9_LAMBDAS = (8.0, 6.0, 5.0, 4.0, 3.0, 2.5, 2.0, 1.5)
+C9_HSEED = 99
 # the synthetic Hessian of c8: 14 positive outliers, 2 negative ones, a flat bulk of 1e-5
 C8_LAMBDAS = (20.0, 15.0, 11.0, 8.5, 6.5, 5.0, 4.0, 3.0, 2.5, 2.0, 1.6, 1.3, 1.1, 1.0, -3.0, -1.5)
 C8_SHIFT = 1e-5
 C8_HSEED = 4242
-INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001, "c8": 1008}
+INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001, "c8": 1008,
+              "c9": 1009}
 # variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
 GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4, "c7": 1.0}
 
@@ -128,3 +136,21 @@ def c8_hessian(device):
     lam = np.array(C8_LAMBDAS, dtype=np.float32)
     H = SyntheticHessian(CONFIGS["c8"]["shapes"], len(lam), lam, C8_SHIFT, C8_HSEED, max_batch=1, device=device)
     return H, dict(rank=len(lam), lambdas=lam, shift=float(np.float32(C8_SHIFT)), seed=C8_HSEED)
+
+
+def c9_problem(device):
+    """The objective's Hessian of c9 on `device`, its parameters as the oracle takes them, and theta0
+    = V V^T x with x ~ N(0, 1) seeded (built with a unit-weight Hessian on the same sign vectors)."""
+    import numpy as np
+
+    from paper_2402_03994_amd import SyntheticHessian
+
+    shapes = CONFIGS["c9"]["shapes"]
+    lam = np.array(C9_LAMBDAS, dtype=np.float32)
+    H = SyntheticHessian(shapes, len(lam), lam, 0.0, C9_HSEED, device=device)
+    unit = SyntheticHessian(shapes, len(lam), np.ones(len(lam), dtype=np.float32), 0.0, C9_HSEED, device=device)
+    gen = generator("c9", device)
+    x = torch.randn((1, shapes[0][0] * shapes[0][1]), generator=gen, device=device)
+    theta0 = unit.apply([x])[0].reshape(-1)
+    unit.close()
+    return H, dict(rank=len(lam), lambdas=lam, shift=0.0, seed=C9_HSEED), [theta0]
