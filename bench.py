@@ -45,7 +45,7 @@ MFMA_F32_PEAK_TFLOPS = 157.3
 # kernel launched by each single-kernel profile class (the rocprofv3 name)
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
              "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
-             "fjl:prolog": "k_fjl_prolog", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
+             "fjl:prolog": "k_fjl_pass0", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
              "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
              "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
              "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T"}

@@ -733,8 +733,11 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
       case SK_FJL:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
-          SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_prolog(s, l, grads[l - l0], dtype, b0, bc, s->ws, st));
-          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+          {
+            const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the signed load
+            SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_pass0(s, l, grads[l - l0], dtype, b0, bc, s->ws, lgw, st));
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from(s->ws, bc, ld.lgnp, lgw, st));
+          }
           SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
                   launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st));
         }

@@ -48,9 +48,12 @@ __global__ __launch_bounds__(256) void k_fwht_pass(float *data, int lgn, int lo,
   for (int e = threadIdx.x; e < total; e += 256) base[((int64_t)(e >> lgcs) << lo) + (e & cmask)] = s[p16(e)] * scale;
 }
 
-void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) {
+void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) { fwht_inplace_from(data, V, lgn, 0, st); }
+
+// The passes of fwht_inplace from index bit lo0 on (bits below lo0 already transformed).
+void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st) {
   if (lgn == 0 || V == 0) return;
-  int lo = 0;
+  int lo = lo0;
   while (lo < lgn) {
     int w, lgcs;
     if (lo == 0) {
@@ -1055,32 +1058,58 @@ void launch_affd_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_
 // ===========================================================================
 // FJL: w = B x zero-padded, H_N' (generic passes), y_i = sqrt(N'/D) g_i w[idx_i].
 // ===========================================================================
+// FJL forward, first transform pass fused with the signed load: one workgroup per
+// (vector, tile of 2^w coordinates of N'), w = min(log2 N', 13); the tile's sign
+// words (one Philox block per 128 coordinates) are built in LDS, the signed
+// inputs (zeros past n) transformed over bits [0, w) in LDS and written to the
+// workspace [vector][N'] with the pass scale.  The remaining bits go through
+// fwht_inplace_from(w).
 template <bool BF16>
-__global__ void k_fjl_prolog(const LayerDesc *__restrict__ layers, int layer, const void *__restrict__ x,
-                             int64_t b_begin, int64_t bc, float *__restrict__ w, Key key) {
+__global__ __launch_bounds__(256) void k_fjl_pass0(const LayerDesc *__restrict__ layers, int layer,
+                                                   const void *__restrict__ x, int w, int64_t b_begin,
+                                                   float *__restrict__ out, float scale, Key key) {
+  extern __shared__ float sm[];
   const LayerDesc &ld = layers[layer];
-  const int64_t j0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
-  if (j0 >= ld.np) return;
-  const int64_t lim = ld.n - j0;
-  uint32_t bits = 0;
-  if (lim > 0) bits = sign_word((uint64_t)j0, (uint32_t)ld.layer_id, key) >> (j0 & 31);
-  for (int64_t v = 0; v < bc; ++v) {
-    float val[4] = {0.f, 0.f, 0.f, 0.f};
-    if (lim > 0) load4<BF16, false>(x, (b_begin + v) * ld.n + j0, lim, val);
-    float4 o = make_float4(flip(val[0], bits & 1u), flip(val[1], (bits >> 1) & 1u), flip(val[2], (bits >> 2) & 1u),
-                           flip(val[3], (bits >> 3) & 1u));
-    *(float4 *)(w + v * ld.np + j0) = o;
+  const int T = 1 << w;
+  float *s = sm;
+  uint32_t *sgn = reinterpret_cast<uint32_t *>(sm + ((p16_floats(T) + 3) & ~3));  // 16-byte aligned
+  const int64_t tiles = ld.np >> w;
+  const int64_t v = blockIdx.x / tiles;
+  const int64_t base = (blockIdx.x - v * tiles) << w;
+  const int nblk = (T + 127) >> 7;  // T >= 16: base is a multiple of T
+  if ((int)threadIdx.x < nblk && base + 128 * (int64_t)threadIdx.x < ld.n) {
+    const W4 wd = philox(((uint64_t)base >> 7) + threadIdx.x, (uint32_t)ld.layer_id, ST_SIGN, key);
+    *reinterpret_cast<uint4 *>(&sgn[4 * threadIdx.x]) = make_uint4(wd.w[0], wd.w[1], wd.w[2], wd.w[3]);
   }
+  __syncthreads();
+  const int64_t row = (b_begin + v) * ld.n;
+  for (int e = threadIdx.x; e < T; e += 256) {
+    const int64_t j = base + e;
+    float val = 0.0f;
+    if (j < ld.n) {
+      const float xv = BF16 ? bf16_to_f32(((const uint16_t *)x)[row + j]) : ((const float *)x)[row + j];
+      // base is 128-aligned when T >= 128; smaller tiles are the whole vector (base = 0)
+      val = flip(xv, (sgn[((int64_t)e >> 5)] >> (j & 31)) & 1u);
+    }
+    s[p16(e)] = val;
+  }
+  lds_fwht_regs(s, w, 0);
+  float *o = out + v * ld.np + base;
+  for (int e = threadIdx.x; e < T; e += 256) o[e] = s[p16(e)] * scale;
 }
 
-void launch_fjl_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                       float *w, hipStream_t st) {
+void launch_fjl_pass0(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *w,
+                      int lgw, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
-  dim3 grid((unsigned)((ld.np / 4 + 255) / 256));
+  const int64_t tiles = bc * (ld.np >> lgw);
+  const size_t shm = sizeof(float) * ((p16_floats(1 << lgw) + 3) & ~3) + sizeof(uint32_t) * ((((1 << lgw) + 127) >> 7) * 4);
+  const float scale = (float)(1.0 / std::sqrt((double)(1ll << lgw)));
   if (dtype == SK_BF16)
-    hipLaunchKernelGGL(k_fjl_prolog<true>, grid, dim3(256), 0, st, s->d_layers, layer, x, b_begin, bc, w, s->key);
+    hipLaunchKernelGGL(k_fjl_pass0<true>, dim3((unsigned)tiles), dim3(256), shm, st, s->d_layers, layer, x, lgw,
+                       b_begin, w, scale, s->key);
   else
-    hipLaunchKernelGGL(k_fjl_prolog<false>, grid, dim3(256), 0, st, s->d_layers, layer, x, b_begin, bc, w, s->key);
+    hipLaunchKernelGGL(k_fjl_pass0<false>, dim3((unsigned)tiles), dim3(256), shm, st, s->d_layers, layer, x, lgw,
+                       b_begin, w, scale, s->key);
   SK_CHECK_LAUNCH();
 }
 

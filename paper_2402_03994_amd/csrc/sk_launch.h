@@ -8,6 +8,12 @@ namespace sk {
 // Generic in-place normalised Walsh-Hadamard transform of V contiguous
 // vectors of length 2^lgn, as a sequence of LDS-tiled passes.
 void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st);
+// The passes of fwht_inplace from index bit lo0 on (the first pass of fwht_inplace covers bits
+// [0, min(lgn, 13)), so lo0 = min(lgn, 13) continues after a fused first pass).
+void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st);
+// FJL forward: signed load fused with the transform over index bits [0, lgw) (lgw = min(log2 N', 13)).
+void launch_fjl_pass0(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *w,
+                      int lgw, hipStream_t st);
 
 void launch_fill_zero(float *p, int64_t n, hipStream_t st);
 
@@ -138,8 +144,6 @@ void launch_affd_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_
                        int out_dtype, const float *theta0, hipStream_t st);
 
 // ---- FJL ----
-void launch_fjl_prolog(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                       float *w, hipStream_t st);
 void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
                        bool accumulate, hipStream_t st);
 void launch_fjl_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,

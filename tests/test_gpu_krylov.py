@@ -248,3 +248,20 @@ def test_id_search_matches_oracle(dev, case):
     assert abs(got["L0"] - ref["L0"]) < 1e-5 * ref["L0"]
     om = got["omega"].cpu().numpy()
     assert np.all(om[ref["ds"][-1]:] == 0.0)
+
+
+def test_id_search_full_size_known_answer(dev):
+    """The benchmark's search (FFD on a 1e8-entry vector, D_max = 2^20, rank-8 quadratic without bulk,
+    theta0 in the span of the spikes): a subspace of d >= 8 free coordinates removes the whole loss, so the
+    search from d = 2 must end at d = 8 with tau near 1 (8 fp32 CG steps on the 8 x 8 reduced system: exact in
+    exact arithmetic, 0.997 measured), d = 2 and 4 leaving most of it."""
+    import workloads as W
+    from paper_2402_03994_amd import Sketch, id_search
+    c = W.CONFIGS["c9"]
+    sk = Sketch("ffd", c["shapes"], c["D"], c["seed"], device=dev)
+    H, _, theta0 = W.c9_problem(dev)
+    r = id_search(sk, H, theta0, c["d_min"], c["tau_target"], c["delta"], c["cg_steps"], c["max_rounds"])
+    assert r["status"] == 0 and r["d"] == 8
+    assert r["taus"][-1] > 0.99
+    assert all(t < 0.9 for t in r["taus"][:-1])
+    assert torch.all(r["omega"][8:] == 0)
