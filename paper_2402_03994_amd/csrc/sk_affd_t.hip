@@ -503,10 +503,16 @@ __global__ __launch_bounds__(256, 3) void k_affdT_topM(const LayerDesc *__restri
     int64_t l, v0;
     int nv;
   };
+  // item -> (column l, vector group): it = ((l / 8) ngroups + group) 8 + l % 8, so the vector groups of
+  // a column fall on workgroups 8 apart, i.e. on one XCD (workgroups are dealt to the 8 XCDs in turn and
+  // the grid is a multiple of 8), and read that column's M rows from the XCD's L2
+  const int64_t ngroups = (bc + 7) / 8;
   auto open = [&](int64_t it) {
     Item r;
-    r.l = it & 1023;
-    r.v0 = (it >> 10) * 8;
+    const int64_t q = it >> 3;
+    const int64_t grp = q % ngroups;
+    r.l = ((q / ngroups) << 3) | (it & 7);
+    r.v0 = grp * 8;
     r.nv = (int)((bc - r.v0) < 8 ? (bc - r.v0) : 8);
     return r;
   };
