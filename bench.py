@@ -84,12 +84,24 @@ def qh_flops(kind, shapes, D):
     return {"qh_first": first, "qh_second": second, "qh_t": trans}
 
 
-def source_hash() -> str:
+# kernel sources behind each kind (the shared headers and the dispatcher are hashed for every config)
+_COMMON_SRC = ("sk_api.hip", "sk_internal.h", "sk_launch.h", "sk_kcommon.h", "sk_device.h")
+_KIND_SRC = {"fjl": ("sk_fwht.hip",), "ffd": ("sk_fwht.hip", "sk_ffd_l.hip"), "afjl": ("sk_fwht.hip",),
+             "affd": ("sk_fwht.hip", "sk_affd.hip", "sk_affd_s.hip", "sk_affd_t.hip"), "qk": ("sk_qk.hip",),
+             "qkh": ("sk_qhaar.hip",), "afjlq": ("sk_qhaar.hip",), "affdq": ("sk_qhaar.hip",)}
+
+
+def source_hash(cfg: str) -> str:
+    """Hash of the kernel sources a workload runs: counter records taken on other sources are stale."""
+    files = set(_COMMON_SRC)
+    for k in W.CONFIGS[cfg]["kinds"]:
+        files.update(_KIND_SRC[k])
+    if cfg in ("c8", "c9"):
+        files.add("sk_hvp.hip")
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2402_03994_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    for f in sorted(files):
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -99,7 +111,7 @@ def measured_traffic(cfg: str, kclass: str):
     if not os.path.exists(p):
         return None
     rec = json.load(open(p))
-    if rec.get("source_hash") != source_hash():
+    if rec.get("source_hash") != source_hash(cfg):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -143,7 +155,7 @@ def traffic_json(cfg: str, kclass: str, fetch_csv: str, write_csv: str, copy_fet
     cw_kib, _ = _counter_per_launch(copy_write_csv, "copy", "WRITE_SIZE")
     ref_kib = (1 << 30) / 1024
     cal_f, cal_w = ref_kib / cf_kib, ref_kib / cw_kib
-    rec = {"config": cfg, "class": kclass, "kernel": kname, "source_hash": source_hash(),
+    rec = {"config": cfg, "class": kclass, "kernel": kname, "source_hash": source_hash(cfg),
            "fetch_kib_per_launch": round(f_kib, 1), "write_kib_per_launch": round(w_kib, 1), "launches": nf,
            "copy_fetch_kib_per_gib": round(cf_kib, 1), "copy_write_kib_per_gib": round(cw_kib, 1),
            "fetch_scale": round(cal_f, 4), "write_scale": round(cal_w, 4),
@@ -506,7 +518,7 @@ def main() -> int:
         "per_call_ms": call_ms,
         "kernel_classes_ms_per_step": {c: round(v[0] / ncal, 3) for c, v in sorted(classes.items())},
         "roofline": roofline,
-        "source_hash": source_hash(),
+        "source_hash": source_hash(cfg),
     }
     if cfg == "c9":
         r = result["r"]
