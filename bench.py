@@ -412,7 +412,7 @@ def main() -> int:
         return traffic_json(args.config, *args.traffic_json)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the sketch shards by "
-              "batch or by layer groups with one all-reduce of [batch, D]; see DESIGN.md)", file=sys.stderr)
+              "batch or by layer groups with one all-reduce of [batch, D])", file=sys.stderr)
         return 2
 
     import numpy as np

@@ -232,10 +232,10 @@ def id_search(kind: str, shapes, D: int, seed: int, hp: dict, theta0, d_min: int
         tau = 1.0 - L / L0
         taus.append(tau)
         ds.append(d)
-        verdict, d_next = id_decide(tau, tau_old, d, tau_target, delta, D)
-        if verdict == "done":
+        decision, d_next = id_decide(tau, tau_old, d, tau_target, delta, D)
+        if decision == "done":
             return dict(d=d, status=0, taus=taus, ds=ds, omega=omega, L0=L0)
-        if verdict == "fail":
+        if decision == "fail":
             return dict(d=0, status=1, taus=taus, ds=ds, omega=omega, L0=L0)
         d, tau_old = d_next, tau
     return dict(d=0, status=2, taus=taus, ds=ds, omega=omega, L0=L0)
