@@ -411,7 +411,7 @@ def main() -> int:
     if args.traffic_json:
         return traffic_json(args.config, *args.traffic_json)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the sketch shards by "
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the sketch shards by "
               "batch or by layer groups with one all-reduce of [batch, D])", file=sys.stderr)
         return 2
 
