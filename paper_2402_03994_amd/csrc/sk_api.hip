@@ -69,6 +69,7 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_pos);
   f(s->d_fjl_seg);
   f(s->d_fjl_smp);
+  f(s->d_fjl_toff);
   f(s->d_qka);
   f(s->d_qkb);
   f(s->d_qkah);
@@ -354,9 +355,10 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
 
   // FJL transpose: samples grouped by position (deterministic order).
-  std::vector<uint32_t> fpos, fseg, fsmp;
+  std::vector<uint32_t> fpos, fseg, fsmp, ftoff;
   if (kind == SK_FJL) {
     s->fjl_uoff.assign(n_layers + 1, 0);
+    s->fjl_toff_at.assign(n_layers, 0);
     std::vector<std::pair<uint32_t, uint32_t>> v(D);
     for (int l = 0; l < n_layers; ++l) {
       const LayerDesc &ld = s->layers[l];
@@ -372,6 +374,16 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       }
       fseg.push_back(base + (uint32_t)D);  // sentinel
       s->fjl_uoff[l + 1] = (int64_t)fpos.size();
+      // tile table of the fused transpose pass: the layer's unique positions in tile t are
+      // [ftoff[at + t], ftoff[at + t + 1]) (indices relative to the layer's first one)
+      const int lgw = std::min(ld.lgnp, 13);
+      const int64_t tiles = ld.np >> lgw, u0 = s->fjl_uoff[l];
+      s->fjl_toff_at[l] = (int64_t)ftoff.size();
+      int64_t u = u0;
+      for (int64_t t = 0; t <= tiles; ++t) {
+        while (u < s->fjl_uoff[l + 1] && ((int64_t)fpos[u] >> lgw) < t) ++u;
+        ftoff.push_back((uint32_t)(u - u0));
+      }
     }
   }
 
@@ -419,6 +431,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_fjl_pos, sizeof(uint32_t) * fpos.size()));
   SK_TRY(alloc((void **)&s->d_fjl_seg, sizeof(uint32_t) * fseg.size()));
   SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_toff, sizeof(uint32_t) * ftoff.size()));
   SK_TRY(alloc((void **)&s->d_qka, sizeof(float) * fac_a));
   SK_TRY(alloc((void **)&s->d_qkb, sizeof(uint16_t) * 2 * fac_b));
   SK_TRY(alloc((void **)&s->d_qkah, sizeof(uint16_t) * 2 * fac_a));
@@ -438,6 +451,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(h2d(s->d_fjl_pos, fpos.data(), sizeof(uint32_t) * fpos.size()));
   SK_TRY(h2d(s->d_fjl_seg, fseg.data(), sizeof(uint32_t) * fseg.size()));
   SK_TRY(h2d(s->d_fjl_smp, fsmp.data(), sizeof(uint32_t) * fsmp.size()));
+  SK_TRY(h2d(s->d_fjl_toff, ftoff.data(), sizeof(uint32_t) * ftoff.size()));
 
   // workspace: room for up to 256 vectors of the largest per-vector need
   const int64_t pv = std::max(per_vector_bytes(s, 0, n_layers, false), per_vector_bytes(s, 0, n_layers, true));
@@ -881,16 +895,15 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
           SK_PROF(SK_PROF_GATHER, obytes, launch_affd_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st));
           break;
-        case SK_FJL:
-          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, {
-            launch_fill_zero(s->ws, bc * ld.np, st);
-            launch_fjl_T_scatter(s, l, z, b0, bc, s->ws, st);
-          });
-          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, bc, ld.lgnp, st));
+        case SK_FJL: {
+          const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the scatter
+          SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_fjl_T_pass0(s, l, z, b0, bc, s->ws, lgw, st));
+          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from(s->ws, bc, ld.lgnp, lgw, st));
           SK_PROF(SK_PROF_GATHER, obytes,
                   launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th,
                                     (float)std::sqrt((double)ld.np / (double)s->D), st));
           break;
+        }
         case SK_FFD:
           if (lgD <= kFfdSmallMax) {
             SK_PROF(SK_PROF_FFD_T, obytes + bc * s->D * 4,

@@ -1135,32 +1135,55 @@ void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_
   SK_CHECK_LAUNCH();
 }
 
-// FJL transpose: w[pos] = sum over the samples at pos (in id order) of g_i z_i.
-__global__ void k_fjl_T_scatter(const float *__restrict__ gtab, int layer, const uint32_t *__restrict__ pos,
-                                const uint32_t *__restrict__ seg, const uint32_t *__restrict__ smp, int64_t nuniq,
-                                int64_t np, const float *__restrict__ z, int64_t D, int64_t b_begin, int64_t bc,
-                                float *__restrict__ w) {
-  const int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (u >= nuniq) return;
-  const uint32_t p = pos[u], s0 = seg[u], s1 = seg[u + 1];
+// FJL transpose, first transform pass fused with the scatter of the D samples:
+// one workgroup per (vector, tile of 2^w positions of N'), w = min(log2 N', 13).
+// The tile starts at zero in LDS; every unique sample position inside it (a
+// contiguous run of the position-sorted list, located by the tile table) gets
+// the sum of g_i z_i over its samples in id order; then bits [0, w) are
+// transformed and the tile written to the workspace [vector][N'] with the pass
+// scale.  The remaining bits go through fwht_inplace_from(w).
+__global__ __launch_bounds__(256) void k_fjl_T_pass0(const float *__restrict__ gtab, int layer,
+                                                     const uint32_t *__restrict__ pos, const uint32_t *__restrict__ seg,
+                                                     const uint32_t *__restrict__ smp,
+                                                     const uint32_t *__restrict__ toff, int64_t np, int w,
+                                                     const float *__restrict__ z, int64_t D, int64_t b_begin,
+                                                     float *__restrict__ out, float scale) {
+  extern __shared__ float sm[];
+  const int T = 1 << w;
+  const int64_t tiles = np >> w;
+  const int64_t v = blockIdx.x / tiles;
+  const int64_t t = blockIdx.x - v * tiles;
+  const int64_t base = t << w;
+  for (int e = threadIdx.x; e < T; e += 256) sm[p16(e)] = 0.0f;
+  __syncthreads();
   const float *g = gtab + (int64_t)layer * D;
-  for (int64_t v = 0; v < bc; ++v) {
+  const float *zv = z + (b_begin + v) * D;
+  const uint32_t u1 = toff[t + 1];
+  for (uint32_t u = toff[t] + threadIdx.x; u < u1; u += 256) {
     float acc = 0.0f;
-    for (uint32_t k = s0; k < s1; ++k) {
+    const uint32_t k1 = seg[u + 1];
+    for (uint32_t k = seg[u]; k < k1; ++k) {
       const uint32_t i = smp[k];
-      acc += g[i] * z[(b_begin + v) * D + i];
+      acc += g[i] * zv[i];
     }
-    w[v * np + p] = acc;
+    sm[p16((int)(pos[u] - base))] = acc;  // positions are unique: no two threads share a slot
   }
+  lds_fwht_regs(sm, w, 0);  // opens and closes with a barrier
+  float *o = out + v * np + base;
+  for (int e = threadIdx.x; e < T; e += 256) o[e] = sm[p16(e)] * scale;
 }
 
-void launch_fjl_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
-                          hipStream_t st) {
-  const int64_t u0 = s->fjl_uoff[layer], nuniq = s->fjl_uoff[layer + 1] - u0;
+void launch_fjl_T_pass0(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w, int lgw,
+                        hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const int64_t u0 = s->fjl_uoff[layer];
   const int64_t seg0 = u0 + layer;  // one sentinel per layer
-  hipLaunchKernelGGL(k_fjl_T_scatter, dim3((unsigned)((nuniq + 255) / 256)), dim3(256), 0, st, s->d_gtab, layer,
-                     s->d_fjl_pos + u0, s->d_fjl_seg + seg0, s->d_fjl_smp, nuniq, s->layers[layer].np, z, s->D,
-                     b_begin, bc, w);
+  const int64_t tiles = bc * (ld.np >> lgw);
+  const size_t shm = sizeof(float) * p16_floats(1 << lgw);
+  const float scale = (float)(1.0 / std::sqrt((double)(1ll << lgw)));
+  hipLaunchKernelGGL(k_fjl_T_pass0, dim3((unsigned)tiles), dim3(256), shm, st, s->d_gtab, layer, s->d_fjl_pos + u0,
+                     s->d_fjl_seg + seg0, s->d_fjl_smp, s->d_fjl_toff + s->fjl_toff_at[layer], ld.np, lgw, z, s->D,
+                     b_begin, w, scale);
   SK_CHECK_LAUNCH();
 }
 
@@ -1381,8 +1404,62 @@ __global__ void k_reduce_partials(const float *__restrict__ part, int64_t nslots
   *o = accumulate ? *o + acc : acc;
 }
 
+// The same sum for D % 4 == 0 and 16-byte aligned buffers, in 16-byte pieces: a
+// 1024-thread workgroup owns 32 pieces (128 consecutive outputs); lane l of wave
+// q takes piece l % 32 and sums slots k = r, r + 32, r + 64, ... with
+// r = 2 q + l / 32; the 32 residue sums are then added in the order r = 0 .. 31.
+// The order depends on nslots only (not on the batch), and nothing is atomic.
+__global__ __launch_bounds__(1024) void k_reduce_partials4(const float *__restrict__ part, int64_t nslots,
+                                                           int64_t n4, int64_t D, int64_t b_begin,
+                                                           float *__restrict__ out, int accumulate) {
+  __shared__ float4 red[32][33];
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int c = lane & 31, r = 2 * q + (lane >> 5);
+  const int64_t p = (int64_t)blockIdx.x * 32 + c;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (p < n4) {
+    const float4 *src = reinterpret_cast<const float4 *>(part) + p;
+    for (int64_t k = r; k < nslots; k += 32) {
+      const float4 a = src[k * n4];
+      acc.x += a.x;
+      acc.y += a.y;
+      acc.z += a.z;
+      acc.w += a.w;
+    }
+  }
+  red[r][c] = acc;
+  __syncthreads();
+  if (threadIdx.x < 32 && p < n4) {
+    float4 t = red[0][c];
+    for (int k = 1; k < 32; ++k) {
+      const float4 a = red[k][c];
+      t.x += a.x;
+      t.y += a.y;
+      t.z += a.z;
+      t.w += a.w;
+    }
+    const int64_t i = p * 4, v = i / D;
+    float4 *o = reinterpret_cast<float4 *>(out + (b_begin + v) * D + (i - v * D));
+    if (accumulate) {
+      const float4 a = *o;
+      t.x += a.x;
+      t.y += a.y;
+      t.z += a.z;
+      t.w += a.w;
+    }
+    *o = t;
+  }
+}
+
 void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64_t D, int64_t b_begin, float *out,
                             bool accumulate, hipStream_t st) {
+  if (D % 4 == 0 && ((uintptr_t)part & 15) == 0 && ((uintptr_t)out & 15) == 0) {
+    const int64_t n4 = bc * D / 4;
+    hipLaunchKernelGGL(k_reduce_partials4, dim3((unsigned)((n4 + 31) / 32)), dim3(1024), 0, st, part, nslots, n4, D,
+                       b_begin, out, (int)accumulate);
+    SK_CHECK_LAUNCH();
+    return;
+  }
   hipLaunchKernelGGL(k_reduce_partials, dim3((unsigned)((bc * D + 255) / 256)), dim3(256), 0, st, part, nslots, bc, D,
                      b_begin, out, (int)accumulate);
   SK_CHECK_LAUNCH();

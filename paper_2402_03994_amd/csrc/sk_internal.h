@@ -88,6 +88,8 @@ struct sk_sketch {
   uint32_t *d_fjl_pos = nullptr;   // unique positions
   uint32_t *d_fjl_seg = nullptr;   // segment starts into d_fjl_smp (per unique position, +1 sentinel per layer)
   uint32_t *d_fjl_smp = nullptr;   // sample ids sorted by (position, id)
+  std::vector<int64_t> fjl_toff_at; // per layer: offset of its tile table in d_fjl_toff
+  uint32_t *d_fjl_toff = nullptr;  // per layer and tile of 2^min(lg N', 13) positions: first unique index (+1 end)
   // QK
   float *d_qka = nullptr;       // A factors, fp32
   uint16_t *d_qkah = nullptr;   // A factors as bf16 hi terms, then bf16 lo terms (A-first contraction)

@@ -146,8 +146,8 @@ void launch_affd_T_out(const sk_sketch *s, int layer, const float *w, int64_t b_
 // ---- FJL ----
 void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
                        bool accumulate, hipStream_t st);
-void launch_fjl_T_scatter(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w,
-                          hipStream_t st);
+void launch_fjl_T_pass0(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *w, int lgw,
+                        hipStream_t st);
 void launch_signed_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
                        int out_dtype, const float *theta0, float scale, hipStream_t st);
 

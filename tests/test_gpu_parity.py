@@ -320,3 +320,36 @@ def test_ffd_small_D_vector_tiles(D, dev):
     for o, r in zip(outs, refs):
         assert rel_err(o.cpu().numpy(), r) < TOL_F32
     s.close()
+
+
+@pytest.mark.parametrize("shapes,D", [([(1, 5000), (1, 20000), (1, 9)], 16384), ([(1, 2 ** 20), (2, 3)], 16)])
+def test_fjl_transpose_tiles(shapes, D, dev):
+    """FJL transpose with the sample scatter fused into the first transform pass (a per-tile range of
+    the position-sorted sample list): D > N' (several samples per position, summed in id order), empty
+    tiles (D = 16 samples over 128 tiles of 2^13), tiny layers (N' < 16), three vectors, theta0."""
+    seed = 77 + D
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((3, D), generator=g)
+    th = [torch.randn(r * c, generator=g) * 0.02 for r, c in shapes]
+    s = sk("fjl", shapes, D, seed, dev)
+    outs = s.apply_T(z.to(dev), theta0=[t.to(dev) for t in th])
+    refs = O.apply_T("fjl", shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL_F32
+    s.close()
+
+
+def test_ffd_partials_reduction_many_slots(dev):
+    """FFD forward with D = 64 over 2^16 + 5 coordinates: 513 partial sums per output reduced in
+    16-byte pieces (32 residues per workgroup, combined in a fixed order), accumulated over two layers;
+    the result is bitwise the same in one batch and in two."""
+    shapes = [(1, 2 ** 16 + 5), (4, 33)]
+    D = 64
+    xs = rand_inputs(shapes, 6, 91)
+    s = sk("ffd", shapes, D, 91, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu()
+    ref = O.apply("ffd", shapes, D, 91, [x.numpy() for x in xs])
+    assert rel_err(y.numpy(), ref) < TOL_F32
+    y2 = torch.cat([s.apply([x[:2].to(dev) for x in xs]).cpu(), s.apply([x[2:].to(dev) for x in xs]).cpu()])
+    assert torch.equal(y, y2)
+    s.close()
