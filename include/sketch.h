@@ -136,7 +136,9 @@ enum {
  *             (D > 2^20 is SK_EUNSUPPORTED).  QK: D = sum qk_da*qk_db.
  *             SK_QKH, SK_AFJLQ, SK_AFFDQ: a power of two, 2048 <= D <= 2^20
  *             (smaller D is SK_EUNSUPPORTED by the kernels); SK_AFFDQ also
- *             needs N'_l <= 2^26 for every layer.
+ *             needs N'_l <= 2^26 for every layer.  SK_FJL needs N'_l <= 2^32
+ *             (a sample position is one 32-bit random word masked to N'_l - 1;
+ *             larger layers are SK_EUNSUPPORTED).  Every layer: rows*cols <= 2^40.
  *   seed      64-bit key of every random stream.
  *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).
  * On success *out receives the handle (destroy with sketch_destroy).  The

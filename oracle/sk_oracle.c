@@ -110,6 +110,8 @@ double orc_gauss(uint64_t seed, uint32_t layer, uint32_t stream, uint64_t j) {
 }
 
 /* FJL sample position i: word (i mod 4) of block i/4, masked to [0, Np). */
+/* FJL sample position i in [0, np): word i mod 4 of block i / 4, masked to
+ * np - 1 (np a power of two of at most 2^32, so the mask is exactly uniform). */
 uint64_t orc_index(uint64_t seed, uint32_t layer, uint64_t i, uint64_t np) {
   uint32_t w[4];
   block(seed, layer, ST_INDEX, i >> 2, w);
@@ -161,18 +163,19 @@ uint32_t orc_perm_inv(uint64_t seed, uint32_t layer, uint32_t stream, uint32_t p
   return (hi << wl) | lo;
 }
 
-/* Kronecker factor shapes of n (a power of two): repeatedly peel off a block
- * of min(n, 1024) and divide n by 1024, then list the blocks from the most
- * significant one (the remainder) to the least significant.  Returns K. */
+/* Kronecker factor shapes of n = 2^L (Sec. 3, "Removing the lookup
+ * bottleneck": H_{AB} = H_A (x) H_B with factors of at most 1024 columns).
+ * The fewest factors of at most 2^10 whose product is n: K = ceil(L / 10);
+ * every factor but the most significant is 1024, the most significant takes
+ * what is left, 2^(L - 10 (K - 1)).  dims[0] is the most significant factor
+ * (row-major digit order).  n = 1 has no factor.  Returns K. */
 int orc_kron_shapes(uint64_t n, uint64_t dims[8]) {
-  uint64_t tmp[8];
-  int k = 0;
-  while (n > 1) {
-    tmp[k++] = n < 1024 ? n : 1024;
-    n /= 1024;
-  }
-  for (int i = 0; i < k; ++i) dims[i] = tmp[k - 1 - i];
-  return k;
+  int L = 0;
+  while ((1ull << L) < n) ++L;
+  const int K = (L + 9) / 10;
+  for (int k = 0; k < K; ++k) dims[k] = 1024;
+  if (K > 0) dims[0] = 1ull << (L - 10 * (K - 1));
+  return K;
 }
 
 /* Normalised Walsh-Hadamard transform in place: the textbook radix-2 butterfly
@@ -449,6 +452,13 @@ static void qk_T(const double *z, uint64_t m, uint64_t n, uint64_t da, uint64_t 
 /* Work items (layer, row) run in parallel; per-row partial sums are added  */
 /* in layer order so the result does not depend on the thread count.        */
 /* ------------------------------------------------------------------------ */
+/* The FJL position stream is defined for padded lengths up to 2^32. */
+static int fjl_sizes_ok(int n_layers, const int64_t *rows, const int64_t *cols, int64_t d) {
+  for (int l = 0; l < n_layers; ++l)
+    if (orc_padded((uint64_t)rows[l] * (uint64_t)cols[l], (uint64_t)d) > (1ull << 32)) return 0;
+  return 1;
+}
+
 int orc_apply(int kind, int layer0, int n_layers, const int64_t *rows, const int64_t *cols, const int32_t *da,
               const int32_t *db, int64_t d, uint64_t seed, int64_t batch, int dtype, const void *const *x,
               double *y, int nthreads, int qk_bf16) {
@@ -458,6 +468,7 @@ int orc_apply(int kind, int layer0, int n_layers, const int64_t *rows, const int
     for (int l = 0; l < n_layers; ++l) tot += (int64_t)da[l] * db[l];
     if (tot != d) return -1;
   }
+  if (kind == K_FJL && !fjl_sizes_ok(n_layers, rows, cols, d)) return -1;
   int64_t nitems = (int64_t)n_layers * batch;
   double **part = (double **)calloc((size_t)nitems, sizeof(double *));
   int64_t *qoff = (int64_t *)calloc((size_t)n_layers + 1, sizeof(int64_t));
@@ -530,6 +541,7 @@ int orc_apply_T(int kind, int layer0, int n_layers, const int64_t *rows, const i
                 const int32_t *db, int64_t d, uint64_t seed, int64_t batch, const double *z, double *const *out,
                 int nthreads, int qk_bf16) {
   if (d < 1 || batch < 1 || n_layers < 1) return -1;
+  if (kind == K_FJL && !fjl_sizes_ok(n_layers, rows, cols, d)) return -1;
   int64_t *qoff = (int64_t *)calloc((size_t)n_layers + 1, sizeof(int64_t));
   for (int l = 0; l < n_layers; ++l) qoff[l + 1] = qoff[l] + (kind == K_QK ? (int64_t)da[l] * db[l] : 0);
   int64_t nitems = (int64_t)n_layers * batch;

@@ -200,6 +200,12 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       for (int l = 0; l < n_layers; ++l)
         if (shapes[l].rows * shapes[l].cols > (1ll << 26))
           return fail(SK_EUNSUPPORTED, "AFFDQ: layer " + std::to_string(l) + " pads beyond 2^26 elements");
+    // FJL sample positions are one 32-bit Philox word masked to N' - 1, uniform
+    // only while N' <= 2^32
+    if (kind == SK_FJL)
+      for (int l = 0; l < n_layers; ++l)
+        if (shapes[l].rows * shapes[l].cols > (1ll << 32))
+          return fail(SK_EUNSUPPORTED, "FJL: layer " + std::to_string(l) + " pads beyond 2^32 elements");
   } else {
     int64_t tot = 0;
     for (int l = 0; l < n_layers; ++l) {

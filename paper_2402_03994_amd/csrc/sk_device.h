@@ -177,17 +177,15 @@ SK_HD uint32_t perm_inv(const PermKey &p, uint32_t y) {
   return (hi << p.wl) | lo;
 }
 
-// Kronecker factor shapes of a power of two n: blocks of 1024 from the least
-// significant end, the remainder first.  Returns K and fills lg[k] = log2 of
-// factor k (k = 0 most significant).
+// Kronecker digits of N' = 2^lgn (Sec. 3, factors of at most 1024 columns):
+// K = ceil(lgn / 10) digits, each of 10 bits except the most significant one,
+// which holds the remaining lgn - 10 (K - 1) bits.  Returns K and fills
+// lg[k] = log2 of digit k's range (k = 0 most significant).
 SK_HD int kron_shapes_log2(int lgn, int lg[8]) {
-  int k = 0, tmp[8];
-  while (lgn > 0) {
-    tmp[k++] = lgn < 10 ? lgn : 10;
-    lgn -= 10;
-  }
-  for (int i = 0; i < k; ++i) lg[i] = tmp[k - 1 - i];
-  return k;
+  const int K = (lgn + 9) / 10;
+  for (int k = 1; k < K; ++k) lg[k] = 10;
+  if (K > 0) lg[0] = lgn - 10 * (K - 1);
+  return K;
 }
 
 }  // namespace sk

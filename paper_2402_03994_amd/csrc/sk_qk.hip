@@ -2,10 +2,11 @@
 // Y = A X B^T with A (dA x m) ~ N(0, 1/dA) and B (dB x n) ~ N(0, 1/dB)
 // (eq. straight with two Kronecker factors; the contraction is that of
 // eq. qk_proof_tensor_dec).  Factors are generated on the device at creation
-// in fp32.  A is kept in fp32; B is stored as two bf16 terms, hi = bf16(B)
-// and lo = bf16(B - hi) (both rounded to nearest even), so that the bf16
-// MFMA contraction X B^T = X hi^T + X lo^T sees B to 16 mantissa bits.
-// Products accumulate in fp32.
+// in fp32.  A and B are kept in fp32 and, for the bf16 matrix-core
+// contractions of bf16 inputs, also as two bf16 terms, hi = bf16(F) and
+// lo = bf16(F - hi) (both rounded to nearest even), so that X B^T =
+// X hi^T + X lo^T sees B to 16 mantissa bits.  fp32 inputs and the transpose
+// multiply by the fp32 factors.  Products accumulate in fp32.
 #include <algorithm>
 
 #include "sk_launch.h"
@@ -61,21 +62,24 @@ int64_t qk_workspace_elems(const sk_sketch *s, int layer, int64_t bc) {
   return bc * std::max((int64_t)ld.m * ld.db, (int64_t)ld.da * ld.nc);
 }
 
-// T[v][i][c] = sum_j X[v][i][j] B[c][j]
+// T[v][i][c] = sum_j X[v][i][j] B[c][j] with the fp32 B (inputs that the
+// matrix-core path does not take: fp32, or shapes off its tiling).  These
+// one-thread-per-output loops sum in fp64 and round once, so their error does
+// not grow with the contraction length.
 template <bool BF16>
-__global__ void k_qk_xbt(const void *__restrict__ x, const uint16_t *__restrict__ B, const uint16_t *__restrict__ Blo,
-                         int m, int n, int db, int64_t b_begin, float *__restrict__ t) {
+__global__ void k_qk_xbt(const void *__restrict__ x, const float *__restrict__ B, int m, int n, int db,
+                         int64_t b_begin, float *__restrict__ t) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * db) return;
   const int64_t i = e / db, c = e - (e / db) * db;
   const int64_t xo = ((b_begin + v) * m + i) * (int64_t)n;
-  float acc = 0.0f;
+  double acc = 0.0;
   for (int64_t j = 0; j < n; ++j) {
     const float xv = BF16 ? qk_bf2f(((const uint16_t *)x)[xo + j]) : ((const float *)x)[xo + j];
-    acc += xv * (qk_bf2f(B[c * n + j]) + qk_bf2f(Blo[c * n + j]));
+    acc = fma((double)xv, (double)B[c * n + j], acc);
   }
-  t[(v * m + i) * db + c] = acc;
+  t[(v * m + i) * db + c] = (float)acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -395,10 +399,10 @@ __global__ void k_qk_at(const float *__restrict__ A, const float *__restrict__ t
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)da * db) return;
   const int64_t a = e / db, c = e - (e / db) * db;
-  float acc = 0.0f;
-  for (int64_t i = 0; i < m; ++i) acc += A[a * m + i] * t[(v * m + i) * db + c];
+  double acc = 0.0;
+  for (int64_t i = 0; i < m; ++i) acc = fma((double)A[a * m + i], (double)t[(v * m + i) * db + c], acc);
   float *o = out + (b_begin + v) * D + col + e;
-  *o = accumulate ? *o + acc : acc;
+  *o = accumulate ? *o + (float)acc : (float)acc;
 }
 
 void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
@@ -454,10 +458,11 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
   }
   if (stages & 1) {
     dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
+    const float *Bf = s->d_qkbf + ld.fb_off;
     if (dtype == SK_BF16)
-      hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
+      hipLaunchKernelGGL(k_qk_xbt<true>, g1, dim3(256), 0, st, x, Bf, ld.m, ld.nc, ld.db, b_begin, t_ws);
     else
-      hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, B, Blo, ld.m, ld.nc, ld.db, b_begin, t_ws);
+      hipLaunchKernelGGL(k_qk_xbt<false>, g1, dim3(256), 0, st, x, Bf, ld.m, ld.nc, ld.db, b_begin, t_ws);
   }
   if (stages & 2) {
     dim3 g2((unsigned)(((int64_t)ld.da * ld.db + 255) / 256), (unsigned)bc);
@@ -474,38 +479,38 @@ __global__ void k_qk_atz(const float *__restrict__ A, const float *__restrict__ 
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * db) return;
   const int64_t i = e / db, c = e - (e / db) * db;
-  float acc = 0.0f;
-  for (int64_t a = 0; a < da; ++a) acc += A[a * m + i] * z[(b_begin + v) * D + col + a * db + c];
-  u[(v * m + i) * db + c] = acc;
+  double acc = 0.0;
+  for (int64_t a = 0; a < da; ++a) acc = fma((double)A[a * m + i], (double)z[(b_begin + v) * D + col + a * db + c], acc);
+  u[(v * m + i) * db + c] = (float)acc;
 }
 
-// X'[v][i][j] = sum_c U[v][i][c] B[c][j] (+ theta0)
-__global__ void k_qk_ub(const uint16_t *__restrict__ B, const uint16_t *__restrict__ Blo, const float *__restrict__ u,
-                        int m, int n, int db,
+// X'[v][i][j] = sum_c U[v][i][c] B[c][j] (+ theta0), fp32 B
+__global__ void k_qk_ub(const float *__restrict__ B, const float *__restrict__ u, int m, int n, int db,
                         int64_t b_begin, void *__restrict__ out, int out_dtype, const float *__restrict__ theta0) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t v = blockIdx.y;
   if (e >= (int64_t)m * n) return;
   const int64_t i = e / n, j = e - (e / n) * n;
-  float acc = 0.0f;
-  for (int64_t c = 0; c < db; ++c) acc += u[(v * m + i) * db + c] * (qk_bf2f(B[c * n + j]) + qk_bf2f(Blo[c * n + j]));
+  double acc = 0.0;
+  for (int64_t c = 0; c < db; ++c) acc = fma((double)u[(v * m + i) * db + c], (double)B[c * n + j], acc);
   if (theta0) acc += theta0[e];
+  const float r = (float)acc;
   const int64_t o = (b_begin + v) * (int64_t)m * n + e;
   if (out_dtype == SK_BF16)
-    ((uint16_t *)out)[o] = qk_f2bf(acc);
+    ((uint16_t *)out)[o] = qk_f2bf(r);
   else
-    ((float *)out)[o] = acc;
+    ((float *)out)[o] = r;
 }
 
 void launch_qk_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *t_ws,
                        void *out, int out_dtype, const float *theta0, hipStream_t st) {
   const LayerDesc &ld = s->layers[layer];
   const float *A = s->d_qka + ld.fa_off;
-  const uint16_t *B = s->d_qkb + ld.fb_off, *Blo = s->d_qkb + s->qk_b_elems + ld.fb_off;
+  const float *Bf = s->d_qkbf + ld.fb_off;
   dim3 g1((unsigned)(((int64_t)ld.m * ld.db + 255) / 256), (unsigned)bc);
   hipLaunchKernelGGL(k_qk_atz, g1, dim3(256), 0, st, A, z, ld.m, ld.da, ld.db, s->D, ld.qk_col, b_begin, t_ws);
   dim3 g2((unsigned)(((int64_t)ld.m * ld.nc + 255) / 256), (unsigned)bc);
-  hipLaunchKernelGGL(k_qk_ub, g2, dim3(256), 0, st, B, Blo, t_ws, ld.m, ld.nc, ld.db, b_begin, out, out_dtype, theta0);
+  hipLaunchKernelGGL(k_qk_ub, g2, dim3(256), 0, st, Bf, t_ws, ld.m, ld.nc, ld.db, b_begin, out, out_dtype, theta0);
   (void)hipGetLastError();
 }
 

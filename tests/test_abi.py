@@ -57,6 +57,7 @@ def shapes(*ss):
     (6, [(1, 10)], 3000, 0, -1),          # AFJLQ: D not a power of two
     (8, [(1, 10)], 4096, 0, -1),          # unknown kind
     (7, [(1, 1 << 27)], 4096, 0, -5),     # AFFDQ: N' above 2^26
+    (0, [(2, (1 << 31) + 1)], 4096, 0, -5),  # FJL: N' above 2^32 (positions are 32-bit words)
 ])
 def test_create_rejects_invalid_arguments(kind, shp, D, flags, code):
     L = _lib.load()

@@ -1,6 +1,8 @@
 """GPU parity at the benchmark workloads' full sizes, in the launch configuration
 the benchmark times (same sketches, batch sizes, dtypes, streaming and input
-generators), checked row by row against the fp64 oracle on sampled batch rows.
+generators), checked row by row against the fp64 oracle: every batch row of
+the flat-vector and GPT-2-small workloads, the first and last rows of the
+1.3B-decoder QK and the Llama-3-8B AFJL workloads.
 
 Rows are compared with the same metric and bounds as the reduced-size parity
 tests: max_i |y_i - o_i| / max(|o_i|, rms(o)) <= 1e-5 (fp32 inputs) or 2e-2
@@ -82,17 +84,20 @@ def test_fullsize_c2_afjl_affd(dev):
     shapes, D, B, seed = c["shapes"], c["D"], c["batch"], c["seed"]
     gen = W.generator("c2", dev)
     xs = [W.gaussian((B, r * cc), 1e-4, gen, dev) for r, cc in shapes]
-    rows = [0, 37, B - 1]
-    xh = [host_rows(x, rows) for x in xs]
+    ys = {}
     for kind in c["kinds"]:
-        say(f"c2 {kind}: GPT-2 small, 148 tensors, batch {B}, D=2^16")
         sk = Sketch(kind, shapes, D, seed, device=dev)
-        y = sk.apply(xs)
-        torch.cuda.synchronize()
-        e = rel_err(y[rows].cpu().numpy(), O.apply(kind, shapes, D, seed, xh, nthreads=CORES))
-        say(f"c2 {kind}: rel err {e:.2e}")
-        assert e <= TOL_F32
+        ys[kind] = sk.apply(xs).cpu().numpy()
         sk.close()
+    # every row, 16 at a time (8 GB of host copies per chunk)
+    for r0 in range(0, B, 16):
+        rows = list(range(r0, min(B, r0 + 16)))
+        xh = [host_rows(x, rows) for x in xs]
+        for kind in c["kinds"]:
+            e = rel_err(ys[kind][rows], O.apply(kind, shapes, D, seed, xh, nthreads=CORES))
+            say(f"c2 {kind}: GPT-2 small, 148 tensors, D=2^16, rows {rows[0]}..{rows[-1]} of {B}: rel err {e:.2e}")
+            assert e <= TOL_F32
+        del xh
 
 
 def test_fullsize_c3_qk_subset(dev):
@@ -113,6 +118,17 @@ def test_fullsize_c3_qk_subset(dev):
     e = rel_err(y[rows, :ncol].cpu().numpy(), o)
     say(f"c3 qk: rel err {e:.2e}")
     assert e <= TOL_BF16
+    del xs
+    # the transpose of the same sketch on the same matrices (two z rows, fp32 factors: the fp32 bound)
+    z = torch.randn((2, D), generator=gen, device=dev)
+    outs = sk.apply_T(z, first_layer=0, n_layers=len(sub))
+    torch.cuda.synchronize()
+    zc = z[:, :ncol].cpu().numpy().astype(np.float64)
+    refs = O.apply_T("qk", sub, ncol, seed, zc, nthreads=CORES)
+    for i, (g, r) in enumerate(zip(outs, refs)):
+        e = rel_err(g.cpu().numpy(), r)
+        say(f"c3 qk T: matrix {i}: rel err {e:.2e}")
+        assert e <= TOL_F32
     sk.close()
 
 
@@ -130,16 +146,16 @@ def test_fullsize_c4_ffd(dev):
     theta = sk.apply_T(z, theta0=[theta0])[0]
     y = sk.apply([x])
     torch.cuda.synchronize()
-    r = B - 1
     th0 = theta0.cpu().numpy()
-    ot = O.apply_T("ffd", shapes, D, seed, z[r:r + 1].cpu().numpy(), nthreads=CORES, theta0=[th0])[0]
-    e = rel_err(theta[r:r + 1].cpu().numpy(), ot)
-    say(f"c4 ffd T: rel err {e:.2e}")
+    # every row, both directions
+    ot = O.apply_T("ffd", shapes, D, seed, z.cpu().numpy(), nthreads=CORES, theta0=[th0])[0]
+    e = rel_err(theta.cpu().numpy(), ot)
+    say(f"c4 ffd T: rows 0..{B - 1}: rel err {e:.2e}")
     assert e <= TOL_F32
-    del ot
-    oy = O.apply("ffd", shapes, D, seed, [host_rows(x, [0])], nthreads=CORES)
-    e = rel_err(y[:1].cpu().numpy(), oy)
-    say(f"c4 ffd fwd: rel err {e:.2e}")
+    del ot, theta
+    oy = O.apply("ffd", shapes, D, seed, [host_rows(x, list(range(B)))], nthreads=CORES)
+    e = rel_err(y.cpu().numpy(), oy)
+    say(f"c4 ffd fwd: rows 0..{B - 1}: rel err {e:.2e}")
     assert e <= TOL_F32
     sk.close()
 
@@ -155,17 +171,17 @@ def test_fullsize_c5_afjl_streamed_subset(dev):
     gen = W.generator("c5", dev)
     sk = Sketch("afjl", shapes, D, seed, device=dev)
     out = torch.empty((B, D), device=dev)
-    row = 5
-    ref = np.zeros((1, D))
+    rows = [0, B - 1]
+    ref = np.zeros((len(rows), D))
     for i, (f, cnt) in enumerate(calls):
         say(f"c5 afjl: call {i} layers {f}..{f + cnt - 1}, batch {B}, D=2^20, bf16")
         xs = [W.gaussian((B, s[0] * s[1]), 1e-5, gen, dev, dtype=torch.bfloat16) for s in shapes[f:f + cnt]]
         sk.apply(xs, out=out, first_layer=f, accumulate=i > 0)
         torch.cuda.synchronize()
-        ref += O.apply("afjl", shapes[f:f + cnt], D, seed, [host_rows(x, [row]) for x in xs], dtype="bf16",
+        ref += O.apply("afjl", shapes[f:f + cnt], D, seed, [host_rows(x, rows) for x in xs], dtype="bf16",
                        layer0=f, nthreads=CORES)
         del xs
-    e = rel_err(out[row:row + 1].cpu().numpy(), ref)
-    say(f"c5 afjl: rel err {e:.2e}")
+    e = rel_err(out[rows].cpu().numpy(), ref)
+    say(f"c5 afjl: rows {rows}: rel err {e:.2e}")
     assert e <= TOL_BF16
     sk.close()

@@ -254,12 +254,19 @@ def test_id_search_full_size_known_answer(dev):
     """The benchmark's search (FFD on a 1e8-entry vector, D_max = 2^20, rank-8 quadratic without bulk,
     theta0 in the span of the spikes): a subspace of d >= 8 free coordinates removes the whole loss, so the
     search from d = 2 must end at d = 8 with tau near 1 (8 fp32 CG steps on the 8 x 8 reduced system: exact in
-    exact arithmetic, 0.997 measured), d = 2 and 4 leaving most of it."""
+    exact arithmetic, 0.997 measured), d = 2 and 4 leaving most of it.  theta0 = V V^T x is formed by the
+    oracle's synthetic-Hessian passes (unit weights, no shift) from the benchmark's seeded x."""
     import workloads as W
-    from paper_2402_03994_amd import Sketch, id_search
+    from paper_2402_03994_amd import Sketch, SyntheticHessian, id_search
     c = W.CONFIGS["c9"]
-    sk = Sketch("ffd", c["shapes"], c["D"], c["seed"], device=dev)
-    H, _, theta0 = W.c9_problem(dev)
+    shapes = c["shapes"]
+    lam = np.array(W.C9_LAMBDAS, dtype=np.float32)
+    x = W.c9_x(dev).cpu().numpy().astype(np.float64)
+    th0 = K.hvp(shapes, len(lam), np.ones(len(lam)), 0.0, W.C9_HSEED, [x])[0][0].astype(np.float32)
+    del x
+    sk = Sketch("ffd", shapes, c["D"], c["seed"], device=dev)
+    H = SyntheticHessian(shapes, len(lam), lam, 0.0, W.C9_HSEED, device=dev)
+    theta0 = [torch.tensor(th0, device=dev)]
     r = id_search(sk, H, theta0, c["d_min"], c["tau_target"], c["delta"], c["cg_steps"], c["max_rounds"])
     assert r["status"] == 0 and r["d"] == 8
     assert r["taus"][-1] > 0.99

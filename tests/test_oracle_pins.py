@@ -76,6 +76,32 @@ def test_index_stream_uniform():
     assert scipy.stats.chisquare(counts).pvalue > 1e-4
 
 
+@pytest.mark.parametrize("np_len", [16, 1 << 20, 1 << 32])
+def test_index_stream_layout(np_len):
+    # position i: word i%4 of the block with counter (i/4, 0, layer, stream 3), masked to N' - 1
+    seed, layer = 0xFEEDFACE0BADF00D, 11
+    idx = O.indices(seed, layer, 0, 4096, np_len)
+    for i in [0, 1, 2, 3, 4, 7, 1001, 4095]:
+        w = O.philox([i >> 2, 0, layer, O.STREAMS["index"]], [seed & 0xFFFFFFFF, seed >> 32])
+        assert int(idx[i]) == int(w[i & 3]) & (np_len - 1)
+    # a start offset reads the same positions
+    assert np.array_equal(O.indices(seed, layer, 1001, 7, np_len), idx[1001:1008])
+
+
+def test_oracle_rejects_fjl_beyond_32bit_positions():
+    import ctypes
+    L = O.lib()
+    rows = np.array([2], dtype=np.int64)
+    cols = np.array([(1 << 31) + 1], dtype=np.int64)
+    zero = np.zeros(1, dtype=np.int32)
+    y = np.zeros(16, dtype=np.float64)
+    ptrs = (ctypes.c_void_p * 1)(None)
+    assert L.orc_apply(0, 0, 1, O._ptr(rows), O._ptr(cols), O._ptr(zero), O._ptr(zero), 16, 0, 1, 0, ptrs,
+                       O._ptr(y), 1, 0) == -1
+    assert L.orc_apply_T(0, 0, 1, O._ptr(rows), O._ptr(cols), O._ptr(zero), O._ptr(zero), 16, 0, 1, O._ptr(y),
+                         ptrs, 1, 0) == -1
+
+
 @pytest.mark.parametrize("w", list(range(0, 17)))
 def test_feistel_is_a_bijection_with_inverse(w):
     t = O.perm(11, 3, "pi1", 2, w)

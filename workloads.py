@@ -138,6 +138,12 @@ def c8_hessian(device):
     return H, dict(rank=len(lam), lambdas=lam, shift=float(np.float32(C8_SHIFT)), seed=C8_HSEED)
 
 
+def c9_x(device) -> torch.Tensor:
+    """The seeded vector x ~ N(0, 1) ([1, n]) that c9's theta0 = V V^T x projects."""
+    shapes = CONFIGS["c9"]["shapes"]
+    return torch.randn((1, shapes[0][0] * shapes[0][1]), generator=generator("c9", device), device=device)
+
+
 def c9_problem(device):
     """The objective's Hessian of c9 on `device`, its parameters as the oracle takes them, and theta0
     = V V^T x with x ~ N(0, 1) seeded (built with a unit-weight Hessian on the same sign vectors)."""
@@ -149,8 +155,6 @@ def c9_problem(device):
     lam = np.array(C9_LAMBDAS, dtype=np.float32)
     H = SyntheticHessian(shapes, len(lam), lam, 0.0, C9_HSEED, device=device)
     unit = SyntheticHessian(shapes, len(lam), np.ones(len(lam), dtype=np.float32), 0.0, C9_HSEED, device=device)
-    gen = generator("c9", device)
-    x = torch.randn((1, shapes[0][0] * shapes[0][1]), generator=gen, device=device)
-    theta0 = unit.apply([x])[0].reshape(-1)
+    theta0 = unit.apply([c9_x(device)])[0].reshape(-1)
     unit.close()
     return H, dict(rank=len(lam), lambdas=lam, shift=0.0, seed=C9_HSEED), [theta0]
