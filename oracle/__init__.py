@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for the structured sketches (FJL, FFD, AFFD, AFJL, QK, QKH, AFJLQ).
+"""fp64 CPU oracle for the structured sketches (FJL, FFD, AFFD, AFJL, QK, QKH, AFJLQ, AFFDQ, AFJLF).
 
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import this package.  The product
@@ -9,8 +9,9 @@ Walsh-Hadamard transform, literal operator chains of the paper's equations
 ailon_chazelle, fastfood, bami, frikadel and straight).  This module only
 marshals numpy arrays into that library.  The kinds with the random-orthogonal
 Kronecker pre-conditioner (QKH, AFJLQ, AFFDQ) are in ``qhaar.py`` (numpy, fp64);
-the synthetic Hessian, the sketched HVP operator and the Arnoldi iteration on
-it are in ``krylov.py``.
+the kind with the Fourier pre-conditioner (AFJLF) is in ``fourier.py`` (numpy,
+fp64); the synthetic Hessian, the sketched HVP operator and the Arnoldi
+iteration on it are in ``krylov.py``.
 """
 from __future__ import annotations
 
@@ -27,6 +28,8 @@ _LIB = os.path.join(_HERE, "libsk_oracle.so")
 KINDS = {"fjl": 0, "ffd": 1, "affd": 2, "afjl": 3, "qk": 4}
 # kinds with the random-orthogonal Kronecker pre-conditioner (numpy, qhaar.py)
 QKINDS = ("qkh", "afjlq", "affdq")
+# kinds with the Fourier pre-conditioner (numpy, fourier.py)
+FKINDS = ("afjlf",)
 DTYPES = {"f32": 0, "bf16": 1}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9,
            "hvp": 10}
@@ -174,6 +177,9 @@ def apply(kind: str, shapes, D: int, seed: int, xs, dtype: str = "f32", layer0: 
     if kind in QKINDS:
         from . import qhaar
         return qhaar.apply(kind, shapes, D, seed, xs, dtype, layer0)
+    if kind in FKINDS:
+        from . import fourier
+        return fourier.apply(kind, shapes, D, seed, xs, dtype, layer0)
     rows, cols, da, db = _shape_arrays(shapes)
     want = np.float32 if dtype == "f32" else np.uint16
     arrs = [np.ascontiguousarray(x, dtype=want) for x in xs]
@@ -196,6 +202,9 @@ def apply_T(kind: str, shapes, D: int, seed: int, z: np.ndarray, layer0: int = 0
     if kind in QKINDS:
         from . import qhaar
         return qhaar.apply_T(kind, shapes, D, seed, z, layer0, theta0)
+    if kind in FKINDS:
+        from . import fourier
+        return fourier.apply_T(kind, shapes, D, seed, z, layer0, theta0)
     rows, cols, da, db = _shape_arrays(shapes)
     z = np.ascontiguousarray(z, dtype=np.float64)
     batch = z.shape[0]
