@@ -179,6 +179,28 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
                  int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream);
 
 /*
+ * sketch_apply without any allocation or use of the handle's workspace, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Arguments, results
+ * and errors are those of sketch_apply.  The per-call scratch is a static
+ * device array of 64 MiB (SK_STATIC_SCRATCH_BYTES) that each device the
+ * library runs on holds until the process ends; its device address is looked
+ * up on the first call on each device (hipGetSymbolAddress, which may fail with
+ * SK_EHIP).  Layer ranges whose one vector needs more scratch than that (for
+ * instance AFFD or FJL layers of 2^24 or more padded elements, AFJL with
+ * D = 2^20, QK matrices whose first stage holds more than 16 M floats per
+ * vector) are rejected with SK_EUNSUPPORTED before any launch, leaving `out`
+ * untouched; larger batches go through in chunks that fit.  The kernels write
+ * every scratch element they read, so leftovers of earlier calls do not
+ * matter.  All calls on one device share its array: calls that may overlap in
+ * time on one device (other streams, other host threads, other handles) race
+ * and must be serialised by the caller.
+ */
+#define SK_STATIC_SCRATCH_BYTES (64ll << 20)
+int sketch_apply_noalloc(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t batch, float *out,
+                         int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream);
+
+/*
  * Transpose x_l = S_l^T z (+ theta0_l) for the selected layers.
  *   z        device [batch, D] fp32.
  *   out      host array of n_layers device pointers, out[i] is

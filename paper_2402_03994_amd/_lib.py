@@ -13,7 +13,7 @@ SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9,
            "hvp": 10}
-EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_T", "sketch_destroy", "sketch_query",
+EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_noalloc", "sketch_apply_T", "sketch_destroy", "sketch_query",
            "sketch_debug_stream", "sketch_profile", "sketch_profile_read", "sketch_last_error",
            "sketch_status_string", "sk_hvp_create", "sk_hvp_apply", "sk_hvp_destroy", "sketch_hvp",
            "sketch_arnoldi_work_floats", "sketch_arnoldi_step", "sketch_arnoldi", "sk_hvp_profile",
@@ -58,6 +58,8 @@ def load() -> ctypes.CDLL:
     L.sketch_create.restype = ctypes.c_int
     L.sketch_apply.argtypes = [P, ctypes.POINTER(P), ctypes.c_int, i64, P, i32, i32, i32, P]
     L.sketch_apply.restype = ctypes.c_int
+    L.sketch_apply_noalloc.argtypes = [P, ctypes.POINTER(P), ctypes.c_int, i64, P, i32, i32, i32, P]
+    L.sketch_apply_noalloc.restype = ctypes.c_int
     L.sketch_apply_T.argtypes = [P, P, i64, ctypes.POINTER(P), ctypes.c_int, ctypes.POINTER(P), i32, i32, P]
     L.sketch_apply_T.restype = ctypes.c_int
     L.sketch_destroy.argtypes = [P]

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -152,6 +153,53 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
   return need;
 }
 
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Allocation-free forward sketch.  The per-call scratch (fold partials, FJL
+// and FFD intermediates, QK first-stage products) lives in `scratch`, a
+// file-scope device array of kStaticScratchBytes that every device the library
+// runs on holds until the process ends.  Host code never uses the array's
+// name as an address (on the host it is only a stand-in for the symbol): the
+// device address of each device's copy is looked up once per device with
+// hipGetSymbolAddress, with that device current, and kept in g_scratch_ptr.
+// ---------------------------------------------------------------------------
+constexpr int64_t kStaticScratchBytes = SK_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+namespace {
+constexpr int kMaxScratchDevices = 64;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+std::mutex g_scratch_mu;
+
+// Device address of `device`'s copy of scratch (the device must be current).
+int scratch_ptr(int device, void **ptr) {
+  if (device < 0 || device >= kMaxScratchDevices) return fail(SK_EUNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SK_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[device] = p;
+  }
+  *ptr = g_scratch_ptr[device];
+  return SK_OK;
+}
+
+// Points the handle's workspace at other memory for one call.
+struct WorkspaceSwap {
+  sk_sketch *s;
+  float *ws;
+  int64_t bytes;
+  WorkspaceSwap(sk_sketch *s_, void *p, int64_t b) : s(s_), ws(s_->ws), bytes(s_->ws_bytes) {
+    s->ws = (float *)p;
+    s->ws_bytes = b;
+  }
+  ~WorkspaceSwap() {
+    s->ws = ws;
+    s->ws_bytes = bytes;
+  }
+};
 }  // namespace
 
 namespace sk {
@@ -839,6 +887,26 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(SK_EHIP, std::string("kernel launch failed: ") + hipGetErrorString(e));
   return SK_OK;
+}
+
+// Allocation-free forward sketch: sketch_apply with the per-call scratch in
+// the static device array below instead of the handle's workspace.
+int sketch_apply_noalloc(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t batch, float *out,
+                         int32_t first_layer, int32_t n_layers, int32_t accumulate, void *stream) {
+  if (!s) return fail(SK_EINVAL, "sketch is NULL");
+  if (dtype != SK_F32 && dtype != SK_BF16) return fail(SK_EDTYPE, "dtype must be SK_F32 or SK_BF16");
+  if (batch < 0) return fail(SK_EINVAL, "batch must be >= 0");
+  if (int rc = check_range(s, first_layer, n_layers)) return rc;
+  const int64_t pv = per_vector_bytes(s, first_layer, first_layer + n_layers, false);
+  if (pv > kStaticScratchBytes)
+    return fail(SK_EUNSUPPORTED, "one vector of these layers needs " + std::to_string(pv) +
+                                     " bytes of scratch; the static scratch holds " +
+                                     std::to_string(kStaticScratchBytes));
+  DeviceGuard guard(s->device);
+  void *p = nullptr;
+  if (int rc = scratch_ptr(s->device, &p)) return rc;
+  WorkspaceSwap swap(s, p, kStaticScratchBytes);
+  return sketch_apply(s, grads, dtype, batch, out, first_layer, n_layers, accumulate, stream);
 }
 
 int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out, sk_dtype out_dtype,

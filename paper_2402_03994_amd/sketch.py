@@ -70,8 +70,11 @@ class Sketch:
         return {k: getattr(inf, k) for k, _ in _lib.Info._fields_}
 
     def apply(self, grads: Sequence[torch.Tensor], out: Optional[torch.Tensor] = None, first_layer: int = 0,
-              accumulate: bool = False) -> torch.Tensor:
-        """out[batch, D] (+)= sum over layers first_layer.. of S_l grads[l] (grads[l]: [batch, numel])."""
+              accumulate: bool = False, noalloc: bool = False) -> torch.Tensor:
+        """out[batch, D] (+)= sum over layers first_layer.. of S_l grads[l] (grads[l]: [batch, numel]).
+
+        noalloc: call sketch_apply_noalloc (scratch in the library's static device array, not the handle's
+        workspace); pass `out` as well for a call that allocates nothing at all."""
         grads = list(grads)
         dt = grads[0].dtype
         batch = grads[0].shape[0]
@@ -83,8 +86,9 @@ class Sketch:
         elif out.dtype != torch.float32 or tuple(out.shape) != (batch, self.D) or not out.is_contiguous():
             raise ValueError("out must be contiguous float32 [batch, D]")
         ptrs = (ctypes.c_void_p * len(grads))(*[g.data_ptr() for g in grads])
-        _lib.check(self.lib.sketch_apply(self._h, ptrs, _DT[dt], batch, out.data_ptr(), first_layer, len(grads),
-                                         int(accumulate), _stream_ptr(self.device)))
+        fn = self.lib.sketch_apply_noalloc if noalloc else self.lib.sketch_apply
+        _lib.check(fn(self._h, ptrs, _DT[dt], batch, out.data_ptr(), first_layer, len(grads), int(accumulate),
+                      _stream_ptr(self.device)))
         return out
 
     def apply_T(self, z: torch.Tensor, out_dtype=torch.float32, theta0: Optional[Sequence] = None,
