@@ -25,6 +25,12 @@
  *   SK_AFFDQ y = sqrt(N/D) R_D Q'_N G Q_N x               (eq. bami with both
  *            H_N replaced by independent Q_N, Q'_N; G over N'.  Dense work:
  *            about 4 GFLOP per vector and 2^20-element slab)
+ *   SK_AFJLF y = sqrt(N/D) G R_D F_N B x                  (eq. frikadel with the
+ *            pre-conditioner H_N replaced by the FFT, Sec. 3 "Alternative
+ *            pre-conditioners".  F_N is the real orthonormal Fourier matrix:
+ *            rows 1/sqrt(N), (-1)^n/sqrt(N), then per frequency k >= 1 the
+ *            pair sqrt(2/N) (cos, -sin)(2 pi k n / N); so y holds X_0, X_{N/2}
+ *            and Re, Im of X_1 .. X_{D/2-1} of the DFT X of B x, scaled)
  *
  * H_N is the normalised Walsh-Hadamard matrix (appendix definition), R_D keeps
  * the first D coordinates, B is a diagonal of random signs, G a diagonal of
@@ -75,7 +81,8 @@ typedef enum {
   SK_QK = 4,
   SK_QKH = 5,
   SK_AFJLQ = 6,
-  SK_AFFDQ = 7
+  SK_AFFDQ = 7,
+  SK_AFJLF = 8
 } sk_kind;
 typedef enum { SK_F32 = 0, SK_BF16 = 1 } sk_dtype;
 
@@ -113,7 +120,7 @@ typedef struct {
 /* Random-stream identifiers (the fourth Philox counter word). */
 enum {
   SK_STREAM_SIGN = 1,    /* B signs, one per coordinate of N'_l            */
-  SK_STREAM_GAUSS = 2,   /* G entries (AFFD, FFD: N'_l; FJL, AFJL: D)      */
+  SK_STREAM_GAUSS = 2,   /* G entries (AFFD, FFD: N'_l; FJL, AFJL, AFJLF: D) */
   SK_STREAM_INDEX = 3,   /* FJL sample positions in [0, N'_l)              */
   SK_STREAM_FFDPERM = 4, /* FFD block permutation Pi_b                     */
   SK_STREAM_PI1 = 5,     /* digit permutation before the first H           */
@@ -138,7 +145,11 @@ enum {
  *             (smaller D is SK_EUNSUPPORTED by the kernels); SK_AFFDQ also
  *             needs N'_l <= 2^26 for every layer.  SK_FJL needs N'_l <= 2^32
  *             (a sample position is one 32-bit random word masked to N'_l - 1;
- *             larger layers are SK_EUNSUPPORTED).  Every layer: rows*cols <= 2^40.
+ *             larger layers are SK_EUNSUPPORTED).  SK_AFJLF: a power of two,
+ *             2048 <= D <= 2^20, and each layer either has N'_l = D and at
+ *             most 16384 entries, or 2 <= N'_l/(D/2) <= 4096 and
+ *             D^2/(4 N'_l) <= 16384 (otherwise SK_EUNSUPPORTED).
+ *             Every layer: rows*cols <= 2^40.
  *   seed      64-bit key of every random stream.
  *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).
  * On success *out receives the handle (destroy with sketch_destroy).  The
@@ -265,7 +276,10 @@ enum {
   SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ/SK_AFFDQ second contraction        */
   SK_PROF_QH_T = 13,     /* SK_QKH/SK_AFJLQ/SK_AFFDQ transposes               */
   SK_PROF_FFD_T = 14,    /* FFD transpose with D <= 2^13 (one launch)        */
-  SK_PROF_CLASSES = 15
+  SK_PROF_FF_ROWS = 15,  /* AFJLF kernels that read the gradients (pass 1 and
+                            the one-kernel small layers)                     */
+  SK_PROF_FF_RES = 16,   /* AFJLF residue pass and the layer sum             */
+  SK_PROF_CLASSES = 17
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

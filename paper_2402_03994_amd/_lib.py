@@ -8,7 +8,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsketch.so")
 
-SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ, SK_AFFDQ = range(8)
+SK_FJL, SK_FFD, SK_AFFD, SK_AFJL, SK_QK, SK_QKH, SK_AFJLQ, SK_AFFDQ, SK_AFJLF = range(9)
 SK_F32, SK_BF16 = 0, 1
 STATUS = {0: "SK_OK", -1: "SK_EINVAL", -2: "SK_EDTYPE", -3: "SK_ENOMEM", -4: "SK_EHIP", -5: "SK_EUNSUPPORTED"}
 STREAMS = {"sign": 1, "gauss": 2, "index": 3, "ffdperm": 4, "pi1": 5, "pi2": 6, "qka": 7, "qkb": 8, "qh": 9,
@@ -21,7 +21,7 @@ EXPORTS = ("sketch_create", "sketch_apply", "sketch_apply_noalloc", "sketch_appl
 HVP_PROF_CLASSES = ["hvp_dots", "hvp_combine", "arnoldi_orth"]
 HVP_MAX_RANK = 32
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
-                "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t", "ffd_t"]
+                "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t", "ffd_t", "ff_rows", "ff_res"]
 
 
 class IdResult(ctypes.Structure):

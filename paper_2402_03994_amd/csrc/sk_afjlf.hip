@@ -1,0 +1,727 @@
+// sk_afjlf.hip -- AFJLF: eq. frikadel with the Walsh-Hadamard pre-conditioner
+// replaced by the FFT (Sec. 3, "Alternative pre-conditioners"; Table
+// tab:gains_design_choices, rows H_N -> FFT):
+//
+//   y = sqrt(N/D) G R_D F_N B pad(x)
+//
+// with F_N the real orthonormal Fourier matrix whose rows are 1/sqrt(N),
+// (-1)^n/sqrt(N) and then, per frequency k = 1 .. N/2 - 1, the pair
+// sqrt(2/N) (cos, -sin)(2 pi k n / N).  R_D keeps the first D rows, i.e. the
+// DFT values X_0 .. X_{M-1} (M = D/2) and X_{N/2}:
+//   y_0 = g_0 X_0 / sqrt(D),  y_1 = g_1 X_{N/2} / sqrt(D),
+//   y_{2k} = sqrt(2/D) g_{2k} Re X_k,  y_{2k+1} = sqrt(2/D) g_{2k+1} Im X_k.
+//
+// Only M of the N DFT values are needed.  With the layer viewed as P = N/M
+// rows of M (n = t M + b) and k = r + P j (r < P, j < J = M/P):
+//   u_r[b]      = sum_t x[t][b] w_P^{t r}                        (pass 1)
+//   X_{r + P j} = sum_q w_N^{q (r + P j)} sum_s v[q][s] w_J^{s j}  (pass 2)
+//   v[q][s]     = u_r[q + P s] w_M^{s r},   q < P, s < J
+// (w_L = exp(-2 pi i / L)).  Pass 1 reads the signed input once and writes u
+// for r <= P/2 (the rest follow from u_{P-r} = conj(u_r)); pass 2 gives both
+// residues r and P - r from one J-point transform per column q:
+//   X_{(P-r) + P (J-1-j)} = sum_q conj(w_N^{q r} w_M^{q j} W_q[j]) w_P^{q}.
+// Layers with N = D and at most 16384 live entries take one kernel instead
+// (k = c + (N/L) e: N/L transforms of L >= n points of the twiddled input).
+// The transpose runs the same passes backwards.  All transforms are the LDS
+// Stockham FFTs of sk_fft.h with twiddles from a table made in double
+// precision at creation.
+#include <algorithm>
+#include <cmath>
+#include <functional>
+#include <vector>
+
+#include "sk_fft.h"
+#include "sk_launch.h"
+
+namespace sk {
+
+namespace {
+
+constexpr int kNT = 1024;        // threads per workgroup
+constexpr int kCap = 16384;      // complex values of one workgroup's transform buffer (128 KB)
+constexpr int kLgCap = 14;
+constexpr int kMaxE = kCap / kNT;
+constexpr int kMaxQb = 2048;     // q columns of one pass-2 block (their twiddles live in LDS)
+constexpr int kSlots = 32;       // layers per launch
+
+struct FfLayers {
+  int32_t n;                     // layers in this launch
+  int32_t layer[kSlots];         // index into the layer table
+  int64_t item0[kSlots + 1];     // first work item of each layer (+ total)
+  const void *x[kSlots];         // forward: the layer's input; transpose: its output ([batch, n])
+  float *u[kSlots];              // pass buffer of the layer, vector 0 of the tile
+  int64_t us[kSlots];            // floats per vector of that buffer
+  float *y[kSlots];              // forward: the layer's contribution, vector 0 of the tile ([tile][D])
+  const float *th[kSlots];       // transpose: theta0 or null
+};
+
+__device__ __forceinline__ int find_slot(const FfLayers &g, int64_t item) {
+  int s = 0;
+  while (s + 1 < g.n && g.item0[s + 1] <= item) ++s;
+  return s;
+}
+
+// Linear workgroup id -> (item, vector) with every item of vector v on XCD v % 8.
+__device__ __forceinline__ bool xcd_decode(int64_t nitems, int64_t bc, int64_t &item, int64_t &v) {
+  const int64_t L = blockIdx.x;
+  const int64_t rest = L >> 3;
+  item = rest % nitems;
+  v = (rest / nitems) * 8 + (L & 7);
+  return v < bc;
+}
+
+__device__ __forceinline__ float load_x(const void *x, int dtype, int64_t j) {
+  if (dtype == SK_BF16) return __uint_as_float((uint32_t)((const uint16_t *)x)[j] << 16);
+  return ((const float *)x)[j];
+}
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ void store_out(void *o, int dtype, int64_t j, float v) {
+  if (dtype == SK_BF16)
+    ((uint16_t *)o)[j] = f2bf(v);
+  else
+    ((float *)o)[j] = v;
+}
+
+// Column block of pass 1: W real columns of the P x M view (P * W <= 2 kCap).
+__device__ __host__ __forceinline__ int ff_lgW(int lgP) { return std::min(10, kLgCap + 1 - lgP); }
+
+// Sign words of rows t < rows, columns [b0, b0 + 2^lgW) of the P x M view
+// into sw[t * nw + w] (nw = max(1, W / 32)).
+__device__ __forceinline__ void build_row_signs(uint32_t *sw, int64_t rows, int lgM, int64_t b0, int lgW,
+                                                uint32_t layer, Key key) {
+  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
+  for (int64_t e = threadIdx.x; e < rows * nw; e += kNT) {
+    const int64_t t = e / nw, w = e - t * nw;
+    const int64_t j = (t << lgM) + b0 + (w << 5);
+    sw[e] = sign_word((uint64_t)j, layer, key);
+  }
+}
+
+__device__ __forceinline__ uint32_t row_sign_bit(const uint32_t *sw, int64_t t, int nw, int lgM, int64_t b0,
+                                                 int64_t j) {
+  const int64_t base = ((t << lgM) + b0) >> 5;
+  return (sw[t * nw + ((j >> 5) - base)] >> (j & 31)) & 1u;
+}
+
+// ---------------------------------------------------------------------------
+// Pass 1, forward: u_r[b] = sum_t B x [t][b] w_P^{t r}, r <= P/2, for one
+// column block; two real columns per complex transform column.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffr_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
+                                                 int lgD, int64_t b_begin, int64_t bc,
+                                                 const float2 *__restrict__ tw, int lgS, Key key) {
+  __shared__ float2 buf[kCap];
+  __shared__ uint32_t sw[4096];
+  int64_t item, v;
+  if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
+  const int slot = find_slot(g, item);
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgW = ff_lgW(lgP), lgWc = lgW - 1;
+  const int64_t M = 1ll << lgM, n = ld.n;
+  const int64_t b0 = (item - g.item0[slot]) << lgW;
+  const int64_t rows = std::min<int64_t>((n + M - 1) >> lgM, 1ll << lgP);
+  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
+  const uint32_t lid = (uint32_t)ld.layer_id;
+  build_row_signs(sw, rows, lgM, b0, lgW, lid, key);
+  __syncthreads();
+  const void *x = g.x[slot];
+  const int64_t xo = (b_begin + v) * n;
+  const int total = 1 << (lgP + lgWc);
+  for (int e = threadIdx.x; e < total; e += kNT) {
+    const int64_t t = e >> lgWc;
+    const int c = e & ((1 << lgWc) - 1);
+    float2 val = make_float2(0.f, 0.f);
+    if (t < rows) {
+      const int64_t j = (t << lgM) + b0 + 2 * c;
+      if (j < n) val.x = flip(load_x(x, dtype, xo + j), row_sign_bit(sw, t, nw, lgM, b0, j));
+      if (j + 1 < n) val.y = flip(load_x(x, dtype, xo + j + 1), row_sign_bit(sw, t, nw, lgM, b0, j + 1));
+    }
+    buf[e] = val;
+  }
+  lds_fft<false, kNT, kMaxE>(buf, lgP, lgWc, tw, lgS);
+  // split the two real columns and write r = 0 .. P/2
+  float *u = g.u[slot] + v * g.us[slot];
+  const int P = 1 << lgP;
+  const int tot2 = (P / 2 + 1) << lgWc;
+  for (int e = threadIdx.x; e < tot2; e += kNT) {
+    const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
+    const float2 zr = buf[(r << lgWc) + c];
+    const float2 zm = buf[(((P - r) & (P - 1)) << lgWc) + c];
+    const float4 o = make_float4(0.5f * (zr.x + zm.x), 0.5f * (zr.y - zm.y),   // (Z_r + conj Z_{P-r}) / 2
+                                 0.5f * (zr.y + zm.y), 0.5f * (zm.x - zr.x));  // -i (Z_r - conj Z_{P-r}) / 2
+    *(float4 *)(u + (((int64_t)r << lgM) + b0 + 2 * c) * 2) = o;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2, forward: for residue r (and P - r) of one layer and vector, the J
+// outputs X_{r + P j} (and X_{(P-r) + P (J-1-j)}), scaled by G into y.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffq_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
+                                                 int64_t bc, const float *__restrict__ gtab, float c1, float c2,
+                                                 const float2 *__restrict__ tw, int lgS) {
+  __shared__ float2 buf[kCap];
+  __shared__ float2 tq[kMaxQb];
+  int64_t item, v;
+  if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
+  const int slot = find_slot(g, item);
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgJ = lgM - lgP, lgN = ld.lgnp;
+  const int P = 1 << lgP, J = 1 << lgJ;
+  const int r = (int)(item - g.item0[slot]);
+  const bool pair = r > 0 && 2 * r < P;
+  const int lgQb = std::min(std::min(lgP, kLgCap - lgJ), 11);
+  const int Qb = 1 << lgQb, nqb = P >> lgQb;
+  const int lgG = lgJ <= 10 ? 10 - lgJ : 0;  // threads per output row
+  const int G = 1 << lgG;
+  const int rpt = lgJ > 10 ? 1 << (lgJ - 10) : 1;  // rows per thread
+  const int j0 = threadIdx.x >> lgG, gi = threadIdx.x & (G - 1);
+  const float2 *u = (const float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgM);
+  float *y = g.y[slot] + v * ((int64_t)1 << lgD);
+  const float *gl = gtab + (int64_t)ld.layer_id * ((int64_t)1 << lgD);
+  const float tscale = ldexpf(-2.0f, -lgN);  // -2 / N
+  // y (+)= the scaled sums of output row j (sets A and B, X_{N/2} for r = 0)
+  auto emit = [&](int j, float2 a, float2 b, float2 nn, bool add) {
+    const int64_t ka = r + ((int64_t)j << lgP);
+    float2 va, vb = make_float2(0.f, 0.f);
+    int64_t ia, ib = 0;
+    if (ka == 0) {
+      ia = 0;
+      va = make_float2(c1 * gl[0] * a.x, c1 * gl[1] * nn.x);
+    } else {
+      ia = 2 * ka;
+      va = make_float2(c2 * gl[ia] * a.x, c2 * gl[ia + 1] * a.y);
+    }
+    if (pair) {
+      ib = 2 * ((P - r) + ((int64_t)(J - 1 - j) << lgP));
+      vb = make_float2(c2 * gl[ib] * b.x, c2 * gl[ib + 1] * b.y);
+    }
+    float2 *pa = (float2 *)(y + ia), *pb = (float2 *)(y + ib);
+    if (add) {
+      va = cadd(va, *pa);
+      if (pair) vb = cadd(vb, *pb);
+    }
+    *pa = va;
+    if (pair) *pb = vb;
+  };
+  for (int qb = 0; qb < nqb; ++qb) {
+    const int q0 = qb << lgQb;
+    for (int qq = threadIdx.x; qq < Qb; qq += kNT) {
+      float sn, cs;
+      sincospif(tscale * (float)((int64_t)(q0 + qq) * r), &sn, &cs);  // w_N^{q r}
+      tq[qq] = make_float2(cs, sn);
+    }
+    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
+      const int s = e >> lgQb, qq = e & (Qb - 1);
+      const float2 val = u[q0 + qq + ((int64_t)s << lgP)];
+      buf[e] = cmul(val, twiddle<false>(tw, lgS, lgM, (int64_t)s * r));
+    }
+    lds_fft<false, kNT, kMaxE>(buf, lgJ, lgQb, tw, lgS);
+    for (int i = 0; i < rpt; ++i) {
+      const int j = j0 + (i << (10 - lgG));
+      float2 a = make_float2(0.f, 0.f), b = a, nn = a;
+      for (int qq = gi; qq < Qb; qq += G) {
+        const int q = q0 + qq;
+        const float2 w = buf[(j << lgQb) + qq];
+        const float2 tA = cmul(cmul(w, tq[qq]), twiddle<false>(tw, lgS, lgM, (int64_t)q * j));
+        a = cadd(a, tA);
+        if (pair) b = cadd(b, cmul(cconj(tA), twiddle<false>(tw, lgS, lgP, q)));
+        if (r == 0 && j == 0) nn = (q & 1) ? csub(nn, w) : cadd(nn, w);
+      }
+      if (G == 1) {
+        emit(j, a, b, nn, qb > 0);
+      } else {
+        // combine the G partial sums of this row in a fixed order
+        __syncthreads();
+        buf[threadIdx.x] = a;
+        buf[kNT + threadIdx.x] = b;
+        buf[2 * kNT + threadIdx.x] = nn;
+        __syncthreads();
+        if ((int)threadIdx.x < J) {
+          float2 sa = make_float2(0.f, 0.f), sb = sa, sn2 = sa;
+          for (int k = 0; k < G; ++k) {
+            sa = cadd(sa, buf[(threadIdx.x << lgG) + k]);
+            sb = cadd(sb, buf[kNT + (threadIdx.x << lgG) + k]);
+            sn2 = cadd(sn2, buf[2 * kNT + (threadIdx.x << lgG) + k]);
+          }
+          emit((int)threadIdx.x, sa, sb, sn2, qb > 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Layers with N = D and n <= 16384: X_{c + (N/L) e} = FFT_L(v_b w_N^{b c})[e].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffs_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
+                                                 int lgD, int64_t b_begin, int64_t bc, const float *__restrict__ gtab,
+                                                 float c1, float c2, const float2 *__restrict__ tw, int lgS, Key key) {
+  __shared__ float2 buf[kCap];
+  __shared__ uint32_t sw[kCap / 32];
+  int64_t item, v;
+  if (!xcd_decode(g.n, bc, item, v)) return;
+  const int slot = (int)item;
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int64_t n = ld.n;
+  int lgL = 1;
+  while ((1ll << lgL) < n) ++lgL;
+  const int L = 1 << lgL;
+  const int lgcs = lgD - lgL;                       // log2 of the number of c values
+  const int lgcg = std::min(lgcs, kLgCap - lgL);    // c values per group
+  const uint32_t lid = (uint32_t)ld.layer_id;
+  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += kNT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
+  __syncthreads();
+  const void *x = g.x[slot];
+  const int64_t xo = (b_begin + v) * n;
+  float *y = g.y[slot] + v * ((int64_t)1 << lgD);
+  const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
+  for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
+    for (int e = threadIdx.x; e < (L << lgcg); e += kNT) {
+      const int b = e >> lgcg, cc = e & ((1 << lgcg) - 1);
+      float2 val = make_float2(0.f, 0.f);
+      if (b < n) {
+        const float xv = flip(load_x(x, dtype, xo + b), (sw[b >> 5] >> (b & 31)) & 1u);
+        val = cscale(twiddle<false>(tw, lgS, lgD, (int64_t)b * (c0 + cc)), xv);
+      }
+      buf[e] = val;
+    }
+    lds_fft<false, kNT, kMaxE>(buf, lgL, lgcg, tw, lgS);
+    for (int e = threadIdx.x; e < ((L / 2) << lgcg); e += kNT) {
+      const int ee = e >> lgcg, cc = e & ((1 << lgcg) - 1);
+      const int64_t k = (c0 + cc) + ((int64_t)ee << lgcs);
+      const float2 X = buf[e];
+      if (k == 0) {
+        y[0] = c1 * gl[0] * X.x;
+        y[1] = c1 * gl[1] * buf[(L / 2) << lgcg].x;  // X_{N/2}: c = 0, e = L/2
+      } else {
+        y[2 * k] = c2 * gl[2 * k] * X.x;
+        y[2 * k + 1] = c2 * gl[2 * k + 1] * X.y;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// out[v] (+)= sum over the call's layers of y[l][v], in layer order
+__global__ void k_ff_tail(const float *__restrict__ y, int nl, int64_t lstride, int64_t D, int64_t b_begin,
+                          float *__restrict__ out, int accumulate) {
+  const int64_t i = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+  const int64_t v = blockIdx.y;
+  if (i >= D) return;
+  if ((uintptr_t)out & 15) {  // an output view without 16-byte alignment
+    for (int k = 0; k < 4; ++k) {
+      float a = 0.f;
+      for (int l = 0; l < nl; ++l) a += y[l * lstride + v * D + i + k];
+      float *o = out + (b_begin + v) * D + i + k;
+      *o = accumulate ? *o + a : a;
+    }
+    return;
+  }
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int l = 0; l < nl; ++l) {
+    const float4 t = *(const float4 *)(y + l * lstride + v * D + i);
+    a.x += t.x;
+    a.y += t.y;
+    a.z += t.z;
+    a.w += t.w;
+  }
+  float4 *o = (float4 *)(out + (b_begin + v) * D + i);
+  if (accumulate) {
+    const float4 p = *o;
+    a.x += p.x;
+    a.y += p.y;
+    a.z += p.z;
+    a.w += p.w;
+  }
+  *o = a;
+}
+
+// coefficient c_k of the transpose (k < M): c_0 = g_0 z_0 / sqrt(D),
+// c_k = sqrt(2/D) (g_{2k} z_{2k} + i g_{2k+1} z_{2k+1})
+__device__ __forceinline__ float2 coef(const float *z, const float *gl, int64_t k, float c1, float c2) {
+  if (k == 0) return make_float2(c1 * gl[0] * z[0], 0.f);
+  return make_float2(c2 * gl[2 * k] * z[2 * k], c2 * gl[2 * k + 1] * z[2 * k + 1]);
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2, transpose: E~_r[q + P s] (r <= P/2) from the coefficients of
+// residues r and P - r (one inverse J-point transform per column q).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffq_T(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
+                                               const float *__restrict__ z, int64_t b_begin, int64_t bc,
+                                               const float *__restrict__ gtab, float c1, float c2,
+                                               const float2 *__restrict__ tw, int lgS) {
+  __shared__ float2 buf[kCap];
+  __shared__ float2 tq[kMaxQb];
+  int64_t item, v;
+  if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
+  const int slot = find_slot(g, item);
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgJ = lgM - lgP, lgN = ld.lgnp;
+  const int P = 1 << lgP, J = 1 << lgJ;
+  const int r = (int)(item - g.item0[slot]);
+  const bool pair = r > 0 && 2 * r < P;
+  const int lgQb = std::min(std::min(lgP, kLgCap - lgJ), 11);
+  const int Qb = 1 << lgQb, nqb = P >> lgQb;
+  const float *zv = z + (b_begin + v) * ((int64_t)1 << lgD);
+  const float *gl = gtab + (int64_t)ld.layer_id * ((int64_t)1 << lgD);
+  const float cN2 = c1 * gl[1] * zv[1];
+  float2 *u = (float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgM);
+  const float tscale = ldexpf(-2.0f, -lgN);
+  for (int qb = 0; qb < nqb; ++qb) {
+    const int q0 = qb << lgQb;
+    for (int qq = threadIdx.x; qq < Qb; qq += kNT) {
+      float sn, cs;
+      sincospif(tscale * (float)((int64_t)(q0 + qq) * r), &sn, &cs);
+      tq[qq] = make_float2(cs, sn);  // w_N^{q r}
+    }
+    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
+      const int m = e >> lgQb, qq = e & (Qb - 1);
+      const int64_t q = q0 + qq;
+      float2 a = cmul(coef(zv, gl, r + ((int64_t)m << lgP), c1, c2), twiddle<true>(tw, lgS, lgM, q * m));
+      if (pair) {
+        const float2 cp = coef(zv, gl, (P - r) + ((int64_t)(J - m - 1) << lgP), c1, c2);
+        a = cadd(a, cmul(cconj(cp), twiddle<false>(tw, lgS, lgM, q * (J - m))));
+      }
+      buf[e] = a;
+    }
+    lds_fft<true, kNT, kMaxE>(buf, lgJ, lgQb, tw, lgS);
+    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
+      const int s = e >> lgQb, qq = e & (Qb - 1);
+      float2 E = cmulc(cmulc(buf[e], tq[qq]), twiddle<false>(tw, lgS, lgM, (int64_t)s * r));
+      if (r == 0) E.x += ((q0 + qq) & 1) ? -cN2 : cN2;
+      u[q0 + qq + ((int64_t)s << lgP)] = E;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 1, transpose: x[t][b] = Re sum_{r <= P/2} w_P^{-t r} E~_r[b] for one
+// column block (a complex-to-real inverse transform of two columns at a
+// time), signed, plus theta0, truncated to the layer.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffr_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
+                                               int lgD, int64_t b_begin, int64_t bc,
+                                               const float2 *__restrict__ tw, int lgS, Key key) {
+  __shared__ float2 buf[kCap];
+  __shared__ uint32_t sw[4096];
+  int64_t item, v;
+  if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
+  const int slot = find_slot(g, item);
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgW = ff_lgW(lgP), lgWc = lgW - 1;
+  const int64_t M = 1ll << lgM, n = ld.n;
+  const int P = 1 << lgP;
+  const int64_t b0 = (item - g.item0[slot]) << lgW;
+  const int64_t rows = std::min<int64_t>((n + M - 1) >> lgM, (int64_t)P);
+  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
+  build_row_signs(sw, rows, lgM, b0, lgW, (uint32_t)ld.layer_id, key);
+  const float *u = g.u[slot] + v * g.us[slot];
+  const int tot = (P / 2 + 1) << lgWc;
+  for (int e = threadIdx.x; e < tot; e += kNT) {
+    const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
+    const float4 E = *(const float4 *)(u + (((int64_t)r << lgM) + b0 + 2 * c) * 2);
+    const bool edge = r == 0 || 2 * r == P;
+    const float2 ha = edge ? make_float2(E.x, 0.f) : make_float2(0.5f * E.x, 0.5f * E.y);
+    const float2 hb = edge ? make_float2(E.z, 0.f) : make_float2(0.5f * E.z, 0.5f * E.w);
+    buf[(r << lgWc) + c] = make_float2(ha.x - hb.y, ha.y + hb.x);          // H_a + i H_b
+    if (!edge) buf[((P - r) << lgWc) + c] = make_float2(ha.x + hb.y, hb.x - ha.y);  // conj H_a + i conj H_b
+  }
+  lds_fft<true, kNT, kMaxE>(buf, lgP, lgWc, tw, lgS);
+  void *o = (void *)g.x[slot];
+  const float *th = g.th[slot];
+  const int64_t oo = (b_begin + v) * n;
+  for (int e = threadIdx.x; e < (int)(rows << lgWc); e += kNT) {
+    const int64_t t = e >> lgWc;
+    const int c = e & ((1 << lgWc) - 1);
+    const float2 zt = buf[e];
+    const int64_t j = (t << lgM) + b0 + 2 * c;
+    if (j < n) {
+      float a = flip(zt.x, row_sign_bit(sw, t, nw, lgM, b0, j));
+      if (th) a += th[j];
+      store_out(o, out_dtype, oo + j, a);
+    }
+    if (j + 1 < n) {
+      float b = flip(zt.y, row_sign_bit(sw, t, nw, lgM, b0, j + 1));
+      if (th) b += th[j + 1];
+      store_out(o, out_dtype, oo + j + 1, b);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Small layers, transpose: x_b = Re sum_c w_N^{-b c} IFFT_L(coef_c)[b].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kNT) void k_ffs_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
+                                               int lgD, const float *__restrict__ z, int64_t b_begin, int64_t bc,
+                                               const float *__restrict__ gtab, float c1, float c2,
+                                               const float2 *__restrict__ tw, int lgS, Key key) {
+  __shared__ float2 buf[kCap];
+  __shared__ uint32_t sw[kCap / 32];
+  int64_t item, v;
+  if (!xcd_decode(g.n, bc, item, v)) return;
+  const int slot = (int)item;
+  const LayerDesc &ld = layers[g.layer[slot]];
+  const int64_t n = ld.n;
+  int lgL = 1;
+  while ((1ll << lgL) < n) ++lgL;
+  const int L = 1 << lgL;
+  const int lgcs = lgD - lgL;
+  const int lgcg = std::min(lgcs, kLgCap - lgL);
+  const uint32_t lid = (uint32_t)ld.layer_id;
+  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += kNT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
+  const float *zv = z + (b_begin + v) * ((int64_t)1 << lgD);
+  const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
+  float acc[kMaxE];
+#pragma unroll
+  for (int i = 0; i < kMaxE; ++i) acc[i] = 0.f;
+  for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < (L << lgcg); e += kNT) {
+      const int ee = e >> lgcg, cc = e & ((1 << lgcg) - 1);
+      const int c = c0 + cc;
+      float2 a = make_float2(0.f, 0.f);
+      if (2 * ee < L) {
+        a = coef(zv, gl, c + ((int64_t)ee << lgcs), c1, c2);
+      } else if (2 * ee == L && c == 0) {
+        a = make_float2(c1 * gl[1] * zv[1], 0.f);  // the (-1)^b row
+      }
+      buf[e] = a;
+    }
+    lds_fft<true, kNT, kMaxE>(buf, lgL, lgcg, tw, lgS);
+    for (int cc = 0; cc < (1 << lgcg); ++cc) {
+#pragma unroll
+      for (int i = 0; i < kMaxE; ++i) {
+        const int b = threadIdx.x + i * kNT;
+        if (b < L) {
+          const float2 w = buf[(b << lgcg) + cc];
+          const float2 t = twiddle<false>(tw, lgS, lgD, (int64_t)b * (c0 + cc));
+          acc[i] += w.x * t.x + w.y * t.y;  // Re(w conj(t))
+        }
+      }
+    }
+  }
+  void *o = (void *)g.x[slot];
+  const float *th = g.th[slot];
+  const int64_t oo = (b_begin + v) * n;
+#pragma unroll
+  for (int i = 0; i < kMaxE; ++i) {
+    const int b = threadIdx.x + i * kNT;
+    if (b < n) {
+      float a = flip(acc[i], (sw[b >> 5] >> (b & 31)) & 1u);
+      if (th) a += th[b];
+      store_out(o, out_dtype, oo + b, a);
+    }
+  }
+}
+
+}  // namespace
+
+// ------------------------------- host side ---------------------------------
+
+namespace {
+int lg2(int64_t v) {
+  int l = 0;
+  while ((1ll << l) < v) ++l;
+  return l;
+}
+int64_t ceil8(int64_t v) { return (v + 7) / 8 * 8; }
+}  // namespace
+
+bool afjlf_small_layer(const sk_sketch *s, int layer) {
+  const LayerDesc &ld = s->layers[layer];
+  return ld.np == s->D && ld.n <= kCap;
+}
+
+// floats per vector of a layer's pass buffer: (P/2 + 1) M complex
+int64_t afjlf_u_floats(const sk_sketch *s, int layer) {
+  return afjlf_small_layer(s, layer) ? 0 : s->layers[layer].np + s->D;
+}
+
+int64_t afjlf_bytes_per_vector(const sk_sketch *s, int l0, int l1, bool transpose) {
+  int64_t u = 0;
+  for (int l = l0; l < l1; ++l) u = std::max(u, afjlf_u_floats(s, l));
+  return (u + (transpose ? 0 : (int64_t)(l1 - l0) * s->D)) * 4;
+}
+
+void afjlf_twiddles(int64_t D, std::vector<float> &host, int &lgS) {
+  const int64_t S = std::max<int64_t>(D, 4096);
+  lgS = lg2(S);
+  host.resize(2 * S);
+  for (int64_t m = 0; m < S; ++m) {
+    const double a = -2.0 * M_PI * (double)m / (double)S;
+    host[2 * m] = (float)std::cos(a);
+    host[2 * m + 1] = (float)std::sin(a);
+  }
+}
+
+namespace {
+
+// The call's general (two-pass) layers in groups: a group holds up to kSlots
+// layers whose pass buffers for `tile` vectors fit in ufl floats; a layer too
+// large for the whole chunk is a group of its own, run in vector tiles.
+template <class F>
+void for_groups(const sk_sketch *s, int l0, int l1, int64_t bc, int64_t ufl, F &&f) {
+  int l = l0;
+  while (l < l1) {
+    if (afjlf_small_layer(s, l)) {
+      ++l;
+      continue;
+    }
+    std::vector<int> grp{l};
+    int64_t used = afjlf_u_floats(s, l) * bc;
+    int64_t tile = bc;
+    int lend = l + 1;
+    if (used > ufl) {
+      tile = std::max<int64_t>(1, ufl / afjlf_u_floats(s, l));
+    } else {
+      while (lend < l1 && (int)grp.size() < kSlots) {
+        if (afjlf_small_layer(s, lend)) {
+          ++lend;
+          continue;
+        }
+        const int64_t nd = afjlf_u_floats(s, lend) * bc;
+        if (used + nd > ufl) break;
+        used += nd;
+        grp.push_back(lend++);
+      }
+    }
+    f(grp, tile);
+    l = lend;
+  }
+}
+
+void small_groups(const sk_sketch *s, int l0, int l1, const std::function<void(FfLayers &)> &f) {
+  FfLayers g{};
+  for (int l = l0; l < l1; ++l) {
+    if (!afjlf_small_layer(s, l)) continue;
+    g.layer[g.n++] = l;
+    if (g.n == kSlots) {
+      f(g);
+      g = FfLayers{};
+    }
+  }
+  if (g.n) f(g);
+}
+
+}  // namespace
+
+// Forward of layers [l0, l1) for vectors b_begin .. b_begin + bc - 1.  ws
+// holds (l1 - l0) bc D floats of per-layer contributions, then pass buffers.
+void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int dtype, int64_t b_begin,
+                   int64_t bc, float *ws, int64_t ws_floats, float *out, bool accumulate, hipStream_t st) {
+  const int esz = dtype == SK_BF16 ? 2 : 4;
+  const int64_t D = s->D;
+  const int lgD = lg2(D);
+  const float c1 = (float)(1.0 / std::sqrt((double)D)), c2 = (float)std::sqrt(2.0 / (double)D);
+  const int nl = l1 - l0;
+  const int64_t lstride = bc * D;
+  float *ybase = ws, *ubase = ws + (int64_t)nl * lstride;
+  const int64_t ufl = ws_floats - (int64_t)nl * lstride;
+  const float2 *tw = (const float2 *)s->d_ftw;
+  small_groups(s, l0, l1, [&](FfLayers &g) {
+    int64_t gb = 0;
+    for (int i = 0; i < g.n; ++i) {
+      g.x[i] = grads[g.layer[i] - l0];
+      g.y[i] = ybase + (int64_t)(g.layer[i] - l0) * lstride;
+      gb += bc * s->layers[g.layer[i]].n * esz;
+    }
+    SK_PROF(SK_PROF_FF_ROWS, gb,
+            hipLaunchKernelGGL(k_ffs_fwd, dim3((unsigned)(g.n * ceil8(bc))), dim3(kNT), 0, st, s->d_layers, g,
+                               dtype, lgD, b_begin, bc, s->d_gtab, c1, c2, tw, s->ftw_lg, s->key));
+  });
+  for_groups(s, l0, l1, bc, ufl, [&](const std::vector<int> &grp, int64_t tile) {
+    for (int64_t t0 = 0; t0 < bc; t0 += tile) {
+      const int64_t tb = std::min(tile, bc - t0);
+      FfLayers g1{}, g2{};
+      int64_t off = 0, gb = 0;
+      for (int l : grp) {
+        const int i = g1.n;
+        const LayerDesc &ld = s->layers[l];
+        const int lgP = ld.lgnp - (lgD - 1);
+        gb += tb * ld.n * esz;
+        g1.layer[i] = g2.layer[i] = l;
+        g1.x[i] = grads[l - l0];
+        g1.u[i] = g2.u[i] = ubase + off;
+        g1.us[i] = g2.us[i] = afjlf_u_floats(s, l);
+        g2.y[i] = ybase + (int64_t)(l - l0) * lstride + t0 * D;
+        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (lgD - 1 - ff_lgW(lgP)));
+        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (lgP - 1)) + 1;
+        off += g1.us[i] * tb;
+        ++g1.n;
+        ++g2.n;
+      }
+      SK_PROF(SK_PROF_FF_ROWS, gb,
+              hipLaunchKernelGGL(k_ffr_fwd, dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(kNT), 0, st,
+                                 s->d_layers, g1, dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
+      SK_PROF(SK_PROF_FF_RES, 0,
+              hipLaunchKernelGGL(k_ffq_fwd, dim3((unsigned)(g2.item0[g2.n] * ceil8(tb))), dim3(kNT), 0, st,
+                                 s->d_layers, g2, lgD, tb, s->d_gtab, c1, c2, tw, s->ftw_lg));
+    }
+  });
+  const dim3 gt((unsigned)((D / 4 + 255) / 256), (unsigned)bc);
+  SK_PROF(SK_PROF_FF_RES, bc * D * 4,
+          hipLaunchKernelGGL(k_ff_tail, gt, dim3(256), 0, st, ybase, nl, lstride, D, b_begin, out, (int)accumulate));
+}
+
+// Transpose of layers [l0, l1) for vectors b_begin .. b_begin + bc - 1; ws holds the pass buffers.
+void run_afjlf_T(sk_sketch *s, int l0, int l1, const float *z, int64_t b_begin, int64_t bc, float *ws,
+                 int64_t ws_floats, void *const *outs, int out_dtype, const void *const *theta0, hipStream_t st) {
+  const int osz = out_dtype == SK_BF16 ? 2 : 4;
+  const int64_t D = s->D;
+  const int lgD = lg2(D);
+  const float c1 = (float)(1.0 / std::sqrt((double)D)), c2 = (float)std::sqrt(2.0 / (double)D);
+  const float2 *tw = (const float2 *)s->d_ftw;
+  small_groups(s, l0, l1, [&](FfLayers &g) {
+    int64_t ob = 0;
+    for (int i = 0; i < g.n; ++i) {
+      const int64_t n = s->layers[g.layer[i]].n;
+      g.x[i] = outs[g.layer[i] - l0];
+      g.th[i] = theta0 ? (const float *)theta0[g.layer[i] - l0] : nullptr;
+      ob += bc * n * osz + (g.th[i] ? n * 4 : 0);
+    }
+    SK_PROF(SK_PROF_GATHER, ob,
+            hipLaunchKernelGGL(k_ffs_T, dim3((unsigned)(g.n * ceil8(bc))), dim3(kNT), 0, st, s->d_layers, g,
+                               out_dtype, lgD, z, b_begin, bc, s->d_gtab, c1, c2, tw, s->ftw_lg, s->key));
+  });
+  for_groups(s, l0, l1, bc, ws_floats, [&](const std::vector<int> &grp, int64_t tile) {
+    for (int64_t t0 = 0; t0 < bc; t0 += tile) {
+      const int64_t tb = std::min(tile, bc - t0);
+      FfLayers g1{}, g2{};
+      int64_t off = 0, ob = 0;
+      for (int l : grp) {
+        const int i = g1.n;
+        const LayerDesc &ld = s->layers[l];
+        const int lgP = ld.lgnp - (lgD - 1);
+        g1.layer[i] = g2.layer[i] = l;
+        g1.x[i] = outs[l - l0];
+        g1.th[i] = theta0 ? (const float *)theta0[l - l0] : nullptr;
+        ob += tb * ld.n * osz + (g1.th[i] ? ld.n * 4 : 0);
+        g1.u[i] = g2.u[i] = ws + off;
+        g1.us[i] = g2.us[i] = afjlf_u_floats(s, l);
+        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (lgD - 1 - ff_lgW(lgP)));
+        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (lgP - 1)) + 1;
+        off += g1.us[i] * tb;
+        ++g1.n;
+        ++g2.n;
+      }
+      SK_PROF(SK_PROF_FF_RES, tb * D * 4,
+              hipLaunchKernelGGL(k_ffq_T, dim3((unsigned)(g2.item0[g2.n] * ceil8(tb))), dim3(kNT), 0, st,
+                                 s->d_layers, g2, lgD, z, b_begin + t0, tb, s->d_gtab, c1, c2, tw, s->ftw_lg));
+      SK_PROF(SK_PROF_GATHER, ob,
+              hipLaunchKernelGGL(k_ffr_T, dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(kNT), 0, st,
+                                 s->d_layers, g1, out_dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
+    }
+  });
+}
+
+}  // namespace sk

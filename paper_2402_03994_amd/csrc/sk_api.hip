@@ -78,6 +78,7 @@ void free_all(sk_sketch *s) {
   f(s->d_mtab);
   f(s->d_gsmall);
   f(s->d_qh);
+  f(s->d_ftw);
   f(s->ws);
   for (hipEvent_t e : s->evpool) (void)hipEventDestroy(e);
   s->evpool.clear();
@@ -86,29 +87,10 @@ void free_all(sk_sketch *s) {
 bool fwht_kind(int k) { return k == SK_FJL || k == SK_FFD || k == SK_AFFD || k == SK_AFJL; }
 bool q_kind(int k) { return k == SK_QKH || k == SK_AFJLQ || k == SK_AFFDQ; }
 // kinds on the padded per-layer length N' with its Kronecker digits
-bool padded_kind(int k) { return fwht_kind(k) || q_kind(k); }
+bool padded_kind(int k) { return fwht_kind(k) || q_kind(k) || k == SK_AFJLF; }
+// kinds whose kernels need D >= 2048
+bool big_d_kind(int k) { return q_kind(k) || k == SK_AFJLF; }
 
-// Brackets a group of launches with a pair of pooled events when profiling.
-struct ProfScope {
-  sk_sketch *s;
-  int idx = -1;
-  hipStream_t st;
-  ProfScope(sk_sketch *s_, int cls, int64_t bytes, hipStream_t st_) : s(s_), st(st_) {
-    if (!((s->prof_mask >> cls) & 1u) || s->evnext + 2 > (int)s->evpool.size()) return;
-    idx = s->evnext;
-    s->evnext += 2;
-    s->recs.push_back(sk_sketch::ProfRec{cls, idx, bytes});
-    (void)hipEventRecord(s->evpool[idx], st);
-  }
-  ~ProfScope() {
-    if (idx >= 0) (void)hipEventRecord(s->evpool[idx + 1], st);
-  }
-};
-#define SK_PROF(cls, bytes, ...)          \
-  do {                                    \
-    ProfScope ps_(s, (cls), (bytes), st); \
-    __VA_ARGS__;                          \
-  } while (0)
 
 // Bytes of workspace one vector needs for one call over layers [l0, l1).
 int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
@@ -137,6 +119,8 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
       case SK_AFFDQ:
         b = qh_bytes_per_vector(s, l, transpose);
         break;
+      case SK_AFJLF:  // the whole range at once below
+        break;
       case SK_QK:  // T = X B^T (m x dB) or, A first, U = A X (dA x n)
         b = std::max((int64_t)ld.m * ld.db, (int64_t)ld.da * ld.nc) * 4;
         break;
@@ -145,6 +129,7 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
   }
   if ((s->kind == SK_QKH || s->kind == SK_AFJLQ) && !transpose)
     need = std::max(need, qh_small_bytes_per_vector(s, l0, l1));
+  if (s->kind == SK_AFJLF) need = afjlf_bytes_per_vector(s, l0, l1, transpose);
   if (s->kind == SK_AFJL && !transpose) {
     // fold partials of every item of the call, plus the tail's per-group sums
     const int64_t items = s->layers[l1 - 1].item_off + s->layers[l1 - 1].n_items - s->layers[l0].item_off;
@@ -230,7 +215,7 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
                   uint32_t flags, int32_t device, sk_sketch **out) {
   if (!out) return fail(SK_EINVAL, "out is NULL");
   *out = nullptr;
-  if ((int)kind < 0 || (int)kind > 7) return fail(SK_EINVAL, "unknown sketch kind");
+  if ((int)kind < 0 || (int)kind > 8) return fail(SK_EINVAL, "unknown sketch kind");
   if (!shapes || n_layers < 1) return fail(SK_EINVAL, "need at least one layer shape");
   if (flags & ~SK_FLAG_AFFD_NO_MTAB) return fail(SK_EINVAL, "unknown flags");
   for (int l = 0; l < n_layers; ++l) {
@@ -241,13 +226,27 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
   if (padded_kind(kind)) {
     if (!is_pow2(D)) return fail(SK_EINVAL, "D must be a power of two");
-    if (D < (q_kind(kind) ? 2048 : 16))
-      return fail(SK_EUNSUPPORTED, std::string("D < ") + (q_kind(kind) ? "2048" : "16") + " is not supported by the kernels");
+    if (D < (big_d_kind(kind) ? 2048 : 16))
+      return fail(SK_EUNSUPPORTED, std::string("D < ") + (big_d_kind(kind) ? "2048" : "16") + " is not supported by the kernels");
     if (D > (1ll << 20)) return fail(SK_EUNSUPPORTED, "D > 2^20 is not supported by the kernels");
     if (kind == SK_AFFDQ)
       for (int l = 0; l < n_layers; ++l)
         if (shapes[l].rows * shapes[l].cols > (1ll << 26))
           return fail(SK_EUNSUPPORTED, "AFFDQ: layer " + std::to_string(l) + " pads beyond 2^26 elements");
+    // AFJLF: one-kernel layers (N' = D, at most 16384 entries) or two passes with
+    // 2 <= P = N'/(D/2) <= 4096 and J = D/(2P) between 1 and 16384
+    if (kind == SK_AFJLF)
+      for (int l = 0; l < n_layers; ++l) {
+        const int64_t n = shapes[l].rows * shapes[l].cols;
+        int lgn = 0;
+        while ((1ll << lgn) < std::max(n, D)) ++lgn;
+        const int lgM = ilog2(D) - 1, lgP = lgn - lgM, lgJ = lgM - lgP;
+        const bool small = lgn == ilog2(D) && n <= 16384;
+        if (!small && (lgP < 1 || lgP > 12 || lgJ < 0 || lgJ > 14))
+          return fail(SK_EUNSUPPORTED, "AFJLF: layer " + std::to_string(l) +
+                                           " needs N'/(D/2) <= 4096 and D^2/(4 N') <= 16384 (or N' = D and at most "
+                                           "16384 entries)");
+      }
     // FJL sample positions are one 32-bit Philox word masked to N' - 1, uniform
     // only while N' <= 2^32
     if (kind == SK_FJL)
@@ -450,6 +449,12 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
     }
     return SK_OK;
   };
+  auto h2d_sync = [&](void *d, const void *h, size_t bytes) -> int {
+    if (bytes == 0) return SK_OK;
+    if (hipMemcpy(d, h, bytes, hipMemcpyHostToDevice) != hipSuccess)
+      return fail(SK_EHIP, std::string("hipMemcpy: ") + hipGetErrorString(hipGetLastError()));
+    return SK_OK;
+  };
   int rc = SK_OK;
 #define SK_TRY(expr)      \
   do {                    \
@@ -463,8 +468,14 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_layers, sizeof(LayerDesc) * n_layers));
   SK_TRY(alloc((void **)&s->d_ptab, sizeof(uint16_t) * ptab.size()));
   s->h_ptab = ptab;
-  if (kind == SK_AFJL || kind == SK_FJL || kind == SK_AFJLQ)
+  if (kind == SK_AFJL || kind == SK_FJL || kind == SK_AFJLQ || kind == SK_AFJLF)
     SK_TRY(alloc((void **)&s->d_gtab, sizeof(float) * n_layers * D));
+  if (kind == SK_AFJLF) {
+    std::vector<float> tw;
+    afjlf_twiddles(D, tw, s->ftw_lg);
+    SK_TRY(alloc((void **)&s->d_ftw, sizeof(float) * tw.size()));
+    SK_TRY(h2d_sync(s->d_ftw, tw.data(), sizeof(float) * tw.size()));
+  }
   if (qh_floats > 0) {
     SK_TRY(alloc((void **)&s->d_qh, sizeof(float) * qh_floats));
     std::vector<float> host((size_t)qh_floats, 0.0f);
@@ -865,6 +876,9 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         }
         break;
       }
+      case SK_AFJLF:
+        run_afjlf_fwd(s, l0, l1, grads, dtype, b0, bc, s->ws, s->ws_bytes / 4, out, accumulate != 0, st);
+        break;
       case SK_AFFDQ:
         for (int l = l0; l < l1; ++l) {
           const bool acc = accumulate || l > l0;
@@ -949,6 +963,10 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
         SK_PROF(SK_PROF_FWHT, 0, fwht_inplace(s->ws, (int64_t)ng * bc, lgD, st));
         SK_PROF(SK_PROF_GATHER, obytes, launch_afjl_T_out(s, g, ng, s->ws, b0, bc, out_dtype, st));
       }
+      continue;
+    }
+    if (s->kind == SK_AFJLF) {
+      run_afjlf_T(s, l0, l1, z, b0, bc, s->ws, s->ws_bytes / 4, out, out_dtype, theta0, st);
       continue;
     }
     for (int l = l0; l < l1; ++l) {

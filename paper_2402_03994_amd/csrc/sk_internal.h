@@ -104,6 +104,9 @@ struct sk_sketch {
   std::vector<int64_t> gsmall_off;  // per layer: float offset into d_gsmall, -1 if none
   // QKH / AFJLQ: per layer A, A^T, Qt, Qt^T, w (fp32)
   float *d_qh = nullptr;
+  // AFJLF: twiddle table exp(-2 pi i m / 2^ftw_lg), m < 2^ftw_lg (complex fp32)
+  float *d_ftw = nullptr;
+  int ftw_lg = 0;
   // kernel timing
   struct ProfRec {
     int cls;
@@ -119,3 +122,29 @@ struct sk_sketch {
   int64_t ws_bytes = 0;
   int64_t total_numel = 0, total_padded = 0;
 };
+
+namespace sk {
+
+// Brackets a group of launches with a pair of pooled events when profiling.
+struct ProfScope {
+  sk_sketch *s;
+  int idx = -1;
+  hipStream_t st;
+  ProfScope(sk_sketch *s_, int cls, int64_t bytes, hipStream_t st_) : s(s_), st(st_) {
+    if (!((s->prof_mask >> cls) & 1u) || s->evnext + 2 > (int)s->evpool.size()) return;
+    idx = s->evnext;
+    s->evnext += 2;
+    s->recs.push_back(sk_sketch::ProfRec{cls, idx, bytes});
+    (void)hipEventRecord(s->evpool[idx], st);
+  }
+  ~ProfScope() {
+    if (idx >= 0) (void)hipEventRecord(s->evpool[idx + 1], st);
+  }
+};
+#define SK_PROF(cls, bytes, ...)          \
+  do {                                    \
+    ProfScope ps_(s, (cls), (bytes), st); \
+    __VA_ARGS__;                          \
+  } while (0)
+
+}  // namespace sk

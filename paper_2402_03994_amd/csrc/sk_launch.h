@@ -48,6 +48,21 @@ void run_affdq_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
 void run_affdq_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, float *ws,
                        void *out, int out_dtype, const float *theta0, hipStream_t st);
 
+// ---- AFJLF (Fourier pre-conditioner) ----
+// layers with N' = D and at most 16384 entries (one kernel per direction)
+bool afjlf_small_layer(const sk_sketch *s, int layer);
+int64_t afjlf_bytes_per_vector(const sk_sketch *s, int l0, int l1, bool transpose);
+// exp(-2 pi i m / S), S = max(D, 4096), as (cos, sin) pairs, computed in double
+void afjlf_twiddles(int64_t D, std::vector<float> &host, int &lgS);
+// Kernel timing classes: SK_PROF_FF_ROWS brackets the launches that read the
+// gradients (pass 1, small layers), SK_PROF_FF_RES the residue passes and the
+// layer sum (forward); the transpose uses SK_PROF_FF_RES for pass 2 and
+// SK_PROF_GATHER for the kernels that write the outputs.
+void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int dtype, int64_t b_begin,
+                   int64_t bc, float *ws, int64_t ws_floats, float *out, bool accumulate, hipStream_t st);
+void run_afjlf_T(sk_sketch *s, int l0, int l1, const float *z, int64_t b_begin, int64_t bc, float *ws,
+                 int64_t ws_floats, void *const *outs, int out_dtype, const void *const *theta0, hipStream_t st);
+
 // ---- AFJL ----
 void launch_afjl_fold(const sk_sketch *s, const PtrPack &ptrs, int first_layer, int dtype, bool vec, int64_t batch,
                       int64_t b_begin, int64_t bc, int item_begin, int item_end, float *part, hipStream_t st);

@@ -13,7 +13,7 @@ import torch
 from . import _lib
 
 KINDS = {"fjl": _lib.SK_FJL, "ffd": _lib.SK_FFD, "affd": _lib.SK_AFFD, "afjl": _lib.SK_AFJL, "qk": _lib.SK_QK,
-         "qkh": _lib.SK_QKH, "afjlq": _lib.SK_AFJLQ, "affdq": _lib.SK_AFFDQ}
+         "qkh": _lib.SK_QKH, "afjlq": _lib.SK_AFJLQ, "affdq": _lib.SK_AFFDQ, "afjlf": _lib.SK_AFJLF}
 _DT = {torch.float32: _lib.SK_F32, torch.bfloat16: _lib.SK_BF16}
 
 
