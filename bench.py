@@ -12,15 +12,18 @@ intrinsic-dimension search.  Prints one JSON line.
 "value" is parameter-space bytes per second: gradient bytes read by forward
 sketches plus parameter-vector bytes written by transposes, summed over the
 calls of a step.  The roofline object covers the kernel class with the largest
-share of device time, found in an untimed calibration pass that brackets every
-kernel class and every call with HIP events (the per-class and per-call
-breakdowns come from it).  In the timed region only that class's launches are
-bracketed, with HIP events on the stream they run on; "achieved" is the
-algorithmic bytes of those launches (inputs read once, outputs written once)
-over their summed duration.  HBM traffic measured with
-rocprofv3 counters is attached from profiles/ when it was taken on the
-current kernel source.  The fp64 oracle is timed on the host on a bounded
-sample of the same workload.
+share of device time (intermediate-only classes included), found in an
+untimed calibration pass that brackets every kernel class with HIP events (the
+per-class breakdown comes from it).  In the timed region only that class's
+launches are bracketed, with HIP events on the stream they run on; "achieved"
+is the algorithmic bytes of those launches (inputs read once, outputs written
+once) over their summed duration.  "per_kind" gives the same fraction for
+whole calls, every kernel of a kind included, from an untimed pass with
+events around the calls only.  Traffic measured with rocprofv3 counters
+(FETCH_SIZE / WRITE_SIZE: bytes between the L2 caches and the memory fabric,
+so hits in the memory-side cache count too; an upper bound on HBM bytes) is
+attached from profiles/ when it was taken on the current kernel source.  The
+fp64 oracle is timed on the host on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -48,7 +51,9 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "fjl:prolog": "k_fjl_pass0", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
              "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
              "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
-             "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T"}
+             "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd",
+             "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
+             "affd:gather": "k_affdT_outm"}
 
 
 def qh_flops(kind, shapes, D):
@@ -88,7 +93,8 @@ def qh_flops(kind, shapes, D):
 _COMMON_SRC = ("sk_api.hip", "sk_internal.h", "sk_launch.h", "sk_kcommon.h", "sk_device.h")
 _KIND_SRC = {"fjl": ("sk_fwht.hip",), "ffd": ("sk_fwht.hip", "sk_ffd_l.hip"), "afjl": ("sk_fwht.hip",),
              "affd": ("sk_fwht.hip", "sk_affd.hip", "sk_affd_s.hip", "sk_affd_t.hip"), "qk": ("sk_qk.hip",),
-             "qkh": ("sk_qhaar.hip",), "afjlq": ("sk_qhaar.hip",), "affdq": ("sk_qhaar.hip",)}
+             "qkh": ("sk_qhaar.hip",), "afjlq": ("sk_qhaar.hip",), "affdq": ("sk_qhaar.hip",),
+             "afjlf": ("sk_afjlf.hip", "sk_fft.h")}
 
 
 def source_hash(cfg: str) -> str:
@@ -196,12 +202,16 @@ def cpu_baseline(cfg: str):
             O.apply_T(k, shapes, D, seed, z, nthreads=cores)
         nbytes = 2 * len(c["kinds"]) * c["batch"] * shapes[0][1] * 4
         sample = f"all {c['batch']} rows, FJL+FFD forward and transpose"
-    elif cfg == "c2":
-        xs = rows_for(shapes, 1)
+    elif cfg in ("c2", "c10"):
+        # the first two transformer blocks (24 tensors, 14.2M parameters), 16 rows (every core busy)
+        sub, nrows = shapes[2:26], 16
+        xs = rows_for(sub, nrows)
         for k in c["kinds"]:
-            O.apply(k, shapes, D, seed, xs, nthreads=cores)
-        nbytes = len(c["kinds"]) * sum(r * cc for r, cc in shapes) * 4
-        sample = f"1 of {c['batch']} rows, all {len(shapes)} tensors, AFJL+AFFD"
+            O.apply(k, sub, D, seed, xs, layer0=2, nthreads=cores)
+        nbytes = len(c["kinds"]) * nrows * sum(r * cc for r, cc in sub) * 4
+        names = "+".join(k.upper() for k in c["kinds"])
+        sample = f"{nrows} of {c['batch']} rows, the first two transformer blocks ({len(sub)} of {len(shapes)} " \
+                 f"tensors), {names}"
     elif cfg == "c3":
         sub = shapes[1:7]  # one decoder layer: q, k, v, o, fc1, fc2
         bf = [W.bf16_bits(x) for x in rows_for(sub, 1)]
@@ -260,8 +270,16 @@ def cpu_baseline(cfg: str):
         nbytes = sum(s[0] * s[1] for s in sub) * 2
         sample = "1 of 8 rows, one transformer block (9 of 291 tensors), AFJL"
     dt = time.perf_counter() - t0
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
-            "sample": f"{sample} ({dt:.1f} s)"}
+            "cpu": model, "sample": f"{sample} ({dt:.1f} s)"}
 
 
 # ------------------------------------------------------------------ GPU steps
@@ -297,17 +315,24 @@ def build_step(cfg: str, dev):
         return sks, step, 2 * len(c["kinds"]) * B * numels[0] * 4, B, \
             f"flat fp32 vectors N=2^20 entries N(0,1), batch {B}, D=4096, seed 0: {names} forward + transpose"
 
-    if cfg in ("c2", "c6"):
+    if cfg in ("c2", "c6", "c10"):
         xs = [W.gaussian((B, n), 1e-4, gen, dev) for n in numels]
         outs = {k: torch.empty((B, D), device=dev) for k in c["kinds"]}
+        sks["_inputs"] = xs
 
         def step(ev):
             for k in c["kinds"]:
                 ev(k, "fwd", lambda k=k: sks[k].apply(xs, out=outs[k]))
         names = " and ".join(k.upper() for k in c["kinds"])
+        extra = ""
+        if "affd" in c["kinds"]:
+            pads = [1 << max(0, (max(n, D) - 1).bit_length()) for n in numels]
+            mb = sum(p for p in pads if p >= 1 << 20) * 4 / 2**20
+            extra = (f"; AFFD reads the per-layer tables M = H_TT(signs . G) stored at creation "
+                     f"(about {mb:.0f} MB), regenerated-Gaussian figure in affd_no_mtab")
         return sks, step, len(c["kinds"]) * B * sum(numels) * 4, B, \
             (f"GPT-2-small-shaped fp32 gradients N(0,1e-4), {len(shapes)} tensors, N={sum(numels)}, batch {B}, "
-             f"D=2^16, seed 1: {names}")
+             f"D=2^16, seed 1: {names}{extra}")
 
     if cfg == "c3":
         # one resident input per distinct matrix shape, shared by the matrices of that shape
@@ -394,6 +419,61 @@ def build_step(cfg: str, dev):
          f"D=2^20, seed 7, streamed one transformer block per call")
 
 
+def call_bytes(cfg: str, kind: str, tag: str) -> int:
+    """Algorithmic bytes of one call: inputs read once plus outputs written once."""
+    c = W.CONFIGS[cfg]
+    n = sum(s[0] * s[1] for s in c["shapes"])
+    esz = 2 if c["dtype"] == "bf16" else 4
+    D, B = c["D"], c["batch"]
+    if tag == "fwd":
+        return B * n * esz + B * D * 4
+    if tag == "T":
+        th = n * 4 if cfg == "c4" else 0  # theta0 read
+        return B * n * 4 + B * D * 4 + th
+    return 0
+
+
+def per_kind_roofline(cfg: str, call_ms: dict) -> dict:
+    """Whole-call figures per kind and direction: every kernel of the call counts, intermediates included."""
+    out = {}
+    B = W.CONFIGS[cfg]["batch"]
+    for key, ms in call_ms.items():
+        kind, tag = key.split(":", 1)
+        by = call_bytes(cfg, kind, tag)
+        if not by or not ms:
+            continue
+        gbs = by / (ms * 1e-3) / 1e9
+        out[key] = {"ms_per_call": ms, "algorithmic_gb": round(by / 1e9, 3), "achieved_gb_s": round(gbs, 1),
+                    "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "vectors_per_s": round(B / (ms * 1e-3), 1)}
+    return out
+
+
+def time_affd_no_mtab(xs, dev, calls: int = 5) -> dict:
+    """AFFD on the same inputs with the Gaussians regenerated on every call (SK_FLAG_AFFD_NO_MTAB): no
+    per-layer tables stored at creation.  Whole calls timed with HIP events after two untimed calls."""
+    import torch
+
+    from paper_2402_03994_amd import Sketch
+
+    c = W.CONFIGS["c2"]
+    sk = Sketch("affd", c["shapes"], c["D"], c["seed"], device=dev, flags=Sketch.AFFD_NO_MTAB)
+    out = torch.empty((c["batch"], c["D"]), device=dev)
+    for _ in range(2):
+        sk.apply(xs, out=out)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(calls):
+        sk.apply(xs, out=out)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / calls
+    sk.close()
+    by = call_bytes("c2", "affd", "fwd")
+    return {"ms_per_call": round(ms, 3), "achieved_gb_s": round(by / (ms * 1e-3) / 1e9, 1),
+            "frac_hbm": round(by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "vectors_per_s": round(c["batch"] / (ms * 1e-3), 1)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -422,6 +502,7 @@ def main() -> int:
     cfg = args.config
     sks, step, pbytes, vecs, desc = build_step(cfg, dev)
     result = sks.pop("_result", None)
+    inputs = sks.pop("_inputs", None)
     torch.cuda.synchronize()
 
     def ev_none(kind, tag, fn):
@@ -440,14 +521,20 @@ def main() -> int:
         b.record()
         per_call.setdefault(f"{kind}:{tag}", []).append((a, b))
 
-    # calibration pass (untimed): HIP events around every kernel-class launch
-    # group and around every call, to find the class with the largest share of
-    # device time and to report the per-class breakdown
+    # call timing pass (untimed): HIP events around every call only
     ncal = max(1, min(args.steps, 3))
+    for _ in range(ncal):
+        step(ev_timed)
+    torch.cuda.synchronize()
+    call_ms = {k: round(sum(a.elapsed_time(b) for a, b in v) / ncal, 3) for k, v in per_call.items()}
+
+    # calibration pass (untimed): HIP events around every kernel-class launch
+    # group, to find the class with the largest share of device time and to
+    # report the per-class breakdown
     for s in sks.values():
         s.profile(True)
     for _ in range(ncal):
-        step(ev_timed)
+        step(ev_none)
     torch.cuda.synchronize()
     cal = {k: s.profile_read() for k, s in sks.items()}
     for s in sks.values():
@@ -459,9 +546,9 @@ def main() -> int:
             e[0] += t
             e[1] += n
             e[2] += by
-    # the dominant kernel class among those that read the gradients (or write
-    # the parameter vectors): the others move only intermediates
-    dom = max((c for c in classes if classes[c][2] > 0), key=lambda c: classes[c][0])
+    # the dominant kernel class by device time (classes that move only
+    # intermediates count, with zero algorithmic bytes)
+    dom = max(classes, key=lambda c: classes[c][0])
     dom_kind, dom_cls = dom.split(":", 1)
 
     # timed region: K steps, with HIP events (on the stream the kernels run on)
@@ -483,7 +570,6 @@ def main() -> int:
         hvps = r["rounds"] * (c["cg_steps"] + 1)  # the sketched HVPs of the search (+ the gradient at theta0)
         pbytes = (2 * hvps + 1) * c["shapes"][0][0] * c["shapes"][0][1] * 4
     value = pbytes / (ms * 1e-3) / 1e9
-    call_ms = {k: round(sum(a.elapsed_time(b) for a, b in v) / ncal, 3) for k, v in per_call.items()}
     achieved = by_dom / (t_dom * 1e-3) / 1e9 if t_dom > 0 else 0.0
     roofline = {"bound": "hbm", "kernel": KERNEL_OF.get(dom, dom), "class": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS,
@@ -516,6 +602,7 @@ def main() -> int:
                    "kinds": list(W.CONFIGS[cfg]["kinds"])},
         "vectors_per_s": round(vecs / (ms * 1e-3), 1),
         "per_call_ms": call_ms,
+        "per_kind": per_kind_roofline(cfg, call_ms),
         "kernel_classes_ms_per_step": {c: round(v[0] / ncal, 3) for c, v in sorted(classes.items())},
         "roofline": roofline,
         "source_hash": source_hash(cfg),
@@ -534,6 +621,8 @@ def main() -> int:
         line["krylov_steps_per_s"] = line.pop("vectors_per_s")
         line["ritz_top"] = [round(float(v), 4) for v in ritz[:6]] + [round(float(v), 4) for v in ritz[-2:]]
         line["hessian_spikes"] = sorted(W.C8_LAMBDAS, reverse=True)
+    if cfg == "c2" and inputs is not None:
+        line["affd_no_mtab"] = time_affd_no_mtab(inputs, dev)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(line), flush=True)

@@ -146,9 +146,10 @@ enum {
  *             needs N'_l <= 2^26 for every layer.  SK_FJL needs N'_l <= 2^32
  *             (a sample position is one 32-bit random word masked to N'_l - 1;
  *             larger layers are SK_EUNSUPPORTED).  SK_AFJLF: a power of two,
- *             2048 <= D <= 2^20, and each layer either has N'_l = D and at
- *             most 16384 entries, or 2 <= N'_l/(D/2) <= 4096 and
- *             D^2/(4 N'_l) <= 16384 (otherwise SK_EUNSUPPORTED).
+ *             2048 <= D <= 2^20; a layer with N'_l = D needs at most 16384
+ *             entries or D <= 2^16, and layers with D < N'_l < 128 D need
+ *             D^2/(4 N'_l) <= 16384 (D >= 2^17 excludes some; otherwise
+ *             SK_EUNSUPPORTED).
  *             Every layer: rows*cols <= 2^40.
  *   seed      64-bit key of every random stream.
  *   flags     0 or SK_FLAG_AFFD_NO_MTAB (see below).

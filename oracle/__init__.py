@@ -179,7 +179,7 @@ def apply(kind: str, shapes, D: int, seed: int, xs, dtype: str = "f32", layer0: 
         return qhaar.apply(kind, shapes, D, seed, xs, dtype, layer0)
     if kind in FKINDS:
         from . import fourier
-        return fourier.apply(kind, shapes, D, seed, xs, dtype, layer0)
+        return fourier.apply(kind, shapes, D, seed, xs, dtype, layer0, nthreads)
     rows, cols, da, db = _shape_arrays(shapes)
     want = np.float32 if dtype == "f32" else np.uint16
     arrs = [np.ascontiguousarray(x, dtype=want) for x in xs]
@@ -204,7 +204,7 @@ def apply_T(kind: str, shapes, D: int, seed: int, z: np.ndarray, layer0: int = 0
         return qhaar.apply_T(kind, shapes, D, seed, z, layer0, theta0)
     if kind in FKINDS:
         from . import fourier
-        return fourier.apply_T(kind, shapes, D, seed, z, layer0, theta0)
+        return fourier.apply_T(kind, shapes, D, seed, z, layer0, theta0, nthreads)
     rows, cols, da, db = _shape_arrays(shapes)
     z = np.ascontiguousarray(z, dtype=np.float64)
     batch = z.shape[0]

@@ -28,59 +28,70 @@ The reading used here (parity target of the GPU kind SK_AFJLF):
 * Several layers: the sum of the per-layer sketches; transposes are the exact
   adjoints truncated to the layer's n entries.
 
-The arithmetic is the definition written out: numpy's real FFT (pocketfft,
-fp64) is the one library step, the packing is spelled out, and the pins check
-the result against the dense cos / sin matrix and the complex FFT.
+The arithmetic is the definition written out: scipy's real FFT (fp64, the
+vectors of a batch transformed together on `workers` threads) is the one
+library step, the packing is spelled out, and the pins check the result
+against the dense cos / sin matrix and numpy's complex FFT.
 """
 from __future__ import annotations
 
+import os
+
 import numpy as np
+import scipy.fft
 
 from . import gauss, padded, signs
 
 FKINDS = ("afjlf",)
 
 
-def packed_rfft(v: np.ndarray) -> np.ndarray:
-    """F_N v for a real fp64 vector of even length N."""
+def _workers(nthreads: int = 0) -> int:
+    return nthreads or int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+
+
+def packed_rfft(v: np.ndarray, nthreads: int = 0) -> np.ndarray:
+    """F_N v for real fp64 vectors of even length N (the last axis)."""
     v = np.asarray(v, dtype=np.float64)
     N = v.shape[-1]
-    X = np.fft.rfft(v)
-    out = np.empty(N, dtype=np.float64)
-    out[0] = X[0].real
-    out[1] = X[N // 2].real
-    out[2::2] = np.sqrt(2.0) * X[1:N // 2].real
-    out[3::2] = np.sqrt(2.0) * X[1:N // 2].imag
+    X = scipy.fft.rfft(v, axis=-1, workers=_workers(nthreads))
+    out = np.empty(v.shape, dtype=np.float64)
+    out[..., 0] = X[..., 0].real
+    out[..., 1] = X[..., N // 2].real
+    out[..., 2::2] = np.sqrt(2.0) * X[..., 1:N // 2].real
+    out[..., 3::2] = np.sqrt(2.0) * X[..., 1:N // 2].imag
     return out / np.sqrt(N)
 
 
-def packed_irfft(p: np.ndarray, N: int) -> np.ndarray:
-    """F_N^T p, p holding the first len(p) <= N packed coordinates (zero beyond)."""
-    q = np.zeros(N, dtype=np.float64)
-    q[:len(p)] = p
-    Y = np.empty(N // 2 + 1, dtype=np.complex128)
-    Y[0] = q[0]
-    Y[N // 2] = q[1]
-    Y[1:N // 2] = (q[2::2] + 1j * q[3::2]) / np.sqrt(2.0)
+def packed_irfft(p: np.ndarray, N: int, nthreads: int = 0) -> np.ndarray:
+    """F_N^T p for coefficient vectors p holding the first p.shape[-1] <= N packed coordinates (zero beyond)."""
+    p = np.asarray(p, dtype=np.float64)
+    q = np.zeros(p.shape[:-1] + (N,), dtype=np.float64)
+    q[..., :p.shape[-1]] = p
+    Y = np.empty(p.shape[:-1] + (N // 2 + 1,), dtype=np.complex128)
+    Y[..., 0] = q[..., 0]
+    Y[..., N // 2] = q[..., 1]
+    Y[..., 1:N // 2] = (q[..., 2::2] + 1j * q[..., 3::2]) / np.sqrt(2.0)
     # irfft(Y)_n = (Y_0 + Y_{N/2} (-1)^n + 2 sum_k Re(Y_k e^{2 pi i k n / N})) / N
-    return np.fft.irfft(Y * np.sqrt(N), n=N)
+    return scipy.fft.irfft(Y * np.sqrt(N), n=N, axis=-1, workers=_workers(nthreads))
 
 
-def layer_forward(kind: str, x: np.ndarray, n: int, D: int, seed: int, layer: int) -> np.ndarray:
+def layer_forward(kind: str, x: np.ndarray, n: int, D: int, seed: int, layer: int, nthreads: int = 0) -> np.ndarray:
+    """The layer's sketch of a batch x [batch, n]: [batch, D]."""
     assert kind == "afjlf"
     N = padded(n, D)
-    v = np.zeros(N, dtype=np.float64)
-    v[:n] = signs(seed, layer, 0, n) * x
+    v = np.zeros((x.shape[0], N), dtype=np.float64)
+    v[:, :n] = signs(seed, layer, 0, n)[None, :] * x
     g = gauss(seed, layer, "gauss", 0, D)
-    return np.sqrt(N / D) * g * packed_rfft(v)[:D]
+    return np.sqrt(N / D) * g[None, :] * packed_rfft(v, nthreads)[:, :D]
 
 
-def layer_transpose(kind: str, z: np.ndarray, n: int, D: int, seed: int, layer: int) -> np.ndarray:
+def layer_transpose(kind: str, z: np.ndarray, n: int, D: int, seed: int, layer: int, nthreads: int = 0):
+    """The layer's transpose of a batch z [batch, D]: [batch, n]."""
     assert kind == "afjlf"
     N = padded(n, D)
     g = gauss(seed, layer, "gauss", 0, D)
-    w = packed_irfft(g * np.asarray(z, dtype=np.float64), N)
-    return np.sqrt(N / D) * signs(seed, layer, 0, n) * w[:n]
+    w = packed_irfft(g[None, :] * np.asarray(z, dtype=np.float64), N, nthreads)
+    return np.sqrt(N / D) * signs(seed, layer, 0, n)[None, :] * w[:, :n]
 
 
 def _to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
@@ -90,25 +101,24 @@ def _to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     return u.view(np.float32).astype(np.float64)
 
 
-def apply(kind: str, shapes, D: int, seed: int, xs, dtype: str = "f32", layer0: int = 0) -> np.ndarray:
+def apply(kind: str, shapes, D: int, seed: int, xs, dtype: str = "f32", layer0: int = 0,
+          nthreads: int = 0) -> np.ndarray:
     """Forward sketch of a batch: the sum over layers of the per-layer sketches; fp64 [batch, D]."""
     batch = np.asarray(xs[0]).shape[0]
     y = np.zeros((batch, D), dtype=np.float64)
     for i, (s, x) in enumerate(zip(shapes, xs)):
         n = int(s[0]) * int(s[1])
-        xv = _to_f64(x, dtype).reshape(batch, n)
-        for b in range(batch):
-            y[b] += layer_forward(kind, xv[b], n, D, seed, layer0 + i)
+        y += layer_forward(kind, _to_f64(x, dtype).reshape(batch, n), n, D, seed, layer0 + i, nthreads)
     return y
 
 
-def apply_T(kind: str, shapes, D: int, seed: int, z: np.ndarray, layer0: int = 0, theta0=None):
+def apply_T(kind: str, shapes, D: int, seed: int, z: np.ndarray, layer0: int = 0, theta0=None, nthreads: int = 0):
     """Transpose of a batch z [batch, D]: per layer fp64 [batch, n] (plus theta0 where given)."""
     z = np.asarray(z, dtype=np.float64)
     outs = []
     for i, s in enumerate(shapes):
         n = int(s[0]) * int(s[1])
-        o = np.stack([layer_transpose(kind, z[b], n, D, seed, layer0 + i) for b in range(z.shape[0])])
+        o = layer_transpose(kind, z, n, D, seed, layer0 + i, nthreads)
         if theta0 is not None and theta0[i] is not None:
             o = o + np.asarray(theta0[i], dtype=np.float64)[None, :]
         outs.append(o)

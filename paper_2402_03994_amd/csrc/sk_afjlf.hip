@@ -11,20 +11,22 @@
 //   y_0 = g_0 X_0 / sqrt(D),  y_1 = g_1 X_{N/2} / sqrt(D),
 //   y_{2k} = sqrt(2/D) g_{2k} Re X_k,  y_{2k+1} = sqrt(2/D) g_{2k+1} Im X_k.
 //
-// Only M of the N DFT values are needed.  With the layer viewed as P = N/M
-// rows of M (n = t M + b) and k = r + P j (r < P, j < J = M/P):
-//   u_r[b]      = sum_t x[t][b] w_P^{t r}                        (pass 1)
-//   X_{r + P j} = sum_q w_N^{q (r + P j)} sum_s v[q][s] w_J^{s j}  (pass 2)
-//   v[q][s]     = u_r[q + P s] w_M^{s r},   q < P, s < J
+// Only M of the N DFT values are needed.  With the layer viewed as P rows of
+// R (n = t R + b; R >= M, P = N/R <= 256 so that a row piece is at least 512
+// bytes), Q = N/M, J = M/P and k = r + P j (r < P, j < J), b = q + Q s:
+//   u_r[b]      = sum_t x[t][b] w_P^{t r}                          (pass 1)
+//   X_{r + P j} = sum_q w_N^{q r} w_R^{q j} W_q[j],                 (pass 2)
+//   W_q         = FFT_J over s of u_r[q + Q s] w_M^{s r},   q < Q, s < J
 // (w_L = exp(-2 pi i / L)).  Pass 1 reads the signed input once and writes u
-// for r <= P/2 (the rest follow from u_{P-r} = conj(u_r)); pass 2 gives both
-// residues r and P - r from one J-point transform per column q:
-//   X_{(P-r) + P (J-1-j)} = sum_q conj(w_N^{q r} w_M^{q j} W_q[j]) w_P^{q}.
+// for r <= P/2 (u_{P-r} = conj(u_r)); pass 2 gives the residues r and P - r
+// from one J-point transform per column q:
+//   X_{(P-r) + P (J-1-j)} = sum_q conj(w_N^{q r} w_R^{q j} W_q[j]) w_Q^{q}.
 // Layers with N = D and at most 16384 live entries take one kernel instead
 // (k = c + (N/L) e: N/L transforms of L >= n points of the twiddled input).
 // The transpose runs the same passes backwards.  All transforms are the LDS
-// Stockham FFTs of sk_fft.h with twiddles from a table made in double
-// precision at creation.
+// Stockham FFTs of sk_fft.h (their twiddles from a table made in double
+// precision at creation); the per-element twiddles of pass 2 run as short
+// recurrences from values computed with sincospif.
 #include <algorithm>
 #include <cmath>
 #include <functional>
@@ -37,11 +39,15 @@ namespace sk {
 
 namespace {
 
-constexpr int kNT = 1024;        // threads per workgroup
-constexpr int kCap = 16384;      // complex values of one workgroup's transform buffer (128 KB)
+// Kernels come in two sizes: 512 threads with an 8192-value transform buffer
+// (64 KB of LDS: two workgroups per CU, so one's loads overlap the other's
+// transforms) and, for transforms longer than 8192 points, 1024 threads with
+// 16384 values.
+constexpr int kCap = 16384;      // largest transform buffer (complex values)
 constexpr int kLgCap = 14;
-constexpr int kMaxE = kCap / kNT;
-constexpr int kMaxQb = 2048;     // q columns of one pass-2 block (their twiddles live in LDS)
+constexpr int kLgCapS = 13;      // the default size
+constexpr int kMaxQb = 1024;     // q columns of one pass-2 block (their twiddles live in LDS)
+constexpr int kLgPMax = 8;       // rows of the pass-1 view: P = N/R <= 256
 constexpr int kSlots = 32;       // layers per launch
 
 struct FfLayers {
@@ -88,74 +94,121 @@ __device__ __forceinline__ void store_out(void *o, int dtype, int64_t j, float v
     ((float *)o)[j] = v;
 }
 
-// Column block of pass 1: W real columns of the P x M view (P * W <= 2 kCap).
-__device__ __host__ __forceinline__ int ff_lgW(int lgP) { return std::min(10, kLgCap + 1 - lgP); }
+// Geometry of a two-pass layer (all log2): N = N', M = D/2, P rows of R,
+// Q = N/M columns q, J = M/P outputs per residue; pass 1 column blocks of W.
+struct FfGeom {
+  int lgN, lgM, lgP, lgR, lgQ, lgJ, lgW;
+};
+__device__ __host__ __forceinline__ FfGeom ff_geom(int lgnp, int lgD, int lgcap = kLgCapS) {
+  FfGeom g;
+  g.lgN = lgnp;
+  g.lgM = lgD - 1;
+  g.lgQ = lgnp - g.lgM;
+  g.lgP = g.lgQ < kLgPMax ? g.lgQ : kLgPMax;
+  g.lgR = lgnp - g.lgP;
+  g.lgJ = g.lgM - g.lgP;
+  const int w = lgcap + 1 - g.lgP;  // P * W <= 2 * (buffer size) real values
+  g.lgW = std::min(std::min(10, w), g.lgR);
+  return g;
+}
 
-// Sign words of rows t < rows, columns [b0, b0 + 2^lgW) of the P x M view
-// into sw[t * nw + w] (nw = max(1, W / 32)).
-__device__ __forceinline__ void build_row_signs(uint32_t *sw, int64_t rows, int lgM, int64_t b0, int lgW,
+// exp(-2 pi i m / 2^lgL) for 0 <= m < 2^lgL
+__device__ __forceinline__ float2 cis_neg(int64_t m, int lgL) {
+  float s, c;
+  sincospif(ldexpf(-2.0f * (float)m, -lgL), &s, &c);
+  return make_float2(c, s);
+}
+
+// Sign words of rows t < rows, columns [b0, b0 + 2^lgW) of the P x R view
+// into sw[t * nw + w] (nw = W / 32; W >= 128).
+template <int NT>
+__device__ __forceinline__ void build_row_signs(uint32_t *sw, int64_t rows, int lgR, int64_t b0, int lgW,
                                                 uint32_t layer, Key key) {
-  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
-  for (int64_t e = threadIdx.x; e < rows * nw; e += kNT) {
-    const int64_t t = e / nw, w = e - t * nw;
-    const int64_t j = (t << lgM) + b0 + (w << 5);
+  const int lgnw = lgW - 5;
+  for (int64_t e = threadIdx.x; e < (rows << lgnw); e += NT) {
+    const int64_t t = e >> lgnw, w = e & ((1 << lgnw) - 1);
+    const int64_t j = (t << lgR) + b0 + (w << 5);
     sw[e] = sign_word((uint64_t)j, layer, key);
   }
 }
 
-__device__ __forceinline__ uint32_t row_sign_bit(const uint32_t *sw, int64_t t, int nw, int lgM, int64_t b0,
+__device__ __forceinline__ uint32_t row_sign_bit(const uint32_t *sw, int64_t t, int nw, int lgR, int64_t b0,
                                                  int64_t j) {
-  const int64_t base = ((t << lgM) + b0) >> 5;
-  return (sw[t * nw + ((j >> 5) - base)] >> (j & 31)) & 1u;
+  return (sw[t * nw + ((j - (t << lgR) - b0) >> 5)] >> (j & 31)) & 1u;
 }
 
 // ---------------------------------------------------------------------------
 // Pass 1, forward: u_r[b] = sum_t B x [t][b] w_P^{t r}, r <= P/2, for one
-// column block; two real columns per complex transform column.
+// column block of W; two real columns per complex transform column.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffr_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
                                                  int lgD, int64_t b_begin, int64_t bc,
                                                  const float2 *__restrict__ tw, int lgS, Key key) {
-  __shared__ float2 buf[kCap];
-  __shared__ uint32_t sw[4096];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
+  __shared__ uint32_t sw[1024];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
   const LayerDesc &ld = layers[g.layer[slot]];
-  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgW = ff_lgW(lgP), lgWc = lgW - 1;
-  const int64_t M = 1ll << lgM, n = ld.n;
+  const FfGeom fg = ff_geom(ld.lgnp, lgD);
+  const int lgR = fg.lgR, lgP = fg.lgP, lgW = fg.lgW, lgWc = lgW - 1;
+  const int64_t R = 1ll << lgR, n = ld.n;
   const int64_t b0 = (item - g.item0[slot]) << lgW;
-  const int64_t rows = std::min<int64_t>((n + M - 1) >> lgM, 1ll << lgP);
-  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
-  const uint32_t lid = (uint32_t)ld.layer_id;
-  build_row_signs(sw, rows, lgM, b0, lgW, lid, key);
+  const int64_t rows = std::min<int64_t>((n + R - 1) >> lgR, 1ll << lgP);
+  const int nw = 1 << (lgW - 5);
+  build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
   __syncthreads();
-  const void *x = g.x[slot];
   const int64_t xo = (b_begin + v) * n;
-  const int total = 1 << (lgP + lgWc);
-  for (int e = threadIdx.x; e < total; e += kNT) {
-    const int64_t t = e >> lgWc;
-    const int c = e & ((1 << lgWc) - 1);
-    float2 val = make_float2(0.f, 0.f);
+  // four real columns (two complex ones) per element; 16-byte (fp32) or 8-byte (bf16) loads when aligned
+  const int lgW4 = lgW - 2;
+  const int total = 1 << (lgP + lgW4);
+  const bool vec = dtype == SK_BF16 ? !(((uintptr_t)g.x[slot] + 2 * xo) & 7) : !(((uintptr_t)g.x[slot] + 4 * xo) & 15);
+  for (int e = threadIdx.x; e < total; e += NT) {
+    const int64_t t = e >> lgW4;
+    const int c4 = e & ((1 << lgW4) - 1);
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
     if (t < rows) {
-      const int64_t j = (t << lgM) + b0 + 2 * c;
-      if (j < n) val.x = flip(load_x(x, dtype, xo + j), row_sign_bit(sw, t, nw, lgM, b0, j));
-      if (j + 1 < n) val.y = flip(load_x(x, dtype, xo + j + 1), row_sign_bit(sw, t, nw, lgM, b0, j + 1));
+      const int64_t j = (t << lgR) + b0 + 4 * c4;
+      if (vec && j + 3 < n) {
+        if (dtype == SK_BF16) {
+          const uint2 u = *(const uint2 *)((const uint16_t *)g.x[slot] + xo + j);
+          a[0] = __uint_as_float(u.x << 16);
+          a[1] = __uint_as_float(u.x & 0xFFFF0000u);
+          a[2] = __uint_as_float(u.y << 16);
+          a[3] = __uint_as_float(u.y & 0xFFFF0000u);
+        } else {
+          const float4 f = *(const float4 *)((const float *)g.x[slot] + xo + j);
+          a[0] = f.x;
+          a[1] = f.y;
+          a[2] = f.z;
+          a[3] = f.w;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (j + k < n) a[k] = load_x(g.x[slot], dtype, xo + j + k);
+      }
+      const uint32_t wd = sw[t * nw + (((b0 + 4 * c4) >> 5) - (b0 >> 5))] >> ((b0 + 4 * c4) & 31);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) a[k] = flip(a[k], (wd >> k) & 1u);
     }
-    buf[e] = val;
+    buf[(t << lgWc) + 2 * c4] = make_float2(a[0], a[1]);
+    buf[(t << lgWc) + 2 * c4 + 1] = make_float2(a[2], a[3]);
   }
-  lds_fft<false, kNT, kMaxE>(buf, lgP, lgWc, tw, lgS);
+  lds_fft<false, NT, MAXE>(buf, lgP, lgWc, tw, lgS);
   // split the two real columns and write r = 0 .. P/2
   float *u = g.u[slot] + v * g.us[slot];
   const int P = 1 << lgP;
   const int tot2 = (P / 2 + 1) << lgWc;
-  for (int e = threadIdx.x; e < tot2; e += kNT) {
+  for (int e = threadIdx.x; e < tot2; e += NT) {
     const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
     const float2 zr = buf[(r << lgWc) + c];
     const float2 zm = buf[(((P - r) & (P - 1)) << lgWc) + c];
     const float4 o = make_float4(0.5f * (zr.x + zm.x), 0.5f * (zr.y - zm.y),   // (Z_r + conj Z_{P-r}) / 2
                                  0.5f * (zr.y + zm.y), 0.5f * (zm.x - zr.x));  // -i (Z_r - conj Z_{P-r}) / 2
-    *(float4 *)(u + (((int64_t)r << lgM) + b0 + 2 * c) * 2) = o;
+    *(float4 *)(u + (((int64_t)r << lgR) + b0 + 2 * c) * 2) = o;
   }
 }
 
@@ -163,29 +216,35 @@ __global__ __launch_bounds__(kNT) void k_ffr_fwd(const LayerDesc *__restrict__ l
 // Pass 2, forward: for residue r (and P - r) of one layer and vector, the J
 // outputs X_{r + P j} (and X_{(P-r) + P (J-1-j)}), scaled by G into y.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffq_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
                                                  int64_t bc, const float *__restrict__ gtab, float c1, float c2,
                                                  const float2 *__restrict__ tw, int lgS) {
-  __shared__ float2 buf[kCap];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
   __shared__ float2 tq[kMaxQb];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
   const LayerDesc &ld = layers[g.layer[slot]];
-  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgJ = lgM - lgP, lgN = ld.lgnp;
+  const FfGeom fg = ff_geom(ld.lgnp, lgD);
+  const int lgM = fg.lgM, lgP = fg.lgP, lgJ = fg.lgJ, lgQ = fg.lgQ, lgR = fg.lgR, lgN = fg.lgN;
   const int P = 1 << lgP, J = 1 << lgJ;
   const int r = (int)(item - g.item0[slot]);
   const bool pair = r > 0 && 2 * r < P;
-  const int lgQb = std::min(std::min(lgP, kLgCap - lgJ), 11);
-  const int Qb = 1 << lgQb, nqb = P >> lgQb;
-  const int lgG = lgJ <= 10 ? 10 - lgJ : 0;  // threads per output row
+  const int lgQb = std::min(std::min(lgQ, LGCAP - lgJ), LGNT);
+  const int Qb = 1 << lgQb, nqb = 1 << (lgQ - lgQb);
+  const int lgG = lgJ <= LGNT ? LGNT - lgJ : 0;  // threads per output row
   const int G = 1 << lgG;
-  const int rpt = lgJ > 10 ? 1 << (lgJ - 10) : 1;  // rows per thread
+  const int rpt = lgJ > LGNT ? 1 << (lgJ - LGNT) : 1;  // rows per thread
   const int j0 = threadIdx.x >> lgG, gi = threadIdx.x & (G - 1);
-  const float2 *u = (const float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgM);
+  const float2 *u = (const float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgR);
   float *y = g.y[slot] + v * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)ld.layer_id * ((int64_t)1 << lgD);
-  const float tscale = ldexpf(-2.0f, -lgN);  // -2 / N
+  // load mapping: each thread keeps column qq, rows s = s0 + i * ds
+  const int qq_l = threadIdx.x & (Qb - 1), s0 = threadIdx.x >> lgQb, ds = NT >> lgQb;
+  const float2 rstep = cis_neg(((int64_t)ds * r) & ((1ll << lgM) - 1), lgM);   // w_M^{ds r}
+  const float2 rstart = cis_neg(((int64_t)s0 * r) & ((1ll << lgM) - 1), lgM);  // w_M^{s0 r}
   // y (+)= the scaled sums of output row j (sets A and B, X_{N/2} for r = 0)
   auto emit = [&](int j, float2 a, float2 b, float2 nn, bool add) {
     const int64_t ka = r + ((int64_t)j << lgP);
@@ -211,28 +270,33 @@ __global__ __launch_bounds__(kNT) void k_ffq_fwd(const LayerDesc *__restrict__ l
     if (pair) *pb = vb;
   };
   for (int qb = 0; qb < nqb; ++qb) {
-    const int q0 = qb << lgQb;
-    for (int qq = threadIdx.x; qq < Qb; qq += kNT) {
-      float sn, cs;
-      sincospif(tscale * (float)((int64_t)(q0 + qq) * r), &sn, &cs);  // w_N^{q r}
-      tq[qq] = make_float2(cs, sn);
+    const int64_t q0 = (int64_t)qb << lgQb;
+    for (int qq = threadIdx.x; qq < Qb; qq += NT) tq[qq] = cis_neg((q0 + qq) * r, lgN);  // w_N^{q r}
+    {
+      float2 tr = rstart;
+      for (int s = s0, i = 0; s < J; s += ds, ++i) {
+        const float2 val = u[q0 + qq_l + ((int64_t)s << lgQ)];
+        buf[(s << lgQb) + qq_l] = cmul(val, tr);
+        tr = cmul(tr, rstep);
+      }
     }
-    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
-      const int s = e >> lgQb, qq = e & (Qb - 1);
-      const float2 val = u[q0 + qq + ((int64_t)s << lgP)];
-      buf[e] = cmul(val, twiddle<false>(tw, lgS, lgM, (int64_t)s * r));
-    }
-    lds_fft<false, kNT, kMaxE>(buf, lgJ, lgQb, tw, lgS);
+    lds_fft<false, NT, MAXE>(buf, lgJ, lgQb, tw, lgS);
     for (int i = 0; i < rpt; ++i) {
-      const int j = j0 + (i << (10 - lgG));
+      const int j = j0 + (i << (LGNT - lgG));
       float2 a = make_float2(0.f, 0.f), b = a, nn = a;
+      // q = q0 + gi + G m: w_R^{q j} and w_Q^{q} by recurrence over m (at most 16 steps)
+      float2 wr = cis_neg(((q0 + gi) * j) & ((1ll << lgR) - 1), lgR);
+      const float2 wrs = cis_neg(((int64_t)G * j) & ((1ll << lgR) - 1), lgR);
+      float2 wq = cis_neg((q0 + gi) & ((1ll << lgQ) - 1), lgQ);
+      const float2 wqs = cis_neg(G & ((1 << lgQ) - 1), lgQ);
       for (int qq = gi; qq < Qb; qq += G) {
-        const int q = q0 + qq;
         const float2 w = buf[(j << lgQb) + qq];
-        const float2 tA = cmul(cmul(w, tq[qq]), twiddle<false>(tw, lgS, lgM, (int64_t)q * j));
+        const float2 tA = cmul(cmul(w, tq[qq]), wr);
         a = cadd(a, tA);
-        if (pair) b = cadd(b, cmul(cconj(tA), twiddle<false>(tw, lgS, lgP, q)));
-        if (r == 0 && j == 0) nn = (q & 1) ? csub(nn, w) : cadd(nn, w);
+        if (pair) b = cadd(b, cmul(cconj(tA), wq));
+        if (r == 0 && j == 0) nn = ((q0 + qq) & 1) ? csub(nn, w) : cadd(nn, w);
+        wr = cmul(wr, wrs);
+        wq = cmul(wq, wqs);
       }
       if (G == 1) {
         emit(j, a, b, nn, qb > 0);
@@ -240,15 +304,15 @@ __global__ __launch_bounds__(kNT) void k_ffq_fwd(const LayerDesc *__restrict__ l
         // combine the G partial sums of this row in a fixed order
         __syncthreads();
         buf[threadIdx.x] = a;
-        buf[kNT + threadIdx.x] = b;
-        buf[2 * kNT + threadIdx.x] = nn;
+        buf[NT + threadIdx.x] = b;
+        buf[2 * NT + threadIdx.x] = nn;
         __syncthreads();
         if ((int)threadIdx.x < J) {
           float2 sa = make_float2(0.f, 0.f), sb = sa, sn2 = sa;
           for (int k = 0; k < G; ++k) {
             sa = cadd(sa, buf[(threadIdx.x << lgG) + k]);
-            sb = cadd(sb, buf[kNT + (threadIdx.x << lgG) + k]);
-            sn2 = cadd(sn2, buf[2 * kNT + (threadIdx.x << lgG) + k]);
+            sb = cadd(sb, buf[NT + (threadIdx.x << lgG) + k]);
+            sn2 = cadd(sn2, buf[2 * NT + (threadIdx.x << lgG) + k]);
           }
           emit((int)threadIdx.x, sa, sb, sn2, qb > 0);
         }
@@ -261,11 +325,13 @@ __global__ __launch_bounds__(kNT) void k_ffq_fwd(const LayerDesc *__restrict__ l
 // ---------------------------------------------------------------------------
 // Layers with N = D and n <= 16384: X_{c + (N/L) e} = FFT_L(v_b w_N^{b c})[e].
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffs_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
                                                  int lgD, int64_t b_begin, int64_t bc, const float *__restrict__ gtab,
                                                  float c1, float c2, const float2 *__restrict__ tw, int lgS, Key key) {
-  __shared__ float2 buf[kCap];
-  __shared__ uint32_t sw[kCap / 32];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
+  __shared__ uint32_t sw[CAP / 32];
   int64_t item, v;
   if (!xcd_decode(g.n, bc, item, v)) return;
   const int slot = (int)item;
@@ -275,16 +341,16 @@ __global__ __launch_bounds__(kNT) void k_ffs_fwd(const LayerDesc *__restrict__ l
   while ((1ll << lgL) < n) ++lgL;
   const int L = 1 << lgL;
   const int lgcs = lgD - lgL;                       // log2 of the number of c values
-  const int lgcg = std::min(lgcs, kLgCap - lgL);    // c values per group
+  const int lgcg = std::min(lgcs, LGCAP - lgL);    // c values per group
   const uint32_t lid = (uint32_t)ld.layer_id;
-  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += kNT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
+  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += NT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
   __syncthreads();
   const void *x = g.x[slot];
   const int64_t xo = (b_begin + v) * n;
   float *y = g.y[slot] + v * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
   for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
-    for (int e = threadIdx.x; e < (L << lgcg); e += kNT) {
+    for (int e = threadIdx.x; e < (L << lgcg); e += NT) {
       const int b = e >> lgcg, cc = e & ((1 << lgcg) - 1);
       float2 val = make_float2(0.f, 0.f);
       if (b < n) {
@@ -293,8 +359,8 @@ __global__ __launch_bounds__(kNT) void k_ffs_fwd(const LayerDesc *__restrict__ l
       }
       buf[e] = val;
     }
-    lds_fft<false, kNT, kMaxE>(buf, lgL, lgcg, tw, lgS);
-    for (int e = threadIdx.x; e < ((L / 2) << lgcg); e += kNT) {
+    lds_fft<false, NT, MAXE>(buf, lgL, lgcg, tw, lgS);
+    for (int e = threadIdx.x; e < ((L / 2) << lgcg); e += NT) {
       const int ee = e >> lgcg, cc = e & ((1 << lgcg) - 1);
       const int64_t k = (c0 + cc) + ((int64_t)ee << lgcs);
       const float2 X = buf[e];
@@ -352,53 +418,63 @@ __device__ __forceinline__ float2 coef(const float *z, const float *gl, int64_t 
 }
 
 // ---------------------------------------------------------------------------
-// Pass 2, transpose: E~_r[q + P s] (r <= P/2) from the coefficients of
-// residues r and P - r (one inverse J-point transform per column q).
+// Pass 2, transpose: E~_r[q + Q s] (r <= P/2) from the coefficients of
+// residues r and P - r (one inverse J-point transform per column q):
+//   a_q[m] = c_{r+Pm} w_R^{-q m} + conj(c_{P-r+P(J-1-m)}) w_R^{q (J-m)},
+//   E~_r[q + Q s] = w_N^{-q r} w_M^{-s r} IFFT_J(a_q)[s]  (+ (-1)^q c_{N/2}, r = 0).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffq_T(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffq_T(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
                                                const float *__restrict__ z, int64_t b_begin, int64_t bc,
                                                const float *__restrict__ gtab, float c1, float c2,
                                                const float2 *__restrict__ tw, int lgS) {
-  __shared__ float2 buf[kCap];
-  __shared__ float2 tq[kMaxQb];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
   const LayerDesc &ld = layers[g.layer[slot]];
-  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgJ = lgM - lgP, lgN = ld.lgnp;
+  const FfGeom fg = ff_geom(ld.lgnp, lgD);
+  const int lgM = fg.lgM, lgP = fg.lgP, lgJ = fg.lgJ, lgQ = fg.lgQ, lgR = fg.lgR, lgN = fg.lgN;
   const int P = 1 << lgP, J = 1 << lgJ;
   const int r = (int)(item - g.item0[slot]);
   const bool pair = r > 0 && 2 * r < P;
-  const int lgQb = std::min(std::min(lgP, kLgCap - lgJ), 11);
-  const int Qb = 1 << lgQb, nqb = P >> lgQb;
+  const int lgQb = std::min(std::min(lgQ, LGCAP - lgJ), LGNT);
+  const int Qb = 1 << lgQb, nqb = 1 << (lgQ - lgQb);
   const float *zv = z + (b_begin + v) * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)ld.layer_id * ((int64_t)1 << lgD);
   const float cN2 = c1 * gl[1] * zv[1];
-  float2 *u = (float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgM);
-  const float tscale = ldexpf(-2.0f, -lgN);
+  float2 *u = (float2 *)(g.u[slot] + v * g.us[slot]) + ((int64_t)r << lgR);
+  const int qq_l = threadIdx.x & (Qb - 1), s0 = threadIdx.x >> lgQb, ds = NT >> lgQb;
+  const float2 rstep = cis_neg(((int64_t)ds * r) & ((1ll << lgM) - 1), lgM);   // w_M^{ds r}
+  const float2 rstart = cis_neg(((int64_t)s0 * r) & ((1ll << lgM) - 1), lgM);  // w_M^{s0 r}
   for (int qb = 0; qb < nqb; ++qb) {
-    const int q0 = qb << lgQb;
-    for (int qq = threadIdx.x; qq < Qb; qq += kNT) {
-      float sn, cs;
-      sincospif(tscale * (float)((int64_t)(q0 + qq) * r), &sn, &cs);
-      tq[qq] = make_float2(cs, sn);  // w_N^{q r}
-    }
-    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
-      const int m = e >> lgQb, qq = e & (Qb - 1);
-      const int64_t q = q0 + qq;
-      float2 a = cmul(coef(zv, gl, r + ((int64_t)m << lgP), c1, c2), twiddle<true>(tw, lgS, lgM, q * m));
-      if (pair) {
-        const float2 cp = coef(zv, gl, (P - r) + ((int64_t)(J - m - 1) << lgP), c1, c2);
-        a = cadd(a, cmul(cconj(cp), twiddle<false>(tw, lgS, lgM, q * (J - m))));
+    const int64_t q = ((int64_t)qb << lgQb) + qq_l;
+    // rows m = s0 + i ds: w_R^{q m} by recurrence; w_R^{q (J - m)} = w_Q^{q} conj(w_R^{q m})
+    {
+      float2 wm = cis_neg((q * s0) & ((1ll << lgR) - 1), lgR);
+      const float2 wst = cis_neg((q * ds) & ((1ll << lgR) - 1), lgR);
+      const float2 wqq = cis_neg(q & ((1ll << lgQ) - 1), lgQ);
+      for (int m = s0; m < J; m += ds) {
+        float2 a = cmulc(coef(zv, gl, r + ((int64_t)m << lgP), c1, c2), wm);
+        if (pair) {
+          const float2 cp = coef(zv, gl, (P - r) + ((int64_t)(J - m - 1) << lgP), c1, c2);
+          a = cadd(a, cmul(cconj(cp), cmulc(wqq, wm)));
+        }
+        buf[(m << lgQb) + qq_l] = a;
+        wm = cmul(wm, wst);
       }
-      buf[e] = a;
     }
-    lds_fft<true, kNT, kMaxE>(buf, lgJ, lgQb, tw, lgS);
-    for (int e = threadIdx.x; e < (J << lgQb); e += kNT) {
-      const int s = e >> lgQb, qq = e & (Qb - 1);
-      float2 E = cmulc(cmulc(buf[e], tq[qq]), twiddle<false>(tw, lgS, lgM, (int64_t)s * r));
-      if (r == 0) E.x += ((q0 + qq) & 1) ? -cN2 : cN2;
-      u[q0 + qq + ((int64_t)s << lgP)] = E;
+    lds_fft<true, NT, MAXE>(buf, lgJ, lgQb, tw, lgS);
+    {
+      const float2 tq = cis_neg((q * r) & ((1ll << lgN) - 1), lgN);  // w_N^{q r}
+      float2 tr = rstart;
+      for (int s = s0; s < J; s += ds) {
+        float2 E = cmulc(cmulc(buf[(s << lgQb) + qq_l], tq), tr);
+        if (r == 0) E.x += (q & 1) ? -cN2 : cN2;
+        u[q + ((int64_t)s << lgQ)] = E;
+        tr = cmul(tr, rstep);
+      }
     }
     __syncthreads();
   }
@@ -409,49 +485,52 @@ __global__ __launch_bounds__(kNT) void k_ffq_T(const LayerDesc *__restrict__ lay
 // column block (a complex-to-real inverse transform of two columns at a
 // time), signed, plus theta0, truncated to the layer.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffr_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffr_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
                                                int lgD, int64_t b_begin, int64_t bc,
                                                const float2 *__restrict__ tw, int lgS, Key key) {
-  __shared__ float2 buf[kCap];
-  __shared__ uint32_t sw[4096];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
+  __shared__ uint32_t sw[1024];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
   const LayerDesc &ld = layers[g.layer[slot]];
-  const int lgM = lgD - 1, lgP = ld.lgnp - lgM, lgW = ff_lgW(lgP), lgWc = lgW - 1;
-  const int64_t M = 1ll << lgM, n = ld.n;
+  const FfGeom fg = ff_geom(ld.lgnp, lgD);
+  const int lgR = fg.lgR, lgP = fg.lgP, lgW = fg.lgW, lgWc = lgW - 1;
+  const int64_t R = 1ll << lgR, n = ld.n;
   const int P = 1 << lgP;
   const int64_t b0 = (item - g.item0[slot]) << lgW;
-  const int64_t rows = std::min<int64_t>((n + M - 1) >> lgM, (int64_t)P);
-  const int nw = lgW >= 5 ? 1 << (lgW - 5) : 1;
-  build_row_signs(sw, rows, lgM, b0, lgW, (uint32_t)ld.layer_id, key);
+  const int64_t rows = std::min<int64_t>((n + R - 1) >> lgR, (int64_t)P);
+  const int nw = 1 << (lgW - 5);
+  build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
   const float *u = g.u[slot] + v * g.us[slot];
   const int tot = (P / 2 + 1) << lgWc;
-  for (int e = threadIdx.x; e < tot; e += kNT) {
+  for (int e = threadIdx.x; e < tot; e += NT) {
     const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
-    const float4 E = *(const float4 *)(u + (((int64_t)r << lgM) + b0 + 2 * c) * 2);
+    const float4 E = *(const float4 *)(u + (((int64_t)r << lgR) + b0 + 2 * c) * 2);
     const bool edge = r == 0 || 2 * r == P;
     const float2 ha = edge ? make_float2(E.x, 0.f) : make_float2(0.5f * E.x, 0.5f * E.y);
     const float2 hb = edge ? make_float2(E.z, 0.f) : make_float2(0.5f * E.z, 0.5f * E.w);
     buf[(r << lgWc) + c] = make_float2(ha.x - hb.y, ha.y + hb.x);          // H_a + i H_b
     if (!edge) buf[((P - r) << lgWc) + c] = make_float2(ha.x + hb.y, hb.x - ha.y);  // conj H_a + i conj H_b
   }
-  lds_fft<true, kNT, kMaxE>(buf, lgP, lgWc, tw, lgS);
+  lds_fft<true, NT, MAXE>(buf, lgP, lgWc, tw, lgS);
   void *o = (void *)g.x[slot];
   const float *th = g.th[slot];
   const int64_t oo = (b_begin + v) * n;
-  for (int e = threadIdx.x; e < (int)(rows << lgWc); e += kNT) {
+  for (int e = threadIdx.x; e < (int)(rows << lgWc); e += NT) {
     const int64_t t = e >> lgWc;
     const int c = e & ((1 << lgWc) - 1);
     const float2 zt = buf[e];
-    const int64_t j = (t << lgM) + b0 + 2 * c;
+    const int64_t j = (t << lgR) + b0 + 2 * c;
     if (j < n) {
-      float a = flip(zt.x, row_sign_bit(sw, t, nw, lgM, b0, j));
+      float a = flip(zt.x, row_sign_bit(sw, t, nw, lgR, b0, j));
       if (th) a += th[j];
       store_out(o, out_dtype, oo + j, a);
     }
     if (j + 1 < n) {
-      float b = flip(zt.y, row_sign_bit(sw, t, nw, lgM, b0, j + 1));
+      float b = flip(zt.y, row_sign_bit(sw, t, nw, lgR, b0, j + 1));
       if (th) b += th[j + 1];
       store_out(o, out_dtype, oo + j + 1, b);
     }
@@ -461,12 +540,14 @@ __global__ __launch_bounds__(kNT) void k_ffr_T(const LayerDesc *__restrict__ lay
 // ---------------------------------------------------------------------------
 // Small layers, transpose: x_b = Re sum_c w_N^{-b c} IFFT_L(coef_c)[b].
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_ffs_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
+template <int LGNT, int LGCAP>
+__global__ __launch_bounds__(1 << LGNT) void k_ffs_T(const LayerDesc *__restrict__ layers, FfLayers g, int out_dtype,
                                                int lgD, const float *__restrict__ z, int64_t b_begin, int64_t bc,
                                                const float *__restrict__ gtab, float c1, float c2,
                                                const float2 *__restrict__ tw, int lgS, Key key) {
-  __shared__ float2 buf[kCap];
-  __shared__ uint32_t sw[kCap / 32];
+  constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
+  __shared__ float2 buf[CAP];
+  __shared__ uint32_t sw[CAP / 32];
   int64_t item, v;
   if (!xcd_decode(g.n, bc, item, v)) return;
   const int slot = (int)item;
@@ -476,17 +557,17 @@ __global__ __launch_bounds__(kNT) void k_ffs_T(const LayerDesc *__restrict__ lay
   while ((1ll << lgL) < n) ++lgL;
   const int L = 1 << lgL;
   const int lgcs = lgD - lgL;
-  const int lgcg = std::min(lgcs, kLgCap - lgL);
+  const int lgcg = std::min(lgcs, LGCAP - lgL);
   const uint32_t lid = (uint32_t)ld.layer_id;
-  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += kNT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
+  for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += NT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
   const float *zv = z + (b_begin + v) * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
-  float acc[kMaxE];
+  float acc[MAXE];
 #pragma unroll
-  for (int i = 0; i < kMaxE; ++i) acc[i] = 0.f;
+  for (int i = 0; i < MAXE; ++i) acc[i] = 0.f;
   for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
     __syncthreads();
-    for (int e = threadIdx.x; e < (L << lgcg); e += kNT) {
+    for (int e = threadIdx.x; e < (L << lgcg); e += NT) {
       const int ee = e >> lgcg, cc = e & ((1 << lgcg) - 1);
       const int c = c0 + cc;
       float2 a = make_float2(0.f, 0.f);
@@ -497,11 +578,11 @@ __global__ __launch_bounds__(kNT) void k_ffs_T(const LayerDesc *__restrict__ lay
       }
       buf[e] = a;
     }
-    lds_fft<true, kNT, kMaxE>(buf, lgL, lgcg, tw, lgS);
+    lds_fft<true, NT, MAXE>(buf, lgL, lgcg, tw, lgS);
     for (int cc = 0; cc < (1 << lgcg); ++cc) {
 #pragma unroll
-      for (int i = 0; i < kMaxE; ++i) {
-        const int b = threadIdx.x + i * kNT;
+      for (int i = 0; i < MAXE; ++i) {
+        const int b = threadIdx.x + i * NT;
         if (b < L) {
           const float2 w = buf[(b << lgcg) + cc];
           const float2 t = twiddle<false>(tw, lgS, lgD, (int64_t)b * (c0 + cc));
@@ -514,8 +595,8 @@ __global__ __launch_bounds__(kNT) void k_ffs_T(const LayerDesc *__restrict__ lay
   const float *th = g.th[slot];
   const int64_t oo = (b_begin + v) * n;
 #pragma unroll
-  for (int i = 0; i < kMaxE; ++i) {
-    const int b = threadIdx.x + i * kNT;
+  for (int i = 0; i < MAXE; ++i) {
+    const int b = threadIdx.x + i * NT;
     if (b < n) {
       float a = flip(acc[i], (sw[b >> 5] >> (b & 31)) & 1u);
       if (th) a += th[b];
@@ -542,9 +623,16 @@ bool afjlf_small_layer(const sk_sketch *s, int layer) {
   return ld.np == s->D && ld.n <= kCap;
 }
 
-// floats per vector of a layer's pass buffer: (P/2 + 1) M complex
+// floats per vector of a layer's pass buffer: (P/2 + 1) R complex
 int64_t afjlf_u_floats(const sk_sketch *s, int layer) {
-  return afjlf_small_layer(s, layer) ? 0 : s->layers[layer].np + s->D;
+  if (afjlf_small_layer(s, layer)) return 0;
+  const FfGeom fg = ff_geom(s->layers[layer].lgnp, lg2(s->D));
+  return s->layers[layer].np + (2ll << fg.lgR);
+}
+
+bool afjlf_two_pass_ok(int lgnp, int lgD) {
+  const FfGeom fg = ff_geom(lgnp, lgD);
+  return fg.lgQ >= 1 && fg.lgJ >= 0 && fg.lgJ <= kLgCap;
 }
 
 int64_t afjlf_bytes_per_vector(const sk_sketch *s, int l0, int l1, bool transpose) {
@@ -566,51 +654,63 @@ void afjlf_twiddles(int64_t D, std::vector<float> &host, int &lgS) {
 
 namespace {
 
+// whether a two-pass layer's residue pass needs the 16384-value kernels
+bool big_residue(const sk_sketch *s, int layer) {
+  return ff_geom(s->layers[layer].lgnp, lg2(s->D)).lgJ > kLgCapS;
+}
+// whether a one-kernel layer needs the 16384-value kernels
+bool big_small(const sk_sketch *s, int layer) { return s->layers[layer].n > (1 << kLgCapS); }
+
 // The call's general (two-pass) layers in groups: a group holds up to kSlots
-// layers whose pass buffers for `tile` vectors fit in ufl floats; a layer too
-// large for the whole chunk is a group of its own, run in vector tiles.
+// layers of one residue-kernel size whose pass buffers for `tile` vectors fit
+// in ufl floats; a layer too large for the whole chunk is a group of its own,
+// run in vector tiles.
 template <class F>
 void for_groups(const sk_sketch *s, int l0, int l1, int64_t bc, int64_t ufl, F &&f) {
-  int l = l0;
-  while (l < l1) {
-    if (afjlf_small_layer(s, l)) {
-      ++l;
-      continue;
-    }
-    std::vector<int> grp{l};
-    int64_t used = afjlf_u_floats(s, l) * bc;
-    int64_t tile = bc;
-    int lend = l + 1;
-    if (used > ufl) {
-      tile = std::max<int64_t>(1, ufl / afjlf_u_floats(s, l));
-    } else {
-      while (lend < l1 && (int)grp.size() < kSlots) {
-        if (afjlf_small_layer(s, lend)) {
-          ++lend;
-          continue;
-        }
-        const int64_t nd = afjlf_u_floats(s, lend) * bc;
-        if (used + nd > ufl) break;
-        used += nd;
-        grp.push_back(lend++);
+  for (int big = 0; big < 2; ++big) {
+    int l = l0;
+    while (l < l1) {
+      if (afjlf_small_layer(s, l) || (int)big_residue(s, l) != big) {
+        ++l;
+        continue;
       }
+      std::vector<int> grp{l};
+      int64_t used = afjlf_u_floats(s, l) * bc;
+      int64_t tile = bc;
+      int lend = l + 1;
+      if (used > ufl) {
+        tile = std::max<int64_t>(1, ufl / afjlf_u_floats(s, l));
+      } else {
+        while (lend < l1 && (int)grp.size() < kSlots) {
+          if (afjlf_small_layer(s, lend) || (int)big_residue(s, lend) != big) {
+            ++lend;
+            continue;
+          }
+          const int64_t nd = afjlf_u_floats(s, lend) * bc;
+          if (used + nd > ufl) break;
+          used += nd;
+          grp.push_back(lend++);
+        }
+      }
+      f(grp, tile, big != 0);
+      l = lend;
     }
-    f(grp, tile);
-    l = lend;
   }
 }
 
-void small_groups(const sk_sketch *s, int l0, int l1, const std::function<void(FfLayers &)> &f) {
-  FfLayers g{};
-  for (int l = l0; l < l1; ++l) {
-    if (!afjlf_small_layer(s, l)) continue;
-    g.layer[g.n++] = l;
-    if (g.n == kSlots) {
-      f(g);
-      g = FfLayers{};
+void small_groups(const sk_sketch *s, int l0, int l1, const std::function<void(FfLayers &, bool)> &f) {
+  for (int big = 0; big < 2; ++big) {
+    FfLayers g{};
+    for (int l = l0; l < l1; ++l) {
+      if (!afjlf_small_layer(s, l) || (int)big_small(s, l) != big) continue;
+      g.layer[g.n++] = l;
+      if (g.n == kSlots) {
+        f(g, big != 0);
+        g = FfLayers{};
+      }
     }
+    if (g.n) f(g, big != 0);
   }
-  if (g.n) f(g);
 }
 
 }  // namespace
@@ -628,18 +728,24 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
   float *ybase = ws, *ubase = ws + (int64_t)nl * lstride;
   const int64_t ufl = ws_floats - (int64_t)nl * lstride;
   const float2 *tw = (const float2 *)s->d_ftw;
-  small_groups(s, l0, l1, [&](FfLayers &g) {
+  small_groups(s, l0, l1, [&](FfLayers &g, bool big) {
     int64_t gb = 0;
     for (int i = 0; i < g.n; ++i) {
       g.x[i] = grads[g.layer[i] - l0];
       g.y[i] = ybase + (int64_t)(g.layer[i] - l0) * lstride;
       gb += bc * s->layers[g.layer[i]].n * esz;
     }
-    SK_PROF(SK_PROF_FF_ROWS, gb,
-            hipLaunchKernelGGL(k_ffs_fwd, dim3((unsigned)(g.n * ceil8(bc))), dim3(kNT), 0, st, s->d_layers, g,
-                               dtype, lgD, b_begin, bc, s->d_gtab, c1, c2, tw, s->ftw_lg, s->key));
+    const dim3 grid((unsigned)(g.n * ceil8(bc)));
+    SK_PROF(SK_PROF_FF_ROWS, gb, {
+      if (big)
+        hipLaunchKernelGGL((k_ffs_fwd<10, 14>), grid, dim3(1024), 0, st, s->d_layers, g, dtype, lgD, b_begin, bc,
+                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+      else
+        hipLaunchKernelGGL((k_ffs_fwd<9, 13>), grid, dim3(512), 0, st, s->d_layers, g, dtype, lgD, b_begin, bc,
+                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+    });
   });
-  for_groups(s, l0, l1, bc, ufl, [&](const std::vector<int> &grp, int64_t tile) {
+  for_groups(s, l0, l1, bc, ufl, [&](const std::vector<int> &grp, int64_t tile, bool big) {
     for (int64_t t0 = 0; t0 < bc; t0 += tile) {
       const int64_t tb = std::min(tile, bc - t0);
       FfLayers g1{}, g2{};
@@ -647,25 +753,31 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
       for (int l : grp) {
         const int i = g1.n;
         const LayerDesc &ld = s->layers[l];
-        const int lgP = ld.lgnp - (lgD - 1);
+        const FfGeom fg = ff_geom(ld.lgnp, lgD);
         gb += tb * ld.n * esz;
         g1.layer[i] = g2.layer[i] = l;
         g1.x[i] = grads[l - l0];
         g1.u[i] = g2.u[i] = ubase + off;
         g1.us[i] = g2.us[i] = afjlf_u_floats(s, l);
         g2.y[i] = ybase + (int64_t)(l - l0) * lstride + t0 * D;
-        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (lgD - 1 - ff_lgW(lgP)));
-        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (lgP - 1)) + 1;
+        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (fg.lgR - fg.lgW));
+        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (fg.lgP - 1)) + 1;
         off += g1.us[i] * tb;
         ++g1.n;
         ++g2.n;
       }
       SK_PROF(SK_PROF_FF_ROWS, gb,
-              hipLaunchKernelGGL(k_ffr_fwd, dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(kNT), 0, st,
-                                 s->d_layers, g1, dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
-      SK_PROF(SK_PROF_FF_RES, 0,
-              hipLaunchKernelGGL(k_ffq_fwd, dim3((unsigned)(g2.item0[g2.n] * ceil8(tb))), dim3(kNT), 0, st,
-                                 s->d_layers, g2, lgD, tb, s->d_gtab, c1, c2, tw, s->ftw_lg));
+              hipLaunchKernelGGL((k_ffr_fwd<9, 13>), dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(512), 0,
+                                 st, s->d_layers, g1, dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
+      const dim3 grid2((unsigned)(g2.item0[g2.n] * ceil8(tb)));
+      SK_PROF(SK_PROF_FF_RES, 0, {
+        if (big)
+          hipLaunchKernelGGL((k_ffq_fwd<10, 14>), grid2, dim3(1024), 0, st, s->d_layers, g2, lgD, tb, s->d_gtab, c1,
+                             c2, tw, s->ftw_lg);
+        else
+          hipLaunchKernelGGL((k_ffq_fwd<9, 13>), grid2, dim3(512), 0, st, s->d_layers, g2, lgD, tb, s->d_gtab, c1,
+                             c2, tw, s->ftw_lg);
+      });
     }
   });
   const dim3 gt((unsigned)((D / 4 + 255) / 256), (unsigned)bc);
@@ -681,7 +793,7 @@ void run_afjlf_T(sk_sketch *s, int l0, int l1, const float *z, int64_t b_begin, 
   const int lgD = lg2(D);
   const float c1 = (float)(1.0 / std::sqrt((double)D)), c2 = (float)std::sqrt(2.0 / (double)D);
   const float2 *tw = (const float2 *)s->d_ftw;
-  small_groups(s, l0, l1, [&](FfLayers &g) {
+  small_groups(s, l0, l1, [&](FfLayers &g, bool big) {
     int64_t ob = 0;
     for (int i = 0; i < g.n; ++i) {
       const int64_t n = s->layers[g.layer[i]].n;
@@ -689,11 +801,17 @@ void run_afjlf_T(sk_sketch *s, int l0, int l1, const float *z, int64_t b_begin, 
       g.th[i] = theta0 ? (const float *)theta0[g.layer[i] - l0] : nullptr;
       ob += bc * n * osz + (g.th[i] ? n * 4 : 0);
     }
-    SK_PROF(SK_PROF_GATHER, ob,
-            hipLaunchKernelGGL(k_ffs_T, dim3((unsigned)(g.n * ceil8(bc))), dim3(kNT), 0, st, s->d_layers, g,
-                               out_dtype, lgD, z, b_begin, bc, s->d_gtab, c1, c2, tw, s->ftw_lg, s->key));
+    const dim3 grid((unsigned)(g.n * ceil8(bc)));
+    SK_PROF(SK_PROF_GATHER, ob, {
+      if (big)
+        hipLaunchKernelGGL((k_ffs_T<10, 14>), grid, dim3(1024), 0, st, s->d_layers, g, out_dtype, lgD, z, b_begin,
+                           bc, s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+      else
+        hipLaunchKernelGGL((k_ffs_T<9, 13>), grid, dim3(512), 0, st, s->d_layers, g, out_dtype, lgD, z, b_begin, bc,
+                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+    });
   });
-  for_groups(s, l0, l1, bc, ws_floats, [&](const std::vector<int> &grp, int64_t tile) {
+  for_groups(s, l0, l1, bc, ws_floats, [&](const std::vector<int> &grp, int64_t tile, bool big) {
     for (int64_t t0 = 0; t0 < bc; t0 += tile) {
       const int64_t tb = std::min(tile, bc - t0);
       FfLayers g1{}, g2{};
@@ -701,24 +819,30 @@ void run_afjlf_T(sk_sketch *s, int l0, int l1, const float *z, int64_t b_begin, 
       for (int l : grp) {
         const int i = g1.n;
         const LayerDesc &ld = s->layers[l];
-        const int lgP = ld.lgnp - (lgD - 1);
+        const FfGeom fg = ff_geom(ld.lgnp, lgD);
         g1.layer[i] = g2.layer[i] = l;
         g1.x[i] = outs[l - l0];
         g1.th[i] = theta0 ? (const float *)theta0[l - l0] : nullptr;
         ob += tb * ld.n * osz + (g1.th[i] ? ld.n * 4 : 0);
         g1.u[i] = g2.u[i] = ws + off;
         g1.us[i] = g2.us[i] = afjlf_u_floats(s, l);
-        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (lgD - 1 - ff_lgW(lgP)));
-        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (lgP - 1)) + 1;
+        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (fg.lgR - fg.lgW));
+        g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (fg.lgP - 1)) + 1;
         off += g1.us[i] * tb;
         ++g1.n;
         ++g2.n;
       }
-      SK_PROF(SK_PROF_FF_RES, tb * D * 4,
-              hipLaunchKernelGGL(k_ffq_T, dim3((unsigned)(g2.item0[g2.n] * ceil8(tb))), dim3(kNT), 0, st,
-                                 s->d_layers, g2, lgD, z, b_begin + t0, tb, s->d_gtab, c1, c2, tw, s->ftw_lg));
+      const dim3 grid2((unsigned)(g2.item0[g2.n] * ceil8(tb)));
+      SK_PROF(SK_PROF_FF_RES, tb * D * 4, {
+        if (big)
+          hipLaunchKernelGGL((k_ffq_T<10, 14>), grid2, dim3(1024), 0, st, s->d_layers, g2, lgD, z, b_begin + t0, tb,
+                             s->d_gtab, c1, c2, tw, s->ftw_lg);
+        else
+          hipLaunchKernelGGL((k_ffq_T<9, 13>), grid2, dim3(512), 0, st, s->d_layers, g2, lgD, z, b_begin + t0, tb,
+                             s->d_gtab, c1, c2, tw, s->ftw_lg);
+      });
       SK_PROF(SK_PROF_GATHER, ob,
-              hipLaunchKernelGGL(k_ffr_T, dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(kNT), 0, st,
+              hipLaunchKernelGGL((k_ffr_T<9, 13>), dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(512), 0, st,
                                  s->d_layers, g1, out_dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
     }
   });

@@ -233,19 +233,18 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       for (int l = 0; l < n_layers; ++l)
         if (shapes[l].rows * shapes[l].cols > (1ll << 26))
           return fail(SK_EUNSUPPORTED, "AFFDQ: layer " + std::to_string(l) + " pads beyond 2^26 elements");
-    // AFJLF: one-kernel layers (N' = D, at most 16384 entries) or two passes with
-    // 2 <= P = N'/(D/2) <= 4096 and J = D/(2P) between 1 and 16384
+    // AFJLF: one-kernel layers (N' = D, at most 16384 entries) or two passes
+    // with at most 16384 outputs per residue
     if (kind == SK_AFJLF)
       for (int l = 0; l < n_layers; ++l) {
         const int64_t n = shapes[l].rows * shapes[l].cols;
         int lgn = 0;
         while ((1ll << lgn) < std::max(n, D)) ++lgn;
-        const int lgM = ilog2(D) - 1, lgP = lgn - lgM, lgJ = lgM - lgP;
         const bool small = lgn == ilog2(D) && n <= 16384;
-        if (!small && (lgP < 1 || lgP > 12 || lgJ < 0 || lgJ > 14))
+        if (!small && !afjlf_two_pass_ok(lgn, ilog2(D)))
           return fail(SK_EUNSUPPORTED, "AFJLF: layer " + std::to_string(l) +
-                                           " needs N'/(D/2) <= 4096 and D^2/(4 N') <= 16384 (or N' = D and at most "
-                                           "16384 entries)");
+                                           ": more than 16384 outputs per residue (D^2/(4 N') with N' < 256 D/2; "
+                                           "or N' = D with more than 16384 entries)");
       }
     // FJL sample positions are one 32-bit Philox word masked to N' - 1, uniform
     // only while N' <= 2^32

@@ -51,6 +51,8 @@ void run_affdq_apply_T(const sk_sketch *s, int layer, const float *z, int64_t b_
 // ---- AFJLF (Fourier pre-conditioner) ----
 // layers with N' = D and at most 16384 entries (one kernel per direction)
 bool afjlf_small_layer(const sk_sketch *s, int layer);
+// whether the two-pass kernels take a layer of N' = 2^lgnp at D = 2^lgD (D^2 / (4 N') <= 16384 outputs per residue)
+bool afjlf_two_pass_ok(int lgnp, int lgD);
 int64_t afjlf_bytes_per_vector(const sk_sketch *s, int l0, int l1, bool transpose);
 // exp(-2 pi i m / S), S = max(D, 4096), as (cos, sin) pairs, computed in double
 void afjlf_twiddles(int64_t D, std::vector<float> &host, int &lgS);

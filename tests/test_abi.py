@@ -59,8 +59,8 @@ def shapes(*ss):
     (7, [(1, 1 << 27)], 4096, 0, -5),     # AFFDQ: N' above 2^26
     (0, [(2, (1 << 31) + 1)], 4096, 0, -5),  # FJL: N' above 2^32 (positions are 32-bit words)
     (8, [(1, 10)], 1024, 0, -5),          # AFJLF: D below 2048
-    (8, [(1, 1 << 22)], 2048, 0, -5),     # AFJLF: N'/(D/2) = 4096 > D/2 (fewer than one output per residue)
-    (8, [(1, 40000)], 1 << 17, 0, -5),    # AFJLF: N' = D with more than 16384 entries and J = 2^15
+    (8, [(1, 40000)], 1 << 17, 0, -5),    # AFJLF: N' = D with more than 16384 entries and 2^15 outputs per residue
+    (8, [(1, 1 << 21)], 1 << 20, 0, -5),  # AFJLF: N' = 2D: 2^18 outputs per residue
     (9, [(1, 10)], 4096, 0, -1),          # unknown kind
 ])
 def test_create_rejects_invalid_arguments(kind, shp, D, flags, code):

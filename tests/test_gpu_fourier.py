@@ -2,8 +2,9 @@
 "Alternative pre-conditioners") against the fp64 oracle (oracle/fourier.py), through the C ABI.
 
 Cases cover the one-kernel path (layers with N' = D and at most 16384 entries), the two-pass path over the whole
-range of P = N'/(D/2) (2 .. 2048) and J = D^2/(4 N') (1 .. 16384), several layers per launch, ragged rows, bf16
-inputs and outputs, theta0, streaming with accumulate and bitwise determinism.  Same metric and bounds as the
+range of Q = N'/(D/2) (2 .. 2048, rows of R = N'/256 once Q exceeds 256) and of the outputs per residue (4 .. 16384),
+several layers per launch, ragged rows, bf16 inputs and outputs, theta0, streaming with accumulate and bitwise
+determinism.  Same metric and bounds as the
 other kinds: max_i |y_i - o_i| / max(|o_i|, rms(o)) <= 1e-5.
 """
 import numpy as np
@@ -52,7 +53,8 @@ CASES = [
     (LAYERS, 2048),                                   # small path, P = 8 and 64 (J = 128, 16)
     (LAYERS, 4096),
     ([(1, 70000), (3, 500)], 4096),                   # P = 64, J = 32
-    ([(1, 1 << 20)], 2048),                           # P = 1024 = M: J = 1
+    ([(1, 1 << 20)], 2048),                           # N'/M = 1024: rows of R = 4M (P = 256), J = 4
+    ([(1, 3 * 2 ** 20 + 5), (2, 999)], 4096),         # N'/M = 2048: P = 256, R = 2^14, J = 8, two q-blocks
     ([(1, 3 * 2 ** 20 + 11)], 1 << 16),               # P = 128, J = 256, two q-blocks
     ([(1, 768), (1, 2304), (96, 1024), (1, 3072), (2, 3000), (1, 8200), (1, 20000)], 1 << 16),  # P = 2 .. 4
     ([(1, 2 ** 22 - 9), (5, 999)], 1 << 17),          # P = 64, J = 1024

@@ -185,3 +185,30 @@ def test_fullsize_c5_afjl_streamed_subset(dev):
     say(f"c5 afjl: rows {rows}: rel err {e:.2e}")
     assert e <= TOL_BF16
     sk.close()
+
+
+def test_fullsize_c10_afjlf(dev):
+    """The C2 gradients through AFJLF (the Fourier pre-conditioner), the benchmark's batch of 64: rows 0 and 63
+    against the oracle, and the transpose of two z rows."""
+    from paper_2402_03994_amd import Sketch
+    c = W.CONFIGS["c10"]
+    shapes, D, B, seed = c["shapes"], c["D"], c["batch"], c["seed"]
+    gen = W.generator("c10", dev)
+    xs = [W.gaussian((B, r * cc), 1e-4, gen, dev) for r, cc in shapes]
+    sk = Sketch("afjlf", shapes, D, seed, device=dev)
+    y = sk.apply(xs).cpu().numpy()
+    rows = [0, B - 1]
+    say(f"c10 afjlf: GPT-2 small, 148 tensors, batch {B}, D=2^16, rows {rows}")
+    o = O.apply("afjlf", shapes, D, seed, [host_rows(x, rows) for x in xs], nthreads=CORES)
+    e = rel_err(y[rows], o)
+    say(f"c10 afjlf: rel err {e:.2e}")
+    assert e <= TOL_F32
+    del xs
+    z = torch.randn((2, D), generator=gen, device=dev)
+    outs = sk.apply_T(z)
+    torch.cuda.synchronize()
+    refs = O.apply_T("afjlf", shapes, D, seed, z.cpu().numpy().astype(np.float64), nthreads=CORES)
+    e = max(rel_err(g.cpu().numpy(), r) for g, r in zip(outs, refs))
+    say(f"c10 afjlf T: rel err {e:.2e}")
+    assert e <= TOL_F32
+    sk.close()

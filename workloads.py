@@ -70,6 +70,8 @@ CONFIGS = {
     "c5": dict(kinds=("afjl",), shapes=llama3_8b_shapes(), D=1 << 20, batch=8, seed=7, dtype="bf16"),
     # the C2 gradients through the sketches with the random-orthogonal pre-conditioner Q
     "c6": dict(kinds=("afjlq", "qkh"), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
+    # the C2 gradients through the sketch with the Fourier pre-conditioner (eq. frikadel, H_N -> FFT)
+    "c10": dict(kinds=("afjlf",), shapes=gpt2_small_shapes(), D=1 << 16, batch=64, seed=1, dtype="f32"),
     # AFFD with Q (dense: ~4.3 GFLOP per vector and 2^20-element slab each way) on C1's vectors
     "c7": dict(kinds=("affdq",), shapes=[(1, 1 << 20)], D=4096, batch=8, seed=0, dtype="f32"),
     # sketched Hessian eigenvalues: Arnoldi (64 steps) on v -> S H S^T v, GPT-2-small parameters, a
@@ -88,9 +90,9 @@ C8_LAMBDAS = (20.0, 15.0, 11.0, 8.5, 6.5, 5.0, 4.0, 3.0, 2.5, 2.0, 1.6, 1.3, 1.1
 C8_SHIFT = 1e-5
 C8_HSEED = 4242
 INPUT_SEED = {"c1": 1001, "c2": 1002, "c3": 1003, "c4": 1004, "c5": 1005, "c6": 1002, "c7": 1001, "c8": 1008,
-              "c9": 1009}
+              "c9": 1009, "c10": 1002}
 # variance of the gradient entries (N(0, var)); C4's forward input is Student-t(3)
-GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4, "c7": 1.0}
+GRAD_VAR = {"c1": 1.0, "c2": 1e-4, "c3": 1e-4, "c4": None, "c5": 1e-5, "c6": 1e-4, "c7": 1.0, "c10": 1e-4}
 
 
 def gaussian(shape, var: float, gen: torch.Generator, device, dtype=torch.float32) -> torch.Tensor:
