@@ -203,8 +203,9 @@ def cpu_baseline(cfg: str):
         nbytes = 2 * len(c["kinds"]) * c["batch"] * shapes[0][1] * 4
         sample = f"all {c['batch']} rows, FJL+FFD forward and transpose"
     elif cfg in ("c2", "c10"):
-        # the first two transformer blocks (24 tensors, 14.2M parameters), 16 rows (every core busy)
-        sub, nrows = shapes[2:26], 16
+        # the first two transformer blocks (24 tensors, 14.2M parameters): every row of the batch for the C
+        # oracle, 16 rows for the numpy one
+        sub, nrows = shapes[2:26], (c["batch"] if cfg == "c2" else 16)
         xs = rows_for(sub, nrows)
         for k in c["kinds"]:
             O.apply(k, sub, D, seed, xs, layer0=2, nthreads=cores)

@@ -46,7 +46,6 @@ namespace {
 constexpr int kCap = 16384;      // largest transform buffer (complex values)
 constexpr int kLgCap = 14;
 constexpr int kLgCapS = 13;      // the default size
-constexpr int kMaxQb = 1024;     // q columns of one pass-2 block (their twiddles live in LDS)
 constexpr int kLgPMax = 8;       // rows of the pass-1 view: P = N/R <= 256
 constexpr int kSlots = 32;       // layers per launch
 
@@ -222,7 +221,6 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
                                                  const float2 *__restrict__ tw, int lgS) {
   constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
   __shared__ float2 buf[CAP];
-  __shared__ float2 tq[kMaxQb];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
@@ -271,7 +269,6 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
   };
   for (int qb = 0; qb < nqb; ++qb) {
     const int64_t q0 = (int64_t)qb << lgQb;
-    for (int qq = threadIdx.x; qq < Qb; qq += NT) tq[qq] = cis_neg((q0 + qq) * r, lgN);  // w_N^{q r}
     {
       float2 tr = rstart;
       for (int s = s0, i = 0; s < J; s += ds, ++i) {
@@ -284,19 +281,21 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
     for (int i = 0; i < rpt; ++i) {
       const int j = j0 + (i << (LGNT - lgG));
       float2 a = make_float2(0.f, 0.f), b = a, nn = a;
-      // q = q0 + gi + G m: w_R^{q j} and w_Q^{q} by recurrence over m (at most 16 steps)
-      float2 wr = cis_neg(((q0 + gi) * j) & ((1ll << lgR) - 1), lgR);
-      const float2 wrs = cis_neg(((int64_t)G * j) & ((1ll << lgR) - 1), lgR);
-      float2 wq = cis_neg((q0 + gi) & ((1ll << lgQ) - 1), lgQ);
-      const float2 wqs = cis_neg(G & ((1 << lgQ) - 1), lgQ);
+      // q = q0 + gi + G m, k = r + P j: set A adds w_N^{q k} W_q[j], set B adds
+      // conj(W_q[j]) w_N^{q (M - k)} (= conj(w_N^{q k} W_q[j]) w_Q^q); both twiddles
+      // by recurrence over m (at most 16 steps) from values computed directly
+      const int64_t k = r + ((int64_t)j << lgP), nmask = (1ll << lgN) - 1;
+      float2 wa = cis_neg(((q0 + gi) * k) & nmask, lgN);
+      const float2 was = cis_neg(((int64_t)G * k) & nmask, lgN);
+      float2 wb = cis_neg(((q0 + gi) * (((int64_t)1 << lgM) - k)) & nmask, lgN);
+      const float2 wbs = cis_neg(((int64_t)G * (((int64_t)1 << lgM) - k)) & nmask, lgN);
       for (int qq = gi; qq < Qb; qq += G) {
         const float2 w = buf[(j << lgQb) + qq];
-        const float2 tA = cmul(cmul(w, tq[qq]), wr);
-        a = cadd(a, tA);
-        if (pair) b = cadd(b, cmul(cconj(tA), wq));
+        a = cadd(a, cmul(w, wa));
+        if (pair) b = cadd(b, cmul(cconj(w), wb));
         if (r == 0 && j == 0) nn = ((q0 + qq) & 1) ? csub(nn, w) : cadd(nn, w);
-        wr = cmul(wr, wrs);
-        wq = cmul(wq, wqs);
+        wa = cmul(wa, was);
+        if (pair) wb = cmul(wb, wbs);
       }
       if (G == 1) {
         emit(j, a, b, nn, qb > 0);

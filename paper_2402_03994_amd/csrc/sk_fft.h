@@ -32,6 +32,12 @@ __device__ __forceinline__ float2 twiddle(const float2 *__restrict__ tw, int lgS
   const float2 w = tw[(m & ((1ll << lgn) - 1)) << (lgS - lgn)];
   return INV ? cconj(w) : w;
 }
+// the same for m < 2^lgn < 2^31 (32-bit index arithmetic)
+template <bool INV>
+__device__ __forceinline__ float2 twiddle32(const float2 *__restrict__ tw, int lgS, int lgn, uint32_t m) {
+  const float2 w = tw[m << (lgS - lgn)];
+  return INV ? cconj(w) : w;
+}
 
 // One Stockham stage of radix R over the whole block's butterflies.
 template <bool INV, int R, int NT, int MAXB>
@@ -59,8 +65,14 @@ __device__ __forceinline__ void fft_stage(float2 *buf, int lgL, int lgC, int lgN
       const int col = e & (C - 1), j = e >> lgC;
       const int k = j & ((1 << lgNs) - 1);
       if (k) {
-#pragma unroll
-        for (int r = 1; r < R; ++r) v[i][r] = cmul(v[i][r], twiddle<INV>(tw, lgS, lgNs + lgR, (int64_t)k * r));
+        // w^k from the table, w^2k and w^3k by products (one load per butterfly)
+        const float2 w1 = twiddle32<INV>(tw, lgS, lgNs + lgR, (uint32_t)k);
+        v[i][1] = cmul(v[i][1], w1);
+        if (R == 4) {
+          const float2 w2 = cmul(w1, w1);
+          v[i][2] = cmul(v[i][2], w2);
+          v[i][3] = cmul(v[i][3], cmul(w1, w2));
+        }
       }
       if (R == 4) {
         const float2 a0 = cadd(v[i][0], v[i][2]), a1 = csub(v[i][0], v[i][2]);
