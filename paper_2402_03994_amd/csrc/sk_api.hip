@@ -71,6 +71,9 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_seg);
   f(s->d_fjl_smp);
   f(s->d_fjl_toff);
+  f(s->d_fjl_lsmp);
+  f(s->d_fjl_lpos);
+  f(s->d_fjl_loff);
   f(s->d_qka);
   f(s->d_qkb);
   f(s->d_qkah);
@@ -407,10 +410,13 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
 
   // FJL transpose: samples grouped by position (deterministic order).
-  std::vector<uint32_t> fpos, fseg, fsmp, ftoff;
+  std::vector<uint32_t> fpos, fseg, fsmp, ftoff, flsmp, flpos, floff;
   if (kind == SK_FJL) {
     s->fjl_uoff.assign(n_layers + 1, 0);
     s->fjl_toff_at.assign(n_layers, 0);
+    s->fjl_loff_at.assign(n_layers, 0);
+    flsmp.assign((size_t)n_layers * D, 0);
+    flpos.assign((size_t)n_layers * D, 0);
     std::vector<std::pair<uint32_t, uint32_t>> v(D);
     for (int l = 0; l < n_layers; ++l) {
       const LayerDesc &ld = s->layers[l];
@@ -435,6 +441,30 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       for (int64_t t = 0; t <= tiles; ++t) {
         while (u < s->fjl_uoff[l + 1] && ((int64_t)fpos[u] >> lgw) < t) ++u;
         ftoff.push_back((uint32_t)(u - u0));
+      }
+      // forward: the samples by block of the last transform pass (positions whose low `lo` bits fall in
+      // [cb 2^lgcs, (cb + 1) 2^lgcs)), ids ascending within a block
+      s->fjl_loff_at[l] = (int64_t)floff.size();
+      if (ld.lgnp > 13) {
+        int los[64], wsp[64], lgcss[64];
+        const int np = fwht_pass_plan(ld.lgnp, 13, los, wsp, lgcss);
+        const int lo = los[np - 1], lgcs = lgcss[np - 1];
+        const int64_t nblk = 1ll << (lo - lgcs);
+        std::vector<std::pair<uint32_t, uint32_t>> bs(D);
+        for (int64_t i = 0; i < D; ++i) {
+          const uint32_t p = sample_index((uint64_t)i, (uint32_t)l, s->key, (uint64_t)ld.np);
+          bs[i] = {(uint32_t)((p & ((1u << lo) - 1)) >> lgcs), (uint32_t)i};
+        }
+        std::sort(bs.begin(), bs.end());
+        int64_t k = 0;
+        for (int64_t b = 0; b <= nblk; ++b) {
+          while (k < D && (int64_t)bs[k].first < b) ++k;
+          floff.push_back((uint32_t)k);
+        }
+        for (int64_t i = 0; i < D; ++i) {
+          flsmp[(size_t)l * D + i] = bs[i].second;
+          flpos[(size_t)l * D + i] = sample_index((uint64_t)bs[i].second, (uint32_t)l, s->key, (uint64_t)ld.np);
+        }
       }
     }
   }
@@ -496,6 +526,9 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_fjl_seg, sizeof(uint32_t) * fseg.size()));
   SK_TRY(alloc((void **)&s->d_fjl_smp, sizeof(uint32_t) * fsmp.size()));
   SK_TRY(alloc((void **)&s->d_fjl_toff, sizeof(uint32_t) * ftoff.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_lsmp, sizeof(uint32_t) * flsmp.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_lpos, sizeof(uint32_t) * flpos.size()));
+  SK_TRY(alloc((void **)&s->d_fjl_loff, sizeof(uint32_t) * floff.size()));
   SK_TRY(alloc((void **)&s->d_qka, sizeof(float) * fac_a));
   SK_TRY(alloc((void **)&s->d_qkb, sizeof(uint16_t) * 2 * fac_b));
   SK_TRY(alloc((void **)&s->d_qkah, sizeof(uint16_t) * 2 * fac_a));
@@ -516,6 +549,9 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(h2d(s->d_fjl_seg, fseg.data(), sizeof(uint32_t) * fseg.size()));
   SK_TRY(h2d(s->d_fjl_smp, fsmp.data(), sizeof(uint32_t) * fsmp.size()));
   SK_TRY(h2d(s->d_fjl_toff, ftoff.data(), sizeof(uint32_t) * ftoff.size()));
+  SK_TRY(h2d(s->d_fjl_lsmp, flsmp.data(), sizeof(uint32_t) * flsmp.size()));
+  SK_TRY(h2d(s->d_fjl_lpos, flpos.data(), sizeof(uint32_t) * flpos.size()));
+  SK_TRY(h2d(s->d_fjl_loff, floff.data(), sizeof(uint32_t) * floff.size()));
 
   // workspace: room for up to 256 vectors of the largest per-vector need
   const int64_t pv = std::max(per_vector_bytes(s, 0, n_layers, false), per_vector_bytes(s, 0, n_layers, true));
@@ -811,13 +847,17 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
       case SK_FJL:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
-          {
-            const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the signed load
-            SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_pass0(s, l, grads[l - l0], dtype, b0, bc, s->ws, lgw, st));
-            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from(s->ws, bc, ld.lgnp, lgw, st));
+          const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the signed load
+          SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_pass0(s, l, grads[l - l0], dtype, b0, bc, s->ws, lgw, st));
+          if (ld.lgnp > 13) {
+            // the middle passes, then the last one fused with the sample gather
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from_but_last(s->ws, bc, ld.lgnp, lgw, st));
+            SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                    launch_fjl_last_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st));
+          } else {
+            SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                    launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st));
           }
-          SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
-                  launch_fjl_gather(s, l, s->ws, b0, bc, out, accumulate || l > l0, st));
         }
         break;
       case SK_FFD: {

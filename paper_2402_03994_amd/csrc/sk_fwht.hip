@@ -50,10 +50,8 @@ __global__ __launch_bounds__(256) void k_fwht_pass(float *data, int lgn, int lo,
 
 void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st) { fwht_inplace_from(data, V, lgn, 0, st); }
 
-// The passes of fwht_inplace from index bit lo0 on (bits below lo0 already transformed).
-void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st) {
-  if (lgn == 0 || V == 0) return;
-  int lo = lo0;
+int fwht_pass_plan(int lgn, int lo0, int *los, int *ws, int *lgcss) {
+  int np = 0, lo = lo0;
   while (lo < lgn) {
     int w, lgcs;
     if (lo == 0) {
@@ -64,13 +62,40 @@ void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st)
       lgcs = 13 - w;
       if (lgcs > lo) lgcs = lo;
     }
+    los[np] = lo;
+    ws[np] = w;
+    lgcss[np] = lgcs;
+    ++np;
+    lo += w;
+  }
+  return np;
+}
+
+// Passes [first, end) of the plan of fwht_pass_plan(lgn, lo0).
+static void fwht_passes(float *data, int64_t V, int lgn, int lo0, int first, int end, hipStream_t st) {
+  int los[64], ws[64], lgcss[64];
+  const int np = fwht_pass_plan(lgn, lo0, los, ws, lgcss);
+  for (int k = first; k < std::min(end, np); ++k) {
+    const int lo = los[k], w = ws[k], lgcs = lgcss[k];
     const int64_t tiles = V * ((1ll << lgn) >> (w + lgcs));
     const float scale = (float)(1.0 / sqrt((double)(1ll << w)));
     const size_t shm = sizeof(float) * p16_floats(1 << (w + lgcs));
     hipLaunchKernelGGL(k_fwht_pass, dim3((unsigned)tiles), dim3(256), shm, st, data, lgn, lo, w, lgcs, scale);
     SK_CHECK_LAUNCH();
-    lo += w;
   }
+}
+
+// The passes of fwht_inplace from index bit lo0 on (bits below lo0 already transformed).
+void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st) {
+  if (lgn == 0 || V == 0) return;
+  fwht_passes(data, V, lgn, lo0, 0, 64, st);
+}
+
+void fwht_inplace_from_but_last(float *data, int64_t V, int lgn, int lo0, hipStream_t st) {
+  if (lgn == 0 || V == 0) return;
+  int los[64], ws[64], lgcss[64];
+  const int np = fwht_pass_plan(lgn, lo0, los, ws, lgcss);
+  fwht_passes(data, V, lgn, lo0, 0, np - 1, st);
 }
 
 __global__ void k_fill_zero(float *p, int64_t n) {
@@ -1132,6 +1157,54 @@ void launch_fjl_gather(const sk_sketch *s, int layer, const float *w, int64_t b_
                        bool accumulate, hipStream_t st) {
   hipLaunchKernelGGL(k_fjl_gather, dim3((unsigned)((s->D + 255) / 256)), dim3(256), 0, st, s->d_layers, s->d_gtab,
                      layer, w, s->D, b_begin, bc, out, (int)accumulate, s->key);
+  SK_CHECK_LAUNCH();
+}
+
+// FJL forward, last transform pass fused with the gather of the D samples: the
+// pass over index bits [lo, lo + w) = the top bits, one workgroup per (vector,
+// block of 2^lgcs low positions); after the transform the workgroup writes
+// out[i] = sqrt(N'/D) g_i w[idx_i] for the samples whose position falls in its
+// block (a list sorted by block at creation), and nothing else.
+__global__ __launch_bounds__(256) void k_fjl_last_gather(const float *__restrict__ data, int lgn, int lo, int w,
+                                                         int lgcs, float scale, const uint32_t *__restrict__ smp,
+                                                         const uint32_t *__restrict__ spos,
+                                                         const uint32_t *__restrict__ soff,
+                                                         const float *__restrict__ g, float gscale, int64_t D,
+                                                         int64_t b_begin, float *__restrict__ out, int accumulate) {
+  extern __shared__ float sm[];
+  const int64_t n = 1ll << lgn;
+  const int64_t tiles = n >> (w + lgcs);
+  const int64_t v = blockIdx.x / tiles;
+  const int64_t cb = blockIdx.x - v * tiles;
+  const float *base = data + v * n + (cb << lgcs);
+  const int total = 1 << (w + lgcs);
+  const int cmask = (1 << lgcs) - 1;
+  for (int e = threadIdx.x; e < total; e += 256) sm[p16(e)] = base[((int64_t)(e >> lgcs) << lo) + (e & cmask)];
+  lds_fwht_regs(sm, w + lgcs, lgcs);
+  const uint32_t k0 = soff[cb], k1 = soff[cb + 1];
+  float *o = out + (b_begin + v) * D;
+  for (uint32_t k = k0 + threadIdx.x; k < k1; k += 256) {
+    const uint32_t i = smp[k], p = spos[k];
+    const int e = (int)(((p >> lo) << lgcs) + (p & cmask));
+    const float val = (g[i] * gscale) * (sm[p16(e)] * scale);
+    o[i] = accumulate ? o[i] + val : val;
+  }
+}
+
+void launch_fjl_last_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
+                            bool accumulate, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  int los[64], ws[64], lgcss[64];
+  const int np = fwht_pass_plan(ld.lgnp, std::min(ld.lgnp, 13), los, ws, lgcss);
+  const int lo = los[np - 1], wl = ws[np - 1], lgcs = lgcss[np - 1];
+  const int64_t tiles = bc * ((1ll << ld.lgnp) >> (wl + lgcs));
+  const size_t shm = sizeof(float) * p16_floats(1 << (wl + lgcs));
+  const float scale = (float)(1.0 / sqrt((double)(1ll << wl)));
+  const int64_t so = s->fjl_loff_at[layer];
+  hipLaunchKernelGGL(k_fjl_last_gather, dim3((unsigned)tiles), dim3(256), shm, st, w, ld.lgnp, lo, wl, lgcs, scale,
+                     s->d_fjl_lsmp + (int64_t)layer * s->D, s->d_fjl_lpos + (int64_t)layer * s->D, s->d_fjl_loff + so,
+                     s->d_gtab + (int64_t)layer * s->D, (float)sqrt((double)ld.np / (double)s->D), s->D, b_begin,
+                     out, (int)accumulate);
   SK_CHECK_LAUNCH();
 }
 

@@ -90,6 +90,10 @@ struct sk_sketch {
   uint32_t *d_fjl_smp = nullptr;   // sample ids sorted by (position, id)
   std::vector<int64_t> fjl_toff_at; // per layer: offset of its tile table in d_fjl_toff
   uint32_t *d_fjl_toff = nullptr;  // per layer and tile of 2^min(lg N', 13) positions: first unique index (+1 end)
+  // FJL forward with N' > 2^13: per layer, the D samples sorted by the block of the last transform pass that
+  // holds their position (ids and positions, D each) and the blocks' first entries (+ end)
+  uint32_t *d_fjl_lsmp = nullptr, *d_fjl_lpos = nullptr, *d_fjl_loff = nullptr;
+  std::vector<int64_t> fjl_loff_at;
   // QK
   float *d_qka = nullptr;       // A factors, fp32
   uint16_t *d_qkah = nullptr;   // A factors as bf16 hi terms, then bf16 lo terms (A-first contraction)

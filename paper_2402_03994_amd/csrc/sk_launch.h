@@ -11,6 +11,15 @@ void fwht_inplace(float *data, int64_t V, int lgn, hipStream_t st);
 // The passes of fwht_inplace from index bit lo0 on (the first pass of fwht_inplace covers bits
 // [0, min(lgn, 13)), so lo0 = min(lgn, 13) continues after a fused first pass).
 void fwht_inplace_from(float *data, int64_t V, int lgn, int lo0, hipStream_t st);
+// The same passes except the last one.
+void fwht_inplace_from_but_last(float *data, int64_t V, int lgn, int lo0, hipStream_t st);
+// The passes fwht_inplace_from(lgn, lo0) makes: n passes over index bits [los[k], los[k] + ws[k]) with
+// 2^lgcss[k] columns per tile (arrays of at least 64 entries).
+int fwht_pass_plan(int lgn, int lo0, int *los, int *ws, int *lgcss);
+// FJL forward, the last transform pass of layers with N' > 2^13 fused with the sample gather
+// (sample lists sorted by the pass's blocks at creation).
+void launch_fjl_last_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
+                            bool accumulate, hipStream_t st);
 // FJL forward: signed load fused with the transform over index bits [0, lgw) (lgw = min(log2 N', 13)).
 void launch_fjl_pass0(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc, float *w,
                       int lgw, hipStream_t st);
