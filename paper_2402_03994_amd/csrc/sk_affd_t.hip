@@ -187,7 +187,6 @@ __global__ __launch_bounds__(1024) void k_affdT_rows(const LayerDesc *__restrict
   };
   load(cur, sslab);
   const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;  // transform: row ri, columns 32 rc ..
-  const int soff = (32 * rc * 1024 + ri) * 4;
   for (;;) {
     __syncthreads();  // the previous tile's reads of s and sg are done
     // sign words of the 32 rows: 8 Philox blocks of 128 signs per row, one per
@@ -220,11 +219,17 @@ __global__ __launch_bounds__(1024) void k_affdT_rows(const LayerDesc *__restrict
     // H_l (unnormalised; the 1/32 is applied by the readers of W^T)
     float e[32];
     fwht1024_rows32(s, e);
-    // column 32 rc + m, row p0 + ri of slab t: byte (32 rc + m) 4096 + 4 (p0 + ri)
-    const __amdgpu_buffer_rsrc_t ws = buf_rsrc(w + cur.v * vstride + (compact ? cur.sl : cur.t) * lo_len + cur.p0,
-                                               (uint32_t)((lo_len - cur.p0) * 4));
+    // column 32 rc + m, row p0 + ri of the slab: byte (32 rc + m) cstride + 4 (p0 + ri), cstride = 4096
+    // bytes ([slab][l][p], one slab after the other) or, compact, vslabs 4096 ([l][slab][p]: a column's
+    // slabs contiguous, so the top kernel reads one region per column and vector)
+    const __amdgpu_buffer_rsrc_t ws =
+        compact ? buf_rsrc(w + cur.v * vstride + cur.sl * 1024 + cur.p0, (uint32_t)((vstride - cur.sl * 1024 - cur.p0) * 4))
+                : buf_rsrc(w + cur.v * vstride + cur.t * lo_len + cur.p0, (uint32_t)((lo_len - cur.p0) * 4));
+    const uint32_t cstride = compact ? (uint32_t)((vstride >> 20) * 4096) : 4096u;
+    const uint32_t soffc = 32u * (uint32_t)rc * cstride + 4u * (uint32_t)ri;
 #pragma unroll
-    for (int m = 0; m < 32; ++m) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m]), ws, soff, m * 4096, 0);
+    for (int m = 0; m < 32; ++m)
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m]), ws, soffc, m * cstride, 0);
     if (!more) break;
     tile = ntile;
     cur = nxt;
@@ -424,7 +429,7 @@ __global__ __launch_bounds__(256) void k_affd_mtab(const LayerDesc *__restrict__
 // once per slab) and accumulates F.  Two register sets alternate between the
 // slab being transformed and the next live slab being loaded.
 // The slabs are the group's live slabs s_first .. s_first + nsl - 1, stored
-// compactly (W^T of group slab j of vector v at w + v vstride + j 2^20).  A
+// compactly (W^T of group slab j of vector v, column l at w + v vstride + (l vslabs + j) 1024).  A
 // layer whose slabs come in several groups carries F between launches in
 // facc[v][l][p] (fmode bit 0: start from facc, bit 1: last group, finish).
 namespace {
@@ -536,8 +541,8 @@ __global__ __launch_bounds__(256, 3) void k_affdT_topM(const LayerDesc *__restri
     }
   };
   auto fetch = [&](const Item &it, int j, float(&e)[32], float4 &mv) {
-    // W^T of group slab j, M of slab s_t[j]
-    const float *src = w + vrow(it) * vstride + j * lo_len + it.l * 1024 + c;
+    // W^T of group slab j ([l][slab][p] per vector), M of slab s_t[j]
+    const float *src = w + vrow(it) * vstride + (it.l * (vstride >> 20) + j) * 1024 + c;
 #pragma unroll
     for (int k = 0; k < 32; ++k) e[k] = src[32 * k];
     mv = *(const float4 *)(mt + (int64_t)s_t[j] * lo_len + it.l * 1024 + 4 * threadIdx.x);
