@@ -679,6 +679,7 @@ void for_groups(const sk_sketch *s, int l0, int l1, int64_t bc, int64_t ufl, F &
       int lend = l + 1;
       if (used > ufl) {
         tile = std::max<int64_t>(1, ufl / afjlf_u_floats(s, l));
+        if (tile > 8) tile &= ~7ll;  // whole XCD rounds (a vector's items run on XCD v mod 8)
       } else {
         while (lend < l1 && (int)grp.size() < kSlots) {
           if (afjlf_small_layer(s, lend) || (int)big_residue(s, lend) != big) {

@@ -657,6 +657,9 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
   const int64_t pv = per_vector_bytes(s, l0, l1, false);
   int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
   if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
+  // AFJLF kernels place every work item of a vector on XCD (vector mod 8): chunks of a
+  // multiple of 8 vectors keep the eight XCDs equally loaded
+  if (s->kind == SK_AFJLF && bcmax > 8 && batch > bcmax) bcmax &= ~7ll;
   const int esz = dtype == SK_BF16 ? 2 : 4;
   if (s->kind == SK_AFFD) {
     bool all_fast = true;
@@ -978,6 +981,7 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
   const int64_t pv = per_vector_bytes(s, l0, l1, true);
   int64_t bcmax = pv > 0 ? s->ws_bytes / pv : batch;
   if (bcmax < 1) return fail(SK_EUNSUPPORTED, "workspace too small for one vector");
+  if (s->kind == SK_AFJLF && bcmax > 8 && batch > bcmax) bcmax &= ~7ll;
   const int lgD = ilog2(s->D);
   const int osz = out_dtype == SK_BF16 ? 2 : 4;
   for (int64_t b0 = 0; b0 < batch; b0 += bcmax) {
