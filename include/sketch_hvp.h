@@ -117,7 +117,9 @@ int sketch_arnoldi_step(float *Q, int64_t D, int32_t j, float *Hbar, int32_t k, 
  * k Arnoldi steps on the sketched synthetic HVP operator v -> S H S^T v from
  * v0 (device [D] fp32): Q [k+1, D] and Hbar [k+1, k] as above (device).  The
  * eigenvalues of Hbar[0:k, 0:k] (the Ritz values) estimate the extreme
- * eigenvalues of S H S^T; the small k x k eigenproblem is left to the caller.
+ * eigenvalues of S H S^T.  The small k x k eigenproblem is the caller's: the
+ * library stops at Hbar (the Python binding's ritz_values solves it with numpy
+ * on the host).
  * The orthogonalisation scratch lives in the handle's workspace (it must hold
  * sketch_arnoldi_work_floats(D, k) floats, else SK_EUNSUPPORTED).
  */

@@ -6,8 +6,10 @@
 // digits of pi2(0),
 //   AFFD(x)[a 1024 + b] = sqrt(N'/D) (H_p (x) H_l F)[pi2_p(a), pi2_l(b)],
 //   F[p, l] = sum_t H_TT[h*, t] g[t, p, l] ((H_TT (x) H_p (x) H_l) w)[t, p, l].
-// Each slab t of w is written transposed, W^T[t][l][p], so that every
-// transform along p runs over contiguous memory:
+// Each slab t of w is written transposed, so that every transform along p
+// runs over contiguous memory: W^T[t][l][p] (slab after slab) or, with the
+// stored M tables, W^T[l][t][p] over the live slabs only (a column's slabs
+// one after the other, which C reads in that order):
 //   A  16 destination rows per workgroup: load, sign, pi1 on the columns,
 //      H_l, write 16 consecutive p of every column l            -> W^T
 //   C  per column l, with the stored M = H_TT (s . g): for each live slab

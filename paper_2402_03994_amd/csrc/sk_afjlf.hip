@@ -26,13 +26,17 @@
 // The transpose runs the same passes backwards.  All transforms are the LDS
 // Stockham FFTs of sk_fft.h (their twiddles from a table made in double
 // precision at creation); the per-element twiddles of pass 2 run as short
-// recurrences from values computed with sincospif.
+// recurrences from values computed with sincospif.  Every thread issues all
+// its global loads of a block before it uses the first (in-order memory
+// counters would otherwise serialise them), and the forward residue pass
+// loads the next column block during the current block's transform.
 #include <algorithm>
 #include <cmath>
 #include <functional>
 #include <vector>
 
 #include "sk_fft.h"
+#include "sk_kcommon.h"
 #include "sk_launch.h"
 
 namespace sk {
@@ -48,6 +52,11 @@ constexpr int kLgCap = 14;
 constexpr int kLgCapS = 13;      // the default size
 constexpr int kLgPMax = 8;       // rows of the pass-1 view: P = N/R <= 256
 constexpr int kSlots = 32;       // layers per launch
+// Residue-pass transforms of at most 2^kLgTwl points read their twiddles from
+// a copy of the table in LDS: they then issue no global loads, so the loads of
+// the next column block stay in flight across the transform.
+constexpr int kLgTwl = 10;
+constexpr int kLgRows = 13;      // forward pass 1: transform buffer of 2^kLgRows values, 2^(kLgRows-4) threads
 
 struct FfLayers {
   int32_t n;                     // layers in this launch
@@ -146,12 +155,12 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
                                                  const float2 *__restrict__ tw, int lgS, Key key) {
   constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
   __shared__ float2 buf[CAP];
-  __shared__ uint32_t sw[1024];
+  __shared__ uint32_t sw[CAP / 16];  // rows * W / 32 <= CAP / 16
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
   const LayerDesc &ld = layers[g.layer[slot]];
-  const FfGeom fg = ff_geom(ld.lgnp, lgD);
+  const FfGeom fg = ff_geom(ld.lgnp, lgD, LGCAP);
   const int lgR = fg.lgR, lgP = fg.lgP, lgW = fg.lgW, lgWc = lgW - 1;
   const int64_t R = 1ll << lgR, n = ld.n;
   const int64_t b0 = (item - g.item0[slot]) << lgW;
@@ -160,31 +169,65 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
   build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
   __syncthreads();
   const int64_t xo = (b_begin + v) * n;
-  // four real columns (two complex ones) per element; 16-byte (fp32) or 8-byte (bf16) loads when aligned
+  // four real columns (two complex ones) per element, at most CAP / (2 NT) elements per thread; every
+  // 16-byte (fp32) or 8-byte (bf16) load of the thread is issued before the first one is used
+  constexpr int MAXL = CAP / (2 * NT);
   const int lgW4 = lgW - 2;
   const int total = 1 << (lgP + lgW4);
   const bool vec = dtype == SK_BF16 ? !(((uintptr_t)g.x[slot] + 2 * xo) & 7) : !(((uintptr_t)g.x[slot] + 4 * xo) & 15);
-  for (int e = threadIdx.x; e < total; e += NT) {
+  uint4 raw[MAXL];
+  uint32_t full = 0;
+#pragma unroll
+  for (int i = 0; i < MAXL; ++i) {
+    const int e = threadIdx.x + i * NT;
+    const int64_t t = e >> lgW4;
+    const int64_t j = (t << lgR) + b0 + 4 * (e & ((1 << lgW4) - 1));
+    raw[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (vec && e < total && t < rows && j + 3 < n) full |= 1u << i;
+  }
+  // one loop per dtype, so that no load result is merged with another before the last load is issued
+  if (dtype == SK_BF16) {
+    const uint16_t *xb = (const uint16_t *)g.x[slot] + xo + b0;
+#pragma unroll
+    for (int i = 0; i < MAXL; ++i) {
+      const int e = threadIdx.x + i * NT;
+      if ((full >> i) & 1u) {
+        const uint2 w2 = *(const uint2 *)(xb + ((int64_t)(e >> lgW4) << lgR) + 4 * (e & ((1 << lgW4) - 1)));
+        raw[i].x = w2.x;
+        raw[i].y = w2.y;
+      }
+    }
+  } else {
+    const float *xf = (const float *)g.x[slot] + xo + b0;
+#pragma unroll
+    for (int i = 0; i < MAXL; ++i) {
+      const int e = threadIdx.x + i * NT;
+      if ((full >> i) & 1u)
+        raw[i] = *(const uint4 *)(xf + ((int64_t)(e >> lgW4) << lgR) + 4 * (e & ((1 << lgW4) - 1)));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXL; ++i) {
+    const int e = threadIdx.x + i * NT;
+    if (e >= total) break;
     const int64_t t = e >> lgW4;
     const int c4 = e & ((1 << lgW4) - 1);
     float a[4] = {0.f, 0.f, 0.f, 0.f};
     if (t < rows) {
-      const int64_t j = (t << lgR) + b0 + 4 * c4;
-      if (vec && j + 3 < n) {
+      if ((full >> i) & 1u) {
         if (dtype == SK_BF16) {
-          const uint2 u = *(const uint2 *)((const uint16_t *)g.x[slot] + xo + j);
-          a[0] = __uint_as_float(u.x << 16);
-          a[1] = __uint_as_float(u.x & 0xFFFF0000u);
-          a[2] = __uint_as_float(u.y << 16);
-          a[3] = __uint_as_float(u.y & 0xFFFF0000u);
+          a[0] = __uint_as_float(raw[i].x << 16);
+          a[1] = __uint_as_float(raw[i].x & 0xFFFF0000u);
+          a[2] = __uint_as_float(raw[i].y << 16);
+          a[3] = __uint_as_float(raw[i].y & 0xFFFF0000u);
         } else {
-          const float4 f = *(const float4 *)((const float *)g.x[slot] + xo + j);
-          a[0] = f.x;
-          a[1] = f.y;
-          a[2] = f.z;
-          a[3] = f.w;
+          a[0] = __uint_as_float(raw[i].x);
+          a[1] = __uint_as_float(raw[i].y);
+          a[2] = __uint_as_float(raw[i].z);
+          a[3] = __uint_as_float(raw[i].w);
         }
-      } else {
+      } else {  // the layer's tail, or an input without 16-byte alignment
+        const int64_t j = (t << lgR) + b0 + 4 * c4;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           if (j + k < n) a[k] = load_x(g.x[slot], dtype, xo + j + k);
@@ -216,11 +259,12 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
 // outputs X_{r + P j} (and X_{(P-r) + P (J-1-j)}), scaled by G into y.
 // ---------------------------------------------------------------------------
 template <int LGNT, int LGCAP>
-__global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
+__global__ __launch_bounds__(1 << LGNT, 4) void k_ffq_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int lgD,
                                                  int64_t bc, const float *__restrict__ gtab, float c1, float c2,
                                                  const float2 *__restrict__ tw, int lgS) {
   constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
   __shared__ float2 buf[CAP];
+  __shared__ float2 twl[1 << kLgTwl];
   int64_t item, v;
   if (!xcd_decode(g.item0[g.n], bc, item, v)) return;
   const int slot = find_slot(g, item);
@@ -232,6 +276,9 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
   const bool pair = r > 0 && 2 * r < P;
   const int lgQb = std::min(std::min(lgQ, LGCAP - lgJ), LGNT);
   const int Qb = 1 << lgQb, nqb = 1 << (lgQ - lgQb);
+  const bool twlds = lgJ <= kLgTwl;
+  if (twlds)
+    for (int m = threadIdx.x; m < J; m += NT) twl[m] = tw[(int64_t)m << (lgS - lgJ)];  // w_J^m
   const int lgG = lgJ <= LGNT ? LGNT - lgJ : 0;  // threads per output row
   const int G = 1 << lgG;
   const int rpt = lgJ > LGNT ? 1 << (lgJ - LGNT) : 1;  // rows per thread
@@ -243,6 +290,13 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
   const int qq_l = threadIdx.x & (Qb - 1), s0 = threadIdx.x >> lgQb, ds = NT >> lgQb;
   const float2 rstep = cis_neg(((int64_t)ds * r) & ((1ll << lgM) - 1), lgM);   // w_M^{ds r}
   const float2 rstart = cis_neg(((int64_t)s0 * r) & ((1ll << lgM) - 1), lgM);  // w_M^{s0 r}
+  // the residue's R = J Q values through a buffer resource (8 R bytes < 2^32): lane offset of row s0,
+  // column qq_l; uniform step of ds rows
+  const __amdgpu_buffer_rsrc_t ur = buf_rsrc(u, (uint32_t)(8ll << lgR));
+  const uint32_t vo = (uint32_t)(qq_l + ((int64_t)s0 << lgQ)) * 8u;
+  const uint32_t sstep = (uint32_t)(((int64_t)ds << lgQ) * 8);
+  const int nr = (J << lgQb) >= NT ? (J << lgQb) >> LGNT : 1;
+  const bool act = s0 < J;
   // y (+)= the scaled sums of output row j (sets A and B, X_{N/2} for r = 0)
   auto emit = [&](int j, float2 a, float2 b, float2 nn, bool add) {
     const int64_t ka = r + ((int64_t)j << lgP);
@@ -267,17 +321,38 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_fwd(const LayerDesc *__restri
     *pa = va;
     if (pair) *pb = vb;
   };
+  // J Qb <= CAP values per column block: nr <= MAXE rows s = s0 + i ds per thread; the lane's element
+  // (s, qq_l) goes to buf[threadIdx.x + i NT].  The next block's loads are issued before this block's
+  // transform, so they are in flight during it.
+  typedef unsigned int u2v __attribute__((ext_vector_type(2)));
+  float2 val[MAXE];
+  auto load_block = [&](int64_t q0) {
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      if (i < nr && act) {
+        const u2v w2 = __builtin_amdgcn_raw_buffer_load_b64(ur, (int)vo, (int)(q0 * 8 + i * sstep), 0);
+        val[i] = make_float2(__uint_as_float(w2.x), __uint_as_float(w2.y));
+      }
+    }
+  };
+  load_block(0);
   for (int qb = 0; qb < nqb; ++qb) {
     const int64_t q0 = (int64_t)qb << lgQb;
     {
       float2 tr = rstart;
-      for (int s = s0, i = 0; s < J; s += ds, ++i) {
-        const float2 val = u[q0 + qq_l + ((int64_t)s << lgQ)];
-        buf[(s << lgQb) + qq_l] = cmul(val, tr);
-        tr = cmul(tr, rstep);
+#pragma unroll
+      for (int i = 0; i < MAXE; ++i) {
+        if (i < nr && act) {
+          buf[threadIdx.x + i * NT] = cmul(val[i], tr);
+          tr = cmul(tr, rstep);
+        }
       }
     }
-    lds_fft<false, NT, MAXE>(buf, lgJ, lgQb, tw, lgS);
+    if (qb + 1 < nqb) load_block(q0 + Qb);
+    if (twlds)
+      lds_fft<false, NT, MAXE, true>(buf, lgJ, lgQb, twl, lgJ);
+    else
+      lds_fft<false, NT, MAXE, true>(buf, lgJ, lgQb, tw, lgS);
     for (int i = 0; i < rpt; ++i) {
       const int j = j0 + (i << (LGNT - lgG));
       float2 a = make_float2(0.f, 0.f), b = a, nn = a;
@@ -454,14 +529,27 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffq_T(const LayerDesc *__restrict
       float2 wm = cis_neg((q * s0) & ((1ll << lgR) - 1), lgR);
       const float2 wst = cis_neg((q * ds) & ((1ll << lgR) - 1), lgR);
       const float2 wqq = cis_neg(q & ((1ll << lgQ) - 1), lgQ);
-      for (int m = s0; m < J; m += ds) {
-        float2 a = cmulc(coef(zv, gl, r + ((int64_t)m << lgP), c1, c2), wm);
-        if (pair) {
-          const float2 cp = coef(zv, gl, (P - r) + ((int64_t)(J - m - 1) << lgP), c1, c2);
-          a = cadd(a, cmul(cconj(cp), cmulc(wqq, wm)));
+      // coefficient loads four rows at a time, issued before they are used
+      for (int m0 = s0; m0 < J; m0 += 4 * ds) {
+        float2 ca[4], cp[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int m = m0 + k * ds;
+          if (m < J) {
+            ca[k] = coef(zv, gl, r + ((int64_t)m << lgP), c1, c2);
+            if (pair) cp[k] = coef(zv, gl, (P - r) + ((int64_t)(J - m - 1) << lgP), c1, c2);
+          }
         }
-        buf[(m << lgQb) + qq_l] = a;
-        wm = cmul(wm, wst);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int m = m0 + k * ds;
+          if (m < J) {
+            float2 a = cmulc(ca[k], wm);
+            if (pair) a = cadd(a, cmul(cconj(cp[k]), cmulc(wqq, wm)));
+            buf[(m << lgQb) + qq_l] = a;
+            wm = cmul(wm, wst);
+          }
+        }
       }
     }
     lds_fft<true, NT, MAXE>(buf, lgJ, lgQb, tw, lgS);
@@ -504,10 +592,24 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_T(const LayerDesc *__restrict
   const int nw = 1 << (lgW - 5);
   build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
   const float *u = g.u[slot] + v * g.us[slot];
+  // (P/2 + 1) Wc <= CAP/2 + Wc values: at most MAXL per thread, loaded before use
+  constexpr int MAXL = CAP / (2 * NT) + 1;
   const int tot = (P / 2 + 1) << lgWc;
-  for (int e = threadIdx.x; e < tot; e += NT) {
+  float4 Ev[MAXL];
+#pragma unroll
+  for (int i = 0; i < MAXL; ++i) {
+    const int e = threadIdx.x + i * NT;
+    if (e < tot) {
+      const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
+      Ev[i] = *(const float4 *)(u + (((int64_t)r << lgR) + b0 + 2 * c) * 2);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXL; ++i) {
+    const int e = threadIdx.x + i * NT;
+    if (e >= tot) break;
     const int r = e >> lgWc, c = e & ((1 << lgWc) - 1);
-    const float4 E = *(const float4 *)(u + (((int64_t)r << lgR) + b0 + 2 * c) * 2);
+    const float4 E = Ev[i];
     const bool edge = r == 0 || 2 * r == P;
     const float2 ha = edge ? make_float2(E.x, 0.f) : make_float2(0.5f * E.x, 0.5f * E.y);
     const float2 hb = edge ? make_float2(E.z, 0.f) : make_float2(0.5f * E.z, 0.5f * E.w);
@@ -518,19 +620,35 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_T(const LayerDesc *__restrict
   void *o = (void *)g.x[slot];
   const float *th = g.th[slot];
   const int64_t oo = (b_begin + v) * n;
-  for (int e = threadIdx.x; e < (int)(rows << lgWc); e += NT) {
+  // rows * Wc <= CAP values: at most MAXE per thread; the theta0 loads go out before the sums
+  const int tot1 = (int)(rows << lgWc);
+  float2 thv[MAXE];
+  if (th) {
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      const int e = threadIdx.x + i * NT;
+      const int64_t j = ((int64_t)(e >> lgWc) << lgR) + b0 + 2 * (e & ((1 << lgWc) - 1));
+      thv[i] = make_float2(0.f, 0.f);
+      if (e < tot1 && j < n) thv[i].x = th[j];
+      if (e < tot1 && j + 1 < n) thv[i].y = th[j + 1];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int e = threadIdx.x + i * NT;
+    if (e >= tot1) break;
     const int64_t t = e >> lgWc;
     const int c = e & ((1 << lgWc) - 1);
     const float2 zt = buf[e];
     const int64_t j = (t << lgR) + b0 + 2 * c;
     if (j < n) {
       float a = flip(zt.x, row_sign_bit(sw, t, nw, lgR, b0, j));
-      if (th) a += th[j];
+      if (th) a += thv[i].x;
       store_out(o, out_dtype, oo + j, a);
     }
     if (j + 1 < n) {
       float b = flip(zt.y, row_sign_bit(sw, t, nw, lgR, b0, j + 1));
-      if (th) b += th[j + 1];
+      if (th) b += thv[i].y;
       store_out(o, out_dtype, oo + j + 1, b);
     }
   }
@@ -631,7 +749,8 @@ int64_t afjlf_u_floats(const sk_sketch *s, int layer) {
 
 bool afjlf_two_pass_ok(int lgnp, int lgD) {
   const FfGeom fg = ff_geom(lgnp, lgD);
-  return fg.lgQ >= 1 && fg.lgJ >= 0 && fg.lgJ <= kLgCap;
+  // (the residue buffers are addressed with 32-bit byte offsets: 8 R <= 2^30)
+  return fg.lgQ >= 1 && fg.lgJ >= 0 && fg.lgJ <= kLgCap && fg.lgR <= 27;
 }
 
 int64_t afjlf_bytes_per_vector(const sk_sketch *s, int l0, int l1, bool transpose) {
@@ -754,20 +873,22 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
         const int i = g1.n;
         const LayerDesc &ld = s->layers[l];
         const FfGeom fg = ff_geom(ld.lgnp, lgD);
+        const FfGeom fg1 = ff_geom(ld.lgnp, lgD, kLgRows);  // pass 1 column blocks
         gb += tb * ld.n * esz;
         g1.layer[i] = g2.layer[i] = l;
         g1.x[i] = grads[l - l0];
         g1.u[i] = g2.u[i] = ubase + off;
         g1.us[i] = g2.us[i] = afjlf_u_floats(s, l);
         g2.y[i] = ybase + (int64_t)(l - l0) * lstride + t0 * D;
-        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (fg.lgR - fg.lgW));
+        g1.item0[i + 1] = g1.item0[i] + ((int64_t)1 << (fg1.lgR - fg1.lgW));
         g2.item0[i + 1] = g2.item0[i] + ((int64_t)1 << (fg.lgP - 1)) + 1;
         off += g1.us[i] * tb;
         ++g1.n;
         ++g2.n;
       }
       SK_PROF(SK_PROF_FF_ROWS, gb,
-              hipLaunchKernelGGL((k_ffr_fwd<9, 13>), dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))), dim3(512), 0,
+              hipLaunchKernelGGL((k_ffr_fwd<kLgRows - 4, kLgRows>), dim3((unsigned)(g1.item0[g1.n] * ceil8(tb))),
+                                 dim3(1 << (kLgRows - 4)), 0,
                                  st, s->d_layers, g1, dtype, lgD, b_begin + t0, tb, tw, s->ftw_lg, s->key));
       const dim3 grid2((unsigned)(g2.item0[g2.n] * ceil8(tb)));
       SK_PROF(SK_PROF_FF_RES, 0, {

@@ -39,18 +39,24 @@ __device__ __forceinline__ float2 twiddle32(const float2 *__restrict__ tw, int l
   return INV ? cconj(w) : w;
 }
 
-// One Stockham stage of radix R over the whole block's butterflies.
-template <bool INV, int R, int NT, int MAXB>
+// One Stockham stage of radix R over the whole block's butterflies.  OPQ: the
+// thread index passes through an empty asm, so the index arithmetic stays
+// inside the caller's loops instead of being hoisted out of them into
+// registers that outlive the transform (for transforms inside a loop that
+// keeps other loads in flight).
+template <bool INV, int R, int NT, int MAXB, bool OPQ>
 __device__ __forceinline__ void fft_stage(float2 *buf, int lgL, int lgC, int lgNs, const float2 *__restrict__ tw,
                                           int lgS) {
   constexpr int lgR = R == 4 ? 2 : 1;
+  int tid = threadIdx.x;
+  if (OPQ) asm volatile("" : "+v"(tid));
   const int C = 1 << lgC;
   const int nb = 1 << (lgL + lgC - lgR);  // butterflies of the stage
   const int q = 1 << (lgL - lgR);         // L / R
   float2 v[MAXB][R];
 #pragma unroll
   for (int i = 0; i < MAXB; ++i) {
-    const int e = threadIdx.x + NT * i;
+    const int e = tid + NT * i;
     if (e < nb) {
       const int col = e & (C - 1), j = e >> lgC;
 #pragma unroll
@@ -60,7 +66,7 @@ __device__ __forceinline__ void fft_stage(float2 *buf, int lgL, int lgC, int lgN
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < MAXB; ++i) {
-    const int e = threadIdx.x + NT * i;
+    const int e = tid + NT * i;
     if (e < nb) {
       const int col = e & (C - 1), j = e >> lgC;
       const int k = j & ((1 << lgNs) - 1);
@@ -97,12 +103,12 @@ __device__ __forceinline__ void fft_stage(float2 *buf, int lgL, int lgC, int lgN
 }
 
 // In-place FFT of length 2^lgL along pos for 2^lgC columns.
-template <bool INV, int NT, int MAXE>
-__device__ void lds_fft(float2 *buf, int lgL, int lgC, const float2 *__restrict__ tw, int lgS) {
+template <bool INV, int NT, int MAXE, bool OPQ = false>
+__device__ __forceinline__ void lds_fft(float2 *buf, int lgL, int lgC, const float2 *__restrict__ tw, int lgS) {
   __syncthreads();  // the caller's writes to buf are visible to every thread
   int lgNs = 0;
-  for (; lgNs + 2 <= lgL; lgNs += 2) fft_stage<INV, 4, NT, (MAXE + 3) / 4>(buf, lgL, lgC, lgNs, tw, lgS);
-  if (lgNs < lgL) fft_stage<INV, 2, NT, (MAXE + 1) / 2>(buf, lgL, lgC, lgNs, tw, lgS);
+  for (; lgNs + 2 <= lgL; lgNs += 2) fft_stage<INV, 4, NT, (MAXE + 3) / 4, OPQ>(buf, lgL, lgC, lgNs, tw, lgS);
+  if (lgNs < lgL) fft_stage<INV, 2, NT, (MAXE + 1) / 2, OPQ>(buf, lgL, lgC, lgNs, tw, lgS);
 }
 
 }  // namespace sk

@@ -330,8 +330,9 @@ def test_ffd_small_D_vector_tiles(D, dev):
 @pytest.mark.parametrize("shapes,D", [([(1, 5000), (1, 20000), (1, 9)], 16384), ([(1, 2 ** 20), (2, 3)], 16)])
 def test_fjl_transpose_tiles(shapes, D, dev):
     """FJL transpose with the sample scatter fused into the first transform pass (a per-tile range of
-    the position-sorted sample list): D > N' (several samples per position, summed in id order), empty
-    tiles (D = 16 samples over 128 tiles of 2^13), tiny layers (N' < 16), three vectors, theta0."""
+    the position-sorted sample list): layers shorter than D padded to N' = D (D samples over D positions,
+    so many positions take several samples, summed in id order), empty tiles (16 samples over the 128
+    tiles of 2^13 entries of an N' = 2^20 layer), tiny layers (n = 9 and 6), three vectors, theta0."""
     seed = 77 + D
     g = torch.Generator().manual_seed(seed)
     z = torch.randn((3, D), generator=g)
