@@ -52,7 +52,7 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
              "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
              "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd",
-             "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
+             "afjlf:ff_small": "k_ffs_fwd", "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
              "affd:gather": "k_affdT_outm"}
 
 
@@ -203,9 +203,8 @@ def cpu_baseline(cfg: str):
         nbytes = 2 * len(c["kinds"]) * c["batch"] * shapes[0][1] * 4
         sample = f"all {c['batch']} rows, FJL+FFD forward and transpose"
     elif cfg in ("c2", "c10"):
-        # the first two transformer blocks (24 tensors, 14.2M parameters): every row of the batch for the C
-        # oracle, 16 rows for the numpy one
-        sub, nrows = shapes[2:26], (c["batch"] if cfg == "c2" else 16)
+        # the first two transformer blocks (24 tensors, 14.2M parameters), every row of the batch
+        sub, nrows = shapes[2:26], c["batch"]
         xs = rows_for(sub, nrows)
         for k in c["kinds"]:
             O.apply(k, sub, D, seed, xs, layer0=2, nthreads=cores)

@@ -277,10 +277,10 @@ enum {
   SK_PROF_QH_SECOND = 12,/* SK_QKH/SK_AFJLQ/SK_AFFDQ second contraction        */
   SK_PROF_QH_T = 13,     /* SK_QKH/SK_AFJLQ/SK_AFFDQ transposes               */
   SK_PROF_FFD_T = 14,    /* FFD transpose with D <= 2^13 (one launch)        */
-  SK_PROF_FF_ROWS = 15,  /* AFJLF kernels that read the gradients (pass 1 and
-                            the one-kernel small layers)                     */
+  SK_PROF_FF_ROWS = 15,  /* AFJLF pass 1 over the rows (reads the gradients) */
   SK_PROF_FF_RES = 16,   /* AFJLF residue pass and the layer sum             */
-  SK_PROF_CLASSES = 17
+  SK_PROF_FF_SMALL = 17, /* AFJLF one-kernel layers (N' = D, forward)        */
+  SK_PROF_CLASSES = 18
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

@@ -855,7 +855,7 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
       gb += bc * s->layers[g.layer[i]].n * esz;
     }
     const dim3 grid((unsigned)(g.n * ceil8(bc)));
-    SK_PROF(SK_PROF_FF_ROWS, gb, {
+    SK_PROF(SK_PROF_FF_SMALL, gb, {
       if (big)
         hipLaunchKernelGGL((k_ffs_fwd<10, 14>), grid, dim3(1024), 0, st, s->d_layers, g, dtype, lgD, b_begin, bc,
                            s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
@@ -902,7 +902,7 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
     }
   });
   const dim3 gt((unsigned)((D / 4 + 255) / 256), (unsigned)bc);
-  SK_PROF(SK_PROF_FF_RES, bc * D * 4,
+  SK_PROF(SK_PROF_GATHER, bc * D * 4,
           hipLaunchKernelGGL(k_ff_tail, gt, dim3(256), 0, st, ybase, nl, lstride, D, b_begin, out, (int)accumulate));
 }
 
