@@ -1032,11 +1032,17 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           break;
         case SK_FJL: {
           const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the scatter
+          const float oscale = (float)std::sqrt((double)ld.np / (double)s->D);
           SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_fjl_T_pass0(s, l, z, b0, bc, s->ws, lgw, st));
-          SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from(s->ws, bc, ld.lgnp, lgw, st));
-          SK_PROF(SK_PROF_GATHER, obytes,
-                  launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th,
-                                    (float)std::sqrt((double)ld.np / (double)s->D), st));
+          if (fjl_last_signed_ok(s, l, lgw)) {
+            // the remaining passes, the last one writing the signed output
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from_but_last(s->ws, bc, ld.lgnp, lgw, st));
+            SK_PROF(SK_PROF_GATHER, obytes,
+                    launch_fjl_last_signed(s, l, s->ws, lgw, b0, bc, o, out_dtype, th, oscale, st));
+          } else {
+            SK_PROF(SK_PROF_FWHT, 0, fwht_inplace_from(s->ws, bc, ld.lgnp, lgw, st));
+            SK_PROF(SK_PROF_GATHER, obytes, launch_signed_out(s, l, s->ws, b0, bc, o, out_dtype, th, oscale, st));
+          }
           break;
         }
         case SK_FFD:

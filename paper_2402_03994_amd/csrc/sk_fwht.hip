@@ -1208,6 +1208,72 @@ void launch_fjl_last_gather(const sk_sketch *s, int layer, const float *w, int64
   SK_CHECK_LAUNCH();
 }
 
+// FJL transpose, last transform pass fused with the signed output: the pass
+// over index bits [lo, lo + w) (the top bits; runs of 2^lgcs >= 32
+// consecutive positions per row of the tile), then
+// out[j] = oscale b_j (H w)[j] (+ theta0[j]) for the positions j < n of the
+// tile, so the transformed vector is never written back.  The tile's sign
+// words are built into LDS first (one word per 32 positions of a run).
+__global__ __launch_bounds__(256) void k_fjl_last_signed(const LayerDesc *__restrict__ layers, int layer,
+                                                         const float *__restrict__ data, int lo, int w, int lgcs,
+                                                         float scale, int64_t b_begin, void *__restrict__ out,
+                                                         int out_dtype, const float *__restrict__ theta0, Key key) {
+  extern __shared__ float sm[];
+  const LayerDesc &ld = layers[layer];
+  const int lgn = ld.lgnp;
+  const int64_t n = ld.n;
+  const int total = 1 << (w + lgcs);
+  float *sv = sm;
+  uint32_t *sw = reinterpret_cast<uint32_t *>(sm + p16_floats(total));
+  const int64_t tiles_per_vec = (1ll << lgn) >> (w + lgcs);
+  const int64_t v = blockIdx.x / tiles_per_vec;
+  const int64_t tv = blockIdx.x - v * tiles_per_vec;
+  const int lgcb = lo - lgcs;
+  const int64_t j0 = ((tv >> lgcb) << (lo + w)) + ((tv & ((1ll << lgcb) - 1)) << lgcs);  // first position
+  const float *base = data + v * (1ll << lgn) + j0;
+  const int cmask = (1 << lgcs) - 1;
+  const int lgwpr = lgcs - 5;  // sign words per row of the tile
+  for (int k = threadIdx.x; k < (total >> 5); k += 256) {
+    const int64_t j = j0 + ((int64_t)(k >> lgwpr) << lo) + ((int64_t)(k & ((1 << lgwpr) - 1)) << 5);
+    sw[k] = sign_word((uint64_t)j, (uint32_t)ld.layer_id, key);
+  }
+  for (int e = threadIdx.x; e < total; e += 256) sv[p16(e)] = base[((int64_t)(e >> lgcs) << lo) + (e & cmask)];
+  lds_fwht_regs(sv, w + lgcs, lgcs);
+  const int64_t ob = (b_begin + v) * n;
+  for (int e = threadIdx.x; e < total; e += 256) {
+    const int64_t j = j0 + ((int64_t)(e >> lgcs) << lo) + (e & cmask);
+    if (j < n) {
+      float val = flip(sv[p16(e)] * scale, (sw[e >> 5] >> (e & 31)) & 1u);
+      if (theta0) val += theta0[j];
+      store_out(out, out_dtype, ob + j, val);
+    }
+  }
+}
+
+// True when the FJL transpose of a layer ends with a pass that
+// k_fjl_last_signed can take (a pass after bit lo0 whose tile rows hold runs of
+// at least 32 consecutive positions).
+bool fjl_last_signed_ok(const sk_sketch *s, int layer, int lo0) {
+  const LayerDesc &ld = s->layers[layer];
+  int los[64], ws[64], lgcss[64];
+  const int np = fwht_pass_plan(ld.lgnp, lo0, los, ws, lgcss);
+  return np >= 1 && lo0 < ld.lgnp && lgcss[np - 1] >= 5;
+}
+
+void launch_fjl_last_signed(const sk_sketch *s, int layer, const float *w, int lo0, int64_t b_begin, int64_t bc,
+                            void *out, int out_dtype, const float *theta0, float oscale, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  int los[64], ws[64], lgcss[64];
+  const int np = fwht_pass_plan(ld.lgnp, lo0, los, ws, lgcss);
+  const int lo = los[np - 1], wl = ws[np - 1], lgcs = lgcss[np - 1];
+  const int64_t tiles = bc * ((1ll << ld.lgnp) >> (wl + lgcs));
+  const size_t shm = sizeof(float) * p16_floats(1 << (wl + lgcs)) + sizeof(uint32_t) * ((1 << (wl + lgcs)) >> 5);
+  const float scale = (float)(oscale / std::sqrt((double)(1ll << wl)));
+  hipLaunchKernelGGL(k_fjl_last_signed, dim3((unsigned)tiles), dim3(256), shm, st, s->d_layers, layer, w, lo, wl,
+                     lgcs, scale, b_begin, out, out_dtype, theta0, s->key);
+  SK_CHECK_LAUNCH();
+}
+
 // FJL transpose, first transform pass fused with the scatter of the D samples:
 // one workgroup per (vector, tile of 2^w positions of N'), w = min(log2 N', 13).
 // The tile starts at zero in LDS; every unique sample position inside it (a
@@ -1304,7 +1370,7 @@ int64_t ffd_live_blocks(const sk_sketch *s, int layer) {
   return (ld.n + s->D - 1) / s->D;
 }
 
-constexpr int kFfdGroup = 2;  // blocks per workgroup (small D)
+constexpr int kFfdGroup = 1;  // blocks per workgroup (small D)
 
 int64_t ffd_small_groups(const sk_sketch *s, int layer) {
   return (ffd_live_blocks(s, layer) + kFfdGroup - 1) / kFfdGroup;
@@ -1460,9 +1526,9 @@ void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtyp
                           float *part, int64_t slot0, int64_t groups, hipStream_t st) {
   const int lgD = log2_exact(s->D);
   if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
-  // tiles of 2 vectors: twice the workgroups of 4-vector tiles (measured faster on 2^20-entry
-  // vectors, D = 4096) for twice the table builds
-  ffd_small_fwd_go<2>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, st);
+  // one block and 4 vectors per workgroup (2^20-entry vectors, batch 8, D = 4096, forward per call:
+  // 2 blocks x 2 vectors 64.3 us, 2 x 4 81.8, 1 x 2 63.6, 1 x 4 57.5, 1 x 8 82.0)
+  ffd_small_fwd_go<4>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, st);
   SK_CHECK_LAUNCH();
 }
 
@@ -1592,7 +1658,7 @@ void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b
                         int out_dtype, const float *theta0, hipStream_t st) {
   const int lgD = log2_exact(s->D);
   if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
-  constexpr int VT = 2;
+  constexpr int VT = 4;  // vectors per workgroup (same workload, per call: 2 -> 58.4 us, 4 -> 51.2, 8 -> 73.4)
   const dim3 grid((unsigned)ffd_live_blocks(s, layer), (unsigned)((bc + VT - 1) / VT));
   const size_t shm = ffd_small_shm(s->D);
 #define SK_FFDT(PER)                                                                                              \

@@ -18,6 +18,9 @@ void fwht_inplace_from_but_last(float *data, int64_t V, int lgn, int lo0, hipStr
 int fwht_pass_plan(int lgn, int lo0, int *los, int *ws, int *lgcss);
 // FJL forward, the last transform pass of layers with N' > 2^13 fused with the sample gather
 // (sample lists sorted by the pass's blocks at creation).
+bool fjl_last_signed_ok(const sk_sketch *s, int layer, int lo0);
+void launch_fjl_last_signed(const sk_sketch *s, int layer, const float *w, int lo0, int64_t b_begin, int64_t bc,
+                            void *out, int out_dtype, const float *theta0, float oscale, hipStream_t st);
 void launch_fjl_last_gather(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, float *out,
                             bool accumulate, hipStream_t st);
 // FJL forward: signed load fused with the transform over index bits [0, lgw) (lgw = min(log2 N', 13)).
