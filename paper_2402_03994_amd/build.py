@@ -1,8 +1,11 @@
 """Build the gfx950 sketch library (libsketch.so) in-tree with hipcc.
 
 Every .hip file under csrc/ is compiled for gfx950 only, with packed-fp32
-instruction selection disabled, and linked into one shared library placed next
-to this file.  Always recompiles (the caller decides when to build).
+instruction selection disabled and without the promotion of per-thread arrays
+to LDS (the kernels size their LDS and occupancy by hand; the pass had moved a
+register staging array of the QK contraction into LDS, an extra LDS round trip
+and 8 KB per workgroup), and linked into one shared library placed next to this
+file.  Always recompiles (the caller decides when to build).
 """
 from __future__ import annotations
 
@@ -22,6 +25,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-disable-promote-alloca-to-lds",
     "-Wall", "-Wno-unused-function", "-I", INCLUDE, "-I", CSRC,
 ]
 
