@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, c
   for (int mr = 0; mr < kQkMR; ++mr) {
     const int64_t row = r0 + mr * 16 + li;
     rv[mr] = row < rows;
-    xr[mr] = x + (b_begin * m + (rv[mr] ? row : 0)) * n + g * 32;
+    xr[mr] = x + (b_begin * m + (rv[mr] ? row : 0)) * n + g * 8;
   }
   floatx4 acc[kQkMR][NT];
 #pragma unroll
@@ -129,13 +129,15 @@ __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, c
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[mr][t] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int64_t k0 = 0; k0 < n; k0 += 128) {
-    // this wave's X fragments: 64 contiguous bytes of each of its rows
+    // this wave's X fragments: MFMA cc takes k = k0 + 32 cc + 8 g .. + 7 in lane (li, g), so each load
+    // instruction reads 64 contiguous bytes of each of 16 rows (16 cache lines, not 32 half-used ones:
+    // the address units bound this loop)
     Pack8 a[kQkMR][4];
 #pragma unroll
     for (int mr = 0; mr < kQkMR; ++mr)
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc)
-        a[mr][cc].u = rv[mr] ? *(const uint4 *)(xr[mr] + k0 + cc * 8) : make_uint4(0, 0, 0, 0);
+        a[mr][cc].u = rv[mr] ? *(const uint4 *)(xr[mr] + k0 + cc * 32) : make_uint4(0, 0, 0, 0);
     __syncthreads();  // previous chunk of B consumed
     // B[hi|lo][row][k0 .. k0+127] -> LDS, 16 bytes per thread per step
     for (int e = threadIdx.x; e < 2 * DB * 16; e += 256) {
@@ -147,13 +149,13 @@ __global__ __launch_bounds__(256) void k_qk_s1(const uint16_t *__restrict__ x, c
     __syncthreads();
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const unsigned char *bh = bs + (t * 16 + li) * kQkBRow + g * 64;
+      const unsigned char *bh = bs + (t * 16 + li) * kQkBRow + g * 16;
       const unsigned char *bl = bh + DB * kQkBRow;
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc) {
         Pack8 vh, vl;
-        vh.u = *(const uint4 *)(bh + cc * 16);
-        vl.u = *(const uint4 *)(bl + cc * 16);
+        vh.u = *(const uint4 *)(bh + cc * 64);
+        vl.u = *(const uint4 *)(bl + cc * 64);
 #pragma unroll
         for (int mr = 0; mr < kQkMR; ++mr)
           acc[mr][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mr][cc].v, vh.v, acc[mr][t], 0, 0, 0);
