@@ -12,7 +12,8 @@ intrinsic-dimension search.  Prints one JSON line.
 "value" is parameter-space bytes per second: gradient bytes read by forward
 sketches plus parameter-vector bytes written by transposes, summed over the
 calls of a step.  The roofline object covers the kernel class with the largest
-share of device time (intermediate-only classes included), found in an
+share of device time among the classes that read the inputs (a class that moves
+only intermediates and takes longer is named in it as largest_class), found in an
 untimed calibration pass that brackets every kernel class with HIP events (the
 per-class breakdown comes from it).  In the timed region only that class's
 launches are bracketed, with HIP events on the stream they run on; "achieved"
@@ -47,13 +48,23 @@ MFMA_F32_PEAK_TFLOPS = 157.3
 
 # kernel launched by each single-kernel profile class (the rocprofv3 name)
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
-             "ffd:ffd": "k_ffd_small_fwd", "ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
-             "fjl:prolog": "k_fjl_pass0", "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm",
-             "afjlq:qh_second": "k_qh_gemm", "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm",
-             "affdq:qh_t": "k_qh_gemm", "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine",
-             "afjl:gather": "k_afjl_T_out", "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd",
-             "afjlf:ff_small": "k_ffs_fwd", "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
+             "ffd:ffd": "k_ffd_small_fwd", "ffd:gather": "k_reduce_partials", "fjl:prolog": "k_fjl_pass0",
+             "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm", "afjlq:qh_second": "k_qh_gemm",
+             "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm", "affdq:qh_t": "k_qh_gemm",
+             "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine", "afjl:gather": "k_afjl_T_out",
+             "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd", "afjlf:ff_small": "k_ffs_fwd",
+             "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
              "affd:gather": "k_affdT_outm"}
+# FFD with D = 2^20 (rows / cols passes): prolog = the first rows pass of the forward, gather = the last cols
+# pass of the transpose; the ffd class groups the middle passes (several kernels)
+KERNEL_OF_FFD_LARGE = {"ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
+                       "ffd:ffd": "k_ffdL middle passes"}
+
+
+def kernel_of(cfg: str, kclass: str) -> str:
+    if W.CONFIGS[cfg]["D"] == 1 << 20 and kclass in KERNEL_OF_FFD_LARGE:
+        return KERNEL_OF_FFD_LARGE[kclass]
+    return KERNEL_OF.get(kclass, kclass)
 
 
 def qh_flops(kind, shapes, D):
@@ -112,14 +123,16 @@ def source_hash(cfg: str) -> str:
 
 
 def measured_traffic(cfg: str, kclass: str):
-    """HBM bytes per launch of a kernel class from a committed rocprofv3 counter summary, if current."""
+    """Bytes per launch between the L2 caches and the memory fabric (rocprofv3 FETCH_SIZE + WRITE_SIZE, EA
+    traffic: hits in the memory-side cache included, so an upper bound on HBM bytes) of a kernel class from a
+    committed counter summary, if it was taken on the current sources."""
     p = os.path.join(ROOT, "profiles", f"traffic_{cfg}_{kclass.replace(':', '_')}.json")
     if not os.path.exists(p):
         return None
     rec = json.load(open(p))
     if rec.get("source_hash") != source_hash(cfg):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("ea_bytes_per_launch")
 
 
 def copy_probe() -> int:
@@ -151,10 +164,10 @@ def _counter_per_launch(csv_path: str, name: str, counter: str):
 
 def traffic_json(cfg: str, kclass: str, fetch_csv: str, write_csv: str, copy_fetch_csv: str,
                  copy_write_csv: str) -> int:
-    """Per-launch HBM bytes of a kernel class from rocprofv3 --pmc FETCH_SIZE and
+    """Per-launch EA bytes (L2 <-> memory fabric) of a kernel class from rocprofv3 --pmc FETCH_SIZE and
     WRITE_SIZE runs (KiB per dispatch), each scaled by the reading for the 1 GiB
     copy of copy_probe(); written to profiles/ with the current source hash."""
-    kname = KERNEL_OF[kclass]
+    kname = kernel_of(cfg, kclass)
     f_kib, nf = _counter_per_launch(fetch_csv, kname, "FETCH_SIZE")
     w_kib, nw = _counter_per_launch(write_csv, kname, "WRITE_SIZE")
     cf_kib, _ = _counter_per_launch(copy_fetch_csv, "copy", "FETCH_SIZE")
@@ -165,9 +178,9 @@ def traffic_json(cfg: str, kclass: str, fetch_csv: str, write_csv: str, copy_fet
            "fetch_kib_per_launch": round(f_kib, 1), "write_kib_per_launch": round(w_kib, 1), "launches": nf,
            "copy_fetch_kib_per_gib": round(cf_kib, 1), "copy_write_kib_per_gib": round(cw_kib, 1),
            "fetch_scale": round(cal_f, 4), "write_scale": round(cal_w, 4),
-           "hbm_read_bytes_per_launch": round(f_kib * 1024 * cal_f),
-           "hbm_write_bytes_per_launch": round(w_kib * 1024 * cal_w),
-           "hbm_bytes_per_launch": round(f_kib * 1024 * cal_f + w_kib * 1024 * cal_w)}
+           "ea_read_bytes_per_launch": round(f_kib * 1024 * cal_f),
+           "ea_write_bytes_per_launch": round(w_kib * 1024 * cal_w),
+           "ea_bytes_per_launch": round(f_kib * 1024 * cal_f + w_kib * 1024 * cal_w)}
     out = os.path.join(ROOT, "profiles", f"traffic_{cfg}_{kclass.replace(':', '_')}.json")
     with open(out, "w") as fh:
         json.dump(rec, fh, indent=1)
@@ -558,9 +571,12 @@ def main() -> int:
             e[0] += t
             e[1] += n
             e[2] += by
-    # the dominant kernel class by device time (classes that move only
-    # intermediates count, with zero algorithmic bytes)
-    dom = max(classes, key=lambda c: classes[c][0])
+    # the dominant kernel class: the largest by device time among the classes that read the inputs (their
+    # algorithmic bytes give "achieved"); when a class that moves only intermediates takes more time, it is
+    # named beside it (largest_class), and per_kind covers every kernel of each call
+    dom_any = max(classes, key=lambda c: classes[c][0])
+    cands = [c for c in classes if classes[c][2] > 0] or list(classes)
+    dom = max(cands, key=lambda c: classes[c][0])
     dom_kind, dom_cls = dom.split(":", 1)
 
     # timed region: K steps, with HIP events (on the stream the kernels run on)
@@ -583,12 +599,16 @@ def main() -> int:
         pbytes = (2 * hvps + 1) * c["shapes"][0][0] * c["shapes"][0][1] * 4
     value = pbytes / (ms * 1e-3) / 1e9
     achieved = by_dom / (t_dom * 1e-3) / 1e9 if t_dom > 0 else 0.0
-    roofline = {"bound": "hbm", "kernel": KERNEL_OF.get(dom, dom), "class": dom, "achieved": round(achieved, 1),
+    roofline = {"bound": "hbm", "kernel": kernel_of(cfg, dom), "class": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(cfg, dom),
                 "launches": n_dom, "avg_launch_ms": round(t_dom / max(n_dom, 1), 4),
                 "algorithmic_bytes_per_launch": round(by_dom / max(n_dom, 1))}
+    if dom_any != dom:
+        roofline["largest_class"] = {"class": dom_any, "kernel": kernel_of(cfg, dom_any),
+                                     "ms_per_step": round(classes[dom_any][0] / ncal, 3),
+                                     "reads": "intermediates only (no algorithmic bytes)"}
     if cfg == "c3":
         c = W.CONFIGS[cfg]
         flops = sum(2 * s[0] * s[1] * s[3] + 2 * s[2] * s[0] * s[3] for s in c["shapes"]) * c["batch"]
