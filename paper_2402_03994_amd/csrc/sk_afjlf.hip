@@ -56,6 +56,7 @@ constexpr int kSlots = 32;       // layers per launch
 // a copy of the table in LDS: they then issue no global loads, so the loads of
 // the next column block stay in flight across the transform.
 constexpr int kLgTwl = 10;
+constexpr int kLgTwSplit = 9;    // two-level twiddle tables of the one-kernel layers: 2 x 512 entries
 constexpr int kLgRows = 13;      // forward pass 1: transform buffer of 2^kLgRows values, 2^(kLgRows-4) threads
 
 struct FfLayers {
@@ -239,7 +240,7 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
     buf[(t << lgWc) + 2 * c4] = make_float2(a[0], a[1]);
     buf[(t << lgWc) + 2 * c4 + 1] = make_float2(a[2], a[3]);
   }
-  lds_fft<false, NT, MAXE>(buf, lgP, lgWc, tw, lgS);
+  lds_fft<false, NT, MAXE, false, true>(buf, lgP, lgWc, tw, lgS);
   // split the two real columns and write r = 0 .. P/2
   float *u = g.u[slot] + v * g.us[slot];
   const int P = 1 << lgP;
@@ -350,9 +351,9 @@ __global__ __launch_bounds__(1 << LGNT, 4) void k_ffq_fwd(const LayerDesc *__res
     }
     if (qb + 1 < nqb) load_block(q0 + Qb);
     if (twlds)
-      lds_fft<false, NT, MAXE, true>(buf, lgJ, lgQb, twl, lgJ);
+      lds_fft<false, NT, MAXE, true, true>(buf, lgJ, lgQb, twl, lgJ);
     else
-      lds_fft<false, NT, MAXE, true>(buf, lgJ, lgQb, tw, lgS);
+      lds_fft<false, NT, MAXE, true, true>(buf, lgJ, lgQb, tw, lgS);
     for (int i = 0; i < rpt; ++i) {
       const int j = j0 + (i << (LGNT - lgG));
       float2 a = make_float2(0.f, 0.f), b = a, nn = a;
@@ -406,6 +407,7 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
   constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
   __shared__ float2 buf[CAP];
   __shared__ uint32_t sw[CAP / 32];
+  __shared__ float2 tlo[1 << kLgTwSplit], thi[1 << kLgTwSplit];
   int64_t item, v;
   if (!xcd_decode(g.n, bc, item, v)) return;
   const int slot = (int)item;
@@ -416,35 +418,65 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
   const int L = 1 << lgL;
   const int lgcs = lgD - lgL;                       // log2 of the number of c values
   const int lgcg = std::min(lgcs, LGCAP - lgL);    // c values per group
+  const int tot = L << lgcg;                        // transform values per group (<= CAP)
   const uint32_t lid = (uint32_t)ld.layer_id;
+  // w_N^m = thi[m >> lgLo] tlo[m & (2^lgLo - 1)] from two small LDS tables (D <= 2^(2 kLgTwSplit))
+  const int lgLo = lgD >> 1, lgHi = lgD - lgLo;
+  const bool split = lgHi <= kLgTwSplit;
+  if (split) {
+    for (int m = threadIdx.x; m < (1 << lgLo); m += NT) tlo[m] = tw[(int64_t)m << (lgS - lgD)];
+    for (int m = threadIdx.x; m < (1 << lgHi); m += NT) thi[m] = tw[(int64_t)m << (lgS - lgHi)];
+  }
   for (int w = threadIdx.x; w < (int)((n + 31) >> 5); w += NT) sw[w] = sign_word((uint64_t)w << 5, lid, key);
-  __syncthreads();
+  // element e = threadIdx.x + i NT of every column group takes input b = e >> lgcg: the thread's inputs
+  // are the same in every group, so they are loaded once (all loads issued before the first use)
   const void *x = g.x[slot];
   const int64_t xo = (b_begin + v) * n;
+  float xr[MAXE];
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int e = threadIdx.x + i * NT, b = e >> lgcg;
+    xr[i] = (e < tot && b < n) ? load_x(x, dtype, xo + b) : 0.f;
+  }
+  __syncthreads();  // sign words and twiddle tables
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int b = (threadIdx.x + i * NT) >> lgcg;
+    if (b < n) xr[i] = flip(xr[i], (sw[b >> 5] >> (b & 31)) & 1u);
+  }
   float *y = g.y[slot] + v * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
   for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
-    for (int e = threadIdx.x; e < (L << lgcg); e += NT) {
-      const int b = e >> lgcg, cc = e & ((1 << lgcg) - 1);
-      float2 val = make_float2(0.f, 0.f);
-      if (b < n) {
-        const float xv = flip(load_x(x, dtype, xo + b), (sw[b >> 5] >> (b & 31)) & 1u);
-        val = cscale(twiddle<false>(tw, lgS, lgD, (int64_t)b * (c0 + cc)), xv);
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      const int e = threadIdx.x + i * NT;
+      if (e < tot) {
+        const int b = e >> lgcg, cc = e & ((1 << lgcg) - 1);
+        const uint32_t m = (uint32_t)b * (uint32_t)(c0 + cc);  // < N
+        const float2 w = split ? cmul(thi[m >> lgLo], tlo[m & ((1u << lgLo) - 1)]) : twiddle32<false>(tw, lgS, lgD, m);
+        buf[e] = cscale(w, xr[i]);
       }
-      buf[e] = val;
     }
     lds_fft<false, NT, MAXE>(buf, lgL, lgcg, tw, lgS);
-    for (int e = threadIdx.x; e < ((L / 2) << lgcg); e += NT) {
-      const int ee = e >> lgcg, cc = e & ((1 << lgcg) - 1);
-      const int64_t k = (c0 + cc) + ((int64_t)ee << lgcs);
+    // outputs k = c + (N / L) ee, ee < L / 2: the G pairs loaded first
+    const int tot2 = (L / 2) << lgcg;
+    float2 gv[MAXE / 2];
+#pragma unroll
+    for (int i = 0; i < MAXE / 2; ++i) {
+      const int e = threadIdx.x + i * NT;
+      const int64_t k = (c0 + (e & ((1 << lgcg) - 1))) + ((int64_t)(e >> lgcg) << lgcs);
+      if (e < tot2) gv[i] = *(const float2 *)(gl + 2 * k);
+    }
+#pragma unroll
+    for (int i = 0; i < MAXE / 2; ++i) {
+      const int e = threadIdx.x + i * NT;
+      if (e >= tot2) break;
+      const int64_t k = (c0 + (e & ((1 << lgcg) - 1))) + ((int64_t)(e >> lgcg) << lgcs);
       const float2 X = buf[e];
-      if (k == 0) {
-        y[0] = c1 * gl[0] * X.x;
-        y[1] = c1 * gl[1] * buf[(L / 2) << lgcg].x;  // X_{N/2}: c = 0, e = L/2
-      } else {
-        y[2 * k] = c2 * gl[2 * k] * X.x;
-        y[2 * k + 1] = c2 * gl[2 * k + 1] * X.y;
-      }
+      if (k == 0)
+        *(float2 *)y = make_float2(c1 * gv[i].x * X.x, c1 * gv[i].y * buf[(L / 2) << lgcg].x);  // X_{N/2}: c = 0, e = L/2
+      else
+        *(float2 *)(y + 2 * k) = make_float2(c2 * gv[i].x * X.x, c2 * gv[i].y * X.y);
     }
     __syncthreads();
   }
@@ -616,7 +648,7 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_T(const LayerDesc *__restrict
     buf[(r << lgWc) + c] = make_float2(ha.x - hb.y, ha.y + hb.x);          // H_a + i H_b
     if (!edge) buf[((P - r) << lgWc) + c] = make_float2(ha.x + hb.y, hb.x - ha.y);  // conj H_a + i conj H_b
   }
-  lds_fft<true, NT, MAXE>(buf, lgP, lgWc, tw, lgS);
+  lds_fft<true, NT, MAXE, false, true>(buf, lgP, lgWc, tw, lgS);
   void *o = (void *)g.x[slot];
   const float *th = g.th[slot];
   const int64_t oo = (b_begin + v) * n;
