@@ -56,6 +56,7 @@ constexpr int kSlots = 32;       // layers per launch
 // a copy of the table in LDS: they then issue no global loads, so the loads of
 // the next column block stay in flight across the transform.
 constexpr int kLgTwl = 10;
+constexpr int kRAcc = 2;         // residue pass: rows per thread whose sums stay in registers
 constexpr int kLgTwSplit = 9;    // two-level twiddle tables of the one-kernel layers: 2 x 512 entries
 constexpr int kLgRows = 13;      // forward pass 1: transform buffer of 2^kLgRows values, 2^(kLgRows-4) threads
 
@@ -336,6 +337,30 @@ __global__ __launch_bounds__(1 << LGNT, 4) void k_ffq_fwd(const LayerDesc *__res
       }
     }
   };
+  // this thread's part of row j over the block's columns q = q0 + gi + G m, k = r + P j: set A adds
+  // w_N^{q k} W_q[j], set B adds conj(W_q[j]) w_N^{q (M - k)} (= conj(w_N^{q k} W_q[j]) w_Q^q); both
+  // twiddles by recurrence over m (at most 16 steps) from values computed directly
+  auto row_sums = [&](int j, int64_t q0, float2 &a, float2 &b, float2 &nn) {
+    a = b = nn = make_float2(0.f, 0.f);
+    const int64_t k = r + ((int64_t)j << lgP), nmask = (1ll << lgN) - 1;
+    float2 wa = cis_neg(((q0 + gi) * k) & nmask, lgN);
+    const float2 was = cis_neg(((int64_t)G * k) & nmask, lgN);
+    float2 wb = cis_neg(((q0 + gi) * (((int64_t)1 << lgM) - k)) & nmask, lgN);
+    const float2 wbs = cis_neg(((int64_t)G * (((int64_t)1 << lgM) - k)) & nmask, lgN);
+    for (int qq = gi; qq < Qb; qq += G) {
+      const float2 w = buf[(j << lgQb) + qq];
+      a = cadd(a, cmul(w, wa));
+      if (pair) b = cadd(b, cmul(cconj(w), wb));
+      if (r == 0 && j == 0) nn = ((q0 + qq) & 1) ? csub(nn, w) : cadd(nn, w);
+      wa = cmul(wa, was);
+      if (pair) wb = cmul(wb, wbs);
+    }
+  };
+  // rows per thread <= kRAcc: the sums stay in registers across the column blocks and are written once
+  const bool racc = rpt <= kRAcc;
+  float2 acc_a[kRAcc], acc_b[kRAcc], acc_n = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < kRAcc; ++i) acc_a[i] = acc_b[i] = make_float2(0.f, 0.f);
   load_block(0);
   for (int qb = 0; qb < nqb; ++qb) {
     const int64_t q0 = (int64_t)qb << lgQb;
@@ -354,46 +379,48 @@ __global__ __launch_bounds__(1 << LGNT, 4) void k_ffq_fwd(const LayerDesc *__res
       lds_fft<false, NT, MAXE, true, true>(buf, lgJ, lgQb, twl, lgJ);
     else
       lds_fft<false, NT, MAXE, true, true>(buf, lgJ, lgQb, tw, lgS);
-    for (int i = 0; i < rpt; ++i) {
-      const int j = j0 + (i << (LGNT - lgG));
-      float2 a = make_float2(0.f, 0.f), b = a, nn = a;
-      // q = q0 + gi + G m, k = r + P j: set A adds w_N^{q k} W_q[j], set B adds
-      // conj(W_q[j]) w_N^{q (M - k)} (= conj(w_N^{q k} W_q[j]) w_Q^q); both twiddles
-      // by recurrence over m (at most 16 steps) from values computed directly
-      const int64_t k = r + ((int64_t)j << lgP), nmask = (1ll << lgN) - 1;
-      float2 wa = cis_neg(((q0 + gi) * k) & nmask, lgN);
-      const float2 was = cis_neg(((int64_t)G * k) & nmask, lgN);
-      float2 wb = cis_neg(((q0 + gi) * (((int64_t)1 << lgM) - k)) & nmask, lgN);
-      const float2 wbs = cis_neg(((int64_t)G * (((int64_t)1 << lgM) - k)) & nmask, lgN);
-      for (int qq = gi; qq < Qb; qq += G) {
-        const float2 w = buf[(j << lgQb) + qq];
-        a = cadd(a, cmul(w, wa));
-        if (pair) b = cadd(b, cmul(cconj(w), wb));
-        if (r == 0 && j == 0) nn = ((q0 + qq) & 1) ? csub(nn, w) : cadd(nn, w);
-        wa = cmul(wa, was);
-        if (pair) wb = cmul(wb, wbs);
-      }
-      if (G == 1) {
-        emit(j, a, b, nn, qb > 0);
-      } else {
-        // combine the G partial sums of this row in a fixed order
-        __syncthreads();
-        buf[threadIdx.x] = a;
-        buf[NT + threadIdx.x] = b;
-        buf[2 * NT + threadIdx.x] = nn;
-        __syncthreads();
-        if ((int)threadIdx.x < J) {
-          float2 sa = make_float2(0.f, 0.f), sb = sa, sn2 = sa;
-          for (int k = 0; k < G; ++k) {
-            sa = cadd(sa, buf[(threadIdx.x << lgG) + k]);
-            sb = cadd(sb, buf[NT + (threadIdx.x << lgG) + k]);
-            sn2 = cadd(sn2, buf[2 * NT + (threadIdx.x << lgG) + k]);
-          }
-          emit((int)threadIdx.x, sa, sb, sn2, qb > 0);
+    if (racc) {
+#pragma unroll
+      for (int i = 0; i < kRAcc; ++i) {
+        if (i < rpt) {
+          float2 a, b, nn;
+          row_sums(j0 + (i << (LGNT - lgG)), q0, a, b, nn);
+          acc_a[i] = cadd(acc_a[i], a);
+          acc_b[i] = cadd(acc_b[i], b);
+          acc_n = cadd(acc_n, nn);
         }
+      }
+    } else {
+      for (int i = 0; i < rpt; ++i) {  // here G = 1
+        const int j = j0 + (i << (LGNT - lgG));
+        float2 a, b, nn;
+        row_sums(j, q0, a, b, nn);
+        emit(j, a, b, nn, qb > 0);
       }
     }
     __syncthreads();
+  }
+  if (racc) {
+    if (G == 1) {
+#pragma unroll
+      for (int i = 0; i < kRAcc; ++i)
+        if (i < rpt) emit(j0 + (i << (LGNT - lgG)), acc_a[i], acc_b[i], acc_n, false);
+    } else {
+      // combine the G partial sums of each row in a fixed order
+      buf[threadIdx.x] = acc_a[0];
+      buf[NT + threadIdx.x] = acc_b[0];
+      buf[2 * NT + threadIdx.x] = acc_n;
+      __syncthreads();
+      if ((int)threadIdx.x < J) {
+        float2 sa = make_float2(0.f, 0.f), sb = sa, sn2 = sa;
+        for (int k = 0; k < G; ++k) {
+          sa = cadd(sa, buf[(threadIdx.x << lgG) + k]);
+          sb = cadd(sb, buf[NT + (threadIdx.x << lgG) + k]);
+          sn2 = cadd(sn2, buf[2 * NT + (threadIdx.x << lgG) + k]);
+        }
+        emit((int)threadIdx.x, sa, sb, sn2, false);
+      }
+    }
   }
 }
 
