@@ -131,14 +131,24 @@ __device__ __forceinline__ float2 cis_neg(int64_t m, int lgL) {
 
 // Sign words of rows t < rows, columns [b0, b0 + 2^lgW) of the P x R view
 // into sw[t * nw + w] (nw = W / 32; W >= 128).
+// One Philox block holds the sign words of 128 consecutive coordinates: each
+// block is generated once and its words of [b0, b0 + W) are written (row
+// starts t R are multiples of 128, b0 a multiple of W >= 32).
 template <int NT>
 __device__ __forceinline__ void build_row_signs(uint32_t *sw, int64_t rows, int lgR, int64_t b0, int lgW,
                                                 uint32_t layer, Key key) {
-  const int lgnw = lgW - 5;
-  for (int64_t e = threadIdx.x; e < (rows << lgnw); e += NT) {
-    const int64_t t = e >> lgnw, w = e & ((1 << lgnw) - 1);
-    const int64_t j = (t << lgR) + b0 + (w << 5);
-    sw[e] = sign_word((uint64_t)j, layer, key);
+  const int nw = 1 << (lgW - 5);
+  const int w0 = (int)((b0 >> 5) & 3);                   // word of b0 in its block
+  const int nblk = (w0 + nw + 3) >> 2;                   // blocks per row
+  for (int64_t e = threadIdx.x; e < rows * nblk; e += NT) {
+    const int64_t t = e / nblk;
+    const int bk = (int)(e - t * nblk);
+    const W4 q = philox((uint64_t)(((t << lgR) + b0) >> 7) + bk, layer, ST_SIGN, key);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int w = 4 * bk + k - w0;  // word index within the row piece
+      if (w >= 0 && w < nw) sw[t * nw + w] = q.w[k];
+    }
   }
 }
 
