@@ -220,16 +220,17 @@ def cpu_baseline(cfg: str):
         nbytes = reps * 2 * len(c["kinds"]) * c["batch"] * shapes[0][1] * 4
         sample = f"all {c['batch']} rows, FJL+FFD forward and transpose, {reps} passes"
     elif cfg in ("c2", "c10"):
-        # the first two transformer blocks (24 tensors, 14.2M parameters), every row of the batch
-        sub, nrows = shapes[2:26], c["batch"]
+        # every row of the batch over the first transformer blocks: three for the C oracle (36 tensors,
+        # 21.3M parameters), two for the numpy one (24 tensors, 14.2M)
+        sub, nrows = (shapes[2:38] if cfg == "c2" else shapes[2:26]), c["batch"]
         xs = rows_for(sub, nrows)
         t0 = time.perf_counter()
         for k in c["kinds"]:
             O.apply(k, sub, D, seed, xs, layer0=2, nthreads=cores)
         nbytes = len(c["kinds"]) * nrows * sum(r * cc for r, cc in sub) * 4
         names = "+".join(k.upper() for k in c["kinds"])
-        sample = f"{nrows} of {c['batch']} rows, the first two transformer blocks ({len(sub)} of {len(shapes)} " \
-                 f"tensors), {names}"
+        sample = f"{nrows} of {c['batch']} rows, the first {len(sub) // 12} transformer blocks ({len(sub)} of " \
+                 f"{len(shapes)} tensors), {names}"
     elif cfg == "c3":
         sub = shapes[1:7]  # one decoder layer: q, k, v, o, fc1, fc2
         bf = [W.bf16_bits(x) for x in rows_for(sub, 1)]
