@@ -112,8 +112,8 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
         b = ld.np * 4;
         break;
       case SK_FFD:
-        if (ilog2(s->D) <= kFfdSmallMax)
-          b = transpose ? 0 : ffd_small_groups(s, l) * s->D * 4;
+        if (ilog2(s->D) <= kFfdSmallMax)  // partial sums (forward), then the call's block tables
+          b = ((transpose ? 0 : ffd_small_groups(s, l) * s->D) + ffd_small_table_floats(s, l)) * 4;
         else
           b = 2 * ffd_live_blocks(s, l) * s->D * 4;
         break;
@@ -868,8 +868,10 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
         for (int l = l0; l < l1; ++l) {
           if (lgD <= kFfdSmallMax) {
             const int64_t groups = ffd_small_groups(s, l);
+            float *tab = s->ws + bc * groups * s->D;  // after the partial sums
+            SK_PROF(SK_PROF_PROLOG, 0, launch_ffd_tables(s, l, tab, st));
             SK_PROF(SK_PROF_FFD, bc * s->layers[l].n * esz,
-                    launch_ffd_small_fwd(s, l, grads[l - l0], dtype, b0, bc, s->ws, 0, groups, st));
+                    launch_ffd_small_fwd(s, l, grads[l - l0], dtype, b0, bc, s->ws, 0, groups, tab, st));
             SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
                     launch_reduce_partials(s->ws, groups, bc, s->D, b0, out, accumulate || l > l0, st));
           } else if (ffd_large_path(s)) {
@@ -1047,8 +1049,9 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
         }
         case SK_FFD:
           if (lgD <= kFfdSmallMax) {
+            SK_PROF(SK_PROF_PROLOG, 0, launch_ffd_tables(s, l, s->ws, st));
             SK_PROF(SK_PROF_FFD_T, obytes + bc * s->D * 4,
-                    launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, st));
+                    launch_ffd_small_T(s, l, z, b0, bc, o, out_dtype, th, s->ws, st));
           } else if (ffd_large_path(s)) {
             SK_PROF(SK_PROF_FFD, 0, run_ffd_large_T(s, l, z, b0, bc, o, out_dtype, th, 1, st));
             SK_PROF(SK_PROF_GATHER, obytes + bc * s->D * 4, run_ffd_large_T(s, l, z, b0, bc, o, out_dtype, th, 2, st));

@@ -1370,146 +1370,205 @@ int64_t ffd_live_blocks(const sk_sketch *s, int layer) {
   return (ld.n + s->D - 1) / s->D;
 }
 
-constexpr int kFfdGroup = 1;  // blocks per workgroup (small D)
+// Partial sums of the small-D forward: one per live block (and vector).
+int64_t ffd_small_groups(const sk_sketch *s, int layer) { return ffd_live_blocks(s, layer); }
 
-int64_t ffd_small_groups(const sk_sketch *s, int layer) {
-  return (ffd_live_blocks(s, layer) + kFfdGroup - 1) / kFfdGroup;
+// The random ingredients of the live blocks of a layer (D <= 2^13), made once
+// per call by k_ffd_tables into the workspace and read by the block kernels:
+// g_b (nlive x D floats), Pi_b (nlive x D 16-bit entries) and the sign bits of
+// the block's coordinates (nlive rows of ffd_tab_words(D) words, bit i % 32 of
+// word i / 32 for coordinate b D + i).  Nothing is kept between calls.
+__host__ __device__ inline int ffd_tab_words(int D) { return D >= 32 ? D / 32 : 1; }
+
+int64_t ffd_small_table_floats(const sk_sketch *s, int layer) {
+  const int64_t D = s->D, nl = ffd_live_blocks(s, layer);
+  return ((nl * D + nl * D / 2 + nl * ffd_tab_words((int)D)) + 63) & ~63ll;
 }
 
-// The random ingredients of block b of the layer, built once per workgroup into
-// LDS and shared by its tile of vectors: Pi_b as a table (16-bit entries,
-// D <= 2^13), g_b, and the sign words of the block's coordinates.
-__device__ __forceinline__ void ffd_block_tables(const LayerDesc &ld, int64_t b, int lgD, Key key, uint16_t *tperm,
-                                                 float *tg, uint32_t *tsgn) {
+struct FfdTab {
+  const float *g;
+  const uint16_t *perm;
+  const uint32_t *sgn;
+};
+
+__host__ __device__ inline FfdTab ffd_tab(const float *tab, int64_t nlive, int D) {
+  FfdTab t;
+  t.g = tab;
+  t.perm = reinterpret_cast<const uint16_t *>(tab + nlive * D);
+  t.sgn = reinterpret_cast<const uint32_t *>(tab + nlive * D + nlive * D / 2);
+  return t;
+}
+
+// One thread per 4 consecutive coordinates i4 .. i4 + 3 of block b = blockIdx.y
+// (one Philox block of Gaussians, four permutation entries; the first thread
+// of a 32-coordinate run also its sign word); the block's permutation key is
+// made once per workgroup.
+__global__ __launch_bounds__(256) void k_ffd_tables(const LayerDesc *__restrict__ layers, int layer, int lgD,
+                                                    int64_t nlive, float *__restrict__ tab, Key key) {
+  __shared__ PermKey s_pk;
+  const LayerDesc &ld = layers[layer];
   const int D = 1 << lgD;
+  const int64_t b = blockIdx.y;
+  if (threadIdx.x == 0) s_pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
+  __syncthreads();
+  const int i4 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i4 >= D) return;
+  float *g = tab + b * D;
+  uint16_t *perm = reinterpret_cast<uint16_t *>(tab + nlive * D) + b * D;
+  uint32_t *sgn = reinterpret_cast<uint32_t *>(tab + nlive * D + nlive * D / 2) + b * ffd_tab_words(D);
   const int64_t base = b * D;
-  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)lgD, key);
-  for (int i = threadIdx.x; i < D; i += 256) tperm[i] = (uint16_t)perm_fwd(pk, (uint32_t)i);
-  for (int i4 = threadIdx.x * 4; i4 < D; i4 += 1024) {
-    float g[4];
-    gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+  float gv[4];
+  gauss4((uint64_t)(base + i4) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, gv);
+  *reinterpret_cast<float4 *>(g + i4) = make_float4(gv[0], gv[1], gv[2], gv[3]);
+  const PermKey pk = s_pk;
+  uint32_t pp[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (i4 + q < D) tg[i4 + q] = g[q];
+  for (int q = 0; q < 4; ++q) pp[q] = perm_fwd(pk, (uint32_t)(i4 + q));
+  *reinterpret_cast<uint2 *>(perm + i4) = make_uint2(pp[0] | (pp[1] << 16), pp[2] | (pp[3] << 16));
+  if ((i4 & 31) == 0) {
+    // bits of coordinates base + i4 .. + 31 (or the D = 16 coordinates of a block that
+    // starts half-way through a global 32-coordinate word)
+    const int64_t j = base + i4;
+    const int sh = (int)(j & 31);
+    uint32_t w = sign_word((uint64_t)j, (uint32_t)ld.layer_id, key) >> sh;
+    if (sh) w |= sign_word((uint64_t)(j + 32), (uint32_t)ld.layer_id, key) << (32 - sh);
+    sgn[i4 >> 5] = w;
   }
-  // sign words of the global 32-coordinate runs the block touches (blocks of D < 128 need not
-  // start on a Philox block): word w covers coordinates 32 ((base >> 5) + w) ..
-  const int nw = (int)(((base + D - 1) >> 5) - (base >> 5)) + 1;
-  for (int w = threadIdx.x; w < nw; w += 256) tsgn[w] = sign_word((uint64_t)(((base >> 5) + w) << 5), (uint32_t)ld.layer_id, key);
 }
 
-// Sign bit of coordinate i of the block starting at base, from ffd_block_tables' words.
-__device__ __forceinline__ uint32_t ffd_sign_bit(const uint32_t *tsgn, int64_t base, int i) {
-  const int64_t j = base + i;
-  return (tsgn[(j >> 5) - (base >> 5)] >> (j & 31)) & 1u;
+void launch_ffd_tables(const sk_sketch *s, int layer, float *tab, hipStream_t st) {
+  const int lgD = log2_exact(s->D);
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  const dim3 grid((unsigned)((s->D / 4 + 255) / 256), (unsigned)nlive);
+  hipLaunchKernelGGL(k_ffd_tables, grid, dim3(256), 0, st, s->d_layers, layer, lgD, nlive, tab, s->key);
+  SK_CHECK_LAUNCH();
 }
 
-// Forward, D <= 2^13: a workgroup takes kFfdGroup blocks and VT vectors; per
-// block the tables are built once, then for each vector: load, H_D, scatter
-// through Pi_b with g, H_D, signs, accumulated over the group's blocks in
-// registers (PER = D / 256 values per thread and vector).
+// Thread t's share of block b's tables: coordinates i = t + 256 k (k < PER;
+// with PER = 1 only t < D).  pv[k] = p16(Pi_b(i)), the LDS place of the
+// permuted coordinate.
+template <int PER>
+__device__ __forceinline__ void ffd_load_tab(const FfdTab &tb, int64_t b, int D, float (&gv)[PER], int (&pv)[PER],
+                                             uint32_t &sb) {
+  // row bases are uniform; per-thread offsets are 32-bit
+  const float *g = tb.g + b * D;
+  const uint16_t *pm = tb.perm + b * D;
+  const uint32_t *sw = tb.sgn + b * ffd_tab_words(D);
+  sb = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const uint32_t i = threadIdx.x + k * 256;
+    gv[k] = 0.0f;
+    pv[k] = 0;
+    if (PER > 1 || i < (uint32_t)D) {
+      gv[k] = g[i];
+      pv[k] = p16(pm[i]);
+      sb |= ((sw[i >> 5] >> (i & 31)) & 1u) << k;
+    }
+  }
+}
+
+// LDS place of coordinate t + 256 k in the p16 layout: p16(t) + 272 k.
+__device__ __forceinline__ int ffd_p16_base() {
+  const int t = threadIdx.x;
+  return p16(t);
+}
+
+// Forward, D <= 2^13: a workgroup takes one block and VT vectors; per vector:
+// load, H_D, scatter through Pi_b with g, H_D, signs, kept in registers
+// (PER = D / 256 values per thread and vector) and written as the block's
+// partial sum.  One LDS tile (the scatter goes through registers), so that
+// several workgroups share a compute unit.
 template <bool BF16, int VT, int PER>
 __global__ __launch_bounds__(256) void k_ffd_small_fwd(const LayerDesc *__restrict__ layers, int layer,
                                                        const void *__restrict__ x, int lgD, int64_t b_begin,
                                                        int64_t bc, float *__restrict__ part, int64_t slot0,
-                                                       int64_t nlive, Key key) {
+                                                       int64_t nlive, const float *__restrict__ tab) {
   extern __shared__ float sm[];
   const int D = 1 << lgD;
-  float *s = sm;                  // p16 layout
-  float *u = sm + p16_floats(D);  // p16 layout
-  float *tg = sm + 2 * p16_floats(D);
-  uint32_t *tsgn = reinterpret_cast<uint32_t *>(tg + D);
-  uint16_t *tperm = reinterpret_cast<uint16_t *>(tsgn + (D + 31) / 32 + 4);
+  float *s = sm;  // p16 layout
   const LayerDesc &ld = layers[layer];
   const int64_t v0 = (int64_t)blockIdx.y * VT;
-  const int64_t blk0 = (int64_t)blockIdx.x * kFfdGroup;
+  const int64_t b = blockIdx.x;
+  const int64_t base = b * D;
+  const bool act = PER > 1 || (int)threadIdx.x < D;  // PER = 1: threads past D hold nothing
+  float gv[PER];
+  int pv[PER];
+  uint32_t sb;
+  ffd_load_tab<PER>(ffd_tab(tab, nlive, D), b, D, gv, pv, sb);
+  // coordinates of this block present in the vector (only the last block may be cut)
+  const int lim = ld.n - base < D ? (int)(ld.n - base) : D;
+  float xr[PER];
+  auto load_x = [&](int64_t vv) {
+    const int64_t row = (b_begin + vv) * ld.n + base;
+    const uint16_t *xh = (const uint16_t *)x + row;
+    const float *xf = (const float *)x + row;
+    const bool full = lim == D && vv < bc;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const uint32_t i = threadIdx.x + k * 256;
+      float val = 0.0f;
+      if (full ? act : ((int)i < lim && vv < bc)) val = BF16 ? bf16_to_f32(xh[i]) : xf[i];
+      xr[k] = val;
+    }
+  };
+  load_x(v0);
+  const float inv = 1.0f / (float)D;
   float acc[VT][PER];
 #pragma unroll
-  for (int v = 0; v < VT; ++v)
+  for (int v = 0; v < VT; ++v) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) acc[v][k] = 0.0f;
-  const float inv = 1.0f / (float)D;
-  for (int64_t b = blk0; b < blk0 + kFfdGroup && b < nlive; ++b) {
-    const int64_t base = b * D;
-    __syncthreads();  // the previous block's readers of the tables are done
-    ffd_block_tables(ld, b, lgD, key, tperm, tg, tsgn);
+    if (v0 + v >= bc) break;
+    if (v > 0) __syncthreads();  // the previous vector's last reads of s are done
+    float *sp = s + ffd_p16_base();
+    if (act) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) sp[272 * k] = xr[k];
+    }
+    if (v + 1 < VT) load_x(v0 + v + 1);
+    lds_fwht_regs(s, lgD, 0);
+    float t[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) t[k] = act ? sp[272 * k] : 0.0f;
     __syncthreads();
-    // the next vector's coordinates are loaded into registers while the current one is transformed
-    // (PER independent loads in flight instead of one dependent load per loop trip)
-    float xr[PER];
-    auto load_x = [&](int64_t vv) {
+    if (act) {
 #pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int i = threadIdx.x + k * 256;
-        const int64_t j = base + i;
-        float val = 0.0f;
-        if (i < D && j < ld.n && vv < bc) {
-          const int64_t e = (b_begin + vv) * ld.n + j;
-          val = BF16 ? bf16_to_f32(((const uint16_t *)x)[e]) : ((const float *)x)[e];
-        }
-        xr[k] = val;
-      }
-    };
-    load_x(v0);
+      for (int k = 0; k < PER; ++k) s[pv[k]] = gv[k] * t[k];
+    }
+    lds_fwht_regs(s, lgD, 0);
+    if (act) {
 #pragma unroll
-    for (int v = 0; v < VT; ++v) {
-      if (v0 + v >= bc) break;
-#pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int i = threadIdx.x + k * 256;
-        if (i < D) s[p16(i)] = xr[k];
-      }
-      if (v + 1 < VT) load_x(v0 + v + 1);
-      lds_fwht_regs(s, lgD, 0);
-      for (int i = threadIdx.x; i < D; i += 256) u[p16(tperm[i])] = tg[i] * s[p16(i)];
-      lds_fwht_regs(u, lgD, 0);
-#pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int i = threadIdx.x + k * 256;
-        if (i < D) acc[v][k] += flip(u[p16(i)] * inv, ffd_sign_bit(tsgn, base, i));
-      }
+      for (int k = 0; k < PER; ++k) acc[v][k] = flip(sp[272 * k] * inv, (sb >> k) & 1u);
     }
   }
+  if (!act) return;
 #pragma unroll
   for (int v = 0; v < VT; ++v) {
     if (v0 + v >= bc) break;
-    float *dst = part + ((slot0 + blockIdx.x) * bc + v0 + v) * D;
+    float *dst = part + ((slot0 + b) * bc + v0 + v) * D;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = threadIdx.x + k * 256;
-      if (i < D) dst[i] = acc[v][k];
-    }
+    for (int k = 0; k < PER; ++k) dst[threadIdx.x + k * 256] = acc[v][k];
   }
 }
 
-// LDS of the small-D FFD kernels: s, u (p16 layout), g (D floats), sign words, Pi (16-bit).
-static size_t ffd_small_shm(int64_t D) {
-  return (size_t)(2 * p16_floats((int)D) + D) * 4 + ((D + 31) / 32 + 4) * 4 + (size_t)D * 2 + 16;
-}
-
-// Dynamic LDS above 64 KB (D = 2^13: 116 KB of the 160 KB a gfx950 workgroup may use) is
-// requested explicitly.
-static void ffd_allow_shm(const void *fn, size_t shm) {
-  if (shm > 65536) (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-}
+// LDS of the small-D FFD kernels: one p16 tile of D floats (36 KB at D = 2^13).
+static size_t ffd_small_shm(int64_t D) { return (size_t)p16_floats((int)D) * 4; }
 
 template <int VT>
 static void ffd_small_fwd_go(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                             float *part, int64_t slot0, int64_t groups, int lgD, hipStream_t st) {
+                             float *part, int64_t slot0, int64_t groups, int lgD, const float *tab, hipStream_t st) {
   const dim3 grid((unsigned)groups, (unsigned)((bc + VT - 1) / VT));
   const size_t shm = ffd_small_shm(s->D);
   const int64_t nlive = ffd_live_blocks(s, layer);
 #define SK_FFDS(PER)                                                                                             \
   do {                                                                                                           \
-    if (dtype == SK_BF16) {                                                                                      \
-      ffd_allow_shm((const void *)k_ffd_small_fwd<true, VT, PER>, shm);                                          \
+    if (dtype == SK_BF16)                                                                                        \
       hipLaunchKernelGGL((k_ffd_small_fwd<true, VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, x, lgD, \
-                         b_begin, bc, part, slot0, nlive, s->key);                                                \
-    } else {                                                                                                     \
-      ffd_allow_shm((const void *)k_ffd_small_fwd<false, VT, PER>, shm);                                         \
+                         b_begin, bc, part, slot0, nlive, tab);                                                   \
+    else                                                                                                         \
       hipLaunchKernelGGL((k_ffd_small_fwd<false, VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, x,     \
-                         lgD, b_begin, bc, part, slot0, nlive, s->key);                                           \
-    }                                                                                                            \
+                         lgD, b_begin, bc, part, slot0, nlive, tab);                                              \
   } while (0)
   switch (lgD <= 8 ? 1 : 1 << (lgD - 8)) {
     case 1: SK_FFDS(1); break;
@@ -1522,13 +1581,18 @@ static void ffd_small_fwd_go(const sk_sketch *s, int layer, const void *x, int d
 #undef SK_FFDS
 }
 
+// Vectors per workgroup of the small-D kernels (2^20-entry vectors, batch 8,
+// D = 4096, per call, forward / transpose: 1 vector 29 / 30 us, 2 31 / 35,
+// 4 36 / 35; the kernels that made their tables in LDS per workgroup took
+// 56 / 56 at their best, 4 vectors)
+constexpr int kFfdVtFwd = 1;
+constexpr int kFfdVtT = 1;
+
 void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                          float *part, int64_t slot0, int64_t groups, hipStream_t st) {
+                          float *part, int64_t slot0, int64_t groups, const float *tab, hipStream_t st) {
   const int lgD = log2_exact(s->D);
   if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
-  // one block and 4 vectors per workgroup (2^20-entry vectors, batch 8, D = 4096, forward per call:
-  // 2 blocks x 2 vectors 64.3 us, 2 x 4 81.8, 1 x 2 63.6, 1 x 4 57.5, 1 x 8 82.0)
-  ffd_small_fwd_go<4>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, st);
+  ffd_small_fwd_go<kFfdVtFwd>(s, layer, x, dtype, b_begin, bc, part, slot0, groups, lgD, tab, st);
   SK_CHECK_LAUNCH();
 }
 
@@ -1604,69 +1668,100 @@ void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64
   SK_CHECK_LAUNCH();
 }
 
-// Transpose, D <= 2^13: a workgroup takes one block and VT vectors; the
-// block's tables are built once, then per vector: signs, H_D, gather through
-// Pi_b with g, H_D, theta0, store.
+// Transpose, D <= 2^13: a workgroup takes one block and VT vectors; per
+// vector: signs, H_D, gather through Pi_b with g, H_D, theta0, store.  One
+// LDS tile, as in the forward.
 template <int VT, int PER>
 __global__ __launch_bounds__(256) void k_ffd_small_T(const LayerDesc *__restrict__ layers, int layer,
                                                      const float *__restrict__ z, int lgD, int64_t b_begin,
                                                      int64_t bc, void *__restrict__ out, int out_dtype,
-                                                     const float *__restrict__ theta0, Key key) {
+                                                     const float *__restrict__ theta0, int64_t nlive,
+                                                     const float *__restrict__ tab) {
   extern __shared__ float sm[];
   const int D = 1 << lgD;
-  float *s = sm;                  // p16 layout
-  float *u = sm + p16_floats(D);  // p16 layout
-  float *tg = sm + 2 * p16_floats(D);
-  uint32_t *tsgn = reinterpret_cast<uint32_t *>(tg + D);
-  uint16_t *tperm = reinterpret_cast<uint16_t *>(tsgn + (D + 31) / 32 + 4);
+  float *s = sm;  // p16 layout
   const LayerDesc &ld = layers[layer];
   const int64_t b = blockIdx.x;
   const int64_t v0 = (int64_t)blockIdx.y * VT;
   const int64_t base = b * D;
-  ffd_block_tables(ld, b, lgD, key, tperm, tg, tsgn);
-  __syncthreads();
+  const bool act = PER > 1 || (int)threadIdx.x < D;
+  float gv[PER];
+  int pv[PER];
+  uint32_t sb;
+  ffd_load_tab<PER>(ffd_tab(tab, nlive, D), b, D, gv, pv, sb);
+  const int lim = ld.n - base < D ? (int)(ld.n - base) : D;
   const float inv = 1.0f / (float)D;
   float zr[PER];
   auto load_z = [&](int64_t vv) {
+    const float *zv = z + (b_begin + vv) * D;
+    const bool ok = act && vv < bc;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = threadIdx.x + k * 256;
-      zr[k] = (i < D && vv < bc) ? z[(b_begin + vv) * D + i] : 0.0f;
-    }
+    for (int k = 0; k < PER; ++k) zr[k] = ok ? zv[threadIdx.x + k * 256] : 0.0f;
   };
   load_z(v0);
+#pragma unroll 1
   for (int v = 0; v < VT; ++v) {
     if (v0 + v >= bc) break;
+    if (v > 0) __syncthreads();  // the previous vector's last reads of s are done
+    float *sp = s + ffd_p16_base();
+    if (act) {
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = threadIdx.x + k * 256;
-      if (i < D) s[p16(i)] = flip(zr[k], ffd_sign_bit(tsgn, base, i));
+      for (int k = 0; k < PER; ++k) sp[272 * k] = flip(zr[k], (sb >> k) & 1u);
     }
     if (v + 1 < VT) load_z(v0 + v + 1);
     lds_fwht_regs(s, lgD, 0);
-    for (int i = threadIdx.x; i < D; i += 256) u[p16(i)] = tg[i] * s[p16(tperm[i])];
-    lds_fwht_regs(u, lgD, 0);
-    for (int i = threadIdx.x; i < D; i += 256) {
-      const int64_t j = base + i;
-      if (j < ld.n)
-        store_out(out, out_dtype, (b_begin + v0 + v) * ld.n + j, u[p16(i)] * inv + (theta0 ? theta0[j] : 0.0f));
+    float t[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) t[k] = act ? s[pv[k]] : 0.0f;
+    __syncthreads();
+    if (act) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) sp[272 * k] = gv[k] * t[k];
+    }
+    lds_fwht_regs(s, lgD, 0);
+    if (!act) continue;
+    const int64_t row = (b_begin + v0 + v) * ld.n + base;
+    uint16_t *oh = (uint16_t *)out + row;
+    float *of = (float *)out + row;
+    const float *th = theta0 ? theta0 + base : nullptr;
+    const bool full = lim == D;
+    float r[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) r[k] = sp[272 * k] * inv;
+    if (th) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const uint32_t i = threadIdx.x + k * 256;
+        if (full || (int)i < lim) r[k] += th[i];
+      }
+    }
+    if (out_dtype == SK_BF16) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const uint32_t i = threadIdx.x + k * 256;
+        if (full || (int)i < lim) oh[i] = f32_to_bf16(r[k]);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const uint32_t i = threadIdx.x + k * 256;
+        if (full || (int)i < lim) of[i] = r[k];
+      }
     }
   }
 }
 
 void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
-                        int out_dtype, const float *theta0, hipStream_t st) {
+                        int out_dtype, const float *theta0, const float *tab, hipStream_t st) {
   const int lgD = log2_exact(s->D);
   if (lgD < 4 || lgD > kFfdSmallMax) return;  // the small-D path: 2^4 <= D <= 2^13
-  constexpr int VT = 4;  // vectors per workgroup (same workload, per call: 2 -> 58.4 us, 4 -> 51.2, 8 -> 73.4)
-  const dim3 grid((unsigned)ffd_live_blocks(s, layer), (unsigned)((bc + VT - 1) / VT));
+  constexpr int VT = kFfdVtT;
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  const dim3 grid((unsigned)nlive, (unsigned)((bc + VT - 1) / VT));
   const size_t shm = ffd_small_shm(s->D);
 #define SK_FFDT(PER)                                                                                              \
-  do {                                                                                                            \
-    ffd_allow_shm((const void *)k_ffd_small_T<VT, PER>, shm);                                                     \
-    hipLaunchKernelGGL((k_ffd_small_T<VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, z, lgD, b_begin, bc, \
-                       out, out_dtype, theta0, s->key);                                                           \
-  } while (0)
+  hipLaunchKernelGGL((k_ffd_small_T<VT, PER>), grid, dim3(256), shm, st, s->d_layers, layer, z, lgD, b_begin, bc, \
+                     out, out_dtype, theta0, nlive, tab)
   switch (lgD <= 8 ? 1 : 1 << (lgD - 8)) {
     case 1: SK_FFDT(1); break;
     case 2: SK_FFDT(2); break;

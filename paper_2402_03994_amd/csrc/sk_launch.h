@@ -182,13 +182,18 @@ void launch_signed_out(const sk_sketch *s, int layer, const float *w, int64_t b_
 
 // ---- FFD ----
 int64_t ffd_live_blocks(const sk_sketch *s, int layer);
+// Small D (<= 2^13): the layer's block tables (g, Pi, signs) are made per call
+// by launch_ffd_tables into ffd_small_table_floats floats of the workspace,
+// which the block kernels then read.
+int64_t ffd_small_table_floats(const sk_sketch *s, int layer);
+void launch_ffd_tables(const sk_sketch *s, int layer, float *tab, hipStream_t st);
 void launch_ffd_small_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
-                          float *part, int64_t slot0, int64_t groups, hipStream_t st);
+                          float *part, int64_t slot0, int64_t groups, const float *tab, hipStream_t st);
 int64_t ffd_small_groups(const sk_sketch *s, int layer);
 void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64_t D, int64_t b_begin, float *out,
                             bool accumulate, hipStream_t st);
 void launch_ffd_small_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
-                        int out_dtype, const float *theta0, hipStream_t st);
+                        int out_dtype, const float *theta0, const float *tab, hipStream_t st);
 void launch_ffd_copy_blocks(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                             float *w, hipStream_t st);
 void launch_ffd_gperm_fwd(const sk_sketch *s, int layer, const float *w, int64_t bc, float *w2, hipStream_t st);
