@@ -54,7 +54,7 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine", "afjl:gather": "k_afjl_T_out",
              "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd", "afjlf:ff_small": "k_ffs_fwd",
              "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
-             "affd:gather": "k_affdT_outm"}
+             "affd:gather": "k_affdT_outm", "ffd:prolog": "k_ffd_tables"}
 # FFD with D = 2^20 (rows / cols passes): prolog = the first rows pass of the forward, gather = the last cols
 # pass of the transpose; the ffd class groups the middle passes (several kernels)
 KERNEL_OF_FFD_LARGE = {"ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
