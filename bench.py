@@ -48,13 +48,14 @@ MFMA_F32_PEAK_TFLOPS = 157.3
 
 # kernel launched by each single-kernel profile class (the rocprofv3 name)
 KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", "qk:qk_xb": "k_qk_s1",
-             "ffd:ffd": "k_ffd_small_fwd", "ffd:gather": "k_reduce_partials", "fjl:prolog": "k_fjl_pass0",
+             "ffd:ffd": "k_ffd_small_fwd", "ffd:gather": "k_reduce_partials", "fjl:prolog": "k_fjl_fwd_onepass",
              "afjlq:qh_first": "k_qh_gemm", "qkh:qh_first": "k_qh_gemm", "afjlq:qh_second": "k_qh_gemm",
              "qkh:qh_second": "k_qh_gemm", "affdq:qh_first": "k_qh_gemm", "affdq:qh_t": "k_qh_gemm",
              "hvp:hvp_dots": "k_hvp_dots", "hvp:hvp_combine": "k_hvp_combine", "afjl:gather": "k_afjl_T_out",
              "ffd:ffd_t": "k_ffd_small_T", "afjlf:ff_rows": "k_ffr_fwd", "afjlf:ff_small": "k_ffs_fwd",
              "afjlf:ff_res": "k_ffq_fwd", "affd:affd_fold": "k_affdT_topM", "afjl:afjl_tail": "k_afjl_tail",
-             "affd:gather": "k_affdT_outm", "ffd:prolog": "k_ffd_tables"}
+             "affd:gather": "k_affdT_outm", "ffd:prolog": "k_ffd_tables",
+             "fjl:fjl_t": "k_fjl_T_onepass"}
 # FFD with D = 2^20 (rows / cols passes): prolog = the first rows pass of the forward, gather = the last cols
 # pass of the transpose; the ffd class groups the middle passes (several kernels)
 KERNEL_OF_FFD_LARGE = {"ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",

@@ -280,7 +280,8 @@ enum {
   SK_PROF_FF_ROWS = 15,  /* AFJLF pass 1 over the rows (reads the gradients) */
   SK_PROF_FF_RES = 16,   /* AFJLF residue pass and the layer sum             */
   SK_PROF_FF_SMALL = 17, /* AFJLF one-kernel layers (N' = D, forward)        */
-  SK_PROF_CLASSES = 18
+  SK_PROF_FJL_T = 18,    /* FJL transpose in one pass (2^14 <= N' <= 2^21)   */
+  SK_PROF_CLASSES = 19
 };
 #define SK_PROF_ALL ((1u << SK_PROF_CLASSES) - 1u)
 int sketch_profile(sk_sketch *s, uint32_t classes);

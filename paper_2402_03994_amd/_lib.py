@@ -22,7 +22,7 @@ HVP_PROF_CLASSES = ["hvp_dots", "hvp_combine", "arnoldi_orth"]
 HVP_MAX_RANK = 32
 PROF_CLASSES = ["afjl_fold", "afjl_tail", "fwht", "prolog", "affd_fold", "gather", "ffd", "qk", "other",
                 "affd_rows", "qk_xb", "qh_first", "qh_second", "qh_t", "ffd_t", "ff_rows", "ff_res",
-                "ff_small"]
+                "ff_small", "fjl_t"]
 
 
 class IdResult(ctypes.Structure):

@@ -74,6 +74,9 @@ void free_all(sk_sketch *s) {
   f(s->d_fjl_lsmp);
   f(s->d_fjl_lpos);
   f(s->d_fjl_loff);
+  f(s->d_fjlb_off);
+  f(s->d_fjlb_ent);
+  f(s->d_fjlb_pos);
   f(s->d_qka);
   f(s->d_qkb);
   f(s->d_qkah);
@@ -410,8 +413,11 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
 
   // FJL transpose: samples grouped by position (deterministic order).
-  std::vector<uint32_t> fpos, fseg, fsmp, ftoff, flsmp, flpos, floff;
+  std::vector<uint32_t> fpos, fseg, fsmp, ftoff, flsmp, flpos, floff, fboff, fbent, fbpos;
   if (kind == SK_FJL) {
+    s->fjlb_pos_at.assign(n_layers, -1);
+    s->fjlb_off_at.assign(n_layers, -1);
+    s->fjlb_ent_at.assign(n_layers, -1);
     s->fjl_uoff.assign(n_layers + 1, 0);
     s->fjl_toff_at.assign(n_layers, 0);
     s->fjl_loff_at.assign(n_layers, 0);
@@ -465,6 +471,28 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
           flsmp[(size_t)l * D + i] = bs[i].second;
           flpos[(size_t)l * D + i] = sample_index((uint64_t)bs[i].second, (uint32_t)l, s->key, (uint64_t)ld.np);
         }
+      }
+      if (fjl_onepass_T_ok(ld.lgnp, D)) {
+        // cell (p_h, p_c) = (p >> 13, low B = 26 - lgnp bits) of the one-pass transpose's tile; entries of a
+        // cell by id, each (id << 8) | the H = lgnp - 13 middle bits
+        const int Hb = ld.lgnp - 13, Bb = 13 - Hb;
+        std::vector<std::pair<uint32_t, uint32_t>> cs(D);
+        for (int64_t i = 0; i < D; ++i) {
+          const uint32_t p = sample_index((uint64_t)i, (uint32_t)l, s->key, (uint64_t)ld.np);
+          const uint32_t cell = ((p >> 13) << Bb) | (p & ((1u << Bb) - 1));
+          cs[i] = {cell, ((uint32_t)i << 8) | ((p >> Bb) & ((1u << Hb) - 1))};
+        }
+        s->fjlb_pos_at[l] = (int64_t)fbpos.size();
+        for (int64_t i = 0; i < D; ++i) fbpos.push_back((cs[i].first << 8) | (cs[i].second & 255u));
+        std::sort(cs.begin(), cs.end());
+        s->fjlb_off_at[l] = (int64_t)fboff.size();
+        s->fjlb_ent_at[l] = (int64_t)fbent.size();
+        int64_t k = 0;
+        for (uint32_t c = 0; c <= 8192; ++c) {
+          while (k < D && cs[k].first < c) ++k;
+          fboff.push_back((uint32_t)k);
+        }
+        for (int64_t i = 0; i < D; ++i) fbent.push_back(cs[i].second);
       }
     }
   }
@@ -529,6 +557,11 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(alloc((void **)&s->d_fjl_lsmp, sizeof(uint32_t) * flsmp.size()));
   SK_TRY(alloc((void **)&s->d_fjl_lpos, sizeof(uint32_t) * flpos.size()));
   SK_TRY(alloc((void **)&s->d_fjl_loff, sizeof(uint32_t) * floff.size()));
+  if (!fboff.empty()) {
+    SK_TRY(alloc((void **)&s->d_fjlb_off, sizeof(uint32_t) * fboff.size()));
+    SK_TRY(alloc((void **)&s->d_fjlb_ent, sizeof(uint32_t) * fbent.size()));
+    SK_TRY(alloc((void **)&s->d_fjlb_pos, sizeof(uint32_t) * fbpos.size()));
+  }
   SK_TRY(alloc((void **)&s->d_qka, sizeof(float) * fac_a));
   SK_TRY(alloc((void **)&s->d_qkb, sizeof(uint16_t) * 2 * fac_b));
   SK_TRY(alloc((void **)&s->d_qkah, sizeof(uint16_t) * 2 * fac_a));
@@ -552,6 +585,11 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   SK_TRY(h2d(s->d_fjl_lsmp, flsmp.data(), sizeof(uint32_t) * flsmp.size()));
   SK_TRY(h2d(s->d_fjl_lpos, flpos.data(), sizeof(uint32_t) * flpos.size()));
   SK_TRY(h2d(s->d_fjl_loff, floff.data(), sizeof(uint32_t) * floff.size()));
+  if (!fboff.empty()) {
+    SK_TRY(h2d(s->d_fjlb_off, fboff.data(), sizeof(uint32_t) * fboff.size()));
+    SK_TRY(h2d(s->d_fjlb_ent, fbent.data(), sizeof(uint32_t) * fbent.size()));
+    SK_TRY(h2d(s->d_fjlb_pos, fbpos.data(), sizeof(uint32_t) * fbpos.size()));
+  }
 
   // workspace: room for up to 256 vectors of the largest per-vector need
   const int64_t pv = std::max(per_vector_bytes(s, 0, n_layers, false), per_vector_bytes(s, 0, n_layers, true));
@@ -850,6 +888,14 @@ int sketch_apply(sk_sketch *s, const void *const *grads, sk_dtype dtype, int64_t
       case SK_FJL:
         for (int l = l0; l < l1; ++l) {
           const LayerDesc &ld = s->layers[l];
+          if (s->fjlb_pos_at[l] >= 0) {
+            // one pass into 2^(lgnp - 13) partial slots, then their sum
+            SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz,
+                    launch_fjl_fwd_onepass(s, l, grads[l - l0], dtype, b0, bc, s->ws, st));
+            SK_PROF(SK_PROF_GATHER, (l == l1 - 1 ? bc * s->D * 4 : 0),
+                    launch_reduce_partials(s->ws, 1ll << (ld.lgnp - 13), bc, s->D, b0, out, accumulate || l > l0, st));
+            continue;
+          }
           const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the signed load
           SK_PROF(SK_PROF_PROLOG, bc * ld.n * esz, launch_fjl_pass0(s, l, grads[l - l0], dtype, b0, bc, s->ws, lgw, st));
           if (ld.lgnp > 13) {
@@ -1033,6 +1079,11 @@ int sketch_apply_T(sk_sketch *s, const float *z, int64_t batch, void *const *out
           SK_PROF(SK_PROF_GATHER, obytes, launch_affd_T_out(s, l, s->ws, b0, bc, o, out_dtype, th, st));
           break;
         case SK_FJL: {
+          if (s->fjlb_off_at[l] >= 0) {
+            SK_PROF(SK_PROF_FJL_T, obytes + bc * s->D * 4,
+                    launch_fjl_T_onepass(s, l, z, b0, bc, o, out_dtype, th, st));
+            break;
+          }
           const int lgw = std::min(ld.lgnp, 13);  // fwht_inplace's first pass, fused with the scatter
           const float oscale = (float)std::sqrt((double)ld.np / (double)s->D);
           SK_PROF(SK_PROF_PROLOG, bc * s->D * 4, launch_fjl_T_pass0(s, l, z, b0, bc, s->ws, lgw, st));

@@ -1274,6 +1274,192 @@ void launch_fjl_last_signed(const sk_sketch *s, int layer, const float *w, int l
   SK_CHECK_LAUNCH();
 }
 
+// FJL transpose in one pass, 2^14 <= N' <= 2^21, D <= 2^13 (the adjoint of
+// eq. ailon_chazelle).  With N' = 2^(13 + H) a coordinate is j = (h, a, c): h
+// the top H bits, a the next H, c the low B = 13 - H (>= 5); the normalised
+// transform factors as H_N'[j, p] = H[h, p_h] H[a, p_a] H[c, p_c] / sqrt(N').
+// Workgroup (a, vector): the 2^H x 2^B tile U[p_h][p_c] = sum over samples i
+// at (p_h, p_a, p_c) of H[a, p_a] g_i z_i, its unnormalised 13-bit transform,
+// then signs, the scale 1/sqrt(D) and theta0; every output is written once.
+// The products H[a, p_a] g_i z_i are made first, all loads of a thread in
+// flight together, and staged in LDS in cell order; each cell is then summed
+// by one thread in id order (deterministic), the cell offsets loaded in one
+// batch.
+bool fjl_onepass_T_ok(int lgnp, int64_t D) { return lgnp >= 14 && lgnp <= 21 && D <= (1 << 13); }
+
+template <int R>  // entries per thread: D <= 256 R
+__global__ __launch_bounds__(256) void k_fjl_T_onepass(const LayerDesc *__restrict__ layers, int layer,
+                                                       const float *__restrict__ gtab,
+                                                       const uint32_t *__restrict__ boff,
+                                                       const uint32_t *__restrict__ bent,
+                                                       const float *__restrict__ z, int D, int64_t b_begin,
+                                                       void *__restrict__ out, int out_dtype,
+                                                       const float *__restrict__ theta0, float scale, Key key) {
+  extern __shared__ float sm[];
+  float *tile = sm;                                                        // p16 layout, 2^13 cells
+  float *ce = sm;                                                          // first: the D products, cell order
+  uint32_t *sw = reinterpret_cast<uint32_t *>(sm + p16_floats(1 << 13));  // sign words in tile order
+  const LayerDesc &ld = layers[layer];
+  const int H = ld.lgnp - 13, B = 13 - H;
+  const int a = blockIdx.x;
+  const int64_t v = blockIdx.y;
+  const float *g = gtab + (int64_t)layer * D;
+  const float *zv = z + (b_begin + v) * D;
+  // cell offsets of the thread's 32 cells k = tid + 256 m, both ends
+  uint32_t o0[32], o1[32];
+#pragma unroll
+  for (int m = 0; m < 32; ++m) {
+    o0[m] = boff[threadIdx.x + 256 * m];
+    o1[m] = boff[threadIdx.x + 256 * m + 1];
+  }
+  // products of entries e = tid + 256 r (r < R)
+  {
+    uint32_t q[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = threadIdx.x + 256 * r;
+      q[r] = e < D ? bent[e] : 0u;
+    }
+    float gz[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = threadIdx.x + 256 * r;
+      const uint32_t i = q[r] >> 8;
+      gz[r] = e < D ? g[i] * zv[i] : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = threadIdx.x + 256 * r;
+      if (e < D) ce[e] = flip(gz[r], (uint32_t)__popc((uint32_t)a & q[r] & 255u) & 1u);
+    }
+  }
+  {
+    // word w: tile cells 32 w .. 32 w + 31 = row h = w >> (B - 5), columns from 32 (w mod 2^(B - 5))
+    const int w = threadIdx.x;
+    const int64_t j = ((int64_t)(w >> (B - 5)) << 13) + ((int64_t)a << B) + ((w & ((1 << (B - 5)) - 1)) << 5);
+    sw[w] = sign_word((uint64_t)j, (uint32_t)ld.layer_id, key);
+  }
+  __syncthreads();
+  float u[32];
+#pragma unroll
+  for (int m = 0; m < 32; ++m) {
+    float acc = 0.0f;
+    for (uint32_t e = o0[m]; e < o1[m]; ++e) acc += ce[e];
+    u[m] = acc;
+  }
+  __syncthreads();  // the products are read; the tile takes their place
+#pragma unroll
+  for (int m = 0; m < 32; ++m) tile[p16(threadIdx.x + 256 * m)] = u[m];
+  lds_fwht_regs(tile, 13, 0);  // opens and closes with a barrier
+  const int64_t row = (b_begin + v) * ld.n;
+  for (int m = 0; m < 32; ++m) {
+    const int k = threadIdx.x + 256 * m;
+    const int64_t j = ((int64_t)(k >> B) << 13) + ((int64_t)a << B) + (k & ((1 << B) - 1));
+    if (j < ld.n) {
+      float val = flip(tile[p16(k)] * scale, (sw[k >> 5] >> (k & 31)) & 1u);
+      if (theta0) val += theta0[j];
+      store_out(out, out_dtype, row + j, val);
+    }
+  }
+}
+
+// FJL forward in one pass for the same layers (eq. ailon_chazelle), the
+// factorisation above read the other way: workgroup (a, vector) loads the
+// tile X[h][c] = b_j x_j of the coordinates j = (h, a, c) (runs of 2^B >= 32
+// consecutive ones), transforms it (Y = (H (x) H) X over all 13 bits), and
+// writes for every sample i at p = (p_h, p_a, p_c) its share
+// H[a, p_a] Y[p_h][p_c] g_i / sqrt(D) into partial slot a; the 2^H slots are
+// then summed in a fixed order (launch_reduce_partials).
+template <bool BF16, int R>
+__global__ __launch_bounds__(256) void k_fjl_fwd_onepass(const LayerDesc *__restrict__ layers, int layer,
+                                                         const float *__restrict__ gtab,
+                                                         const uint32_t *__restrict__ bpos,
+                                                         const void *__restrict__ x, int D, int64_t b_begin,
+                                                         int64_t bc, float *__restrict__ part, float scale, Key key) {
+  extern __shared__ float sm[];
+  float *tile = sm;                                                        // p16 layout, 2^13 cells
+  uint32_t *sw = reinterpret_cast<uint32_t *>(sm + p16_floats(1 << 13));  // sign words in tile order
+  const LayerDesc &ld = layers[layer];
+  const int H = ld.lgnp - 13, B = 13 - H;
+  const int a = blockIdx.x;
+  const int64_t v = blockIdx.y;
+  const int64_t row = (b_begin + v) * ld.n;
+  // coordinates past the layer's end read its last one (always valid) and are replaced by zero,
+  // a select rather than a branch per element
+  // (N' <= 2^21: coordinates fit 32-bit offsets from the row's uniform base)
+  const uint16_t *xh = (const uint16_t *)x + row;
+  const float *xf = (const float *)x + row;
+  const uint32_t nlast = (uint32_t)(ld.n - 1);
+  float xv[32];
+#pragma unroll
+  for (int m = 0; m < 32; ++m) {
+    const int k = threadIdx.x + 256 * m;
+    const uint32_t j = ((uint32_t)(k >> B) << 13) + ((uint32_t)a << B) + (uint32_t)(k & ((1 << B) - 1));
+    const uint32_t jc = j < nlast ? j : nlast;
+    const float t = BF16 ? bf16_to_f32(xh[jc]) : xf[jc];
+    xv[m] = j <= nlast ? t : 0.0f;
+  }
+  {
+    const int w = threadIdx.x;
+    const int64_t j = ((int64_t)(w >> (B - 5)) << 13) + ((int64_t)a << B) + ((w & ((1 << (B - 5)) - 1)) << 5);
+    sw[w] = sign_word((uint64_t)j, (uint32_t)ld.layer_id, key);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < 32; ++m) {
+    const int k = threadIdx.x + 256 * m;
+    tile[p16(k)] = flip(xv[m], (sw[k >> 5] >> (k & 31)) & 1u);
+  }
+  lds_fwht_regs(tile, 13, 0);  // opens and closes with a barrier
+  const float *g = gtab + (int64_t)layer * D;
+  float *o = part + ((int64_t)a * bc + v) * D;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = threadIdx.x + 256 * r;
+    if (i < D) {
+      const uint32_t q = bpos[i];
+      o[i] = flip(tile[p16((int)(q >> 8))], (uint32_t)__popc((uint32_t)a & q & 255u) & 1u) * (g[i] * scale);
+    }
+  }
+}
+
+void launch_fjl_fwd_onepass(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                            float *part, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const int H = ld.lgnp - 13;
+  const size_t shm = sizeof(float) * p16_floats(1 << 13) + sizeof(uint32_t) * 256;
+  const float scale = (float)(1.0 / std::sqrt((double)s->D));
+  const uint32_t *bpos = s->d_fjlb_pos + s->fjlb_pos_at[layer];
+#define SK_FJLF1(BF, R)                                                                                          \
+  hipLaunchKernelGGL((k_fjl_fwd_onepass<BF, R>), dim3(1u << H, (unsigned)bc), dim3(256), shm, st, s->d_layers,     \
+                     layer, s->d_gtab, bpos, x, (int)s->D, b_begin, bc, part, scale, s->key)
+  if (dtype == SK_BF16) {
+    if (s->D <= 4096) SK_FJLF1(true, 16); else SK_FJLF1(true, 32);
+  } else {
+    if (s->D <= 4096) SK_FJLF1(false, 16); else SK_FJLF1(false, 32);
+  }
+#undef SK_FJLF1
+  SK_CHECK_LAUNCH();
+}
+
+void launch_fjl_T_onepass(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
+                          int out_dtype, const float *theta0, hipStream_t st) {
+  const LayerDesc &ld = s->layers[layer];
+  const int H = ld.lgnp - 13;
+  const size_t shm = sizeof(float) * p16_floats(1 << 13) + sizeof(uint32_t) * 256;
+  const float scale = (float)(1.0 / std::sqrt((double)s->D));
+#define SK_FJLT1(R)                                                                                              \
+  hipLaunchKernelGGL(k_fjl_T_onepass<R>, dim3(1u << H, (unsigned)bc), dim3(256), shm, st, s->d_layers, layer,      \
+                     s->d_gtab, s->d_fjlb_off + s->fjlb_off_at[layer], s->d_fjlb_ent + s->fjlb_ent_at[layer], z,   \
+                     (int)s->D, b_begin, out, out_dtype, theta0, scale, s->key)
+  if (s->D <= 4096)
+    SK_FJLT1(16);
+  else
+    SK_FJLT1(32);
+#undef SK_FJLT1
+  SK_CHECK_LAUNCH();
+}
+
 // FJL transpose, first transform pass fused with the scatter of the D samples:
 // one workgroup per (vector, tile of 2^w positions of N'), w = min(log2 N', 13).
 // The tile starts at zero in LDS; every unique sample position inside it (a

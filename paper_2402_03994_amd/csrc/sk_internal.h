@@ -94,6 +94,13 @@ struct sk_sketch {
   // holds their position (ids and positions, D each) and the blocks' first entries (+ end)
   uint32_t *d_fjl_lsmp = nullptr, *d_fjl_lpos = nullptr, *d_fjl_loff = nullptr;
   std::vector<int64_t> fjl_loff_at;
+  // one-pass FJL transpose (2^14 <= N' <= 2^21): per layer, the samples sorted by tile cell
+  // (top bits, low bits), entry (id << 8) | middle bits, with 2^13 + 1 cell offsets
+  uint32_t *d_fjlb_off = nullptr, *d_fjlb_ent = nullptr;
+  std::vector<int64_t> fjlb_off_at, fjlb_ent_at;
+  // and for the one-pass forward, each sample's (cell << 8) | middle bits, by id
+  uint32_t *d_fjlb_pos = nullptr;
+  std::vector<int64_t> fjlb_pos_at;
   // QK
   float *d_qka = nullptr;       // A factors, fp32
   uint16_t *d_qkah = nullptr;   // A factors as bf16 hi terms, then bf16 lo terms (A-first contraction)

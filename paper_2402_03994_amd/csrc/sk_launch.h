@@ -180,6 +180,15 @@ void launch_fjl_T_pass0(const sk_sketch *s, int layer, const float *z, int64_t b
 void launch_signed_out(const sk_sketch *s, int layer, const float *w, int64_t b_begin, int64_t bc, void *out,
                        int out_dtype, const float *theta0, float scale, hipStream_t st);
 
+// One-pass FJL transpose for 2^14 <= N' <= 2^21 (tables built at creation).
+bool fjl_onepass_T_ok(int lgnp, int64_t D);
+void launch_fjl_T_onepass(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
+                          int out_dtype, const float *theta0, hipStream_t st);
+// One-pass FJL forward for the same layers: 2^(lgnp - 13) partial slots of
+// bc x D floats at part, summed afterwards by launch_reduce_partials.
+void launch_fjl_fwd_onepass(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
+                            float *part, hipStream_t st);
+
 // ---- FFD ----
 int64_t ffd_live_blocks(const sk_sketch *s, int layer);
 // Small D (<= 2^13): the layer's block tables (g, Pi, signs) are made per call
