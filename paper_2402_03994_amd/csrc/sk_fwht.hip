@@ -1321,11 +1321,28 @@ __global__ __launch_bounds__(256) void k_fjl_T_onepass(const LayerDesc *__restri
       q[r] = e < D ? bent[e] : 0u;
     }
     float gz[R];
+    if (R <= 16) {
+      // D <= 4096: g z by id, loaded in order, staged after the products (inside the tile), then
+      // gathered from LDS in cell order
+      float *gzs = sm + D;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int e = threadIdx.x + 256 * r;
-      const uint32_t i = q[r] >> 8;
-      gz[r] = e < D ? g[i] * zv[i] : 0.0f;
+      for (int r = 0; r < R; ++r) {
+        const int i = threadIdx.x + 256 * r;
+        if (i < D) gzs[i] = g[i] * zv[i];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int e = threadIdx.x + 256 * r;
+        gz[r] = e < D ? gzs[q[r] >> 8] : 0.0f;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int e = threadIdx.x + 256 * r;
+        const uint32_t i = q[r] >> 8;
+        gz[r] = e < D ? g[i] * zv[i] : 0.0f;
+      }
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
