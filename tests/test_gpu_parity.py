@@ -416,3 +416,26 @@ def test_affd_large_D_regenerated_gaussians(dev):
         y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
         assert rel_err(y, ref) < TOL_F32
         s.close()
+
+
+@pytest.mark.parametrize("kind", ["fjl", "ffd"])
+def test_d8192_parity(kind, dev):
+    """D = 2^13, the widest small-D FFD blocks (32 values per thread) and the one-pass FJL with 32
+    samples per thread (the transpose's products gathered from global memory): an N' = 2^21 layer
+    (B = 5 low bits per tile row), an N' = 2^14 layer (B = 12) and one padded to N' = D, which keeps
+    the pass-based path; forward, then the transpose with theta0."""
+    shapes, D = [(1, 2 ** 20 + 3), (3, 5000), (1, 9)], 8192
+    seed = 88
+    xs = rand_inputs(shapes, 3, seed)
+    s = sk(kind, shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply(kind, shapes, D, seed, [x.numpy() for x in xs])
+    assert rel_err(y, ref) < TOL_F32
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((2, D), generator=g)
+    th = [torch.randn(r * c, generator=g) * 0.02 for r, c in shapes]
+    outs = s.apply_T(z.to(dev), theta0=[t.to(dev) for t in th])
+    refs = O.apply_T(kind, shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.cpu().numpy(), r) < TOL_F32
+    s.close()
