@@ -436,17 +436,28 @@ __global__ __launch_bounds__(1 << LGNT, 4) void k_ffq_fwd(const LayerDesc *__res
 
 // ---------------------------------------------------------------------------
 // Layers with N = D and n <= 16384: X_{c + (N/L) e} = FFT_L(v_b w_N^{b c})[e].
+// The c values go in groups of CAP / L (max(1, D / CAP) groups whatever L is):
+// one workgroup per (group, layer, vector), blockIdx.x = group * ipg + the
+// (layer, vector) index of xcd_decode (ipg a multiple of 8, so a vector's
+// workgroups stay on one XCD).
 // ---------------------------------------------------------------------------
 template <int LGNT, int LGCAP>
 __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restrict__ layers, FfLayers g, int dtype,
                                                  int lgD, int64_t b_begin, int64_t bc, const float *__restrict__ gtab,
-                                                 float c1, float c2, const float2 *__restrict__ tw, int lgS, Key key) {
+                                                 float c1, float c2, const float2 *__restrict__ tw, int lgS, Key key,
+                                                 int64_t ipg) {
   constexpr int NT = 1 << LGNT, CAP = 1 << LGCAP, MAXE = CAP / NT;
   __shared__ float2 buf[CAP];
   __shared__ uint32_t sw[CAP / 32];
   __shared__ float2 tlo[1 << kLgTwSplit], thi[1 << kLgTwSplit];
+  const int cgrp = (int)(blockIdx.x / ipg);
   int64_t item, v;
-  if (!xcd_decode(g.n, bc, item, v)) return;
+  {
+    const int64_t L = blockIdx.x - cgrp * ipg, rest = L >> 3;
+    item = rest % g.n;
+    v = (rest / g.n) * 8 + (L & 7);
+    if (v >= bc) return;
+  }
   const int slot = (int)item;
   const LayerDesc &ld = layers[g.layer[slot]];
   const int64_t n = ld.n;
@@ -483,7 +494,8 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
   }
   float *y = g.y[slot] + v * ((int64_t)1 << lgD);
   const float *gl = gtab + (int64_t)lid * ((int64_t)1 << lgD);
-  for (int c0 = 0; c0 < (1 << lgcs); c0 += 1 << lgcg) {
+  {
+    const int c0 = cgrp << lgcg;  // this workgroup's group of c values (c0 < 2^lgcs: the grid has D / CAP groups)
 #pragma unroll
     for (int i = 0; i < MAXE; ++i) {
       const int e = threadIdx.x + i * NT;
@@ -515,7 +527,6 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
       else
         *(float2 *)(y + 2 * k) = make_float2(c2 * gv[i].x * X.x, c2 * gv[i].y * X.y);
     }
-    __syncthreads();
   }
 }
 
@@ -923,14 +934,17 @@ void run_afjlf_fwd(sk_sketch *s, int l0, int l1, const void *const *grads, int d
       g.y[i] = ybase + (int64_t)(g.layer[i] - l0) * lstride;
       gb += bc * s->layers[g.layer[i]].n * esz;
     }
-    const dim3 grid((unsigned)(g.n * ceil8(bc)));
+    // one workgroup per group of c values: max(1, D / CAP) groups for every layer
+    const int64_t ipg = (int64_t)g.n * ceil8(bc);
+    const int64_t ncg = std::max<int64_t>(1, D >> (big ? 14 : 13));
+    const dim3 grid((unsigned)(ipg * ncg));
     SK_PROF(SK_PROF_FF_SMALL, gb, {
       if (big)
         hipLaunchKernelGGL((k_ffs_fwd<10, 14>), grid, dim3(1024), 0, st, s->d_layers, g, dtype, lgD, b_begin, bc,
-                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key, ipg);
       else
         hipLaunchKernelGGL((k_ffs_fwd<9, 13>), grid, dim3(512), 0, st, s->d_layers, g, dtype, lgD, b_begin, bc,
-                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key);
+                           s->d_gtab, c1, c2, tw, s->ftw_lg, s->key, ipg);
     });
   });
   for_groups(s, l0, l1, bc, ufl, [&](const std::vector<int> &grp, int64_t tile, bool big) {
