@@ -178,8 +178,6 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
   const int64_t b0 = (item - g.item0[slot]) << lgW;
   const int64_t rows = std::min<int64_t>((n + R - 1) >> lgR, 1ll << lgP);
   const int nw = 1 << (lgW - 5);
-  build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
-  __syncthreads();
   const int64_t xo = (b_begin + v) * n;
   // four real columns (two complex ones) per element, at most CAP / (2 NT) elements per thread; every
   // 16-byte (fp32) or 8-byte (bf16) load of the thread is issued before the first one is used
@@ -218,6 +216,9 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffr_fwd(const LayerDesc *__restri
         raw[i] = *(const uint4 *)(xf + ((int64_t)(e >> lgW4) << lgR) + 4 * (e & ((1 << lgW4) - 1)));
     }
   }
+  // the block's sign words while the loads are in flight
+  build_row_signs<NT>(sw, rows, lgR, b0, lgW, (uint32_t)ld.layer_id, key);
+  __syncthreads();
 #pragma unroll
   for (int i = 0; i < MAXL; ++i) {
     const int e = threadIdx.x + i * NT;
