@@ -151,6 +151,20 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols(const LayerDesc *__restrict_
     b = u >> 5;
   }
   const int64_t blk = (v * nlive + b) * kD;
+  // kColsOutT: this thread's theta0 values (row 32 rc + m, column c0 + ri after the transform) are loaded
+  // with the block, so the transform hides their latency; positions past n read the last one
+  float th[32];
+  if (MODE == kColsOutT && theta0) {
+    const int ri0 = threadIdx.x & 31, rc0 = threadIdx.x >> 5;
+    const float *tb = theta0 + b * kD + c0 + ri0;
+    const int64_t lim = ld.n - 1 - (b * kD + c0 + ri0);  // last valid offset from tb
+#pragma unroll
+    for (int m = 0; m < 32; ++m) {
+      const int64_t o = (int64_t)(32 * rc0 + m) * 1024;
+      const float tv = tb[o < lim ? o : lim];
+      th[m] = o <= lim ? tv : 0.0f;
+    }
+  }
   {
     // thread: rows 4 k + quarter, elements r = 4 t .. 4 t + 3 (16-byte loads)
     const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
@@ -172,12 +186,12 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols(const LayerDesc *__restrict_
   fwht1024_rows32(s, e);
   const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
   if (MODE == kColsOutT) {
-#pragma unroll 8
+#pragma unroll
     for (int m = 0; m < 32; ++m) {
       const int r = 32 * rc + m;
       const int64_t jj = b * kD + (int64_t)r * 1024 + c0 + ri;
       if (jj < ld.n)
-        store_out(out, out_dtype, (b_begin + v) * ld.n + jj, e[m] * (1.0f / 32.0f) + (theta0 ? theta0[jj] : 0.0f));
+        store_out(out, out_dtype, (b_begin + v) * ld.n + jj, e[m] * (1.0f / 32.0f) + (theta0 ? th[m] : 0.0f));
     }
     return;
   }
