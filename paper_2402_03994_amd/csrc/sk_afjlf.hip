@@ -507,8 +507,8 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
         buf[e] = cscale(w, xr[i]);
       }
     }
-    lds_fft<false, NT, MAXE>(buf, lgL, lgcg, tw, lgS);
-    // outputs k = c + (N / L) ee, ee < L / 2: the G pairs loaded first
+    // outputs k = c + (N / L) ee, ee < L / 2: their G pairs are loaded before the transform, which
+    // hides the latency
     const int tot2 = (L / 2) << lgcg;
     float2 gv[MAXE / 2];
 #pragma unroll
@@ -517,6 +517,7 @@ __global__ __launch_bounds__(1 << LGNT) void k_ffs_fwd(const LayerDesc *__restri
       const int64_t k = (c0 + (e & ((1 << lgcg) - 1))) + ((int64_t)(e >> lgcg) << lgcs);
       if (e < tot2) gv[i] = *(const float2 *)(gl + 2 * k);
     }
+    lds_fft<false, NT, MAXE>(buf, lgL, lgcg, tw, lgS);
 #pragma unroll
     for (int i = 0; i < MAXE / 2; ++i) {
       const int e = threadIdx.x + i * NT;
