@@ -258,6 +258,73 @@ __global__ __launch_bounds__(256) void k_qk_s1a(const uint16_t *__restrict__ x, 
     }
 }
 
+// The same stage with 16-byte loads: each lane reads eight columns j0 .. j0 + 7
+// (two 128-byte lines per row for 16 lanes, half the load instructions of the
+// 8-byte form for the same bytes), which gives eight 16-column sets per MFMA
+// group; steps of 32 rows, the next step's rows loading during the MFMAs.
+template <int MT>
+__global__ __launch_bounds__(256) void k_qk_s1aw(const uint16_t *__restrict__ x, const uint16_t *__restrict__ Ah,
+                                                 const uint16_t *__restrict__ Al, int64_t m, int64_t n,
+                                                 int64_t b_begin, float *__restrict__ u) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, g = lane >> 4;
+  const int64_t v = blockIdx.y;
+  const int64_t j0 = (int64_t)blockIdx.x * 512 + wave * 128 + 8 * li;  // this lane's eight columns
+  const uint16_t *xc = x + (b_begin + v) * m * n + j0 + (int64_t)(g * 8) * n;
+  const uint16_t *ah = Ah + (int64_t)li * m + g * 8;
+  const uint16_t *al = Al + (int64_t)li * m + g * 8;
+  floatx4 acc[MT][8];
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[t][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint4 w[8];  // rows k0 + 8 g + r, columns j0 .. j0 + 7
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) w[r] = *(const uint4 *)(xc + (k0 + r) * n);
+  };
+  fetch(0);
+  for (int64_t k0 = 0; k0 < m; k0 += 32) {
+    // K fragments (rows k0 + 8 g .. + 7) of columns j0 + q, q < 8
+    Pack8 f[8];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t e[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) e[r] = p == 0 ? w[r].x : p == 1 ? w[r].y : p == 2 ? w[r].z : w[r].w;
+      f[2 * p].u = make_uint4(__builtin_amdgcn_perm(e[1], e[0], 0x05040100u),
+                              __builtin_amdgcn_perm(e[3], e[2], 0x05040100u),
+                              __builtin_amdgcn_perm(e[5], e[4], 0x05040100u),
+                              __builtin_amdgcn_perm(e[7], e[6], 0x05040100u));
+      f[2 * p + 1].u = make_uint4(__builtin_amdgcn_perm(e[1], e[0], 0x07060302u),
+                                  __builtin_amdgcn_perm(e[3], e[2], 0x07060302u),
+                                  __builtin_amdgcn_perm(e[5], e[4], 0x07060302u),
+                                  __builtin_amdgcn_perm(e[7], e[6], 0x07060302u));
+    }
+    if (k0 + 32 < m) fetch(k0 + 32);  // w is free once packed
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      Pack8 hv, lv;
+      hv.u = *(const uint4 *)(ah + (int64_t)(t * 16) * m + k0);
+      lv.u = *(const uint4 *)(al + (int64_t)(t * 16) * m + k0);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hv.v, f[q].v, acc[t][q], 0, 0, 0);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[t][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lv.v, f[q].v, acc[t][q], 0, 0, 0);
+    }
+  }
+  // D layout: lane holds rows 4 g .. 4 g + 3 (a) of its column in each set
+  float *ub = u + v * (int64_t)(MT * 16) * n + j0;
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t a = t * 16 + g * 4 + i;
+      *(float4 *)(ub + a * n) = make_float4(acc[t][0][i], acc[t][1][i], acc[t][2][i], acc[t][3][i]);
+      *(float4 *)(ub + a * n + 4) = make_float4(acc[t][4][i], acc[t][5][i], acc[t][6][i], acc[t][7][i]);
+    }
+}
+
 bool qk_afirst_ok(const LayerDesc &ld, int dtype) {
   return dtype == SK_BF16 && ld.da < ld.db && ld.da % 16 == 0 && ld.da <= 64 && ld.db % 16 == 0 && ld.m % 64 == 0 &&
          ld.nc % 256 == 0;
@@ -416,7 +483,16 @@ void launch_qk_apply(const sk_sketch *s, int layer, const void *x, int dtype, in
     if (stages & 1) {
       const uint16_t *Ah = s->d_qkah + ld.fa_off, *Al = s->d_qkah + s->qk_a_elems + ld.fa_off;
       const dim3 g1((unsigned)(ld.nc / 256), (unsigned)bc);
-      switch (ld.da / 16) {
+      if (ld.nc % 512 == 0 && ld.da <= 32) {
+        // eight columns per lane (16-byte loads)
+        const dim3 g1w((unsigned)(ld.nc / 512), (unsigned)bc);
+        if (ld.da == 16)
+          hipLaunchKernelGGL(k_qk_s1aw<1>, g1w, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                             (int64_t)ld.nc, b_begin, t_ws);
+        else
+          hipLaunchKernelGGL(k_qk_s1aw<2>, g1w, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
+                             (int64_t)ld.nc, b_begin, t_ws);
+      } else switch (ld.da / 16) {
         case 1: hipLaunchKernelGGL(k_qk_s1a<1>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,
                                    (int64_t)ld.nc, b_begin, t_ws); break;
         case 2: hipLaunchKernelGGL(k_qk_s1a<2>, g1, dim3(256), 0, st, (const uint16_t *)x, Ah, Al, (int64_t)ld.m,

@@ -241,7 +241,10 @@ def test_debug_streams_bit_exact(dev):
                                         (208, 384, 64, 48)], 512 + 4096 + 4096 + 3072),
                                       # dA < dB: the A-first contraction, one to four 16-row tiles of A
                                       ([(64, 512, 48, 64), (128, 256, 16, 32), (192, 768, 64, 80)],
-                                       48 * 64 + 16 * 32 + 64 * 80)])
+                                       48 * 64 + 16 * 32 + 64 * 80),
+                                      # A-first with columns a multiple of 512: eight columns per lane,
+                                      # one and two 16-row tiles of A
+                                      ([(64, 512, 16, 32), (128, 1024, 32, 48)], 16 * 32 + 32 * 48)])
 def test_qk_parity(shapes, D, dev):
     seed = 21
     xs = rand_inputs(shapes, 3, seed, dtype=torch.bfloat16, scale=0.01)
