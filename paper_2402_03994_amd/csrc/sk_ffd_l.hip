@@ -252,13 +252,13 @@ __global__ __launch_bounds__(256) void k_ffdL_sum(const LayerDesc *__restrict__ 
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = threadIdx.x + 256 * j;
+      // columns c0 .. c0 + 7 (c0 a multiple of 8) lie in one 32-coordinate sign word
+      const int64_t jj = b * kD + (int64_t)r * 1024 + c0;
+      const uint32_t bits = sign_word((uint64_t)jj, (uint32_t)ld.layer_id, key) >> (jj & 31);
 #pragma unroll
-      for (int q4 = 0; q4 < 2; ++q4) {
-        const int64_t jj = b * kD + (int64_t)r * 1024 + c0 + 4 * q4;
-        const uint32_t bits = sign_word((uint64_t)jj, (uint32_t)ld.layer_id, key) >> (jj & 31);
+      for (int q4 = 0; q4 < 2; ++q4)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) acc[j][q4][q] += flip(lds[L::idx(4 * q4 + q, r)], (bits >> q) & 1u);
-      }
+        for (int q = 0; q < 4; ++q) acc[j][q4][q] += flip(lds[L::idx(4 * q4 + q, r)], (bits >> (4 * q4 + q)) & 1u);
     }
   }
 #pragma unroll
