@@ -218,14 +218,20 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols(const LayerDesc *__restrict_
 
 // Forward epilogue: out[v][i] (+)= sum_b B_b(i) (H over r of block b)[i] for 8
 // columns per workgroup; the next block's columns load during the current one.
+// blockIdx.z picks a run of bseg consecutive blocks; with part set, run z
+// writes its sum to part[(z bc + v) D + i] (summed afterwards in the order of
+// z), else the one run covers every block and goes to out.
 __global__ __launch_bounds__(256) void k_ffdL_sum(const LayerDesc *__restrict__ layers, int layer,
                                                   const float *__restrict__ src, int64_t b_begin, int64_t nlive,
-                                                  float *__restrict__ out, int accumulate, Key key) {
+                                                  int64_t bseg, float *__restrict__ part, float *__restrict__ out,
+                                                  int accumulate, Key key) {
   using L = Lds1024<8>;
   __shared__ __align__(16) float lds[L::kFloats];
   const LayerDesc &ld = layers[layer];
   const int c0 = blockIdx.x * 8;
   const int64_t v = blockIdx.y;
+  const int64_t b_lo = (int64_t)blockIdx.z * bseg;
+  const int64_t b_hi = b_lo + bseg < nlive ? b_lo + bseg : nlive;
   // thread: rows r = tid + 256 j (j < 4), column groups c0 + 4 q4 (q4 < 2)
   float acc[4][2][4];
 #pragma unroll
@@ -241,12 +247,12 @@ __global__ __launch_bounds__(256) void k_ffdL_sum(const LayerDesc *__restrict__ 
 #pragma unroll
     for (int k = 0; k < 32; ++k) e[k] = p[32 * k];
   };
-  fetch(0);
-  for (int64_t b = 0; b < nlive; ++b) {
+  fetch(b_lo);
+  for (int64_t b = b_lo; b < b_hi; ++b) {
     float cur[32];
 #pragma unroll
     for (int k = 0; k < 32; ++k) cur[k] = e[k];
-    if (b + 1 < nlive) fetch(b + 1);
+    if (b + 1 < b_hi) fetch(b + 1);
     __syncthreads();  // the previous block's reads of lds are done
     fwht1024_lds_regs<8>(lds, cur);
 #pragma unroll
@@ -266,13 +272,14 @@ __global__ __launch_bounds__(256) void k_ffdL_sum(const LayerDesc *__restrict__ 
     const int r = threadIdx.x + 256 * j;
 #pragma unroll
     for (int q4 = 0; q4 < 2; ++q4) {
-      float *o = out + (b_begin + v) * kD + (int64_t)r * 1024 + c0 + 4 * q4;
+      float *o = (part ? part + ((int64_t)blockIdx.z * gridDim.y + v) * kD : out + (b_begin + v) * kD) +
+                 (int64_t)r * 1024 + c0 + 4 * q4;
       float4 a = make_float4(acc[j][q4][0], acc[j][q4][1], acc[j][q4][2], acc[j][q4][3]);
       a.x *= 1.0f / 32.0f;
       a.y *= 1.0f / 32.0f;
       a.z *= 1.0f / 32.0f;
       a.w *= 1.0f / 32.0f;
-      if (accumulate) {
+      if (accumulate && !part) {
         const float4 p = *(const float4 *)o;
         a.x += p.x;
         a.y += p.y;
@@ -306,8 +313,15 @@ void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, 
                        0, nullptr, s->key);
     hipLaunchKernelGGL((k_ffdL_rows<kRowsPermFwd, false>), gr, dim3(1024), 0, st, s->d_layers, layer, B, b_begin,
                        nlive, A, s->key);
-    hipLaunchKernelGGL(k_ffdL_sum, dim3(128u, (unsigned)bc), dim3(256), 0, st, s->d_layers, layer, A, b_begin, nlive,
-                       out, (int)accumulate, s->key);
+    // Under two workgroups per CU (128 column groups per vector), the blocks
+    // split into runs, for about four per CU, whose partial sums land in B
+    // (free here); at two or more the extra pass costs more than it gains.
+    const int64_t want = 128 * bc < 512 ? (1024 + 128 * bc - 1) / (128 * bc) : 1;
+    const int64_t nseg0 = want < nlive ? want : nlive;
+    const int64_t bseg = (nlive + nseg0 - 1) / nseg0, nseg = (nlive + bseg - 1) / bseg;
+    hipLaunchKernelGGL(k_ffdL_sum, dim3(128u, (unsigned)bc, (unsigned)nseg), dim3(256), 0, st, s->d_layers, layer, A,
+                       b_begin, nlive, bseg, nseg > 1 ? B : nullptr, out, (int)accumulate, s->key);
+    if (nseg > 1) launch_reduce_partials(B, nseg, bc, kD, b_begin, out, accumulate, st);
   }
   (void)hipGetLastError();
 }
