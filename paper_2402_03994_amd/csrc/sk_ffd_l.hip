@@ -291,6 +291,302 @@ __global__ __launch_bounds__(256) void k_ffdL_sum(const LayerDesc *__restrict__ 
   }
 }
 
+// Groups of four vectors (calls whose vector count is a multiple of 4).  The
+// intermediates that the permutation gathers from and writes to keep the four
+// vectors of group u interleaved: I4[((u nlive + b) D + pos) 4 + w] holds
+// position pos of block b of vector 4 u + w.  One 16-byte gather then fetches
+// a coordinate of all four vectors (a quarter of the cache-line requests of
+// four 4-byte gathers), and the permutation, g and the signs are evaluated
+// once per group instead of once per vector.
+
+// H over r of 8 columns c0.. of the group's four vectors (tile row 8 w + cq);
+// src per vector in pos order.  kColsG / kColsPlain: times g (kColsG), written
+// I4.  kColsOutT: src is I4; + theta0, natural order out (8 consecutive
+// outputs per vector and row; the four workgroups of a 32-column block run
+// back to back on one XCD, whose L2 joins their pieces of a line).
+template <int MODE>
+__global__ __launch_bounds__(1024) void k_ffdL_cols4(const LayerDesc *__restrict__ layers, int layer,
+                                                     const float *__restrict__ src, int64_t b_begin, int64_t nlive,
+                                                     float *__restrict__ dst, void *__restrict__ out, int out_dtype,
+                                                     const float *__restrict__ theta0, Key key) {
+  using L = Lds1024R32;
+  __shared__ __align__(16) float s[L::kFloats];
+  const LayerDesc &ld = layers[layer];
+  int c0 = blockIdx.x * 8;
+  int64_t b = blockIdx.y, u = blockIdx.z;
+  const int64_t ng = gridDim.z;
+  if (MODE == kColsOutT && (nlive * ng) % 8 == 0) {
+    // workgroup id g runs on XCD g mod 8; XCD x takes (block, group) pairs x,
+    // x + 8, ... (groups fastest, so theta0 is read from HBM once), and per
+    // pair the 32-column blocks one at a time, each as 4 consecutive tasks
+    const int64_t g = blockIdx.x + 128 * (blockIdx.y + nlive * blockIdx.z);
+    const int64_t k = g >> 3;
+    const int64_t pair = 8 * (k >> 7) + (g & 7);
+    c0 = (int)(k & 127) * 8;
+    b = pair / ng;
+    u = pair - b * ng;
+  }
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
+  // kColsOutT: theta0 of row 32 rc + m, column c0 + (ri & 7), loaded with the
+  // block so the transform hides its latency; positions past n read the last one
+  float th[32];
+  if (MODE == kColsOutT && theta0) {
+    const float *tb = theta0 + b * kD + c0 + (ri & 7);
+    const int64_t lim = ld.n - 1 - (b * kD + c0 + (ri & 7));
+#pragma unroll
+    for (int m = 0; m < 32; ++m) {
+      const int64_t o = (int64_t)(32 * rc + m) * 1024;
+      const float tv = tb[o < lim ? o : lim];
+      th[m] = o <= lim ? tv : 0.0f;
+    }
+  }
+  {
+    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+    if (MODE == kColsOutT) {
+      // I4 source: thread takes r = 256 quarter + t of the 8 columns, 4 vectors per load
+      const float4 *p = (const float4 *)src + (u * nlive + b) * kD + (int64_t)c0 * 1024 + 256 * quarter + t;
+      float4 val[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) val[k] = p[k * 1024];
+      const int r = 256 * quarter + t;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        s[L::idx(k, r)] = val[k].x;
+        s[L::idx(8 + k, r)] = val[k].y;
+        s[L::idx(16 + k, r)] = val[k].z;
+        s[L::idx(24 + k, r)] = val[k].w;
+      }
+    } else {
+      // per-vector source: thread takes vector 4 u + quarter, r = 4 t .. 4 t + 3 of each column
+      const float *p = src + ((4 * u + quarter) * nlive + b) * kD + (int64_t)c0 * 1024 + 4 * t;
+      float4 val[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) val[k] = *(const float4 *)(p + k * 1024);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = 8 * quarter + k;
+        s[L::idx(i, 4 * t)] = val[k].x;
+        s[L::idx(i, 4 * t + 1)] = val[k].y;
+        s[L::idx(i, 4 * t + 2)] = val[k].z;
+        s[L::idx(i, 4 * t + 3)] = val[k].w;
+      }
+    }
+  }
+  __syncthreads();
+  float e[32];
+  fwht1024_rows32(s, e);
+  if (MODE == kColsOutT) {
+    // lanes ri = 8 w + cq: row r of vector 4 u + w, column c0 + cq
+    const int64_t v = 4 * u + (ri >> 3);
+#pragma unroll
+    for (int m = 0; m < 32; ++m) {
+      const int r = 32 * rc + m;
+      const int64_t jj = b * kD + (int64_t)r * 1024 + c0 + (ri & 7);
+      if (jj < ld.n)
+        store_out(out, out_dtype, (b_begin + v) * ld.n + jj, e[m] * (1.0f / 32.0f) + (theta0 ? th[m] : 0.0f));
+    }
+    return;
+  }
+  // back to the block (tile row ri, element r), then thread r writes the 8
+  // columns of its row, four vectors per 16-byte store
+  __syncthreads();  // every thread's pass-2 reads are done
+  float *bq = s + ri * L::kStride + 33 * rc;
+#pragma unroll
+  for (int m = 0; m < 32; ++m) bq[m] = e[m];
+  __syncthreads();
+  const int r = threadIdx.x;
+  float4 *d4 = (float4 *)dst + (u * nlive + b) * kD + (int64_t)c0 * 1024 + r;
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    float g[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    if (MODE == kColsG)
+      gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + c0 + 4 * a) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cq = 4 * a + q;
+      const float f = g[q] * (1.0f / 32.0f);
+      d4[cq * 1024] = make_float4(s[L::idx(cq, r)] * f, s[L::idx(8 + cq, r)] * f, s[L::idx(16 + cq, r)] * f,
+                                  s[L::idx(24 + cq, r)] * f);
+    }
+  }
+}
+
+// Gather through the permutation and H over c for 8 rows r0.. of the group's
+// four vectors (tile row 4 rr + w), I4 in and I4 out (for each column the
+// 8 rows x 4 vectors are 32 consecutive floats: one 128-byte line).
+// kRowsPermFwd: k = pi^{-1}(d); kRowsPermT: g_i w[pi(i)].
+template <int MODE>
+__global__ __launch_bounds__(1024) void k_ffdL_rows4(const LayerDesc *__restrict__ layers, int layer,
+                                                     const float *__restrict__ src, int64_t nlive,
+                                                     float *__restrict__ dst, Key key) {
+  using L = Lds1024R32;
+  __shared__ __align__(16) float s[L::kFloats];
+  const LayerDesc &ld = layers[layer];
+  int r0 = blockIdx.x * 8;
+  int64_t b = blockIdx.y, u = blockIdx.z;
+  if ((nlive * gridDim.z) % 8 == 0) {
+    // workgroup id g runs on XCD g mod 8: XCD x takes (group, block) pairs
+    // x, x + 8, ... one at a time, so its random reads stay in its own L2
+    const int64_t g = blockIdx.x + 128 * (blockIdx.y + nlive * blockIdx.z);
+    const int64_t k = g >> 3;
+    const int64_t pair = 8 * (k >> 7) + (g & 7);
+    r0 = (int)(k & 127) * 8;
+    u = pair / nlive;
+    b = pair - u * nlive;
+  }
+  const int64_t blk = (u * nlive + b) * kD;  // this block's I4 region, in float4
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
+  const float4 *s4 = (const float4 *)src + blk;
+  // thread: rows rr = 2 quarter + h (h < 2); all its gathers are issued first
+  const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+  float4 val[2][4];
+  if (MODE == kRowsPermT) {
+    // columns 4 t + q, which share one Philox block of g
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t e0 = (uint32_t)(r0 + 2 * quarter + h) * 1024u + 4u * t;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) val[h][q] = s4[tpos(perm_fwd(pk, e0 + q))];
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int rr = 2 * quarter + h;
+      const uint32_t e0 = (uint32_t)(r0 + rr) * 1024u + 4u * t;
+      float g[4];
+      gauss4((uint64_t)(b * kD + e0) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = 4 * t + q;
+        s[L::idx(4 * rr, c)] = g[q] * val[h][q].x;
+        s[L::idx(4 * rr + 1, c)] = g[q] * val[h][q].y;
+        s[L::idx(4 * rr + 2, c)] = g[q] * val[h][q].z;
+        s[L::idx(4 * rr + 3, c)] = g[q] * val[h][q].w;
+      }
+    }
+  } else {
+    // columns t + 256 q, consecutive over the lanes
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        val[h][q] = s4[tpos(perm_inv(pk, (uint32_t)(r0 + 2 * quarter + h) * 1024u + (uint32_t)(t + 256 * q)))];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int rr = 2 * quarter + h;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = t + 256 * q;
+        s[L::idx(4 * rr, c)] = val[h][q].x;
+        s[L::idx(4 * rr + 1, c)] = val[h][q].y;
+        s[L::idx(4 * rr + 2, c)] = val[h][q].z;
+        s[L::idx(4 * rr + 3, c)] = val[h][q].w;
+      }
+    }
+  }
+  __syncthreads();
+  float e[32];
+  fwht1024_rows32(s, e);
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
+  // column 32 rc + m, tile row ri: float ((32 rc + m) 1024 + r0) 4 + ri of the block's I4 region
+  const __amdgpu_buffer_rsrc_t ws = buf_rsrc(dst + (blk + r0) * 4, (uint32_t)((kD - r0) * 16));
+  const int soff = (32 * rc * 4096 + ri) * 4;
+#pragma unroll
+  for (int m = 0; m < 32; ++m)
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m] * (1.0f / 32.0f)), ws, soff, m * 16384, 0);
+}
+
+// Forward epilogue of a group: for 2 columns c0.. of the four vectors (tile
+// row 4 cq + w), sum over the blocks b_lo .. b_hi - 1 of run z of B_b times
+// H over r; the next block's columns load during the current one.  Writes
+// part[((z bc + v) 1024 + c) 1024 + r] (k_ffdL_outT turns it into out).
+__global__ __launch_bounds__(256) void k_ffdL_sum4(const LayerDesc *__restrict__ layers, int layer,
+                                                   const float *__restrict__ src, int64_t nlive, int64_t bseg,
+                                                   float *__restrict__ part, Key key) {
+  using L = Lds1024<8>;
+  __shared__ __align__(16) float lds[L::kFloats];
+  const LayerDesc &ld = layers[layer];
+  const int c0 = blockIdx.x * 2;
+  const int64_t u = blockIdx.y, bc = 4 * (int64_t)gridDim.y;
+  const int64_t b_lo = (int64_t)blockIdx.z * bseg;
+  const int64_t b_hi = b_lo + bseg < nlive ? b_lo + bseg : nlive;
+  float acc[4][8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[j][q] = 0.0f;
+  // loads: column c0 + cq0, rows rl + 128 k, four vectors each
+  const int cq0 = threadIdx.x >> 7, rl = threadIdx.x & 127;
+  const float4 *base = (const float4 *)src + (int64_t)(c0 + cq0) * 1024 + rl;
+  float4 e[8];
+  auto fetch = [&](int64_t b) {
+    const float4 *p = base + (u * nlive + b) * kD;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) e[k] = p[128 * k];
+  };
+  fetch(b_lo);
+  for (int64_t b = b_lo; b < b_hi; ++b) {
+    float4 cur[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) cur[k] = e[k];
+    if (b + 1 < b_hi) fetch(b + 1);
+    __syncthreads();  // the previous block's reads of lds are done
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int r = rl + 128 * k;
+      lds[L::idx(4 * cq0, r)] = cur[k].x;
+      lds[L::idx(4 * cq0 + 1, r)] = cur[k].y;
+      lds[L::idx(4 * cq0 + 2, r)] = cur[k].z;
+      lds[L::idx(4 * cq0 + 3, r)] = cur[k].w;
+    }
+    __syncthreads();
+    fwht1024_lds<8>(lds);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = threadIdx.x + 256 * j;
+      // columns c0, c0 + 1 (c0 even) lie in one 32-coordinate sign word
+      const int64_t jj = b * kD + (int64_t)r * 1024 + c0;
+      const uint32_t bits = sign_word((uint64_t)jj, (uint32_t)ld.layer_id, key) >> (jj & 31);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[j][q] += flip(lds[L::idx(q, r)], (bits >> (q >> 2)) & 1u);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = threadIdx.x + 256 * j;
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      part[(((int64_t)blockIdx.z * bc + 4 * u + (q & 3)) * 1024 + c0 + (q >> 2)) * 1024 + r] =
+          acc[j][q] * (1.0f / 32.0f);
+  }
+}
+
+// out[v][r 1024 + c] (+)= sum over runs z < nseg of part[((z bc + v) 1024 + c)
+// 1024 + r], in the order of z; 32 x 32 tiles through LDS (128-byte reads and
+// writes).  Grid (32, 32, bc).
+__global__ __launch_bounds__(256) void k_ffdL_outT(const float *__restrict__ part, int64_t nseg, int64_t bc,
+                                                   int64_t b_begin, float *__restrict__ out, int accumulate) {
+  __shared__ float tl[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int64_t v = blockIdx.z;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = c0 + ty + 8 * k;
+    float a = 0.0f;
+    for (int64_t z = 0; z < nseg; ++z) a += part[((z * bc + v) * 1024 + c) * 1024 + r0 + tx];
+    tl[ty + 8 * k][tx] = a;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = r0 + ty + 8 * k;
+    float *o = out + (b_begin + v) * kD + (int64_t)r * 1024 + c0 + tx;
+    float a = tl[tx][ty + 8 * k];
+    if (accumulate) a += *o;
+    *o = a;
+  }
+}
+
 }  // namespace
 
 bool ffd_large_path(const sk_sketch *s) { return s->D == kD; }
@@ -308,7 +604,22 @@ void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, 
       hipLaunchKernelGGL((k_ffdL_rows<kRowsX, false>), gr, dim3(1024), 0, st, s->d_layers, layer, x, b_begin, nlive,
                          A, s->key);
   }
-  if (phases & 2) {
+  if ((phases & 2) && bc % 4 == 0) {
+    const int64_t ng = bc / 4;
+    const dim3 g4(128u, (unsigned)nlive, (unsigned)ng);
+    hipLaunchKernelGGL(k_ffdL_cols4<kColsG>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
+                       nullptr, 0, nullptr, s->key);
+    hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermFwd>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+    // 512 column pairs per group: split the blocks into runs only when that
+    // leaves under two workgroups per CU
+    const int64_t want = 512 * ng < 512 ? 2 : 1;
+    const int64_t nseg0 = want < nlive ? want : nlive;
+    const int64_t bseg = (nlive + nseg0 - 1) / nseg0, nseg = (nlive + bseg - 1) / bseg;
+    hipLaunchKernelGGL(k_ffdL_sum4, dim3(512u, (unsigned)ng, (unsigned)nseg), dim3(256), 0, st, s->d_layers, layer, A,
+                       nlive, bseg, B, s->key);
+    hipLaunchKernelGGL(k_ffdL_outT, dim3(32u, 32u, (unsigned)bc), dim3(256), 0, st, B, nseg, bc, b_begin, out,
+                       (int)accumulate);
+  } else if (phases & 2) {
     hipLaunchKernelGGL(k_ffdL_cols<kColsG>, gr, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B, nullptr,
                        0, nullptr, s->key);
     hipLaunchKernelGGL((k_ffdL_rows<kRowsPermFwd, false>), gr, dim3(1024), 0, st, s->d_layers, layer, B, b_begin,
@@ -331,6 +642,21 @@ void run_ffd_large_T(const sk_sketch *s, int layer, const float *z, int64_t b_be
   const int64_t nlive = ffd_live_blocks(s, layer);
   float *A = s->ws, *B = s->ws + bc * nlive * kD;
   const dim3 gr(32u, (unsigned)nlive, (unsigned)bc);
+  if (bc % 4 == 0) {
+    const dim3 g4(128u, (unsigned)nlive, (unsigned)(bc / 4));
+    if (phases & 1) {
+      hipLaunchKernelGGL((k_ffdL_rows<kRowsZ, false>), gr, dim3(1024), 0, st, s->d_layers, layer, z, b_begin, nlive,
+                         A, s->key);
+      hipLaunchKernelGGL(k_ffdL_cols4<kColsPlain>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
+                         nullptr, 0, nullptr, s->key);
+      hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermT>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+    }
+    if (phases & 2)
+      hipLaunchKernelGGL(k_ffdL_cols4<kColsOutT>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive,
+                         nullptr, out, out_dtype, theta0, s->key);
+    (void)hipGetLastError();
+    return;
+  }
   if (phases & 1) {
     hipLaunchKernelGGL((k_ffdL_rows<kRowsZ, false>), gr, dim3(1024), 0, st, s->d_layers, layer, z, b_begin, nlive, A,
                        s->key);

@@ -167,6 +167,28 @@ def test_ffd_large_D(dtype, dev):
         assert rel_err(o.float().cpu().numpy(), r) < (TOL_BF16 if dtype == "bf16" else TOL_F32)
 
 
+@pytest.mark.parametrize("batch,dtype", [(4, "f32"), (8, "bf16")])
+def test_ffd_large_D_groups(batch, dtype, dev):
+    """FFD with D = 2^20 on a batch that is a multiple of four: the four-vector
+    groups with interleaved intermediates.  Forward over three blocks with a
+    ragged tail plus a one-block layer (accumulated into the same output), and
+    theta0 + S^T z with fp32 or bf16 outputs."""
+    shapes, D, seed = [(1, 2 ** 21 + 5), (3, 1000)], 2 ** 20, 43
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xs = rand_inputs(shapes, batch, seed, dtype=tdt)
+    s = sk("ffd", shapes, D, seed, dev)
+    y = s.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("ffd", shapes, D, seed, [oracle_in(x)[0] for x in xs], dtype=dtype)
+    assert rel_err(y, ref) < TOL_F32
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((batch, D), generator=g)
+    th = [torch.randn(sh[0] * sh[1], generator=g) * 0.02 for sh in shapes]
+    outs = s.apply_T(z.to(dev), out_dtype=tdt, theta0=[t.to(dev) for t in th])
+    refs = O.apply_T("ffd", shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r in zip(outs, refs):
+        assert rel_err(o.float().cpu().numpy(), r) < (TOL_BF16 if dtype == "bf16" else TOL_F32)
+
+
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
 def test_forward_parity_bf16(kind, dev):
     shapes, D = CASES[3]
