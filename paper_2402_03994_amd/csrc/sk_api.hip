@@ -83,6 +83,7 @@ void free_all(sk_sketch *s) {
   f(s->d_qkbf);
   f(s->d_mtab);
   f(s->d_gsmall);
+  f(s->d_ffdb);
   f(s->d_qh);
   f(s->d_ftw);
   f(s->ws);
@@ -117,8 +118,8 @@ int64_t per_vector_bytes(const sk_sketch *s, int l0, int l1, bool transpose) {
       case SK_FFD:
         if (ilog2(s->D) <= kFfdSmallMax)  // partial sums (forward), then the call's block tables
           b = ((transpose ? 0 : ffd_small_groups(s, l) * s->D) + ffd_small_table_floats(s, l)) * 4;
-        else
-          b = 2 * ffd_live_blocks(s, l) * s->D * 4;
+        else  // two intermediates, plus a uint16 bucket index per position and group of four vectors
+          b = 2 * ffd_live_blocks(s, l) * s->D * 4 + ffd_live_blocks(s, l) * s->D / 2;
         break;
       case SK_QKH:
       case SK_AFJLQ:
@@ -634,6 +635,22 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
       SK_TRY(alloc((void **)&s->d_gsmall, (size_t)total * 4));
       for (int l = 0; l < n_layers; ++l)
         if (s->gsmall_off[l] >= 0) launch_affd_small_gtab(s, l, s->d_gsmall + s->gsmall_off[l], nullptr);
+    }
+  }
+  if (kind == SK_FFD && ffd_large_path(s)) {
+    // bucket offsets of the permutation of every live block (64 KB per block),
+    // when they take at most 1 GiB
+    int64_t total = 0;
+    s->ffdb_off.assign(n_layers, -1);
+    for (int l = 0; l < n_layers; ++l) {
+      s->ffdb_off[l] = total;
+      total += ffd_live_blocks(s, l) * kFfdBucketTab;
+    }
+    if (total * 2 <= (1ll << 30)) {
+      SK_TRY(alloc((void **)&s->d_ffdb, (size_t)total * 2));
+      for (int l = 0; l < n_layers; ++l) launch_ffd_bucket_tab(s, l, s->d_ffdb + s->ffdb_off[l], nullptr);
+    } else {
+      s->ffdb_off.assign(n_layers, -1);
     }
   }
   if (s->d_gtab) launch_gauss_table(s, s->d_gtab, nullptr);

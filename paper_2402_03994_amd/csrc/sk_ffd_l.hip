@@ -587,9 +587,232 @@ __global__ __launch_bounds__(256) void k_ffdL_outT(const float *__restrict__ par
   }
 }
 
+// Permutation through buckets (groups of four vectors, bucket offsets stored
+// at creation).  The producer (a cols pass: source positions k of 8 columns
+// c0.. and all rows, source group s = c0 / 8) computes each destination d,
+// counting-sorts its 8192 coordinates in LDS by destination chunk q = d >> 13
+// (8 rows), and writes each chunk's run, four vectors per 16-byte word, at its
+// offset in chunk q's bucket of 8192 words, with d & 8191 beside it (uint16).
+// The consumer (a rows pass over chunk q) reads the bucket as one contiguous
+// range and places every word at its destination in LDS: both passes read and
+// write whole lines, where the gather read a line per coordinate.  The order
+// inside a run follows LDS atomics; the placement, hence the result, does not.
+
+// Per (source group s, block b, direction): how many of its 8192 coordinates
+// go to each destination chunk.
+__global__ __launch_bounds__(1024) void k_ffdL_bcount(const LayerDesc *__restrict__ layers, int layer,
+                                                      uint16_t *__restrict__ tab, Key key) {
+  __shared__ uint32_t hist[128];
+  const LayerDesc &ld = layers[layer];
+  const int sg = blockIdx.x, dir = blockIdx.z;
+  const int64_t b = blockIdx.y;
+  if (threadIdx.x < 128) hist[threadIdx.x] = 0u;
+  __syncthreads();
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
+#pragma unroll
+  for (int cq = 0; cq < 8; ++cq) {
+    const uint32_t k = (uint32_t)threadIdx.x * 1024u + 8u * sg + cq;
+    const uint32_t d = dir ? perm_inv(pk, k) : perm_fwd(pk, k);
+    atomicAdd(&hist[d >> 13], 1u);
+  }
+  __syncthreads();
+  if (threadIdx.x < 128) tab[((b * 2 + dir) * 128 + sg) * 128 + threadIdx.x] = (uint16_t)hist[threadIdx.x];
+}
+
+// Counts -> run starts: exclusive prefix over the source groups of each chunk.
+__global__ __launch_bounds__(128) void k_ffdL_bscan(uint16_t *__restrict__ tab) {
+  uint16_t *t = tab + (int64_t)blockIdx.x * 128 * 128 + threadIdx.x;
+  uint32_t run = 0;
+  for (int sg = 0; sg < 128; ++sg) {
+    const uint32_t c = t[sg * 128];
+    t[sg * 128] = (uint16_t)run;
+    run += c;
+  }
+}
+
+// Producer: H over r of 8 columns c0.. of the group's four vectors (as
+// k_ffdL_cols4, times g for kColsG), then the bucket writes.  kColsG (forward)
+// sends k to d = pi(k), kColsPlain (transpose) to d = pi^{-1}(k).
+template <int MODE>
+__global__ __launch_bounds__(1024) void k_ffdL_cols4b(const LayerDesc *__restrict__ layers, int layer,
+                                                      const float *__restrict__ src, int64_t nlive,
+                                                      const uint16_t *__restrict__ tab, float *__restrict__ dst,
+                                                      uint16_t *__restrict__ didx, Key key) {
+  using L = Lds1024R32;
+  // after the transform: 8192 words, their uint16 destinations, then counts,
+  // run starts in this workgroup and run starts in the buckets (128 each)
+  constexpr int kStage = 8192 * 4 + 8192 / 2 + 3 * 128;
+  constexpr int kFl = kStage > L::kFloats ? kStage : L::kFloats;
+  __shared__ __align__(16) float s[kFl];
+  const LayerDesc &ld = layers[layer];
+  const int sg = blockIdx.x, c0 = 8 * sg;
+  const int64_t b = blockIdx.y, u = blockIdx.z;
+  constexpr int dir = MODE == kColsG ? 0 : 1;
+  {
+    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+    const float *p = src + ((4 * u + quarter) * nlive + b) * kD + (int64_t)c0 * 1024 + 4 * t;
+    float4 val[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) val[k] = *(const float4 *)(p + k * 1024);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = 8 * quarter + k;
+      s[L::idx(i, 4 * t)] = val[k].x;
+      s[L::idx(i, 4 * t + 1)] = val[k].y;
+      s[L::idx(i, 4 * t + 2)] = val[k].z;
+      s[L::idx(i, 4 * t + 3)] = val[k].w;
+    }
+  }
+  __syncthreads();
+  float e[32];
+  fwht1024_rows32(s, e);
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
+  __syncthreads();  // every thread's pass-2 reads are done
+  {
+    float *bq = s + ri * L::kStride + 33 * rc;
+#pragma unroll
+    for (int m = 0; m < 32; ++m) bq[m] = e[m];
+  }
+  __syncthreads();
+  // thread r: the 8 columns of row r, four vectors each
+  const int r = threadIdx.x;
+  float4 v4[8];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    float g[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    if (MODE == kColsG)
+      gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + c0 + 4 * a) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cq = 4 * a + q;
+      const float f = g[q] * (1.0f / 32.0f);
+      v4[cq] = make_float4(s[L::idx(cq, r)] * f, s[L::idx(8 + cq, r)] * f, s[L::idx(16 + cq, r)] * f,
+                           s[L::idx(24 + cq, r)] * f);
+    }
+  }
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
+  uint32_t dd[8];
+#pragma unroll
+  for (int cq = 0; cq < 8; ++cq) {
+    const uint32_t k = (uint32_t)r * 1024u + (uint32_t)(c0 + cq);
+    dd[cq] = dir ? perm_inv(pk, k) : perm_fwd(pk, k);
+  }
+  float4 *stg = (float4 *)s;
+  uint16_t *sdd = (uint16_t *)(s + 8192 * 4);
+  uint32_t *cnt = (uint32_t *)(s + 8192 * 4 + 8192 / 2), *loc = cnt + 128, *boff = cnt + 256;
+  __syncthreads();  // the tile has been read: its space becomes the staging area
+  if (threadIdx.x < 128) {
+    cnt[threadIdx.x] = 0u;
+    boff[threadIdx.x] = tab[((b * 2 + dir) * 128 + sg) * 128 + threadIdx.x];
+  }
+  __syncthreads();
+  uint32_t rank[8];
+#pragma unroll
+  for (int cq = 0; cq < 8; ++cq) rank[cq] = atomicAdd(&cnt[dd[cq] >> 13], 1u);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+#pragma unroll 8
+    for (int q = 0; q < 128; ++q) {
+      loc[q] = run;
+      run += cnt[q];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int cq = 0; cq < 8; ++cq) {
+    const uint32_t pos = loc[dd[cq] >> 13] + rank[cq];
+    stg[pos] = v4[cq];
+    sdd[pos] = (uint16_t)(dd[cq] & 8191u);
+  }
+  __syncthreads();
+  // slot j of the sorted order belongs to the last chunk q with loc[q] <= j
+  float4 *d4 = (float4 *)dst + (u * nlive + b) * kD;
+  uint16_t *dx = didx + (u * nlive + b) * kD;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const uint32_t j = threadIdx.x + 1024u * m;
+    uint32_t q = 0;
+#pragma unroll
+    for (uint32_t step = 64; step > 0; step >>= 1)
+      if (loc[q + step] <= j) q += step;
+    const uint32_t at = boff[q] + (j - loc[q]);
+    if (at < 8192u) {
+      d4[q * 8192 + at] = stg[j];
+      dx[q * 8192 + at] = sdd[j];
+    }
+  }
+}
+
+// Consumer: chunk q (rows 8 q ..) of the group's four vectors from its bucket
+// (tile row 4 rr + w), g_i for kRowsPermT, H over c, written I4 as k_ffdL_rows4.
+template <int MODE>
+__global__ __launch_bounds__(1024) void k_ffdL_rows4b(const LayerDesc *__restrict__ layers, int layer,
+                                                      const float *__restrict__ src,
+                                                      const uint16_t *__restrict__ didx, int64_t nlive,
+                                                      float *__restrict__ dst, Key key) {
+  using L = Lds1024R32;
+  __shared__ __align__(16) float s[L::kFloats];
+  const LayerDesc &ld = layers[layer];
+  const int q = blockIdx.x, r0 = 8 * q;
+  const int64_t b = blockIdx.y, u = blockIdx.z;
+  const int64_t blk = (u * nlive + b) * kD;
+  {
+    const float4 *s4 = (const float4 *)src + blk + q * 8192;
+    const uint16_t *ix = didx + blk + q * 8192;
+    float4 val[8];
+    uint32_t dd[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      val[m] = s4[threadIdx.x + 1024 * m];
+      dd[m] = ix[threadIdx.x + 1024 * m];
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int rr = (int)(dd[m] >> 10) & 7, c = (int)(dd[m] & 1023u);
+      s[L::idx(4 * rr, c)] = val[m].x;
+      s[L::idx(4 * rr + 1, c)] = val[m].y;
+      s[L::idx(4 * rr + 2, c)] = val[m].z;
+      s[L::idx(4 * rr + 3, c)] = val[m].w;
+    }
+  }
+  __syncthreads();
+  if (MODE == kRowsPermT) {
+    // g_i of the destination: columns 4 t + qq of rows 2 quarter + h, one Philox block each
+    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int rr = 2 * quarter + h;
+      float g[4];
+      gauss4((uint64_t)(b * kD + (int64_t)(r0 + rr) * 1024 + 4 * t) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) s[L::idx(4 * rr + w, 4 * t + qq)] *= g[qq];
+    }
+    __syncthreads();
+  }
+  float e[32];
+  fwht1024_rows32(s, e);
+  const int ri = threadIdx.x & 31, rc = threadIdx.x >> 5;
+  const __amdgpu_buffer_rsrc_t ws = buf_rsrc(dst + (blk + r0) * 4, (uint32_t)((kD - r0) * 16));
+  const int soff = (32 * rc * 4096 + ri) * 4;
+#pragma unroll
+  for (int m = 0; m < 32; ++m)
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e[m] * (1.0f / 32.0f)), ws, soff, m * 16384, 0);
+}
+
 }  // namespace
 
 bool ffd_large_path(const sk_sketch *s) { return s->D == kD; }
+
+void launch_ffd_bucket_tab(const sk_sketch *s, int layer, uint16_t *tab, hipStream_t st) {
+  const int64_t nlive = ffd_live_blocks(s, layer);
+  hipLaunchKernelGGL(k_ffdL_bcount, dim3(128u, (unsigned)nlive, 2u), dim3(1024), 0, st, s->d_layers, layer, tab,
+                     s->key);
+  hipLaunchKernelGGL(k_ffdL_bscan, dim3((unsigned)(nlive * 2)), dim3(128), 0, st, tab);
+  (void)hipGetLastError();
+}
 
 void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                        float *out, bool accumulate, int phases, hipStream_t st) {
@@ -607,9 +830,17 @@ void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, 
   if ((phases & 2) && bc % 4 == 0) {
     const int64_t ng = bc / 4;
     const dim3 g4(128u, (unsigned)nlive, (unsigned)ng);
-    hipLaunchKernelGGL(k_ffdL_cols4<kColsG>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
-                       nullptr, 0, nullptr, s->key);
-    hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermFwd>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+    if (s->d_ffdb && s->ffdb_off[layer] >= 0) {
+      uint16_t *ix = (uint16_t *)(s->ws + 2 * bc * nlive * kD);
+      hipLaunchKernelGGL(k_ffdL_cols4b<kColsG>, g4, dim3(1024), 0, st, s->d_layers, layer, A, nlive,
+                         s->d_ffdb + s->ffdb_off[layer], B, ix, s->key);
+      hipLaunchKernelGGL(k_ffdL_rows4b<kRowsPermFwd>, g4, dim3(1024), 0, st, s->d_layers, layer, B, ix, nlive, A,
+                         s->key);
+    } else {
+      hipLaunchKernelGGL(k_ffdL_cols4<kColsG>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
+                         nullptr, 0, nullptr, s->key);
+      hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermFwd>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+    }
     // 512 column pairs per group: split the blocks into runs only when that
     // leaves under two workgroups per CU
     const int64_t want = 512 * ng < 512 ? 2 : 1;
@@ -647,9 +878,17 @@ void run_ffd_large_T(const sk_sketch *s, int layer, const float *z, int64_t b_be
     if (phases & 1) {
       hipLaunchKernelGGL((k_ffdL_rows<kRowsZ, false>), gr, dim3(1024), 0, st, s->d_layers, layer, z, b_begin, nlive,
                          A, s->key);
-      hipLaunchKernelGGL(k_ffdL_cols4<kColsPlain>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive, B,
-                         nullptr, 0, nullptr, s->key);
-      hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermT>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+      if (s->d_ffdb && s->ffdb_off[layer] >= 0) {
+        uint16_t *ix = (uint16_t *)(s->ws + 2 * bc * nlive * kD);
+        hipLaunchKernelGGL(k_ffdL_cols4b<kColsPlain>, g4, dim3(1024), 0, st, s->d_layers, layer, A, nlive,
+                           s->d_ffdb + s->ffdb_off[layer], B, ix, s->key);
+        hipLaunchKernelGGL(k_ffdL_rows4b<kRowsPermT>, g4, dim3(1024), 0, st, s->d_layers, layer, B, ix, nlive, A,
+                           s->key);
+      } else {
+        hipLaunchKernelGGL(k_ffdL_cols4<kColsPlain>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive,
+                           B, nullptr, 0, nullptr, s->key);
+        hipLaunchKernelGGL(k_ffdL_rows4<kRowsPermT>, g4, dim3(1024), 0, st, s->d_layers, layer, B, nlive, A, s->key);
+      }
     }
     if (phases & 2)
       hipLaunchKernelGGL(k_ffdL_cols4<kColsOutT>, g4, dim3(1024), 0, st, s->d_layers, layer, A, b_begin, nlive,

@@ -113,6 +113,10 @@ struct sk_sketch {
   // AFFD: G over [0, D) of each small-path layer (N' = D)
   float *d_gsmall = nullptr;
   std::vector<int64_t> gsmall_off;  // per layer: float offset into d_gsmall, -1 if none
+  // FFD, D = 2^20: per block and direction, where each 8-column source group's
+  // run starts in the bucket of each 8-row destination chunk (uint16 [2][128][128])
+  uint16_t *d_ffdb = nullptr;
+  std::vector<int64_t> ffdb_off;  // per layer: offset into d_ffdb, -1 if none
   // QKH / AFJLQ: per layer A, A^T, Qt, Qt^T, w (fp32)
   float *d_qh = nullptr;
   // AFJLF: twiddle table exp(-2 pi i m / 2^ftw_lg), m < 2^ftw_lg (complex fp32)

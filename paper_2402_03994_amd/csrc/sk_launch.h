@@ -222,6 +222,12 @@ void launch_debug_stream(const sk_sketch *s, int layer, int stream_id, uint64_t 
 // FFD with D = 2^20: rows/cols kernels over transposed intermediates.
 // phases: bit 0 = the kernel that reads the input, bit 1 = the rest.
 bool ffd_large_path(const sk_sketch *s);
+// Bucket offsets of the permutations of a layer's live blocks: uint16
+// [block][direction][source group s < 128][destination chunk q < 128] = the
+// start of group s's run inside chunk q's bucket of 8192 (direction 0: d =
+// pi(k), 1: d = pi^{-1}(k)).
+constexpr int64_t kFfdBucketTab = 2 * 128 * 128;
+void launch_ffd_bucket_tab(const sk_sketch *s, int layer, uint16_t *tab, hipStream_t st);
 void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, int64_t b_begin, int64_t bc,
                        float *out, bool accumulate, int phases, hipStream_t st);
 void run_ffd_large_T(const sk_sketch *s, int layer, const float *z, int64_t b_begin, int64_t bc, void *out,
