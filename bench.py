@@ -57,13 +57,17 @@ KERNEL_OF = {"affd:affd_rows": "k_affdT_rows", "afjl:afjl_fold": "k_afjl_fold", 
              "affd:gather": "k_affdT_outm", "ffd:prolog": "k_ffd_tables",
              "fjl:fjl_t": "k_fjl_T_onepass"}
 # FFD with D = 2^20 (rows / cols passes): prolog = the first rows pass of the forward, gather = the last cols
-# pass of the transpose; the ffd class groups the middle passes (several kernels)
+# pass of the transpose (the four-vector form when the batch is a multiple of 4); the ffd class groups the
+# middle passes (several kernels)
 KERNEL_OF_FFD_LARGE = {"ffd:prolog": "k_ffdL_rows<0", "ffd:gather": "k_ffdL_cols<2>",
                        "ffd:ffd": "k_ffdL middle passes"}
 
 
 def kernel_of(cfg: str, kclass: str) -> str:
-    if W.CONFIGS[cfg]["D"] == 1 << 20 and kclass in KERNEL_OF_FFD_LARGE:
+    c = W.CONFIGS[cfg]
+    if c["D"] == 1 << 20 and kclass in KERNEL_OF_FFD_LARGE:
+        if kclass == "ffd:gather" and c["batch"] % 4 == 0:
+            return "k_ffdL_cols4<2>"
         return KERNEL_OF_FFD_LARGE[kclass]
     return KERNEL_OF.get(kclass, kclass)
 
