@@ -639,29 +639,67 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols4b(const LayerDesc *__restric
                                                       const uint16_t *__restrict__ tab, float *__restrict__ dst,
                                                       uint16_t *__restrict__ didx, Key key) {
   using L = Lds1024R32;
-  // after the transform: 8192 words, their uint16 destinations, then counts,
-  // run starts in this workgroup and run starts in the buckets (128 each)
-  constexpr int kStage = 8192 * 4 + 8192 / 2 + 3 * 128;
-  constexpr int kFl = kStage > L::kFloats ? kStage : L::kFloats;
+  // after the transform: 8192 words and their uint16 destinations; past the
+  // tile: counts, run starts in this workgroup and run starts in the buckets
+  constexpr int kStage = 8192 * 4 + 8192 / 2;
+  constexpr int kFl = (kStage > L::kFloats ? kStage : L::kFloats) + 3 * 128;
   __shared__ __align__(16) float s[kFl];
   const LayerDesc &ld = layers[layer];
   const int sg = blockIdx.x, c0 = 8 * sg;
   const int64_t b = blockIdx.y, u = blockIdx.z;
   constexpr int dir = MODE == kColsG ? 0 : 1;
+  uint32_t *cnt = (uint32_t *)(s + kFl - 3 * 128), *loc = cnt + 128, *boff = cnt + 256;
+  // the run starts, then the tile, are loaded first; everything that depends
+  // only on positions (destinations, ranks, run offsets, g) is made while the
+  // tile is in flight
+  uint32_t tb = 0;
+  if (threadIdx.x < 128) tb = tab[((b * 2 + dir) * 128 + sg) * 128 + threadIdx.x];
+  const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+  float4 val[8];
   {
-    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
     const float *p = src + ((4 * u + quarter) * nlive + b) * kD + (int64_t)c0 * 1024 + 4 * t;
-    float4 val[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) val[k] = *(const float4 *)(p + k * 1024);
+  }
+  if (threadIdx.x < 128) cnt[threadIdx.x] = 0u;
+  // thread r: sources k = r 1024 + c0 + cq of row r
+  const int r = threadIdx.x;
+  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
+  uint32_t dd[8], rank[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int i = 8 * quarter + k;
-      s[L::idx(i, 4 * t)] = val[k].x;
-      s[L::idx(i, 4 * t + 1)] = val[k].y;
-      s[L::idx(i, 4 * t + 2)] = val[k].z;
-      s[L::idx(i, 4 * t + 3)] = val[k].w;
+  for (int cq = 0; cq < 8; ++cq) {
+    const uint32_t k = (uint32_t)r * 1024u + (uint32_t)(c0 + cq);
+    dd[cq] = dir ? perm_inv(pk, k) : perm_fwd(pk, k);
+  }
+  float g[8];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    if (MODE == kColsG)
+      gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + c0 + 4 * a) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g + 4 * a);
+    else
+      g[4 * a] = g[4 * a + 1] = g[4 * a + 2] = g[4 * a + 3] = 1.0f;
+  }
+  if (threadIdx.x < 128) boff[threadIdx.x] = tb;
+  __syncthreads();  // counters zeroed
+#pragma unroll
+  for (int cq = 0; cq < 8; ++cq) rank[cq] = atomicAdd(&cnt[dd[cq] >> 13], 1u);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+#pragma unroll 8
+    for (int q = 0; q < 128; ++q) {
+      loc[q] = run;
+      run += cnt[q];
     }
+  }
+  // tile: H over r of the 8 columns of the four vectors (tile row 8 w + cq)
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int i = 8 * quarter + k;
+    s[L::idx(i, 4 * t)] = val[k].x;
+    s[L::idx(i, 4 * t + 1)] = val[k].y;
+    s[L::idx(i, 4 * t + 2)] = val[k].z;
+    s[L::idx(i, 4 * t + 3)] = val[k].w;
   }
   __syncthreads();
   float e[32];
@@ -674,51 +712,16 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols4b(const LayerDesc *__restric
     for (int m = 0; m < 32; ++m) bq[m] = e[m];
   }
   __syncthreads();
-  // thread r: the 8 columns of row r, four vectors each
-  const int r = threadIdx.x;
   float4 v4[8];
 #pragma unroll
-  for (int a = 0; a < 2; ++a) {
-    float g[4] = {1.0f, 1.0f, 1.0f, 1.0f};
-    if (MODE == kColsG)
-      gauss4((uint64_t)(b * kD + (int64_t)r * 1024 + c0 + 4 * a) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int cq = 4 * a + q;
-      const float f = g[q] * (1.0f / 32.0f);
-      v4[cq] = make_float4(s[L::idx(cq, r)] * f, s[L::idx(8 + cq, r)] * f, s[L::idx(16 + cq, r)] * f,
-                           s[L::idx(24 + cq, r)] * f);
-    }
-  }
-  const PermKey pk = perm_key((uint32_t)ld.layer_id, ST_FFDPERM, (uint32_t)b, (uint32_t)kLgD, key);
-  uint32_t dd[8];
-#pragma unroll
   for (int cq = 0; cq < 8; ++cq) {
-    const uint32_t k = (uint32_t)r * 1024u + (uint32_t)(c0 + cq);
-    dd[cq] = dir ? perm_inv(pk, k) : perm_fwd(pk, k);
+    const float f = g[cq] * (1.0f / 32.0f);
+    v4[cq] = make_float4(s[L::idx(cq, r)] * f, s[L::idx(8 + cq, r)] * f, s[L::idx(16 + cq, r)] * f,
+                         s[L::idx(24 + cq, r)] * f);
   }
   float4 *stg = (float4 *)s;
   uint16_t *sdd = (uint16_t *)(s + 8192 * 4);
-  uint32_t *cnt = (uint32_t *)(s + 8192 * 4 + 8192 / 2), *loc = cnt + 128, *boff = cnt + 256;
   __syncthreads();  // the tile has been read: its space becomes the staging area
-  if (threadIdx.x < 128) {
-    cnt[threadIdx.x] = 0u;
-    boff[threadIdx.x] = tab[((b * 2 + dir) * 128 + sg) * 128 + threadIdx.x];
-  }
-  __syncthreads();
-  uint32_t rank[8];
-#pragma unroll
-  for (int cq = 0; cq < 8; ++cq) rank[cq] = atomicAdd(&cnt[dd[cq] >> 13], 1u);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t run = 0;
-#pragma unroll 8
-    for (int q = 0; q < 128; ++q) {
-      loc[q] = run;
-      run += cnt[q];
-    }
-  }
-  __syncthreads();
 #pragma unroll
   for (int cq = 0; cq < 8; ++cq) {
     const uint32_t pos = loc[dd[cq] >> 13] + rank[cq];
@@ -757,6 +760,8 @@ __global__ __launch_bounds__(1024) void k_ffdL_rows4b(const LayerDesc *__restric
   const int q = blockIdx.x, r0 = 8 * q;
   const int64_t b = blockIdx.y, u = blockIdx.z;
   const int64_t blk = (u * nlive + b) * kD;
+  const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
+  float g[2][4];
   {
     const float4 *s4 = (const float4 *)src + blk + q * 8192;
     const uint16_t *ix = didx + blk + q * 8192;
@@ -767,6 +772,13 @@ __global__ __launch_bounds__(1024) void k_ffdL_rows4b(const LayerDesc *__restric
       val[m] = s4[threadIdx.x + 1024 * m];
       dd[m] = ix[threadIdx.x + 1024 * m];
     }
+    // kRowsPermT: g_i of the destinations columns 4 t + qq of rows 2 quarter + h,
+    // made while the bucket is in flight
+    if (MODE == kRowsPermT)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        gauss4((uint64_t)(b * kD + (int64_t)(r0 + 2 * quarter + h) * 1024 + 4 * t) >> 2, (uint32_t)ld.layer_id,
+               ST_GAUSS, key, g[h]);
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int rr = (int)(dd[m] >> 10) & 7, c = (int)(dd[m] & 1023u);
@@ -778,17 +790,13 @@ __global__ __launch_bounds__(1024) void k_ffdL_rows4b(const LayerDesc *__restric
   }
   __syncthreads();
   if (MODE == kRowsPermT) {
-    // g_i of the destination: columns 4 t + qq of rows 2 quarter + h, one Philox block each
-    const int quarter = threadIdx.x >> 8, t = threadIdx.x & 255;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int rr = 2 * quarter + h;
-      float g[4];
-      gauss4((uint64_t)(b * kD + (int64_t)(r0 + rr) * 1024 + 4 * t) >> 2, (uint32_t)ld.layer_id, ST_GAUSS, key, g);
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) s[L::idx(4 * rr + w, 4 * t + qq)] *= g[qq];
+        for (int w = 0; w < 4; ++w) s[L::idx(4 * rr + w, 4 * t + qq)] *= g[h][qq];
     }
     __syncthreads();
   }
