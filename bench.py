@@ -72,6 +72,14 @@ def kernel_of(cfg: str, kclass: str) -> str:
     return KERNEL_OF.get(kclass, kclass)
 
 
+def qk_flops(m, n, da, db):
+    """MFMA flops of one vector through a QK matrix in the contraction order the library takes: A first
+    (U = A X) when that makes fewer products, or when the 16-byte-load A-first kernel applies (dA <= 32,
+    dA <= 2 dB, columns a multiple of 512), else B first (T = X B^T)."""
+    afirst = m % 64 == 0 and n % 256 == 0 and ((da < db and da <= 64) or (da <= 32 and da <= 2 * db and n % 512 == 0))
+    return 2 * da * m * n + 2 * da * n * db if afirst else 2 * m * n * db + 2 * da * m * db
+
+
 def qh_flops(kind, shapes, D):
     """Multiply-add flops (2 per product) per vector of the contractions of the Q kinds, per profile
     class (qh_first reads the input, qh_second forms the output, qh_t the transpose), following the
@@ -617,7 +625,7 @@ def main() -> int:
                                      "reads": "intermediates only (no algorithmic bytes)"}
     if cfg == "c3":
         c = W.CONFIGS[cfg]
-        flops = sum(2 * s[0] * s[1] * s[3] + 2 * s[2] * s[0] * s[3] for s in c["shapes"]) * c["batch"]
+        flops = sum(qk_flops(*s) for s in c["shapes"]) * c["batch"]
         roofline["mfma_tflops"] = round(flops / (t_dom * 1e-3 / args.steps) / 1e12, 1)
         roofline["mfma_frac"] = round(roofline["mfma_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4)
     if cfg in ("c6", "c7"):

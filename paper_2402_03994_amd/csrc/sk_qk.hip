@@ -325,9 +325,12 @@ __global__ __launch_bounds__(256) void k_qk_s1aw(const uint16_t *__restrict__ x,
     }
 }
 
+// A first when it makes fewer products, and also when the 16-byte-load
+// A-first kernel applies at most twice the products of the B-first order
+// (the matrix cores are far from busy there; its whole-line X loads are not).
 bool qk_afirst_ok(const LayerDesc &ld, int dtype) {
-  return dtype == SK_BF16 && ld.da < ld.db && ld.da % 16 == 0 && ld.da <= 64 && ld.db % 16 == 0 && ld.m % 64 == 0 &&
-         ld.nc % 256 == 0;
+  if (dtype != SK_BF16 || ld.da % 16 != 0 || ld.db % 16 != 0 || ld.m % 64 != 0 || ld.nc % 256 != 0) return false;
+  return (ld.da < ld.db && ld.da <= 64) || (ld.da <= 32 && ld.da <= 2 * ld.db && ld.nc % 512 == 0);
 }
 
 // Stage 2: Y[v][a][c] = sum_k P[a][k] Q[c][k] (P: dA rows, Q: dB rows, both
