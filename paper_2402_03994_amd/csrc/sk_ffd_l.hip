@@ -639,9 +639,10 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols4b(const LayerDesc *__restric
                                                       const uint16_t *__restrict__ tab, float *__restrict__ dst,
                                                       uint16_t *__restrict__ didx, Key key) {
   using L = Lds1024R32;
-  // after the transform: 8192 words and their uint16 destinations; past the
-  // tile: counts, run starts in this workgroup and run starts in the buckets
-  constexpr int kStage = 8192 * 4 + 8192 / 2;
+  // after the transform: 8192 words, their uint16 destinations and uint8
+  // chunks; past the tile: counts, run starts in this workgroup and run
+  // starts in the buckets
+  constexpr int kStage = 8192 * 4 + 8192 / 2 + 8192 / 4;
   constexpr int kFl = (kStage > L::kFloats ? kStage : L::kFloats) + 3 * 128;
   __shared__ __align__(16) float s[kFl];
   const LayerDesc &ld = layers[layer];
@@ -721,24 +722,22 @@ __global__ __launch_bounds__(1024) void k_ffdL_cols4b(const LayerDesc *__restric
   }
   float4 *stg = (float4 *)s;
   uint16_t *sdd = (uint16_t *)(s + 8192 * 4);
+  uint8_t *sq = (uint8_t *)(s + 8192 * 4 + 8192 / 2);
   __syncthreads();  // the tile has been read: its space becomes the staging area
 #pragma unroll
   for (int cq = 0; cq < 8; ++cq) {
-    const uint32_t pos = loc[dd[cq] >> 13] + rank[cq];
+    const uint32_t q = dd[cq] >> 13, pos = loc[q] + rank[cq];
     stg[pos] = v4[cq];
     sdd[pos] = (uint16_t)(dd[cq] & 8191u);
+    sq[pos] = (uint8_t)q;
   }
   __syncthreads();
-  // slot j of the sorted order belongs to the last chunk q with loc[q] <= j
   float4 *d4 = (float4 *)dst + (u * nlive + b) * kD;
   uint16_t *dx = didx + (u * nlive + b) * kD;
 #pragma unroll
   for (int m = 0; m < 8; ++m) {
     const uint32_t j = threadIdx.x + 1024u * m;
-    uint32_t q = 0;
-#pragma unroll
-    for (uint32_t step = 64; step > 0; step >>= 1)
-      if (loc[q + step] <= j) q += step;
+    const uint32_t q = sq[j];
     const uint32_t at = boff[q] + (j - loc[q]);
     if (at < 8192u) {
       d4[q * 8192 + at] = stg[j];
