@@ -173,6 +173,15 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
 #define SK_FLAG_AFFD_NO_MTAB 1u
 
 /*
+ * FFD with D = 2^20: for every live block, sketch_create stores where each
+ * group of 8 source columns starts its run inside the bucket of each run of
+ * 8 destination rows, for Pi_b and its inverse (uint16, 64 KB per block), when
+ * all of them fit in SK_FFD_BUCKET_MB MiB (environment, default 1024).  Calls
+ * on batches that are a multiple of 4 then permute through those buckets;
+ * without the tables they gather through Pi_b.  The results are identical.
+ */
+
+/*
  * Forward sketch y = sum over the selected layers of S_l x_l.
  *   grads       host array of n_layers device pointers; grads[i] holds layer
  *               first_layer+i as [batch, rows*cols] row-major, contiguous, in

@@ -639,14 +639,16 @@ int sketch_create(sk_kind kind, const sk_layer_shape *shapes, int32_t n_layers, 
   }
   if (kind == SK_FFD && ffd_large_path(s)) {
     // bucket offsets of the permutation of every live block (64 KB per block),
-    // when they take at most 1 GiB
+    // when they fit SK_FFD_BUCKET_MB MiB
     int64_t total = 0;
     s->ffdb_off.assign(n_layers, -1);
     for (int l = 0; l < n_layers; ++l) {
       s->ffdb_off[l] = total;
       total += ffd_live_blocks(s, l) * kFfdBucketTab;
     }
-    if (total * 2 <= (1ll << 30)) {
+    const char *e = std::getenv("SK_FFD_BUCKET_MB");
+    const int64_t mb = e ? std::atoll(e) : 1024;
+    if (total * 2 <= (mb << 20)) {
       SK_TRY(alloc((void **)&s->d_ffdb, (size_t)total * 2));
       for (int l = 0; l < n_layers; ++l) launch_ffd_bucket_tab(s, l, s->d_ffdb + s->ffdb_off[l], nullptr);
     } else {

@@ -189,6 +189,32 @@ def test_ffd_large_D_groups(batch, dtype, dev):
         assert rel_err(o.float().cpu().numpy(), r) < (TOL_BF16 if dtype == "bf16" else TOL_F32)
 
 
+def test_ffd_large_D_groups_gather(dev, monkeypatch):
+    """The four-vector groups without the bucket tables (SK_FFD_BUCKET_MB=0):
+    the permutation gathers one 16-byte word per coordinate; forward and
+    transpose against the oracle, and equal to the bucketed path bit for bit
+    (both place the same values, the sums run in the same order)."""
+    shapes, D, seed = [(1, 2 ** 21 + 5), (3, 1000)], 2 ** 20, 47
+    xs = rand_inputs(shapes, 4, seed)
+    g = torch.Generator().manual_seed(seed)
+    z = torch.randn((4, D), generator=g)
+    th = [torch.randn(sh[0] * sh[1], generator=g) * 0.02 for sh in shapes]
+    s_b = sk("ffd", shapes, D, seed, dev)
+    yb = s_b.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ob = [o.cpu().numpy() for o in s_b.apply_T(z.to(dev), theta0=[t.to(dev) for t in th])]
+    monkeypatch.setenv("SK_FFD_BUCKET_MB", "0")
+    s_g = sk("ffd", shapes, D, seed, dev)
+    y = s_g.apply([x.to(dev) for x in xs]).cpu().numpy()
+    ref = O.apply("ffd", shapes, D, seed, [x.numpy() for x in xs])
+    assert rel_err(y, ref) < TOL_F32
+    assert np.array_equal(y, yb)
+    outs = [o.cpu().numpy() for o in s_g.apply_T(z.to(dev), theta0=[t.to(dev) for t in th])]
+    refs = O.apply_T("ffd", shapes, D, seed, z.numpy().astype(np.float64), theta0=[t.numpy() for t in th])
+    for o, r, o2 in zip(outs, refs, ob):
+        assert rel_err(o, r) < TOL_F32
+        assert np.array_equal(o, o2)
+
+
 @pytest.mark.parametrize("kind", ["afjl", "affd", "fjl", "ffd"])
 def test_forward_parity_bf16(kind, dev):
     shapes, D = CASES[3]
