@@ -560,6 +560,36 @@ __global__ __launch_bounds__(256) void k_ffdL_sum4(const LayerDesc *__restrict__
   }
 }
 
+// out[v][i] (+)= sum over runs z < nseg (at most 8) of part[(z bc + v) D + i],
+// in the order of z: one float4 per thread, all its runs' loads in flight.
+__global__ __launch_bounds__(256) void k_ffdL_segsum(const float *__restrict__ part, int nseg, int64_t bc,
+                                                     int64_t b_begin, float *__restrict__ out, int accumulate) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;  // float4 index within the vector
+  const int64_t v = blockIdx.y;
+  float4 t[8];
+#pragma unroll
+  for (int z = 0; z < 8; ++z)
+    if (z < nseg) t[z] = ((const float4 *)part)[(z * bc + v) * (kD / 4) + p];
+  float4 a = t[0];
+#pragma unroll
+  for (int z = 1; z < 8; ++z)
+    if (z < nseg) {
+      a.x += t[z].x;
+      a.y += t[z].y;
+      a.z += t[z].z;
+      a.w += t[z].w;
+    }
+  float4 *o = (float4 *)(out + (b_begin + v) * kD) + p;
+  if (accumulate) {
+    const float4 q = *o;
+    a.x += q.x;
+    a.y += q.y;
+    a.z += q.z;
+    a.w += q.w;
+  }
+  *o = a;
+}
+
 // out[v][r 1024 + c] (+)= sum over runs z < nseg of part[((z bc + v) 1024 + c)
 // 1024 + r], in the order of z; 32 x 32 tiles through LDS (128-byte reads and
 // writes).  Grid (32, 32, bc).
@@ -870,7 +900,11 @@ void run_ffd_large_fwd(const sk_sketch *s, int layer, const void *x, int dtype, 
     const int64_t bseg = (nlive + nseg0 - 1) / nseg0, nseg = (nlive + bseg - 1) / bseg;
     hipLaunchKernelGGL(k_ffdL_sum, dim3(128u, (unsigned)bc, (unsigned)nseg), dim3(256), 0, st, s->d_layers, layer, A,
                        b_begin, nlive, bseg, nseg > 1 ? B : nullptr, out, (int)accumulate, s->key);
-    if (nseg > 1) launch_reduce_partials(B, nseg, bc, kD, b_begin, out, accumulate, st);
+    if (nseg > 1 && ((uintptr_t)out & 15) == 0)  // nseg <= 8 here
+      hipLaunchKernelGGL(k_ffdL_segsum, dim3((unsigned)(kD / 4 / 256), (unsigned)bc), dim3(256), 0, st, B, (int)nseg,
+                         bc, b_begin, out, (int)accumulate);
+    else if (nseg > 1)
+      launch_reduce_partials(B, nseg, bc, kD, b_begin, out, accumulate, st);
   }
   (void)hipGetLastError();
 }
