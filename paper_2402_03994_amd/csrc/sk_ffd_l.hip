@@ -4,13 +4,16 @@
 // H_D = H_1024(r) (x) H_1024(c).  Intermediates are kept transposed: position
 // pos(i) = c 1024 + r holds element i, so that both 1024-point transforms read
 // and write whole rows:
-//   rows kernel  16 rows r of a block: gather / load, H over c, write pos()
-//   cols kernel  16 columns c (contiguous in pos order): H over r, epilogue
+//   rows kernel  32 rows r of a block: gather / load, H over c, write pos()
+//   cols kernel  32 columns c (contiguous in pos order): H over r, epilogue
 // Forward y = sum_b B_b H Pi_b^T G_b H x_b:
 //   rows(x) -> cols(. g, pos order) -> rows(gather k = pi^{-1}(d)) -> sum over
 //   blocks of B_b . cols(.) in registers -> y.
 // Transpose block b = H G_b Pi_b H B_b z:
 //   rows(B_b z) -> cols -> rows(g_i . gather k = pi(i)) -> cols -> theta.
+// Batches that are a multiple of four run the middle passes on groups of four
+// vectors with interleaved intermediates, and move the data through Pi_b by
+// buckets (a counting sort in LDS by destination chunk) instead of a gather.
 // Each kernel applies 1/32 (a normalised H_1024).
 #include "sk_kcommon.h"
 #include "sk_launch.h"
