@@ -295,7 +295,10 @@ def test_debug_streams_bit_exact(dev):
                                        48 * 64 + 16 * 32 + 64 * 80),
                                       # A-first with columns a multiple of 512: eight columns per lane,
                                       # one and two 16-row tiles of A
-                                      ([(64, 512, 16, 32), (128, 1024, 32, 48)], 16 * 32 + 32 * 48)])
+                                      ([(64, 512, 16, 32), (128, 1024, 32, 48)], 16 * 32 + 32 * 48),
+                                      # B first with four and five 16-column tiles of B (two 16-row
+                                      # tiles per wave), stacked rows ragged against the workgroup
+                                      ([(256, 512, 128, 64), (208, 256, 96, 80)], 128 * 64 + 96 * 80)])
 def test_qk_parity(shapes, D, dev):
     seed = 21
     xs = rand_inputs(shapes, 3, seed, dtype=torch.bfloat16, scale=0.01)
