@@ -192,12 +192,14 @@ def test_ffd_large_D_groups(batch, dtype, dev):
         assert rel_err(o.float().cpu().numpy(), r) < (TOL_BF16 if dtype == "bf16" else TOL_F32)
 
 
-def test_ffd_large_D_groups_gather(dev, monkeypatch):
+@pytest.mark.parametrize("shapes", [[(1, 2 ** 21 + 5), (3, 1000)], [(1, 8 * 2 ** 20 - 5)]])
+def test_ffd_large_D_groups_gather(shapes, dev, monkeypatch):
     """The four-vector groups without the bucket tables (SK_FFD_BUCKET_MB=0):
     the permutation gathers one 16-byte word per coordinate; forward and
     transpose against the oracle, and equal to the bucketed path bit for bit
-    (both place the same values, the sums run in the same order)."""
-    shapes, D, seed = [(1, 2 ** 21 + 5), (3, 1000)], 2 ** 20, 47
+    (both place the same values, the sums run in the same order).  Eight
+    blocks (one group) take the XCD-grouped workgroup order."""
+    D, seed = 2 ** 20, 47
     xs = rand_inputs(shapes, 4, seed)
     g = torch.Generator().manual_seed(seed)
     z = torch.randn((4, D), generator=g)
