@@ -1857,8 +1857,49 @@ __global__ __launch_bounds__(1024) void k_reduce_partials4(const float *__restri
   }
 }
 
+// The same sum for at most 16 slots: one 16-byte piece per thread with every
+// slot's load in flight together, added from zero in slot order (the order
+// k_reduce_partials4 takes for these counts, so the results are identical).
+__global__ __launch_bounds__(256) void k_reduce_partials4_few(const float *__restrict__ part, int nslots, int64_t n4,
+                                                              int64_t D, int64_t b_begin, float *__restrict__ out,
+                                                              int accumulate) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= n4) return;
+  const float4 *src = reinterpret_cast<const float4 *>(part) + p;
+  float4 t[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    if (k < nslots) t[k] = src[k * n4];
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    if (k < nslots) {
+      a.x += t[k].x;
+      a.y += t[k].y;
+      a.z += t[k].z;
+      a.w += t[k].w;
+    }
+  const int64_t i = p * 4, v = i / D;
+  float4 *o = reinterpret_cast<float4 *>(out + (b_begin + v) * D + (i - v * D));
+  if (accumulate) {
+    const float4 q = *o;
+    a.x += q.x;
+    a.y += q.y;
+    a.z += q.z;
+    a.w += q.w;
+  }
+  *o = a;
+}
+
 void launch_reduce_partials(const float *part, int64_t nslots, int64_t bc, int64_t D, int64_t b_begin, float *out,
                             bool accumulate, hipStream_t st) {
+  if (nslots <= 16 && D % 4 == 0 && ((uintptr_t)part & 15) == 0 && ((uintptr_t)out & 15) == 0) {
+    const int64_t n4 = bc * D / 4;
+    hipLaunchKernelGGL(k_reduce_partials4_few, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, st, part,
+                       (int)nslots, n4, D, b_begin, out, (int)accumulate);
+    SK_CHECK_LAUNCH();
+    return;
+  }
   if (D % 4 == 0 && ((uintptr_t)part & 15) == 0 && ((uintptr_t)out & 15) == 0) {
     const int64_t n4 = bc * D / 4;
     hipLaunchKernelGGL(k_reduce_partials4, dim3((unsigned)((n4 + 31) / 32)), dim3(1024), 0, st, part, nslots, n4, D,
