@@ -132,15 +132,28 @@ __global__ __launch_bounds__(256) void k_affdS_top8(const LayerDesc *__restrict_
   const int nh = (int)ld.rows_live;  // <= kSmallRows
   const float rs = rsqrtf((float)ld.dk1);
   const float *wz = w + z * wslot + v * ld.np + threadIdx.x;
-  float wv[kSmallRows][4];
+  // every load is issued before the first use: the row ids, the 8 rows' G,
+  // then the live rows (rows h >= nh read row q[0] and are not used)
   int q[kSmallRows];
 #pragma unroll
-  for (int h = 0; h < kSmallRows; ++h) {
-    q[h] = h < nh ? ptab[ld.poff[0][0][0] + h] : 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) wv[h][k] = h < nh ? wz[(int64_t)q[h] * 1024 + 256 * k] : 0.0f;
-  }
+  for (int h = 0; h < kSmallRows; ++h) q[h] = ptab[ld.poff[0][0][0] + (h < nh ? h : 0)];
   const float *gz = g.gt[z] + threadIdx.x;
+  float gv[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) gv[i][k] = gz[(int64_t)(p0 + i) * 1024 + 256 * k];
+  float wv[kSmallRows][4];
+#pragma unroll
+  for (int h = 0; h < kSmallRows; ++h)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) wv[h][k] = wz[(int64_t)q[h] * 1024 + 256 * k];
+  // rows past nh add zero (a select, not a branch per row, which would hold
+  // each row's load back until its test)
+#pragma unroll
+  for (int h = 0; h < kSmallRows; ++h)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) wv[h][k] = h < nh ? wv[h][k] : 0.0f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int p = p0 + i;
@@ -148,9 +161,8 @@ __global__ __launch_bounds__(256) void k_affdS_top8(const LayerDesc *__restrict_
     for (int k = 0; k < 4; ++k) {
       float acc = 0.0f;
 #pragma unroll
-      for (int h = 0; h < kSmallRows; ++h)
-        if (h < nh) acc += flip(wv[h][k], (uint32_t)__popc((uint32_t)(p & q[h])) & 1u);
-      s[L::idx(i, threadIdx.x + 256 * k)] = acc * (gz[(int64_t)p * 1024 + 256 * k] * rs);
+      for (int h = 0; h < kSmallRows; ++h) acc += flip(wv[h][k], (uint32_t)__popc((uint32_t)(p & q[h])) & 1u);
+      s[L::idx(i, threadIdx.x + 256 * k)] = acc * (gv[i][k] * rs);
     }
   }
   __syncthreads();
