@@ -194,6 +194,31 @@ __device__ __forceinline__ f4v load_p4(const QhArgs &a, int64_t v, int row, int 
 template <int QM, int PF>
 __device__ __forceinline__ void load_tile(const QhArgs &a, int64_t v, int k0, int c0, int lane, f4v (&r)[PF][4]) {
   const int cc = c0 + 4 * (lane & 15);
+  // a tile wholly inside K and the input (tested once, uniformly): every load
+  // is issued without a branch, so they are all in flight together
+  if (QM == kQNNFold && a.q_vec && k0 + 15 < a.K &&
+      (int64_t)(PF - 1) * a.slab + (int64_t)(k0 + 15) * a.N + c0 + 63 < a.n_in) {
+    const int64_t base = (a.b_in + v) * a.n_in;
+    if (a.dtype == SK_BF16) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int t = 0; t < PF; ++t) {
+          const uint2 u = *(const uint2 *)((const uint16_t *)a.q + base + t * a.slab +
+                                           (int64_t)(k0 + 4 * q + (lane >> 4)) * a.N + cc);
+          r[t][q] = f4v{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                        __uint_as_float(u.y & 0xFFFF0000u)};
+        }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int t = 0; t < PF; ++t)
+          r[t][q] = *(const f4v *)((const float *)a.q + base + t * a.slab + (int64_t)(k0 + 4 * q + (lane >> 4)) * a.N +
+                                   cc);
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int k = k0 + 4 * q + (lane >> 4);
