@@ -296,8 +296,15 @@ __global__ __launch_bounds__(256) void k_qh_gemm(QhArgs a, QhSlots sl) {
   if (QM != kQNT && kb < ke) load_tile<QM, NR>(a, v, kb, c0, lane, raw);
   for (int k0 = kb; k0 < ke; k0 += 16) {
     f4v pv[TA], qv[TB];
+    if (PM == kPBuf && a.p_vec && r0 + 16 * TA <= a.M && k0 + 15 < a.K) {
+      // the workgroup's rows and this step wholly inside P (tested once): no per-load branch
+      const float *pb = (const float *)a.p + v * a.p_vs;
 #pragma unroll
-    for (int i = 0; i < TA; ++i) pv[i] = load_p4<PM>(a, v, r0 + 16 * i + li, k0 + 4 * g);
+      for (int i = 0; i < TA; ++i) pv[i] = *(const f4v *)(pb + (int64_t)(r0 + 16 * i + li) * a.ldp + k0 + 4 * g);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TA; ++i) pv[i] = load_p4<PM>(a, v, r0 + 16 * i + li, k0 + 4 * g);
+    }
     if (QM == kQNT) {
       // Q rows are output columns, K-contiguous; K is a multiple of 16 here
 #pragma unroll
