@@ -97,9 +97,11 @@ __global__ __launch_bounds__(1024) void k_ffdL_rows(const LayerDesc *__restrict_
         const int c = t + 256 * q;
         const uint32_t e = (uint32_t)(r0 + i) * 1024u + (uint32_t)c;
         if (MODE == kRowsX) {
+          // past the layer the index is clamped and the value selected, so no load waits behind a branch
           const int64_t j = b * kD + e;
-          const int64_t x = (b_begin + v) * ld.n + j;
-          val[k][q] = j < ld.n ? (BF16 ? bf16_to_f32(((const uint16_t *)src)[x]) : ((const float *)src)[x]) : 0.0f;
+          const int64_t x = (b_begin + v) * ld.n + (j < ld.n ? j : ld.n - 1);
+          const float t = BF16 ? bf16_to_f32(((const uint16_t *)src)[x]) : ((const float *)src)[x];
+          val[k][q] = j < ld.n ? t : 0.0f;
         } else if (MODE == kRowsZ) {
           const uint32_t bit = (sg[i * 32 + (c >> 5)] >> (c & 31)) & 1u;
           val[k][q] = flip(((const float *)src)[(b_begin + v) * kD + e], bit);
